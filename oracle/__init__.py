@@ -1,0 +1,288 @@
+"""CPU oracle of the selective-differentiation layers (TEST INFRASTRUCTURE).
+
+Only tests/, __graft_entry__.smoke() and bench.py's cpu_baseline leg may
+import this package.  It is the plain definition of what the GPU library
+computes (Sec. 2.2.1 and App. C of the paper), evaluated in float64 by the C
+loops of oracle.c, plus the closed-form save rule in `oracle.policy`.  It
+shares no code with the HIP library and never reads anything the GPU wrote.
+
+All arrays are numpy arrays in the logical PyTorch order (conv/BN/avgpool:
+N,C,H,W; conv weight: K,C,R,S; linear: X[M,K_in], W[N_out,K_in]); inputs of
+any float dtype are widened to float64, outputs are float64.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+__all__ = [
+    "conv2d_forward", "conv2d_forward_at", "conv2d_input_grad", "conv2d_input_grad_at",
+    "conv2d_weight_grad", "conv2d_weight_grad_at", "conv2d_bias_grad", "conv_out_hw",
+    "linear_forward", "linear_forward_at", "linear_input_grad", "linear_input_grad_at",
+    "linear_weight_grad", "linear_weight_grad_at", "linear_bias_grad",
+    "bn_eval_forward", "bn_eval_backward", "avgpool_forward", "avgpool_backward",
+    "round_to", "rel_err",
+]
+
+_lib = None
+_D = ctypes.POINTER(ctypes.c_double)
+_I = ctypes.c_int64
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        path = _build.build(force=False)
+        _lib = ctypes.CDLL(path)
+    return _lib
+
+
+def _d(a):
+    if a is None:
+        return None
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _p(a):
+    if a is None:
+        return ctypes.cast(None, _D)
+    return a.ctypes.data_as(_D)
+
+
+def _idx(idx, width):
+    a = np.ascontiguousarray(idx, dtype=np.int64).reshape(-1, width)
+    return a, a.shape[0]
+
+
+def conv_out_hw(H, W, R, S, stride, pad):
+    P = (H + 2 * pad[0] - R) // stride[0] + 1
+    Q = (W + 2 * pad[1] - S) // stride[1] + 1
+    if P < 1 or Q < 1:
+        raise ValueError("convolution output would be empty")
+    return P, Q
+
+
+def _conv_args(x_shape, w_shape, stride, pad):
+    N, C, H, W = x_shape
+    K, C2, R, S = w_shape
+    if C2 != C:
+        raise ValueError("channel mismatch")
+    return [_I(v) for v in (N, C, H, W, K, R, S, stride[0], stride[1], pad[0], pad[1])]
+
+
+# ----------------------------------------------------------------- conv2d
+def conv2d_forward(x, w, b=None, stride=(1, 1), pad=(0, 0)):
+    """y = W * x + b (cross-correlation, zero padding), Sec. 2.2.1."""
+    x, w, b = _d(x), _d(w), _d(b)
+    N, _, H, W = x.shape
+    K, _, R, S = w.shape
+    P, Q = conv_out_hw(H, W, R, S, stride, pad)
+    y = np.empty((N, K, P, Q), np.float64)
+    _load().orc_conv2d_forward(_p(x), _p(w), _p(b), _p(y), *_conv_args(x.shape, w.shape, stride, pad))
+    return y
+
+
+def conv2d_forward_at(x, w, b, stride, pad, idx):
+    """Forward values at sampled (n, k, p, q) coordinates."""
+    x, w, b = _d(x), _d(w), _d(b)
+    ia, n = _idx(idx, 4)
+    out = np.empty(n, np.float64)
+    _load().orc_conv2d_forward_at(_p(x), _p(w), _p(b), *_conv_args(x.shape, w.shape, stride, pad),
+                                  ia.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), _I(n), _p(out))
+    return out
+
+
+def conv2d_input_grad(dy, w, x_shape, stride=(1, 1), pad=(0, 0)):
+    """dx for grad dy (needs W only), as the adjoint scatter of the forward."""
+    dy, w = _d(dy), _d(w)
+    dx = np.empty(tuple(x_shape), np.float64)
+    _load().orc_conv2d_input_grad(_p(dy), _p(w), _p(dx), *_conv_args(x_shape, w.shape, stride, pad))
+    return dx
+
+
+def conv2d_input_grad_at(dy, w, x_shape, stride, pad, idx):
+    """dx at sampled (n, c, h, w) coordinates, gathered entry by entry."""
+    dy, w = _d(dy), _d(w)
+    ia, n = _idx(idx, 4)
+    out = np.empty(n, np.float64)
+    _load().orc_conv2d_input_grad_at(_p(dy), _p(w), *_conv_args(x_shape, w.shape, stride, pad),
+                                     ia.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), _I(n), _p(out))
+    return out
+
+
+def conv2d_weight_grad(dy, x, w_shape, stride=(1, 1), pad=(0, 0)):
+    """dW for grad dy (needs x only)."""
+    dy, x = _d(dy), _d(x)
+    dw = np.empty(tuple(w_shape), np.float64)
+    _load().orc_conv2d_weight_grad(_p(dy), _p(x), _p(dw), *_conv_args(x.shape, w_shape, stride, pad))
+    return dw
+
+
+def conv2d_weight_grad_at(dy, x, w_shape, stride, pad, idx):
+    """dW at sampled (k, c, r, s) coordinates."""
+    dy, x = _d(dy), _d(x)
+    ia, n = _idx(idx, 4)
+    out = np.empty(n, np.float64)
+    _load().orc_conv2d_weight_grad_at(_p(dy), _p(x), *_conv_args(x.shape, w_shape, stride, pad),
+                                      ia.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), _I(n), _p(out))
+    return out
+
+
+def conv2d_bias_grad(dy):
+    dy = _d(dy)
+    N, K, P, Q = dy.shape
+    db = np.empty(K, np.float64)
+    _load().orc_conv2d_bias_grad(_p(dy), _p(db), _I(N), _I(K), _I(P), _I(Q))
+    return db
+
+
+# ----------------------------------------------------------------- linear
+def linear_forward(X, W, b=None):
+    """Y = X W^T + b: the layer y = W x + b applied to every row of X."""
+    X, W, b = _d(X), _d(W), _d(b)
+    M, Kin = X.shape
+    Nout, K2 = W.shape
+    if K2 != Kin:
+        raise ValueError("feature mismatch")
+    Y = np.empty((M, Nout), np.float64)
+    _load().orc_linear_forward(_p(X), _p(W), _p(b), _p(Y), _I(M), _I(Kin), _I(Nout))
+    return Y
+
+
+def linear_forward_at(X, W, b, idx):
+    X, W, b = _d(X), _d(W), _d(b)
+    ia, n = _idx(idx, 2)
+    out = np.empty(n, np.float64)
+    _load().orc_linear_forward_at(_p(X), _p(W), _p(b), _I(X.shape[0]), _I(X.shape[1]), _I(W.shape[0]),
+                                  ia.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), _I(n), _p(out))
+    return out
+
+
+def linear_input_grad(dY, W):
+    dY, W = _d(dY), _d(W)
+    M, Nout = dY.shape
+    Kin = W.shape[1]
+    dX = np.empty((M, Kin), np.float64)
+    _load().orc_linear_input_grad(_p(dY), _p(W), _p(dX), _I(M), _I(Kin), _I(Nout))
+    return dX
+
+
+def linear_input_grad_at(dY, W, idx):
+    dY, W = _d(dY), _d(W)
+    ia, n = _idx(idx, 2)
+    out = np.empty(n, np.float64)
+    _load().orc_linear_input_grad_at(_p(dY), _p(W), _I(dY.shape[0]), _I(W.shape[1]), _I(W.shape[0]),
+                                     ia.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), _I(n), _p(out))
+    return out
+
+
+def linear_weight_grad(dY, X):
+    dY, X = _d(dY), _d(X)
+    M, Nout = dY.shape
+    Kin = X.shape[1]
+    dW = np.empty((Nout, Kin), np.float64)
+    _load().orc_linear_weight_grad(_p(dY), _p(X), _p(dW), _I(M), _I(Kin), _I(Nout))
+    return dW
+
+
+def linear_weight_grad_at(dY, X, idx):
+    dY, X = _d(dY), _d(X)
+    ia, n = _idx(idx, 2)
+    out = np.empty(n, np.float64)
+    _load().orc_linear_weight_grad_at(_p(dY), _p(X), _I(dY.shape[0]), _I(X.shape[1]), _I(dY.shape[1]),
+                                      ia.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), _I(n), _p(out))
+    return out
+
+
+def linear_bias_grad(dY):
+    dY = _d(dY)
+    M, Nout = dY.shape
+    db = np.empty(Nout, np.float64)
+    _load().orc_linear_bias_grad(_p(dY), _p(db), _I(M), _I(Nout))
+    return db
+
+
+# ----------------------------------------------------------------- BN eval
+def _ncl(shape):
+    if len(shape) == 2:
+        return shape[0], shape[1], 1
+    N, C = shape[0], shape[1]
+    L = 1
+    for s in shape[2:]:
+        L *= s
+    return N, C, L
+
+
+def bn_eval_forward(x, mean, var, gamma=None, beta=None, eps=1e-5):
+    """y = gamma (x - mu_hat) / sqrt(sigma_hat^2 + eps) + beta per channel (App. C)."""
+    x, mean, var, gamma, beta = map(_d, (x, mean, var, gamma, beta))
+    y = np.empty(x.shape, np.float64)
+    N, C, L = _ncl(x.shape)
+    _load().orc_bn_eval_forward(_p(x), _p(mean), _p(var), _p(gamma), _p(beta),
+                                ctypes.c_double(eps), _p(y), _I(N), _I(C), _I(L))
+    return y
+
+
+def bn_eval_backward(dy, x, mean, var, gamma=None, eps=1e-5,
+                     want_dx=True, want_dgamma=True, want_dbeta=True):
+    """(dx, dgamma, dbeta) of BN-eval; each None unless requested.  x may be
+    None when dgamma is not requested (the input gradient does not need it)."""
+    dy, x, mean, var, gamma = map(_d, (dy, x, mean, var, gamma))
+    N, C, L = _ncl(dy.shape)
+    if want_dgamma and x is None:
+        raise ValueError("dgamma needs x")
+    dx = np.empty(dy.shape, np.float64) if want_dx else None
+    dg = np.empty(C, np.float64) if want_dgamma else None
+    dbt = np.empty(C, np.float64) if want_dbeta else None
+    xx = x if x is not None else dy  # never read when dgamma is not requested
+    _load().orc_bn_eval_backward(_p(dy), _p(xx), _p(mean), _p(var), _p(gamma), ctypes.c_double(eps),
+                                 _p(dx), _p(dg), _p(dbt), _I(N), _I(C), _I(L))
+    return dx, dg, dbt
+
+
+# ----------------------------------------------------------------- avgpool
+def avgpool_forward(x):
+    x = _d(x)
+    N, C, L = _ncl(x.shape)
+    y = np.empty((N, C), np.float64)
+    _load().orc_avgpool_forward(_p(x), _p(y), _I(N), _I(C), _I(L))
+    return y
+
+
+def avgpool_backward(dy, x_shape):
+    dy = _d(dy)
+    N, C, L = _ncl(x_shape)
+    dx = np.empty(tuple(x_shape), np.float64)
+    _load().orc_avgpool_backward(_p(dy), _p(dx), _I(N), _I(C), _I(L))
+    return dx
+
+
+# ----------------------------------------------------------------- rounding, error
+def round_to(a, dtype):
+    """Round float64 values once to 'f32' or 'bf16' (ties to even); float64 out."""
+    a = np.array(a, dtype=np.float64, copy=True, order="C")
+    code = {"f32": 0, "bf16": 1}[dtype]
+    _load().orc_round(_p(a), _I(a.size), ctypes.c_int(code))
+    return a
+
+
+def rel_err(got, ref):
+    """Normwise max relative error max|got - ref| / max|ref|; inf on any
+    non-finite value in `got`."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    if got.shape != ref.shape:
+        raise ValueError(f"shape mismatch {got.shape} vs {ref.shape}")
+    if got.size == 0:
+        return 0.0
+    if not np.all(np.isfinite(got)):
+        return float("inf")
+    den = float(np.max(np.abs(ref)))
+    num = float(np.max(np.abs(got - ref)))
+    if den == 0.0:
+        return 0.0 if num == 0.0 else float("inf")
+    return num / den

@@ -1,0 +1,412 @@
+/*
+ * CPU oracle for the selective-differentiation layers (TEST INFRASTRUCTURE).
+ *
+ * This file is the plain, slow, obviously correct definition of what the
+ * GPU path computes: the value and the vector-Jacobian products of the three
+ * layers that are linear in both their input and their parameters
+ * (Sec. 2.2.1: convolution Z = W * X + b, the fully-connected layer
+ * y = W x + b of App. C, and batch normalisation in evaluation mode,
+ * y = W (x - mu_hat) / sqrt(sigma_hat^2 + eps) + b of App. C), plus the
+ * parameter-free global average pool used to shape the ResNet-18-like stack.
+ *
+ * Only tests/, __graft_entry__.smoke() and the cpu_baseline leg of bench.py
+ * may load or call this code.  It shares nothing with the HIP library: no
+ * header, helper, table or constant.  Every array is a dense row-major
+ * float64 array in the logical PyTorch order (conv/BN: N,C,H,W; conv weight:
+ * K,C,R,S; linear: X[M,K_in], W[N_out,K_in]).  Every sum is accumulated in
+ * float64 in the ascending order of its indices; outputs stay float64 and
+ * orc_round() rounds them once to a storage precision when a caller needs it.
+ *
+ * Convolution is cross-correlation with zero padding, dilation 1, groups 1,
+ * as torch.nn.Conv2d computes it (the '*' of Sec. 2.2.1 is read that way).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+typedef int64_t i64;
+
+#define IDX4(a, b, c, d, B, C, D) ((((a) * (B) + (b)) * (C) + (c)) * (D) + (d))
+
+static i64 out_extent(i64 in, i64 pad, i64 k, i64 stride)
+{
+    return (in + 2 * pad - k) / stride + 1;
+}
+
+/* ---------------------------------------------------------------------------
+ * Conv2d forward (Sec. 2.2.1, Z = W * X + b):
+ *   y[n,k,p,q] = b[k] + sum_{c,r,s} W[k,c,r,s] * x[n,c, p*sh-ph+r, q*sw-pw+s]
+ * with x taken as zero outside [0,H) x [0,W).  b may be NULL (no bias).
+ * ------------------------------------------------------------------------- */
+static double conv_fwd_one(const double *x, const double *w, const double *b,
+                           i64 n, i64 k, i64 p, i64 q,
+                           i64 C, i64 H, i64 W, i64 R, i64 S,
+                           i64 sh, i64 sw, i64 ph, i64 pw)
+{
+    double acc = 0.0;
+    for (i64 c = 0; c < C; ++c)
+        for (i64 r = 0; r < R; ++r) {
+            i64 ih = p * sh - ph + r;
+            if (ih < 0 || ih >= H) continue;
+            for (i64 s = 0; s < S; ++s) {
+                i64 iw = q * sw - pw + s;
+                if (iw < 0 || iw >= W) continue;
+                acc += w[IDX4(k, c, r, s, C, R, S)] * x[IDX4(n, c, ih, iw, C, H, W)];
+            }
+        }
+    return acc + (b ? b[k] : 0.0);
+}
+
+void orc_conv2d_forward(const double *x, const double *w, const double *b, double *y,
+                        i64 N, i64 C, i64 H, i64 W, i64 K, i64 R, i64 S,
+                        i64 sh, i64 sw, i64 ph, i64 pw)
+{
+    i64 P = out_extent(H, ph, R, sh), Q = out_extent(W, pw, S, sw);
+#pragma omp parallel for collapse(2) schedule(static)
+    for (i64 n = 0; n < N; ++n)
+        for (i64 k = 0; k < K; ++k)
+            for (i64 p = 0; p < P; ++p)
+                for (i64 q = 0; q < Q; ++q)
+                    y[IDX4(n, k, p, q, K, P, Q)] =
+                        conv_fwd_one(x, w, b, n, k, p, q, C, H, W, R, S, sh, sw, ph, pw);
+}
+
+/* The same value at `count` sampled output coordinates idx[4*i..4*i+3] =
+ * (n, k, p, q). */
+void orc_conv2d_forward_at(const double *x, const double *w, const double *b,
+                           i64 N, i64 C, i64 H, i64 W, i64 K, i64 R, i64 S,
+                           i64 sh, i64 sw, i64 ph, i64 pw,
+                           const i64 *idx, i64 count, double *out)
+{
+    (void)N; (void)K;
+#pragma omp parallel for schedule(static)
+    for (i64 i = 0; i < count; ++i)
+        out[i] = conv_fwd_one(x, w, b, idx[4 * i], idx[4 * i + 1], idx[4 * i + 2],
+                              idx[4 * i + 3], C, H, W, R, S, sh, sw, ph, pw);
+}
+
+/* ---------------------------------------------------------------------------
+ * Conv2d input gradient (Sec. 2.2.1: the input Jacobian depends on W only).
+ * Written as the adjoint of the forward map: every product the forward adds
+ * into y[n,k,p,q] from x[n,c,ih,iw] sends W[k,c,r,s] * dy[n,k,p,q] back to
+ * dx[n,c,ih,iw].
+ * ------------------------------------------------------------------------- */
+void orc_conv2d_input_grad(const double *dy, const double *w, double *dx,
+                           i64 N, i64 C, i64 H, i64 W, i64 K, i64 R, i64 S,
+                           i64 sh, i64 sw, i64 ph, i64 pw)
+{
+    i64 P = out_extent(H, ph, R, sh), Q = out_extent(W, pw, S, sw);
+#pragma omp parallel for schedule(static)
+    for (i64 n = 0; n < N; ++n) {
+        double *dxn = dx + n * C * H * W;
+        memset(dxn, 0, sizeof(double) * (size_t)(C * H * W));
+        for (i64 k = 0; k < K; ++k)
+            for (i64 p = 0; p < P; ++p)
+                for (i64 q = 0; q < Q; ++q) {
+                    double g = dy[IDX4(n, k, p, q, K, P, Q)];
+                    for (i64 c = 0; c < C; ++c)
+                        for (i64 r = 0; r < R; ++r) {
+                            i64 ih = p * sh - ph + r;
+                            if (ih < 0 || ih >= H) continue;
+                            for (i64 s = 0; s < S; ++s) {
+                                i64 iw = q * sw - pw + s;
+                                if (iw < 0 || iw >= W) continue;
+                                dxn[(c * H + ih) * W + iw] += w[IDX4(k, c, r, s, C, R, S)] * g;
+                            }
+                        }
+                }
+    }
+}
+
+/* One input-gradient entry dx[n,c,h,w], gathered: the sum over (k,r,s) of
+ * W[k,c,r,s] * dy[n,k,p,q] for the output positions (p,q) whose receptive
+ * field covers (h,w) through tap (r,s), i.e. p*sh - ph + r = h. */
+void orc_conv2d_input_grad_at(const double *dy, const double *w,
+                              i64 N, i64 C, i64 H, i64 W, i64 K, i64 R, i64 S,
+                              i64 sh, i64 sw, i64 ph, i64 pw,
+                              const i64 *idx, i64 count, double *out)
+{
+    (void)N;
+    i64 P = out_extent(H, ph, R, sh), Q = out_extent(W, pw, S, sw);
+#pragma omp parallel for schedule(static)
+    for (i64 i = 0; i < count; ++i) {
+        i64 n = idx[4 * i], c = idx[4 * i + 1], h = idx[4 * i + 2], x = idx[4 * i + 3];
+        double acc = 0.0;
+        for (i64 k = 0; k < K; ++k)
+            for (i64 r = 0; r < R; ++r) {
+                i64 th = h + ph - r;
+                if (th < 0 || th % sh != 0) continue;
+                i64 p = th / sh;
+                if (p >= P) continue;
+                for (i64 s = 0; s < S; ++s) {
+                    i64 tw = x + pw - s;
+                    if (tw < 0 || tw % sw != 0) continue;
+                    i64 q = tw / sw;
+                    if (q >= Q) continue;
+                    acc += w[IDX4(k, c, r, s, C, R, S)] * dy[IDX4(n, k, p, q, K, P, Q)];
+                }
+            }
+        out[i] = acc;
+    }
+}
+
+/* ---------------------------------------------------------------------------
+ * Conv2d weight gradient (Sec. 2.2.1: the weight Jacobian depends on X only):
+ *   dW[k,c,r,s] = sum_{n,p,q} dy[n,k,p,q] * x[n,c, p*sh-ph+r, q*sw-pw+s]
+ * ------------------------------------------------------------------------- */
+static double conv_wgrad_one(const double *dy, const double *x,
+                             i64 k, i64 c, i64 r, i64 s,
+                             i64 N, i64 C, i64 H, i64 W, i64 K, i64 P, i64 Q,
+                             i64 sh, i64 sw, i64 ph, i64 pw)
+{
+    double acc = 0.0;
+    for (i64 n = 0; n < N; ++n)
+        for (i64 p = 0; p < P; ++p) {
+            i64 ih = p * sh - ph + r;
+            if (ih < 0 || ih >= H) continue;
+            for (i64 q = 0; q < Q; ++q) {
+                i64 iw = q * sw - pw + s;
+                if (iw < 0 || iw >= W) continue;
+                acc += dy[IDX4(n, k, p, q, K, P, Q)] * x[IDX4(n, c, ih, iw, C, H, W)];
+            }
+        }
+    return acc;
+}
+
+void orc_conv2d_weight_grad(const double *dy, const double *x, double *dw,
+                            i64 N, i64 C, i64 H, i64 W, i64 K, i64 R, i64 S,
+                            i64 sh, i64 sw, i64 ph, i64 pw)
+{
+    i64 P = out_extent(H, ph, R, sh), Q = out_extent(W, pw, S, sw);
+#pragma omp parallel for collapse(2) schedule(static)
+    for (i64 k = 0; k < K; ++k)
+        for (i64 c = 0; c < C; ++c)
+            for (i64 r = 0; r < R; ++r)
+                for (i64 s = 0; s < S; ++s)
+                    dw[IDX4(k, c, r, s, C, R, S)] =
+                        conv_wgrad_one(dy, x, k, c, r, s, N, C, H, W, K, P, Q, sh, sw, ph, pw);
+}
+
+/* Sampled weight-gradient entries, idx[4*i..] = (k, c, r, s). */
+void orc_conv2d_weight_grad_at(const double *dy, const double *x,
+                               i64 N, i64 C, i64 H, i64 W, i64 K, i64 R, i64 S,
+                               i64 sh, i64 sw, i64 ph, i64 pw,
+                               const i64 *idx, i64 count, double *out)
+{
+    i64 P = out_extent(H, ph, R, sh), Q = out_extent(W, pw, S, sw);
+#pragma omp parallel for schedule(dynamic, 16)
+    for (i64 i = 0; i < count; ++i)
+        out[i] = conv_wgrad_one(dy, x, idx[4 * i], idx[4 * i + 1], idx[4 * i + 2],
+                                idx[4 * i + 3], N, C, H, W, K, P, Q, sh, sw, ph, pw);
+}
+
+/* Conv2d bias gradient (Sec. 2.2.1: no dependency): db[k] = sum_{n,p,q} dy. */
+void orc_conv2d_bias_grad(const double *dy, double *db, i64 N, i64 K, i64 P, i64 Q)
+{
+#pragma omp parallel for schedule(static)
+    for (i64 k = 0; k < K; ++k) {
+        double acc = 0.0;
+        for (i64 n = 0; n < N; ++n)
+            for (i64 p = 0; p < P; ++p)
+                for (i64 q = 0; q < Q; ++q)
+                    acc += dy[IDX4(n, k, p, q, K, P, Q)];
+        db[k] = acc;
+    }
+}
+
+/* ---------------------------------------------------------------------------
+ * Fully-connected layer (App. C, y = W x + b, applied to every row of X):
+ *   Y[m,j]  = b[j] + sum_i X[m,i] W[j,i]
+ *   dX[m,i] = sum_j dY[m,j] W[j,i]          (needs W only)
+ *   dW[j,i] = sum_m dY[m,j] X[m,i]          (needs X only)
+ *   db[j]   = sum_m dY[m,j]                 (needs nothing)
+ * ------------------------------------------------------------------------- */
+static double lin_fwd_one(const double *X, const double *Wt, const double *b,
+                          i64 m, i64 j, i64 Kin)
+{
+    double acc = 0.0;
+    for (i64 i = 0; i < Kin; ++i) acc += X[m * Kin + i] * Wt[j * Kin + i];
+    return acc + (b ? b[j] : 0.0);
+}
+
+void orc_linear_forward(const double *X, const double *Wt, const double *b, double *Y,
+                        i64 M, i64 Kin, i64 Nout)
+{
+#pragma omp parallel for schedule(static)
+    for (i64 m = 0; m < M; ++m)
+        for (i64 j = 0; j < Nout; ++j) Y[m * Nout + j] = lin_fwd_one(X, Wt, b, m, j, Kin);
+}
+
+void orc_linear_forward_at(const double *X, const double *Wt, const double *b,
+                           i64 M, i64 Kin, i64 Nout, const i64 *idx, i64 count, double *out)
+{
+    (void)M; (void)Nout;
+#pragma omp parallel for schedule(static)
+    for (i64 i = 0; i < count; ++i) out[i] = lin_fwd_one(X, Wt, b, idx[2 * i], idx[2 * i + 1], Kin);
+}
+
+static double lin_dgrad_one(const double *dY, const double *Wt, i64 m, i64 i, i64 Kin, i64 Nout)
+{
+    double acc = 0.0;
+    for (i64 j = 0; j < Nout; ++j) acc += dY[m * Nout + j] * Wt[j * Kin + i];
+    return acc;
+}
+
+void orc_linear_input_grad(const double *dY, const double *Wt, double *dX,
+                           i64 M, i64 Kin, i64 Nout)
+{
+#pragma omp parallel for schedule(static)
+    for (i64 m = 0; m < M; ++m)
+        for (i64 i = 0; i < Kin; ++i) dX[m * Kin + i] = lin_dgrad_one(dY, Wt, m, i, Kin, Nout);
+}
+
+void orc_linear_input_grad_at(const double *dY, const double *Wt, i64 M, i64 Kin, i64 Nout,
+                              const i64 *idx, i64 count, double *out)
+{
+    (void)M;
+#pragma omp parallel for schedule(static)
+    for (i64 i = 0; i < count; ++i) out[i] = lin_dgrad_one(dY, Wt, idx[2 * i], idx[2 * i + 1], Kin, Nout);
+}
+
+static double lin_wgrad_one(const double *dY, const double *X, i64 j, i64 i,
+                            i64 M, i64 Kin, i64 Nout)
+{
+    double acc = 0.0;
+    for (i64 m = 0; m < M; ++m) acc += dY[m * Nout + j] * X[m * Kin + i];
+    return acc;
+}
+
+void orc_linear_weight_grad(const double *dY, const double *X, double *dW,
+                            i64 M, i64 Kin, i64 Nout)
+{
+#pragma omp parallel for schedule(static)
+    for (i64 j = 0; j < Nout; ++j)
+        for (i64 i = 0; i < Kin; ++i) dW[j * Kin + i] = lin_wgrad_one(dY, X, j, i, M, Kin, Nout);
+}
+
+void orc_linear_weight_grad_at(const double *dY, const double *X, i64 M, i64 Kin, i64 Nout,
+                               const i64 *idx, i64 count, double *out)
+{
+#pragma omp parallel for schedule(dynamic, 16)
+    for (i64 i = 0; i < count; ++i)
+        out[i] = lin_wgrad_one(dY, X, idx[2 * i], idx[2 * i + 1], M, Kin, Nout);
+}
+
+void orc_linear_bias_grad(const double *dY, double *db, i64 M, i64 Nout)
+{
+#pragma omp parallel for schedule(static)
+    for (i64 j = 0; j < Nout; ++j) {
+        double acc = 0.0;
+        for (i64 m = 0; m < M; ++m) acc += dY[m * Nout + j];
+        db[j] = acc;
+    }
+}
+
+/* ---------------------------------------------------------------------------
+ * Batch normalisation in evaluation mode (App. C):
+ *   y = gamma * (x - mu_hat) / sqrt(sigma_hat^2 + eps) + beta
+ * per channel c of x[N, C, L] (L = H*W; L = 1 for a [N, C] input), with the
+ * running statistics mu_hat, sigma_hat^2 fixed buffers.  gamma == NULL means
+ * gamma = 1 and beta == NULL means beta = 0 (affine=False).
+ * Backward (the map is affine in x, gamma and beta):
+ *   dx     = dy * gamma / sqrt(sigma_hat^2 + eps)              (no x needed)
+ *   dgamma = sum_{n,l} dy * (x - mu_hat) / sqrt(sigma_hat^2 + eps)
+ *   dbeta  = sum_{n,l} dy
+ * Any of dx, dgamma, dbeta may be NULL to skip it.
+ * ------------------------------------------------------------------------- */
+void orc_bn_eval_forward(const double *x, const double *mean, const double *var,
+                         const double *gamma, const double *beta, double eps, double *y,
+                         i64 N, i64 C, i64 L)
+{
+#pragma omp parallel for collapse(2) schedule(static)
+    for (i64 n = 0; n < N; ++n)
+        for (i64 c = 0; c < C; ++c) {
+            double g = gamma ? gamma[c] : 1.0, bt = beta ? beta[c] : 0.0;
+            for (i64 l = 0; l < L; ++l) {
+                i64 o = (n * C + c) * L + l;
+                y[o] = g * (x[o] - mean[c]) / sqrt(var[c] + eps) + bt;
+            }
+        }
+}
+
+void orc_bn_eval_backward(const double *dy, const double *x, const double *mean,
+                          const double *var, const double *gamma, double eps,
+                          double *dx, double *dgamma, double *dbeta,
+                          i64 N, i64 C, i64 L)
+{
+    if (dx) {
+#pragma omp parallel for collapse(2) schedule(static)
+        for (i64 n = 0; n < N; ++n)
+            for (i64 c = 0; c < C; ++c) {
+                double g = gamma ? gamma[c] : 1.0;
+                for (i64 l = 0; l < L; ++l) {
+                    i64 o = (n * C + c) * L + l;
+                    dx[o] = dy[o] * g / sqrt(var[c] + eps);
+                }
+            }
+    }
+    if (dgamma || dbeta) {
+#pragma omp parallel for schedule(static)
+        for (i64 c = 0; c < C; ++c) {
+            double sg = 0.0, sb = 0.0;
+            for (i64 n = 0; n < N; ++n)
+                for (i64 l = 0; l < L; ++l) {
+                    i64 o = (n * C + c) * L + l;
+                    if (dgamma) sg += dy[o] * (x[o] - mean[c]) / sqrt(var[c] + eps);
+                    sb += dy[o];
+                }
+            if (dgamma) dgamma[c] = sg;
+            if (dbeta) dbeta[c] = sb;
+        }
+    }
+}
+
+/* ---------------------------------------------------------------------------
+ * Global average pool x[N,C,H,W] -> y[N,C] and its adjoint.
+ * ------------------------------------------------------------------------- */
+void orc_avgpool_forward(const double *x, double *y, i64 N, i64 C, i64 L)
+{
+#pragma omp parallel for collapse(2) schedule(static)
+    for (i64 n = 0; n < N; ++n)
+        for (i64 c = 0; c < C; ++c) {
+            double acc = 0.0;
+            for (i64 l = 0; l < L; ++l) acc += x[(n * C + c) * L + l];
+            y[n * C + c] = acc / (double)L;
+        }
+}
+
+void orc_avgpool_backward(const double *dy, double *dx, i64 N, i64 C, i64 L)
+{
+#pragma omp parallel for collapse(2) schedule(static)
+    for (i64 n = 0; n < N; ++n)
+        for (i64 c = 0; c < C; ++c)
+            for (i64 l = 0; l < L; ++l) dx[(n * C + c) * L + l] = dy[n * C + c] / (double)L;
+}
+
+/* ---------------------------------------------------------------------------
+ * Round float64 values once to a storage precision, in place:
+ *   dtype 0: IEEE binary32, round to nearest even (the C conversion);
+ *   dtype 1: bfloat16 (8 significant bits, binary32 exponent range), round
+ *            to nearest even directly from the float64 value.
+ * ------------------------------------------------------------------------- */
+static double round_to_bf16(double v)
+{
+    if (!isfinite(v) || v == 0.0) return v;
+    const double maxbf = ldexp(255.0, 120);     /* (2 - 2^-7) * 2^127 */
+    int e;
+    double m = frexp(fabs(v), &e);               /* |v| = m * 2^e, m in [0.5, 1) */
+    int q = e - 8;                               /* quantum exponent for 8 significant bits */
+    if (q < -133) q = -133;                      /* bf16 subnormal spacing is 2^-133 */
+    (void)m;
+    double r = nearbyint(ldexp(fabs(v), -q));    /* default rounding: ties to even */
+    double out = ldexp(r, q);
+    if (out > maxbf) out = INFINITY;
+    return v < 0 ? -out : out;
+}
+
+void orc_round(double *a, i64 n, int dtype)
+{
+#pragma omp parallel for schedule(static)
+    for (i64 i = 0; i < n; ++i)
+        a[i] = dtype == 1 ? round_to_bf16(a[i]) : (double)(float)a[i];
+}
