@@ -1,0 +1,192 @@
+/*
+ * memsave.h -- C ABI of the MI355X (gfx950) selective-differentiation layers.
+ *
+ * The library implements the forward and backward pass of the layers that
+ * are linear in both their input and their parameters -- Conv2d, Linear and
+ * BatchNorm in evaluation mode -- driven by a differentiability mask
+ * (Sec. 2.2.1 of "Lowering PyTorch's Memory Consumption for Selective
+ * Differentiation", arXiv 2404.12406).  The input Jacobian of such a layer
+ * needs only the weight, the weight Jacobian needs only the input and the
+ * bias Jacobian needs nothing, so a forward call keeps the layer input only
+ * when the weight gradient is requested, and a backward call launches only
+ * the gradient work whose flag is set.  Selective differentiation -- asking
+ * for gradients of a subset of the leaves -- is the problem statement of
+ * Sec. 1; the forward/backward pair mirrors the autograd primitive of
+ * Sec. 2.2 (a forward that decides what to save, a backward that returns
+ * only the needed gradients).
+ *
+ * Conventions shared by every entry point
+ *  - Every buffer is caller-allocated device memory; the library never
+ *    frees or copies caller memory.  `ms_tensor.data` is a device pointer.
+ *  - Shapes are given in logical PyTorch order, strides in elements.
+ *    4-D activations and conv weights must be channels-last (NHWC / KRSC
+ *    memory order, i.e. torch.channels_last); 2-D tensors row-major; 1-D
+ *    tensors contiguous.  Anything else returns MS_E_LAYOUT.
+ *  - dtypes: MS_F32 or MS_BF16; all tensors of one call share one dtype.
+ *    Products are accumulated in fp32 and rounded once to the output dtype
+ *    (round to nearest even).
+ *  - Every tensor has fewer than 2^31 elements (MS_E_UNSUPPORTED otherwise).
+ *  - All work is enqueued on the caller's stream (`stream` is a
+ *    hipStream_t; NULL = the null stream); no call synchronises the device
+ *    except the first use of a larger transient workspace on a stream.
+ *  - Validation runs before any launch.  On error no kernel is launched, no
+ *    record is created and the ledger is unchanged; the status says why and
+ *    ms_last_error() gives a human-readable detail (thread-local).
+ *  - Asynchronous device faults surface as MS_E_HIP from a later call.
+ *  - Calls on different streams that overlap on one device are safe: each
+ *    stream gets its own transient workspace.
+ */
+#ifndef MEMSAVE_H
+#define MEMSAVE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MS_OK = 0,
+    MS_E_NULL = 1,        /* a required pointer is NULL                          */
+    MS_E_MASK = 2,        /* mask bits invalid, or grad buffers do not match it  */
+    MS_E_SHAPE = 3,       /* shapes inconsistent                                 */
+    MS_E_DTYPE = 4,       /* unsupported or mixed dtypes                         */
+    MS_E_LAYOUT = 5,      /* strides are not the required memory order           */
+    MS_E_UNSUPPORTED = 6, /* valid but not implemented (dilation, size limits)   */
+    MS_E_CONSUMED = 7,    /* backward already ran on this record                 */
+    MS_E_NOMEM = 8,       /* transient workspace allocation failed               */
+    MS_E_HIP = 9,         /* a HIP runtime call or kernel launch failed          */
+    MS_E_ARG = 10         /* any other invalid argument                          */
+} ms_status;
+
+/* Differentiability mask (requires_grad of the layer's parents). For BN-eval
+ * the weight is gamma and the bias is beta. */
+enum { MS_RG_INPUT = 1u, MS_RG_WEIGHT = 2u, MS_RG_BIAS = 4u };
+
+typedef enum { MS_F32 = 0, MS_BF16 = 1 } ms_dtype;
+
+/* A device tensor view.  `data` may be NULL only when the tensor has zero
+ * elements. */
+typedef struct {
+    void *data;
+    int32_t dtype;       /* ms_dtype */
+    int32_t ndim;        /* 1, 2 or 4 */
+    int64_t shape[4];
+    int64_t stride[4];   /* in elements */
+} ms_tensor;
+
+typedef enum {
+    MS_CONV2D = 0,       /* y = W * x + b, cross-correlation, zero padding, dilation 1, groups 1
+                            x[N,C,H,W], W[K,C,R,S], b[K] or NULL, y[N,K,P,Q],
+                            P = (H + 2 pad_h - R) / stride_h + 1 (likewise Q)              */
+    MS_LINEAR = 1,       /* y = x W^T + b: x[M,K_in], W[N_out,K_in], b[N_out] or NULL, y[M,N_out] */
+    MS_BN_EVAL = 2,      /* y = gamma (x - mean) / sqrt(var + eps) + beta per channel,
+                            x[N,C,H,W] (channels-last) or x[N,C]; W = gamma[C], b = beta[C]
+                            (both NULL for affine=False); running stats are fixed buffers  */
+    MS_AVGPOOL = 3       /* global average pool x[N,C,H,W] -> y[N,C]; no parameters        */
+} ms_kind;
+
+typedef struct {
+    int32_t kind;               /* ms_kind */
+    int32_t stride[2];          /* conv: stride (h, w), each >= 1 */
+    int32_t pad[2];             /* conv: zero padding (h, w), each >= 0 */
+    float eps;                  /* BN-eval: epsilon (> 0) */
+    const ms_tensor *running_mean;  /* BN-eval: mu_hat[C]; never differentiable */
+    const ms_tensor *running_var;   /* BN-eval: sigma_hat^2[C]; never differentiable */
+} ms_layer;
+
+/* Opaque saved-tensor record (the AD tape entry of one layer call). */
+typedef struct ms_record ms_record;
+
+/* Bits of ms_account.borrowed: which caller tensors a record keeps. */
+enum { MS_SAVED_X = 1u, MS_SAVED_W = 2u, MS_SAVED_MEAN = 4u, MS_SAVED_VAR = 8u };
+
+/* Bits of ms_account.kernels: what the record's backward will launch. */
+enum { MS_K_DGRAD = 1u, MS_K_WGRAD = 2u, MS_K_BGRAD = 4u };
+
+typedef struct {
+    uint64_t saved_activation_bytes;  /* bytes of non-parameter tensors kept (the layer input) */
+    uint64_t referenced_param_bytes;  /* bytes of parameters / running stats kept by reference */
+    uint64_t transient_workspace_bytes; /* workspace the backward needs (released after it)   */
+    uint32_t mask;                    /* the mask the record was created with               */
+    uint32_t borrowed;                /* MS_SAVED_* bits                                   */
+    uint32_t kernels;                 /* MS_K_* bits: backward launch plan                  */
+    uint32_t reserved;
+} ms_account;
+
+/* Comparison policies of ms_policy_account(). */
+enum {
+    MS_POLICY_SELECTIVE = 0,       /* the rule of Sec. 2.2.1 (what this library does)      */
+    MS_POLICY_PYTORCH_DEFAULT = 1, /* stock PyTorch: conv/BN-eval keep x whenever any flag
+                                      is set (Fig. 2, App. B); Linear is already selective */
+    MS_POLICY_ALL_TRUE = 2         /* every parent requires grad ("All", Sec. 3)          */
+};
+
+/*
+ * ms_layer_forward -- y = layer(x; W, b), then record what backward needs.
+ *
+ * Sec. 2.2.1: with mask bit WEIGHT set the record borrows x (the weight
+ * Jacobian needs it); with bit INPUT set it borrows W (the input Jacobian
+ * needs it; for BN-eval gamma and running_var); nothing is kept for the
+ * bias.  A record borrows: the caller must keep the borrowed tensors alive
+ * and unmodified until ms_layer_backward() or ms_record_free().
+ * mask == 0 launches the forward only and sets *rec = NULL (no record, as
+ * autograd records no node).  Otherwise *rec receives a new record and its
+ * saved_activation_bytes are added to the process-wide ledger.
+ * x, W, b, y: see ms_kind.  W must be NULL for MS_AVGPOOL; b may be NULL.
+ * y is caller-allocated and fully overwritten.
+ */
+ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_tensor *W,
+                           const ms_tensor *b, uint32_t mask, const ms_tensor *y,
+                           ms_record **rec, void *stream);
+
+/*
+ * ms_layer_backward -- write exactly the requested gradients for grad_y.
+ *
+ * grad_x / grad_W / grad_b must be non-NULL exactly for the INPUT / WEIGHT /
+ * BIAS bits of the record's mask (MS_E_MASK otherwise), have the shape and
+ * dtype of their primal, and are overwritten (not accumulated).  Launches the
+ * input-gradient kernel iff INPUT, the weight-gradient contraction iff
+ * WEIGHT, the bias-gradient reduction iff BIAS (Sec. 2.2.1).  Consumes the
+ * record: its borrowed tensors are released (ledger decremented) and a
+ * second call returns MS_E_CONSUMED.  The record itself stays allocated until
+ * ms_record_free().
+ */
+ms_status ms_layer_backward(ms_record *rec, const ms_tensor *grad_y, const ms_tensor *grad_x,
+                            const ms_tensor *grad_W, const ms_tensor *grad_b, void *stream);
+
+/* Copy a record's accounting into *out. */
+ms_status ms_record_account(const ms_record *rec, ms_account *out);
+
+/* Release a record (and its borrowed bytes if backward did not run).  NULL is a no-op. */
+void ms_record_free(ms_record *rec);
+
+/* Process-wide ledger of borrowed activation bytes: current and peak since
+ * the last reset (Sec. 2's proxy for the stored graph is the forward peak). */
+ms_status ms_ledger_read(uint64_t *live, uint64_t *peak);
+/* Reset the peak to the current live value. */
+ms_status ms_ledger_reset(void);
+
+/*
+ * ms_policy_account -- the accounting a forward call would produce under
+ * `policy` (MS_POLICY_*), without launching anything or touching the ledger.
+ * Tensors are validated like ms_layer_forward (data pointers may be NULL).
+ */
+ms_status ms_policy_account(const ms_layer *layer, const ms_tensor *x, const ms_tensor *W,
+                            const ms_tensor *b, uint32_t mask, int32_t policy, ms_account *out);
+
+/* Static description of a status code. */
+const char *ms_status_str(int32_t status);
+
+/* Detail of the last error on the calling thread ("" if none). */
+const char *ms_last_error(void);
+
+/* Library version string. */
+const char *ms_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MEMSAVE_H */

@@ -1,0 +1,271 @@
+"""Python binding of libmemsave: torch tensors in, the C ABI of
+include/memsave.h underneath.  Only argument marshalling happens here; every
+arithmetic step runs in the library's HIP kernels.  PyTorch provides device
+memory (tensors the caller or this module allocates) and the stream.
+
+    y, rec = layer_forward(Conv2d(stride=1, pad=1), x, W, b, mask=MASK_INPUT)
+    gx, gW, gb = layer_backward(rec, grad_y)     # gW, gb are None here
+
+4-D activations and conv weights must be channels-last (torch.channels_last);
+2-D tensors row-major; 1-D tensors contiguous; dtypes float32 or bfloat16.
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+from typing import Optional, Tuple
+
+import torch
+
+from . import _lib
+from ._lib import (MS_AVGPOOL, MS_BN_EVAL, MS_CONV2D, MS_LINEAR, MS_RG_BIAS, MS_RG_INPUT,
+                   MS_RG_WEIGHT, MS_SAVED_MEAN, MS_SAVED_VAR, MS_SAVED_W, MS_SAVED_X, MsAccount,
+                   MsLayer, MsTensor, check)
+
+MASK_INPUT, MASK_WEIGHT, MASK_BIAS = MS_RG_INPUT, MS_RG_WEIGHT, MS_RG_BIAS
+POLICY_SELECTIVE, POLICY_PYTORCH_DEFAULT, POLICY_ALL_TRUE = 0, 1, 2
+
+_DT = {torch.float32: _lib.MS_F32, torch.bfloat16: _lib.MS_BF16}
+
+
+# ------------------------------------------------------------------ layer specs
+@dataclass(frozen=True)
+class Conv2d:
+    """y = W * x + b (cross-correlation, zero padding, dilation 1, groups 1)."""
+    stride: Tuple[int, int] | int = 1
+    pad: Tuple[int, int] | int = 0
+
+
+@dataclass(frozen=True)
+class Linear:
+    """y = x W^T + b for x[M, K_in], W[N_out, K_in]."""
+
+
+@dataclass
+class BatchNormEval:
+    """y = gamma (x - running_mean) / sqrt(running_var + eps) + beta."""
+    running_mean: torch.Tensor
+    running_var: torch.Tensor
+    eps: float = 1e-5
+
+
+@dataclass(frozen=True)
+class AvgPool:
+    """Global average pool x[N, C, H, W] -> y[N, C]."""
+
+
+def _pair(v):
+    return (int(v), int(v)) if isinstance(v, int) else (int(v[0]), int(v[1]))
+
+
+def tensor_desc(t: Optional[torch.Tensor]) -> Optional[MsTensor]:
+    """Describe a torch tensor for the C ABI (pointer, dtype, shape, strides)."""
+    if t is None:
+        return None
+    if t.dtype not in _DT:
+        raise TypeError(f"unsupported dtype {t.dtype}; use float32 or bfloat16")
+    if t.dim() > 4 or t.dim() < 1:
+        raise ValueError("tensors must have 1 to 4 dims")
+    d = MsTensor()
+    d.data = t.data_ptr() if t.numel() > 0 else None
+    d.dtype = _DT[t.dtype]
+    d.ndim = t.dim()
+    for i in range(t.dim()):
+        d.shape[i] = t.shape[i]
+        d.stride[i] = t.stride(i)
+    return d
+
+
+def _ptr(d: Optional[MsTensor]):
+    return ctypes.byref(d) if d is not None else None
+
+
+class _LayerDesc:
+    """Keeps the MsLayer and the tensors it points to alive together."""
+
+    def __init__(self, spec):
+        self.layer = MsLayer()
+        self.mean = self.var = None
+        self.spec = spec
+        if isinstance(spec, Conv2d):
+            self.layer.kind = MS_CONV2D
+            s, p = _pair(spec.stride), _pair(spec.pad)
+            self.layer.stride[0], self.layer.stride[1] = s
+            self.layer.pad[0], self.layer.pad[1] = p
+        elif isinstance(spec, Linear):
+            self.layer.kind = MS_LINEAR
+        elif isinstance(spec, BatchNormEval):
+            self.layer.kind = MS_BN_EVAL
+            self.layer.eps = float(spec.eps)
+            self.mean = tensor_desc(spec.running_mean)
+            self.var = tensor_desc(spec.running_var)
+            self.layer.running_mean = ctypes.pointer(self.mean)
+            self.layer.running_var = ctypes.pointer(self.var)
+        elif isinstance(spec, AvgPool):
+            self.layer.kind = MS_AVGPOOL
+        else:
+            raise TypeError(f"unknown layer spec {spec!r}")
+
+
+def _stream(device) -> ctypes.c_void_p:
+    if device is None or device.type != "cuda":
+        return ctypes.c_void_p(0)
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def output_shape(spec, x: torch.Tensor, W: Optional[torch.Tensor]):
+    if isinstance(spec, Conv2d):
+        N, _, H, Wd = x.shape
+        K, _, R, S = W.shape
+        (sh, sw), (ph, pw) = _pair(spec.stride), _pair(spec.pad)
+        return (N, K, (H + 2 * ph - R) // sh + 1, (Wd + 2 * pw - S) // sw + 1)
+    if isinstance(spec, Linear):
+        return (x.shape[0], W.shape[0])
+    if isinstance(spec, BatchNormEval):
+        return tuple(x.shape)
+    if isinstance(spec, AvgPool):
+        return (x.shape[0], x.shape[1])
+    raise TypeError(spec)
+
+
+def empty_like_layout(shape, like: torch.Tensor) -> torch.Tensor:
+    """Uninitialised tensor of `shape` on like's device in the layout the
+    library requires (channels-last for 4-D)."""
+    if len(shape) == 4:
+        return torch.empty(shape, dtype=like.dtype, device=like.device, memory_format=torch.channels_last)
+    return torch.empty(shape, dtype=like.dtype, device=like.device)
+
+
+# ------------------------------------------------------------------ records
+class Record:
+    """A saved-tensor record: the C record plus torch references to exactly
+    the tensors it borrows (so the caching allocator sees the same retained
+    bytes as the ledger)."""
+
+    def __init__(self, handle: ctypes.c_void_p, desc: _LayerDesc, x, W, b, y_shape, y_like):
+        self._h = handle
+        self._desc = desc
+        acct = self.account()
+        self.mask = acct["mask"]
+        bor = acct["borrowed"]
+        self._keep = {}
+        if bor & MS_SAVED_X:
+            self._keep["x"] = x
+        if bor & MS_SAVED_W:
+            self._keep["W"] = W
+        if bor & (MS_SAVED_MEAN | MS_SAVED_VAR):
+            self._keep["stats"] = (desc.spec.running_mean, desc.spec.running_var)
+        self._x_meta = (tuple(x.shape), x.dtype, x.device)
+        self._w_meta = (tuple(W.shape), W.dtype) if W is not None else None
+        self._b_meta = (tuple(b.shape), b.dtype) if b is not None else None
+        self.y_shape = y_shape
+        self.consumed = False
+
+    @property
+    def saved(self):
+        return dict(self._keep)
+
+    def account(self) -> dict:
+        a = MsAccount()
+        check(_lib.load().ms_record_account(self._h, ctypes.byref(a)), "ms_record_account")
+        return a.as_dict()
+
+    def release_refs(self):
+        self._keep = {}
+
+    def free(self):
+        if self._h is not None:
+            lib = _lib._lib
+            if lib is not None:
+                lib.ms_record_free(self._h)
+            self._h = None
+            self._keep = {}
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def _on_gpu(*ts):
+    """The library dereferences device pointers only: refuse host tensors."""
+    dev = None
+    for t in ts:
+        if t is None:
+            continue
+        if t.device.type != "cuda":
+            raise TypeError("libmemsave computes on the GPU only; got a tensor on " + str(t.device))
+        if dev is not None and t.device != dev:
+            raise ValueError("all tensors of one call must be on the same device")
+        dev = t.device
+    if dev is not None:
+        torch.cuda.set_device(dev)
+
+
+def layer_forward(spec, x: torch.Tensor, W: Optional[torch.Tensor] = None, b: Optional[torch.Tensor] = None,
+                  mask: int = 0, y: Optional[torch.Tensor] = None):
+    """Run the layer's forward kernel on the current stream; return (y, record).
+    record is None when mask == 0 (nothing is saved)."""
+    lib = _lib.load()
+    desc = _LayerDesc(spec)
+    extra = (spec.running_mean, spec.running_var) if isinstance(spec, BatchNormEval) else ()
+    _on_gpu(x, W, b, y, *extra)
+    if y is None:
+        y = empty_like_layout(output_shape(spec, x, W), x)
+    dx, dw, db, dy = tensor_desc(x), tensor_desc(W), tensor_desc(b), tensor_desc(y)
+    h = ctypes.c_void_p()
+    st = lib.ms_layer_forward(ctypes.byref(desc.layer), _ptr(dx), _ptr(dw), _ptr(db), int(mask), _ptr(dy),
+                              ctypes.byref(h), _stream(x.device))
+    check(st, "ms_layer_forward")
+    if not h.value:
+        return y, None
+    return y, Record(h, desc, x, W, b, tuple(y.shape), y)
+
+
+def layer_backward(rec: Record, grad_y: torch.Tensor, grad_x: Optional[torch.Tensor] = None,
+                   grad_W: Optional[torch.Tensor] = None, grad_b: Optional[torch.Tensor] = None):
+    """Write exactly the requested gradients; return (grad_x, grad_W, grad_b)
+    with None for every gradient the record's mask does not request.
+    Gradient buffers not passed in are allocated here."""
+    lib = _lib.load()
+    _on_gpu(grad_y, grad_x, grad_W, grad_b)
+    m = rec.mask
+    if m & MASK_INPUT and grad_x is None:
+        grad_x = empty_like_layout(rec._x_meta[0], grad_y)
+    if m & MASK_WEIGHT and grad_W is None:
+        grad_W = empty_like_layout(rec._w_meta[0], grad_y)
+    if m & MASK_BIAS and grad_b is None:
+        grad_b = torch.empty(rec._b_meta[0], dtype=grad_y.dtype, device=grad_y.device)
+    gy, gx, gw, gb = tensor_desc(grad_y), tensor_desc(grad_x), tensor_desc(grad_W), tensor_desc(grad_b)
+    st = lib.ms_layer_backward(rec._h, _ptr(gy), _ptr(gx), _ptr(gw), _ptr(gb), _stream(grad_y.device))
+    check(st, "ms_layer_backward")
+    rec.consumed = True
+    rec.release_refs()
+    return grad_x, grad_W, grad_b
+
+
+def policy_account(spec, x: torch.Tensor, W: Optional[torch.Tensor] = None, b: Optional[torch.Tensor] = None,
+                   mask: int = 0, policy: int = POLICY_SELECTIVE) -> dict:
+    """Accounting a forward call would produce under `policy`; launches nothing."""
+    lib = _lib.load()
+    desc = _LayerDesc(spec)
+    a = MsAccount()
+    st = lib.ms_policy_account(ctypes.byref(desc.layer), _ptr(tensor_desc(x)), _ptr(tensor_desc(W)),
+                               _ptr(tensor_desc(b)), int(mask), int(policy), ctypes.byref(a))
+    check(st, "ms_policy_account")
+    return a.as_dict()
+
+
+def ledger_read() -> Tuple[int, int]:
+    live, peak = ctypes.c_uint64(), ctypes.c_uint64()
+    check(_lib.load().ms_ledger_read(ctypes.byref(live), ctypes.byref(peak)), "ms_ledger_read")
+    return int(live.value), int(peak.value)
+
+
+def ledger_reset():
+    check(_lib.load().ms_ledger_reset(), "ms_ledger_reset")
+
+
+def version() -> str:
+    return _lib.load().ms_version().decode()

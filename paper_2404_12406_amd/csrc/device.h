@@ -1,0 +1,67 @@
+// Interface between the host runtime (memsave.cpp, plain C++) and the HIP
+// kernel launchers (kernels/*.hip).  Plain types only, so the host runtime
+// compiles without HIP headers.  Every launcher enqueues on `stream` (a
+// hipStream_t) and returns 0 or the hipError_t of the failed launch.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ms {
+
+enum Dtype : int { kF32 = 0, kBF16 = 1 };
+
+// Convolution geometry.  Activations are NHWC, filters KRSC, all dense.
+// The fully-connected layer is the special case H = W = R = S = P = Q = 1,
+// stride 1, pad 0 (x[M,K_in] = NHWC with N = M, C = K_in; W[N_out,K_in] = KRSC).
+struct ConvGeom {
+    int N, C, H, W;   // input
+    int K, R, S;      // filters
+    int P, Q;         // output extent
+    int sh, sw, ph, pw;
+};
+
+// y = W * x + b (b may be null).
+int launch_conv_fwd(int dtype, const ConvGeom &g, const void *x, const void *w,
+                    const void *bias, void *y, void *stream);
+
+// dx = input gradient of the convolution for grad dy (needs w only).
+int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *w,
+                      void *dx, void *stream);
+
+// dw = weight gradient for grad dy and input x.  Needs conv_wgrad_workspace()
+// bytes of device workspace (may be 0).
+size_t conv_wgrad_workspace(int dtype, const ConvGeom &g);
+int launch_conv_wgrad(int dtype, const ConvGeom &g, const void *dy, const void *x,
+                      void *dw, void *ws, void *stream);
+
+// out[j] = sum_i in[i][j] for a dense row-major [rows][cols] matrix (bias
+// gradient of conv over N*P*Q rows, of linear over M rows).
+size_t colsum_workspace(int dtype, int64_t rows, int cols);
+int launch_colsum(int dtype, const void *in, int64_t rows, int cols, void *out,
+                  void *ws, void *stream);
+
+// BN-eval over x[rows][C] (NHWC pixels x channels).  gamma/beta may be null.
+int launch_bn_fwd(int dtype, const void *x, const void *mean, const void *var,
+                  const void *gamma, const void *beta, float eps, int64_t rows, int C,
+                  void *y, void *stream);
+size_t bn_bwd_workspace(int dtype, int64_t rows, int C);
+// Any of dx, dgamma, dbeta may be null (not requested); x and mean are read
+// only when dgamma is requested.
+int launch_bn_bwd(int dtype, const void *dy, const void *x, const void *mean,
+                  const void *var, const void *gamma, float eps, int64_t rows, int C,
+                  void *dx, void *dgamma, void *dbeta, void *ws, void *stream);
+
+// Global average pool x[N][L][C] -> y[N][C] and its adjoint.
+int launch_avgpool_fwd(int dtype, const void *x, int N, int L, int C, void *y, void *stream);
+int launch_avgpool_bwd(int dtype, const void *dy, int N, int L, int C, void *dx, void *stream);
+
+// Per-stream transient workspace (workspace.hip).  Returns null and sets
+// *err on failure.
+void *workspace_get(void *stream, size_t bytes, int *err);
+// Test hook: make the next `n` workspace growths fail.
+void workspace_fail_next(int n);
+
+int device_last_error();  // hipGetLastError()
+
+}  // namespace ms

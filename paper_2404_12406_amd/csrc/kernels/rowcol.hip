@@ -1,0 +1,445 @@
+// Bandwidth-bound kernels over an NHWC activation viewed as [rows][C]
+// (rows = N*H*W pixels, C channels contiguous):
+//   - BN in evaluation mode, forward y = gamma (x - mu)/sqrt(var + eps) + beta
+//     folded per channel into y = x*s + t (s = gamma/sqrt(var+eps),
+//     t = beta - mu*s, computed in fp32 by each thread for its channels);
+//   - BN-eval backward: dx = dy*s (needs gamma and var, not x),
+//     dgamma = sum dy*(x - mu)/sqrt(var+eps) (the only use of x),
+//     dbeta = sum dy;
+//   - bias gradient of conv / linear: column sums of dy;
+//   - global average pool and its adjoint.
+//
+// Thread map: a block is RG x TC threads; thread (rg, tc) owns the channel
+// vector tc of its block's column tile for the whole kernel and walks rows
+// rg, rg+RG, ... of its block's row chunk, so per-channel constants live in
+// registers and a wave reads whole contiguous rows (coalesced 16-byte loads).
+// Reductions: per-thread fp32 partials -> LDS reduction over RG -> one fp32
+// partial per (row chunk, channel) -> finalize kernel (deterministic order).
+#include <algorithm>
+
+#include "common.h"
+#include "../device.h"
+
+namespace ms {
+
+namespace {
+
+struct RowColPlan {
+    int V;        // elements per vector (16 bytes, or 1 for the scalar path)
+    int nvc;      // vectors per row
+    int TC, RG;   // block shape
+    int gx, gy;   // grid
+    int64_t chunk;  // rows per block (y)
+};
+
+RowColPlan plan_rowcol(int dtype, int64_t rows, int C, bool vec_ok, int target_blocks) {
+    RowColPlan p;
+    p.V = vec_ok ? (dtype == kBF16 ? 8 : 4) : 1;
+    p.nvc = C / p.V;
+    p.TC = std::min(p.nvc, 256);
+    p.RG = 256 / p.TC;
+    p.gx = (p.nvc + p.TC - 1) / p.TC;
+    int64_t want_y = std::max<int64_t>(1, target_blocks / p.gx);
+    // at least 4 rows per thread
+    int64_t max_y = std::max<int64_t>(1, rows / (int64_t)(p.RG * 4));
+    p.gy = (int)std::max<int64_t>(1, std::min<int64_t>(want_y, max_y));
+    p.gy = std::min(p.gy, 65535);
+    p.chunk = (rows + p.gy - 1) / p.gy;
+    return p;
+}
+
+bool al16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+template <typename T, int V> struct VecT;
+template <typename T> struct VecT<T, 1> {
+    T e[1];
+    __device__ __forceinline__ void load(const T *p) { e[0] = p[0]; }
+    __device__ __forceinline__ void store(T *p) const { p[0] = e[0]; }
+};
+template <typename T> struct VecT<T, 16 / sizeof(T)> {
+    union {
+        u32x4 u;
+        T e[16 / sizeof(T)];
+    };
+    __device__ __forceinline__ void load(const T *p) { u = *reinterpret_cast<const u32x4 *>(p); }
+    __device__ __forceinline__ void store(T *p) const { *reinterpret_cast<u32x4 *>(p) = u; }
+};
+
+}  // namespace
+
+// ---------------------------------------------------------------- BN-eval fwd
+template <typename T, int V>
+__global__ __launch_bounds__(256) void bn_fwd_kernel(const T *__restrict__ x, const T *__restrict__ mean,
+                                                     const T *__restrict__ var, const T *__restrict__ gamma,
+                                                     const T *__restrict__ beta, float eps, int64_t rows,
+                                                     int C, int TC, int RG, int64_t chunk,
+                                                     T *__restrict__ y) {
+    const int tc = threadIdx.x % TC, rg = threadIdx.x / TC;
+    if (rg >= RG) return;
+    const int cv = blockIdx.x * TC + tc;
+    if (cv * V >= C) return;
+    const int c0 = cv * V;
+    float s[V], t[V];
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+        const float g = gamma ? to_f32(gamma[c0 + e]) : 1.f;
+        const float b = beta ? to_f32(beta[c0 + e]) : 0.f;
+        const float inv = 1.f / sqrtf(to_f32(var[c0 + e]) + eps);
+        s[e] = g * inv;
+        t[e] = b - to_f32(mean[c0 + e]) * s[e];
+    }
+    const int64_t r0 = (int64_t)blockIdx.y * chunk;
+    const int64_t r1 = min(rows, r0 + chunk);
+    int64_t r = r0 + rg;
+    constexpr int U = 4;
+    for (; r + (U - 1) * RG < r1; r += U * RG) {
+        VecT<T, V> v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u].load(x + (r + u * RG) * C + c0);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) v[u].e[e] = from_f32<T>(fmaf(to_f32(v[u].e[e]), s[e], t[e]));
+            v[u].store(y + (r + u * RG) * C + c0);
+        }
+    }
+    for (; r < r1; r += RG) {
+        VecT<T, V> v;
+        v.load(x + r * C + c0);
+#pragma unroll
+        for (int e = 0; e < V; ++e) v.e[e] = from_f32<T>(fmaf(to_f32(v.e[e]), s[e], t[e]));
+        v.store(y + r * C + c0);
+    }
+}
+
+// ------------------------------------------- BN-eval bwd / column sums (partials)
+// MODE 0: column sums of a (bias gradient): part0[by][c] = sum a
+// MODE 1: BN-eval backward: dx = a*s (if dx), part0 = sum a*(x-mu)*inv (if want_g),
+//         part1 = sum a (if want_b)
+template <typename T, int V, int MODE>
+__global__ __launch_bounds__(256) void rowcol_reduce_kernel(
+    const T *__restrict__ a, const T *__restrict__ x, const T *__restrict__ mean,
+    const T *__restrict__ var, const T *__restrict__ gamma, float eps, int64_t rows, int C, int TC,
+    int RG, int64_t chunk, T *__restrict__ dx, bool want_g, bool want_b, float *__restrict__ part0,
+    float *__restrict__ part1) {
+    __shared__ float red[2][256 * V];
+    const int tc = threadIdx.x % TC, rg = threadIdx.x / TC;
+    const int cv = blockIdx.x * TC + tc;
+    const bool active = rg < RG && cv * V < C;
+    const int c0 = cv * V;
+    float acc_g[V], acc_b[V], s[V], mu[V], inv[V];
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+        acc_g[e] = 0.f;
+        acc_b[e] = 0.f;
+        s[e] = mu[e] = inv[e] = 0.f;
+    }
+    if (active) {
+        if constexpr (MODE == 1) {
+            // var is read only when dx or dgamma is requested: a beta-only
+            // record does not keep the running statistics (var == nullptr).
+            if (dx || want_g) {
+#pragma unroll
+                for (int e = 0; e < V; ++e) {
+                    inv[e] = 1.f / sqrtf(to_f32(var[c0 + e]) + eps);
+                    s[e] = (gamma ? to_f32(gamma[c0 + e]) : 1.f) * inv[e];
+                    mu[e] = want_g ? to_f32(mean[c0 + e]) : 0.f;
+                }
+            }
+        }
+        const int64_t r0 = (int64_t)blockIdx.y * chunk;
+        const int64_t r1 = min(rows, r0 + chunk);
+        int64_t r = r0 + rg;
+        constexpr int U = 4;
+        auto body = [&](const VecT<T, V> &va, const VecT<T, V> *vx, int64_t rr) {
+            if constexpr (MODE == 0) {
+#pragma unroll
+                for (int e = 0; e < V; ++e) acc_b[e] += to_f32(va.e[e]);
+            } else {
+                if (dx) {
+                    VecT<T, V> o;
+#pragma unroll
+                    for (int e = 0; e < V; ++e) o.e[e] = from_f32<T>(to_f32(va.e[e]) * s[e]);
+                    o.store(dx + rr * C + c0);
+                }
+#pragma unroll
+                for (int e = 0; e < V; ++e) {
+                    const float d = to_f32(va.e[e]);
+                    acc_b[e] += d;
+                    if (vx) acc_g[e] += d * ((to_f32(vx->e[e]) - mu[e]) * inv[e]);
+                }
+            }
+        };
+        for (; r + (U - 1) * RG < r1; r += U * RG) {
+            VecT<T, V> va[U], vx[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) va[u].load(a + (r + u * RG) * C + c0);
+            if (MODE == 1 && want_g) {
+#pragma unroll
+                for (int u = 0; u < U; ++u) vx[u].load(x + (r + u * RG) * C + c0);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) body(va[u], (MODE == 1 && want_g) ? &vx[u] : nullptr, r + u * RG);
+        }
+        for (; r < r1; r += RG) {
+            VecT<T, V> va, vx;
+            va.load(a + r * C + c0);
+            if (MODE == 1 && want_g) vx.load(x + r * C + c0);
+            body(va, (MODE == 1 && want_g) ? &vx : nullptr, r);
+        }
+    }
+    const bool need_b = MODE == 0 || want_b;
+    const bool need_g = MODE == 1 && want_g;
+    if (!need_b && !need_g) return;   // uniform over the block
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+        red[0][threadIdx.x * V + e] = acc_b[e];
+        red[1][threadIdx.x * V + e] = acc_g[e];
+    }
+    __syncthreads();
+    if (rg == 0 && active) {
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            float sb = 0.f, sg = 0.f;
+            for (int q = 0; q < RG; ++q) {
+                sb += red[0][(q * TC + tc) * V + e];
+                sg += red[1][(q * TC + tc) * V + e];
+            }
+            const int64_t o = (int64_t)blockIdx.y * C + c0 + e;
+            if (MODE == 0) {
+                part0[o] = sb;
+            } else {
+                if (need_g) part0[o] = sg;
+                if (want_b) part1[o] = sb;
+            }
+        }
+    }
+}
+
+// out[c] = sum_y part[y][c], rounded once to T.
+template <typename T>
+__global__ __launch_bounds__(256) void finalize_kernel(const float *__restrict__ part, int gy, int C,
+                                                       T *__restrict__ out) {
+    const int c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= C) return;
+    float s = 0.f;
+    for (int y = 0; y < gy; ++y) s += part[(int64_t)y * C + c];
+    out[c] = from_f32<T>(s);
+}
+
+// ---------------------------------------------------------------- avgpool
+// y[n][c] = (1/L) sum_l x[n][l][c]; grid (column tiles, N)
+template <typename T, int V>
+__global__ __launch_bounds__(256) void avgpool_fwd_kernel(const T *__restrict__ x, int L, int C, int TC,
+                                                          int RG, T *__restrict__ y) {
+    __shared__ float red[256 * V];
+    const int tc = threadIdx.x % TC, rg = threadIdx.x / TC;
+    const int cv = blockIdx.x * TC + tc;
+    const bool active = rg < RG && cv * V < C;
+    const int c0 = cv * V;
+    const int n = blockIdx.y;
+    float acc[V];
+#pragma unroll
+    for (int e = 0; e < V; ++e) acc[e] = 0.f;
+    if (active) {
+        for (int l = rg; l < L; l += RG) {
+            VecT<T, V> v;
+            v.load(x + ((int64_t)n * L + l) * C + c0);
+#pragma unroll
+            for (int e = 0; e < V; ++e) acc[e] += to_f32(v.e[e]);
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < V; ++e) red[threadIdx.x * V + e] = acc[e];
+    __syncthreads();
+    if (rg == 0 && active) {
+        VecT<T, V> o;
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            float s = 0.f;
+            for (int q = 0; q < RG; ++q) s += red[(q * TC + tc) * V + e];
+            o.e[e] = from_f32<T>(s / (float)L);
+        }
+        o.store(y + (int64_t)n * C + c0);
+    }
+}
+
+// dx[n][l][c] = dy[n][c] / L
+template <typename T, int V>
+__global__ __launch_bounds__(256) void avgpool_bwd_kernel(const T *__restrict__ dy, int N, int L, int C,
+                                                          T *__restrict__ dx) {
+    const int nvc = C / V;
+    const int64_t total = (int64_t)N * L * nvc;
+    const float invL = 1.f / (float)L;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int cv = (int)(i % nvc);
+        const int64_t pix = i / nvc;
+        const int n = (int)(pix / L);
+        VecT<T, V> v;
+        v.load(dy + (int64_t)n * C + cv * V);
+#pragma unroll
+        for (int e = 0; e < V; ++e) v.e[e] = from_f32<T>(to_f32(v.e[e]) * invL);
+        v.store(dx + pix * C + cv * V);
+    }
+}
+
+// ------------------------------------------------------------------ launchers
+namespace {
+constexpr int kTargetBlocks = 2048;
+
+template <typename T, int V>
+int bn_fwd_t(const RowColPlan &p, const void *x, const void *mean, const void *var, const void *gamma,
+             const void *beta, float eps, int64_t rows, int C, void *y, hipStream_t st) {
+    hipLaunchKernelGGL((bn_fwd_kernel<T, V>), dim3(p.gx, p.gy), dim3(256), 0, st, (const T *)x,
+                       (const T *)mean, (const T *)var, (const T *)gamma, (const T *)beta, eps, rows, C,
+                       p.TC, p.RG, p.chunk, (T *)y);
+    return (int)hipGetLastError();
+}
+
+template <typename T, int V, int MODE>
+int reduce_t(const RowColPlan &p, const void *a, const void *x, const void *mean, const void *var,
+             const void *gamma, float eps, int64_t rows, int C, void *dx, bool want_g, bool want_b,
+             float *part0, float *part1, hipStream_t st) {
+    hipLaunchKernelGGL((rowcol_reduce_kernel<T, V, MODE>), dim3(p.gx, p.gy), dim3(256), 0, st,
+                       (const T *)a, (const T *)x, (const T *)mean, (const T *)var, (const T *)gamma, eps,
+                       rows, C, p.TC, p.RG, p.chunk, (T *)dx, want_g, want_b, part0, part1);
+    return (int)hipGetLastError();
+}
+
+template <typename T>
+int finalize_t(const float *part, int gy, int C, void *out, hipStream_t st) {
+    hipLaunchKernelGGL(finalize_kernel<T>, dim3((C + 255) / 256), dim3(256), 0, st, part, gy, C, (T *)out);
+    return (int)hipGetLastError();
+}
+
+int finalize(int dtype, const float *part, int gy, int C, void *out, hipStream_t st) {
+    return dtype == kBF16 ? finalize_t<bf16>(part, gy, C, out, st) : finalize_t<float>(part, gy, C, out, st);
+}
+
+}  // namespace
+
+int launch_bn_fwd(int dtype, const void *x, const void *mean, const void *var, const void *gamma,
+                  const void *beta, float eps, int64_t rows, int C, void *y, void *stream) {
+    if (rows == 0 || C == 0) return 0;
+    const int V = dtype == kBF16 ? 8 : 4;
+    const bool vec = C % V == 0 && al16(x) && al16(y);
+    RowColPlan p = plan_rowcol(dtype, rows, C, vec, kTargetBlocks);
+    hipStream_t st = (hipStream_t)stream;
+    if (dtype == kBF16)
+        return vec ? bn_fwd_t<bf16, 8>(p, x, mean, var, gamma, beta, eps, rows, C, y, st)
+                   : bn_fwd_t<bf16, 1>(p, x, mean, var, gamma, beta, eps, rows, C, y, st);
+    return vec ? bn_fwd_t<float, 4>(p, x, mean, var, gamma, beta, eps, rows, C, y, st)
+               : bn_fwd_t<float, 1>(p, x, mean, var, gamma, beta, eps, rows, C, y, st);
+}
+
+static RowColPlan bn_bwd_plan(int dtype, int64_t rows, int C, bool vec) {
+    return plan_rowcol(dtype, rows, C, vec, kTargetBlocks);
+}
+
+size_t bn_bwd_workspace(int dtype, int64_t rows, int C) {
+    // sized for the scalar plan too (it can only have more row chunks)
+    RowColPlan p1 = bn_bwd_plan(dtype, rows, C, true), p0 = bn_bwd_plan(dtype, rows, C, false);
+    const int gy = std::max(p1.gy, p0.gy);
+    return (size_t)2 * gy * C * sizeof(float);
+}
+
+int launch_bn_bwd(int dtype, const void *dy, const void *x, const void *mean, const void *var,
+                  const void *gamma, float eps, int64_t rows, int C, void *dx, void *dgamma, void *dbeta,
+                  void *ws, void *stream) {
+    if (C == 0) return 0;
+    // pointers the requested outputs need (the host runtime guarantees them)
+    if ((dx || dgamma) && !var) return (int)hipErrorInvalidValue;
+    if (dgamma && (!x || !mean)) return (int)hipErrorInvalidValue;
+    hipStream_t st = (hipStream_t)stream;
+    const int V = dtype == kBF16 ? 8 : 4;
+    const bool vec = C % V == 0 && al16(dy) && (!x || al16(x)) && (!dx || al16(dx));
+    RowColPlan p = bn_bwd_plan(dtype, rows, C, vec);
+    const bool want_g = dgamma != nullptr, want_b = dbeta != nullptr;
+    float *part0 = static_cast<float *>(ws);
+    float *part1 = part0 + (size_t)p.gy * C;
+    if (rows > 0) {
+        int err;
+        if (dtype == kBF16)
+            err = vec ? reduce_t<bf16, 8, 1>(p, dy, x, mean, var, gamma, eps, rows, C, dx, want_g, want_b, part0, part1, st)
+                      : reduce_t<bf16, 1, 1>(p, dy, x, mean, var, gamma, eps, rows, C, dx, want_g, want_b, part0, part1, st);
+        else
+            err = vec ? reduce_t<float, 4, 1>(p, dy, x, mean, var, gamma, eps, rows, C, dx, want_g, want_b, part0, part1, st)
+                      : reduce_t<float, 1, 1>(p, dy, x, mean, var, gamma, eps, rows, C, dx, want_g, want_b, part0, part1, st);
+        if (err) return err;
+    }
+    const int gy = rows > 0 ? p.gy : 0;
+    if (want_g) {
+        int err = finalize(dtype, part0, gy, C, dgamma, st);
+        if (err) return err;
+    }
+    if (want_b) {
+        int err = finalize(dtype, part1, gy, C, dbeta, st);
+        if (err) return err;
+    }
+    return 0;
+}
+
+size_t colsum_workspace(int dtype, int64_t rows, int C) {
+    RowColPlan p1 = plan_rowcol(dtype, rows, C, true, kTargetBlocks);
+    RowColPlan p0 = plan_rowcol(dtype, rows, C, false, kTargetBlocks);
+    return (size_t)std::max(p1.gy, p0.gy) * C * sizeof(float);
+}
+
+int launch_colsum(int dtype, const void *in, int64_t rows, int C, void *out, void *ws, void *stream) {
+    if (C == 0) return 0;
+    hipStream_t st = (hipStream_t)stream;
+    const int V = dtype == kBF16 ? 8 : 4;
+    const bool vec = C % V == 0 && al16(in);
+    RowColPlan p = plan_rowcol(dtype, rows, C, vec, kTargetBlocks);
+    float *part = static_cast<float *>(ws);
+    if (rows > 0) {
+        int err;
+        if (dtype == kBF16)
+            err = vec ? reduce_t<bf16, 8, 0>(p, in, nullptr, nullptr, nullptr, nullptr, 0.f, rows, C, nullptr, false, true, part, nullptr, st)
+                      : reduce_t<bf16, 1, 0>(p, in, nullptr, nullptr, nullptr, nullptr, 0.f, rows, C, nullptr, false, true, part, nullptr, st);
+        else
+            err = vec ? reduce_t<float, 4, 0>(p, in, nullptr, nullptr, nullptr, nullptr, 0.f, rows, C, nullptr, false, true, part, nullptr, st)
+                      : reduce_t<float, 1, 0>(p, in, nullptr, nullptr, nullptr, nullptr, 0.f, rows, C, nullptr, false, true, part, nullptr, st);
+        if (err) return err;
+    }
+    return finalize(dtype, part, rows > 0 ? p.gy : 0, C, out, st);
+}
+
+int launch_avgpool_fwd(int dtype, const void *x, int N, int L, int C, void *y, void *stream) {
+    if (N == 0 || C == 0) return 0;
+    hipStream_t st = (hipStream_t)stream;
+    const int V = dtype == kBF16 ? 8 : 4;
+    const bool vec = C % V == 0 && al16(x) && al16(y);
+    const int v = vec ? V : 1;
+    const int nvc = C / v;
+    const int TC = std::min(nvc, 256), RG = 256 / TC;
+    dim3 grid((nvc + TC - 1) / TC, N);
+    if (dtype == kBF16) {
+        if (vec) hipLaunchKernelGGL((avgpool_fwd_kernel<bf16, 8>), grid, dim3(256), 0, st, (const bf16 *)x, L, C, TC, RG, (bf16 *)y);
+        else hipLaunchKernelGGL((avgpool_fwd_kernel<bf16, 1>), grid, dim3(256), 0, st, (const bf16 *)x, L, C, TC, RG, (bf16 *)y);
+    } else {
+        if (vec) hipLaunchKernelGGL((avgpool_fwd_kernel<float, 4>), grid, dim3(256), 0, st, (const float *)x, L, C, TC, RG, (float *)y);
+        else hipLaunchKernelGGL((avgpool_fwd_kernel<float, 1>), grid, dim3(256), 0, st, (const float *)x, L, C, TC, RG, (float *)y);
+    }
+    return (int)hipGetLastError();
+}
+
+int launch_avgpool_bwd(int dtype, const void *dy, int N, int L, int C, void *dx, void *stream) {
+    if (N == 0 || C == 0 || L == 0) return 0;
+    hipStream_t st = (hipStream_t)stream;
+    const int V = dtype == kBF16 ? 8 : 4;
+    const bool vec = C % V == 0 && al16(dy) && al16(dx);
+    const int64_t total = (int64_t)N * L * (C / (vec ? V : 1));
+    const int blocks = (int)std::min<int64_t>((total + 255) / 256, 8192);
+    if (dtype == kBF16) {
+        if (vec) hipLaunchKernelGGL((avgpool_bwd_kernel<bf16, 8>), dim3(blocks), dim3(256), 0, st, (const bf16 *)dy, N, L, C, (bf16 *)dx);
+        else hipLaunchKernelGGL((avgpool_bwd_kernel<bf16, 1>), dim3(blocks), dim3(256), 0, st, (const bf16 *)dy, N, L, C, (bf16 *)dx);
+    } else {
+        if (vec) hipLaunchKernelGGL((avgpool_bwd_kernel<float, 4>), dim3(blocks), dim3(256), 0, st, (const float *)dy, N, L, C, (float *)dx);
+        else hipLaunchKernelGGL((avgpool_bwd_kernel<float, 1>), dim3(blocks), dim3(256), 0, st, (const float *)dy, N, L, C, (float *)dx);
+    }
+    return (int)hipGetLastError();
+}
+
+}  // namespace ms

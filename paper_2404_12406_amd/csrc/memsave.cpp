@@ -1,0 +1,574 @@
+// Host runtime of libmemsave: argument validation, the save rule, saved-tensor
+// records, the byte ledger and the C ABI declared in include/memsave.h.
+//
+// The save rule is Sec. 2.2.1 of the paper: for a layer that is linear in its
+// input X and its weight W (and adds a bias b), the input Jacobian depends on
+// W, the weight Jacobian on X and the bias Jacobian on nothing; the forward
+// pass checks which of them require grad and keeps only what the Jacobians
+// that backward will apply need.  BN in evaluation mode follows the same
+// pattern with gamma as the weight (its input gradient needs gamma and the
+// running variance, its gamma gradient needs x, the running mean and
+// variance).  Nothing in this file touches the device except through the
+// launchers of device.h, and every check runs before the first launch.
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "../../include/memsave.h"
+#include "../../include/memsave_testing.h"
+#include "device.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+ms_status fail(ms_status s, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return s;
+}
+
+void clear_err() { g_err.clear(); }
+
+// ------------------------------------------------------------------ ledger
+std::atomic<uint64_t> g_live{0}, g_peak{0};
+std::atomic<int64_t> g_records{0};
+
+void ledger_add(uint64_t n) {
+    uint64_t now = g_live.fetch_add(n) + n;
+    uint64_t pk = g_peak.load();
+    while (now > pk && !g_peak.compare_exchange_weak(pk, now)) {
+    }
+}
+
+void ledger_sub(uint64_t n) { g_live.fetch_sub(n); }
+
+// ------------------------------------------------------------------ tensors
+constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
+constexpr uint32_t kMagic = 0x4d53524bu;  // "MSRK"
+
+int64_t numel(const ms_tensor *t) {
+    int64_t n = 1;
+    for (int i = 0; i < t->ndim; ++i) n *= t->shape[i];
+    return n;
+}
+
+size_t elt_size(int32_t dt) { return dt == MS_BF16 ? 2 : 4; }
+
+bool dtype_ok(int32_t dt) { return dt == MS_F32 || dt == MS_BF16; }
+
+// Basic sanity: ndim, non-negative extents, element limit, dtype.
+ms_status check_tensor(const ms_tensor *t, const char *name, int ndim, bool need_data) {
+    if (!t) return fail(MS_E_NULL, "%s is NULL", name);
+    if (t->ndim != ndim) return fail(MS_E_SHAPE, "%s: expected %d dims, got %d", name, ndim, t->ndim);
+    if (!dtype_ok(t->dtype)) return fail(MS_E_DTYPE, "%s: unsupported dtype %d", name, t->dtype);
+    int64_t n = 1;
+    for (int i = 0; i < ndim; ++i) {
+        if (t->shape[i] < 0) return fail(MS_E_SHAPE, "%s: negative extent", name);
+        if (t->shape[i] > kMaxElems) return fail(MS_E_UNSUPPORTED, "%s: extent too large", name);
+        n *= t->shape[i];
+        if (n > kMaxElems) return fail(MS_E_UNSUPPORTED, "%s: more than 2^31-1 elements", name);
+    }
+    if (need_data && n > 0 && t->data == nullptr) return fail(MS_E_NULL, "%s.data is NULL", name);
+    return MS_OK;
+}
+
+// Channels-last 4-D: memory order N, H, W, C (dims of extent 1 may carry any stride).
+bool is_nhwc(const ms_tensor *t) {
+    if (numel(t) == 0) return true;   // no element is ever addressed
+    const int64_t N = t->shape[0], C = t->shape[1], H = t->shape[2], W = t->shape[3];
+    (void)N;
+    const int64_t want[4] = {H * W * C, 1, W * C, C};
+    for (int i = 0; i < 4; ++i)
+        if (t->shape[i] > 1 && t->stride[i] != want[i]) return false;
+    return true;
+}
+
+bool is_rowmajor2(const ms_tensor *t) {
+    if (numel(t) == 0) return true;
+    if (t->shape[1] > 1 && t->stride[1] != 1) return false;
+    if (t->shape[0] > 1 && t->stride[0] != t->shape[1]) return false;
+    return true;
+}
+
+bool is_contig1(const ms_tensor *t) { return t->shape[0] <= 1 || t->stride[0] == 1; }
+
+bool same_shape(const ms_tensor *a, const ms_tensor *b) {
+    if (a->ndim != b->ndim) return false;
+    for (int i = 0; i < a->ndim; ++i)
+        if (a->shape[i] != b->shape[i]) return false;
+    return true;
+}
+
+ms_tensor shape_only(const ms_tensor *t) {
+    ms_tensor s = *t;
+    s.data = nullptr;
+    return s;
+}
+
+// ------------------------------------------------------------------ layer plan
+struct Plan {
+    int32_t kind = 0;
+    int32_t dtype = 0;
+    ms::ConvGeom g{};      // conv / linear
+    int64_t rows = 0;      // BN / avgpool: pixels; conv/linear bias grad rows
+    int C = 0;             // BN / avgpool channels
+    int L = 0;             // avgpool pixels per sample
+    int Nb = 0;            // avgpool batch
+    bool has_w = false, has_b = false;
+    uint64_t x_bytes = 0, w_bytes = 0, stat_bytes = 0;
+};
+
+ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_tensor *W,
+                           const ms_tensor *b, uint32_t mask, const ms_tensor *y, bool need_data,
+                           Plan *pl) {
+    if (!layer) return fail(MS_E_NULL, "layer is NULL");
+    if (mask & ~7u) return fail(MS_E_MASK, "mask 0x%x has bits outside INPUT|WEIGHT|BIAS", mask);
+    pl->kind = layer->kind;
+    pl->has_w = W != nullptr;
+    pl->has_b = b != nullptr;
+    if ((mask & MS_RG_WEIGHT) && !W) return fail(MS_E_MASK, "WEIGHT bit set but the layer has no weight");
+    if ((mask & MS_RG_BIAS) && !b) return fail(MS_E_MASK, "BIAS bit set but the layer has no bias");
+    ms_status st;
+    switch (layer->kind) {
+    case MS_CONV2D: {
+        if ((st = check_tensor(x, "x", 4, need_data))) return st;
+        if (!W) return fail(MS_E_NULL, "conv2d needs W");
+        if ((st = check_tensor(W, "W", 4, need_data))) return st;
+        if (x->dtype != W->dtype) return fail(MS_E_DTYPE, "x and W dtypes differ");
+        if (!is_nhwc(x)) return fail(MS_E_LAYOUT, "x must be channels-last (NHWC)");
+        if (!is_nhwc(W)) return fail(MS_E_LAYOUT, "W must be channels-last (KRSC)");
+        const int64_t N = x->shape[0], C = x->shape[1], H = x->shape[2], Wd = x->shape[3];
+        const int64_t K = W->shape[0], R = W->shape[2], S = W->shape[3];
+        if (W->shape[1] != C) return fail(MS_E_SHAPE, "W has %lld input channels, x has %lld",
+                                          (long long)W->shape[1], (long long)C);
+        if (layer->stride[0] < 1 || layer->stride[1] < 1) return fail(MS_E_ARG, "stride must be >= 1");
+        if (layer->pad[0] < 0 || layer->pad[1] < 0) return fail(MS_E_ARG, "pad must be >= 0");
+        if (C < 1 || K < 1 || R < 1 || S < 1 || H < 1 || Wd < 1)
+            return fail(MS_E_SHAPE, "conv2d extents C, K, R, S, H, W must be >= 1");
+        const int64_t Hp = H + 2 * (int64_t)layer->pad[0], Wp = Wd + 2 * (int64_t)layer->pad[1];
+        if (Hp < R || Wp < S) return fail(MS_E_SHAPE, "kernel larger than the padded input");
+        if (Hp > kMaxElems || Wp > kMaxElems) return fail(MS_E_UNSUPPORTED, "padding too large");
+        const int64_t P = (Hp - R) / layer->stride[0] + 1, Q = (Wp - S) / layer->stride[1] + 1;
+        if (b) {
+            if ((st = check_tensor(b, "b", 1, need_data))) return st;
+            if (b->dtype != x->dtype) return fail(MS_E_DTYPE, "b dtype differs from x");
+            if (b->shape[0] != K) return fail(MS_E_SHAPE, "b must have K elements");
+            if (!is_contig1(b)) return fail(MS_E_LAYOUT, "b must be contiguous");
+        }
+        if (y) {
+            if ((st = check_tensor(y, "y", 4, need_data))) return st;
+            if (y->dtype != x->dtype) return fail(MS_E_DTYPE, "y dtype differs from x");
+            if (y->shape[0] != N || y->shape[1] != K || y->shape[2] != P || y->shape[3] != Q)
+                return fail(MS_E_SHAPE, "y must be [%lld,%lld,%lld,%lld]", (long long)N, (long long)K,
+                            (long long)P, (long long)Q);
+            if (!is_nhwc(y)) return fail(MS_E_LAYOUT, "y must be channels-last (NHWC)");
+        }
+        pl->dtype = x->dtype;
+        pl->g = ms::ConvGeom{(int)N, (int)C, (int)H, (int)Wd, (int)K, (int)R, (int)S, (int)P, (int)Q,
+                             layer->stride[0], layer->stride[1], layer->pad[0], layer->pad[1]};
+        if (N * P * Q * K > kMaxElems) return fail(MS_E_UNSUPPORTED, "output has more than 2^31-1 elements");
+        pl->rows = N * P * Q;
+        pl->x_bytes = (uint64_t)numel(x) * elt_size(x->dtype);
+        pl->w_bytes = (uint64_t)numel(W) * elt_size(W->dtype);
+        return MS_OK;
+    }
+    case MS_LINEAR: {
+        if ((st = check_tensor(x, "x", 2, need_data))) return st;
+        if (!W) return fail(MS_E_NULL, "linear needs W");
+        if ((st = check_tensor(W, "W", 2, need_data))) return st;
+        if (x->dtype != W->dtype) return fail(MS_E_DTYPE, "x and W dtypes differ");
+        if (!is_rowmajor2(x)) return fail(MS_E_LAYOUT, "x must be row-major");
+        if (!is_rowmajor2(W)) return fail(MS_E_LAYOUT, "W must be row-major");
+        const int64_t M = x->shape[0], Kin = x->shape[1], Nout = W->shape[0];
+        if (W->shape[1] != Kin) return fail(MS_E_SHAPE, "W has %lld input features, x has %lld",
+                                            (long long)W->shape[1], (long long)Kin);
+        if (b) {
+            if ((st = check_tensor(b, "b", 1, need_data))) return st;
+            if (b->dtype != x->dtype) return fail(MS_E_DTYPE, "b dtype differs from x");
+            if (b->shape[0] != Nout) return fail(MS_E_SHAPE, "b must have N_out elements");
+            if (!is_contig1(b)) return fail(MS_E_LAYOUT, "b must be contiguous");
+        }
+        if (y) {
+            if ((st = check_tensor(y, "y", 2, need_data))) return st;
+            if (y->dtype != x->dtype) return fail(MS_E_DTYPE, "y dtype differs from x");
+            if (y->shape[0] != M || y->shape[1] != Nout) return fail(MS_E_SHAPE, "y must be [M, N_out]");
+            if (!is_rowmajor2(y)) return fail(MS_E_LAYOUT, "y must be row-major");
+        }
+        pl->dtype = x->dtype;
+        pl->g = ms::ConvGeom{(int)M, (int)Kin, 1, 1, (int)Nout, 1, 1, 1, 1, 1, 1, 0, 0};
+        pl->rows = M;
+        pl->x_bytes = (uint64_t)numel(x) * elt_size(x->dtype);
+        pl->w_bytes = (uint64_t)numel(W) * elt_size(W->dtype);
+        return MS_OK;
+    }
+    case MS_BN_EVAL: {
+        if (!x) return fail(MS_E_NULL, "x is NULL");
+        const int nd = x->ndim;
+        if (nd != 2 && nd != 4) return fail(MS_E_SHAPE, "BN-eval x must be [N,C] or [N,C,H,W]");
+        if ((st = check_tensor(x, "x", nd, need_data))) return st;
+        if (nd == 4 && !is_nhwc(x)) return fail(MS_E_LAYOUT, "x must be channels-last (NHWC)");
+        if (nd == 2 && !is_rowmajor2(x)) return fail(MS_E_LAYOUT, "x must be row-major");
+        const int64_t C = x->shape[1];
+        if (C < 1) return fail(MS_E_SHAPE, "BN-eval needs C >= 1");
+        const ms_tensor *mean = layer->running_mean, *var = layer->running_var;
+        if (!mean || !var) return fail(MS_E_NULL, "BN-eval needs running_mean and running_var");
+        if ((st = check_tensor(mean, "running_mean", 1, need_data))) return st;
+        if ((st = check_tensor(var, "running_var", 1, need_data))) return st;
+        const ms_tensor *ps[4] = {W, b, mean, var};
+        const char *nm[4] = {"W (gamma)", "b (beta)", "running_mean", "running_var"};
+        for (int i = 0; i < 4; ++i) {
+            if (!ps[i]) continue;
+            if (i < 2 && (st = check_tensor(ps[i], nm[i], 1, need_data))) return st;
+            if (ps[i]->dtype != x->dtype) return fail(MS_E_DTYPE, "%s dtype differs from x", nm[i]);
+            if (ps[i]->shape[0] != C) return fail(MS_E_SHAPE, "%s must have C elements", nm[i]);
+            if (!is_contig1(ps[i])) return fail(MS_E_LAYOUT, "%s must be contiguous", nm[i]);
+        }
+        if (!(layer->eps >= 0.f) || !std::isfinite(layer->eps)) return fail(MS_E_ARG, "eps must be finite and >= 0");
+        if (y) {
+            if ((st = check_tensor(y, "y", nd, need_data))) return st;
+            if (y->dtype != x->dtype) return fail(MS_E_DTYPE, "y dtype differs from x");
+            if (!same_shape(x, y)) return fail(MS_E_SHAPE, "y must have the shape of x");
+            if (nd == 4 && !is_nhwc(y)) return fail(MS_E_LAYOUT, "y must be channels-last (NHWC)");
+            if (nd == 2 && !is_rowmajor2(y)) return fail(MS_E_LAYOUT, "y must be row-major");
+        }
+        pl->dtype = x->dtype;
+        pl->C = (int)C;
+        pl->rows = C > 0 ? numel(x) / C : 0;
+        pl->x_bytes = (uint64_t)numel(x) * elt_size(x->dtype);
+        pl->w_bytes = W ? (uint64_t)C * elt_size(x->dtype) : 0;
+        pl->stat_bytes = (uint64_t)C * elt_size(x->dtype);
+        return MS_OK;
+    }
+    case MS_AVGPOOL: {
+        if (W || b) return fail(MS_E_ARG, "avgpool takes no W or b");
+        if (mask & ~(uint32_t)MS_RG_INPUT) return fail(MS_E_MASK, "avgpool has no parameters");
+        if ((st = check_tensor(x, "x", 4, need_data))) return st;
+        if (!is_nhwc(x)) return fail(MS_E_LAYOUT, "x must be channels-last (NHWC)");
+        const int64_t N = x->shape[0], C = x->shape[1], L = x->shape[2] * x->shape[3];
+        if (C < 1 || L < 1) return fail(MS_E_SHAPE, "avgpool needs C, H, W >= 1");
+        if (y) {
+            if ((st = check_tensor(y, "y", 2, need_data))) return st;
+            if (y->dtype != x->dtype) return fail(MS_E_DTYPE, "y dtype differs from x");
+            if (y->shape[0] != N || y->shape[1] != C) return fail(MS_E_SHAPE, "y must be [N, C]");
+            if (!is_rowmajor2(y)) return fail(MS_E_LAYOUT, "y must be row-major");
+        }
+        pl->dtype = x->dtype;
+        pl->C = (int)C;
+        pl->L = (int)L;
+        pl->Nb = (int)N;
+        pl->rows = N * L;
+        pl->x_bytes = (uint64_t)numel(x) * elt_size(x->dtype);
+        return MS_OK;
+    }
+    default:
+        return fail(MS_E_ARG, "unknown layer kind %d", layer->kind);
+    }
+}
+
+// The save rule.  Returns MS_SAVED_* bits for `mask` under `policy`.
+uint32_t borrowed_bits(int32_t kind, uint32_t mask, int32_t policy, bool has_w, bool has_b) {
+    if (policy == MS_POLICY_ALL_TRUE)
+        mask = MS_RG_INPUT | (has_w ? (uint32_t)MS_RG_WEIGHT : 0u) | (has_b ? (uint32_t)MS_RG_BIAS : 0u);
+    if (mask == 0) return 0;
+    const bool in = mask & MS_RG_INPUT, w = mask & MS_RG_WEIGHT;
+    switch (kind) {
+    case MS_CONV2D:
+        if (policy == MS_POLICY_PYTORCH_DEFAULT) return MS_SAVED_X | MS_SAVED_W;
+        return (w ? (uint32_t)MS_SAVED_X : 0u) | (in ? (uint32_t)MS_SAVED_W : 0u);
+    case MS_LINEAR:   // PyTorch's Linear is already selective (App. B)
+        return (w ? (uint32_t)MS_SAVED_X : 0u) | (in ? (uint32_t)MS_SAVED_W : 0u);
+    case MS_BN_EVAL:
+        if (policy == MS_POLICY_PYTORCH_DEFAULT)
+            return MS_SAVED_X | (has_w ? (uint32_t)MS_SAVED_W : 0u) | MS_SAVED_MEAN | MS_SAVED_VAR;
+        return (w ? (uint32_t)(MS_SAVED_X | MS_SAVED_MEAN) : 0u) | (in && has_w ? (uint32_t)MS_SAVED_W : 0u) |
+               ((in || w) ? (uint32_t)MS_SAVED_VAR : 0u);
+    default:
+        return 0;
+    }
+}
+
+uint32_t kernel_bits(int32_t kind, uint32_t mask) {
+    uint32_t k = 0;
+    if (mask & MS_RG_INPUT) k |= MS_K_DGRAD;
+    if (kind != MS_AVGPOOL) {
+        if (mask & MS_RG_WEIGHT) k |= MS_K_WGRAD;
+        if (mask & MS_RG_BIAS) k |= MS_K_BGRAD;
+    }
+    return k;
+}
+
+size_t backward_workspace(const Plan &pl, uint32_t kernels) {
+    size_t ws = 0;
+    if (pl.kind == MS_CONV2D || pl.kind == MS_LINEAR) {
+        if (kernels & MS_K_WGRAD) ws = std::max(ws, ms::conv_wgrad_workspace(pl.dtype, pl.g));
+        if (kernels & MS_K_BGRAD) ws = std::max(ws, ms::colsum_workspace(pl.dtype, pl.rows, pl.g.K));
+    } else if (pl.kind == MS_BN_EVAL) {
+        if (kernels & (MS_K_WGRAD | MS_K_BGRAD)) ws = ms::bn_bwd_workspace(pl.dtype, pl.rows, pl.C);
+    }
+    return ws;
+}
+
+ms_account make_account(const Plan &pl, uint32_t mask, uint32_t borrowed, uint32_t kernels) {
+    ms_account a{};
+    a.mask = mask;
+    a.borrowed = borrowed;
+    a.kernels = kernels;
+    a.saved_activation_bytes = (borrowed & MS_SAVED_X) ? pl.x_bytes : 0;
+    uint64_t pb = 0;
+    if (borrowed & MS_SAVED_W) pb += pl.w_bytes;
+    if (borrowed & MS_SAVED_MEAN) pb += pl.stat_bytes;
+    if (borrowed & MS_SAVED_VAR) pb += pl.stat_bytes;
+    a.referenced_param_bytes = pb;
+    a.transient_workspace_bytes = backward_workspace(pl, kernels);
+    return a;
+}
+
+ms_status hip_fail(int err, const char *what) {
+    return fail(MS_E_HIP, "%s failed with HIP error %d", what, err);
+}
+
+}  // namespace
+
+struct ms_record {
+    uint32_t magic;
+    Plan plan;
+    float eps;
+    ms_tensor x, W, b, mean, var, y;   // data non-NULL only for borrowed tensors
+    ms_account acct;
+    bool consumed;
+    bool released;
+};
+
+namespace {
+
+void release(ms_record *r) {
+    if (!r->released) {
+        ledger_sub(r->acct.saved_activation_bytes);
+        r->released = true;
+        r->x.data = nullptr;
+        r->W.data = nullptr;
+        r->mean.data = nullptr;
+        r->var.data = nullptr;
+    }
+}
+
+ms_status check_grad(const ms_tensor *g, const ms_tensor *primal, const char *name, int32_t kind) {
+    ms_status st = check_tensor(g, name, primal->ndim, true);
+    if (st) return st;
+    if (g->dtype != primal->dtype) return fail(MS_E_DTYPE, "%s dtype must match its primal", name);
+    if (!same_shape(g, primal)) return fail(MS_E_SHAPE, "%s shape must match its primal", name);
+    if (g->ndim == 4 && !is_nhwc(g)) return fail(MS_E_LAYOUT, "%s must be channels-last", name);
+    if (g->ndim == 2 && !is_rowmajor2(g)) return fail(MS_E_LAYOUT, "%s must be row-major", name);
+    if (g->ndim == 1 && !is_contig1(g)) return fail(MS_E_LAYOUT, "%s must be contiguous", name);
+    (void)kind;
+    return MS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_tensor *W,
+                           const ms_tensor *b, uint32_t mask, const ms_tensor *y, ms_record **rec,
+                           void *stream) {
+    clear_err();
+    if (!rec) return fail(MS_E_NULL, "rec is NULL");
+    *rec = nullptr;
+    if (!y) return fail(MS_E_NULL, "y is NULL");
+    Plan pl;
+    ms_status st = validate_forward(layer, x, W, b, mask, y, true, &pl);
+    if (st) return st;
+    const uint32_t borrowed = borrowed_bits(pl.kind, mask, MS_POLICY_SELECTIVE, pl.has_w, pl.has_b);
+    const uint32_t kernels = kernel_bits(pl.kind, mask);
+    ms_record *r = nullptr;
+    if (mask != 0) {
+        r = new (std::nothrow) ms_record();
+        if (!r) return fail(MS_E_NOMEM, "record allocation failed");
+    }
+    int err = 0;
+    switch (pl.kind) {
+    case MS_CONV2D:
+    case MS_LINEAR:
+        err = ms::launch_conv_fwd(pl.dtype, pl.g, x->data, W->data, b ? b->data : nullptr, y->data, stream);
+        break;
+    case MS_BN_EVAL:
+        err = ms::launch_bn_fwd(pl.dtype, x->data, layer->running_mean->data, layer->running_var->data,
+                                W ? W->data : nullptr, b ? b->data : nullptr, layer->eps, pl.rows, pl.C,
+                                y->data, stream);
+        break;
+    case MS_AVGPOOL:
+        err = ms::launch_avgpool_fwd(pl.dtype, x->data, pl.Nb, pl.L, pl.C, y->data, stream);
+        break;
+    }
+    if (err) {
+        delete r;
+        return hip_fail(err, "forward launch");
+    }
+    if (!r) return MS_OK;
+    r->magic = kMagic;
+    r->plan = pl;
+    r->eps = layer->eps;
+    r->x = shape_only(x);
+    r->y = shape_only(y);
+    std::memset(&r->W, 0, sizeof r->W);
+    std::memset(&r->b, 0, sizeof r->b);
+    std::memset(&r->mean, 0, sizeof r->mean);
+    std::memset(&r->var, 0, sizeof r->var);
+    if (W) r->W = shape_only(W);
+    if (b) r->b = shape_only(b);
+    if (pl.kind == MS_BN_EVAL) {
+        r->mean = shape_only(layer->running_mean);
+        r->var = shape_only(layer->running_var);
+    }
+    if (borrowed & MS_SAVED_X) r->x.data = x->data;
+    if (borrowed & MS_SAVED_W) r->W.data = W->data;
+    if (borrowed & MS_SAVED_MEAN) r->mean.data = layer->running_mean->data;
+    if (borrowed & MS_SAVED_VAR) r->var.data = layer->running_var->data;
+    r->acct = make_account(pl, mask, borrowed, kernels);
+    r->consumed = false;
+    r->released = false;
+    ledger_add(r->acct.saved_activation_bytes);
+    g_records.fetch_add(1);
+    *rec = r;
+    return MS_OK;
+}
+
+ms_status ms_layer_backward(ms_record *r, const ms_tensor *grad_y, const ms_tensor *grad_x,
+                            const ms_tensor *grad_W, const ms_tensor *grad_b, void *stream) {
+    clear_err();
+    if (!r) return fail(MS_E_NULL, "record is NULL");
+    if (r->magic != kMagic) return fail(MS_E_ARG, "not a live record");
+    if (r->consumed) return fail(MS_E_CONSUMED, "backward already ran on this record");
+    const uint32_t mask = r->acct.mask;
+    const Plan &pl = r->plan;
+    if ((grad_x != nullptr) != bool(mask & MS_RG_INPUT))
+        return fail(MS_E_MASK, "grad_x must be given exactly when the INPUT bit is set");
+    if ((grad_W != nullptr) != bool(mask & MS_RG_WEIGHT))
+        return fail(MS_E_MASK, "grad_W must be given exactly when the WEIGHT bit is set");
+    if ((grad_b != nullptr) != bool(mask & MS_RG_BIAS))
+        return fail(MS_E_MASK, "grad_b must be given exactly when the BIAS bit is set");
+    ms_status st = check_grad(grad_y, &r->y, "grad_y", pl.kind);
+    if (st) return st;
+    if (grad_x && (st = check_grad(grad_x, &r->x, "grad_x", pl.kind))) return st;
+    if (grad_W && (st = check_grad(grad_W, &r->W, "grad_W", pl.kind))) return st;
+    if (grad_b && (st = check_grad(grad_b, &r->b, "grad_b", pl.kind))) return st;
+
+    const uint32_t kernels = r->acct.kernels;
+    void *ws = nullptr;
+    const size_t ws_bytes = backward_workspace(pl, kernels);
+    if (ws_bytes) {
+        int werr = 0;
+        ws = ms::workspace_get(stream, ws_bytes, &werr);
+        if (!ws) return werr == 1 ? fail(MS_E_NOMEM, "workspace of %zu bytes unavailable", ws_bytes)
+                                  : hip_fail(ms::device_last_error(), "workspace");
+    }
+    int err = 0;
+    const void *dy = grad_y->data;
+    switch (pl.kind) {
+    case MS_CONV2D:
+    case MS_LINEAR:
+        if (!err && (kernels & MS_K_DGRAD)) err = ms::launch_conv_dgrad(pl.dtype, pl.g, dy, r->W.data, grad_x->data, stream);
+        if (!err && (kernels & MS_K_WGRAD)) err = ms::launch_conv_wgrad(pl.dtype, pl.g, dy, r->x.data, grad_W->data, ws, stream);
+        if (!err && (kernels & MS_K_BGRAD)) err = ms::launch_colsum(pl.dtype, dy, pl.rows, pl.g.K, grad_b->data, ws, stream);
+        break;
+    case MS_BN_EVAL:
+        err = ms::launch_bn_bwd(pl.dtype, dy, (kernels & MS_K_WGRAD) ? r->x.data : nullptr,
+                                (kernels & MS_K_WGRAD) ? r->mean.data : nullptr, r->var.data,
+                                (kernels & MS_K_DGRAD) ? r->W.data : nullptr, r->eps, pl.rows, pl.C,
+                                grad_x ? grad_x->data : nullptr, grad_W ? grad_W->data : nullptr,
+                                grad_b ? grad_b->data : nullptr, ws, stream);
+        break;
+    case MS_AVGPOOL:
+        if (kernels & MS_K_DGRAD) err = ms::launch_avgpool_bwd(pl.dtype, dy, pl.Nb, pl.L, pl.C, grad_x->data, stream);
+        break;
+    }
+    if (err) return hip_fail(err, "backward launch");
+    r->consumed = true;
+    release(r);
+    return MS_OK;
+}
+
+ms_status ms_record_account(const ms_record *r, ms_account *out) {
+    clear_err();
+    if (!r || !out) return fail(MS_E_NULL, "NULL argument");
+    if (r->magic != kMagic) return fail(MS_E_ARG, "not a live record");
+    *out = r->acct;
+    return MS_OK;
+}
+
+void ms_record_free(ms_record *r) {
+    if (!r || r->magic != kMagic) return;
+    release(r);
+    r->magic = 0;
+    g_records.fetch_sub(1);
+    delete r;
+}
+
+ms_status ms_ledger_read(uint64_t *live, uint64_t *peak) {
+    clear_err();
+    if (!live || !peak) return fail(MS_E_NULL, "NULL argument");
+    *live = g_live.load();
+    *peak = g_peak.load();
+    return MS_OK;
+}
+
+ms_status ms_ledger_reset(void) {
+    clear_err();
+    g_peak.store(g_live.load());
+    return MS_OK;
+}
+
+ms_status ms_policy_account(const ms_layer *layer, const ms_tensor *x, const ms_tensor *W,
+                            const ms_tensor *b, uint32_t mask, int32_t policy, ms_account *out) {
+    clear_err();
+    if (!out) return fail(MS_E_NULL, "out is NULL");
+    if (policy < MS_POLICY_SELECTIVE || policy > MS_POLICY_ALL_TRUE) return fail(MS_E_ARG, "unknown policy");
+    Plan pl;
+    ms_status st = validate_forward(layer, x, W, b, mask, nullptr, false, &pl);
+    if (st) return st;
+    uint32_t eff = mask;
+    if (policy == MS_POLICY_ALL_TRUE) {
+        eff = MS_RG_INPUT;
+        if (pl.kind != MS_AVGPOOL) eff |= (W ? (uint32_t)MS_RG_WEIGHT : 0u) | (b ? (uint32_t)MS_RG_BIAS : 0u);
+    }
+    const uint32_t borrowed = borrowed_bits(pl.kind, mask, policy, pl.has_w, pl.has_b);
+    *out = make_account(pl, eff, borrowed, kernel_bits(pl.kind, eff));
+    return MS_OK;
+}
+
+const char *ms_status_str(int32_t s) {
+    switch (s) {
+    case MS_OK: return "ok";
+    case MS_E_NULL: return "null pointer";
+    case MS_E_MASK: return "invalid mask or gradient set";
+    case MS_E_SHAPE: return "shape mismatch";
+    case MS_E_DTYPE: return "unsupported dtype";
+    case MS_E_LAYOUT: return "unsupported memory layout";
+    case MS_E_UNSUPPORTED: return "unsupported configuration";
+    case MS_E_CONSUMED: return "record already consumed";
+    case MS_E_NOMEM: return "out of device memory";
+    case MS_E_HIP: return "HIP error";
+    case MS_E_ARG: return "invalid argument";
+    default: return "unknown status";
+    }
+}
+
+const char *ms_last_error(void) { return g_err.c_str(); }
+
+const char *ms_version(void) { return "memsave-gfx950 0.1.0"; }
+
+void ms_testing_fail_next_workspace(int32_t n) { ms::workspace_fail_next(n); }
+
+int64_t ms_testing_live_records(void) { return g_records.load(); }
+
+}  // extern "C"

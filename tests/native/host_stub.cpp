@@ -1,0 +1,150 @@
+// Stub kernel launchers for host-only tests of the runtime (memsave.cpp).
+//
+// Linked in place of the HIP launchers, they launch nothing: each checks
+// that every pointer the real kernel would dereference for the requested
+// outputs is non-null and 16-byte-or-better plausible, logs the call, and
+// returns 0 -- or 77 when the host runtime handed a kernel a pointer it
+// must not use.  The workspace comes from host memory that nobody touches.
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../paper_2404_12406_amd/csrc/device.h"
+
+namespace {
+std::mutex g_mu;
+std::string g_log;
+std::string g_violation;
+int g_fail_next = 0;
+std::vector<void *> g_ws;
+struct Freer {
+    ~Freer() {
+        for (void *p : g_ws) std::free(p);
+    }
+} g_freer;
+
+void log(const char *s) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_log += s;
+    g_log += ';';
+}
+
+int need(bool ok, const char *what) {
+    if (ok) return 0;
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_violation += what;
+    g_violation += ';';
+    return 77;
+}
+}  // namespace
+
+extern "C" {
+const char *stub_log() { return g_log.c_str(); }
+const char *stub_violations() { return g_violation.c_str(); }
+void stub_reset() {
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_log.clear();
+    g_violation.clear();
+}
+}
+
+namespace ms {
+
+int launch_conv_fwd(int, const ConvGeom &g, const void *x, const void *w, const void *, void *y, void *) {
+    log("conv_fwd");
+    const long long out = (long long)g.N * g.P * g.Q * g.K;
+    const long long red = (long long)g.R * g.S * g.C;
+    int e = 0;
+    if (out > 0) e |= need(y, "conv_fwd:y");
+    if (out > 0 && red > 0) e |= need(x && w, "conv_fwd:x,w");
+    return e;
+}
+
+int launch_conv_dgrad(int, const ConvGeom &g, const void *dy, const void *w, void *dx, void *) {
+    log("conv_dgrad");
+    const long long out = (long long)g.N * g.H * g.W * g.C;
+    int e = 0;
+    if (out > 0) e |= need(dx && w, "conv_dgrad:dx,w");
+    if (out > 0 && (long long)g.N * g.P * g.Q * g.K > 0) e |= need(dy, "conv_dgrad:dy");
+    return e;
+}
+
+size_t conv_wgrad_workspace(int, const ConvGeom &g) {
+    const long long red = (long long)g.N * g.P * g.Q;
+    return red > 4096 ? (size_t)4 * g.K * g.R * g.S * g.C * 4 : 0;
+}
+
+int launch_conv_wgrad(int dtype, const ConvGeom &g, const void *dy, const void *x, void *dw, void *ws, void *) {
+    log("conv_wgrad");
+    int e = 0;
+    if ((long long)g.K * g.R * g.S * g.C > 0) e |= need(dw, "conv_wgrad:dw");
+    if ((long long)g.N * g.P * g.Q > 0) e |= need(dy && x, "conv_wgrad:dy,x");
+    if (conv_wgrad_workspace(dtype, g) > 0) e |= need(ws, "conv_wgrad:ws");
+    return e;
+}
+
+size_t colsum_workspace(int, int64_t, int cols) { return (size_t)cols * 4 * 8; }
+
+int launch_colsum(int, const void *in, int64_t rows, int cols, void *out, void *ws, void *) {
+    log("colsum");
+    int e = 0;
+    if (cols > 0) e |= need(out && ws, "colsum:out,ws");
+    if (rows > 0 && cols > 0) e |= need(in, "colsum:in");
+    return e;
+}
+
+int launch_bn_fwd(int, const void *x, const void *mean, const void *var, const void *, const void *, float,
+                  int64_t rows, int C, void *y, void *) {
+    log("bn_fwd");
+    if (rows > 0 && C > 0) return need(x && y && mean && var, "bn_fwd:x,y,mean,var");
+    return 0;
+}
+
+size_t bn_bwd_workspace(int, int64_t, int C) { return (size_t)C * 4 * 16; }
+
+int launch_bn_bwd(int, const void *dy, const void *x, const void *mean, const void *var, const void *gamma,
+                  float, int64_t rows, int C, void *dx, void *dgamma, void *dbeta, void *ws, void *) {
+    (void)gamma;
+    log("bn_bwd");
+    int e = 0;
+    if (rows > 0 && C > 0) e |= need(dy, "bn_bwd:dy");
+    if (dx || dgamma) e |= need(var, "bn_bwd:var");
+    if (dgamma) e |= need(x && mean, "bn_bwd:x,mean");
+    if (dgamma || dbeta) e |= need(ws, "bn_bwd:ws");
+    return e;
+}
+
+int launch_avgpool_fwd(int, const void *x, int N, int, int C, void *y, void *) {
+    log("avgpool_fwd");
+    return (N > 0 && C > 0) ? need(x && y, "avgpool_fwd:x,y") : 0;
+}
+
+int launch_avgpool_bwd(int, const void *dy, int N, int L, int C, void *dx, void *) {
+    log("avgpool_bwd");
+    return (N > 0 && C > 0 && L > 0) ? need(dy && dx, "avgpool_bwd:dy,dx") : 0;
+}
+
+void *workspace_get(void *, size_t bytes, int *err) {
+    *err = 0;
+    if (bytes == 0) return nullptr;
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (g_fail_next > 0) {
+        --g_fail_next;
+        *err = 1;
+        return nullptr;
+    }
+    void *p = std::malloc(bytes);
+    g_ws.push_back(p);
+    return p;
+}
+
+void workspace_fail_next(int n) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_fail_next = n;
+}
+
+int device_last_error() { return 0; }
+
+}  // namespace ms

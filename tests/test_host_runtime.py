@@ -1,0 +1,365 @@
+"""Host-only tests of the runtime (validation, save rule, records, ledger,
+launch plan) and of the C ABI's exports.  No GPU: the runtime is linked with
+stub launchers (tests/native/host_stub.cpp) that launch nothing and check
+that every pointer a kernel would dereference for the requested outputs is
+present.  The save rule is compared bit-exactly with the oracle's closed
+form; the exports with every declaration in include/*.h."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2404_12406_amd._lib as L
+from oracle import policy as P
+from synth import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+NATIVE = os.path.join(ROOT, "tests", "native")
+BUILD = os.path.join(NATIVE, "_build")
+STUB_SO = os.path.join(BUILD, "libmemsave_hoststub.so")
+DT = {"f32": L.MS_F32, "bf16": L.MS_BF16}
+KIND = {"conv2d": L.MS_CONV2D, "linear": L.MS_LINEAR, "bn_eval": L.MS_BN_EVAL, "avgpool": L.MS_AVGPOOL}
+FAKE = 0x7f0000000000  # a 256-byte aligned address nobody dereferences
+
+
+def _build_stub():
+    os.makedirs(BUILD, exist_ok=True)
+    srcs = [os.path.join(ROOT, "paper_2404_12406_amd", "csrc", "memsave.cpp"), os.path.join(NATIVE, "host_stub.cpp")]
+    tmp = STUB_SO + f".tmp{os.getpid()}"
+    subprocess.run(["g++", "-O1", "-g", "-std=c++17", "-fPIC", "-shared", "-Wall", "-I", os.path.join(ROOT, "include"),
+                    *srcs, "-o", tmp], check=True)
+    os.replace(tmp, STUB_SO)
+
+
+@pytest.fixture(scope="module")
+def stub():
+    _build_stub()
+    lib = L.configure(ctypes.CDLL(STUB_SO))
+    lib.stub_log.restype = ctypes.c_char_p
+    lib.stub_violations.restype = ctypes.c_char_p
+    return lib
+
+
+# ------------------------------------------------------------------ helpers
+def tdesc(shape, dtype="bf16", layout="auto", data=True, addr=FAKE):
+    t = L.MsTensor()
+    t.data = addr if data else None
+    t.dtype = DT[dtype] if isinstance(dtype, str) else dtype
+    t.ndim = len(shape)
+    for i, s in enumerate(shape):
+        t.shape[i] = s
+    if len(shape) == 4 and layout in ("auto", "nhwc"):
+        N, C, H, W = shape
+        st = (H * W * C, 1, W * C, C)
+    else:
+        st, acc = [], 1
+        for s in reversed(shape):
+            st.append(acc)
+            acc *= max(s, 1)
+        st = tuple(reversed(st))
+    for i, s in enumerate(st):
+        t.stride[i] = s
+    return t
+
+
+def ref(t):
+    return ctypes.byref(t) if t is not None else None
+
+
+class LayerArgs:
+    """MsLayer + tensors of one layer description (fake device pointers)."""
+
+    def __init__(self, spec: wl.LayerSpec, dtype, data=True, addr=FAKE):
+        self.spec = spec
+        self.layer = L.MsLayer()
+        self.layer.kind = KIND[spec.kind]
+        self.layer.stride[0], self.layer.stride[1] = spec.stride
+        self.layer.pad[0], self.layer.pad[1] = spec.pad
+        self.layer.eps = spec.eps
+        self.x = tdesc(spec.in_shape, dtype, data=data, addr=addr)
+        ws = spec.weight_shape()
+        self.W = tdesc(ws, dtype, data=data, addr=addr) if ws is not None else None
+        has_b = spec.has_bias and spec.kind != "avgpool"
+        self.b = tdesc((spec.out_ch if spec.kind != "bn_eval" else spec.in_shape[1],), dtype, data=data, addr=addr) if has_b else None
+        self.y = tdesc(spec.out_shape(), dtype, data=data, addr=addr)
+        if spec.kind == "bn_eval":
+            C = spec.in_shape[1]
+            self.mean = tdesc((C,), dtype, data=data, addr=addr)
+            self.var = tdesc((C,), dtype, data=data, addr=addr)
+            self.layer.running_mean = ctypes.pointer(self.mean)
+            self.layer.running_var = ctypes.pointer(self.var)
+
+
+def _numel(shape):
+    n = 1
+    for s in shape:
+        n *= s
+    return n
+
+
+def _all_layers():
+    out = []
+    for name, w in wl.all_workloads().items():
+        seen = set()
+        for l in w.layers:
+            key = (l.kind, l.in_shape, l.out_ch, l.ksize, l.stride, l.pad, l.has_bias)
+            if key in seen:
+                continue
+            seen.add(key)
+            out.append((f"{name}:{l.name}", l, w.dtype))
+    return out
+
+
+ALL_LAYERS = _all_layers()
+
+
+# ------------------------------------------------------------------ exports
+def _declared(headers):
+    names = set()
+    for h in headers:
+        txt = open(h).read()
+        txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+        names |= set(re.findall(r"\b(ms_[a-z_]+)\s*\(", txt))
+    return names
+
+
+def test_headers_declare_what_the_binding_knows():
+    hdrs = [os.path.join(ROOT, "include", f) for f in os.listdir(os.path.join(ROOT, "include")) if f.endswith(".h")]
+    assert _declared(hdrs) == set(L.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    if not os.path.exists(L.LIB_PATH):
+        pytest.skip("libmemsave.so not built")
+    hdrs = [os.path.join(ROOT, "include", f) for f in os.listdir(os.path.join(ROOT, "include")) if f.endswith(".h")]
+    lib = ctypes.CDLL(L.LIB_PATH)
+    for name in _declared(hdrs):
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", L.LIB_PATH], capture_output=True, text=True).stdout
+    for name in _declared(hdrs):
+        assert re.search(rf"\bT {name}$", out, re.M), name
+
+
+def test_real_library_policy_without_gpu():
+    if not os.path.exists(L.LIB_PATH):
+        pytest.skip("libmemsave.so not built")
+    lib = L.load()
+    spec = wl.single_conv_f32().layers[0]
+    a = LayerArgs(spec, "f32", data=False)
+    acct = L.MsAccount()
+    assert lib.ms_policy_account(ctypes.byref(a.layer), ref(a.x), ref(a.W), ref(a.b), 1, 1, ctypes.byref(acct)) == 0
+    assert acct.saved_activation_bytes == 524288
+    assert lib.ms_version().decode().startswith("memsave")
+
+
+# ------------------------------------------------------------------ save rule
+@pytest.mark.parametrize("label,spec,dtype", ALL_LAYERS, ids=[a[0] for a in ALL_LAYERS])
+def test_policy_account_matches_closed_form(stub, label, spec, dtype):
+    a = LayerArgs(spec, dtype, data=False)
+    masks = [0, 1] if spec.kind == "avgpool" else range(8)
+    for mask in masks:
+        if (mask & 4) and a.b is None:
+            continue
+        for pol in (P.SELECTIVE, P.PYTORCH_DEFAULT, P.ALL_TRUE):
+            acct = L.MsAccount()
+            st = stub.ms_policy_account(ctypes.byref(a.layer), ref(a.x), ref(a.W), ref(a.b), mask, pol,
+                                        ctypes.byref(acct))
+            assert st == 0, stub.ms_last_error()
+            want = P.saved_activation_bytes(spec.kind, mask, _numel(spec.in_shape), dtype, pol,
+                                            a.W is not None, a.b is not None)
+            assert acct.saved_activation_bytes == want, (label, mask, pol)
+            sv = P.saved_tensors(spec.kind, mask, pol, a.W is not None, a.b is not None)
+            assert bool(acct.borrowed & L.MS_SAVED_X) == sv["x"]
+
+
+# ------------------------------------------------------------------ records + plan
+def _grads(a, mask):
+    gx = tdesc(a.spec.in_shape, a.x.dtype) if mask & 1 else None
+    gw = tdesc(a.spec.weight_shape(), a.x.dtype) if mask & 2 else None
+    gb = tdesc((a.b.shape[0],), a.x.dtype) if mask & 4 else None
+    return gx, gw, gb
+
+
+@pytest.mark.parametrize("label,spec,dtype", ALL_LAYERS, ids=[a[0] for a in ALL_LAYERS])
+def test_forward_backward_plan(stub, label, spec, dtype):
+    a = LayerArgs(spec, dtype)
+    masks = [0, 1] if spec.kind == "avgpool" else range(8)
+    fwd_name = {"conv2d": "conv_fwd", "linear": "conv_fwd", "bn_eval": "bn_fwd", "avgpool": "avgpool_fwd"}[spec.kind]
+    for mask in masks:
+        if (mask & 4) and a.b is None:
+            continue
+        stub.stub_reset()
+        live0, peak0 = ctypes.c_uint64(), ctypes.c_uint64()
+        stub.ms_ledger_read(ctypes.byref(live0), ctypes.byref(peak0))
+        h = ctypes.c_void_p()
+        st = stub.ms_layer_forward(ctypes.byref(a.layer), ref(a.x), ref(a.W), ref(a.b), mask, ref(a.y),
+                                   ctypes.byref(h), None)
+        assert st == 0, stub.ms_last_error()
+        assert stub.stub_log().decode() == fwd_name + ";"
+        if mask == 0:
+            assert not h.value
+            continue
+        acct = L.MsAccount()
+        stub.ms_record_account(h, ctypes.byref(acct))
+        want = P.saved_activation_bytes(spec.kind, mask, _numel(spec.in_shape), dtype, P.SELECTIVE)
+        assert acct.saved_activation_bytes == want
+        live, peak = ctypes.c_uint64(), ctypes.c_uint64()
+        stub.ms_ledger_read(ctypes.byref(live), ctypes.byref(peak))
+        assert live.value - live0.value == want
+        stub.stub_reset()
+        gy = tdesc(spec.out_shape(), dtype)
+        gx, gw, gb = _grads(a, mask)
+        st = stub.ms_layer_backward(h, ref(gy), ref(gx), ref(gw), ref(gb), None)
+        assert st == 0, (stub.ms_last_error(), stub.stub_violations())
+        assert stub.stub_violations().decode() == ""
+        log = stub.stub_log().decode().split(";")[:-1]
+        plan = P.launched(spec.kind, mask)
+        if spec.kind in ("conv2d", "linear"):
+            assert ("conv_dgrad" in log) == plan["dgrad"]
+            assert ("conv_wgrad" in log) == plan["wgrad"]
+            assert ("colsum" in log) == plan["bgrad"]
+        elif spec.kind == "bn_eval":
+            assert log == ["bn_bwd"]
+        else:
+            assert log == ["avgpool_bwd"]
+        stub.ms_ledger_read(ctypes.byref(live), ctypes.byref(peak))
+        assert live.value == live0.value
+        assert stub.ms_layer_backward(h, ref(gy), ref(gx), ref(gw), ref(gb), None) == L.MS_E_CONSUMED
+        stub.ms_record_free(h)
+    assert stub.ms_testing_live_records() == 0
+
+
+def test_backward_rejects_grad_sets_that_contradict_the_mask(stub):
+    spec = wl.conv_sweep_bf16("11").layers[0]
+    a = LayerArgs(spec, "bf16")
+    for mask in range(1, 8):
+        h = ctypes.c_void_p()
+        assert stub.ms_layer_forward(ctypes.byref(a.layer), ref(a.x), ref(a.W), ref(a.b), mask, ref(a.y),
+                                     ctypes.byref(h), None) == 0
+        gy = tdesc(spec.out_shape())
+        for given in range(8):
+            if given == mask:
+                continue
+            stub.stub_reset()
+            gx, gw, gb = _grads(a, given)
+            assert stub.ms_layer_backward(h, ref(gy), ref(gx), ref(gw), ref(gb), None) == L.MS_E_MASK
+            assert stub.stub_log().decode() == ""          # nothing launched
+        acct = L.MsAccount()
+        stub.ms_record_account(h, ctypes.byref(acct))
+        gx, gw, gb = _grads(a, mask)
+        # wrong grad shape / dtype / layout are caught too
+        if gx is not None:
+            bad = tdesc((1, 2, 3, 4))
+            assert stub.ms_layer_backward(h, ref(gy), ref(bad), ref(gw), ref(gb), None) == L.MS_E_SHAPE
+            badl = tdesc(spec.in_shape, layout="nchw")
+            assert stub.ms_layer_backward(h, ref(gy), ref(badl), ref(gw), ref(gb), None) == L.MS_E_LAYOUT
+            badd = tdesc(spec.in_shape, "f32")
+            assert stub.ms_layer_backward(h, ref(gy), ref(badd), ref(gw), ref(gb), None) == L.MS_E_DTYPE
+        assert stub.ms_layer_backward(h, ref(gy), ref(gx), ref(gw), ref(gb), None) == 0
+        stub.ms_record_free(h)
+
+
+def test_forward_validation_errors_launch_nothing(stub):
+    spec = wl.conv_sweep_bf16("11").layers[0]
+    live0, pk = ctypes.c_uint64(), ctypes.c_uint64()
+    stub.ms_ledger_read(ctypes.byref(live0), ctypes.byref(pk))
+
+    def fwd(a, mask, x=None, W="keep", b="keep", y=None):
+        h = ctypes.c_void_p()
+        stub.stub_reset()
+        st = stub.ms_layer_forward(ctypes.byref(a.layer), ref(x or a.x), ref(a.W if W == "keep" else W),
+                                   ref(a.b if b == "keep" else b), mask, ref(y or a.y), ctypes.byref(h), None)
+        assert stub.stub_log().decode() == "" and not h.value
+        return st
+
+    a = LayerArgs(spec, "bf16")
+    assert fwd(a, 8) == L.MS_E_MASK
+    assert fwd(a, 2, W=None) == L.MS_E_MASK
+    assert fwd(a, 4, b=None) == L.MS_E_MASK
+    assert fwd(a, 1, x=tdesc(spec.in_shape, layout="nchw")) == L.MS_E_LAYOUT
+    assert fwd(a, 1, x=tdesc(spec.in_shape, "f32")) == L.MS_E_DTYPE
+    assert fwd(a, 1, x=tdesc((32, 128, 28, 28))) == L.MS_E_SHAPE
+    assert fwd(a, 1, y=tdesc((32, 256, 27, 28))) == L.MS_E_SHAPE
+    assert fwd(a, 1, x=tdesc(spec.in_shape, data=False)) == L.MS_E_NULL
+    assert fwd(a, 1, x=tdesc(spec.in_shape, 7)) == L.MS_E_DTYPE
+    a.layer.stride[0] = 0
+    assert fwd(a, 1) == L.MS_E_ARG
+    a.layer.stride[0] = 1
+    a.layer.pad[0] = -1
+    assert fwd(a, 1) == L.MS_E_ARG
+    a.layer.pad[0] = 1
+    big = LayerArgs(wl.LayerSpec("linear", "big", (70000, 40000), out_ch=8, has_bias=False), "bf16")
+    assert fwd(big, 1) == L.MS_E_UNSUPPORTED
+    pool = LayerArgs(wl.LayerSpec("avgpool", "p", (2, 8, 4, 4)), "bf16")
+    assert fwd(pool, 2, W=None, b=None) == L.MS_E_MASK
+    bn = LayerArgs(wl.resnet18_shaped_bf16(batch=2, image=32).layers[1], "bf16")
+    bn.layer.running_var = None
+    assert fwd(bn, 1) == L.MS_E_NULL
+    assert "running_var" in stub.ms_last_error().decode()
+    live = ctypes.c_uint64()
+    stub.ms_ledger_read(ctypes.byref(live), ctypes.byref(pk))
+    assert live.value == live0.value
+
+
+def test_workspace_failure_leaves_record_and_ledger_intact(stub):
+    spec = wl.conv_sweep_bf16("01").layers[0]          # W and B trainable: keeps x, needs workspace
+    a = LayerArgs(spec, "bf16")
+    h = ctypes.c_void_p()
+    assert stub.ms_layer_forward(ctypes.byref(a.layer), ref(a.x), ref(a.W), ref(a.b), 6, ref(a.y),
+                                 ctypes.byref(h), None) == 0
+    live1, pk = ctypes.c_uint64(), ctypes.c_uint64()
+    stub.ms_ledger_read(ctypes.byref(live1), ctypes.byref(pk))
+    gy = tdesc(spec.out_shape())
+    _, gw, gb = _grads(a, 6)
+    stub.ms_testing_fail_next_workspace(1)
+    stub.stub_reset()
+    assert stub.ms_layer_backward(h, ref(gy), None, ref(gw), ref(gb), None) == L.MS_E_NOMEM
+    assert stub.stub_log().decode() == ""
+    live2 = ctypes.c_uint64()
+    stub.ms_ledger_read(ctypes.byref(live2), ctypes.byref(pk))
+    assert live2.value == live1.value
+    assert stub.ms_layer_backward(h, ref(gy), None, ref(gw), ref(gb), None) == 0   # retry succeeds
+    stub.ms_record_free(h)
+    stub.ms_record_free(None)
+
+
+def test_ledger_peak_over_a_stack(stub):
+    """Peak retained bytes of the ResNet-18-shaped stack in its 'Input'
+    variant equal the closed form: convs and BN keep nothing, the final
+    Linear keeps its input."""
+    w = wl.resnet18_shaped_bf16(input_requires_grad=True)
+    stub.ms_ledger_reset()
+    live0, pk = ctypes.c_uint64(), ctypes.c_uint64()
+    stub.ms_ledger_read(ctypes.byref(live0), ctypes.byref(pk))
+    stub.ms_ledger_reset()
+    hs = []
+    for spec in w.layers:
+        a = LayerArgs(spec, "bf16")
+        h = ctypes.c_void_p()
+        assert stub.ms_layer_forward(ctypes.byref(a.layer), ref(a.x), ref(a.W), ref(a.b), spec.mask, ref(a.y),
+                                     ctypes.byref(h), None) == 0
+        hs.append(h)
+    live, peak = ctypes.c_uint64(), ctypes.c_uint64()
+    stub.ms_ledger_read(ctypes.byref(live), ctypes.byref(peak))
+    layers = [(l.kind, l.mask, _numel(l.in_shape), "bf16", l.kind != "avgpool", l.has_bias) for l in w.layers]
+    assert peak.value - live0.value == P.stack_saved_bytes(layers, P.SELECTIVE) == 65536
+    for h in hs:
+        stub.ms_record_free(h)
+    stub.ms_ledger_read(ctypes.byref(live), ctypes.byref(peak))
+    assert live.value == live0.value
+
+
+def test_native_driver_under_sanitizers():
+    """The same lifecycle driven from C++ with AddressSanitizer and UBSan."""
+    exe = os.path.join(BUILD, "test_host_runtime")
+    os.makedirs(BUILD, exist_ok=True)
+    subprocess.run(["g++", "-O1", "-g", "-std=c++17", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+                    "-I", os.path.join(ROOT, "include"), os.path.join(ROOT, "paper_2404_12406_amd", "csrc", "memsave.cpp"),
+                    os.path.join(NATIVE, "host_stub.cpp"), os.path.join(NATIVE, "test_host_runtime.cpp"), "-o", exe],
+                   check=True)
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=120,
+                       env={**os.environ, "ASAN_OPTIONS": "detect_leaks=1:abort_on_error=0"})
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "ALL OK" in r.stdout
