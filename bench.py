@@ -1,0 +1,350 @@
+#!/usr/bin/env python3
+"""Benchmark of the selective-differentiation layers on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+Headline step: the bf16 Linear stack X[4096,1024] -> 1024->4096->1024->4096->1024
+with every weight frozen and biases trainable (mask = input + bias per layer):
+four forward GEMMs, then four input-gradient GEMMs and four bias-gradient
+reductions, all through the C ABI of libmemsave.so.  `value` is the
+algorithmic TFLOP/s of the launched contractions (forward + input gradient;
+the weight-gradient GEMMs are skipped by the mask) with every input resident
+in HBM.  The line also carries the ledger's retained activation bytes under
+the selective mask and under an all-true mask, the roofline of the dominant
+kernel (timed with HIP events inside the timed region), the other synthetic
+workloads as context, and the CPU oracle timed on a bounded sample.
+
+One JSON line goes to stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "conv/linear fwd+bwd TFLOP/s (frozen W) + saved-activation bytes vs full AD"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3       # MI355X fp32 (matrix and vector)
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ------------------------------------------------------------------ FLOP / byte accounting
+def layer_flops(spec, mask: int) -> dict:
+    """Algorithmic FLOP (2 x multiply-adds) of the contractions a layer
+    launches: forward always, input gradient iff INPUT, weight gradient iff
+    WEIGHT.  BN, pooling and bias work is not counted."""
+    if spec.kind == "conv2d":
+        n, c, _, _ = spec.in_shape
+        _, k, p, q = spec.out_shape()
+        r, s = spec.ksize
+        f = 2 * n * p * q * k * c * r * s
+    elif spec.kind == "linear":
+        m, kin = spec.in_shape
+        f = 2 * m * kin * spec.out_ch
+    else:
+        return {"fwd": 0, "dgrad": 0, "wgrad": 0}
+    return {"fwd": f, "dgrad": f if mask & 1 else 0, "wgrad": f if mask & 2 else 0}
+
+
+def numel(shape):
+    n = 1
+    for s in shape:
+        n *= s
+    return n
+
+
+# ------------------------------------------------------------------ timing helpers
+def time_chains(chains, steps, warmup, backward=True):
+    import torch
+    for _ in range(warmup):
+        for c in chains:
+            c.forward()
+        if backward:
+            for c in chains:
+                c.backward()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        for c in chains:
+            c.forward()
+        if backward:
+            for c in chains:
+                c.backward()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def ledger_peak_of_forward(chains):
+    """Peak retained activation bytes over one forward of `chains`."""
+    import torch
+    import paper_2404_12406_amd as ms
+    torch.cuda.synchronize()
+    live0, _ = ms.ledger_read()
+    ms.ledger_reset()
+    for c in chains:
+        c.forward()
+    torch.cuda.synchronize()
+    _, peak = ms.ledger_read()
+    return peak - live0
+
+
+def with_masks(w, fn):
+    """A copy of workload w with every layer's mask replaced by fn(layer)."""
+    import copy
+    w2 = copy.deepcopy(w)
+    for l in w2.layers:
+        l.mask = fn(l)
+    return w2
+
+
+def all_true(l):
+    if l.kind == "avgpool":
+        return 1
+    return 1 | 2 | (4 if l.has_bias else 0)
+
+
+# ------------------------------------------------------------------ headline
+def headline(steps, warmup):
+    import torch
+    from synth import draw, gpu
+    from synth import workloads as wl
+
+    w = wl.linear_stack_bf16()
+    ca = draw.chains(w)[0]
+    chain = gpu.build_chain(ca, "bf16")
+    fl = [layer_flops(l, l.mask) for l in w.layers]
+    flop_step = sum(f["fwd"] + f["dgrad"] + f["wgrad"] for f in fl)
+    log(f"[bench] headline {w.name}: {flop_step / 1e9:.2f} GFLOP per step; warmup {warmup}")
+    for _ in range(warmup):
+        chain.forward()
+        chain.backward()
+    torch.cuda.synchronize()
+    # per-launch HIP events around every forward GEMM (the dominant kernel:
+    # one launch per call, on the stream the library launches on)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps * len(chain.prepared))]
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t0.record()
+    k = 0
+    for _ in range(steps):
+        for p in chain.prepared:
+            a, b = evs[k]
+            a.record()
+            p.forward()
+            b.record()
+            k += 1
+        chain.backward()
+    t1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_step = t0.elapsed_time(t1) / steps
+    gemm_ms = [a.elapsed_time(b) for a, b in evs]
+    avg_gemm_ms = sum(gemm_ms) / len(gemm_ms)
+    gemm_flop = fl[0]["fwd"]
+    assert all(f["fwd"] == gemm_flop for f in fl)
+    achieved = gemm_flop / (avg_gemm_ms * 1e-3) / 1e12
+    value = flop_step / (ms_step * 1e-3) / 1e12
+    log(f"[bench] headline {ms_step:.3f} ms/step, {value:.1f} TFLOP/s; forward GEMM avg {avg_gemm_ms * 1e3:.1f} us "
+        f"= {achieved:.1f} TFLOP/s; host wall {wall * 1e3 / steps:.3f} ms/step")
+
+    sel = ledger_peak_of_forward([chain])
+    chain.backward()
+    wt = with_masks(w, all_true)
+    full = gpu.build_chain(draw.chains(wt)[0], "bf16")
+    allb = ledger_peak_of_forward([full])
+    full.backward()
+    torch.cuda.synchronize()
+    del full
+    return {
+        "workload": w,
+        "ms_per_step": ms_step,
+        "value": value,
+        "flop_step": flop_step,
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "kernel": "igemm_kernel<bf16, fwd, 1x1> (Linear forward)",
+                     "flop_per_launch": gemm_flop, "avg_launch_us": round(avg_gemm_ms * 1e3, 2)},
+        "saved": {"selective": sel, "all_true": allb},
+    }
+
+
+# ------------------------------------------------------------------ context workloads
+def run_workload(w, steps, warmup, backward=True):
+    import torch
+    from synth import draw, gpu
+    chains = gpu.build_chains(draw.chains(w), w.dtype)
+    fl = [layer_flops(l, l.mask) for l in w.layers]
+    flop = sum(f["fwd"] + (f["dgrad"] + f["wgrad"] if backward else 0) for f in fl)
+    ms_step = time_chains(chains, steps, warmup, backward)
+    sel = ledger_peak_of_forward(chains)
+    if backward:
+        for c in chains:
+            c.backward()
+    torch.cuda.synchronize()
+    out = {"ms_per_step": round(ms_step, 4), "gflop": round(flop / 1e9, 3),
+           "tflops": round(flop / (ms_step * 1e-3) / 1e12, 2), "saved_selective": sel}
+    del chains
+    torch.cuda.empty_cache()
+    return out
+
+
+def bn_bandwidth(steps, warmup):
+    """BN-eval forward of the ResNet-18-shaped stack's 17 BN layers, each on
+    its own seeded input; HBM bytes = read x + write y."""
+    import torch
+    import paper_2404_12406_amd as ms
+    from synth import draw, gpu
+    from synth import workloads as wl
+    w = wl.resnet18_shaped_bf16()
+    res = []
+    big = torch.empty(1 << 28, dtype=torch.uint8, device="cuda")   # 256 MiB to flush the last-level cache
+    import synth
+    for i, l in enumerate(w.layers):
+        if l.kind != "bn_eval":
+            continue
+        la = draw.layer_arrays(l, "bf16")
+        x = gpu.dev(synth.normal(l.in_shape, 3900 + i, dtype="bf16"), "bf16")
+        spec = ms.BatchNormEval(gpu.dev(la.running_mean, "bf16"), gpu.dev(la.running_var, "bf16"), l.eps)
+        p = ms.PreparedLayer(spec, x, gpu.dev(la.W, "bf16"), gpu.dev(la.b, "bf16"), 0)
+        for _ in range(warmup):
+            p.forward()
+        ts = []
+        for _ in range(steps):
+            big.zero_()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            p.forward()
+            b.record()
+            ts.append((a, b))
+        torch.cuda.synchronize()
+        t = sum(a.elapsed_time(b) for a, b in ts) / len(ts)
+        nbytes = 2 * numel(l.in_shape) * 2
+        res.append({"layer": l.name, "bytes": nbytes, "us": round(t * 1e3, 2),
+                    "GBs": round(nbytes / (t * 1e-3) / 1e9, 1)})
+    del big
+    tot_b = sum(r["bytes"] for r in res)
+    tot_t = sum(r["us"] for r in res) * 1e-6
+    return {"layers": res, "total_bytes": tot_b, "GBs": round(tot_b / tot_t / 1e9, 1),
+            "frac_of_hbm": round(tot_b / tot_t / 1e9 / PEAK_HBM_GBS, 4), "cache": "flushed before each launch"}
+
+
+def extras(steps, warmup):
+    from synth import workloads as wl
+    out = {}
+    steps = max(3, min(steps, 10))
+    warmup = max(1, min(warmup, 3))
+    jobs = [("single_conv2d_f32", wl.single_conv_f32(), True),
+            ("resnet18_shaped_bf16", wl.resnet18_shaped_bf16(), True),
+            ("resnet18_shaped_bf16_input", wl.resnet18_shaped_bf16(input_requires_grad=True), True),
+            ("encoder_linears_bf16", wl.encoder_linears_bf16(), True)]
+    for mk in ("00", "10", "01", "11"):
+        jobs.append((f"conv_sweep_3x3_{mk}", wl.conv_sweep_bf16(mk), True))
+        jobs.append((f"conv_sweep_1x1_{mk}", wl.conv_sweep_bf16(mk, pointwise=True), True))
+    for name, w, bwd in jobs:
+        t0 = time.time()
+        out[name] = run_workload(w, steps, warmup, bwd)
+        log(f"[bench] {name}: {out[name]} ({time.time() - t0:.1f}s)")
+    t0 = time.time()
+    out["bn_eval_forward_resnet18_shaped"] = bn_bandwidth(steps, warmup)
+    log(f"[bench] bn: {out['bn_eval_forward_resnet18_shaped']['GBs']} GB/s ({time.time() - t0:.1f}s)")
+    return out
+
+
+# ------------------------------------------------------------------ CPU baseline
+def cpu_baseline(target_s: float = 12.0):
+    """The oracle (fp64 C loops, OpenMP) on the first `rows` rows of the
+    headline workload: forward, input gradient and bias gradient of the four
+    layers; the rate scales to the whole step by its FLOP count."""
+    import numpy as np
+    import oracle
+    from synth import draw
+    from synth import workloads as wl
+    w = wl.linear_stack_bf16()
+    ca = draw.chains(w)[0]
+
+    def run(rows):
+        x = ca.x[:rows]
+        acts = [x]
+        t = time.perf_counter()
+        for la in ca.layers:
+            acts.append(oracle.round_to(oracle.linear_forward(acts[-1], la.W, la.b), "bf16"))
+        g = ca.grad_y[:rows]
+        for i in range(len(ca.layers) - 1, -1, -1):
+            oracle.linear_bias_grad(g)
+            g = oracle.round_to(oracle.linear_input_grad(g, ca.layers[i].W), "bf16")
+        return time.perf_counter() - t
+
+    per_row = sum(2 * 2 * l.in_shape[1] * l.out_ch for l in w.layers)   # fwd + dgrad
+    t = run(8)
+    rows = int(min(ca.x.shape[0], max(8, 8 * target_s / max(t, 1e-3))))
+    t = run(rows)
+    tflops = rows * per_row / t / 1e12
+    return {"value": round(tflops, 6), "unit": "TFLOP/s", "cores": oracle.threads(), "kind": "oracle",
+            "sample": f"first {rows} of 4096 rows of the Linear stack, forward + input grad + bias grad "
+                      f"of all 4 layers ({rows * per_row / 1e9:.2f} GFLOP in {t:.1f} s, fp64)"}
+
+
+# ------------------------------------------------------------------ main
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-extra", action="store_true", help="skip the context workloads")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the layers need no cross-GPU communication on this "
+              f"path (--gpus {args.gpus} is not supported)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2404_12406_amd as ms
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    log(f"[bench] {ms.version()} on {torch.cuda.get_device_name(0)}")
+    h = headline(args.steps, args.warmup)
+    line = {
+        "metric": METRIC,
+        "value": round(h["value"], 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(h["ms_per_step"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "linear_stack_bf16", "M": 4096, "features": [1024, 4096, 1024, 4096, 1024],
+                   "mask": "input+bias per layer, weights frozen", "flop_per_step": h["flop_step"]},
+        "saved_activation_bytes": {"selective": h["saved"]["selective"], "all_true": h["saved"]["all_true"]},
+        "roofline": h["roofline"],
+    }
+    if not args.no_extra:
+        line["extra"] = extras(args.steps, args.warmup)
+    if not args.no_cpu:
+        log("[bench] cpu baseline (oracle) ...")
+        line["cpu_baseline"] = cpu_baseline()
+        log(f"[bench] cpu baseline {line['cpu_baseline']}")
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

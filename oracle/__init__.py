@@ -286,3 +286,8 @@ def rel_err(got, ref):
     if den == 0.0:
         return 0.0 if num == 0.0 else float("inf")
     return num / den
+
+
+def threads() -> int:
+    """OpenMP threads the oracle's loops use."""
+    return int(_load().orc_threads())

@@ -410,3 +410,16 @@ void orc_round(double *a, i64 n, int dtype)
     for (i64 i = 0; i < n; ++i)
         a[i] = dtype == 1 ? round_to_bf16(a[i]) : (double)(float)a[i];
 }
+
+/* Threads the OpenMP loops above use (reported with CPU timings). */
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+int orc_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

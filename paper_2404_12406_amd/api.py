@@ -269,3 +269,59 @@ def ledger_reset():
 
 def version() -> str:
     return _lib.load().ms_version().decode()
+
+
+# ------------------------------------------------------------------ prepared calls
+class PreparedLayer:
+    """One layer call with its C descriptors built once, for tight loops.
+
+    forward() enqueues ms_layer_forward on the current stream and keeps the
+    raw record; backward() enqueues ms_layer_backward for it and frees it.
+    The object holds references to every tensor it describes, so nothing it
+    points to can be freed while it exists."""
+
+    def __init__(self, spec, x, W=None, b=None, mask: int = 0, y=None,
+                 grad_y=None, grad_x=None, grad_W=None, grad_b=None):
+        extra = (spec.running_mean, spec.running_var) if isinstance(spec, BatchNormEval) else ()
+        _on_gpu(x, W, b, y, grad_y, grad_x, grad_W, grad_b, *extra)
+        self.lib = _lib.load()
+        self.desc = _LayerDesc(spec)
+        if y is None:
+            y = empty_like_layout(output_shape(spec, x, W), x)
+        self.tensors = (x, W, b, y, grad_y, grad_x, grad_W, grad_b)
+        self.y = y
+        self.mask = int(mask)
+        self._d = [tensor_desc(t) for t in self.tensors]
+        self._fa = (ctypes.byref(self.desc.layer),) + tuple(_ptr(d) for d in self._d[:3])
+        self._fy = _ptr(self._d[3])
+        self._ba = tuple(_ptr(d) for d in self._d[4:])
+        self._h = ctypes.c_void_p()
+        self._hp = ctypes.byref(self._h)
+        self._stream = _stream(x.device)
+        self._free = self.lib.ms_record_free
+
+    def forward(self):
+        if self._h.value:
+            self._free(self._h)
+            self._h.value = None
+        check(self.lib.ms_layer_forward(*self._fa, self.mask, self._fy, self._hp, self._stream),
+              "ms_layer_forward")
+
+    def backward(self):
+        if not self._h.value:
+            raise RuntimeError("backward without a live record")
+        check(self.lib.ms_layer_backward(self._h, *self._ba, self._stream), "ms_layer_backward")
+        self._free(self._h)
+        self._h.value = None
+
+    def account(self) -> dict:
+        a = MsAccount()
+        check(self.lib.ms_record_account(self._h, ctypes.byref(a)), "ms_record_account")
+        return a.as_dict()
+
+    def __del__(self):
+        try:
+            if self._h.value:
+                self._free(self._h)
+        except Exception:
+            pass

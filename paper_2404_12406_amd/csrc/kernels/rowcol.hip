@@ -34,8 +34,9 @@ struct RowColPlan {
 
 RowColPlan plan_rowcol(int dtype, int64_t rows, int C, bool vec_ok, int target_blocks) {
     RowColPlan p;
-    p.V = vec_ok ? (dtype == kBF16 ? 8 : 4) : 1;
-    p.nvc = C / p.V;
+    const int V = dtype == kBF16 ? 8 : 4;
+    p.V = (vec_ok && C % V == 0) ? V : 1;   // a row must hold whole vectors
+    p.nvc = std::max(C / p.V, 1);
     p.TC = std::min(p.nvc, 256);
     p.RG = 256 / p.TC;
     p.gx = (p.nvc + p.TC - 1) / p.TC;

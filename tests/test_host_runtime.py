@@ -363,3 +363,40 @@ def test_native_driver_under_sanitizers():
                        env={**os.environ, "ASAN_OPTIONS": "detect_leaks=1:abort_on_error=0"})
     assert r.returncode == 0, r.stdout + r.stderr
     assert "ALL OK" in r.stdout
+
+
+EDGE_SPECS = [
+    wl.LayerSpec("linear", "k0", (5, 0), out_ch=6, has_bias=True),
+    wl.LayerSpec("linear", "odd", (129, 30), out_ch=20, has_bias=True),
+    wl.LayerSpec("linear", "one", (1, 1), out_ch=1, has_bias=True),
+    wl.LayerSpec("linear", "m0", (0, 16), out_ch=8, has_bias=True),
+    wl.LayerSpec("conv2d", "n0", (0, 16, 8, 8), out_ch=8, ksize=(3, 3), pad=(1, 1), has_bias=True),
+    wl.LayerSpec("conv2d", "c3", (2, 3, 30, 29), out_ch=16, ksize=(7, 7), stride=(2, 2), pad=(3, 3), has_bias=True),
+    wl.LayerSpec("conv2d", "c12", (1, 12, 11, 13), out_ch=20, ksize=(3, 2), stride=(3, 2), pad=(0, 1), has_bias=True),
+    wl.LayerSpec("conv2d", "big", (64, 512, 7, 7), out_ch=512, ksize=(3, 3), pad=(1, 1), has_bias=True),
+    wl.LayerSpec("bn_eval", "bn13", (2, 13, 5, 6), has_bias=True),
+    wl.LayerSpec("bn_eval", "bn0", (0, 24, 5, 6), has_bias=True),
+    wl.LayerSpec("bn_eval", "bn2d", (50, 36), has_bias=True),
+]
+
+
+@pytest.mark.parametrize("spec", EDGE_SPECS + [l for _, l, _ in ALL_LAYERS], ids=lambda s: s.name)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_real_library_planners_on_edge_shapes(spec, dtype):
+    """ms_policy_account runs the real launch planners (split-K and
+    reduction workspace sizing) without touching the GPU: every mask and
+    policy must return a result on degenerate and ragged shapes."""
+    if not os.path.exists(L.LIB_PATH):
+        pytest.skip("libmemsave.so not built")
+    lib = L.load()
+    a = LayerArgs(spec, dtype, data=False)
+    for mask in ([0, 1] if spec.kind == "avgpool" else range(8)):
+        if (mask & 4) and a.b is None:
+            continue
+        for pol in (0, 1, 2):
+            acct = L.MsAccount()
+            st = lib.ms_policy_account(ctypes.byref(a.layer), ref(a.x), ref(a.W), ref(a.b), mask, pol,
+                                       ctypes.byref(acct))
+            assert st == 0, lib.ms_last_error()
+            if mask & 4 and pol == 0:          # bias / beta gradients reduce through partials
+                assert acct.transient_workspace_bytes > 0
