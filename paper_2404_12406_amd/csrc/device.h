@@ -30,10 +30,12 @@ int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *
                       void *dx, void *stream);
 
 // dw = weight gradient for grad dy and input x.  Needs conv_wgrad_workspace()
-// bytes of device workspace (may be 0).
-size_t conv_wgrad_workspace(int dtype, const ConvGeom &g);
+// bytes of device workspace (may be 0).  When db is non-null the launcher may
+// also produce the bias gradient db[k] = sum over pixels of dy[.][k] from the
+// operand tiles it already reads; *db_done tells whether it did.
+size_t conv_wgrad_workspace(int dtype, const ConvGeom &g, bool with_db);
 int launch_conv_wgrad(int dtype, const ConvGeom &g, const void *dy, const void *x,
-                      void *dw, void *ws, void *stream);
+                      void *dw, void *db, void *ws, void *stream, bool *db_done);
 
 // out[j] = sum_i in[i][j] for a dense row-major [rows][cols] matrix (bias
 // gradient of conv over N*P*Q rows, of linear over M rows).

@@ -1,0 +1,793 @@
+// bf16 implicit-GEMM kernels for gfx950: the fast path of the three
+// contractions of a layer that is linear in input and weight (Sec. 2.2.1 of
+// the paper) -- forward, input gradient (needs W only) and weight gradient
+// (needs x only) -- for NHWC activations and KRSC filters.  The GEMM views
+// and the stride-phase split of the input gradient are those of igemm.hip.
+//
+// Data movement (per block, 256 threads = 4 waves in a 2 x 2 grid):
+//  * operands go from HBM straight into LDS with buffer_load_dwordx4 ... lds
+//    (no VGPR staging).  Each lane computes the byte offset of its 16-byte
+//    chunk; lanes that fall into padding, a ragged tail or a missing tap use
+//    an offset beyond the buffer's range and the hardware writes zeros.
+//  * STAGES LDS buffers form a ring: tiles kt+1 .. kt+STAGES-1 are in flight
+//    while tile kt feeds the MFMAs (one barrier per BK step).
+//  * operands contiguous along k are stored [row][k] with 16-byte chunks
+//    XOR-swizzled by row and read as MFMA fragments with ds_read_b128;
+//    operands contiguous along m/n are stored [k][mn] with 16-byte slots
+//    swizzled by k-row and read with ds_read_b64_tr_b16, which transposes a
+//    16 x 4 block of b16 within each 16-lane group (two reads = 8 k values).
+//  * v_mfma_f32_32x32x16_bf16 (a single wave issues it at ~92% of the
+//    matrix peak; the 16x16x32 form reaches only ~55%) with the B fragment
+//    as first operand, so each lane ends with groups of 4 consecutive output
+//    columns of one row; the epilogue
+//    packs them to bf16, stages the tile through LDS and writes 16-byte
+//    vectors (fp32 split-K partials are stored as float4 directly).
+//  * weight gradient: long reductions are split over grid z; when the bias
+//    gradient is requested too, the waves that load dy (operand A) add up
+//    its rows from their fragments -- the bias gradient costs no extra read.
+#include <algorithm>
+#include <cstdio>
+#include <cstdlib>
+
+#include "common.h"
+#include "../device.h"
+
+namespace ms {
+namespace g2 {
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
+
+enum Mode { kFwd = 0, kDgrad = 1, kWgrad = 2 };
+
+constexpr uint32_t kOOB = 0xFFFFFFF0u;   // byte offset beyond any buffer: loads return 0
+
+struct Args {
+    const bf16 *a;
+    const bf16 *b;
+    bf16 *c;              // output (or nullptr when the output is fp32 partials)
+    float *part;          // WGRAD split-K partials [splits][M][N]
+    float *dbpart;        // WGRAD fused bias-gradient partials [splits][M] (nullptr: off)
+    const bf16 *bias;     // FWD bias (nullptr: none)
+    ConvGeom g;
+    int M, N, K;          // GEMM extents (DGRAD: bounds over phases)
+    int ntm, ntn;
+    int k_split, splits;
+    uint32_t a_bytes, b_bytes;
+};
+
+struct Phase {
+    int fh, fw, h0, w0, Hp, Wp, Rp, Sp, dh, dw;
+};
+
+__device__ __forceinline__ Phase make_phase(const ConvGeom &g, int z) {
+    Phase f;
+    f.fh = z / g.sw;
+    f.fw = z % g.sw;
+    f.h0 = ((f.fh - g.ph) % g.sh + g.sh) % g.sh;
+    f.w0 = ((f.fw - g.pw) % g.sw + g.sw) % g.sw;
+    f.Hp = f.h0 < g.H ? (g.H - f.h0 + g.sh - 1) / g.sh : 0;
+    f.Wp = f.w0 < g.W ? (g.W - f.w0 + g.sw - 1) / g.sw : 0;
+    f.Rp = f.fh < g.R ? (g.R - f.fh + g.sh - 1) / g.sh : 0;
+    f.Sp = f.fw < g.S ? (g.S - f.fw + g.sw - 1) / g.sw : 0;
+    f.dh = (f.h0 + g.ph - f.fh) / g.sh;
+    f.dw = (f.w0 + g.pw - f.fw) / g.sw;
+    return f;
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+// s_waitcnt with only vmcnt constrained (gfx9 encoding: vmcnt[3:0] | [15:14],
+// expcnt[6:4] = 7, lgkmcnt[11:8] = 15).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// 16-byte chunk swizzle of a K-contiguous tile row (BK = 32: 4 chunks per
+// 64-byte row).  Depends on row bits 1..3 only, so a lane's chunk is the same
+// in every 16-row load instruction; spreads the 16 rows one fragment read
+// touches over distinct bank groups.
+__device__ __forceinline__ int swz_k(int row) { return ((row >> 1) & 3) ^ ((row >> 3) & 1); }
+
+// Slot swizzle of an M/N-contiguous tile k-row ([k][mn], 16-byte slots):
+// XOR with an even value so the two slots one transposed read touches stay
+// adjacent.
+template <int SPR>
+__device__ __forceinline__ int swz_m(int krow) {
+    if constexpr (SPR >= 16) return ((krow & 3) | (((krow >> 3) & 1) << 2)) << 1;
+    else return (krow & 3) << 1;
+}
+
+// MFMA fragment (8 k values of one m/n index) from a [32 k][R mn] tile for
+// the 32x32x16 shape: lane l needs column mn0 + l%32 at k-rows
+// 16*sub + 8*(l/32) .. +7.  ds_read_b64_tr_b16 works per 16-lane group
+// g = l/16: lane 16g + r addresses k-row kb + 4h + r/4 at columns
+// cb + 4*(r%4) .. +3 (kb = 16*sub + 8*(g/2), cb = mn0 + 16*(g%2)) and, after
+// the in-group transpose, holds column cb + r of k-rows kb + 4h .. kb+4h+3.
+template <int R>
+__device__ __forceinline__ bf16x8 frag_mn(const char *base, int mn0, int sub, int lane) {
+    constexpr int SPR = R / 8;
+    const int g = lane >> 4, r = lane & 15;
+    const int kb = 16 * sub + 8 * (g >> 1), cb = mn0 + 16 * (g & 1);
+    bf16x8 v;
+    v4i16 *pv = reinterpret_cast<v4i16 *>(&v);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int krow = kb + 4 * h + (r >> 2);
+        const int mn = cb + 4 * (r & 3);
+        const int pos = (mn >> 3) ^ swz_m<SPR>(krow);
+        const int off = krow * (R * 2) + (pos << 4) + ((mn & 7) << 1);
+        pv[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(base + off));
+    }
+    return v;
+}
+
+// Fragment from a row-major [row][32 k] tile (64-byte rows, swizzled
+// 16-byte chunks): lane l reads row `row` (= tile row + l%32), chunk
+// 2*sub + l/32.
+__device__ __forceinline__ bf16x8 frag_kc(const char *base, int row, int sub, int lane) {
+    const int chunk = 2 * sub + (lane >> 5);
+    const int off = row * 64 + ((chunk ^ swz_k(row)) << 4);
+    return *reinterpret_cast<const bf16x8 *>(base + off);
+}
+
+template <int MODE, int BM, int BN, int STAGES, bool UNIT>
+struct Cfg {
+    static constexpr int BK = 32;
+    static constexpr bool A_KC = MODE != kWgrad;
+    static constexpr bool B_KC = MODE == kFwd;
+    static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
+    static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+    static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;
+    static constexpr int NIA = A_BYTES / 1024 / 4;   // load instructions per wave per tile
+    static constexpr int NIB = B_BYTES / 1024 / 4;
+    static constexpr int WM = BM / 2, WN = BN / 2;
+    static constexpr int TM = WM / 32, TN = WN / 32;   // 32x32 MFMA tiles per wave
+    static constexpr int EPI_PITCH = WN + 8;         // bf16 elements per staged row
+    static constexpr int EPI_ROWS = 32;              // rows staged per pass
+    static_assert(NIA >= 1 && NIB >= 1, "tile too small");
+    static_assert(4 * EPI_ROWS * EPI_PITCH * 2 <= LDS_BYTES, "epilogue staging must fit in LDS");
+    static_assert(BM % 64 == 0 && BN % 64 == 0, "tile sizes");
+};
+
+template <int MODE, int BM, int BN, int STAGES, bool UNIT>
+__global__ __launch_bounds__(256, 1) void gemm_kernel(const Args P) {
+    using G = Cfg<MODE, BM, BN, STAGES, UNIT>;
+    constexpr int BK = G::BK, NIA = G::NIA, NIB = G::NIB, TM = G::TM, TN = G::TN;
+    __shared__ __attribute__((aligned(1024))) char smem[G::LDS_BYTES];
+
+    const ConvGeom &g = P.g;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm0 = (wave >> 1) * G::WM, wn0 = (wave & 1) * G::WN;
+
+    int M = P.M, Kg = P.K, ntm = P.ntm;
+    Phase f{};
+    if constexpr (MODE == kDgrad) {
+        f = make_phase(g, blockIdx.z);
+        M = g.N * f.Hp * f.Wp;
+        Kg = f.Rp * f.Sp * g.K;
+        ntm = (M + BM - 1) / BM;
+    }
+    const int N = P.N;
+    int k_begin = 0, k_end = Kg;
+    if constexpr (MODE == kWgrad) {
+        k_begin = blockIdx.z * P.k_split;
+        k_end = min(Kg, k_begin + P.k_split);
+    }
+    int tm, tn;
+    {
+        const int nb = P.ntm * P.ntn;
+        const int lt = xcd_remap(blockIdx.x, nb);
+        const int GM = 8, per = GM * P.ntn;
+        const int gid = lt / per, first = gid * GM;
+        const int gsz = min(P.ntm - first, GM);
+        const int r = lt - gid * per;
+        tm = first + r % gsz;
+        tn = r / gsz;
+    }
+    if (tm >= ntm || tn >= P.ntn) return;
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int nk = k_end > k_begin ? (k_end - k_begin + BK - 1) / BK : 0;
+
+    const __amdgpu_buffer_rsrc_t ra = rsrc(P.a, P.a_bytes);
+    const __amdgpu_buffer_rsrc_t rb = rsrc(P.b, P.b_bytes);
+
+    // ------------------------------------------------ per-lane load state
+    // K-contiguous operand: instruction j of this wave covers rows
+    // (wave*NI + j)*16 + lane/4, chunk slot lane%4 holding k chunk kc.
+    const int kc_row = lane >> 2;                       // row within a 16-row group
+    const int kc = (lane & 3) ^ swz_k(kc_row);          // k chunk this lane fetches
+    // A state
+    int a_base[NIA], a_y[NIA], a_x[NIA];
+    uint32_t a_mn_off[NIA];                             // MN-contiguous A: element offset along m
+    bool a_ok[NIA];
+    // B state
+    int b_base[NIB];
+    bool b_ok[NIB];
+    uint32_t b_mn_off[NIB];
+    int b_r[NIB], b_s[NIB];
+
+    if constexpr (G::A_KC) {
+#pragma unroll
+        for (int j = 0; j < NIA; ++j) {
+            const int row = (wave * NIA + j) * 16 + kc_row;
+            const int m = m0 + row;
+            a_ok[j] = m < M;
+            const int mm = a_ok[j] ? m : 0;
+            if constexpr (UNIT) {
+                a_base[j] = mm * (MODE == kFwd ? g.C : g.K);
+                a_y[j] = a_x[j] = 0;
+            } else if constexpr (MODE == kFwd) {
+                const int PQ = g.P * g.Q;
+                const int n = mm / PQ, pq = mm - n * PQ;
+                const int p = pq / g.Q, q = pq - p * g.Q;
+                a_base[j] = n * g.H * g.W * g.C;
+                a_y[j] = p * g.sh - g.ph;
+                a_x[j] = q * g.sw - g.pw;
+            } else {
+                const int HW = f.Hp * f.Wp;
+                const int n = HW > 0 ? mm / HW : 0, ij = mm - n * HW;
+                const int i2 = f.Wp > 0 ? ij / f.Wp : 0, j2 = ij - i2 * f.Wp;
+                a_base[j] = n * g.P * g.Q * g.K;
+                a_y[j] = i2 + f.dh;
+                a_x[j] = j2 + f.dw;
+            }
+        }
+    } else {
+        // WGRAD A = dy^T: k-rows are (n,p,q), slots run along m (the K channels)
+        constexpr int SPR = BM / 8, KPI = 64 / SPR;
+#pragma unroll
+        for (int j = 0; j < NIA; ++j) {
+            const int krow = (wave * NIA + j) * KPI + lane / SPR;
+            const int slot = (lane % SPR) ^ swz_m<SPR>(krow);
+            const int m = m0 + slot * 8;
+            a_ok[j] = m < M;
+            a_mn_off[j] = m;
+        }
+    }
+    if constexpr (G::B_KC) {
+#pragma unroll
+        for (int j = 0; j < NIB; ++j) {
+            const int row = (wave * NIB + j) * 16 + kc_row;
+            const int n = n0 + row;
+            b_ok[j] = n < N;
+            b_base[j] = (b_ok[j] ? n : 0) * Kg;
+        }
+    } else {
+        constexpr int SPR = BN / 8, KPI = 64 / SPR;
+#pragma unroll
+        for (int j = 0; j < NIB; ++j) {
+            const int krow = (wave * NIB + j) * KPI + lane / SPR;
+            const int slot = (lane % SPR) ^ swz_m<SPR>(krow);
+            const int nn = n0 + slot * 8;
+            b_ok[j] = nn < N;
+            if constexpr (MODE == kWgrad && !UNIT) {
+                const int nv = b_ok[j] ? nn : 0;
+                const int rs = nv / g.C, c = nv - rs * g.C;
+                b_r[j] = rs / g.S;
+                b_s[j] = rs - b_r[j] * g.S;
+                b_mn_off[j] = c;
+            } else {
+                b_r[j] = b_s[j] = 0;
+                b_mn_off[j] = nn;
+            }
+        }
+    }
+
+    // ------------------------------------------------ issue the loads of one tile
+    auto issue = [&](int stage, int k0) {
+        char *sA = smem + stage * G::STAGE_BYTES;
+        char *sB = sA + G::A_BYTES;
+        // ---- A
+        if constexpr (G::A_KC) {
+            const int kk = k0 + kc * 8;
+            const bool kin = kk < k_end;
+            int dr = 0, ds = 0, off_k = kk;
+            if constexpr (!UNIT) {
+                if constexpr (MODE == kFwd) {
+                    const int rs = kk / g.C;
+                    off_k = kk - rs * g.C;
+                    dr = rs / g.S;
+                    ds = rs - dr * g.S;
+                } else {
+                    const int t = kk / g.K;
+                    off_k = kk - t * g.K;
+                    const int tr = f.Sp > 0 ? t / f.Sp : 0;
+                    dr = -tr;
+                    ds = -(t - tr * f.Sp);
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < NIA; ++j) {
+                bool ok = kin && a_ok[j];
+                int off;
+                if constexpr (UNIT) {
+                    off = a_base[j] + kk;
+                } else if constexpr (MODE == kFwd) {
+                    const int ih = a_y[j] + dr, iw = a_x[j] + ds;
+                    ok = ok && (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
+                    off = a_base[j] + (ih * g.W + iw) * g.C + off_k;
+                } else {
+                    const int p = a_y[j] + dr, q = a_x[j] + ds;
+                    ok = ok && (unsigned)p < (unsigned)g.P && (unsigned)q < (unsigned)g.Q;
+                    off = a_base[j] + (p * g.Q + q) * g.K + off_k;
+                }
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    ra, (lds_void_t *)(sA + (wave * NIA + j) * 1024), 16, ok ? (uint32_t)off * 2u : kOOB, 0, 0, 0);
+            }
+        } else {
+            constexpr int SPR = BM / 8, KPI = 64 / SPR;
+#pragma unroll
+            for (int j = 0; j < NIA; ++j) {
+                const int kk = k0 + (wave * NIA + j) * KPI + lane / SPR;
+                const bool ok = a_ok[j] && kk < k_end;
+                const uint32_t off = (uint32_t)kk * (uint32_t)g.K + a_mn_off[j];
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    ra, (lds_void_t *)(sA + (wave * NIA + j) * 1024), 16, ok ? off * 2u : kOOB, 0, 0, 0);
+            }
+        }
+        // ---- B
+        if constexpr (G::B_KC) {
+            const int kk = k0 + kc * 8;
+            const bool kin = kk < k_end;
+#pragma unroll
+            for (int j = 0; j < NIB; ++j) {
+                const bool ok = kin && b_ok[j];
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rb, (lds_void_t *)(sB + (wave * NIB + j) * 1024), 16,
+                    ok ? (uint32_t)(b_base[j] + kk) * 2u : kOOB, 0, 0, 0);
+            }
+        } else {
+            constexpr int SPR = BN / 8, KPI = 64 / SPR;
+#pragma unroll
+            for (int j = 0; j < NIB; ++j) {
+                const int kk = k0 + (wave * NIB + j) * KPI + lane / SPR;
+                bool ok = b_ok[j] && kk < k_end;
+                uint32_t off = 0;
+                if constexpr (MODE == kDgrad) {
+                    if constexpr (UNIT) {
+                        off = (uint32_t)kk * (uint32_t)g.C + b_mn_off[j];
+                    } else {
+                        const int t = kk / g.K, k = kk - t * g.K;
+                        const int tr = f.Sp > 0 ? t / f.Sp : 0, ts = t - tr * f.Sp;
+                        const int r = f.fh + tr * g.sh, s = f.fw + ts * g.sw;
+                        off = (uint32_t)(((k * g.R + r) * g.S + s) * g.C) + b_mn_off[j];
+                    }
+                } else {   // WGRAD: x im2col, k-row = (n,p,q), slot along (r,s,c)
+                    if constexpr (UNIT) {
+                        off = (uint32_t)kk * (uint32_t)g.C + b_mn_off[j];
+                    } else {
+                        const int PQ = g.P * g.Q;
+                        const int n = kk / PQ, pq = kk - n * PQ;
+                        const int p = pq / g.Q, q = pq - p * g.Q;
+                        const int ih = p * g.sh - g.ph + b_r[j], iw = q * g.sw - g.pw + b_s[j];
+                        ok = ok && (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
+                        off = (uint32_t)(((n * g.H + ih) * g.W + iw) * g.C) + b_mn_off[j];
+                    }
+                }
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rb, (lds_void_t *)(sB + (wave * NIB + j) * 1024), 16, ok ? off * 2u : kOOB, 0, 0, 0);
+            }
+        }
+    };
+
+    const int fr = lane & 31, fh = lane >> 5;   // row within a 32-row tile, k half
+    floatx16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    // fused bias gradient (WGRAD): row sums of dy^T gathered from A fragments
+    const bool db_on = MODE == kWgrad && P.dbpart != nullptr && tn == 0 && wn0 == 0;
+    float dbacc[TM];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) dbacc[i] = 0.f;
+
+    // ------------------------------------------------ main loop (software pipelined)
+    // The prologue fills all STAGES stages.  Step kt holds the fragments of
+    // tile kt in registers (cur); it waits for tile kt+1, refills the stage
+    // tile kt came from with tile kt+STAGES, and reads tile kt+1's fragments
+    // (nxt) from LDS while the MFMAs of tile kt run, so LDS latency and the
+    // DMA issue overlap the matrix work.
+    // fragments of one BK = 32 tile: [sub][i] with sub = k half (16 each)
+    auto read_frags = [&](int stage, bf16x8 *af, bf16x8 *bfr) {
+        const char *sA = smem + stage * G::STAGE_BYTES;
+        const char *sB = sA + G::A_BYTES;
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                if constexpr (G::A_KC) af[sub * TM + i] = frag_kc(sA, wm0 + i * 32 + fr, sub, lane);
+                else af[sub * TM + i] = frag_mn<BM>(sA, wm0 + i * 32, sub, lane);
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                if constexpr (G::B_KC) bfr[sub * TN + j] = frag_kc(sB, wn0 + j * 32 + fr, sub, lane);
+                else bfr[sub * TN + j] = frag_mn<BN>(sB, wn0 + j * 32, sub, lane);
+            }
+        }
+    };
+    // One pipelined step: tiles kt+1 .. kt+STAGES-1 are in flight or landed.
+    // The refill of the stage tile kt came from is issued unconditionally
+    // (past the end of the reduction its loads take the out-of-range path and
+    // write zeros into a stage that is never read), so every step has the
+    // same instruction stream: wait for tile kt+1 (at most STAGES-2 tiles
+    // still in flight), barrier, refill, read tile kt+1's fragments (nxt) and
+    // run tile kt's MFMAs (cur); the scheduler interleaves the loads and LDS
+    // reads between the MFMAs so the matrix pipe never waits for them.
+    constexpr int NMFMA = 2 * TM * TN;
+#ifndef MS_GEMM_INTERLEAVE
+#define MS_GEMM_INTERLEAVE 1
+#endif
+    constexpr bool INTERLEAVE = MS_GEMM_INTERLEAVE;
+    constexpr int NVMEM = NIA + NIB;
+    constexpr int NDS = 2 * ((G::A_KC ? 1 : 2) * TM + (G::B_KC ? 1 : 2) * TN);
+    auto mfmas = [&](const bf16x8 *ca, const bf16x8 *cb) {
+        if (db_on) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                float sum = 0.f;
+#pragma unroll
+                for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) sum += (float)ca[sub * TM + i][e];
+                dbacc[i] += sum;
+            }
+        }
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cb[sub * TN + j], ca[sub * TM + i],
+                                                                        acc[i][j], 0, 0, 0);
+    };
+    auto step = [&](const bf16x8 *ca, const bf16x8 *cb, bf16x8 *na, bf16x8 *nb2, int kt) {
+        wait_vmcnt<(STAGES - 2) * NVMEM>();
+        __builtin_amdgcn_s_waitcnt(0xc07f);   // this wave's reads of tile kt are complete
+        __builtin_amdgcn_s_barrier();
+        issue(kt % STAGES, k_begin + (kt + STAGES) * BK);
+        read_frags((kt + 1) % STAGES, na, nb2);
+        mfmas(ca, cb);
+        // interleave: every MFMA is followed by its share of loads / LDS reads
+#pragma unroll
+        for (int m = 0; m < (INTERLEAVE ? NMFMA : 0); ++m) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // 1 MFMA
+            if (m < NVMEM) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // 1 VMEM load
+            constexpr int DPM = (NDS + NMFMA - 1) / NMFMA;
+            if (m * DPM < NDS) __builtin_amdgcn_sched_group_barrier(0x100, DPM, 0);   // LDS reads
+        }
+    };
+
+#pragma unroll
+    for (int s = 0; s < STAGES; ++s) issue(s, k_begin + s * BK);
+    bf16x8 fa0[2 * TM], fb0[2 * TN], fa1[2 * TM], fb1[2 * TN];
+    if (nk > 0) {
+        wait_vmcnt<(STAGES - 1) * NVMEM>();
+        __builtin_amdgcn_s_barrier();
+        read_frags(0, fa0, fb0);
+    }
+    int kt = 0;
+    for (; kt + 2 < nk; kt += 2) {
+        step(fa0, fb0, fa1, fb1, kt);
+        step(fa1, fb1, fa0, fb0, kt + 1);
+    }
+    if (kt + 1 < nk) {
+        step(fa0, fb0, fa1, fb1, kt);
+        mfmas(fa1, fb1);
+    } else if (kt < nk) {
+        mfmas(fa0, fb0);
+    }
+
+    // ------------------------------------------------ fused bias-gradient partials
+    if (db_on) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            float v = dbacc[i];
+            v += __shfl_xor(v, 32);
+            const int m = m0 + wm0 + i * 32 + fr;
+            if (fh == 0 && m < M) P.dbpart[(size_t)blockIdx.z * M + m] = v;
+        }
+    }
+
+    // ------------------------------------------------ epilogue
+    // lane holds, for MFMA tile (i, j) and register group q = 0..3,
+    // D[m = wm0 + 32i + lane%32][n = wn0 + 32j + 8q + 4*(lane/32) + 0..3]
+    if constexpr (MODE == kWgrad) {
+        if (P.splits > 1) {
+            float *W = P.part + (size_t)blockIdx.z * M * N;
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int m = m0 + wm0 + i * 32 + fr;
+                if (m >= M) continue;
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int n = n0 + wn0 + j * 32 + 8 * q + 4 * fh;
+                        const floatx4 o = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                           acc[i][j][4 * q + 3]};
+                        if (n + 3 < N) {
+                            *reinterpret_cast<floatx4 *>(W + (size_t)m * N + n) = o;
+                        } else {
+                            for (int v = 0; v < 4; ++v)
+                                if (n + v < N) W[(size_t)m * N + n + v] = o[v];
+                        }
+                    }
+            }
+            return;
+        }
+    }
+    __syncthreads();   // every wave is done with the operand stages
+    bf16 *stage = reinterpret_cast<bf16 *>(smem) + wave * G::EPI_ROWS * G::EPI_PITCH;
+    constexpr int SEG = G::WN / 8;                   // 16-byte segments per staged row
+    constexpr int ROWS_PER_PASS = 64 / SEG;
+    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                bf16x4 o;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) o[v] = (bf16)acc[i][j][4 * q + v];
+                *reinterpret_cast<bf16x4 *>(stage + fr * G::EPI_PITCH + j * 32 + 8 * q + 4 * fh) = o;
+            }
+        __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): this wave's staged rows are written
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int r0 = 0; r0 < G::EPI_ROWS; r0 += ROWS_PER_PASS) {
+            const int rl = r0 + lane / SEG;
+            const int cl = (lane % SEG) * 8;
+            const int m = m0 + wm0 + i * 32 + rl;
+            const int n = n0 + wn0 + cl;
+            Vec16<bf16> v;
+            v.u = *reinterpret_cast<const u32x4 *>(stage + rl * G::EPI_PITCH + cl);
+            if (m >= M || n >= N) continue;
+            if constexpr (MODE == kFwd) {
+                if (P.bias) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (n + e < N) v.e[e] = (bf16)((float)v.e[e] + (float)P.bias[n + e]);
+                }
+            }
+            bf16 *dst;
+            if constexpr (MODE == kDgrad && !UNIT) {
+                const int HW = f.Hp * f.Wp;
+                const int nimg = m / HW, ij = m - nimg * HW;
+                const int i2 = ij / f.Wp, j2 = ij - i2 * f.Wp;
+                const int pix = (nimg * g.H + f.h0 + i2 * g.sh) * g.W + f.w0 + j2 * g.sw;
+                dst = P.c + (size_t)pix * g.C + n;
+            } else {
+                dst = P.c + (size_t)m * N + n;
+            }
+            if (n + 8 <= N) {
+                *reinterpret_cast<u32x4 *>(dst) = v.u;
+            } else {
+                for (int e = 0; e < 8 && n + e < N; ++e) dst[e] = v.e[e];
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0xc07f);   // reads done before the next pass overwrites
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
+// Sum split-K partials (and fused bias-gradient partials) to bf16.
+__global__ __launch_bounds__(256) void reduce_kernel(const float *__restrict__ part, int splits, int64_t n,
+                                                     bf16 *__restrict__ out, const float *__restrict__ dbpart,
+                                                     int M, bf16 *__restrict__ db) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t nv = n / 4;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nv; i += stride) {
+        floatx4 s = *reinterpret_cast<const floatx4 *>(part + 4 * i);
+        for (int z = 1; z < splits; ++z) s += *reinterpret_cast<const floatx4 *>(part + (int64_t)z * n + 4 * i);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) out[4 * i + e] = (bf16)s[e];
+    }
+    for (int64_t i = 4 * nv + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        float s = 0.f;
+        for (int z = 0; z < splits; ++z) s += part[(int64_t)z * n + i];
+        out[i] = (bf16)s;
+    }
+    if (dbpart) {
+        for (int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; m < M; m += stride) {
+            float s = 0.f;
+            for (int z = 0; z < splits; ++z) s += dbpart[(int64_t)z * M + m];
+            db[m] = (bf16)s;
+        }
+    }
+}
+
+}  // namespace g2
+}  // namespace ms
+
+// ------------------------------------------------------------------ launchers
+namespace ms {
+namespace g2 {
+namespace {
+
+constexpr int kCUs = 256;
+
+struct Tile {
+    int bm, bn, per_cu;   // tile shape, blocks resident per CU
+    float eff;            // relative MFMA efficiency of the shape
+};
+constexpr Tile kTiles[] = {{256, 128, 1, 0.90f}, {128, 128, 2, 0.80f}, {128, 64, 3, 0.60f}};
+
+// MEMSAVE_GEMM_TILE=<bm>x<bn> forces one tile shape (a debugging and
+// testing knob); returns its index or -1.
+int forced_tile() {
+    const char *e = getenv("MEMSAVE_GEMM_TILE");
+    if (!e || !*e) return -1;
+    int bm = 0, bn = 0;
+    if (sscanf(e, "%dx%d", &bm, &bn) != 2) return -1;
+    for (int i = 0; i < (int)(sizeof(kTiles) / sizeof(kTiles[0])); ++i)
+        if (kTiles[i].bm == bm && kTiles[i].bn == bn) return i;
+    return -1;
+}
+
+// Pick the tile that minimises (waves of blocks) x (time per wave).
+// `first` skips the largest shapes (the weight gradient keeps more live
+// registers and would spill with the 256 x 256 tile).
+Tile pick(long M, long N, long K, int splits_allowed, int *splits_out, int z = 1, int first = 0) {
+    double best = 1e300;
+    Tile bt = kTiles[first];
+    int bs = 1;
+    const int forced = forced_tile();
+    for (int ti = first; ti < (int)(sizeof(kTiles) / sizeof(kTiles[0])); ++ti) {
+        if (forced >= first && ti != forced) continue;
+        const Tile &t = kTiles[ti];
+        const long tiles = ((M + t.bm - 1) / t.bm) * ((N + t.bn - 1) / t.bn) * z;
+        int splits = 1;
+        if (splits_allowed > 1) {
+            const long want = (long)kCUs * t.per_cu;
+            if (tiles < want) splits = (int)std::min<long>((want + tiles - 1) / tiles, splits_allowed);
+        }
+        const long blocks = tiles * splits;
+        const long conc = (long)kCUs * t.per_cu;
+        const long waves = (blocks + conc - 1) / conc;
+        // blocks that actually share a CU in the fullest wave
+        const long resident = std::min<long>(t.per_cu, (blocks + kCUs - 1) / kCUs);
+        const double kper = (double)K / splits;
+        const double cost = (double)waves * resident * t.bm * t.bn * (kper + 64.0) / t.eff;
+        if (cost < best * 0.999) {
+            best = cost;
+            bt = t;
+            bs = splits;
+        }
+    }
+    if (splits_out) *splits_out = bs;
+    return bt;
+}
+
+template <int MODE, int BM, int BN, bool UNIT>
+int go(const Args &a, dim3 grid, hipStream_t st) {
+    hipLaunchKernelGGL((gemm_kernel<MODE, BM, BN, 4, UNIT>), grid, dim3(256), 0, st, a);
+    return (int)hipGetLastError();
+}
+
+template <int MODE, bool UNIT>
+int go_tile(const Tile &t, const Args &a, dim3 grid, hipStream_t st) {
+    if (t.bm == 256 && t.bn == 128) return go<MODE, 256, 128, UNIT>(a, grid, st);
+    if (t.bm == 128 && t.bn == 128) return go<MODE, 128, 128, UNIT>(a, grid, st);
+    return go<MODE, 128, 64, UNIT>(a, grid, st);
+}
+
+template <int MODE>
+int go_mode(const Tile &t, const Args &a, dim3 grid, bool unit, hipStream_t st) {
+    return unit ? go_tile<MODE, true>(t, a, grid, st) : go_tile<MODE, false>(t, a, grid, st);
+}
+
+bool al16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool unit_geom(const ConvGeom &g) {
+    return g.R == 1 && g.S == 1 && g.sh == 1 && g.sw == 1 && g.ph == 0 && g.pw == 0 && g.P == g.H && g.Q == g.W;
+}
+
+uint32_t bytes_of(long elems) { return (uint32_t)(elems * 2); }
+
+struct WgradPlan {
+    Tile t;
+    int splits, k_split;
+};
+
+WgradPlan wgrad_plan(const ConvGeom &g) {
+    const long M = g.K, N = (long)g.R * g.S * g.C, K = (long)g.N * g.P * g.Q;
+    int splits = 1;
+    const int max_splits = (int)std::max<long>(1, K / 256);   // at least 8 BK steps per split
+    Tile t = pick(M, N, K, max_splits, &splits, 1, 0);
+    int k_split = (int)((K + splits - 1) / splits);
+    k_split = (k_split + 31) / 32 * 32;
+    if (K == 0) k_split = 32;
+    splits = K > 0 ? (int)((K + k_split - 1) / k_split) : 1;
+    return {t, splits, k_split};
+}
+
+}  // namespace
+
+// Each returns -1 when the fast path does not apply, else a hipError_t.
+int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, void *y, hipStream_t st) {
+    if (g.C % 8 != 0 || !al16(x) || !al16(w) || !al16(y)) return -1;
+    Args a{};
+    a.a = (const bf16 *)x; a.b = (const bf16 *)w; a.c = (bf16 *)y; a.bias = (const bf16 *)bias; a.g = g;
+    a.M = g.N * g.P * g.Q; a.N = g.K; a.K = g.R * g.S * g.C;
+    if (a.M == 0 || a.N == 0) return 0;
+    Tile t = pick(a.M, a.N, a.K, 1, nullptr);
+    a.ntm = (a.M + t.bm - 1) / t.bm; a.ntn = (a.N + t.bn - 1) / t.bn;
+    a.splits = 1; a.k_split = a.K;
+    a.a_bytes = bytes_of((long)g.N * g.H * g.W * g.C);
+    a.b_bytes = bytes_of((long)g.K * a.K);
+    return go_mode<kFwd>(t, a, dim3(a.ntm * a.ntn, 1, 1), unit_geom(g), st);
+}
+
+int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, hipStream_t st) {
+    if (g.C % 8 != 0 || g.K % 8 != 0 || !al16(dy) || !al16(w) || !al16(dx)) return -1;
+    Args a{};
+    a.a = (const bf16 *)dy; a.b = (const bf16 *)w; a.c = (bf16 *)dx; a.g = g;
+    const int Hb = (g.H + g.sh - 1) / g.sh, Wb = (g.W + g.sw - 1) / g.sw;
+    a.M = g.N * Hb * Wb; a.N = g.C;
+    a.K = ((g.R + g.sh - 1) / g.sh) * ((g.S + g.sw - 1) / g.sw) * g.K;
+    if (a.M == 0 || a.N == 0) return 0;
+    Tile t = pick(a.M, a.N, a.K, 1, nullptr, g.sh * g.sw);
+    a.ntm = (a.M + t.bm - 1) / t.bm; a.ntn = (a.N + t.bn - 1) / t.bn;
+    a.splits = 1; a.k_split = a.K;
+    a.a_bytes = bytes_of((long)g.N * g.P * g.Q * g.K);
+    a.b_bytes = bytes_of((long)g.K * g.R * g.S * g.C);
+    return go_mode<kDgrad>(t, a, dim3(a.ntm * a.ntn, 1, g.sh * g.sw), unit_geom(g), st);
+}
+
+bool wgrad_applies(const ConvGeom &g) { return g.C % 8 == 0 && g.K % 8 == 0; }
+
+size_t wgrad_workspace(const ConvGeom &g, bool with_db) {
+    WgradPlan p = wgrad_plan(g);
+    size_t ws = 0;
+    if (p.splits > 1) ws += (size_t)p.splits * g.K * ((size_t)g.R * g.S * g.C) * sizeof(float);
+    if (with_db) ws += (size_t)p.splits * g.K * sizeof(float);
+    return ws;
+}
+
+int conv_wgrad(const ConvGeom &g, const void *dy, const void *x, void *dw, void *db, void *ws, hipStream_t st) {
+    if (!wgrad_applies(g) || !al16(dy) || !al16(x) || !al16(dw)) return -1;
+    WgradPlan p = wgrad_plan(g);
+    Args a{};
+    a.a = (const bf16 *)dy; a.b = (const bf16 *)x; a.g = g;
+    a.M = g.K; a.N = g.R * g.S * g.C; a.K = g.N * g.P * g.Q;
+    if (a.M == 0 || a.N == 0) return 0;
+    a.ntm = (a.M + p.t.bm - 1) / p.t.bm; a.ntn = (a.N + p.t.bn - 1) / p.t.bn;
+    a.splits = p.splits; a.k_split = p.k_split;
+    float *wsf = static_cast<float *>(ws);
+    size_t used = 0;
+    if (p.splits > 1) {
+        a.part = wsf;
+        used = (size_t)p.splits * a.M * a.N;
+        a.c = nullptr;
+    } else {
+        a.c = (bf16 *)dw;
+    }
+    a.dbpart = db ? wsf + used : nullptr;
+    a.a_bytes = bytes_of((long)g.N * g.P * g.Q * g.K);
+    a.b_bytes = bytes_of((long)g.N * g.H * g.W * g.C);
+    int err = go_mode<kWgrad>(p.t, a, dim3(a.ntm * a.ntn, 1, p.splits), unit_geom(g), st);
+    if (err) return err;
+    if (p.splits > 1 || db) {
+        const int64_t n = p.splits > 1 ? (int64_t)a.M * a.N : 0;
+        const int blocks = (int)std::max<int64_t>(1, std::min<int64_t>((n / 4 + 255) / 256, 2048));
+        hipLaunchKernelGGL(reduce_kernel, dim3(blocks), dim3(256), 0, st, (const float *)a.part, p.splits, n,
+                           (bf16 *)dw, (const float *)a.dbpart, db ? a.M : 0, (bf16 *)db);
+        err = (int)hipGetLastError();
+    }
+    return err;
+}
+
+}  // namespace g2
+}  // namespace ms

@@ -31,6 +31,15 @@
 
 namespace ms {
 
+// bf16 fast path (gemm_bf16.hip); each returns -1 when it does not apply.
+namespace g2 {
+int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, void *y, hipStream_t st);
+int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, hipStream_t st);
+bool wgrad_applies(const ConvGeom &g);
+size_t wgrad_workspace(const ConvGeom &g, bool with_db);
+int conv_wgrad(const ConvGeom &g, const void *dy, const void *x, void *dw, void *db, void *ws, hipStream_t st);
+}  // namespace g2
+
 enum Mode { kFwd = 0, kDgrad = 1, kWgrad = 2 };
 
 struct IgemmParams {
@@ -607,6 +616,10 @@ SplitPlan wgrad_split(int dtype, const ConvGeom &g) {
 
 int launch_conv_fwd(int dtype, const ConvGeom &g, const void *x, const void *w, const void *bias,
                     void *y, void *stream) {
+    if (dtype == kBF16) {
+        const int r = g2::conv_fwd(g, x, w, bias, y, (hipStream_t)stream);
+        if (r >= 0) return r;
+    }
     IgemmParams prm{};
     prm.a = x; prm.b = w; prm.c = y; prm.bias = bias; prm.g = g;
     prm.M = g.N * g.P * g.Q;
@@ -625,6 +638,10 @@ int launch_conv_fwd(int dtype, const ConvGeom &g, const void *x, const void *w, 
 
 int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *w, void *dx,
                       void *stream) {
+    if (dtype == kBF16) {
+        const int r = g2::conv_dgrad(g, dy, w, dx, (hipStream_t)stream);
+        if (r >= 0) return r;
+    }
     IgemmParams prm{};
     prm.a = dy; prm.b = w; prm.c = dx; prm.g = g;
     // bounds over phases: ceil(H / sh) rows, ceil(R / sh) taps
@@ -642,15 +659,24 @@ int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *
     return launch_dtype<kDgrad>(dtype, prm, grid, vec_ok, is_unit(g), (hipStream_t)stream);
 }
 
-size_t conv_wgrad_workspace(int dtype, const ConvGeom &g) {
+size_t conv_wgrad_workspace(int dtype, const ConvGeom &g, bool with_db) {
+    if (dtype == kBF16 && g2::wgrad_applies(g)) return g2::wgrad_workspace(g, with_db);
     SplitPlan sp = wgrad_split(dtype, g);
     if (sp.splits <= 1) return 0;
     return (size_t)sp.splits * (size_t)g.K * (size_t)(g.R * g.S * g.C) * sizeof(float);
 }
 
 int launch_conv_wgrad(int dtype, const ConvGeom &g, const void *dy, const void *x, void *dw,
-                      void *ws, void *stream) {
+                      void *db, void *ws, void *stream, bool *db_done) {
     hipStream_t st = (hipStream_t)stream;
+    *db_done = false;
+    if (dtype == kBF16) {
+        const int r = g2::conv_wgrad(g, dy, x, dw, db, ws, st);
+        if (r >= 0) {
+            *db_done = db != nullptr;
+            return r;
+        }
+    }
     SplitPlan sp = wgrad_split(dtype, g);
     IgemmParams prm{};
     prm.a = dy; prm.b = x; prm.g = g;

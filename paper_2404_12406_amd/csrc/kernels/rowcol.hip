@@ -41,8 +41,8 @@ RowColPlan plan_rowcol(int dtype, int64_t rows, int C, bool vec_ok, int target_b
     p.RG = 256 / p.TC;
     p.gx = (p.nvc + p.TC - 1) / p.TC;
     int64_t want_y = std::max<int64_t>(1, target_blocks / p.gx);
-    // at least 4 rows per thread
-    int64_t max_y = std::max<int64_t>(1, rows / (int64_t)(p.RG * 4));
+    // at least 16 rows per thread, so the partials stay small next to the input
+    int64_t max_y = std::max<int64_t>(1, rows / (int64_t)(p.RG * 16));
     p.gy = (int)std::max<int64_t>(1, std::min<int64_t>(want_y, max_y));
     p.gy = std::min(p.gy, 65535);
     p.chunk = (rows + p.gy - 1) / p.gy;
@@ -217,15 +217,27 @@ __global__ __launch_bounds__(256) void rowcol_reduce_kernel(
     }
 }
 
-// out[c] = sum_y part[y][c], rounded once to T.
+// out[c] = sum_y part[y][c], rounded once to T.  A block owns 64 columns;
+// its 4 thread rows split the partial rows and meet in LDS.
 template <typename T>
 __global__ __launch_bounds__(256) void finalize_kernel(const float *__restrict__ part, int gy, int C,
                                                        T *__restrict__ out) {
-    const int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= C) return;
+    __shared__ float red[4][64];
+    const int cl = threadIdx.x & 63, yg = threadIdx.x >> 6;
+    const int c = blockIdx.x * 64 + cl;
     float s = 0.f;
-    for (int y = 0; y < gy; ++y) s += part[(int64_t)y * C + c];
-    out[c] = from_f32<T>(s);
+    if (c < C) {
+        int y = yg;
+        for (; y + 12 < gy; y += 16) {
+            const float a0 = part[(int64_t)y * C + c], a1 = part[(int64_t)(y + 4) * C + c];
+            const float a2 = part[(int64_t)(y + 8) * C + c], a3 = part[(int64_t)(y + 12) * C + c];
+            s += (a0 + a1) + (a2 + a3);
+        }
+        for (; y < gy; y += 4) s += part[(int64_t)y * C + c];
+    }
+    red[yg][cl] = s;
+    __syncthreads();
+    if (yg == 0 && c < C) out[c] = from_f32<T>((red[0][cl] + red[1][cl]) + (red[2][cl] + red[3][cl]));
 }
 
 // ---------------------------------------------------------------- avgpool
@@ -287,7 +299,7 @@ __global__ __launch_bounds__(256) void avgpool_bwd_kernel(const T *__restrict__ 
 
 // ------------------------------------------------------------------ launchers
 namespace {
-constexpr int kTargetBlocks = 2048;
+constexpr int kTargetBlocks = 1024;
 
 template <typename T, int V>
 int bn_fwd_t(const RowColPlan &p, const void *x, const void *mean, const void *var, const void *gamma,
@@ -310,7 +322,7 @@ int reduce_t(const RowColPlan &p, const void *a, const void *x, const void *mean
 
 template <typename T>
 int finalize_t(const float *part, int gy, int C, void *out, hipStream_t st) {
-    hipLaunchKernelGGL(finalize_kernel<T>, dim3((C + 255) / 256), dim3(256), 0, st, part, gy, C, (T *)out);
+    hipLaunchKernelGGL(finalize_kernel<T>, dim3((C + 63) / 64), dim3(256), 0, st, part, gy, C, (T *)out);
     return (int)hipGetLastError();
 }
 

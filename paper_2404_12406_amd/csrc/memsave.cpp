@@ -310,7 +310,8 @@ uint32_t kernel_bits(int32_t kind, uint32_t mask) {
 size_t backward_workspace(const Plan &pl, uint32_t kernels) {
     size_t ws = 0;
     if (pl.kind == MS_CONV2D || pl.kind == MS_LINEAR) {
-        if (kernels & MS_K_WGRAD) ws = std::max(ws, ms::conv_wgrad_workspace(pl.dtype, pl.g));
+        if (kernels & MS_K_WGRAD)
+            ws = std::max(ws, ms::conv_wgrad_workspace(pl.dtype, pl.g, (kernels & MS_K_BGRAD) != 0));
         if (kernels & MS_K_BGRAD) ws = std::max(ws, ms::colsum_workspace(pl.dtype, pl.rows, pl.g.K));
     } else if (pl.kind == MS_BN_EVAL) {
         if (kernels & (MS_K_WGRAD | MS_K_BGRAD)) ws = ms::bn_bwd_workspace(pl.dtype, pl.rows, pl.C);
@@ -477,9 +478,15 @@ ms_status ms_layer_backward(ms_record *r, const ms_tensor *grad_y, const ms_tens
     switch (pl.kind) {
     case MS_CONV2D:
     case MS_LINEAR:
+    {
+        bool db_done = false;
         if (!err && (kernels & MS_K_DGRAD)) err = ms::launch_conv_dgrad(pl.dtype, pl.g, dy, r->W.data, grad_x->data, stream);
-        if (!err && (kernels & MS_K_WGRAD)) err = ms::launch_conv_wgrad(pl.dtype, pl.g, dy, r->x.data, grad_W->data, ws, stream);
-        if (!err && (kernels & MS_K_BGRAD)) err = ms::launch_colsum(pl.dtype, dy, pl.rows, pl.g.K, grad_b->data, ws, stream);
+        if (!err && (kernels & MS_K_WGRAD))
+            err = ms::launch_conv_wgrad(pl.dtype, pl.g, dy, r->x.data, grad_W->data,
+                                        (kernels & MS_K_BGRAD) ? grad_b->data : nullptr, ws, stream, &db_done);
+        if (!err && (kernels & MS_K_BGRAD) && !db_done)
+            err = ms::launch_colsum(pl.dtype, dy, pl.rows, pl.g.K, grad_b->data, ws, stream);
+    }
         break;
     case MS_BN_EVAL:
         err = ms::launch_bn_bwd(pl.dtype, dy, (kernels & MS_K_WGRAD) ? r->x.data : nullptr,

@@ -71,17 +71,21 @@ int launch_conv_dgrad(int, const ConvGeom &g, const void *dy, const void *w, voi
     return e;
 }
 
-size_t conv_wgrad_workspace(int, const ConvGeom &g) {
+size_t conv_wgrad_workspace(int, const ConvGeom &g, bool with_db) {
     const long long red = (long long)g.N * g.P * g.Q;
-    return red > 4096 ? (size_t)4 * g.K * g.R * g.S * g.C * 4 : 0;
+    return (red > 4096 ? (size_t)4 * g.K * g.R * g.S * g.C * 4 : 0) + (with_db ? (size_t)4 * g.K * 4 : 0);
 }
 
-int launch_conv_wgrad(int dtype, const ConvGeom &g, const void *dy, const void *x, void *dw, void *ws, void *) {
-    log("conv_wgrad");
+// Like the bf16 fast path, fuses the bias gradient when asked for it (the
+// fp32 path does not: the host must then launch the column sum itself).
+int launch_conv_wgrad(int dtype, const ConvGeom &g, const void *dy, const void *x, void *dw, void *db, void *ws,
+                      void *, bool *db_done) {
+    log(db && dtype == kBF16 ? "conv_wgrad+db" : "conv_wgrad");
+    *db_done = db != nullptr && dtype == kBF16;
     int e = 0;
     if ((long long)g.K * g.R * g.S * g.C > 0) e |= need(dw, "conv_wgrad:dw");
     if ((long long)g.N * g.P * g.Q > 0) e |= need(dy && x, "conv_wgrad:dy,x");
-    if (conv_wgrad_workspace(dtype, g) > 0) e |= need(ws, "conv_wgrad:ws");
+    if (conv_wgrad_workspace(dtype, g, db != nullptr) > 0) e |= need(ws, "conv_wgrad:ws");
     return e;
 }
 

@@ -1,0 +1,70 @@
+"""Every tile shape of the bf16 implicit-GEMM fast path, forced through
+MEMSAVE_GEMM_TILE, in all three contractions, on ragged sizes (including a
+strided input gradient and a fused bias gradient), against the oracle."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2404_12406_amd as ms
+import synth
+
+from _gpu import check, dev, host
+
+pytestmark = pytest.mark.gpu
+
+TILES = ["256x128", "128x128", "128x64"]
+
+CASES = [
+    # x shape, w shape, stride, pad
+    ((3, 24, 13, 11), (40, 24, 3, 3), (1, 1), (1, 1)),
+    ((2, 16, 15, 14), (24, 16, 3, 3), (2, 2), (1, 1)),
+    ((2, 64, 9, 10), (136, 64, 1, 1), (1, 1), (0, 0)),
+    ((1, 48, 12, 9), (72, 48, 5, 3), (3, 2), (2, 1)),
+]
+
+
+@pytest.fixture
+def tile(request):
+    old = os.environ.get("MEMSAVE_GEMM_TILE")
+    os.environ["MEMSAVE_GEMM_TILE"] = request.param
+    yield request.param
+    if old is None:
+        del os.environ["MEMSAVE_GEMM_TILE"]
+    else:
+        os.environ["MEMSAVE_GEMM_TILE"] = old
+
+
+@pytest.mark.parametrize("tile", TILES, indirect=True)
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_conv_tiles(tile, case):
+    xs, ws, stride, pad = CASES[case]
+    seed = 7000 + 10 * case
+    x = synth.normal(xs, seed, dtype="bf16")
+    w = synth.kaiming_uniform(ws, seed + 1, ws[1] * ws[2] * ws[3], dtype="bf16")
+    b = synth.normal((ws[0],), seed + 2, 0.1, dtype="bf16")
+    y, rec = ms.layer_forward(ms.Conv2d(stride, pad), dev(x, "bf16"), dev(w, "bf16"), dev(b, "bf16"), 7)
+    check("y", host(y), oracle.conv2d_forward(x, w, b, stride, pad), "bf16")
+    gy = synth.normal(tuple(y.shape), seed + 3, dtype="bf16")
+    gx, gw, gb = ms.layer_backward(rec, dev(gy, "bf16"))
+    check("dx", host(gx), oracle.conv2d_input_grad(gy, w, xs, stride, pad), "bf16")
+    check("dW", host(gw), oracle.conv2d_weight_grad(gy, x, ws, stride, pad), "bf16")
+    check("db", host(gb), oracle.conv2d_bias_grad(gy), "bf16")
+
+
+@pytest.mark.parametrize("tile", TILES, indirect=True)
+@pytest.mark.parametrize("shape", [(300, 72, 136), (520, 264, 392), (1000, 520, 64)])
+def test_linear_tiles(tile, shape):
+    M, Kin, Nout = shape
+    seed = 7500 + M
+    x = synth.normal((M, Kin), seed, dtype="bf16")
+    w = synth.normal((Nout, Kin), seed + 1, 0.05, dtype="bf16")
+    b = synth.normal((Nout,), seed + 2, 0.02, dtype="bf16")
+    y, rec = ms.layer_forward(ms.Linear(), dev(x, "bf16"), dev(w, "bf16"), dev(b, "bf16"), 7)
+    check("y", host(y), oracle.linear_forward(x, w, b), "bf16")
+    gy = synth.normal((M, Nout), seed + 3, dtype="bf16")
+    gx, gw, gb = ms.layer_backward(rec, dev(gy, "bf16"))
+    check("dX", host(gx), oracle.linear_input_grad(gy, w), "bf16")
+    check("dW", host(gw), oracle.linear_weight_grad(gy, x), "bf16")
+    check("db", host(gb), oracle.linear_bias_grad(gy), "bf16")
