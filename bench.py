@@ -115,9 +115,35 @@ def all_true(l):
     return 1 | 2 | (4 if l.has_bias else 0)
 
 
+# ------------------------------------------------------------------ recorded counters
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_linear_stack_bf16_hbm_counters.md")
+GEMM_SOURCES = ("paper_2404_12406_amd/csrc/kernels/gemm_bf16.hip", "paper_2404_12406_amd/csrc/kernels/common.h")
+
+
+def recorded_traffic():
+    """HBM bytes per forward-GEMM launch from the committed FETCH_SIZE /
+    WRITE_SIZE counter summary, or None when the GEMM sources changed since
+    the counters were taken (or the summary is absent)."""
+    import hashlib
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None
+    fields = dict(l.split(": ", 1) for l in text.splitlines() if l.startswith(("traffic_bytes_per_launch: ",
+                                                                                 "kernel_sources_sha256: ")))
+    h = hashlib.sha256()
+    for p in GEMM_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    if fields.get("kernel_sources_sha256", "").strip() != h.hexdigest():
+        return None
+    return int(fields["traffic_bytes_per_launch"])
+
+
 # ------------------------------------------------------------------ headline
 def headline(steps, warmup):
     import torch
+    import paper_2404_12406_amd as ms
     from synth import draw, gpu
     from synth import workloads as wl
 
@@ -131,34 +157,35 @@ def headline(steps, warmup):
         chain.forward()
         chain.backward()
     torch.cuda.synchronize()
-    # per-launch HIP events around every forward GEMM (the dominant kernel:
-    # one launch per call, on the stream the library launches on)
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(steps * len(chain.prepared))]
+    # The library brackets each forward / input-gradient GEMM launch with HIP
+    # events on the stream it launches on; the dominant kernel is the mode
+    # with the larger summed GPU time over the timed region.
+    ms.profile_start(ms.PROF_FWD | ms.PROF_DGRAD)
     t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t0.record()
-    k = 0
     for _ in range(steps):
-        for p in chain.prepared:
-            a, b = evs[k]
-            a.record()
-            p.forward()
-            b.record()
-            k += 1
+        chain.forward()
         chain.backward()
     t1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     ms_step = t0.elapsed_time(t1) / steps
-    gemm_ms = [a.elapsed_time(b) for a, b in evs]
-    avg_gemm_ms = sum(gemm_ms) / len(gemm_ms)
-    gemm_flop = fl[0]["fwd"]
-    assert all(f["fwd"] == gemm_flop for f in fl)
-    achieved = gemm_flop / (avg_gemm_ms * 1e-3) / 1e12
+    kern = {}
+    for name, kind, key in (("forward", ms.PROF_FWD, "fwd"), ("input-gradient", ms.PROF_DGRAD, "dgrad")):
+        n, tot = ms.profile_read(kind)
+        flop = sum(f[key] for f in fl) * steps
+        kern[key] = {"name": name, "launches": n, "ms": tot, "flop": flop}
+    ms.profile_start(0)
+    dom = max(kern.values(), key=lambda k: k["ms"])
+    assert dom["launches"] == steps * len(w.layers), dom
+    avg_ms = dom["ms"] / dom["launches"]
+    achieved = dom["flop"] / (dom["ms"] * 1e-3) / 1e12
     value = flop_step / (ms_step * 1e-3) / 1e12
-    log(f"[bench] headline {ms_step:.3f} ms/step, {value:.1f} TFLOP/s; forward GEMM avg {avg_gemm_ms * 1e3:.1f} us "
+    for k in kern.values():
+        log(f"[bench]   {k['name']} GEMM: {k['launches']} launches, avg {k['ms'] / max(k['launches'], 1) * 1e3:.1f} us, "
+            f"{k['flop'] / max(k['ms'], 1e-9) / 1e9:.1f} TFLOP/s")
+    log(f"[bench] headline {ms_step:.3f} ms/step, {value:.1f} TFLOP/s; dominant {dom['name']} GEMM "
         f"= {achieved:.1f} TFLOP/s; host wall {wall * 1e3 / steps:.3f} ms/step")
 
     sel = ledger_peak_of_forward([chain])
@@ -175,9 +202,11 @@ def headline(steps, warmup):
         "value": value,
         "flop_step": flop_step,
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
-                     "kernel": "igemm_kernel<bf16, fwd, 1x1> (Linear forward)",
-                     "flop_per_launch": gemm_flop, "avg_launch_us": round(avg_gemm_ms * 1e3, 2)},
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": recorded_traffic() if dom["name"] == "forward" else None,
+                     "kernel": f"ms::g2::gemm_kernel ({dom['name']} GEMM of the Linear layers)",
+                     "flop_per_launch": dom["flop"] // dom["launches"], "avg_launch_us": round(avg_ms * 1e3, 2),
+                     "launches": dom["launches"]},
         "saved": {"selective": sel, "all_true": allb},
     }
 
@@ -265,7 +294,7 @@ def extras(steps, warmup):
 
 
 # ------------------------------------------------------------------ CPU baseline
-def cpu_baseline(target_s: float = 12.0):
+def cpu_baseline(target_s: float = 20.0):
     """The oracle (fp64 C loops, OpenMP) on the first `rows` rows of the
     headline workload: forward, input gradient and bias gradient of the four
     layers; the rate scales to the whole step by its FLOP count."""
@@ -298,6 +327,23 @@ def cpu_baseline(target_s: float = 12.0):
                       f"of all 4 layers ({rows * per_row / 1e9:.2f} GFLOP in {t:.1f} s, fp64)"}
 
 
+COPY_BYTES = 256 << 20
+
+
+def copy_calibration():
+    """Three device-to-device copies of COPY_BYTES each (read COPY_BYTES,
+    write COPY_BYTES): the reference kernel against which counter readings
+    of the GEMMs are scaled to bytes."""
+    import torch
+    src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda").normal_()
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"[bench] copy calibration: 3 x {COPY_BYTES >> 20} MiB")
+
+
 # ------------------------------------------------------------------ main
 def main():
     ap = argparse.ArgumentParser()
@@ -306,6 +352,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-extra", action="store_true", help="skip the context workloads")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="first run three plain 256 MiB device copies, the known-size reference "
+                         "for hardware byte counters (FETCH_SIZE / WRITE_SIZE) of the same process")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the layers need no cross-GPU communication on this "
@@ -318,6 +367,8 @@ def main():
         sys.exit(1)
     torch.cuda.set_device(0)
     log(f"[bench] {ms.version()} on {torch.cuda.get_device_name(0)}")
+    if args.calibrate_copy:
+        copy_calibration()
     h = headline(args.steps, args.warmup)
     line = {
         "metric": METRIC,

@@ -176,6 +176,26 @@ ms_status ms_ledger_reset(void);
 ms_status ms_policy_account(const ms_layer *layer, const ms_tensor *x, const ms_tensor *W,
                             const ms_tensor *b, uint32_t mask, int32_t policy, ms_account *out);
 
+/*
+ * Kernel timing (diagnostics).  While armed, the library brackets every
+ * launch of the selected kernel kinds with a pair of HIP events recorded on
+ * the launch stream, so the caller can read the kernels' own GPU time over a
+ * region of its choice.  Only the contraction kernel itself is bracketed
+ * (not the weight transpose or reduction kernels around it).
+ *   MS_PROF_FWD   forward convolution / linear GEMM
+ *   MS_PROF_DGRAD input-gradient GEMM
+ *   MS_PROF_WGRAD weight-gradient GEMM (its split-K partial launch)
+ *   MS_PROF_BN    BN-eval forward kernel
+ * ms_profile_start() discards earlier records and arms `kinds` (0 disarms);
+ * at most 65536 launches per kind are recorded.  ms_profile_read() waits
+ * for the recorded events and returns the number of launches of one kind and
+ * their summed duration in milliseconds.  Calls from several threads or
+ * streams at once are serialised internally.
+ */
+enum { MS_PROF_FWD = 1u, MS_PROF_DGRAD = 2u, MS_PROF_WGRAD = 4u, MS_PROF_BN = 8u };
+ms_status ms_profile_start(uint32_t kinds);
+ms_status ms_profile_read(uint32_t kind, uint64_t *launches, double *total_ms);
+
 /* Static description of a status code. */
 const char *ms_status_str(int32_t status);
 

@@ -10,12 +10,13 @@ with `python -m paper_2404_12406_amd.build`.
 from .api import (AvgPool, BatchNormEval, Conv2d, Linear, MASK_BIAS, MASK_INPUT, MASK_WEIGHT,
                   POLICY_ALL_TRUE, POLICY_PYTORCH_DEFAULT, POLICY_SELECTIVE, PreparedLayer, Record, empty_like_layout,
                   layer_backward, layer_forward, ledger_read, ledger_reset, output_shape, policy_account,
-                  tensor_desc, version)
+                  profile_read, profile_start, PROF_BN, PROF_DGRAD, PROF_FWD, PROF_WGRAD, tensor_desc, version)
 from ._lib import MemsaveError
 
 __all__ = [
     "AvgPool", "BatchNormEval", "Conv2d", "Linear", "MASK_BIAS", "MASK_INPUT", "MASK_WEIGHT",
     "POLICY_ALL_TRUE", "POLICY_PYTORCH_DEFAULT", "POLICY_SELECTIVE", "PreparedLayer", "Record", "MemsaveError",
     "empty_like_layout", "layer_backward", "layer_forward", "ledger_read", "ledger_reset",
-    "output_shape", "policy_account", "tensor_desc", "version",
+    "output_shape", "policy_account", "profile_read", "profile_start", "PROF_BN", "PROF_DGRAD", "PROF_FWD",
+    "PROF_WGRAD", "tensor_desc", "version",
 ]

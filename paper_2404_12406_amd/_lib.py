@@ -22,7 +22,9 @@ EXPORTS = (
     "ms_layer_forward", "ms_layer_backward", "ms_record_account", "ms_record_free",
     "ms_ledger_read", "ms_ledger_reset", "ms_policy_account", "ms_status_str",
     "ms_last_error", "ms_version", "ms_testing_fail_next_workspace", "ms_testing_live_records",
+    "ms_profile_start", "ms_profile_read",
 )
+MS_PROF_FWD, MS_PROF_DGRAD, MS_PROF_WGRAD, MS_PROF_BN = 1, 2, 4, 8
 
 
 class MsTensor(ctypes.Structure):
@@ -83,6 +85,10 @@ def configure(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.ms_testing_fail_next_workspace.restype = None
     lib.ms_testing_live_records.argtypes = []
     lib.ms_testing_live_records.restype = ctypes.c_int64
+    lib.ms_profile_start.argtypes = [ctypes.c_uint32]
+    lib.ms_profile_start.restype = ctypes.c_int
+    lib.ms_profile_read.argtypes = [ctypes.c_uint32, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_double)]
+    lib.ms_profile_read.restype = ctypes.c_int
     return lib
 
 

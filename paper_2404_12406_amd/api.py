@@ -267,6 +267,21 @@ def ledger_reset():
     check(_lib.load().ms_ledger_reset(), "ms_ledger_reset")
 
 
+PROF_FWD, PROF_DGRAD, PROF_WGRAD, PROF_BN = 1, 2, 4, 8
+
+
+def profile_start(kinds: int):
+    """Arm HIP-event timing of the selected kernel kinds (PROF_* bits)."""
+    check(_lib.load().ms_profile_start(int(kinds)), "ms_profile_start")
+
+
+def profile_read(kind: int):
+    """(launches, total milliseconds) of one kernel kind since profile_start."""
+    n, t = ctypes.c_uint64(), ctypes.c_double()
+    check(_lib.load().ms_profile_read(int(kind), ctypes.byref(n), ctypes.byref(t)), "ms_profile_read")
+    return int(n.value), float(t.value)
+
+
 def version() -> str:
     return _lib.load().ms_version().decode()
 

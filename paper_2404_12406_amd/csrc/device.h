@@ -25,9 +25,11 @@ struct ConvGeom {
 int launch_conv_fwd(int dtype, const ConvGeom &g, const void *x, const void *w,
                     const void *bias, void *y, void *stream);
 
-// dx = input gradient of the convolution for grad dy (needs w only).
+// dx = input gradient of the convolution for grad dy (needs w only).  May
+// use conv_dgrad_workspace() bytes of workspace (a transposed copy of w).
+size_t conv_dgrad_workspace(int dtype, const ConvGeom &g);
 int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *w,
-                      void *dx, void *stream);
+                      void *dx, void *ws, void *stream);
 
 // dw = weight gradient for grad dy and input x.  Needs conv_wgrad_workspace()
 // bytes of device workspace (may be 0).  When db is non-null the launcher may
@@ -65,5 +67,12 @@ void *workspace_get(void *stream, size_t bytes, int *err);
 void workspace_fail_next(int n);
 
 int device_last_error();  // hipGetLastError()
+
+// Kernel timing (profile.hip): prof_mark(kind, stream, true) before a launch
+// and (.., false) after it record an event pair when `kind` is armed.
+enum ProfKind : unsigned { kProfFwd = 1u, kProfDgrad = 2u, kProfWgrad = 4u, kProfBn = 8u };
+void prof_mark(unsigned kind, void *stream, bool begin);
+int prof_start(unsigned kinds);
+int prof_read(unsigned kind, uint64_t *launches, double *total_ms);
 
 }  // namespace ms

@@ -140,7 +140,7 @@ template <int MODE, int BM, int BN, int STAGES, bool UNIT>
 struct Cfg {
     static constexpr int BK = 32;
     static constexpr bool A_KC = MODE != kWgrad;
-    static constexpr bool B_KC = MODE == kFwd;
+    static constexpr bool B_KC = MODE != kWgrad;   // DGRAD reads W transposed to [C][R][S][K]
     static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
     static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
     static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;
@@ -256,7 +256,8 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const Args P) {
             const int row = (wave * NIB + j) * 16 + kc_row;
             const int n = n0 + row;
             b_ok[j] = n < N;
-            b_base[j] = (b_ok[j] ? n : 0) * Kg;
+            // FWD: W[n][(r,s,c)] (row length R*S*C); DGRAD: Wt[c][(r,s,k)] (R*S*K)
+            b_base[j] = (b_ok[j] ? n : 0) * (MODE == kFwd ? Kg : g.R * g.S * g.K);
         }
     } else {
         constexpr int SPR = BN / 8, KPI = 64 / SPR;
@@ -335,12 +336,19 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const Args P) {
         if constexpr (G::B_KC) {
             const int kk = k0 + kc * 8;
             const bool kin = kk < k_end;
+            int off_k = kk;
+            if constexpr (MODE == kDgrad && !UNIT) {
+                // kk = (t_r, t_s, k) of this phase -> tap (r, s) of Wt[c][r][s][k]
+                const int t = kk / g.K, k = kk - t * g.K;
+                const int tr = f.Sp > 0 ? t / f.Sp : 0, ts = t - tr * f.Sp;
+                off_k = ((f.fh + tr * g.sh) * g.S + f.fw + ts * g.sw) * g.K + k;
+            }
 #pragma unroll
             for (int j = 0; j < NIB; ++j) {
                 const bool ok = kin && b_ok[j];
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(
                     rb, (lds_void_t *)(sB + (wave * NIB + j) * 1024), 16,
-                    ok ? (uint32_t)(b_base[j] + kk) * 2u : kOOB, 0, 0, 0);
+                    ok ? (uint32_t)(b_base[j] + off_k) * 2u : kOOB, 0, 0, 0);
             }
         } else {
             constexpr int SPR = BN / 8, KPI = 64 / SPR;
@@ -349,16 +357,8 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const Args P) {
                 const int kk = k0 + (wave * NIB + j) * KPI + lane / SPR;
                 bool ok = b_ok[j] && kk < k_end;
                 uint32_t off = 0;
-                if constexpr (MODE == kDgrad) {
-                    if constexpr (UNIT) {
-                        off = (uint32_t)kk * (uint32_t)g.C + b_mn_off[j];
-                    } else {
-                        const int t = kk / g.K, k = kk - t * g.K;
-                        const int tr = f.Sp > 0 ? t / f.Sp : 0, ts = t - tr * f.Sp;
-                        const int r = f.fh + tr * g.sh, s = f.fw + ts * g.sw;
-                        off = (uint32_t)(((k * g.R + r) * g.S + s) * g.C) + b_mn_off[j];
-                    }
-                } else {   // WGRAD: x im2col, k-row = (n,p,q), slot along (r,s,c)
+                {
+                    // WGRAD: x im2col, k-row = (n,p,q), slot along (r,s,c)
                     if constexpr (UNIT) {
                         off = (uint32_t)kk * (uint32_t)g.C + b_mn_off[j];
                     } else {
@@ -582,6 +582,27 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const Args P) {
     }
 }
 
+// Wt[c][rs][k] = W[k][rs][c]: the input gradient reads the (frozen) filter
+// with its reduction index k contiguous.  64 x 64 tiles through LDS, both
+// sides coalesced; grid (C/64, K/64, R*S).
+__global__ __launch_bounds__(256) void transpose_krsc_kernel(const bf16 *__restrict__ W, bf16 *__restrict__ Wt,
+                                                             int K, int RS, int C) {
+    __shared__ bf16 t[64][66];
+    const int c0 = blockIdx.x * 64, k0 = blockIdx.y * 64, rs = blockIdx.z;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+#pragma unroll 4
+    for (int i = ty; i < 64; i += 4) {
+        const int k = k0 + i, c = c0 + tx;
+        if (k < K && c < C) t[i][tx] = W[((size_t)k * RS + rs) * C + c];
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int i = ty; i < 64; i += 4) {
+        const int c = c0 + i, k = k0 + tx;
+        if (k < K && c < C) Wt[((size_t)c * RS + rs) * K + k] = t[tx][i];
+    }
+}
+
 // Sum split-K partials (and fused bias-gradient partials) to bf16.
 __global__ __launch_bounds__(256) void reduce_kernel(const float *__restrict__ part, int splits, int64_t n,
                                                      bf16 *__restrict__ out, const float *__restrict__ dbpart,
@@ -622,7 +643,7 @@ struct Tile {
     int bm, bn, per_cu;   // tile shape, blocks resident per CU
     float eff;            // relative MFMA efficiency of the shape
 };
-constexpr Tile kTiles[] = {{256, 128, 1, 0.90f}, {128, 128, 2, 0.80f}, {128, 64, 3, 0.60f}};
+constexpr Tile kTiles[] = {{256, 128, 1, 1.05f}, {128, 128, 2, 1.00f}, {128, 64, 3, 0.75f}};
 
 // MEMSAVE_GEMM_TILE=<bm>x<bn> forces one tile shape (a debugging and
 // testing knob); returns its index or -1.
@@ -672,8 +693,12 @@ Tile pick(long M, long N, long K, int splits_allowed, int *splits_out, int z = 1
 
 template <int MODE, int BM, int BN, bool UNIT>
 int go(const Args &a, dim3 grid, hipStream_t st) {
+    const unsigned pk = MODE == kFwd ? kProfFwd : MODE == kDgrad ? kProfDgrad : kProfWgrad;
+    prof_mark(pk, st, true);
     hipLaunchKernelGGL((gemm_kernel<MODE, BM, BN, 4, UNIT>), grid, dim3(256), 0, st, a);
-    return (int)hipGetLastError();
+    const int err = (int)hipGetLastError();
+    prof_mark(pk, st, false);
+    return err;
 }
 
 template <int MODE, bool UNIT>
@@ -730,14 +755,23 @@ int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, 
     return go_mode<kFwd>(t, a, dim3(a.ntm * a.ntn, 1, 1), unit_geom(g), st);
 }
 
-int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, hipStream_t st) {
-    if (g.C % 8 != 0 || g.K % 8 != 0 || !al16(dy) || !al16(w) || !al16(dx)) return -1;
+size_t dgrad_workspace(const ConvGeom &g) {
+    if (g.C % 8 != 0 || g.K % 8 != 0) return 0;
+    return (size_t)g.K * g.R * g.S * g.C * sizeof(bf16) + 256;
+}
+
+int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, void *ws, hipStream_t st) {
+    if (g.C % 8 != 0 || g.K % 8 != 0 || !ws || !al16(dy) || !al16(w) || !al16(dx) || !al16(ws)) return -1;
     Args a{};
-    a.a = (const bf16 *)dy; a.b = (const bf16 *)w; a.c = (bf16 *)dx; a.g = g;
+    a.a = (const bf16 *)dy; a.b = (const bf16 *)ws; a.c = (bf16 *)dx; a.g = g;
     const int Hb = (g.H + g.sh - 1) / g.sh, Wb = (g.W + g.sw - 1) / g.sw;
     a.M = g.N * Hb * Wb; a.N = g.C;
     a.K = ((g.R + g.sh - 1) / g.sh) * ((g.S + g.sw - 1) / g.sw) * g.K;
     if (a.M == 0 || a.N == 0) return 0;
+    hipLaunchKernelGGL(transpose_krsc_kernel, dim3((g.C + 63) / 64, (g.K + 63) / 64, g.R * g.S), dim3(256), 0, st,
+                       (const bf16 *)w, (bf16 *)ws, g.K, g.R * g.S, g.C);
+    int err = (int)hipGetLastError();
+    if (err) return err;
     Tile t = pick(a.M, a.N, a.K, 1, nullptr, g.sh * g.sw);
     a.ntm = (a.M + t.bm - 1) / t.bm; a.ntn = (a.N + t.bn - 1) / t.bn;
     a.splits = 1; a.k_split = a.K;

@@ -34,7 +34,8 @@ namespace ms {
 // bf16 fast path (gemm_bf16.hip); each returns -1 when it does not apply.
 namespace g2 {
 int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, void *y, hipStream_t st);
-int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, hipStream_t st);
+size_t dgrad_workspace(const ConvGeom &g);
+int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, void *ws, hipStream_t st);
 bool wgrad_applies(const ConvGeom &g);
 size_t wgrad_workspace(const ConvGeom &g, bool with_db);
 int conv_wgrad(const ConvGeom &g, const void *dy, const void *x, void *dw, void *db, void *ws, hipStream_t st);
@@ -568,8 +569,12 @@ bool is_unit(const ConvGeom &g) {
 template <typename T, int MODE, bool VEC_OK, bool UNIT>
 int launch_t(const IgemmParams &prm, dim3 grid, hipStream_t st) {
     constexpr int BK = bk_of<T>();
+    const unsigned pk = MODE == kFwd ? kProfFwd : MODE == kDgrad ? kProfDgrad : kProfWgrad;
+    prof_mark(pk, st, true);
     hipLaunchKernelGGL((igemm_kernel<T, MODE, kBM, kBN, BK, VEC_OK, UNIT>), grid, dim3(256), 0, st, prm);
-    return (int)hipGetLastError();
+    const int err = (int)hipGetLastError();
+    prof_mark(pk, st, false);
+    return err;
 }
 
 template <typename T, int MODE>
@@ -636,10 +641,14 @@ int launch_conv_fwd(int dtype, const ConvGeom &g, const void *x, const void *w, 
     return launch_dtype<kFwd>(dtype, prm, grid, vec_ok, is_unit(g), (hipStream_t)stream);
 }
 
+size_t conv_dgrad_workspace(int dtype, const ConvGeom &g) {
+    return dtype == kBF16 ? g2::dgrad_workspace(g) : 0;
+}
+
 int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *w, void *dx,
-                      void *stream) {
+                      void *ws, void *stream) {
     if (dtype == kBF16) {
-        const int r = g2::conv_dgrad(g, dy, w, dx, (hipStream_t)stream);
+        const int r = g2::conv_dgrad(g, dy, w, dx, ws, (hipStream_t)stream);
         if (r >= 0) return r;
     }
     IgemmParams prm{};

@@ -304,10 +304,13 @@ constexpr int kTargetBlocks = 1024;
 template <typename T, int V>
 int bn_fwd_t(const RowColPlan &p, const void *x, const void *mean, const void *var, const void *gamma,
              const void *beta, float eps, int64_t rows, int C, void *y, hipStream_t st) {
+    prof_mark(kProfBn, st, true);
     hipLaunchKernelGGL((bn_fwd_kernel<T, V>), dim3(p.gx, p.gy), dim3(256), 0, st, (const T *)x,
                        (const T *)mean, (const T *)var, (const T *)gamma, (const T *)beta, eps, rows, C,
                        p.TC, p.RG, p.chunk, (T *)y);
-    return (int)hipGetLastError();
+    const int err = (int)hipGetLastError();
+    prof_mark(kProfBn, st, false);
+    return err;
 }
 
 template <typename T, int V, int MODE>

@@ -310,6 +310,7 @@ uint32_t kernel_bits(int32_t kind, uint32_t mask) {
 size_t backward_workspace(const Plan &pl, uint32_t kernels) {
     size_t ws = 0;
     if (pl.kind == MS_CONV2D || pl.kind == MS_LINEAR) {
+        if (kernels & MS_K_DGRAD) ws = std::max(ws, ms::conv_dgrad_workspace(pl.dtype, pl.g));
         if (kernels & MS_K_WGRAD)
             ws = std::max(ws, ms::conv_wgrad_workspace(pl.dtype, pl.g, (kernels & MS_K_BGRAD) != 0));
         if (kernels & MS_K_BGRAD) ws = std::max(ws, ms::colsum_workspace(pl.dtype, pl.rows, pl.g.K));
@@ -480,7 +481,7 @@ ms_status ms_layer_backward(ms_record *r, const ms_tensor *grad_y, const ms_tens
     case MS_LINEAR:
     {
         bool db_done = false;
-        if (!err && (kernels & MS_K_DGRAD)) err = ms::launch_conv_dgrad(pl.dtype, pl.g, dy, r->W.data, grad_x->data, stream);
+        if (!err && (kernels & MS_K_DGRAD)) err = ms::launch_conv_dgrad(pl.dtype, pl.g, dy, r->W.data, grad_x->data, ws, stream);
         if (!err && (kernels & MS_K_WGRAD))
             err = ms::launch_conv_wgrad(pl.dtype, pl.g, dy, r->x.data, grad_W->data,
                                         (kernels & MS_K_BGRAD) ? grad_b->data : nullptr, ws, stream, &db_done);
@@ -551,6 +552,22 @@ ms_status ms_policy_account(const ms_layer *layer, const ms_tensor *x, const ms_
     const uint32_t borrowed = borrowed_bits(pl.kind, mask, policy, pl.has_w, pl.has_b);
     *out = make_account(pl, eff, borrowed, kernel_bits(pl.kind, eff));
     return MS_OK;
+}
+
+ms_status ms_profile_start(uint32_t kinds) {
+    clear_err();
+    if (kinds & ~15u) return fail(MS_E_ARG, "unknown profile kinds 0x%x", kinds);
+    const int err = ms::prof_start(kinds);
+    return err ? hip_fail(err, "ms_profile_start") : MS_OK;
+}
+
+ms_status ms_profile_read(uint32_t kind, uint64_t *launches, double *total_ms) {
+    clear_err();
+    if (!launches || !total_ms) return fail(MS_E_NULL, "NULL argument");
+    if (kind != MS_PROF_FWD && kind != MS_PROF_DGRAD && kind != MS_PROF_WGRAD && kind != MS_PROF_BN)
+        return fail(MS_E_ARG, "read one kind at a time");
+    const int err = ms::prof_read(kind, launches, total_ms);
+    return err ? hip_fail(err, "ms_profile_read") : MS_OK;
 }
 
 const char *ms_status_str(int32_t s) {

@@ -62,8 +62,13 @@ int launch_conv_fwd(int, const ConvGeom &g, const void *x, const void *w, const 
     return e;
 }
 
-int launch_conv_dgrad(int, const ConvGeom &g, const void *dy, const void *w, void *dx, void *) {
+size_t conv_dgrad_workspace(int dtype, const ConvGeom &g) {
+    return dtype == kBF16 ? (size_t)g.K * g.R * g.S * g.C * 2 : 0;
+}
+
+int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *w, void *dx, void *ws, void *) {
     log("conv_dgrad");
+    if (conv_dgrad_workspace(dtype, g) > 0 && !ws) return need(false, "conv_dgrad:ws");
     const long long out = (long long)g.N * g.H * g.W * g.C;
     int e = 0;
     if (out > 0) e |= need(dx && w, "conv_dgrad:dx,w");
@@ -150,5 +155,13 @@ void workspace_fail_next(int n) {
 }
 
 int device_last_error() { return 0; }
+
+void prof_mark(unsigned, void *, bool) {}
+int prof_start(unsigned) { return 0; }
+int prof_read(unsigned, uint64_t *launches, double *total_ms) {
+    *launches = 0;
+    *total_ms = 0.0;
+    return 0;
+}
 
 }  // namespace ms

@@ -249,3 +249,21 @@ def test_frozen_weight_input_is_freed_by_allocator():
         assert rec.account()["saved_activation_bytes"] == (nbytes if keeps else 0)
         assert freed == (0 if keeps else nbytes)
         rec.free()
+
+
+def test_kernel_timing_counts_launches():
+    """ms_profile_* brackets exactly the armed contraction launches."""
+    x, w, b = _conv_inputs(7, (2, 32, 16, 16), (64, 32, 3, 3), "bf16")
+    X, Wt, B = dev(x, "bf16"), dev(w, "bf16"), dev(b, "bf16")
+    ms.profile_start(ms.PROF_FWD | ms.PROF_DGRAD)
+    for _ in range(3):
+        y, rec = ms.layer_forward(ms.Conv2d((1, 1), (1, 1)), X, Wt, B, 3)
+        ms.layer_backward(rec, torch.ones_like(y))
+    nf, tf = ms.profile_read(ms.PROF_FWD)
+    nd, td = ms.profile_read(ms.PROF_DGRAD)
+    nw, tw = ms.profile_read(ms.PROF_WGRAD)
+    ms.profile_start(0)
+    assert (nf, nd, nw) == (3, 3, 0)
+    assert tf > 0 and td > 0 and tw == 0
+    y, rec = ms.layer_forward(ms.Conv2d((1, 1), (1, 1)), X, Wt, B, 0)
+    assert ms.profile_read(ms.PROF_FWD) == (0, 0.0)
