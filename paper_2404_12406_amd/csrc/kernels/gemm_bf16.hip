@@ -4,24 +4,27 @@
 // (needs x only) -- for NHWC activations and KRSC filters.  The GEMM views
 // and the stride-phase split of the input gradient are those of igemm.hip.
 //
-// Data movement (per block, 256 threads = 4 waves in a 2 x 2 grid):
+// Data movement (per block of NW = 4 or 8 waves in a WR x WC grid):
 //  * operands go from HBM straight into LDS with buffer_load_dwordx4 ... lds
 //    (no VGPR staging).  Each lane computes the byte offset of its 16-byte
 //    chunk; lanes that fall into padding, a ragged tail or a missing tap use
 //    an offset beyond the buffer's range and the hardware writes zeros.
-//  * STAGES LDS buffers form a ring: tiles kt+1 .. kt+STAGES-1 are in flight
-//    while tile kt feeds the MFMAs (one barrier per BK step).
+//  * the reduction step is BK = 64: a K-contiguous tile row is 128 bytes, one
+//    full cache line, so every load instruction moves eight whole lines
+//    (BK = 32 rows are half lines and cost the vector-memory path twice the
+//    work per byte).
+//  * STAGES LDS buffers form a ring with one barrier per BK step; within a
+//    step the fragments of the next 16-k slice are read from LDS while the
+//    MFMAs of the current slice run (register double buffering per slice).
 //  * operands contiguous along k are stored [row][k] with 16-byte chunks
 //    XOR-swizzled by row and read as MFMA fragments with ds_read_b128;
 //    operands contiguous along m/n are stored [k][mn] with 16-byte slots
 //    swizzled by k-row and read with ds_read_b64_tr_b16, which transposes a
 //    16 x 4 block of b16 within each 16-lane group (two reads = 8 k values).
-//  * v_mfma_f32_32x32x16_bf16 (a single wave issues it at ~92% of the
-//    matrix peak; the 16x16x32 form reaches only ~55%) with the B fragment
-//    as first operand, so each lane ends with groups of 4 consecutive output
-//    columns of one row; the epilogue
-//    packs them to bf16, stages the tile through LDS and writes 16-byte
-//    vectors (fp32 split-K partials are stored as float4 directly).
+//  * v_mfma_f32_32x32x16_bf16 with the B fragment as first operand, so each
+//    lane ends with groups of 4 consecutive output columns of one row; the
+//    epilogue packs them to bf16, stages the tile through LDS and writes
+//    16-byte vectors (fp32 split-K partials are stored as float4 directly).
 //  * weight gradient: long reductions are split over grid z; when the bias
 //    gradient is requested too, the waves that load dy (operand A) add up
 //    its rows from their fragments -- the bias gradient costs no extra read.
@@ -42,6 +45,7 @@ typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
 enum Mode { kFwd = 0, kDgrad = 1, kWgrad = 2 };
 
 constexpr uint32_t kOOB = 0xFFFFFFF0u;   // byte offset beyond any buffer: loads return 0
+constexpr int BK = 64;                   // reduction step (elements)
 
 struct Args {
     const bf16 *a;
@@ -80,6 +84,13 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *p, uint32_t b
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
 }
 
+// One 16-byte LDS-DMA load.  The offset is computed into a named value first:
+// passing a conditional expression straight into the builtin inside a kernel
+// template makes the host pass drop the kernel's launch stub.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, char *lds, uint32_t off) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t *)lds, 16, off, 0, 0, 0);
+}
+
 // s_waitcnt with only vmcnt constrained (gfx9 encoding: vmcnt[3:0] | [15:14],
 // expcnt[6:4] = 7, lgkmcnt[11:8] = 15).
 template <int N>
@@ -87,12 +98,12 @@ __device__ __forceinline__ void wait_vmcnt() {
     static_assert(N >= 0 && N < 64, "vmcnt range");
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xc07f); }
 
-// 16-byte chunk swizzle of a K-contiguous tile row (BK = 32: 4 chunks per
-// 64-byte row).  Depends on row bits 1..3 only, so a lane's chunk is the same
-// in every 16-row load instruction; spreads the 16 rows one fragment read
-// touches over distinct bank groups.
-__device__ __forceinline__ int swz_k(int row) { return ((row >> 1) & 3) ^ ((row >> 3) & 1); }
+// 16-byte chunk swizzle of a K-contiguous tile row (128 bytes = 8 chunks).
+// 16 consecutive rows reading the same logical chunk land on 16 distinct
+// 16-byte bank groups (the LDS serves 256 bytes per clock).
+__device__ __forceinline__ int swz_k(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 
 // Slot swizzle of an M/N-contiguous tile k-row ([k][mn], 16-byte slots):
 // XOR with an even value so the two slots one transposed read touches stay
@@ -103,7 +114,7 @@ __device__ __forceinline__ int swz_m(int krow) {
     else return (krow & 3) << 1;
 }
 
-// MFMA fragment (8 k values of one m/n index) from a [32 k][R mn] tile for
+// MFMA fragment (8 k values of one m/n index) from a [BK k][R mn] tile for
 // the 32x32x16 shape: lane l needs column mn0 + l%32 at k-rows
 // 16*sub + 8*(l/32) .. +7.  ds_read_b64_tr_b16 works per 16-lane group
 // g = l/16: lane 16g + r addresses k-row kb + 4h + r/4 at columns
@@ -127,43 +138,45 @@ __device__ __forceinline__ bf16x8 frag_mn(const char *base, int mn0, int sub, in
     return v;
 }
 
-// Fragment from a row-major [row][32 k] tile (64-byte rows, swizzled
-// 16-byte chunks): lane l reads row `row` (= tile row + l%32), chunk
-// 2*sub + l/32.
+// Fragment from a row-major [row][BK] tile (128-byte rows, swizzled 16-byte
+// chunks): lane l reads row `row` (= tile row + l%32), chunk 2*sub + l/32.
 __device__ __forceinline__ bf16x8 frag_kc(const char *base, int row, int sub, int lane) {
     const int chunk = 2 * sub + (lane >> 5);
-    const int off = row * 64 + ((chunk ^ swz_k(row)) << 4);
+    const int off = row * (BK * 2) + ((chunk ^ swz_k(row)) << 4);
     return *reinterpret_cast<const bf16x8 *>(base + off);
 }
 
-template <int MODE, int BM, int BN, int STAGES, bool UNIT>
+template <int MODE, int BM, int BN, int WR, int WC, int STAGES>
 struct Cfg {
-    static constexpr int BK = 32;
+    static constexpr int NW = WR * WC, NT = NW * 64;
     static constexpr bool A_KC = MODE != kWgrad;
     static constexpr bool B_KC = MODE != kWgrad;   // DGRAD reads W transposed to [C][R][S][K]
     static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
     static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
     static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;
-    static constexpr int NIA = A_BYTES / 1024 / 4;   // load instructions per wave per tile
-    static constexpr int NIB = B_BYTES / 1024 / 4;
-    static constexpr int WM = BM / 2, WN = BN / 2;
+    static constexpr int NIA = A_BYTES / 1024 / NW;   // load instructions per wave per tile
+    static constexpr int NIB = B_BYTES / 1024 / NW;
+    static constexpr int WM = BM / WR, WN = BN / WC;
     static constexpr int TM = WM / 32, TN = WN / 32;   // 32x32 MFMA tiles per wave
-    static constexpr int EPI_PITCH = WN + 8;         // bf16 elements per staged row
-    static constexpr int EPI_ROWS = 32;              // rows staged per pass
-    static_assert(NIA >= 1 && NIB >= 1, "tile too small");
-    static_assert(4 * EPI_ROWS * EPI_PITCH * 2 <= LDS_BYTES, "epilogue staging must fit in LDS");
-    static_assert(BM % 64 == 0 && BN % 64 == 0, "tile sizes");
+    static constexpr int NSUB = BK / 16;               // 16-k slices per step
+    static constexpr int EPI_PITCH = WN + 8;           // bf16 elements per staged row
+    static constexpr int EPI_ROWS = 32;                // rows staged per pass
+    static_assert(NIA >= 1 && NIB >= 1 && NIA * NW * 1024 == A_BYTES && NIB * NW * 1024 == B_BYTES, "load split");
+    static_assert(TM >= 1 && TN >= 1 && WM % 32 == 0 && WN % 32 == 0, "wave tile");
+    static_assert(NW * EPI_ROWS * EPI_PITCH * 2 <= LDS_BYTES, "epilogue staging must fit in LDS");
+    static_assert(LDS_BYTES <= 160 * 1024, "LDS");
 };
 
-template <int MODE, int BM, int BN, int STAGES, bool UNIT>
-__global__ __launch_bounds__(256, 1) void gemm_kernel(const Args P) {
-    using G = Cfg<MODE, BM, BN, STAGES, UNIT>;
-    constexpr int BK = G::BK, NIA = G::NIA, NIB = G::NIB, TM = G::TM, TN = G::TN;
+template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int OCC, bool UNIT>
+__global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
+    using G = Cfg<MODE, BM, BN, WR, WC, STAGES>;
+    constexpr int NIA = G::NIA, NIB = G::NIB, TM = G::TM, TN = G::TN, NSUB = G::NSUB;
     __shared__ __attribute__((aligned(1024))) char smem[G::LDS_BYTES];
 
     const ConvGeom &g = P.g;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm0 = (wave >> 1) * G::WM, wn0 = (wave & 1) * G::WN;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform: LDS bases stay scalar
+    const int wm0 = (wave / WC) * G::WM, wn0 = (wave % WC) * G::WN;
 
     int M = P.M, Kg = P.K, ntm = P.ntm;
     Phase f{};
@@ -190,7 +203,7 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const Args P) {
         tm = first + r % gsz;
         tn = r / gsz;
     }
-    if (tm >= ntm || tn >= P.ntn) return;
+    if (tm >= ntm || tn >= P.ntn) return;   // before any load: nothing in flight
     const int m0 = tm * BM, n0 = tn * BN;
     const int nk = k_end > k_begin ? (k_end - k_begin + BK - 1) / BK : 0;
 
@@ -198,15 +211,15 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const Args P) {
     const __amdgpu_buffer_rsrc_t rb = rsrc(P.b, P.b_bytes);
 
     // ------------------------------------------------ per-lane load state
-    // K-contiguous operand: instruction j of this wave covers rows
-    // (wave*NI + j)*16 + lane/4, chunk slot lane%4 holding k chunk kc.
-    const int kc_row = lane >> 2;                       // row within a 16-row group
-    const int kc = (lane & 3) ^ swz_k(kc_row);          // k chunk this lane fetches
-    // A state
+    // K-contiguous operand: instruction j of this wave covers tile rows
+    // (wave*NI + j)*8 + lane/8; the lane's 16-byte slot lane%8 holds k chunk
+    // (lane%8) ^ swz_k(row), which is c0 or c0 ^ 1 by the parity of the
+    // instruction's row group.
+    const int kc_row = lane >> 3;
+    const int kc0 = (lane & 7) ^ kc_row;
     int a_base[NIA], a_y[NIA], a_x[NIA];
-    uint32_t a_mn_off[NIA];                             // MN-contiguous A: element offset along m
+    uint32_t a_mn_off[NIA];
     bool a_ok[NIA];
-    // B state
     int b_base[NIB];
     bool b_ok[NIB];
     uint32_t b_mn_off[NIB];
@@ -215,7 +228,7 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const Args P) {
     if constexpr (G::A_KC) {
 #pragma unroll
         for (int j = 0; j < NIA; ++j) {
-            const int row = (wave * NIA + j) * 16 + kc_row;
+            const int row = (wave * NIA + j) * 8 + kc_row;
             const int m = m0 + row;
             a_ok[j] = m < M;
             const int mm = a_ok[j] ? m : 0;
@@ -253,7 +266,7 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const Args P) {
     if constexpr (G::B_KC) {
 #pragma unroll
         for (int j = 0; j < NIB; ++j) {
-            const int row = (wave * NIB + j) * 16 + kc_row;
+            const int row = (wave * NIB + j) * 8 + kc_row;
             const int n = n0 + row;
             b_ok[j] = n < N;
             // FWD: W[n][(r,s,c)] (row length R*S*C); DGRAD: Wt[c][(r,s,k)] (R*S*K)
@@ -286,40 +299,47 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const Args P) {
         char *sB = sA + G::A_BYTES;
         // ---- A
         if constexpr (G::A_KC) {
-            const int kk = k0 + kc * 8;
-            const bool kin = kk < k_end;
-            int dr = 0, ds = 0, off_k = kk;
-            if constexpr (!UNIT) {
-                if constexpr (MODE == kFwd) {
-                    const int rs = kk / g.C;
-                    off_k = kk - rs * g.C;
-                    dr = rs / g.S;
-                    ds = rs - dr * g.S;
-                } else {
-                    const int t = kk / g.K;
-                    off_k = kk - t * g.K;
-                    const int tr = f.Sp > 0 ? t / f.Sp : 0;
-                    dr = -tr;
-                    ds = -(t - tr * f.Sp);
+            // the two chunk variants of this lane: (tap, channel offset) of each
+            int dr[2] = {0, 0}, ds[2] = {0, 0}, off_k[2];
+            bool kin[2];
+#pragma unroll
+            for (int v = 0; v < 2; ++v) {
+                const int kk = k0 + (kc0 ^ v) * 8;
+                kin[v] = kk < k_end;
+                off_k[v] = kk;
+                if constexpr (!UNIT) {
+                    if constexpr (MODE == kFwd) {
+                        const int rs = kk / g.C;
+                        off_k[v] = kk - rs * g.C;
+                        dr[v] = rs / g.S;
+                        ds[v] = rs - dr[v] * g.S;
+                    } else {
+                        const int t = kk / g.K;
+                        off_k[v] = kk - t * g.K;
+                        const int tr = f.Sp > 0 ? t / f.Sp : 0;
+                        dr[v] = -tr;
+                        ds[v] = -(t - tr * f.Sp);
+                    }
                 }
             }
 #pragma unroll
             for (int j = 0; j < NIA; ++j) {
-                bool ok = kin && a_ok[j];
+                const int v = (wave * NIA + j) & 1;
+                bool ok = kin[v] && a_ok[j];
                 int off;
                 if constexpr (UNIT) {
-                    off = a_base[j] + kk;
+                    off = a_base[j] + off_k[v];
                 } else if constexpr (MODE == kFwd) {
-                    const int ih = a_y[j] + dr, iw = a_x[j] + ds;
+                    const int ih = a_y[j] + dr[v], iw = a_x[j] + ds[v];
                     ok = ok && (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
-                    off = a_base[j] + (ih * g.W + iw) * g.C + off_k;
+                    off = a_base[j] + (ih * g.W + iw) * g.C + off_k[v];
                 } else {
-                    const int p = a_y[j] + dr, q = a_x[j] + ds;
+                    const int p = a_y[j] + dr[v], q = a_x[j] + ds[v];
                     ok = ok && (unsigned)p < (unsigned)g.P && (unsigned)q < (unsigned)g.Q;
-                    off = a_base[j] + (p * g.Q + q) * g.K + off_k;
+                    off = a_base[j] + (p * g.Q + q) * g.K + off_k[v];
                 }
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    ra, (lds_void_t *)(sA + (wave * NIA + j) * 1024), 16, ok ? (uint32_t)off * 2u : kOOB, 0, 0, 0);
+                const uint32_t boff = ok ? (uint32_t)off * 2u : kOOB;
+                dma16(ra, sA + (wave * NIA + j) * 1024, boff);
             }
         } else {
             constexpr int SPR = BM / 8, KPI = 64 / SPR;
@@ -327,28 +347,32 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const Args P) {
             for (int j = 0; j < NIA; ++j) {
                 const int kk = k0 + (wave * NIA + j) * KPI + lane / SPR;
                 const bool ok = a_ok[j] && kk < k_end;
-                const uint32_t off = (uint32_t)kk * (uint32_t)g.K + a_mn_off[j];
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    ra, (lds_void_t *)(sA + (wave * NIA + j) * 1024), 16, ok ? off * 2u : kOOB, 0, 0, 0);
+                const uint32_t boff = ok ? ((uint32_t)kk * (uint32_t)g.K + a_mn_off[j]) * 2u : kOOB;
+                dma16(ra, sA + (wave * NIA + j) * 1024, boff);
             }
         }
         // ---- B
         if constexpr (G::B_KC) {
-            const int kk = k0 + kc * 8;
-            const bool kin = kk < k_end;
-            int off_k = kk;
-            if constexpr (MODE == kDgrad && !UNIT) {
-                // kk = (t_r, t_s, k) of this phase -> tap (r, s) of Wt[c][r][s][k]
-                const int t = kk / g.K, k = kk - t * g.K;
-                const int tr = f.Sp > 0 ? t / f.Sp : 0, ts = t - tr * f.Sp;
-                off_k = ((f.fh + tr * g.sh) * g.S + f.fw + ts * g.sw) * g.K + k;
+            int off_k[2];
+            bool kin[2];
+#pragma unroll
+            for (int v = 0; v < 2; ++v) {
+                const int kk = k0 + (kc0 ^ v) * 8;
+                kin[v] = kk < k_end;
+                off_k[v] = kk;
+                if constexpr (MODE == kDgrad && !UNIT) {
+                    // kk = (t_r, t_s, k) of this phase -> tap (r, s) of Wt[c][r][s][k]
+                    const int t = kk / g.K, k = kk - t * g.K;
+                    const int tr = f.Sp > 0 ? t / f.Sp : 0, ts = t - tr * f.Sp;
+                    off_k[v] = ((f.fh + tr * g.sh) * g.S + f.fw + ts * g.sw) * g.K + k;
+                }
             }
 #pragma unroll
             for (int j = 0; j < NIB; ++j) {
-                const bool ok = kin && b_ok[j];
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    rb, (lds_void_t *)(sB + (wave * NIB + j) * 1024), 16,
-                    ok ? (uint32_t)(b_base[j] + off_k) * 2u : kOOB, 0, 0, 0);
+                const int v = (wave * NIB + j) & 1;
+                const bool ok = kin[v] && b_ok[j];
+                const uint32_t boff = ok ? (uint32_t)(b_base[j] + off_k[v]) * 2u : kOOB;
+                dma16(rb, sB + (wave * NIB + j) * 1024, boff);
             }
         } else {
             constexpr int SPR = BN / 8, KPI = 64 / SPR;
@@ -357,21 +381,19 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const Args P) {
                 const int kk = k0 + (wave * NIB + j) * KPI + lane / SPR;
                 bool ok = b_ok[j] && kk < k_end;
                 uint32_t off = 0;
-                {
-                    // WGRAD: x im2col, k-row = (n,p,q), slot along (r,s,c)
-                    if constexpr (UNIT) {
-                        off = (uint32_t)kk * (uint32_t)g.C + b_mn_off[j];
-                    } else {
-                        const int PQ = g.P * g.Q;
-                        const int n = kk / PQ, pq = kk - n * PQ;
-                        const int p = pq / g.Q, q = pq - p * g.Q;
-                        const int ih = p * g.sh - g.ph + b_r[j], iw = q * g.sw - g.pw + b_s[j];
-                        ok = ok && (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
-                        off = (uint32_t)(((n * g.H + ih) * g.W + iw) * g.C) + b_mn_off[j];
-                    }
+                // WGRAD: x im2col, k-row = (n,p,q), slot along (r,s,c)
+                if constexpr (UNIT) {
+                    off = (uint32_t)kk * (uint32_t)g.C + b_mn_off[j];
+                } else {
+                    const int PQ = g.P * g.Q;
+                    const int n = kk / PQ, pq = kk - n * PQ;
+                    const int p = pq / g.Q, q = pq - p * g.Q;
+                    const int ih = p * g.sh - g.ph + b_r[j], iw = q * g.sw - g.pw + b_s[j];
+                    ok = ok && (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
+                    off = (uint32_t)(((n * g.H + ih) * g.W + iw) * g.C) + b_mn_off[j];
                 }
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    rb, (lds_void_t *)(sB + (wave * NIB + j) * 1024), 16, ok ? off * 2u : kOOB, 0, 0, 0);
+                const uint32_t boff = ok ? off * 2u : kOOB;
+                dma16(rb, sB + (wave * NIB + j) * 1024, boff);
             }
         }
     };
@@ -391,102 +413,99 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const Args P) {
 #pragma unroll
     for (int i = 0; i < TM; ++i) dbacc[i] = 0.f;
 
-    // ------------------------------------------------ main loop (software pipelined)
-    // The prologue fills all STAGES stages.  Step kt holds the fragments of
-    // tile kt in registers (cur); it waits for tile kt+1, refills the stage
-    // tile kt came from with tile kt+STAGES, and reads tile kt+1's fragments
-    // (nxt) from LDS while the MFMAs of tile kt run, so LDS latency and the
-    // DMA issue overlap the matrix work.
-    // fragments of one BK = 32 tile: [sub][i] with sub = k half (16 each)
-    auto read_frags = [&](int stage, bf16x8 *af, bf16x8 *bfr) {
+    // fragments of one 16-k slice of the tile in `stage`
+    auto read_sub = [&](int stage, int sub, bf16x8 *af, bf16x8 *bfr) {
         const char *sA = smem + stage * G::STAGE_BYTES;
         const char *sB = sA + G::A_BYTES;
 #pragma unroll
-        for (int sub = 0; sub < 2; ++sub) {
+        for (int i = 0; i < TM; ++i) {
+            if constexpr (G::A_KC) af[i] = frag_kc(sA, wm0 + i * 32 + fr, sub, lane);
+            else af[i] = frag_mn<BM>(sA, wm0 + i * 32, sub, lane);
+        }
 #pragma unroll
-            for (int i = 0; i < TM; ++i) {
-                if constexpr (G::A_KC) af[sub * TM + i] = frag_kc(sA, wm0 + i * 32 + fr, sub, lane);
-                else af[sub * TM + i] = frag_mn<BM>(sA, wm0 + i * 32, sub, lane);
-            }
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                if constexpr (G::B_KC) bfr[sub * TN + j] = frag_kc(sB, wn0 + j * 32 + fr, sub, lane);
-                else bfr[sub * TN + j] = frag_mn<BN>(sB, wn0 + j * 32, sub, lane);
-            }
+        for (int j = 0; j < TN; ++j) {
+            if constexpr (G::B_KC) bfr[j] = frag_kc(sB, wn0 + j * 32 + fr, sub, lane);
+            else bfr[j] = frag_mn<BN>(sB, wn0 + j * 32, sub, lane);
         }
     };
-    // One pipelined step: tiles kt+1 .. kt+STAGES-1 are in flight or landed.
-    // The refill of the stage tile kt came from is issued unconditionally
-    // (past the end of the reduction its loads take the out-of-range path and
-    // write zeros into a stage that is never read), so every step has the
-    // same instruction stream: wait for tile kt+1 (at most STAGES-2 tiles
-    // still in flight), barrier, refill, read tile kt+1's fragments (nxt) and
-    // run tile kt's MFMAs (cur); the scheduler interleaves the loads and LDS
-    // reads between the MFMAs so the matrix pipe never waits for them.
-    constexpr int NMFMA = 2 * TM * TN;
-#ifndef MS_GEMM_INTERLEAVE
-#define MS_GEMM_INTERLEAVE 1
-#endif
-    constexpr bool INTERLEAVE = MS_GEMM_INTERLEAVE;
-    constexpr int NVMEM = NIA + NIB;
-    constexpr int NDS = 2 * ((G::A_KC ? 1 : 2) * TM + (G::B_KC ? 1 : 2) * TN);
-    auto mfmas = [&](const bf16x8 *ca, const bf16x8 *cb) {
+    auto mfma_sub = [&](const bf16x8 *ca, const bf16x8 *cb) {
         if (db_on) {
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
                 float sum = 0.f;
 #pragma unroll
-                for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) sum += (float)ca[sub * TM + i][e];
+                for (int e = 0; e < 8; ++e) sum += (float)ca[i][e];
                 dbacc[i] += sum;
             }
         }
 #pragma unroll
-        for (int sub = 0; sub < 2; ++sub)
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cb[sub * TN + j], ca[sub * TM + i],
-                                                                        acc[i][j], 0, 0, 0);
+            for (int j = 0; j < TN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cb[j], ca[i], acc[i][j], 0, 0, 0);
     };
-    auto step = [&](const bf16x8 *ca, const bf16x8 *cb, bf16x8 *na, bf16x8 *nb2, int kt) {
-        wait_vmcnt<(STAGES - 2) * NVMEM>();
-        __builtin_amdgcn_s_waitcnt(0xc07f);   // this wave's reads of tile kt are complete
-        __builtin_amdgcn_s_barrier();
-        issue(kt % STAGES, k_begin + (kt + STAGES) * BK);
-        read_frags((kt + 1) % STAGES, na, nb2);
-        mfmas(ca, cb);
-        // interleave: every MFMA is followed by its share of loads / LDS reads
+    constexpr int NVMEM = NIA + NIB;
+    constexpr int NMF = TM * TN;
+    constexpr int NDS = (G::A_KC ? 1 : 2) * TM + (G::B_KC ? 1 : 2) * TN;
+    // every MFMA is followed by its share of the DMA issues and LDS reads
+    auto interleave = [&](int nvmem) {
 #pragma unroll
-        for (int m = 0; m < (INTERLEAVE ? NMFMA : 0); ++m) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // 1 MFMA
-            if (m < NVMEM) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // 1 VMEM load
-            constexpr int DPM = (NDS + NMFMA - 1) / NMFMA;
-            if (m * DPM < NDS) __builtin_amdgcn_sched_group_barrier(0x100, DPM, 0);   // LDS reads
+        for (int m = 0; m < NMF; ++m) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            constexpr int VPM = (NVMEM + NMF - 1) / NMF;
+            if (m * VPM < nvmem) __builtin_amdgcn_sched_group_barrier(0x020, VPM, 0);
+            constexpr int DPM = (NDS + NMF - 1) / NMF;
+            if (m * DPM < NDS) __builtin_amdgcn_sched_group_barrier(0x100, DPM, 0);
         }
     };
 
+    // ------------------------------------------------ main loop
+    // Stage s = kt % STAGES holds tile kt.  On entry to step kt the fragments
+    // of its first slice are in (fa0, fb0).  Each slice reads the next
+    // slice's fragments while its MFMAs run; the last slice first makes sure
+    // every wave has read tile kt (own LDS reads done, barrier) and tile kt+1
+    // has landed (own DMA done, same barrier), then refills stage s with tile
+    // kt + STAGES and reads tile kt+1's first slice.  Refills past the end of
+    // the reduction take the out-of-range path and write zeros into a stage
+    // that only feeds MFMAs nobody keeps.
+    bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN];
+    auto step = [&](int kt) {
+        const int s = kt % STAGES;
 #pragma unroll
-    for (int s = 0; s < STAGES; ++s) issue(s, k_begin + s * BK);
-    bf16x8 fa0[2 * TM], fb0[2 * TN], fa1[2 * TM], fb1[2 * TN];
-    if (nk > 0) {
-        wait_vmcnt<(STAGES - 1) * NVMEM>();
-        __builtin_amdgcn_s_barrier();
-        read_frags(0, fa0, fb0);
-    }
-    int kt = 0;
-    for (; kt + 2 < nk; kt += 2) {
-        step(fa0, fb0, fa1, fb1, kt);
-        step(fa1, fb1, fa0, fb0, kt + 1);
-    }
-    if (kt + 1 < nk) {
-        step(fa0, fb0, fa1, fb1, kt);
-        mfmas(fa1, fb1);
-    } else if (kt < nk) {
-        mfmas(fa0, fb0);
-    }
+        for (int sub = 0; sub < NSUB; ++sub) {
+            const bf16x8 *ca = (sub & 1) ? fa1 : fa0;
+            const bf16x8 *cb = (sub & 1) ? fb1 : fb0;
+            bf16x8 *na = (sub & 1) ? fa0 : fa1;
+            bf16x8 *nb = (sub & 1) ? fb0 : fb1;
+            __builtin_amdgcn_sched_barrier(0);
+            if (sub + 1 < NSUB) {
+                read_sub(s, sub + 1, na, nb);
+                mfma_sub(ca, cb);
+                interleave(0);
+            } else {
+                wait_vmcnt<(STAGES - 2) * NVMEM>();
+                wait_lgkm0();
+                __builtin_amdgcn_s_barrier();
+                __builtin_amdgcn_sched_barrier(0);
+                issue(s, k_begin + (kt + STAGES) * BK);
+                read_sub((kt + 1) % STAGES, 0, na, nb);
+                mfma_sub(ca, cb);
+                interleave(NVMEM);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    static_assert(NSUB % 2 == 0, "an even number of slices keeps the fragment buffers' roles fixed");
+
+#pragma unroll
+    for (int s2 = 0; s2 < STAGES; ++s2) issue(s2, k_begin + s2 * BK);
+    wait_vmcnt<(STAGES - 1) * NVMEM>();
+    __builtin_amdgcn_s_barrier();
+    read_sub(0, 0, fa0, fb0);
+    for (int kt = 0; kt < nk; ++kt) step(kt);
+    // the refills of the last steps are still writing into LDS: drain them
+    // before LDS is reused or the workgroup ends
+    wait_vmcnt<0>();
 
     // ------------------------------------------------ fused bias-gradient partials
     if (db_on) {
@@ -543,7 +562,7 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const Args P) {
                 for (int v = 0; v < 4; ++v) o[v] = (bf16)acc[i][j][4 * q + v];
                 *reinterpret_cast<bf16x4 *>(stage + fr * G::EPI_PITCH + j * 32 + 8 * q + 4 * fh) = o;
             }
-        __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): this wave's staged rows are written
+        wait_lgkm0();   // this wave's staged rows are written
         __builtin_amdgcn_wave_barrier();
 #pragma unroll
         for (int r0 = 0; r0 < G::EPI_ROWS; r0 += ROWS_PER_PASS) {
@@ -577,7 +596,7 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const Args P) {
                 for (int e = 0; e < 8 && n + e < N; ++e) dst[e] = v.e[e];
             }
         }
-        __builtin_amdgcn_s_waitcnt(0xc07f);   // reads done before the next pass overwrites
+        wait_lgkm0();   // reads done before the next pass overwrites
         __builtin_amdgcn_wave_barrier();
     }
 }
@@ -643,7 +662,11 @@ struct Tile {
     int bm, bn, per_cu;   // tile shape, blocks resident per CU
     float eff;            // relative MFMA efficiency of the shape
 };
-constexpr Tile kTiles[] = {{256, 128, 1, 1.05f}, {128, 128, 2, 1.00f}, {128, 64, 3, 0.75f}};
+// 256x256: 8 waves (2 x 4) of 128 x 64, 2 stages (128 KB LDS);
+// 256x128: 8 waves (2 x 4) of 128 x 32, 3 stages (144 KB);
+// 128x128: 4 waves of 64 x 64, 2 stages (64 KB, two blocks per CU);
+// 128x64:  4 waves of 64 x 32, 2 stages (48 KB, three blocks per CU).
+constexpr Tile kTiles[] = {{256, 256, 1, 1.20f}, {256, 128, 1, 1.00f}, {128, 128, 2, 1.00f}, {128, 64, 3, 0.75f}};
 
 // MEMSAVE_GEMM_TILE=<bm>x<bn> forces one tile shape (a debugging and
 // testing knob); returns its index or -1.
@@ -658,8 +681,7 @@ int forced_tile() {
 }
 
 // Pick the tile that minimises (waves of blocks) x (time per wave).
-// `first` skips the largest shapes (the weight gradient keeps more live
-// registers and would spill with the 256 x 256 tile).
+// `first` skips the largest shapes.
 Tile pick(long M, long N, long K, int splits_allowed, int *splits_out, int z = 1, int first = 0) {
     double best = 1e300;
     Tile bt = kTiles[first];
@@ -691,11 +713,11 @@ Tile pick(long M, long N, long K, int splits_allowed, int *splits_out, int z = 1
     return bt;
 }
 
-template <int MODE, int BM, int BN, bool UNIT>
+template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int OCC, bool UNIT>
 int go(const Args &a, dim3 grid, hipStream_t st) {
     const unsigned pk = MODE == kFwd ? kProfFwd : MODE == kDgrad ? kProfDgrad : kProfWgrad;
     prof_mark(pk, st, true);
-    hipLaunchKernelGGL((gemm_kernel<MODE, BM, BN, 4, UNIT>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((gemm_kernel<MODE, BM, BN, WR, WC, STAGES, OCC, UNIT>), grid, dim3(WR * WC * 64), 0, st, a);
     const int err = (int)hipGetLastError();
     prof_mark(pk, st, false);
     return err;
@@ -703,9 +725,10 @@ int go(const Args &a, dim3 grid, hipStream_t st) {
 
 template <int MODE, bool UNIT>
 int go_tile(const Tile &t, const Args &a, dim3 grid, hipStream_t st) {
-    if (t.bm == 256 && t.bn == 128) return go<MODE, 256, 128, UNIT>(a, grid, st);
-    if (t.bm == 128 && t.bn == 128) return go<MODE, 128, 128, UNIT>(a, grid, st);
-    return go<MODE, 128, 64, UNIT>(a, grid, st);
+    if (t.bm == 256 && t.bn == 256) return go<MODE, 256, 256, 2, 4, 2, 1, UNIT>(a, grid, st);
+    if (t.bm == 256 && t.bn == 128) return go<MODE, 256, 128, 2, 4, 3, 1, UNIT>(a, grid, st);
+    if (t.bm == 128 && t.bn == 128) return go<MODE, 128, 128, 2, 2, 2, 2, UNIT>(a, grid, st);
+    return go<MODE, 128, 64, 2, 2, 2, 3, UNIT>(a, grid, st);
 }
 
 template <int MODE>
@@ -729,11 +752,11 @@ struct WgradPlan {
 WgradPlan wgrad_plan(const ConvGeom &g) {
     const long M = g.K, N = (long)g.R * g.S * g.C, K = (long)g.N * g.P * g.Q;
     int splits = 1;
-    const int max_splits = (int)std::max<long>(1, K / 256);   // at least 8 BK steps per split
+    const int max_splits = (int)std::max<long>(1, K / (8 * BK));   // at least 8 BK steps per split
     Tile t = pick(M, N, K, max_splits, &splits, 1, 0);
     int k_split = (int)((K + splits - 1) / splits);
-    k_split = (k_split + 31) / 32 * 32;
-    if (K == 0) k_split = 32;
+    k_split = (k_split + BK - 1) / BK * BK;
+    if (K == 0) k_split = BK;
     splits = K > 0 ? (int)((K + k_split - 1) / k_split) : 1;
     return {t, splits, k_split};
 }

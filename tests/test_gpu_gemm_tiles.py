@@ -14,7 +14,7 @@ from _gpu import check, dev, host
 
 pytestmark = pytest.mark.gpu
 
-TILES = ["256x128", "128x128", "128x64"]
+TILES = ["256x256", "256x128", "128x128", "128x64"]
 
 CASES = [
     # x shape, w shape, stride, pad
@@ -22,6 +22,7 @@ CASES = [
     ((2, 16, 15, 14), (24, 16, 3, 3), (2, 2), (1, 1)),
     ((2, 64, 9, 10), (136, 64, 1, 1), (1, 1), (0, 0)),
     ((1, 48, 12, 9), (72, 48, 5, 3), (3, 2), (2, 1)),
+    ((2, 80, 20, 18), (264, 80, 3, 3), (1, 1), (1, 1)),   # several 256-wide tiles, ragged in M, N and k
 ]
 
 
