@@ -42,7 +42,10 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
 
-enum Mode { kFwd = 0, kDgrad = 1, kWgrad = 2 };
+// kDgrad reads the filter from a transposed copy Wt[C][R][S][K] (both
+// operands K-contiguous); kDgradN reads W[K][R][S][C] in place as an
+// M/N-contiguous operand (no copy, transposing LDS reads).
+enum Mode { kFwd = 0, kDgrad = 1, kWgrad = 2, kDgradN = 3 };
 
 constexpr uint32_t kOOB = 0xFFFFFFF0u;   // byte offset beyond any buffer: loads return 0
 constexpr int BK = 64;                   // reduction step (elements)
@@ -150,7 +153,7 @@ template <int MODE, int BM, int BN, int WR, int WC, int STAGES>
 struct Cfg {
     static constexpr int NW = WR * WC, NT = NW * 64;
     static constexpr bool A_KC = MODE != kWgrad;
-    static constexpr bool B_KC = MODE != kWgrad;   // DGRAD reads W transposed to [C][R][S][K]
+    static constexpr bool B_KC = MODE == kFwd || MODE == kDgrad;   // kDgrad: W transposed to [C][R][S][K]
     static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
     static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
     static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;
@@ -171,6 +174,7 @@ template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int OCC, bool UN
 __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
     using G = Cfg<MODE, BM, BN, WR, WC, STAGES>;
     constexpr int NIA = G::NIA, NIB = G::NIB, TM = G::TM, TN = G::TN, NSUB = G::NSUB;
+    constexpr bool DG = MODE == kDgrad || MODE == kDgradN;
     __shared__ __attribute__((aligned(1024))) char smem[G::LDS_BYTES];
 
     const ConvGeom &g = P.g;
@@ -180,7 +184,7 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
 
     int M = P.M, Kg = P.K, ntm = P.ntm;
     Phase f{};
-    if constexpr (MODE == kDgrad) {
+    if constexpr (DG) {
         f = make_phase(g, blockIdx.z);
         M = g.N * f.Hp * f.Wp;
         Kg = f.Rp * f.Sp * g.K;
@@ -381,8 +385,17 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
                 const int kk = k0 + (wave * NIB + j) * KPI + lane / SPR;
                 bool ok = b_ok[j] && kk < k_end;
                 uint32_t off = 0;
-                // WGRAD: x im2col, k-row = (n,p,q), slot along (r,s,c)
-                if constexpr (UNIT) {
+                if constexpr (MODE == kDgradN) {
+                    // W in place: k-row kk = (t_r, t_s, k) of this phase, slots along c
+                    if constexpr (UNIT) {
+                        off = (uint32_t)kk * (uint32_t)g.C + b_mn_off[j];
+                    } else {
+                        const int t = kk / g.K, k = kk - t * g.K;
+                        const int tr = f.Sp > 0 ? t / f.Sp : 0, ts = t - tr * f.Sp;
+                        off = (uint32_t)(((k * g.R + f.fh + tr * g.sh) * g.S + f.fw + ts * g.sw) * g.C) + b_mn_off[j];
+                    }
+                } else if constexpr (UNIT) {
+                    // WGRAD: x im2col, k-row = (n,p,q), slot along (r,s,c)
                     off = (uint32_t)kk * (uint32_t)g.C + b_mn_off[j];
                 } else {
                     const int PQ = g.P * g.Q;
@@ -581,7 +594,7 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
                 }
             }
             bf16 *dst;
-            if constexpr (MODE == kDgrad && !UNIT) {
+            if constexpr (DG && !UNIT) {
                 const int HW = f.Hp * f.Wp;
                 const int nimg = m / HW, ij = m - nimg * HW;
                 const int i2 = ij / f.Wp, j2 = ij - i2 * f.Wp;
@@ -602,23 +615,49 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
 }
 
 // Wt[c][rs][k] = W[k][rs][c]: the input gradient reads the (frozen) filter
-// with its reduction index k contiguous.  64 x 64 tiles through LDS, both
-// sides coalesced; grid (C/64, K/64, R*S).
+// with its reduction index k contiguous.  A block moves a 64 (k) x 64 (c)
+// tile of one tap rs through LDS; global reads and writes are 16-byte
+// vectors that cover whole 128-byte rows.  Grid (ceil(C/64), ceil(K/64), R*S).
 __global__ __launch_bounds__(256) void transpose_krsc_kernel(const bf16 *__restrict__ W, bf16 *__restrict__ Wt,
                                                              int K, int RS, int C) {
-    __shared__ bf16 t[64][66];
+    constexpr int PITCH = 64 + 2;   // odd word pitch: the column reads below hit distinct banks
+    __shared__ bf16 t[64 * PITCH];
     const int c0 = blockIdx.x * 64, k0 = blockIdx.y * 64, rs = blockIdx.z;
-    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-#pragma unroll 4
-    for (int i = ty; i < 64; i += 4) {
-        const int k = k0 + i, c = c0 + tx;
-        if (k < K && c < C) t[i][tx] = W[((size_t)k * RS + rs) * C + c];
+    const int tid = threadIdx.x;
+    const bool full = c0 + 64 <= C && k0 + 64 <= K && (C % 8) == 0 && (K % 8) == 0;
+    // read: thread -> (row k = tid/8 + 32 p, 8-column chunk tid%8)
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+        const int kl = tid / 8 + 32 * p, cl = (tid % 8) * 8;
+        const int k = k0 + kl;
+        const bf16 *src = W + ((size_t)k * RS + rs) * C + c0 + cl;
+        if (full) {
+            const Vec16<bf16> v = load16(src);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) t[kl * PITCH + cl + e] = v.e[e];
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                t[kl * PITCH + cl + e] = (k < K && c0 + cl + e < C) ? src[e] : (bf16)0.f;
+        }
     }
     __syncthreads();
-#pragma unroll 4
-    for (int i = ty; i < 64; i += 4) {
-        const int c = c0 + i, k = k0 + tx;
-        if (k < K && c < C) Wt[((size_t)c * RS + rs) * K + k] = t[tx][i];
+    // write: thread -> (row c = tid/8 + 32 p, 8-k chunk tid%8)
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+        const int cl = tid / 8 + 32 * p, kl = (tid % 8) * 8;
+        const int c = c0 + cl;
+        Vec16<bf16> v;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v.e[e] = t[(kl + e) * PITCH + cl];
+        bf16 *dst = Wt + ((size_t)c * RS + rs) * K + k0 + kl;
+        if (full) {
+            store16(dst, v);
+        } else if (c < C) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (k0 + kl + e < K) dst[e] = v.e[e];
+        }
     }
 }
 
@@ -715,7 +754,7 @@ Tile pick(long M, long N, long K, int splits_allowed, int *splits_out, int z = 1
 
 template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int OCC, bool UNIT>
 int go(const Args &a, dim3 grid, hipStream_t st) {
-    const unsigned pk = MODE == kFwd ? kProfFwd : MODE == kDgrad ? kProfDgrad : kProfWgrad;
+    const unsigned pk = MODE == kFwd ? kProfFwd : MODE == kWgrad ? kProfWgrad : kProfDgrad;
     prof_mark(pk, st, true);
     hipLaunchKernelGGL((gemm_kernel<MODE, BM, BN, WR, WC, STAGES, OCC, UNIT>), grid, dim3(WR * WC * 64), 0, st, a);
     const int err = (int)hipGetLastError();
@@ -778,29 +817,44 @@ int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, 
     return go_mode<kFwd>(t, a, dim3(a.ntm * a.ntn, 1, 1), unit_geom(g), st);
 }
 
+// Input gradient through a transposed copy of W (both operands K-contiguous,
+// the faster contraction) or straight from W (no copy, no extra kernel).
+// MEMSAVE_DGRAD=transposed|direct overrides the choice (testing knob).
+bool dgrad_direct(const ConvGeom &g) {
+    const char *e = getenv("MEMSAVE_DGRAD");
+    if (e && *e) return e[0] == 'd';
+    (void)g;
+    return false;
+}
+
 size_t dgrad_workspace(const ConvGeom &g) {
-    if (g.C % 8 != 0 || g.K % 8 != 0) return 0;
+    if (g.C % 8 != 0 || g.K % 8 != 0 || dgrad_direct(g)) return 0;
     return (size_t)g.K * g.R * g.S * g.C * sizeof(bf16) + 256;
 }
 
 int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, void *ws, hipStream_t st) {
-    if (g.C % 8 != 0 || g.K % 8 != 0 || !ws || !al16(dy) || !al16(w) || !al16(dx) || !al16(ws)) return -1;
+    if (g.C % 8 != 0 || g.K % 8 != 0 || !al16(dy) || !al16(w) || !al16(dx)) return -1;
+    const bool direct = dgrad_direct(g);
+    if (!direct && (!ws || !al16(ws))) return -1;
     Args a{};
-    a.a = (const bf16 *)dy; a.b = (const bf16 *)ws; a.c = (bf16 *)dx; a.g = g;
+    a.a = (const bf16 *)dy; a.b = direct ? (const bf16 *)w : (const bf16 *)ws; a.c = (bf16 *)dx; a.g = g;
     const int Hb = (g.H + g.sh - 1) / g.sh, Wb = (g.W + g.sw - 1) / g.sw;
     a.M = g.N * Hb * Wb; a.N = g.C;
     a.K = ((g.R + g.sh - 1) / g.sh) * ((g.S + g.sw - 1) / g.sw) * g.K;
     if (a.M == 0 || a.N == 0) return 0;
-    hipLaunchKernelGGL(transpose_krsc_kernel, dim3((g.C + 63) / 64, (g.K + 63) / 64, g.R * g.S), dim3(256), 0, st,
-                       (const bf16 *)w, (bf16 *)ws, g.K, g.R * g.S, g.C);
-    int err = (int)hipGetLastError();
-    if (err) return err;
+    if (!direct) {
+        hipLaunchKernelGGL(transpose_krsc_kernel, dim3((g.C + 63) / 64, (g.K + 63) / 64, g.R * g.S), dim3(256), 0, st,
+                           (const bf16 *)w, (bf16 *)ws, g.K, g.R * g.S, g.C);
+        const int err = (int)hipGetLastError();
+        if (err) return err;
+    }
     Tile t = pick(a.M, a.N, a.K, 1, nullptr, g.sh * g.sw);
     a.ntm = (a.M + t.bm - 1) / t.bm; a.ntn = (a.N + t.bn - 1) / t.bn;
     a.splits = 1; a.k_split = a.K;
     a.a_bytes = bytes_of((long)g.N * g.P * g.Q * g.K);
     a.b_bytes = bytes_of((long)g.K * g.R * g.S * g.C);
-    return go_mode<kDgrad>(t, a, dim3(a.ntm * a.ntn, 1, g.sh * g.sw), unit_geom(g), st);
+    const dim3 grid(a.ntm * a.ntn, 1, g.sh * g.sw);
+    return direct ? go_mode<kDgradN>(t, a, grid, unit_geom(g), st) : go_mode<kDgrad>(t, a, grid, unit_geom(g), st);
 }
 
 bool wgrad_applies(const ConvGeom &g) { return g.C % 8 == 0 && g.K % 8 == 0; }

@@ -9,10 +9,11 @@
 //   - bias gradient of conv / linear: column sums of dy;
 //   - global average pool and its adjoint.
 //
-// Thread map: a block is RG x TC threads; thread (rg, tc) owns the channel
-// vector tc of its block's column tile for the whole kernel and walks rows
-// rg, rg+RG, ... of its block's row chunk, so per-channel constants live in
-// registers and a wave reads whole contiguous rows (coalesced 16-byte loads).
+// Thread map of the reductions: a block is RG x TC threads; thread (rg, tc)
+// owns the channel vector tc of its block's column tile for the whole kernel
+// and walks rows rg, rg+RG, ... of its block's row chunk, so per-channel
+// constants live in registers and a wave reads whole contiguous rows
+// (coalesced 16-byte loads).  The BN-eval forward is a linear sweep (below).
 // Reductions: per-thread fp32 partials -> LDS reduction over RG -> one fp32
 // partial per (row chunk, channel) -> finalize kernel (deterministic order).
 #include <algorithm>
@@ -69,47 +70,54 @@ template <typename T> struct VecT<T, 16 / sizeof(T)> {
 }  // namespace
 
 // ---------------------------------------------------------------- BN-eval fwd
+// BN-eval forward as one linear sweep: x is viewed as nvec = rows*C/V
+// consecutive V-element vectors, and each thread handles U of them with all
+// U loads in flight at once (the grid covers the tensor in one pass).
+//  * contiguous mapping (256 % nvc == 0, nvc = vectors per row): block b
+//    owns vectors [b*256*U, (b+1)*256*U) and thread t handles
+//    b*256*U + u*256 + t, so a block streams one contiguous 256*U*16-byte
+//    range;
+//  * strided mapping (any nvc): thread i handles i + u*T (T = threads in the
+//    grid, a multiple of nvc).
+// Either way a thread's vectors all hold the same channels, so it folds
+// (s, t) for its V channels once.
+constexpr int kBnU = 8;
+
 template <typename T, int V>
-__global__ __launch_bounds__(256) void bn_fwd_kernel(const T *__restrict__ x, const T *__restrict__ mean,
-                                                     const T *__restrict__ var, const T *__restrict__ gamma,
-                                                     const T *__restrict__ beta, float eps, int64_t rows,
-                                                     int C, int TC, int RG, int64_t chunk,
-                                                     T *__restrict__ y) {
-    const int tc = threadIdx.x % TC, rg = threadIdx.x / TC;
-    if (rg >= RG) return;
-    const int cv = blockIdx.x * TC + tc;
-    if (cv * V >= C) return;
-    const int c0 = cv * V;
+__global__ __launch_bounds__(256) void bn_fwd_flat_kernel(const T *__restrict__ x, const T *__restrict__ mean,
+                                                          const T *__restrict__ var, const T *__restrict__ gamma,
+                                                          const T *__restrict__ beta, float eps, int64_t nvec,
+                                                          int nvc, bool contig, T *__restrict__ y) {
+    const int64_t stride = contig ? 256 : (int64_t)gridDim.x * blockDim.x;
+    const int64_t i0 = contig ? (int64_t)blockIdx.x * 256 * kBnU + threadIdx.x
+                              : (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int c0 = (int)(i0 % nvc) * V;
+    VecT<T, V> pm, pv, pg, pb;
+    pm.load(mean + c0);
+    pv.load(var + c0);
+    if (gamma) pg.load(gamma + c0);
+    if (beta) pb.load(beta + c0);
     float s[V], t[V];
 #pragma unroll
     for (int e = 0; e < V; ++e) {
-        const float g = gamma ? to_f32(gamma[c0 + e]) : 1.f;
-        const float b = beta ? to_f32(beta[c0 + e]) : 0.f;
-        const float inv = 1.f / sqrtf(to_f32(var[c0 + e]) + eps);
-        s[e] = g * inv;
-        t[e] = b - to_f32(mean[c0 + e]) * s[e];
+        const float g = gamma ? to_f32(pg.e[e]) : 1.f;
+        const float b = beta ? to_f32(pb.e[e]) : 0.f;
+        s[e] = g * rsqrtf(to_f32(pv.e[e]) + eps);
+        t[e] = b - to_f32(pm.e[e]) * s[e];
     }
-    const int64_t r0 = (int64_t)blockIdx.y * chunk;
-    const int64_t r1 = min(rows, r0 + chunk);
-    int64_t r = r0 + rg;
-    constexpr int U = 4;
-    for (; r + (U - 1) * RG < r1; r += U * RG) {
-        VecT<T, V> v[U];
+    for (int64_t i = i0; i < nvec; i += contig ? nvec : kBnU * stride) {
+        VecT<T, V> v[kBnU];
 #pragma unroll
-        for (int u = 0; u < U; ++u) v[u].load(x + (r + u * RG) * C + c0);
+        for (int u = 0; u < kBnU; ++u)
+            if (i + u * stride < nvec) v[u].load(x + (i + u * stride) * V);
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
+        for (int u = 0; u < kBnU; ++u) {
+            if (i + u * stride < nvec) {
 #pragma unroll
-            for (int e = 0; e < V; ++e) v[u].e[e] = from_f32<T>(fmaf(to_f32(v[u].e[e]), s[e], t[e]));
-            v[u].store(y + (r + u * RG) * C + c0);
+                for (int e = 0; e < V; ++e) v[u].e[e] = from_f32<T>(fmaf(to_f32(v[u].e[e]), s[e], t[e]));
+                v[u].store(y + (i + u * stride) * V);
+            }
         }
-    }
-    for (; r < r1; r += RG) {
-        VecT<T, V> v;
-        v.load(x + r * C + c0);
-#pragma unroll
-        for (int e = 0; e < V; ++e) v.e[e] = from_f32<T>(fmaf(to_f32(v.e[e]), s[e], t[e]));
-        v.store(y + r * C + c0);
     }
 }
 
@@ -301,18 +309,6 @@ __global__ __launch_bounds__(256) void avgpool_bwd_kernel(const T *__restrict__ 
 namespace {
 constexpr int kTargetBlocks = 1024;
 
-template <typename T, int V>
-int bn_fwd_t(const RowColPlan &p, const void *x, const void *mean, const void *var, const void *gamma,
-             const void *beta, float eps, int64_t rows, int C, void *y, hipStream_t st) {
-    prof_mark(kProfBn, st, true);
-    hipLaunchKernelGGL((bn_fwd_kernel<T, V>), dim3(p.gx, p.gy), dim3(256), 0, st, (const T *)x,
-                       (const T *)mean, (const T *)var, (const T *)gamma, (const T *)beta, eps, rows, C,
-                       p.TC, p.RG, p.chunk, (T *)y);
-    const int err = (int)hipGetLastError();
-    prof_mark(kProfBn, st, false);
-    return err;
-}
-
 template <typename T, int V, int MODE>
 int reduce_t(const RowColPlan &p, const void *a, const void *x, const void *mean, const void *var,
              const void *gamma, float eps, int64_t rows, int C, void *dx, bool want_g, bool want_b,
@@ -339,14 +335,48 @@ int launch_bn_fwd(int dtype, const void *x, const void *mean, const void *var, c
                   const void *beta, float eps, int64_t rows, int C, void *y, void *stream) {
     if (rows == 0 || C == 0) return 0;
     const int V = dtype == kBF16 ? 8 : 4;
-    const bool vec = C % V == 0 && al16(x) && al16(y);
-    RowColPlan p = plan_rowcol(dtype, rows, C, vec, kTargetBlocks);
+    // 16-byte vectors of x, y and of the per-channel parameters
+    const bool vec = C % V == 0 && al16(x) && al16(y) && al16(mean) && al16(var) &&
+                     (!gamma || al16(gamma)) && (!beta || al16(beta));
+    const int Ve = vec ? V : 1;
+    const int nvc = C / Ve;
+    const int64_t nvec = rows * (int64_t)nvc;
+    // one pass of kBnU vectors per thread; the thread count is rounded up to
+    // a multiple of nvc (block granularity q) so every thread keeps its
+    // channels
+    int64_t q = 1;
+    {
+        int64_t a = nvc, b = 256;
+        while (b) { const int64_t r = a % b; a = b; b = r; }
+        q = nvc / a;   // nvc / gcd(nvc, 256)
+    }
+    int64_t blocks = std::max<int64_t>(1, (nvec + 256 * kBnU - 1) / (256 * kBnU));
+    const bool contig = 256 % nvc == 0;
+    if (!contig) blocks = (blocks + q - 1) / q * q;
     hipStream_t st = (hipStream_t)stream;
-    if (dtype == kBF16)
-        return vec ? bn_fwd_t<bf16, 8>(p, x, mean, var, gamma, beta, eps, rows, C, y, st)
-                   : bn_fwd_t<bf16, 1>(p, x, mean, var, gamma, beta, eps, rows, C, y, st);
-    return vec ? bn_fwd_t<float, 4>(p, x, mean, var, gamma, beta, eps, rows, C, y, st)
-               : bn_fwd_t<float, 1>(p, x, mean, var, gamma, beta, eps, rows, C, y, st);
+    prof_mark(kProfBn, st, true);
+    if (dtype == kBF16) {
+        if (vec)
+            hipLaunchKernelGGL((bn_fwd_flat_kernel<bf16, 8>), dim3((unsigned)blocks), dim3(256), 0, st, (const bf16 *)x,
+                               (const bf16 *)mean, (const bf16 *)var, (const bf16 *)gamma, (const bf16 *)beta, eps, nvec,
+                               nvc, contig, (bf16 *)y);
+        else
+            hipLaunchKernelGGL((bn_fwd_flat_kernel<bf16, 1>), dim3((unsigned)blocks), dim3(256), 0, st, (const bf16 *)x,
+                               (const bf16 *)mean, (const bf16 *)var, (const bf16 *)gamma, (const bf16 *)beta, eps, nvec,
+                               nvc, contig, (bf16 *)y);
+    } else {
+        if (vec)
+            hipLaunchKernelGGL((bn_fwd_flat_kernel<float, 4>), dim3((unsigned)blocks), dim3(256), 0, st, (const float *)x,
+                               (const float *)mean, (const float *)var, (const float *)gamma, (const float *)beta, eps,
+                               nvec, nvc, contig, (float *)y);
+        else
+            hipLaunchKernelGGL((bn_fwd_flat_kernel<float, 1>), dim3((unsigned)blocks), dim3(256), 0, st, (const float *)x,
+                               (const float *)mean, (const float *)var, (const float *)gamma, (const float *)beta, eps,
+                               nvec, nvc, contig, (float *)y);
+    }
+    const int err = (int)hipGetLastError();
+    prof_mark(kProfBn, st, false);
+    return err;
 }
 
 static RowColPlan bn_bwd_plan(int dtype, int64_t rows, int C, bool vec) {

@@ -1,5 +1,5 @@
 """Every tile shape of the bf16 implicit-GEMM fast path, forced through
-MEMSAVE_GEMM_TILE, in all three contractions, on ragged sizes (including a
+MEMSAVE_GEMM_TILE, in all three contractions and both input-gradient variants, on ragged sizes (including a
 strided input gradient and a fused bias gradient), against the oracle."""
 import os
 
@@ -26,6 +26,19 @@ CASES = [
 ]
 
 
+@pytest.fixture(params=["transposed", "direct"])
+def dgrad_variant(request):
+    """Both input-gradient variants: through a transposed copy of W, and
+    reading W in place (MEMSAVE_DGRAD)."""
+    old = os.environ.get("MEMSAVE_DGRAD")
+    os.environ["MEMSAVE_DGRAD"] = request.param
+    yield request.param
+    if old is None:
+        del os.environ["MEMSAVE_DGRAD"]
+    else:
+        os.environ["MEMSAVE_DGRAD"] = old
+
+
 @pytest.fixture
 def tile(request):
     old = os.environ.get("MEMSAVE_GEMM_TILE")
@@ -39,7 +52,7 @@ def tile(request):
 
 @pytest.mark.parametrize("tile", TILES, indirect=True)
 @pytest.mark.parametrize("case", range(len(CASES)))
-def test_conv_tiles(tile, case):
+def test_conv_tiles(tile, case, dgrad_variant):
     xs, ws, stride, pad = CASES[case]
     seed = 7000 + 10 * case
     x = synth.normal(xs, seed, dtype="bf16")
@@ -56,7 +69,7 @@ def test_conv_tiles(tile, case):
 
 @pytest.mark.parametrize("tile", TILES, indirect=True)
 @pytest.mark.parametrize("shape", [(300, 72, 136), (520, 264, 392), (1000, 520, 64)])
-def test_linear_tiles(tile, shape):
+def test_linear_tiles(tile, shape, dgrad_variant):
     M, Kin, Nout = shape
     seed = 7500 + M
     x = synth.normal((M, Kin), seed, dtype="bf16")

@@ -1,6 +1,8 @@
 """GPU parity of every layer kind and mask against the oracle, on seeded
 inputs at sizes that span several tiles and end in ragged tails.  Every call
 goes through the C ABI (libmemsave.so) via the Python binding."""
+import gc
+
 import numpy as np
 import pytest
 import torch
@@ -240,10 +242,17 @@ def test_frozen_weight_input_is_freed_by_allocator():
         X = dev(synth.normal(shape, 6, dtype=dt), dt)
         y, rec = ms.layer_forward(ms.Conv2d(1, 1), X, w, None, mask)
         torch.cuda.synchronize()
-        before = torch.cuda.memory_allocated()
-        del X
-        torch.cuda.synchronize()
-        after = torch.cuda.memory_allocated()
+        # memory_allocated() is process-wide: keep the cycle collector from
+        # freeing unrelated tensors inside the measured window
+        gc.collect()
+        gc.disable()
+        try:
+            before = torch.cuda.memory_allocated()
+            del X
+            torch.cuda.synchronize()
+            after = torch.cuda.memory_allocated()
+        finally:
+            gc.enable()
         freed = before - after
         nbytes = int(np.prod(shape)) * 2
         assert rec.account()["saved_activation_bytes"] == (nbytes if keeps else 0)
