@@ -38,7 +38,10 @@ RowColPlan plan_rowcol(int dtype, int64_t rows, int C, bool vec_ok, int target_b
     const int V = dtype == kBF16 ? 8 : 4;
     p.V = (vec_ok && C % V == 0) ? V : 1;   // a row must hold whole vectors
     p.nvc = std::max(C / p.V, 1);
-    p.TC = std::min(p.nvc, 256);
+    // at most 64 channel vectors per block: the other threads of the block
+    // walk more rows of the same columns, which the block reduces in LDS, so
+    // fewer partial rows reach the finalize pass
+    p.TC = std::min(p.nvc, 64);
     p.RG = 256 / p.TC;
     p.gx = (p.nvc + p.TC - 1) / p.TC;
     int64_t want_y = std::max<int64_t>(1, target_blocks / p.gx);
@@ -159,7 +162,7 @@ __global__ __launch_bounds__(256) void rowcol_reduce_kernel(
         const int64_t r0 = (int64_t)blockIdx.y * chunk;
         const int64_t r1 = min(rows, r0 + chunk);
         int64_t r = r0 + rg;
-        constexpr int U = 4;
+        constexpr int U = 8;
         auto body = [&](const VecT<T, V> &va, const VecT<T, V> *vx, int64_t rr) {
             if constexpr (MODE == 0) {
 #pragma unroll
@@ -225,27 +228,33 @@ __global__ __launch_bounds__(256) void rowcol_reduce_kernel(
     }
 }
 
-// out[c] = sum_y part[y][c], rounded once to T.  A block owns 64 columns;
-// its 4 thread rows split the partial rows and meet in LDS.
+// out[c] = sum_y part[y][c], rounded once to T.  A block owns 16 columns;
+// its 16 thread rows split the partial rows (each keeps several loads in
+// flight) and meet in LDS in a fixed order.
 template <typename T>
 __global__ __launch_bounds__(256) void finalize_kernel(const float *__restrict__ part, int gy, int C,
                                                        T *__restrict__ out) {
-    __shared__ float red[4][64];
-    const int cl = threadIdx.x & 63, yg = threadIdx.x >> 6;
-    const int c = blockIdx.x * 64 + cl;
+    __shared__ float red[16][16];
+    const int cl = threadIdx.x & 15, yg = threadIdx.x >> 4;
+    const int c = blockIdx.x * 16 + cl;
     float s = 0.f;
     if (c < C) {
         int y = yg;
-        for (; y + 12 < gy; y += 16) {
-            const float a0 = part[(int64_t)y * C + c], a1 = part[(int64_t)(y + 4) * C + c];
-            const float a2 = part[(int64_t)(y + 8) * C + c], a3 = part[(int64_t)(y + 12) * C + c];
+        for (; y + 48 < gy; y += 64) {
+            const float a0 = part[(int64_t)y * C + c], a1 = part[(int64_t)(y + 16) * C + c];
+            const float a2 = part[(int64_t)(y + 32) * C + c], a3 = part[(int64_t)(y + 48) * C + c];
             s += (a0 + a1) + (a2 + a3);
         }
-        for (; y < gy; y += 4) s += part[(int64_t)y * C + c];
+        for (; y < gy; y += 16) s += part[(int64_t)y * C + c];
     }
     red[yg][cl] = s;
     __syncthreads();
-    if (yg == 0 && c < C) out[c] = from_f32<T>((red[0][cl] + red[1][cl]) + (red[2][cl] + red[3][cl]));
+    if (yg == 0 && c < C) {
+        float t = 0.f;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) t += red[q][cl];
+        out[c] = from_f32<T>(t);
+    }
 }
 
 // ---------------------------------------------------------------- avgpool
@@ -321,7 +330,7 @@ int reduce_t(const RowColPlan &p, const void *a, const void *x, const void *mean
 
 template <typename T>
 int finalize_t(const float *part, int gy, int C, void *out, hipStream_t st) {
-    hipLaunchKernelGGL(finalize_kernel<T>, dim3((C + 63) / 64), dim3(256), 0, st, part, gy, C, (T *)out);
+    hipLaunchKernelGGL(finalize_kernel<T>, dim3((C + 15) / 16), dim3(256), 0, st, part, gy, C, (T *)out);
     return (int)hipGetLastError();
 }
 
