@@ -31,6 +31,7 @@
 #include <algorithm>
 #include <cstdio>
 #include <cstdlib>
+#include <cstring>
 
 #include "common.h"
 #include "../device.h"
@@ -564,6 +565,28 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
     constexpr int SEG = G::WN / 8;                   // 16-byte segments per staged row
     constexpr int ROWS_PER_PASS = 64 / SEG;
     typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+    // forward bias: the lane's output columns are the same for every row it
+    // holds, so its bias values are read once and added in fp32 before the
+    // single rounding to bf16
+    float bcol[TN][4][4];
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) bcol[j][q][v] = 0.f;
+    if constexpr (MODE == kFwd) {
+        if (P.bias) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int n = n0 + wn0 + j * 32 + 8 * q + 4 * fh;
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) bcol[j][q][v] = n + v < N ? (float)P.bias[n + v] : 0.f;
+                }
+        }
+    }
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -572,7 +595,7 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
             for (int q = 0; q < 4; ++q) {
                 bf16x4 o;
 #pragma unroll
-                for (int v = 0; v < 4; ++v) o[v] = (bf16)acc[i][j][4 * q + v];
+                for (int v = 0; v < 4; ++v) o[v] = (bf16)(acc[i][j][4 * q + v] + bcol[j][q][v]);
                 *reinterpret_cast<bf16x4 *>(stage + fr * G::EPI_PITCH + j * 32 + 8 * q + 4 * fh) = o;
             }
         wait_lgkm0();   // this wave's staged rows are written
@@ -586,13 +609,6 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
             Vec16<bf16> v;
             v.u = *reinterpret_cast<const u32x4 *>(stage + rl * G::EPI_PITCH + cl);
             if (m >= M || n >= N) continue;
-            if constexpr (MODE == kFwd) {
-                if (P.bias) {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        if (n + e < N) v.e[e] = (bf16)((float)v.e[e] + (float)P.bias[n + e]);
-                }
-            }
             bf16 *dst;
             if constexpr (DG && !UNIT) {
                 const int HW = f.Hp * f.Wp;
@@ -698,36 +714,48 @@ namespace {
 constexpr int kCUs = 256;
 
 struct Tile {
-    int bm, bn, per_cu;   // tile shape, blocks resident per CU
-    float eff;            // relative MFMA efficiency of the shape
+    const char *name;
+    int bm, bn;       // block tile
+    int wr, wc;       // wave grid (wr * wc waves of (bm/wr) x (bn/wc))
+    int stages;       // LDS ring depth (BK = 64 per stage)
+    int per_cu;       // blocks resident per CU
+    float eff1;       // relative MFMA efficiency with one block on the CU
+    float eff;        // ... with per_cu blocks on the CU
 };
-// 256x256: 8 waves (2 x 4) of 128 x 64, 2 stages (128 KB LDS);
-// 256x128: 8 waves (2 x 4) of 128 x 32, 3 stages (144 KB);
-// 128x128: 4 waves of 64 x 64, 2 stages (64 KB, two blocks per CU);
-// 128x64:  4 waves of 64 x 32, 2 stages (48 KB, three blocks per CU).
-constexpr Tile kTiles[] = {{256, 256, 1, 1.20f}, {256, 128, 1, 1.00f}, {128, 128, 2, 1.00f}, {128, 64, 3, 0.75f}};
+// Efficiencies measured on the Linear and encoder shapes: a 2-stage
+// 128 x 128 block alone on a CU cannot hide its load latency (a co-resident
+// block normally does), where the 4-stage variant can.
+constexpr Tile kTiles[] = {
+    {"256x256", 256, 256, 2, 4, 2, 1, 1.20f, 1.20f},      // 8 waves of 128 x 64, 128 KB LDS
+    {"256x128", 256, 128, 2, 4, 3, 1, 1.00f, 1.00f},      // 8 waves of 128 x 32, 144 KB
+    {"128x128", 128, 128, 2, 2, 2, 2, 0.78f, 1.00f},      // 4 waves of 64 x 64, 64 KB, two blocks per CU
+    {"128x128w8", 128, 128, 2, 4, 2, 2, 0.85f, 1.02f},    // 8 waves of 64 x 32, 64 KB, two blocks per CU
+    {"128x128s4", 128, 128, 2, 2, 4, 1, 0.90f, 0.90f},    // 4 waves of 64 x 64, 4 stages (128 KB)
+    {"128x64", 128, 64, 2, 2, 2, 3, 0.75f, 0.75f},        // 4 waves of 64 x 32, 48 KB, three blocks per CU
+};
+constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
+// tiles the planner chooses from
+constexpr bool kAuto[kNumTiles] = {true, true, true, true, true, true};
 
-// MEMSAVE_GEMM_TILE=<bm>x<bn> forces one tile shape (a debugging and
-// testing knob); returns its index or -1.
+// MEMSAVE_GEMM_TILE=<name> forces one tile shape (a debugging and testing
+// knob); returns its index or -1.
 int forced_tile() {
     const char *e = getenv("MEMSAVE_GEMM_TILE");
     if (!e || !*e) return -1;
-    int bm = 0, bn = 0;
-    if (sscanf(e, "%dx%d", &bm, &bn) != 2) return -1;
-    for (int i = 0; i < (int)(sizeof(kTiles) / sizeof(kTiles[0])); ++i)
-        if (kTiles[i].bm == bm && kTiles[i].bn == bn) return i;
+    for (int i = 0; i < kNumTiles; ++i)
+        if (strcmp(kTiles[i].name, e) == 0) return i;
     return -1;
 }
 
 // Pick the tile that minimises (waves of blocks) x (time per wave).
 // `first` skips the largest shapes.
-Tile pick(long M, long N, long K, int splits_allowed, int *splits_out, int z = 1, int first = 0) {
+Tile pick(long M, long N, long K, int splits_allowed, int *splits_out, int z = 1) {
     double best = 1e300;
-    Tile bt = kTiles[first];
+    Tile bt = kTiles[0];
     int bs = 1;
     const int forced = forced_tile();
-    for (int ti = first; ti < (int)(sizeof(kTiles) / sizeof(kTiles[0])); ++ti) {
-        if (forced >= first && ti != forced) continue;
+    for (int ti = 0; ti < kNumTiles; ++ti) {
+        if (forced >= 0 ? ti != forced : !kAuto[ti]) continue;
         const Tile &t = kTiles[ti];
         const long tiles = ((M + t.bm - 1) / t.bm) * ((N + t.bn - 1) / t.bn) * z;
         int splits = 1;
@@ -741,7 +769,8 @@ Tile pick(long M, long N, long K, int splits_allowed, int *splits_out, int z = 1
         // blocks that actually share a CU in the fullest wave
         const long resident = std::min<long>(t.per_cu, (blocks + kCUs - 1) / kCUs);
         const double kper = (double)K / splits;
-        const double cost = (double)waves * resident * t.bm * t.bn * (kper + 64.0) / t.eff;
+        const double eff = resident > 1 ? t.eff : t.eff1;
+        const double cost = (double)waves * resident * t.bm * t.bn * (kper + 64.0) / eff;
         if (cost < best * 0.999) {
             best = cost;
             bt = t;
@@ -766,6 +795,8 @@ template <int MODE, bool UNIT>
 int go_tile(const Tile &t, const Args &a, dim3 grid, hipStream_t st) {
     if (t.bm == 256 && t.bn == 256) return go<MODE, 256, 256, 2, 4, 2, 1, UNIT>(a, grid, st);
     if (t.bm == 256 && t.bn == 128) return go<MODE, 256, 128, 2, 4, 3, 1, UNIT>(a, grid, st);
+    if (t.bm == 128 && t.bn == 128 && t.wc == 4) return go<MODE, 128, 128, 2, 4, 2, 2, UNIT>(a, grid, st);
+    if (t.bm == 128 && t.bn == 128 && t.stages == 4) return go<MODE, 128, 128, 2, 2, 4, 1, UNIT>(a, grid, st);
     if (t.bm == 128 && t.bn == 128) return go<MODE, 128, 128, 2, 2, 2, 2, UNIT>(a, grid, st);
     return go<MODE, 128, 64, 2, 2, 2, 3, UNIT>(a, grid, st);
 }
@@ -792,7 +823,7 @@ WgradPlan wgrad_plan(const ConvGeom &g) {
     const long M = g.K, N = (long)g.R * g.S * g.C, K = (long)g.N * g.P * g.Q;
     int splits = 1;
     const int max_splits = (int)std::max<long>(1, K / (8 * BK));   // at least 8 BK steps per split
-    Tile t = pick(M, N, K, max_splits, &splits, 1, 0);
+    Tile t = pick(M, N, K, max_splits, &splits, 1);
     int k_split = (int)((K + splits - 1) / splits);
     k_split = (k_split + BK - 1) / BK * BK;
     if (K == 0) k_split = BK;
