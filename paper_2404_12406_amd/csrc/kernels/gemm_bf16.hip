@@ -299,7 +299,9 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
     }
 
     // ------------------------------------------------ issue the loads of one tile
-    auto issue = [&](int stage, int k0) {
+    // Loads j of A are instructions j, loads j of B are NIA + j; issue_range
+    // issues those in [lo, hi).
+    auto issue_range = [&](int stage, int k0, int lo, int hi) {
         char *sA = smem + stage * G::STAGE_BYTES;
         char *sB = sA + G::A_BYTES;
         // ---- A
@@ -344,7 +346,7 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
                     off = a_base[j] + (p * g.Q + q) * g.K + off_k[v];
                 }
                 const uint32_t boff = ok ? (uint32_t)off * 2u : kOOB;
-                dma16(ra, sA + (wave * NIA + j) * 1024, boff);
+                if (j >= lo && j < hi) dma16(ra, sA + (wave * NIA + j) * 1024, boff);
             }
         } else {
             constexpr int SPR = BM / 8, KPI = 64 / SPR;
@@ -353,7 +355,7 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
                 const int kk = k0 + (wave * NIA + j) * KPI + lane / SPR;
                 const bool ok = a_ok[j] && kk < k_end;
                 const uint32_t boff = ok ? ((uint32_t)kk * (uint32_t)g.K + a_mn_off[j]) * 2u : kOOB;
-                dma16(ra, sA + (wave * NIA + j) * 1024, boff);
+                if (j >= lo && j < hi) dma16(ra, sA + (wave * NIA + j) * 1024, boff);
             }
         }
         // ---- B
@@ -377,7 +379,7 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
                 const int v = (wave * NIB + j) & 1;
                 const bool ok = kin[v] && b_ok[j];
                 const uint32_t boff = ok ? (uint32_t)(b_base[j] + off_k[v]) * 2u : kOOB;
-                dma16(rb, sB + (wave * NIB + j) * 1024, boff);
+                if (NIA + j >= lo && NIA + j < hi) dma16(rb, sB + (wave * NIB + j) * 1024, boff);
             }
         } else {
             constexpr int SPR = BN / 8, KPI = 64 / SPR;
@@ -407,10 +409,11 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
                     off = (uint32_t)(((n * g.H + ih) * g.W + iw) * g.C) + b_mn_off[j];
                 }
                 const uint32_t boff = ok ? off * 2u : kOOB;
-                dma16(rb, sB + (wave * NIB + j) * 1024, boff);
+                if (NIA + j >= lo && NIA + j < hi) dma16(rb, sB + (wave * NIB + j) * 1024, boff);
             }
         }
     };
+    auto issue = [&](int stage, int k0) { issue_range(stage, k0, 0, NIA + NIB); };
 
     const int fr = lane & 31, fh = lane >> 5;   // row within a 32-row tile, k half
     floatx16 acc[TM][TN];
@@ -478,33 +481,49 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
     // of its first slice are in (fa0, fb0).  Each slice reads the next
     // slice's fragments while its MFMAs run; the last slice first makes sure
     // every wave has read tile kt (own LDS reads done, barrier) and tile kt+1
-    // has landed (own DMA done, same barrier), then refills stage s with tile
-    // kt + STAGES and reads tile kt+1's first slice.  Refills past the end of
-    // the reduction take the out-of-range path and write zeros into a stage
-    // that only feeds MFMAs nobody keeps.
+    // has landed (own DMA done, same barrier), then reads tile kt+1's first
+    // slice.  The stage tile kt came from is refilled with tile kt + STAGES:
+    //  * with two stages, right after that barrier (the only window);
+    //  * with three or more, spread over the slices of the next step, so the
+    //    load instructions do not arrive at the texture unit in one burst.
+    // Refills past the end of the reduction take the out-of-range path and
+    // write zeros into a stage that only feeds MFMAs nobody keeps.
+    constexpr bool SPREAD = STAGES >= 3;
     bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN];
     auto step = [&](int kt) {
         const int s = kt % STAGES;
+        // refill of the stage step kt-1 consumed (spread mode)
+        const int rs = (kt + STAGES - 1) % STAGES;
+        const int rk = k_begin + (kt - 1 + STAGES) * BK;
+        const bool refill = SPREAD && kt >= 1;
 #pragma unroll
         for (int sub = 0; sub < NSUB; ++sub) {
             const bf16x8 *ca = (sub & 1) ? fa1 : fa0;
             const bf16x8 *cb = (sub & 1) ? fb1 : fb0;
             bf16x8 *na = (sub & 1) ? fa0 : fa1;
             bf16x8 *nb = (sub & 1) ? fb0 : fb1;
+            constexpr int PER = (NVMEM + NSUB - 1) / NSUB;
+            const int lo = sub * PER, hi = min(NVMEM, lo + PER);
             __builtin_amdgcn_sched_barrier(0);
             if (sub + 1 < NSUB) {
+                if constexpr (SPREAD) {
+                    if (refill) issue_range(rs, rk, lo, hi);
+                }
                 read_sub(s, sub + 1, na, nb);
                 mfma_sub(ca, cb);
-                interleave(0);
+                interleave(SPREAD ? hi - lo : 0);
             } else {
+                if constexpr (SPREAD) {
+                    if (refill) issue_range(rs, rk, lo, hi);
+                }
                 wait_vmcnt<(STAGES - 2) * NVMEM>();
                 wait_lgkm0();
                 __builtin_amdgcn_s_barrier();
                 __builtin_amdgcn_sched_barrier(0);
-                issue(s, k_begin + (kt + STAGES) * BK);
+                if constexpr (!SPREAD) issue(s, k_begin + (kt + STAGES) * BK);
                 read_sub((kt + 1) % STAGES, 0, na, nb);
                 mfma_sub(ca, cb);
-                interleave(NVMEM);
+                interleave(SPREAD ? 0 : NVMEM);
             }
             __builtin_amdgcn_sched_barrier(0);
         }
