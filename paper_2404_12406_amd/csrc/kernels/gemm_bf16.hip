@@ -489,13 +489,14 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
     // Refills past the end of the reduction take the out-of-range path and
     // write zeros into a stage that only feeds MFMAs nobody keeps.
     constexpr bool SPREAD = STAGES >= 3;
-    bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN];
-    auto step = [&](int kt) {
+    bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN], fa2[TM], fb2[TN];
+    // three or more stages: refills spread over the next step's slices
+    auto step_spread = [&](int kt) {
         const int s = kt % STAGES;
-        // refill of the stage step kt-1 consumed (spread mode)
+        // refill of the stage step kt-1 consumed
         const int rs = (kt + STAGES - 1) % STAGES;
         const int rk = k_begin + (kt - 1 + STAGES) * BK;
-        const bool refill = SPREAD && kt >= 1;
+        const bool refill = kt >= 1;
 #pragma unroll
         for (int sub = 0; sub < NSUB; ++sub) {
             const bf16x8 *ca = (sub & 1) ? fa1 : fa0;
@@ -505,27 +506,64 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
             constexpr int PER = (NVMEM + NSUB - 1) / NSUB;
             const int lo = sub * PER, hi = min(NVMEM, lo + PER);
             __builtin_amdgcn_sched_barrier(0);
+            if (refill) issue_range(rs, rk, lo, hi);
             if (sub + 1 < NSUB) {
-                if constexpr (SPREAD) {
-                    if (refill) issue_range(rs, rk, lo, hi);
-                }
                 read_sub(s, sub + 1, na, nb);
                 mfma_sub(ca, cb);
-                interleave(SPREAD ? hi - lo : 0);
+                interleave(hi - lo);
             } else {
-                if constexpr (SPREAD) {
-                    if (refill) issue_range(rs, rk, lo, hi);
-                }
                 wait_vmcnt<(STAGES - 2) * NVMEM>();
                 wait_lgkm0();
                 __builtin_amdgcn_s_barrier();
                 __builtin_amdgcn_sched_barrier(0);
-                if constexpr (!SPREAD) issue(s, k_begin + (kt + STAGES) * BK);
                 read_sub((kt + 1) % STAGES, 0, na, nb);
                 mfma_sub(ca, cb);
-                interleave(SPREAD ? 0 : NVMEM);
+                interleave(0);
             }
             __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    // two stages: fragments are read two slices ahead (three buffers), so a
+    // wave's last read of tile kt is issued in slice 1 and the barrier can
+    // come at the start of slice 2; the refill of tile kt's stage with tile
+    // kt+2 is then spread over slices 2 and 3.  On entry (fa0, fb0) and
+    // (fa1, fb1) hold slices 0 and 1 of tile kt; on exit, of tile kt+1.
+    auto step_two = [&](int kt) {
+        const int s = kt % STAGES, s1 = (kt + 1) % STAGES;
+        const int rk = k_begin + (kt + STAGES) * BK;
+        constexpr int HALF = (NVMEM + 1) / 2;
+        __builtin_amdgcn_sched_barrier(0);
+        read_sub(s, 2, fa2, fb2);            // slice 0: read slice 2
+        mfma_sub(fa0, fb0);
+        interleave(0);
+        __builtin_amdgcn_sched_barrier(0);
+        read_sub(s, 3, fa0, fb0);            // slice 1: read slice 3
+        mfma_sub(fa1, fb1);
+        interleave(0);
+        __builtin_amdgcn_sched_barrier(0);
+        wait_vmcnt<0>();                     // slice 2: tile kt+1 landed, tile kt read by all
+        wait_lgkm0();
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        issue_range(s, rk, 0, HALF);
+        read_sub(s1, 0, fa1, fb1);
+        mfma_sub(fa2, fb2);
+        interleave(HALF);
+        __builtin_amdgcn_sched_barrier(0);
+        issue_range(s, rk, HALF, NVMEM);     // slice 3
+        read_sub(s1, 1, fa2, fb2);
+        mfma_sub(fa0, fb0);
+        interleave(NVMEM - HALF);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            fa0[i] = fa1[i];
+            fa1[i] = fa2[i];
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            fb0[j] = fb1[j];
+            fb1[j] = fb2[j];
         }
     };
     static_assert(NSUB % 2 == 0, "an even number of slices keeps the fragment buffers' roles fixed");
@@ -535,7 +573,13 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
     wait_vmcnt<(STAGES - 1) * NVMEM>();
     __builtin_amdgcn_s_barrier();
     read_sub(0, 0, fa0, fb0);
-    for (int kt = 0; kt < nk; ++kt) step(kt);
+    if constexpr (SPREAD) {
+        for (int kt = 0; kt < nk; ++kt) step_spread(kt);
+    } else {
+        static_assert(NSUB == 4, "the two-stage schedule is written for four slices per step");
+        read_sub(0, 1, fa1, fb1);
+        for (int kt = 0; kt < nk; ++kt) step_two(kt);
+    }
     // the refills of the last steps are still writing into LDS: drain them
     // before LDS is reused or the workgroup ends
     wait_vmcnt<0>();
