@@ -135,7 +135,10 @@ enum {
  * autograd records no node).  Otherwise *rec receives a new record and its
  * saved_activation_bytes are added to the process-wide ledger.
  * x, W, b, y: see ms_kind.  W must be NULL for MS_AVGPOOL; b may be NULL.
- * y is caller-allocated and fully overwritten.
+ * y is caller-allocated and fully overwritten.  A bf16 convolution whose
+ * channel count is not a multiple of 8 uses transient workspace for
+ * zero-padded channel copies (MS_E_NOMEM if it cannot be had; nothing is
+ * launched then).
  */
 ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_tensor *W,
                            const ms_tensor *b, uint32_t mask, const ms_tensor *y,

@@ -21,9 +21,11 @@ struct ConvGeom {
     int sh, sw, ph, pw;
 };
 
-// y = W * x + b (b may be null).
+// y = W * x + b (b may be null).  May use conv_fwd_workspace() bytes of
+// workspace (zero-padded channel copies when C is not a multiple of 8).
+size_t conv_fwd_workspace(int dtype, const ConvGeom &g);
 int launch_conv_fwd(int dtype, const ConvGeom &g, const void *x, const void *w,
-                    const void *bias, void *y, void *stream);
+                    const void *bias, void *y, void *ws, void *stream);
 
 // dx = input gradient of the convolution for grad dy (needs w only).  May
 // use conv_dgrad_workspace() bytes of workspace (a transposed copy of w).

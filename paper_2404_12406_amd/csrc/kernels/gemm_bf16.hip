@@ -740,6 +740,37 @@ __global__ __launch_bounds__(256) void transpose_krsc_kernel(const bf16 *__restr
     }
 }
 
+// Channel counts that are not a multiple of 8 (the 3-channel stem): the fast
+// path runs on copies whose channels are padded with zeros to C8 =
+// roundup(C, 8).  dst[row][c] = c < C ? src[row][c] : 0, one 16-byte row
+// vector per thread.
+__global__ __launch_bounds__(256) void pad_channels_kernel(const bf16 *__restrict__ src, int64_t rows, int C, int C8,
+                                                           bf16 *__restrict__ dst) {
+    const int nv = C8 / 8;
+    const int64_t total = rows * nv;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = i / nv;
+        const int c0 = (int)(i - row * nv) * 8;
+        Vec16<bf16> v;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v.e[e] = c0 + e < C ? src[row * C + c0 + e] : (bf16)0.f;
+        store16(dst + row * C8 + c0, v);
+    }
+}
+
+// dst[row][c] = src[row][c] for c < C (drops the padding channels).
+__global__ __launch_bounds__(256) void crop_channels_kernel(const bf16 *__restrict__ src, int64_t rows, int C8, int C,
+                                                            bf16 *__restrict__ dst) {
+    const int64_t total = rows * C;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = i / C;
+        const int c = (int)(i - row * C);
+        dst[i] = src[row * C8 + c];
+    }
+}
+
 // Sum split-K partials (and fused bias-gradient partials) to bf16.
 __global__ __launch_bounds__(256) void reduce_kernel(const float *__restrict__ part, int splits, int64_t n,
                                                      bf16 *__restrict__ out, const float *__restrict__ dbpart,
@@ -877,6 +908,34 @@ bool unit_geom(const ConvGeom &g) {
 
 uint32_t bytes_of(long elems) { return (uint32_t)(elems * 2); }
 
+int pad8(int c) { return (c + 7) / 8 * 8; }
+size_t al256(size_t n) { return (n + 255) / 256 * 256; }
+
+int pad_channels(const void *src, int64_t rows, int C, void *dst, hipStream_t st) {
+    const int C8 = pad8(C);
+    const int64_t total = rows * (C8 / 8);
+    if (total == 0) return 0;
+    const int blocks = (int)std::min<int64_t>((total + 255) / 256, 8192);
+    hipLaunchKernelGGL(pad_channels_kernel, dim3(blocks), dim3(256), 0, st, (const bf16 *)src, rows, C, C8, (bf16 *)dst);
+    return (int)hipGetLastError();
+}
+
+int crop_channels(const void *src, int64_t rows, int C, void *dst, hipStream_t st) {
+    const int64_t total = rows * C;
+    if (total == 0) return 0;
+    const int blocks = (int)std::min<int64_t>((total + 255) / 256, 8192);
+    hipLaunchKernelGGL(crop_channels_kernel, dim3(blocks), dim3(256), 0, st, (const bf16 *)src, rows, pad8(C), C,
+                       (bf16 *)dst);
+    return (int)hipGetLastError();
+}
+
+// The geometry with C padded to a multiple of 8.
+ConvGeom padded(const ConvGeom &g) {
+    ConvGeom g8 = g;
+    g8.C = pad8(g.C);
+    return g8;
+}
+
 struct WgradPlan {
     Tile t;
     int splits, k_split;
@@ -897,8 +956,25 @@ WgradPlan wgrad_plan(const ConvGeom &g) {
 }  // namespace
 
 // Each returns -1 when the fast path does not apply, else a hipError_t.
-int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, void *y, hipStream_t st) {
-    if (g.C % 8 != 0 || !al16(x) || !al16(w) || !al16(y)) return -1;
+// Forward with C % 8 != 0: padded copies of x and W (workspace below).
+size_t fwd_workspace(const ConvGeom &g) {
+    if (g.C % 8 == 0) return 0;
+    const int C8 = pad8(g.C);
+    return al256((size_t)g.N * g.H * g.W * C8 * 2) + al256((size_t)g.K * g.R * g.S * C8 * 2);
+}
+
+int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, void *y, void *ws, hipStream_t st) {
+    if (g.C % 8 != 0) {
+        if (!ws || !al16(ws) || !al16(y)) return -1;
+        const ConvGeom g8 = padded(g);
+        char *xp = static_cast<char *>(ws);
+        char *wp = xp + al256((size_t)g.N * g.H * g.W * g8.C * 2);
+        int err = pad_channels(x, (int64_t)g.N * g.H * g.W, g.C, xp, st);
+        if (!err) err = pad_channels(w, (int64_t)g.K * g.R * g.S, g.C, wp, st);
+        if (err) return err;
+        return conv_fwd(g8, xp, wp, bias, y, nullptr, st);
+    }
+    if (!al16(x) || !al16(w) || !al16(y)) return -1;
     Args a{};
     a.a = (const bf16 *)x; a.b = (const bf16 *)w; a.c = (bf16 *)y; a.bias = (const bf16 *)bias; a.g = g;
     a.M = g.N * g.P * g.Q; a.N = g.K; a.K = g.R * g.S * g.C;
@@ -922,12 +998,32 @@ bool dgrad_direct(const ConvGeom &g) {
 }
 
 size_t dgrad_workspace(const ConvGeom &g) {
-    if (g.C % 8 != 0 || g.K % 8 != 0 || dgrad_direct(g)) return 0;
+    if (g.K % 8 != 0) return 0;
+    if (g.C % 8 != 0) {
+        // padded W, padded dx, then the workspace of the padded contraction
+        const ConvGeom g8 = padded(g);
+        return al256((size_t)g.K * g.R * g.S * g8.C * 2) + al256((size_t)g.N * g.H * g.W * g8.C * 2) +
+               dgrad_workspace(g8);
+    }
+    if (dgrad_direct(g)) return 0;
     return (size_t)g.K * g.R * g.S * g.C * sizeof(bf16) + 256;
 }
 
 int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, void *ws, hipStream_t st) {
-    if (g.C % 8 != 0 || g.K % 8 != 0 || !al16(dy) || !al16(w) || !al16(dx)) return -1;
+    if (g.K % 8 != 0) return -1;
+    if (g.C % 8 != 0) {
+        if (!ws || !al16(ws)) return -1;
+        const ConvGeom g8 = padded(g);
+        char *wp = static_cast<char *>(ws);
+        char *dxp = wp + al256((size_t)g.K * g.R * g.S * g8.C * 2);
+        char *ws2 = dxp + al256((size_t)g.N * g.H * g.W * g8.C * 2);
+        int err = pad_channels(w, (int64_t)g.K * g.R * g.S, g.C, wp, st);
+        if (err) return err;
+        err = conv_dgrad(g8, dy, wp, dxp, ws2, st);
+        if (err) return err;   // -1: not applicable (the caller falls back), else a HIP error
+        return crop_channels(dxp, (int64_t)g.N * g.H * g.W, g.C, dx, st);
+    }
+    if (!al16(dy) || !al16(w) || !al16(dx)) return -1;
     const bool direct = dgrad_direct(g);
     if (!direct && (!ws || !al16(ws))) return -1;
     Args a{};
@@ -951,9 +1047,15 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, void 
     return direct ? go_mode<kDgradN>(t, a, grid, unit_geom(g), st) : go_mode<kDgrad>(t, a, grid, unit_geom(g), st);
 }
 
-bool wgrad_applies(const ConvGeom &g) { return g.C % 8 == 0 && g.K % 8 == 0; }
+bool wgrad_applies(const ConvGeom &g) { return g.K % 8 == 0; }
 
 size_t wgrad_workspace(const ConvGeom &g, bool with_db) {
+    if (g.C % 8 != 0) {
+        // padded x, padded dW, then the workspace of the padded contraction
+        const ConvGeom g8 = padded(g);
+        return al256((size_t)g.N * g.H * g.W * g8.C * 2) + al256((size_t)g.K * g.R * g.S * g8.C * 2) +
+               wgrad_workspace(g8, with_db);
+    }
     WgradPlan p = wgrad_plan(g);
     size_t ws = 0;
     if (p.splits > 1) ws += (size_t)p.splits * g.K * ((size_t)g.R * g.S * g.C) * sizeof(float);
@@ -962,7 +1064,20 @@ size_t wgrad_workspace(const ConvGeom &g, bool with_db) {
 }
 
 int conv_wgrad(const ConvGeom &g, const void *dy, const void *x, void *dw, void *db, void *ws, hipStream_t st) {
-    if (!wgrad_applies(g) || !al16(dy) || !al16(x) || !al16(dw)) return -1;
+    if (!wgrad_applies(g)) return -1;
+    if (g.C % 8 != 0) {
+        if (!ws || !al16(ws) || !al16(dy)) return -1;
+        const ConvGeom g8 = padded(g);
+        char *xp = static_cast<char *>(ws);
+        char *dwp = xp + al256((size_t)g.N * g.H * g.W * g8.C * 2);
+        char *ws2 = dwp + al256((size_t)g.K * g.R * g.S * g8.C * 2);
+        int err = pad_channels(x, (int64_t)g.N * g.H * g.W, g.C, xp, st);
+        if (err) return err;
+        err = conv_wgrad(g8, dy, xp, dwp, db, ws2, st);
+        if (err) return err;   // -1: not applicable (the caller falls back), else a HIP error
+        return crop_channels(dwp, (int64_t)g.K * g.R * g.S, g.C, dw, st);
+    }
+    if (!al16(dy) || !al16(x) || !al16(dw)) return -1;
     WgradPlan p = wgrad_plan(g);
     Args a{};
     a.a = (const bf16 *)dy; a.b = (const bf16 *)x; a.g = g;

@@ -33,7 +33,8 @@ namespace ms {
 
 // bf16 fast path (gemm_bf16.hip); each returns -1 when it does not apply.
 namespace g2 {
-int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, void *y, hipStream_t st);
+size_t fwd_workspace(const ConvGeom &g);
+int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, void *y, void *ws, hipStream_t st);
 size_t dgrad_workspace(const ConvGeom &g);
 int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, void *ws, hipStream_t st);
 bool wgrad_applies(const ConvGeom &g);
@@ -619,10 +620,14 @@ SplitPlan wgrad_split(int dtype, const ConvGeom &g) {
 
 }  // namespace
 
+size_t conv_fwd_workspace(int dtype, const ConvGeom &g) {
+    return dtype == kBF16 ? g2::fwd_workspace(g) : 0;
+}
+
 int launch_conv_fwd(int dtype, const ConvGeom &g, const void *x, const void *w, const void *bias,
-                    void *y, void *stream) {
+                    void *y, void *ws, void *stream) {
     if (dtype == kBF16) {
-        const int r = g2::conv_fwd(g, x, w, bias, y, (hipStream_t)stream);
+        const int r = g2::conv_fwd(g, x, w, bias, y, ws, (hipStream_t)stream);
         if (r >= 0) return r;
     }
     IgemmParams prm{};
@@ -669,10 +674,12 @@ int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *
 }
 
 size_t conv_wgrad_workspace(int dtype, const ConvGeom &g, bool with_db) {
-    if (dtype == kBF16 && g2::wgrad_applies(g)) return g2::wgrad_workspace(g, with_db);
+    // the fallback below may run when the fast path turns out not to apply
+    // (pointer alignment), so the workspace covers both
     SplitPlan sp = wgrad_split(dtype, g);
-    if (sp.splits <= 1) return 0;
-    return (size_t)sp.splits * (size_t)g.K * (size_t)(g.R * g.S * g.C) * sizeof(float);
+    const size_t v1 = sp.splits <= 1 ? 0 : (size_t)sp.splits * (size_t)g.K * (size_t)(g.R * g.S * g.C) * sizeof(float);
+    if (dtype == kBF16 && g2::wgrad_applies(g)) return std::max(v1, g2::wgrad_workspace(g, with_db));
+    return v1;
 }
 
 int launch_conv_wgrad(int dtype, const ConvGeom &g, const void *dy, const void *x, void *dw,

@@ -392,6 +392,18 @@ ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
     if (st) return st;
     const uint32_t borrowed = borrowed_bits(pl.kind, mask, MS_POLICY_SELECTIVE, pl.has_w, pl.has_b);
     const uint32_t kernels = kernel_bits(pl.kind, mask);
+    // transient forward workspace (zero-padded channel copies for channel
+    // counts that are not a multiple of 8), taken before anything is launched
+    void *fws = nullptr;
+    if (pl.kind == MS_CONV2D || pl.kind == MS_LINEAR) {
+        const size_t fb = ms::conv_fwd_workspace(pl.dtype, pl.g);
+        if (fb) {
+            int werr = 0;
+            fws = ms::workspace_get(stream, fb, &werr);
+            if (!fws) return werr == 1 ? fail(MS_E_NOMEM, "workspace of %zu bytes unavailable", fb)
+                                       : hip_fail(ms::device_last_error(), "workspace");
+        }
+    }
     ms_record *r = nullptr;
     if (mask != 0) {
         r = new (std::nothrow) ms_record();
@@ -401,7 +413,7 @@ ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
     switch (pl.kind) {
     case MS_CONV2D:
     case MS_LINEAR:
-        err = ms::launch_conv_fwd(pl.dtype, pl.g, x->data, W->data, b ? b->data : nullptr, y->data, stream);
+        err = ms::launch_conv_fwd(pl.dtype, pl.g, x->data, W->data, b ? b->data : nullptr, y->data, fws, stream);
         break;
     case MS_BN_EVAL:
         err = ms::launch_bn_fwd(pl.dtype, x->data, layer->running_mean->data, layer->running_var->data,

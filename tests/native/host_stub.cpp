@@ -52,8 +52,11 @@ void stub_reset() {
 
 namespace ms {
 
-int launch_conv_fwd(int, const ConvGeom &g, const void *x, const void *w, const void *, void *y, void *) {
+size_t conv_fwd_workspace(int, const ConvGeom &g) { return g.C % 8 ? 256 : 0; }
+
+int launch_conv_fwd(int, const ConvGeom &g, const void *x, const void *w, const void *, void *y, void *ws, void *) {
     log("conv_fwd");
+    if (g.C % 8 && (long long)g.N * g.P * g.Q * g.K > 0) need(ws, "conv_fwd:ws");
     const long long out = (long long)g.N * g.P * g.Q * g.K;
     const long long red = (long long)g.R * g.S * g.C;
     int e = 0;

@@ -23,6 +23,8 @@ CASES = [
     ((2, 64, 9, 10), (136, 64, 1, 1), (1, 1), (0, 0)),
     ((1, 48, 12, 9), (72, 48, 5, 3), (3, 2), (2, 1)),
     ((2, 80, 20, 18), (264, 80, 3, 3), (1, 1), (1, 1)),   # several 256-wide tiles, ragged in M, N and k
+    ((2, 3, 30, 29), (16, 3, 7, 7), (2, 2), (3, 3)),      # 3 channels: zero-padded to 8 for the fast path
+    ((1, 12, 20, 18), (24, 12, 3, 3), (1, 1), (1, 1)),    # 12 channels: padded to 16
 ]
 
 
