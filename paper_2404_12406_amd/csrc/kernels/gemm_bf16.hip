@@ -158,6 +158,10 @@ struct Cfg {
     static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
     static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
     static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;
+    // forward: the block's bias columns, loaded once into LDS past the stages
+    // (one 16-byte load per lane of wave 0)
+    static constexpr int BIAS_OFF = LDS_BYTES;
+    static constexpr int SMEM_BYTES = LDS_BYTES + (MODE == kFwd ? 64 * 16 : 0);
     static constexpr int NIA = A_BYTES / 1024 / NW;   // load instructions per wave per tile
     static constexpr int NIB = B_BYTES / 1024 / NW;
     static constexpr int WM = BM / WR, WN = BN / WC;
@@ -168,7 +172,8 @@ struct Cfg {
     static_assert(NIA >= 1 && NIB >= 1 && NIA * NW * 1024 == A_BYTES && NIB * NW * 1024 == B_BYTES, "load split");
     static_assert(TM >= 1 && TN >= 1 && WM % 32 == 0 && WN % 32 == 0, "wave tile");
     static_assert(NW * EPI_ROWS * EPI_PITCH * 2 <= LDS_BYTES, "epilogue staging must fit in LDS");
-    static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+    static_assert(SMEM_BYTES <= 160 * 1024, "LDS");
+    static_assert(BN * 2 <= 64 * 16, "bias columns fit the bias area");
 };
 
 template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int OCC, bool UNIT>
@@ -176,7 +181,7 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
     using G = Cfg<MODE, BM, BN, WR, WC, STAGES>;
     constexpr int NIA = G::NIA, NIB = G::NIB, TM = G::TM, TN = G::TN, NSUB = G::NSUB;
     constexpr bool DG = MODE == kDgrad || MODE == kDgradN;
-    __shared__ __attribute__((aligned(1024))) char smem[G::LDS_BYTES];
+    __shared__ __attribute__((aligned(1024))) char smem[G::SMEM_BYTES];
 
     const ConvGeom &g = P.g;
     const int lane = threadIdx.x & 63;
@@ -568,6 +573,18 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
     };
     static_assert(NSUB % 2 == 0, "an even number of slices keeps the fragment buffers' roles fixed");
 
+    // Forward bias into LDS before the operand loads (so it is the oldest load
+    // of wave 0 and lands with stage 0).  Every block would otherwise read
+    // the same few bias lines in its epilogue, all at once.  Whole 16-byte
+    // chunks only: columns past N read as zeros.
+    bool bias_lds = false;
+    if constexpr (MODE == kFwd) {
+        bias_lds = P.bias != nullptr && P.N % 8 == 0;
+        if (bias_lds && wave == 0) {
+            const uint32_t off = (uint32_t)(n0 + lane * 8) * 2;
+            dma16(rsrc(P.bias, (uint32_t)P.N * 2), smem + G::BIAS_OFF, off);
+        }
+    }
 #pragma unroll
     for (int s2 = 0; s2 < STAGES; ++s2) issue(s2, k_begin + s2 * BK);
     wait_vmcnt<(STAGES - 1) * NVMEM>();
@@ -615,6 +632,7 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
                         if (n + 3 < N) {
                             *reinterpret_cast<floatx4 *>(W + (size_t)m * N + n) = o;
                         } else {
+#pragma unroll
                             for (int v = 0; v < 4; ++v)
                                 if (n + v < N) W[(size_t)m * N + n + v] = o[v];
                         }
@@ -639,7 +657,19 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
 #pragma unroll
             for (int v = 0; v < 4; ++v) bcol[j][q][v] = 0.f;
     if constexpr (MODE == kFwd) {
-        if (P.bias) {
+        if (bias_lds) {
+            // the bias area is past every stage and the staging rows; its
+            // DMA completed before the barrier above
+            const bf16 *bl = reinterpret_cast<const bf16 *>(smem + G::BIAS_OFF);
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const bf16x4 b4 = *reinterpret_cast<const bf16x4 *>(bl + wn0 + j * 32 + 8 * q + 4 * fh);
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) bcol[j][q][v] = (float)b4[v];
+                }
+        } else if (P.bias) {
 #pragma unroll
             for (int j = 0; j < TN; ++j)
 #pragma unroll
@@ -685,7 +715,12 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
             if (n + 8 <= N) {
                 *reinterpret_cast<u32x4 *>(dst) = v.u;
             } else {
-                for (int e = 0; e < 8 && n + e < N; ++e) dst[e] = v.e[e];
+                // constant indices only: a runtime index into v would make the
+                // compiler place v in LDS, addressed through the dispatch
+                // packet (a host-memory read per wave at the end of the kernel)
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (n + e < N) dst[e] = v.e[e];
             }
         }
         wait_lgkm0();   // reads done before the next pass overwrites
