@@ -120,24 +120,25 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_linear_stack_bf16_hbm_counte
 GEMM_SOURCES = ("paper_2404_12406_amd/csrc/kernels/gemm_bf16.hip", "paper_2404_12406_amd/csrc/kernels/common.h")
 
 
-def recorded_traffic():
-    """HBM bytes per forward-GEMM launch from the committed FETCH_SIZE /
-    WRITE_SIZE counter summary, or None when the GEMM sources changed since
-    the counters were taken (or the summary is absent)."""
+def recorded_traffic(key: str):
+    """HBM bytes per launch of the forward ("fwd") or input-gradient
+    ("dgrad") GEMM from the committed FETCH_SIZE / WRITE_SIZE counter
+    summary, or None when the GEMM sources changed since the counters were
+    taken (or the summary is absent)."""
     import hashlib
     try:
         text = open(TRAFFIC_FILE).read()
     except OSError:
         return None
-    fields = dict(l.split(": ", 1) for l in text.splitlines() if l.startswith(("traffic_bytes_per_launch: ",
-                                                                                 "kernel_sources_sha256: ")))
+    field = f"traffic_bytes_per_launch_{key}: "
+    fields = dict(l.split(": ", 1) for l in text.splitlines() if l.startswith((field, "kernel_sources_sha256: ")))
     h = hashlib.sha256()
     for p in GEMM_SOURCES:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
-    if fields.get("kernel_sources_sha256", "").strip() != h.hexdigest():
+    if fields.get("kernel_sources_sha256", "").strip() != h.hexdigest() or field[:-2] not in fields:
         return None
-    return int(fields["traffic_bytes_per_launch"])
+    return int(fields[field[:-2]])
 
 
 # ------------------------------------------------------------------ headline
@@ -175,7 +176,7 @@ def headline(steps, warmup):
     for name, kind, key in (("forward", ms.PROF_FWD, "fwd"), ("input-gradient", ms.PROF_DGRAD, "dgrad")):
         n, tot = ms.profile_read(kind)
         flop = sum(f[key] for f in fl) * steps
-        kern[key] = {"name": name, "launches": n, "ms": tot, "flop": flop}
+        kern[key] = {"name": name, "key": key, "launches": n, "ms": tot, "flop": flop}
     ms.profile_start(0)
     dom = max(kern.values(), key=lambda k: k["ms"])
     assert dom["launches"] == steps * len(w.layers), dom
@@ -203,7 +204,7 @@ def headline(steps, warmup):
         "flop_step": flop_step,
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": recorded_traffic() if dom["name"] == "forward" else None,
+                     "traffic": recorded_traffic(dom["key"]),
                      "kernel": f"ms::g2::gemm_kernel ({dom['name']} GEMM of the Linear layers)",
                      "flop_per_launch": dom["flop"] // dom["launches"], "avg_launch_us": round(avg_ms * 1e3, 2),
                      "launches": dom["launches"]},

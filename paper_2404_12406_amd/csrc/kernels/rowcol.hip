@@ -124,6 +124,35 @@ __global__ __launch_bounds__(256) void bn_fwd_flat_kernel(const T *__restrict__ 
     }
 }
 
+// One row vector of the reduction.  x comes as a value with a flag and the
+// dgamma term is accumulated without a branch: a pointer to x that may be
+// null, or a conditional update inside the unrolled loop, left the
+// accumulators in per-lane scratch memory.
+template <typename T, int V, int MODE>
+__device__ __forceinline__ void rc_row(const VecT<T, V> &va, const VecT<T, V> &vx, bool use_x, T *__restrict__ dx,
+                                       int64_t off, const float (&s)[V], const float (&mu)[V],
+                                       const float (&inv)[V], float (&acc_b)[V], float (&acc_g)[V]) {
+    if constexpr (MODE == 0) {
+#pragma unroll
+        for (int e = 0; e < V; ++e) acc_b[e] += to_f32(va.e[e]);
+    } else {
+        if (dx) {
+            VecT<T, V> o;
+#pragma unroll
+            for (int e = 0; e < V; ++e) o.e[e] = from_f32<T>(to_f32(va.e[e]) * s[e]);
+            o.store(dx + off);
+        }
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            const float d = to_f32(va.e[e]);
+            acc_b[e] += d;
+            // branch-free: acc_g is written out only when use_x
+            const float xh = use_x ? (to_f32(vx.e[e]) - mu[e]) * inv[e] : 0.f;
+            acc_g[e] += d * xh;
+        }
+    }
+}
+
 // ------------------------------------------- BN-eval bwd / column sums (partials)
 // MODE 0: column sums of a (bias gradient): part0[by][c] = sum a
 // MODE 1: BN-eval backward: dx = a*s (if dx), part0 = sum a*(x-mu)*inv (if want_g),
@@ -163,41 +192,24 @@ __global__ __launch_bounds__(256) void rowcol_reduce_kernel(
         const int64_t r1 = min(rows, r0 + chunk);
         int64_t r = r0 + rg;
         constexpr int U = 8;
-        auto body = [&](const VecT<T, V> &va, const VecT<T, V> *vx, int64_t rr) {
-            if constexpr (MODE == 0) {
-#pragma unroll
-                for (int e = 0; e < V; ++e) acc_b[e] += to_f32(va.e[e]);
-            } else {
-                if (dx) {
-                    VecT<T, V> o;
-#pragma unroll
-                    for (int e = 0; e < V; ++e) o.e[e] = from_f32<T>(to_f32(va.e[e]) * s[e]);
-                    o.store(dx + rr * C + c0);
-                }
-#pragma unroll
-                for (int e = 0; e < V; ++e) {
-                    const float d = to_f32(va.e[e]);
-                    acc_b[e] += d;
-                    if (vx) acc_g[e] += d * ((to_f32(vx->e[e]) - mu[e]) * inv[e]);
-                }
-            }
-        };
+        const bool use_x = MODE == 1 && want_g;
         for (; r + (U - 1) * RG < r1; r += U * RG) {
-            VecT<T, V> va[U], vx[U];
+            VecT<T, V> va[U], vx[U] = {};
 #pragma unroll
             for (int u = 0; u < U; ++u) va[u].load(a + (r + u * RG) * C + c0);
-            if (MODE == 1 && want_g) {
+            if (use_x) {
 #pragma unroll
                 for (int u = 0; u < U; ++u) vx[u].load(x + (r + u * RG) * C + c0);
             }
 #pragma unroll
-            for (int u = 0; u < U; ++u) body(va[u], (MODE == 1 && want_g) ? &vx[u] : nullptr, r + u * RG);
+            for (int u = 0; u < U; ++u)
+                rc_row<T, V, MODE>(va[u], vx[u], use_x, dx, (r + u * RG) * C + c0, s, mu, inv, acc_b, acc_g);
         }
         for (; r < r1; r += RG) {
-            VecT<T, V> va, vx;
+            VecT<T, V> va, vx = {};
             va.load(a + r * C + c0);
-            if (MODE == 1 && want_g) vx.load(x + r * C + c0);
-            body(va, (MODE == 1 && want_g) ? &vx : nullptr, r);
+            if (use_x) vx.load(x + r * C + c0);
+            rc_row<T, V, MODE>(va, vx, use_x, dx, r * C + c0, s, mu, inv, acc_b, acc_g);
         }
     }
     const bool need_b = MODE == 0 || want_b;
