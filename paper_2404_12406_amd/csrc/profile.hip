@@ -36,8 +36,11 @@ hipEvent_t take_event() {
         g_pool.pop_back();
         return e;
     }
+    // timing only: no system-scope fence (cache writeback and invalidate)
+    // when the event completes, so the pair measures the kernel and not the
+    // fence, and the following work is not slowed by it
     hipEvent_t e = nullptr;
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
     return e;
 }
 
@@ -60,7 +63,7 @@ void prof_mark(unsigned kind, void *stream, bool begin) {
         if (l.begin.size() >= kMaxLaunches) return;
         hipEvent_t e = take_event();
         if (!e) return;
-        hipEventRecord(e, (hipStream_t)stream);
+        (void)hipEventRecord(e, (hipStream_t)stream);
         l.begin.push_back(e);
         g_open[k] = true;
     } else {
@@ -70,7 +73,7 @@ void prof_mark(unsigned kind, void *stream, bool begin) {
             g_pool.push_back(l.begin.back());
             l.begin.pop_back();
         } else {
-            hipEventRecord(e, (hipStream_t)stream);
+            (void)hipEventRecord(e, (hipStream_t)stream);
             l.end.push_back(e);
         }
         g_open[k] = false;
@@ -81,7 +84,7 @@ int prof_start(unsigned kinds) {
     std::lock_guard<std::mutex> lk(g_mu);
     for (int i = 0; i < kKinds; ++i) {
         // events of the previous session may still be pending on a stream
-        for (hipEvent_t e : g_log[i].end) hipEventSynchronize(e);
+        for (hipEvent_t e : g_log[i].end) (void)hipEventSynchronize(e);
         recycle(g_log[i]);
         g_open[i] = false;
     }
