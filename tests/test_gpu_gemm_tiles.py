@@ -84,3 +84,40 @@ def test_linear_tiles(tile, shape, dgrad_variant):
     check("dX", host(gx), oracle.linear_input_grad(gy, w), "bf16")
     check("dW", host(gw), oracle.linear_weight_grad(gy, x), "bf16")
     check("db", host(gb), oracle.linear_bias_grad(gy), "bf16")
+
+
+@pytest.mark.parametrize("tile", TILES, indirect=True)
+@pytest.mark.parametrize("shape", [(300, 72, 136), (520, 264, 392), (1000, 520, 64), (4100, 64, 1032)])
+def test_linear_tiles_bias_without_weight_gradient(tile, shape, dgrad_variant):
+    """Mask input + bias (weight frozen, the fine-tuning mask): the input
+    gradient on every tile next to the separate bias column sum, with rows
+    ragged against every block height and reductions ragged against the
+    64-deep step."""
+    M, Kin, Nout = shape
+    seed = 7700 + M
+    x = synth.normal((M, Kin), seed, dtype="bf16")
+    w = synth.normal((Nout, Kin), seed + 1, 0.05, dtype="bf16")
+    b = synth.normal((Nout,), seed + 2, 0.02, dtype="bf16")
+    y, rec = ms.layer_forward(ms.Linear(), dev(x, "bf16"), dev(w, "bf16"), dev(b, "bf16"), 5)
+    gy = synth.normal((M, Nout), seed + 3, dtype="bf16")
+    gx, gw, gb = ms.layer_backward(rec, dev(gy, "bf16"))
+    assert gw is None
+    check("dX", host(gx), oracle.linear_input_grad(gy, w), "bf16")
+    check("db", host(gb), oracle.linear_bias_grad(gy), "bf16")
+
+
+@pytest.mark.parametrize("tile", TILES, indirect=True)
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_conv_tiles_bias_without_weight_gradient(tile, case, dgrad_variant):
+    """Mask input + bias on every conv case and tile."""
+    xs, ws, stride, pad = CASES[case]
+    seed = 7800 + 10 * case
+    x = synth.normal(xs, seed, dtype="bf16")
+    w = synth.kaiming_uniform(ws, seed + 1, ws[1] * ws[2] * ws[3], dtype="bf16")
+    b = synth.normal((ws[0],), seed + 2, 0.1, dtype="bf16")
+    y, rec = ms.layer_forward(ms.Conv2d(stride, pad), dev(x, "bf16"), dev(w, "bf16"), dev(b, "bf16"), 5)
+    gy = synth.normal(tuple(y.shape), seed + 3, dtype="bf16")
+    gx, gw, gb = ms.layer_backward(rec, dev(gy, "bf16"))
+    assert gw is None
+    check("dx", host(gx), oracle.conv2d_input_grad(gy, w, xs, stride, pad), "bf16")
+    check("db", host(gb), oracle.conv2d_bias_grad(gy), "bf16")
