@@ -55,13 +55,14 @@ struct Args {
     const bf16 *a;
     const bf16 *b;
     bf16 *c;              // output (or nullptr when the output is fp32 partials)
-    float *part;          // WGRAD split-K partials [splits][M][N]
+    float *part;          // split-K partials: part_stride floats per split (nullptr: splits == 1)
     float *dbpart;        // WGRAD fused bias-gradient partials [splits][M] (nullptr: off)
+    int64_t part_stride;  // FWD/WGRAD: M*N; DGRAD: N*H*W*C (partials indexed by dx pixel)
     const bf16 *bias;     // FWD bias (nullptr: none)
     ConvGeom g;
     int M, N, K;          // GEMM extents (DGRAD: bounds over phases)
     int ntm, ntn;
-    int k_split, splits;
+    int k_split, splits;  // reduction range per split (a multiple of BK) and split count
     uint32_t a_bytes, b_bytes;
 };
 
@@ -189,17 +190,24 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
     const int wm0 = (wave / WC) * G::WM, wn0 = (wave % WC) * G::WN;
 
     int M = P.M, Kg = P.K, ntm = P.ntm;
+    // grid z = (stride phase, split): the input gradient runs one GEMM per
+    // phase, and each split reduces over its own range of k
+    // (the in-place input-gradient variant never splits: its largest tile
+    // has no registers to spare)
+    constexpr bool SPLIT = MODE != kDgradN;
+    const int zsplit = SPLIT ? (int)blockIdx.z % P.splits : 0;
+    const int zphase = SPLIT ? (int)blockIdx.z / P.splits : (int)blockIdx.z;
     Phase f{};
     if constexpr (DG) {
-        f = make_phase(g, blockIdx.z);
+        f = make_phase(g, zphase);
         M = g.N * f.Hp * f.Wp;
         Kg = f.Rp * f.Sp * g.K;
         ntm = (M + BM - 1) / BM;
     }
     const int N = P.N;
     int k_begin = 0, k_end = Kg;
-    if constexpr (MODE == kWgrad) {
-        k_begin = blockIdx.z * P.k_split;
+    if (SPLIT && P.splits > 1) {
+        k_begin = min(Kg, zsplit * P.k_split);
         k_end = min(Kg, k_begin + P.k_split);
     }
     int tm, tn;
@@ -608,38 +616,46 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
             float v = dbacc[i];
             v += __shfl_xor(v, 32);
             const int m = m0 + wm0 + i * 32 + fr;
-            if (fh == 0 && m < M) P.dbpart[(size_t)blockIdx.z * M + m] = v;
+            if (fh == 0 && m < M) P.dbpart[(size_t)zsplit * M + m] = v;
         }
     }
 
     // ------------------------------------------------ epilogue
     // lane holds, for MFMA tile (i, j) and register group q = 0..3,
     // D[m = wm0 + 32i + lane%32][n = wn0 + 32j + 8q + 4*(lane/32) + 0..3]
-    if constexpr (MODE == kWgrad) {
-        if (P.splits > 1) {
-            float *W = P.part + (size_t)blockIdx.z * M * N;
+    // split-K: fp32 partials of this split (no bias; the reduce adds it).
+    // Rows of the input gradient go to their dx pixel, so the phases of a
+    // strided layer fill disjoint rows of one [N*H*W][C] array per split.
+    if (SPLIT && P.splits > 1) {
+        float *W = P.part + (size_t)zsplit * (size_t)P.part_stride;
 #pragma unroll
-            for (int i = 0; i < TM; ++i) {
-                const int m = m0 + wm0 + i * 32 + fr;
-                if (m >= M) continue;
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const int n = n0 + wn0 + j * 32 + 8 * q + 4 * fh;
-                        const floatx4 o = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
-                                           acc[i][j][4 * q + 3]};
-                        if (n + 3 < N) {
-                            *reinterpret_cast<floatx4 *>(W + (size_t)m * N + n) = o;
-                        } else {
-#pragma unroll
-                            for (int v = 0; v < 4; ++v)
-                                if (n + v < N) W[(size_t)m * N + n + v] = o[v];
-                        }
-                    }
+        for (int i = 0; i < TM; ++i) {
+            const int m = m0 + wm0 + i * 32 + fr;
+            if (m >= M) continue;
+            size_t row = (size_t)m;
+            if constexpr (DG && !UNIT) {
+                const int HW = f.Hp * f.Wp;
+                const int nimg = m / HW, ij = m - nimg * HW;
+                const int i2 = ij / f.Wp, j2 = ij - i2 * f.Wp;
+                row = (size_t)(nimg * g.H + f.h0 + i2 * g.sh) * g.W + f.w0 + j2 * g.sw;
             }
-            return;
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int n = n0 + wn0 + j * 32 + 8 * q + 4 * fh;
+                    const floatx4 o = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                       acc[i][j][4 * q + 3]};
+                    if (n + 3 < N && (N & 3) == 0) {
+                        *reinterpret_cast<floatx4 *>(W + row * N + n) = o;
+                    } else {
+#pragma unroll
+                        for (int v = 0; v < 4; ++v)
+                            if (n + v < N) W[row * N + n + v] = o[v];
+                    }
+                }
         }
+        return;
     }
     __syncthreads();   // every wave is done with the operand stages
     bf16 *stage = reinterpret_cast<bf16 *>(smem) + wave * G::EPI_ROWS * G::EPI_PITCH;
@@ -806,21 +822,28 @@ __global__ __launch_bounds__(256) void crop_channels_kernel(const bf16 *__restri
     }
 }
 
-// Sum split-K partials (and fused bias-gradient partials) to bf16.
+// Sum split-K partials (and fused bias-gradient partials) to bf16; with a
+// bias, out[i] also gets bias[i % ncol] (added in fp32 before the rounding).
 __global__ __launch_bounds__(256) void reduce_kernel(const float *__restrict__ part, int splits, int64_t n,
-                                                     bf16 *__restrict__ out, const float *__restrict__ dbpart,
-                                                     int M, bf16 *__restrict__ db) {
+                                                     int64_t pstride, bf16 *__restrict__ out, const float *__restrict__ dbpart,
+                                                     int M, bf16 *__restrict__ db, const bf16 *__restrict__ bias,
+                                                     int ncol) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int64_t nv = n / 4;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nv; i += stride) {
         floatx4 s = *reinterpret_cast<const floatx4 *>(part + 4 * i);
-        for (int z = 1; z < splits; ++z) s += *reinterpret_cast<const floatx4 *>(part + (int64_t)z * n + 4 * i);
+        for (int z = 1; z < splits; ++z) s += *reinterpret_cast<const floatx4 *>(part + (int64_t)z * pstride + 4 * i);
+        if (bias) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) s[e] += (float)bias[(4 * i + e) % ncol];
+        }
 #pragma unroll
         for (int e = 0; e < 4; ++e) out[4 * i + e] = (bf16)s[e];
     }
     for (int64_t i = 4 * nv + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
         float s = 0.f;
-        for (int z = 0; z < splits; ++z) s += part[(int64_t)z * n + i];
+        for (int z = 0; z < splits; ++z) s += part[(int64_t)z * pstride + i];
+        if (bias) s += (float)bias[i % ncol];
         out[i] = (bf16)s;
     }
     if (dbpart) {
@@ -910,6 +933,84 @@ Tile pick(long M, long N, long K, int splits_allowed, int *splits_out, int z = 1
     return bt;
 }
 
+// ---------------------------------------------------------------- forward / input-gradient planner
+// Estimated run time (microseconds) of a GEMM of M x N x K (z independent
+// GEMMs of that bound, the stride phases of an input gradient) on tile t
+// with the reduction split `splits` ways.  Per BK step a block takes the
+// longer of its MFMA time (shared with the blocks resident on its CU) and
+// the load latency its LDS ring can hide (STAGES - 1 tiles in flight); a
+// wave of blocks also pays a fixed start/drain cost, every output byte is
+// written once (fp32 partials when split), and a split adds the reduce pass.
+// Constants come from kernel traces of the Linear and conv workloads: a
+// 256 x 256 x 64 step of the 8-wave tile takes 1.5 us, a load round trip
+// about 1 us.
+constexpr double kUnitsPerUs = 2.33e6;   // bm*bn*k per us at relative efficiency 1
+constexpr double kLoadUs = 1.0;          // HBM/L2 round trip of a stage's loads
+constexpr double kWaveUs = 5.0;          // start + epilogue + drain of one wave of blocks
+constexpr double kBytesPerUs = 6.0e6;    // streamed HBM bytes per us
+constexpr double kLaunchUs = 3.0;
+
+double est_us(const Tile &t, long M, long N, long K, int z, int splits) {
+    const long tiles = ((M + t.bm - 1) / t.bm) * ((N + t.bn - 1) / t.bn) * z;
+    const long blocks = tiles * splits;
+    const long conc = (long)kCUs * t.per_cu;
+    const long waves = (blocks + conc - 1) / conc;
+    const long resident = std::min<long>(t.per_cu, (blocks + kCUs - 1) / kCUs);
+    const long kper = ((K + splits - 1) / splits + BK - 1) / BK * BK;
+    const double eff = resident > 1 ? t.eff : t.eff1;
+    const double t_mfma = (double)resident * t.bm * t.bn * BK / (kUnitsPerUs * eff);
+    const double t_lat = kLoadUs / (t.stages - 1);
+    const double step = std::max(t_mfma, t_lat);
+    const double out_elems = (double)M * N * z;
+    double us = waves * ((double)(kper / BK) * step + kWaveUs) + out_elems * (splits > 1 ? 4.0 * splits : 2.0) / kBytesPerUs;
+    if (splits > 1) us += kLaunchUs + out_elems * (4.0 * splits + 2.0) / kBytesPerUs;
+    return us;
+}
+
+// MEMSAVE_GEMM_SPLITS=<n> forces the split count of the forward and
+// input-gradient contractions (a testing knob, like MEMSAVE_GEMM_TILE).
+int forced_splits() {
+    const char *e = getenv("MEMSAVE_GEMM_SPLITS");
+    if (!e || !*e) return 0;
+    const int v = atoi(e);
+    return v >= 1 ? std::min(v, 64) : 0;
+}
+
+struct GemmPlan {
+    Tile t;
+    int splits, k_split;
+};
+
+// Tile and split count for the forward (z = 1) or input gradient (z stride
+// phases) with at most max_splits splits of at least 4 BK steps each.
+GemmPlan plan_gemm(long M, long N, long K, int z, int split_cap = 16) {
+    const int forced = forced_tile(), fs = split_cap > 1 ? forced_splits() : 0;
+    const int max_splits = (int)std::max<long>(1, std::min<long>(split_cap, K / (4 * BK)));
+    double best = 1e300;
+    GemmPlan bp{kTiles[0], 1, (int)K};
+    for (int ti = 0; ti < kNumTiles; ++ti) {
+        if (forced >= 0 ? ti != forced : !kAuto[ti]) continue;
+        for (int sp = 1; sp <= (fs ? 1 : max_splits); ++sp) {
+            const int splits = fs ? fs : sp;
+            const double us = est_us(kTiles[ti], M, N, K, z, splits);
+            if (us < best * 0.999) {
+                best = us;
+                bp.t = kTiles[ti];
+                bp.splits = splits;
+            }
+        }
+    }
+    long k_split = (K + bp.splits - 1) / bp.splits;
+    k_split = std::max<long>(BK, (k_split + BK - 1) / BK * BK);
+    bp.k_split = (int)k_split;
+    bp.splits = K > 0 ? (int)((K + k_split - 1) / k_split) : 1;
+    if (fs) bp.splits = fs;   // forced: keep the count even if some splits are empty
+    return bp;
+}
+
+// floats of one split's partials (a multiple of 4: 16-byte aligned splits)
+int64_t part_stride(int64_t elems) { return (elems + 3) / 4 * 4; }
+
 template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int OCC, bool UNIT>
 int go(const Args &a, dim3 grid, hipStream_t st) {
     const unsigned pk = MODE == kFwd ? kProfFwd : MODE == kWgrad ? kProfWgrad : kProfDgrad;
@@ -991,11 +1092,34 @@ WgradPlan wgrad_plan(const ConvGeom &g) {
 }  // namespace
 
 // Each returns -1 when the fast path does not apply, else a hipError_t.
-// Forward with C % 8 != 0: padded copies of x and W (workspace below).
+
+// Sum `splits` partial arrays of n floats (pstride apart) to bf16 `out`,
+// adding bias[i % ncol] when bias is given.
+int reduce_partials(const float *part, int splits, int64_t n, int64_t pstride, bf16 *out, const bf16 *bias, int ncol,
+                    hipStream_t st) {
+    const int blocks = (int)std::max<int64_t>(1, std::min<int64_t>((n / 4 + 255) / 256, 4096));
+    hipLaunchKernelGGL(reduce_kernel, dim3(blocks), dim3(256), 0, st, part, splits, n, pstride, out,
+                       (const float *)nullptr, 0, (bf16 *)nullptr, bias, ncol);
+    return (int)hipGetLastError();
+}
+
+GemmPlan fwd_plan(const ConvGeom &g) {
+    return plan_gemm((long)g.N * g.P * g.Q, g.K, (long)g.R * g.S * g.C, 1);
+}
+
+size_t fwd_split_bytes(const ConvGeom &g) {
+    const GemmPlan p = fwd_plan(g);
+    if (p.splits <= 1) return 0;
+    return al256((size_t)p.splits * part_stride((int64_t)g.N * g.P * g.Q * g.K) * sizeof(float));
+}
+
+// Forward with C % 8 != 0: padded copies of x and W, then the workspace of
+// the padded contraction (split-K partials).
 size_t fwd_workspace(const ConvGeom &g) {
-    if (g.C % 8 == 0) return 0;
+    if (g.C % 8 == 0) return fwd_split_bytes(g);
     const int C8 = pad8(g.C);
-    return al256((size_t)g.N * g.H * g.W * C8 * 2) + al256((size_t)g.K * g.R * g.S * C8 * 2);
+    return al256((size_t)g.N * g.H * g.W * C8 * 2) + al256((size_t)g.K * g.R * g.S * C8 * 2) +
+           fwd_split_bytes(padded(g));
 }
 
 int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, void *y, void *ws, hipStream_t st) {
@@ -1004,22 +1128,34 @@ int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, 
         const ConvGeom g8 = padded(g);
         char *xp = static_cast<char *>(ws);
         char *wp = xp + al256((size_t)g.N * g.H * g.W * g8.C * 2);
+        char *ws2 = wp + al256((size_t)g.K * g.R * g.S * g8.C * 2);
         int err = pad_channels(x, (int64_t)g.N * g.H * g.W, g.C, xp, st);
         if (!err) err = pad_channels(w, (int64_t)g.K * g.R * g.S, g.C, wp, st);
         if (err) return err;
-        return conv_fwd(g8, xp, wp, bias, y, nullptr, st);
+        return conv_fwd(g8, xp, wp, bias, y, ws2, st);
     }
     if (!al16(x) || !al16(w) || !al16(y)) return -1;
     Args a{};
-    a.a = (const bf16 *)x; a.b = (const bf16 *)w; a.c = (bf16 *)y; a.bias = (const bf16 *)bias; a.g = g;
+    a.a = (const bf16 *)x; a.b = (const bf16 *)w; a.c = (bf16 *)y; a.g = g;
     a.M = g.N * g.P * g.Q; a.N = g.K; a.K = g.R * g.S * g.C;
     if (a.M == 0 || a.N == 0) return 0;
-    Tile t = pick(a.M, a.N, a.K, 1, nullptr);
-    a.ntm = (a.M + t.bm - 1) / t.bm; a.ntn = (a.N + t.bn - 1) / t.bn;
-    a.splits = 1; a.k_split = a.K;
+    const GemmPlan p = fwd_plan(g);
+    if (p.splits > 1 && (!ws || !al16(ws))) return -1;
+    a.ntm = (a.M + p.t.bm - 1) / p.t.bm; a.ntn = (a.N + p.t.bn - 1) / p.t.bn;
+    a.splits = p.splits; a.k_split = p.k_split;
     a.a_bytes = bytes_of((long)g.N * g.H * g.W * g.C);
     a.b_bytes = bytes_of((long)g.K * a.K);
-    return go_mode<kFwd>(t, a, dim3(a.ntm * a.ntn, 1, 1), unit_geom(g), st);
+    const int64_t n = (int64_t)a.M * a.N;
+    if (p.splits > 1) {
+        a.part = static_cast<float *>(ws);
+        a.part_stride = part_stride(n);
+        a.c = nullptr;
+    } else {
+        a.bias = (const bf16 *)bias;
+    }
+    int err = go_mode<kFwd>(p.t, a, dim3(a.ntm * a.ntn, 1, p.splits), unit_geom(g), st);
+    if (err || p.splits <= 1) return err;
+    return reduce_partials(a.part, p.splits, n, a.part_stride, (bf16 *)y, (const bf16 *)bias, a.N, st);
 }
 
 // Input gradient through a transposed copy of W (both operands K-contiguous,
@@ -1032,16 +1168,35 @@ bool dgrad_direct(const ConvGeom &g) {
     return false;
 }
 
+// GEMM bounds of the input gradient over the stride phases: ceil(H/sh) x
+// ceil(W/sw) rows per image, ceil(R/sh) x ceil(S/sw) taps.
+GemmPlan dgrad_plan(const ConvGeom &g) {
+    const long Hb = (g.H + g.sh - 1) / g.sh, Wb = (g.W + g.sw - 1) / g.sw;
+    const long Kb = (long)((g.R + g.sh - 1) / g.sh) * ((g.S + g.sw - 1) / g.sw) * g.K;
+    GemmPlan p = plan_gemm((long)g.N * Hb * Wb, g.C, Kb, g.sh * g.sw);
+    if (dgrad_direct(g)) {   // the in-place variant does not split
+        p = plan_gemm((long)g.N * Hb * Wb, g.C, Kb, g.sh * g.sw, 1);
+    }
+    return p;
+}
+
+// transposed filter (when used), then split-K partials indexed by dx pixel
+size_t dgrad_core_workspace(const ConvGeom &g) {
+    size_t ws = dgrad_direct(g) ? 0 : al256((size_t)g.K * g.R * g.S * g.C * sizeof(bf16));
+    const GemmPlan p = dgrad_plan(g);
+    if (p.splits > 1) ws += al256((size_t)p.splits * part_stride((int64_t)g.N * g.H * g.W * g.C) * sizeof(float));
+    return ws;
+}
+
 size_t dgrad_workspace(const ConvGeom &g) {
     if (g.K % 8 != 0) return 0;
     if (g.C % 8 != 0) {
         // padded W, padded dx, then the workspace of the padded contraction
         const ConvGeom g8 = padded(g);
         return al256((size_t)g.K * g.R * g.S * g8.C * 2) + al256((size_t)g.N * g.H * g.W * g8.C * 2) +
-               dgrad_workspace(g8);
+               dgrad_core_workspace(g8);
     }
-    if (dgrad_direct(g)) return 0;
-    return (size_t)g.K * g.R * g.S * g.C * sizeof(bf16) + 256;
+    return dgrad_core_workspace(g);
 }
 
 int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, void *ws, hipStream_t st) {
@@ -1060,26 +1215,38 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, void 
     }
     if (!al16(dy) || !al16(w) || !al16(dx)) return -1;
     const bool direct = dgrad_direct(g);
-    if (!direct && (!ws || !al16(ws))) return -1;
+    const GemmPlan p = dgrad_plan(g);
+    if ((!direct || p.splits > 1) && (!ws || !al16(ws))) return -1;
+    char *wsc = static_cast<char *>(ws);
+    bf16 *wt = direct ? nullptr : reinterpret_cast<bf16 *>(wsc);
+    float *part = nullptr;
+    if (p.splits > 1) part = reinterpret_cast<float *>(wsc + (direct ? 0 : al256((size_t)g.K * g.R * g.S * g.C * sizeof(bf16))));
     Args a{};
-    a.a = (const bf16 *)dy; a.b = direct ? (const bf16 *)w : (const bf16 *)ws; a.c = (bf16 *)dx; a.g = g;
+    a.a = (const bf16 *)dy; a.b = direct ? (const bf16 *)w : wt; a.c = (bf16 *)dx; a.g = g;
     const int Hb = (g.H + g.sh - 1) / g.sh, Wb = (g.W + g.sw - 1) / g.sw;
     a.M = g.N * Hb * Wb; a.N = g.C;
     a.K = ((g.R + g.sh - 1) / g.sh) * ((g.S + g.sw - 1) / g.sw) * g.K;
     if (a.M == 0 || a.N == 0) return 0;
     if (!direct) {
         hipLaunchKernelGGL(transpose_krsc_kernel, dim3((g.C + 63) / 64, (g.K + 63) / 64, g.R * g.S), dim3(256), 0, st,
-                           (const bf16 *)w, (bf16 *)ws, g.K, g.R * g.S, g.C);
+                           (const bf16 *)w, wt, g.K, g.R * g.S, g.C);
         const int err = (int)hipGetLastError();
         if (err) return err;
     }
-    Tile t = pick(a.M, a.N, a.K, 1, nullptr, g.sh * g.sw);
-    a.ntm = (a.M + t.bm - 1) / t.bm; a.ntn = (a.N + t.bn - 1) / t.bn;
-    a.splits = 1; a.k_split = a.K;
+    a.ntm = (a.M + p.t.bm - 1) / p.t.bm; a.ntn = (a.N + p.t.bn - 1) / p.t.bn;
+    a.splits = p.splits; a.k_split = p.k_split;
     a.a_bytes = bytes_of((long)g.N * g.P * g.Q * g.K);
     a.b_bytes = bytes_of((long)g.K * g.R * g.S * g.C);
-    const dim3 grid(a.ntm * a.ntn, 1, g.sh * g.sw);
-    return direct ? go_mode<kDgradN>(t, a, grid, unit_geom(g), st) : go_mode<kDgrad>(t, a, grid, unit_geom(g), st);
+    const int64_t n = (int64_t)g.N * g.H * g.W * g.C;
+    if (p.splits > 1) {
+        a.part = part;
+        a.part_stride = part_stride(n);
+        a.c = nullptr;
+    }
+    const dim3 grid(a.ntm * a.ntn, 1, g.sh * g.sw * p.splits);
+    int err = direct ? go_mode<kDgradN>(p.t, a, grid, unit_geom(g), st) : go_mode<kDgrad>(p.t, a, grid, unit_geom(g), st);
+    if (err || p.splits <= 1) return err;
+    return reduce_partials(part, p.splits, n, a.part_stride, (bf16 *)dx, nullptr, 1, st);
 }
 
 bool wgrad_applies(const ConvGeom &g) { return g.K % 8 == 0; }
@@ -1124,6 +1291,7 @@ int conv_wgrad(const ConvGeom &g, const void *dy, const void *x, void *dw, void 
     size_t used = 0;
     if (p.splits > 1) {
         a.part = wsf;
+        a.part_stride = (int64_t)a.M * a.N;
         used = (size_t)p.splits * a.M * a.N;
         a.c = nullptr;
     } else {
@@ -1137,8 +1305,8 @@ int conv_wgrad(const ConvGeom &g, const void *dy, const void *x, void *dw, void 
     if (p.splits > 1 || db) {
         const int64_t n = p.splits > 1 ? (int64_t)a.M * a.N : 0;
         const int blocks = (int)std::max<int64_t>(1, std::min<int64_t>((n / 4 + 255) / 256, 2048));
-        hipLaunchKernelGGL(reduce_kernel, dim3(blocks), dim3(256), 0, st, (const float *)a.part, p.splits, n,
-                           (bf16 *)dw, (const float *)a.dbpart, db ? a.M : 0, (bf16 *)db);
+        hipLaunchKernelGGL(reduce_kernel, dim3(blocks), dim3(256), 0, st, (const float *)a.part, p.splits, n, n,
+                           (bf16 *)dw, (const float *)a.dbpart, db ? a.M : 0, (bf16 *)db, (const bf16 *)nullptr, 1);
         err = (int)hipGetLastError();
     }
     return err;

@@ -33,6 +33,8 @@ struct RowColPlan {
     int64_t chunk;  // rows per block (y)
 };
 
+constexpr int kRowsPerThread = 8;   // the unroll of the reduction's row loop
+
 RowColPlan plan_rowcol(int dtype, int64_t rows, int C, bool vec_ok, int target_blocks) {
     RowColPlan p;
     const int V = dtype == kBF16 ? 8 : 4;
@@ -45,8 +47,9 @@ RowColPlan plan_rowcol(int dtype, int64_t rows, int C, bool vec_ok, int target_b
     p.RG = 256 / p.TC;
     p.gx = (p.nvc + p.TC - 1) / p.TC;
     int64_t want_y = std::max<int64_t>(1, target_blocks / p.gx);
-    // at least 16 rows per thread, so the partials stay small next to the input
-    int64_t max_y = std::max<int64_t>(1, rows / (int64_t)(p.RG * 16));
+    // at least one batch of kRowsPerThread rows per thread (all its loads in
+    // flight at once), so the partials stay small next to the input
+    int64_t max_y = std::max<int64_t>(1, rows / (int64_t)(p.RG * kRowsPerThread));
     p.gy = (int)std::max<int64_t>(1, std::min<int64_t>(want_y, max_y));
     p.gy = std::min(p.gy, 65535);
     p.chunk = (rows + p.gy - 1) / p.gy;
@@ -191,7 +194,7 @@ __global__ __launch_bounds__(256) void rowcol_reduce_kernel(
         const int64_t r0 = (int64_t)blockIdx.y * chunk;
         const int64_t r1 = min(rows, r0 + chunk);
         int64_t r = r0 + rg;
-        constexpr int U = 8;
+        constexpr int U = kRowsPerThread;
         const bool use_x = MODE == 1 && want_g;
         for (; r + (U - 1) * RG < r1; r += U * RG) {
             VecT<T, V> va[U], vx[U] = {};

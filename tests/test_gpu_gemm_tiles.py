@@ -121,3 +121,59 @@ def test_conv_tiles_bias_without_weight_gradient(tile, case, dgrad_variant):
     assert gw is None
     check("dx", host(gx), oracle.conv2d_input_grad(gy, w, xs, stride, pad), "bf16")
     check("db", host(gb), oracle.conv2d_bias_grad(gy), "bf16")
+
+
+@pytest.fixture
+def splits(request):
+    """Force the split count of the forward and input-gradient GEMMs
+    (MEMSAVE_GEMM_SPLITS): fp32 partials summed by a second pass, the
+    forward bias added there."""
+    old = os.environ.get("MEMSAVE_GEMM_SPLITS")
+    os.environ["MEMSAVE_GEMM_SPLITS"] = request.param
+    yield request.param
+    if old is None:
+        del os.environ["MEMSAVE_GEMM_SPLITS"]
+    else:
+        os.environ["MEMSAVE_GEMM_SPLITS"] = old
+
+
+@pytest.mark.parametrize("splits", ["3"], indirect=True)
+@pytest.mark.parametrize("tile", TILES, indirect=True)
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_conv_tiles_split(tile, case, splits):
+    """Split reductions on every conv case and tile: strided input
+    gradients put each phase's partial rows at their own dx pixels, and
+    splits past a short reduction contribute zeros."""
+    xs, ws, stride, pad = CASES[case]
+    seed = 7900 + 10 * case
+    x = synth.normal(xs, seed, dtype="bf16")
+    w = synth.kaiming_uniform(ws, seed + 1, ws[1] * ws[2] * ws[3], dtype="bf16")
+    b = synth.normal((ws[0],), seed + 2, 0.1, dtype="bf16")
+    y, rec = ms.layer_forward(ms.Conv2d(stride, pad), dev(x, "bf16"), dev(w, "bf16"), dev(b, "bf16"), 7)
+    check("y", host(y), oracle.conv2d_forward(x, w, b, stride, pad), "bf16")
+    gy = synth.normal(tuple(y.shape), seed + 3, dtype="bf16")
+    gx, gw, gb = ms.layer_backward(rec, dev(gy, "bf16"))
+    check("dx", host(gx), oracle.conv2d_input_grad(gy, w, xs, stride, pad), "bf16")
+    check("dW", host(gw), oracle.conv2d_weight_grad(gy, x, ws, stride, pad), "bf16")
+    check("db", host(gb), oracle.conv2d_bias_grad(gy), "bf16")
+
+
+@pytest.mark.parametrize("splits", ["2", "5"], indirect=True)
+@pytest.mark.parametrize("tile", TILES, indirect=True)
+@pytest.mark.parametrize("shape", [(300, 72, 136), (520, 264, 392), (1000, 520, 64), (300, 72, 138)])
+def test_linear_tiles_split(tile, shape, splits):
+    """Split reductions of the Linear forward (bias added by the reduce) and
+    input gradient; N_out = 138 leaves rows of partials that are not whole
+    16-byte vectors (the input gradient then takes the general kernel)."""
+    M, Kin, Nout = shape
+    seed = 7600 + M + Nout
+    x = synth.normal((M, Kin), seed, dtype="bf16")
+    w = synth.normal((Nout, Kin), seed + 1, 0.05, dtype="bf16")
+    b = synth.normal((Nout,), seed + 2, 0.02, dtype="bf16")
+    y, rec = ms.layer_forward(ms.Linear(), dev(x, "bf16"), dev(w, "bf16"), dev(b, "bf16"), 5)
+    check("y", host(y), oracle.linear_forward(x, w, b), "bf16")
+    gy = synth.normal((M, Nout), seed + 3, dtype="bf16")
+    gx, gw, gb = ms.layer_backward(rec, dev(gy, "bf16"))
+    assert gw is None
+    check("dX", host(gx), oracle.linear_input_grad(gy, w), "bf16")
+    check("db", host(gb), oracle.linear_bias_grad(gy), "bf16")
