@@ -89,11 +89,44 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *p, uint32_t b
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
 }
 
-// One 16-byte LDS-DMA load.  The offset is computed into a named value first:
-// passing a conditional expression straight into the builtin inside a kernel
-// template makes the host pass drop the kernel's launch stub.
+// One 16-byte LDS-DMA load: lane l's 16 bytes from byte offset `off` of the
+// buffer land at lds + 16 l (M0 holds the wave's LDS base).
+//
+// Contractions with an M/N-contiguous operand (ASM = true) issue it through
+// inline assembly so that the compiler does not track it: for a pending
+// LDS-DMA load the compiler puts a wait for every outstanding vector-memory
+// operation in front of each transposing LDS read (ds_read_b64_tr_b16),
+// which drains all refill loads in flight at every slice.  The others keep
+// the builtin, whose loads the scheduler can spread between the MFMAs.
+// Ordering in the assembly form is the kernel's own:
+//  * completion: its vmcnt waits before each barrier;
+//  * a refill writes a stage no wave reads until after the next barrier, and
+//    a volatile asm statement never moves across the barrier;
+//  * block_sync() tells the compiler that LDS may have changed, so no LDS
+//    value read before a barrier is reused after it.
+// M0 is reserved by the compiler and no other instruction of these kernels
+// reads it.
+// (The offset is computed into a named value first: passing a conditional
+// expression straight into the builtin inside a kernel template makes the
+// host pass drop the kernel's launch stub.)
+template <bool ASM>
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, char *lds, uint32_t off) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t *)lds, 16, off, 0, 0, 0);
+    if constexpr (ASM) {
+        const uint32_t base = (uint32_t)(uintptr_t)(lds_void_t *)lds;
+        asm volatile("s_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %0, %2, 0 offen lds" ::"v"(off), "s"(base), "s"(r));
+    } else {
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t *)lds, 16, off, 0, 0, 0);
+    }
+}
+
+// Workgroup barrier; with untracked LDS-DMA loads it is also a compiler-level
+// memory fence (the barrier builtin alone does not stop the compiler from
+// keeping LDS values across it).
+template <bool ASM>
+__device__ __forceinline__ void block_sync() {
+    if constexpr (ASM) __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    if constexpr (ASM) __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
 // s_waitcnt with only vmcnt constrained (gfx9 encoding: vmcnt[3:0] | [15:14],
@@ -110,12 +143,16 @@ __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xc07f
 // 16-byte bank groups (the LDS serves 256 bytes per clock).
 __device__ __forceinline__ int swz_k(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 
-// Slot swizzle of an M/N-contiguous tile k-row ([k][mn], 16-byte slots):
-// XOR with an even value so the two slots one transposed read touches stay
-// adjacent.
+// Slot swizzle of an M/N-contiguous tile k-row ([k][mn], 16-byte slots).
+// A transposed read serves 32 lanes at a time: two 16-lane groups that each
+// read 4 k-rows x 2 adjacent slots, the second group 2 slots to the right.
+// Rows of 16 or more slots start on the same bank, so the XOR must spread
+// the 4 rows by 4 slots (the 32 lanes then cover 16 distinct slots = all 64
+// banks); rows of 8 slots alternate between the two bank halves and an XOR
+// by 2 suffices.  Both keep the slot pair of a group adjacent.
 template <int SPR>
 __device__ __forceinline__ int swz_m(int krow) {
-    if constexpr (SPR >= 16) return ((krow & 3) | (((krow >> 3) & 1) << 2)) << 1;
+    if constexpr (SPR >= 16) return (krow & 3) << 2;
     else return (krow & 3) << 1;
 }
 
@@ -182,6 +219,9 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
     using G = Cfg<MODE, BM, BN, WR, WC, STAGES>;
     constexpr int NIA = G::NIA, NIB = G::NIB, TM = G::TM, TN = G::TN, NSUB = G::NSUB;
     constexpr bool DG = MODE == kDgrad || MODE == kDgradN;
+    // LDS-DMA issue form (see dma16): assembly when an operand is read with
+    // transposing LDS reads
+    constexpr bool ASM_DMA = !(G::A_KC && G::B_KC);
     __shared__ __attribute__((aligned(1024))) char smem[G::SMEM_BYTES];
 
     const ConvGeom &g = P.g;
@@ -359,7 +399,7 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
                     off = a_base[j] + (p * g.Q + q) * g.K + off_k[v];
                 }
                 const uint32_t boff = ok ? (uint32_t)off * 2u : kOOB;
-                if (j >= lo && j < hi) dma16(ra, sA + (wave * NIA + j) * 1024, boff);
+                if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
             }
         } else {
             constexpr int SPR = BM / 8, KPI = 64 / SPR;
@@ -368,7 +408,7 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
                 const int kk = k0 + (wave * NIA + j) * KPI + lane / SPR;
                 const bool ok = a_ok[j] && kk < k_end;
                 const uint32_t boff = ok ? ((uint32_t)kk * (uint32_t)g.K + a_mn_off[j]) * 2u : kOOB;
-                if (j >= lo && j < hi) dma16(ra, sA + (wave * NIA + j) * 1024, boff);
+                if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
             }
         }
         // ---- B
@@ -392,7 +432,7 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
                 const int v = (wave * NIB + j) & 1;
                 const bool ok = kin[v] && b_ok[j];
                 const uint32_t boff = ok ? (uint32_t)(b_base[j] + off_k[v]) * 2u : kOOB;
-                if (NIA + j >= lo && NIA + j < hi) dma16(rb, sB + (wave * NIB + j) * 1024, boff);
+                if (NIA + j >= lo && NIA + j < hi) dma16<ASM_DMA>(rb, sB + (wave * NIB + j) * 1024, boff);
             }
         } else {
             constexpr int SPR = BN / 8, KPI = 64 / SPR;
@@ -422,7 +462,7 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
                     off = (uint32_t)(((n * g.H + ih) * g.W + iw) * g.C) + b_mn_off[j];
                 }
                 const uint32_t boff = ok ? off * 2u : kOOB;
-                if (NIA + j >= lo && NIA + j < hi) dma16(rb, sB + (wave * NIB + j) * 1024, boff);
+                if (NIA + j >= lo && NIA + j < hi) dma16<ASM_DMA>(rb, sB + (wave * NIB + j) * 1024, boff);
             }
         }
     };
@@ -527,7 +567,7 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
             } else {
                 wait_vmcnt<(STAGES - 2) * NVMEM>();
                 wait_lgkm0();
-                __builtin_amdgcn_s_barrier();
+                block_sync<ASM_DMA>();
                 __builtin_amdgcn_sched_barrier(0);
                 read_sub((kt + 1) % STAGES, 0, na, nb);
                 mfma_sub(ca, cb);
@@ -556,7 +596,7 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
         __builtin_amdgcn_sched_barrier(0);
         wait_vmcnt<0>();                     // slice 2: tile kt+1 landed, tile kt read by all
         wait_lgkm0();
-        __builtin_amdgcn_s_barrier();
+        block_sync<ASM_DMA>();
         __builtin_amdgcn_sched_barrier(0);
         issue_range(s, rk, 0, HALF);
         read_sub(s1, 0, fa1, fb1);
@@ -590,13 +630,13 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
         bias_lds = P.bias != nullptr && P.N % 8 == 0;
         if (bias_lds && wave == 0) {
             const uint32_t off = (uint32_t)(n0 + lane * 8) * 2;
-            dma16(rsrc(P.bias, (uint32_t)P.N * 2), smem + G::BIAS_OFF, off);
+            dma16<ASM_DMA>(rsrc(P.bias, (uint32_t)P.N * 2), smem + G::BIAS_OFF, off);
         }
     }
 #pragma unroll
     for (int s2 = 0; s2 < STAGES; ++s2) issue(s2, k_begin + s2 * BK);
     wait_vmcnt<(STAGES - 1) * NVMEM>();
-    __builtin_amdgcn_s_barrier();
+    block_sync<ASM_DMA>();
     read_sub(0, 0, fa0, fb0);
     if constexpr (SPREAD) {
         for (int kt = 0; kt < nk; ++kt) step_spread(kt);
@@ -983,13 +1023,16 @@ struct GemmPlan {
 
 // Tile and split count for the forward (z = 1) or input gradient (z stride
 // phases) with at most max_splits splits of at least 4 BK steps each.
-GemmPlan plan_gemm(long M, long N, long K, int z, int split_cap = 16) {
-    const int forced = forced_tile(), fs = split_cap > 1 ? forced_splits() : 0;
+GemmPlan plan_gemm(long M, long N, long K, int z, int split_cap = 16, bool allow_256x256 = true) {
+    int forced = forced_tile();
+    if (forced == 0 && !allow_256x256) forced = 1;   // the next widest tile (256 x 128)
+    const int fs = split_cap > 1 ? forced_splits() : 0;
     const int max_splits = (int)std::max<long>(1, std::min<long>(split_cap, K / (4 * BK)));
     double best = 1e300;
     GemmPlan bp{kTiles[0], 1, (int)K};
     for (int ti = 0; ti < kNumTiles; ++ti) {
         if (forced >= 0 ? ti != forced : !kAuto[ti]) continue;
+        if (ti == 0 && !allow_256x256) continue;
         for (int sp = 1; sp <= (fs ? 1 : max_splits); ++sp) {
             const int splits = fs ? fs : sp;
             const double us = est_us(kTiles[ti], M, N, K, z, splits);
@@ -1021,9 +1064,17 @@ int go(const Args &a, dim3 grid, hipStream_t st) {
     return err;
 }
 
+// The strided input gradient has no 256 x 256 instantiation (its pixel
+// mapping leaves that tile short of registers); the planner never picks it.
+template <int MODE, bool UNIT>
+constexpr bool has_256x256() { return !(MODE == kDgrad && !UNIT); }
+
 template <int MODE, bool UNIT>
 int go_tile(const Tile &t, const Args &a, dim3 grid, hipStream_t st) {
-    if (t.bm == 256 && t.bn == 256) return go<MODE, 256, 256, 2, 4, 2, 1, UNIT>(a, grid, st);
+    if (t.bm == 256 && t.bn == 256) {
+        if constexpr (has_256x256<MODE, UNIT>()) return go<MODE, 256, 256, 2, 4, 2, 1, UNIT>(a, grid, st);
+        else return (int)hipErrorInvalidValue;
+    }
     if (t.bm == 256 && t.bn == 128) return go<MODE, 256, 128, 2, 4, 3, 1, UNIT>(a, grid, st);
     if (t.bm == 128 && t.bn == 128 && t.wc == 4) return go<MODE, 128, 128, 2, 4, 2, 2, UNIT>(a, grid, st);
     if (t.bm == 128 && t.bn == 128 && t.stages == 4) return go<MODE, 128, 128, 2, 2, 4, 1, UNIT>(a, grid, st);
@@ -1158,32 +1209,42 @@ int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, 
     return reduce_partials(a.part, p.splits, n, a.part_stride, (bf16 *)y, (const bf16 *)bias, a.N, st);
 }
 
-// Input gradient through a transposed copy of W (both operands K-contiguous,
-// the faster contraction) or straight from W (no copy, no extra kernel).
+// Input gradient either straight from W (filter read in place through
+// transposing LDS reads; no copy, no extra kernel, no split) or through a
+// transposed copy Wt[C][R][S][K] (both operands K-contiguous).  An 8-wave
+// tile hides the transposing reads (within 2% of the copy's contraction), so
+// W is read in place unless the plan wants a 4-wave tile (which does not) or
+// a split reduction (which only the copy's contraction has).  The strided
+// variant through the copy has no 256 x 256 tile.
 // MEMSAVE_DGRAD=transposed|direct overrides the choice (testing knob).
-bool dgrad_direct(const ConvGeom &g) {
-    const char *e = getenv("MEMSAVE_DGRAD");
-    if (e && *e) return e[0] == 'd';
-    (void)g;
-    return false;
-}
+struct DgradChoice {
+    bool direct;
+    GemmPlan p;
+};
 
-// GEMM bounds of the input gradient over the stride phases: ceil(H/sh) x
-// ceil(W/sw) rows per image, ceil(R/sh) x ceil(S/sw) taps.
-GemmPlan dgrad_plan(const ConvGeom &g) {
+DgradChoice dgrad_choice(const ConvGeom &g) {
+    // GEMM bounds over the stride phases: ceil(H/sh) x ceil(W/sw) rows per
+    // image, ceil(R/sh) x ceil(S/sw) taps
     const long Hb = (g.H + g.sh - 1) / g.sh, Wb = (g.W + g.sw - 1) / g.sw;
     const long Kb = (long)((g.R + g.sh - 1) / g.sh) * ((g.S + g.sw - 1) / g.sw) * g.K;
-    GemmPlan p = plan_gemm((long)g.N * Hb * Wb, g.C, Kb, g.sh * g.sw);
-    if (dgrad_direct(g)) {   // the in-place variant does not split
-        p = plan_gemm((long)g.N * Hb * Wb, g.C, Kb, g.sh * g.sw, 1);
+    const long M = (long)g.N * Hb * Wb;
+    const int z = g.sh * g.sw;
+    const char *e = getenv("MEMSAVE_DGRAD");
+    if (e && *e) {
+        const bool direct = e[0] == 'd';
+        return {direct, plan_gemm(M, g.C, Kb, z, direct ? 1 : 16, direct || unit_geom(g))};
     }
-    return p;
+    const GemmPlan pd = plan_gemm(M, g.C, Kb, z, 1, true);
+    const GemmPlan pt = plan_gemm(M, g.C, Kb, z, 16, unit_geom(g));
+    if (pd.t.wr * pd.t.wc == 8 && pt.splits == 1) return {true, pd};
+    return {false, pt};
 }
 
 // transposed filter (when used), then split-K partials indexed by dx pixel
 size_t dgrad_core_workspace(const ConvGeom &g) {
-    size_t ws = dgrad_direct(g) ? 0 : al256((size_t)g.K * g.R * g.S * g.C * sizeof(bf16));
-    const GemmPlan p = dgrad_plan(g);
+    const DgradChoice dc = dgrad_choice(g);
+    const GemmPlan &p = dc.p;
+    size_t ws = dc.direct ? 0 : al256((size_t)g.K * g.R * g.S * g.C * sizeof(bf16));
     if (p.splits > 1) ws += al256((size_t)p.splits * part_stride((int64_t)g.N * g.H * g.W * g.C) * sizeof(float));
     return ws;
 }
@@ -1214,8 +1275,9 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, void 
         return crop_channels(dxp, (int64_t)g.N * g.H * g.W, g.C, dx, st);
     }
     if (!al16(dy) || !al16(w) || !al16(dx)) return -1;
-    const bool direct = dgrad_direct(g);
-    const GemmPlan p = dgrad_plan(g);
+    const DgradChoice dc = dgrad_choice(g);
+    const bool direct = dc.direct;
+    const GemmPlan &p = dc.p;
     if ((!direct || p.splits > 1) && (!ws || !al16(ws))) return -1;
     char *wsc = static_cast<char *>(ws);
     bf16 *wt = direct ? nullptr : reinterpret_cast<bf16 *>(wsc);
