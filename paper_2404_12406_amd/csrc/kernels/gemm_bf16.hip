@@ -188,9 +188,13 @@ __device__ __forceinline__ bf16x8 frag_kc(const char *base, int row, int sub, in
     return *reinterpret_cast<const bf16x8 *>(base + off);
 }
 
-template <int MODE, int BM, int BN, int WR, int WC, int STAGES>
+// KG k-groups of WR x WC waves: group g computes the whole block tile from
+// the 16-k slices 2g and 2g+1 of every BK step (KG = 2), and the groups add
+// their accumulators through LDS at the end.  Each wave then keeps a 64 x 64
+// tile (one fragment read per MFMA) with two waves per SIMD.
+template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int KG = 1>
 struct Cfg {
-    static constexpr int NW = WR * WC, NT = NW * 64;
+    static constexpr int NW = WR * WC * KG, NT = NW * 64;
     static constexpr bool A_KC = MODE != kWgrad;
     static constexpr bool B_KC = MODE == kFwd || MODE == kDgrad;   // kDgrad: W transposed to [C][R][S][K]
     static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
@@ -212,11 +216,13 @@ struct Cfg {
     static_assert(NW * EPI_ROWS * EPI_PITCH * 2 <= LDS_BYTES, "epilogue staging must fit in LDS");
     static_assert(SMEM_BYTES <= 160 * 1024, "LDS");
     static_assert(BN * 2 <= 64 * 16, "bias columns fit the bias area");
+    static_assert(KG == 1 || (KG == 2 && STAGES >= 3 && MODE != kWgrad), "k-groups: spread pipeline, no weight gradient");
+    static_assert(KG == 1 || (WR * WC) * (WM / 32) * (WN / 32) * 16 * 64 * 4 <= LDS_BYTES, "k-group partials fit LDS");
 };
 
-template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int OCC, bool UNIT>
-__global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
-    using G = Cfg<MODE, BM, BN, WR, WC, STAGES>;
+template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int OCC, bool UNIT, int KG = 1>
+__global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args P) {
+    using G = Cfg<MODE, BM, BN, WR, WC, STAGES, KG>;
     constexpr int NIA = G::NIA, NIB = G::NIB, TM = G::TM, TN = G::TN, NSUB = G::NSUB;
     constexpr bool DG = MODE == kDgrad || MODE == kDgradN;
     // LDS-DMA issue form (see dma16): assembly when an operand is read with
@@ -227,7 +233,8 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
     const ConvGeom &g = P.g;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform: LDS bases stay scalar
-    const int wm0 = (wave / WC) * G::WM, wn0 = (wave % WC) * G::WN;
+    const int wl = wave % (WR * WC), kg = wave / (WR * WC);   // wave within its k-group, k-group
+    const int wm0 = (wl / WC) * G::WM, wn0 = (wl % WC) * G::WN;
 
     int M = P.M, Kg = P.K, ntm = P.ntm;
     // grid z = (stride phase, split): the input gradient runs one GEMM per
@@ -620,6 +627,33 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
         }
     };
     static_assert(NSUB % 2 == 0, "an even number of slices keeps the fragment buffers' roles fixed");
+    // two k-groups (three or more stages): group kg does slices 2kg and
+    // 2kg+1 of each step.  On entry (fa0, fb0) hold slice 2kg of tile kt.
+    // The refill of the stage step kt-1 consumed is split over the two
+    // halves; the wait before the barrier leaves the loads of tiles kt+2 ..
+    // kt+STAGES-1 in flight, so tile kt+1 has landed.
+    auto step_kg = [&](int kt) {
+        const int s = kt % STAGES;
+        const int rs = (kt + STAGES - 1) % STAGES;
+        const int rk = k_begin + (kt - 1 + STAGES) * BK;
+        const bool refill = kt >= 1;
+        constexpr int HALF = (NVMEM + 1) / 2;
+        __builtin_amdgcn_sched_barrier(0);
+        if (refill) issue_range(rs, rk, 0, HALF);
+        read_sub(s, 2 * kg + 1, fa1, fb1);
+        mfma_sub(fa0, fb0);
+        interleave(HALF);
+        __builtin_amdgcn_sched_barrier(0);
+        if (refill) issue_range(rs, rk, HALF, NVMEM);
+        wait_vmcnt<(STAGES - 2) * NVMEM>();
+        wait_lgkm0();
+        block_sync<ASM_DMA>();
+        __builtin_amdgcn_sched_barrier(0);
+        read_sub((kt + 1) % STAGES, 2 * kg, fa0, fb0);
+        mfma_sub(fa1, fb1);
+        interleave(NVMEM - HALF);
+        __builtin_amdgcn_sched_barrier(0);
+    };
 
     // Forward bias into LDS before the operand loads (so it is the oldest load
     // of wave 0 and lands with stage 0).  Every block would otherwise read
@@ -637,8 +671,10 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
     for (int s2 = 0; s2 < STAGES; ++s2) issue(s2, k_begin + s2 * BK);
     wait_vmcnt<(STAGES - 1) * NVMEM>();
     block_sync<ASM_DMA>();
-    read_sub(0, 0, fa0, fb0);
-    if constexpr (SPREAD) {
+    read_sub(0, KG == 2 ? 2 * kg : 0, fa0, fb0);
+    if constexpr (KG == 2) {
+        for (int kt = 0; kt < nk; ++kt) step_kg(kt);
+    } else if constexpr (SPREAD) {
         for (int kt = 0; kt < nk; ++kt) step_spread(kt);
     } else {
         static_assert(NSUB == 4, "the two-stage schedule is written for four slices per step");
@@ -648,6 +684,31 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
     // the refills of the last steps are still writing into LDS: drain them
     // before LDS is reused or the workgroup ends
     wait_vmcnt<0>();
+
+    // ------------------------------------------------ k-groups: add group 1's accumulators to group 0's
+    if constexpr (KG == 2) {
+        float *red = reinterpret_cast<float *>(smem);
+        __syncthreads();   // every wave is done with the operand stages
+        if (kg == 1) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) red[(((wl * TM + i) * TN + j) * 16 + v) * 64 + lane] = acc[i][j][v];
+        }
+        __syncthreads();
+        if (kg == 0) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) acc[i][j][v] += red[(((wl * TM + i) * TN + j) * 16 + v) * 64 + lane];
+        }
+        __syncthreads();   // the partials are read before the epilogue reuses LDS
+        if (kg == 1) return;
+    }
 
     // ------------------------------------------------ fused bias-gradient partials
     if (db_on) {
@@ -697,7 +758,7 @@ __global__ __launch_bounds__(WR * WC * 64, OCC) void gemm_kernel(const Args P) {
         }
         return;
     }
-    __syncthreads();   // every wave is done with the operand stages
+    if constexpr (KG == 1) __syncthreads();   // every wave is done with the operand stages
     bf16 *stage = reinterpret_cast<bf16 *>(smem) + wave * G::EPI_ROWS * G::EPI_PITCH;
     constexpr int SEG = G::WN / 8;                   // 16-byte segments per staged row
     constexpr int ROWS_PER_PASS = 64 / SEG;
@@ -913,6 +974,7 @@ struct Tile {
     int per_cu;       // blocks resident per CU
     float eff1;       // relative MFMA efficiency with one block on the CU
     float eff;        // ... with per_cu blocks on the CU
+    int kg = 1;       // k-groups of wr x wc waves (the block has wr * wc * kg waves)
 };
 // Efficiencies measured on the Linear and encoder shapes: a 2-stage
 // 128 x 128 block alone on a CU cannot hide its load latency (a co-resident
@@ -924,14 +986,17 @@ constexpr Tile kTiles[] = {
     {"128x128w8", 128, 128, 2, 4, 2, 2, 0.85f, 1.02f},    // 8 waves of 64 x 32, 64 KB, two blocks per CU
     {"128x128s4", 128, 128, 2, 2, 4, 1, 0.90f, 0.90f},    // 4 waves of 64 x 64, 4 stages (128 KB)
     {"128x128w8s4", 128, 128, 2, 4, 4, 1, 0.90f, 0.90f},  // 8 waves of 64 x 32, 4 stages (128 KB)
+    {"128x128k2", 128, 128, 2, 2, 4, 1, 0.95f, 0.95f, 2},  // 2 k-groups of 4 waves of 64 x 64, 4 stages
     {"128x64", 128, 64, 2, 2, 2, 3, 0.75f, 0.75f},        // 4 waves of 64 x 32, 48 KB, three blocks per CU
 };
 constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 // tiles the planner chooses from
 // tiles the planner chooses from: the 4-wave 4-stage tile is kept for the
 // tests; its 8-wave twin was as fast or faster on every measured shape
-// (weight gradient 4096 x 1024 x 4096: 57 -> 46 us)
-constexpr bool kAuto[kNumTiles] = {true, true, true, true, false, true, true};
+// (weight gradient 4096 x 1024 x 4096: 57 -> 46 us), and the k-group tile
+// beats that one by ~5% on the forward and input gradient of 4096 x 1024
+// outputs with K = 4096 (38.7 -> 36.3 us)
+constexpr bool kAuto[kNumTiles] = {true, true, true, true, false, true, true, true};
 
 // MEMSAVE_GEMM_TILE=<name> forces one tile shape (a debugging and testing
 // knob); returns its index or -1.
@@ -993,7 +1058,8 @@ struct GemmPlan {
 
 // Tile and split count for the forward or weight gradient (z = 1) or the input gradient (z stride
 // phases) with at most max_splits splits of at least 4 BK steps each.
-GemmPlan plan_gemm(long M, long N, long K, int z, int split_cap = 16, bool allow_256x256 = true) {
+GemmPlan plan_gemm(long M, long N, long K, int z, int split_cap = 16, bool allow_256x256 = true,
+                   bool allow_kgroups = true) {
     int forced = forced_tile();
     if (forced == 0 && !allow_256x256) forced = 1;   // the next widest tile (256 x 128)
     const int fs = split_cap > 1 ? forced_splits() : 0;
@@ -1003,6 +1069,7 @@ GemmPlan plan_gemm(long M, long N, long K, int z, int split_cap = 16, bool allow
     for (int ti = 0; ti < kNumTiles; ++ti) {
         if (forced >= 0 ? ti != forced : !kAuto[ti]) continue;
         if (ti == 0 && !allow_256x256) continue;
+        if (kTiles[ti].kg > 1 && !allow_kgroups) continue;
         for (int sp = 1; sp <= (fs ? 1 : max_splits); ++sp) {
             const int splits = fs ? fs : sp;
             const double us = est_us(kTiles[ti], M, N, K, z, splits);
@@ -1024,11 +1091,11 @@ GemmPlan plan_gemm(long M, long N, long K, int z, int split_cap = 16, bool allow
 // floats of one split's partials (a multiple of 4: 16-byte aligned splits)
 int64_t part_stride(int64_t elems) { return (elems + 3) / 4 * 4; }
 
-template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int OCC, bool UNIT>
+template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int OCC, bool UNIT, int KG = 1>
 int go(const Args &a, dim3 grid, hipStream_t st) {
     const unsigned pk = MODE == kFwd ? kProfFwd : MODE == kWgrad ? kProfWgrad : kProfDgrad;
     prof_mark(pk, st, true);
-    hipLaunchKernelGGL((gemm_kernel<MODE, BM, BN, WR, WC, STAGES, OCC, UNIT>), grid, dim3(WR * WC * 64), 0, st, a);
+    hipLaunchKernelGGL((gemm_kernel<MODE, BM, BN, WR, WC, STAGES, OCC, UNIT, KG>), grid, dim3(WR * WC * KG * 64), 0, st, a);
     const int err = (int)hipGetLastError();
     prof_mark(pk, st, false);
     return err;
@@ -1046,6 +1113,12 @@ int go_tile(const Tile &t, const Args &a, dim3 grid, hipStream_t st) {
         else return (int)hipErrorInvalidValue;
     }
     if (t.bm == 256 && t.bn == 128) return go<MODE, 256, 128, 2, 4, 3, 1, UNIT>(a, grid, st);
+    if (t.kg == 2) {
+        if constexpr (MODE != kWgrad) {
+            if (t.bm == 128 && t.bn == 128) return go<MODE, 128, 128, 2, 2, 4, 1, UNIT, 2>(a, grid, st);
+        }
+        return (int)hipErrorInvalidValue;
+    }
     if (t.bm == 128 && t.bn == 128 && t.wc == 4 && t.stages == 4) return go<MODE, 128, 128, 2, 4, 4, 1, UNIT>(a, grid, st);
     if (t.bm == 128 && t.bn == 128 && t.wc == 4) return go<MODE, 128, 128, 2, 4, 2, 2, UNIT>(a, grid, st);
     if (t.bm == 128 && t.bn == 128 && t.stages == 4) return go<MODE, 128, 128, 2, 2, 4, 1, UNIT>(a, grid, st);
@@ -1113,6 +1186,7 @@ Tile pick_conv_wgrad(long M, long N, long K, int splits_allowed, int *splits_out
     for (int ti = 0; ti < kNumTiles; ++ti) {
         if (forced >= 0 ? ti != forced : !kAuto[ti]) continue;
         const Tile &t = kTiles[ti];
+        if (t.kg > 1) continue;   // no k-group tile for the weight gradient
         const long tiles = ((M + t.bm - 1) / t.bm) * ((N + t.bn - 1) / t.bn) * z;
         int splits = 1;
         if (splits_allowed > 1) {
@@ -1140,7 +1214,8 @@ Tile pick_conv_wgrad(long M, long N, long K, int splits_allowed, int *splits_out
 WgradPlan wgrad_plan(const ConvGeom &g) {
     const long M = g.K, N = (long)g.R * g.S * g.C, K = (long)g.N * g.P * g.Q;
     if (unit_geom(g)) {
-        const GemmPlan p = plan_gemm(M, N, K, 1);
+        // (the weight gradient has no k-group tile)
+        const GemmPlan p = plan_gemm(M, N, K, 1, 16, true, false);
         return {p.t, p.splits, p.k_split};
     }
     int splits = 1;
@@ -1251,7 +1326,7 @@ DgradChoice dgrad_choice(const ConvGeom &g) {
     }
     const GemmPlan pd = plan_gemm(M, g.C, Kb, z, 1, true);
     const GemmPlan pt = plan_gemm(M, g.C, Kb, z, 16, unit_geom(g));
-    if (pd.t.wr * pd.t.wc == 8 && pt.splits == 1) return {true, pd};
+    if (pd.t.wr * pd.t.wc * pd.t.kg == 8 && pt.splits == 1) return {true, pd};
     return {false, pt};
 }
 
