@@ -307,6 +307,60 @@ def bn_bandwidth(steps, warmup):
                       "frac_of_hbm": round(tot_b / (st * 1e-3) / 1e9 / PEAK_HBM_GBS, 4), "launches": len(layers)}}
 
 
+def relu_bandwidth(steps, warmup):
+    """ReLU with a 1-bit saved mask (Sec. 2.2.2) on the stem-output tensor of
+    the ResNet-18-shaped stack (64 x 64 x 112 x 112 bf16, channels-last).
+
+    HBM bytes per launch: forward reads x and writes y and the mask
+    (2 * 2 * n + n / 8), backward reads dy and the mask and writes dx (the
+    same).  Each launch is timed by the library's HIP events after a 512 MiB
+    read sweep evicts the cache.  Retained bytes: this library's mask, the
+    paper's one-byte boolean mask, stock PyTorch's saved output."""
+    import torch
+    import paper_2404_12406_amd as ms
+    shape = (64, 64, 112, 112)
+    n = 64 * 64 * 112 * 112
+    g = torch.Generator(device="cuda").manual_seed(4242)
+    x = torch.randn(shape, generator=g, device="cuda").to(torch.bfloat16).contiguous(memory_format=torch.channels_last)
+    gy = torch.randn(shape, generator=g, device="cuda").to(torch.bfloat16).contiguous(memory_format=torch.channels_last)
+    gx = torch.empty_like(x)
+    p = ms.PreparedLayer(ms.ReLU(), x, mask=ms.MASK_INPUT, grad_y=gy, grad_x=gx)
+    big = torch.ones(1 << 27, dtype=torch.float32, device="cuda")
+    for _ in range(max(1, warmup)):
+        p.forward()
+        p.backward()
+    torch.cuda.synchronize()
+    nbytes = 2 * 2 * n + n // 8
+    out = {"shape": list(shape), "dtype": "bf16", "bytes_per_launch": nbytes}
+    # forwards alone (a prepared layer frees its previous record itself), then
+    # forward + backward pairs: the backward time is the difference of the
+    # summed event times
+    ms.profile_start(ms.PROF_ACT)
+    for _ in range(steps):
+        big.sum()
+        p.forward()
+    torch.cuda.synchronize()
+    cnt, t_fwd = ms.profile_read(ms.PROF_ACT)
+    assert cnt == steps, (cnt, steps)
+    ms.profile_start(ms.PROF_ACT)
+    for _ in range(steps):
+        big.sum()
+        p.forward()
+        big.sum()
+        p.backward()
+    torch.cuda.synchronize()
+    cnt, t_both = ms.profile_read(ms.PROF_ACT)
+    ms.profile_start(0)
+    assert cnt == 2 * steps, (cnt, steps)
+    for name, ms_tot in (("forward", t_fwd), ("backward", t_both - t_fwd)):
+        us = ms_tot / steps * 1e3
+        out[name] = {"us": round(us, 2), "GBs": round(nbytes / (us * 1e-6) / 1e9, 1),
+                     "frac_of_hbm": round(nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+    out["saved_bytes"] = {"bits": ms.relu_mask_bytes(n), "one_byte_bool": n, "stock_output": 2 * n}
+    del big
+    return out
+
+
 def extras(steps, warmup):
     from synth import workloads as wl
     out = {}
@@ -326,6 +380,10 @@ def extras(steps, warmup):
     t0 = time.time()
     out["bn_eval_forward_resnet18_shaped"] = bn = bn_bandwidth(steps, warmup)
     log(f"[bench] bn: stack {bn['stack']['GBs']} GB/s, largest layer {bn['largest_layer']} ({time.time() - t0:.1f}s)")
+    t0 = time.time()
+    out["relu_bitmask_stem_output"] = rl = relu_bandwidth(steps, warmup)
+    log(f"[bench] relu: forward {rl['forward']}, backward {rl['backward']}, saved {rl['saved_bytes']} "
+        f"({time.time() - t0:.1f}s)")
     return out
 
 

@@ -84,7 +84,10 @@ typedef enum {
     MS_BN_EVAL = 2,      /* y = gamma (x - mean) / sqrt(var + eps) + beta per channel,
                             x[N,C,H,W] (channels-last) or x[N,C]; W = gamma[C], b = beta[C]
                             (both NULL for affine=False); running stats are fixed buffers  */
-    MS_AVGPOOL = 3       /* global average pool x[N,C,H,W] -> y[N,C]; no parameters        */
+    MS_AVGPOOL = 3,      /* global average pool x[N,C,H,W] -> y[N,C]; no parameters        */
+    MS_RELU = 4          /* y = max(x, 0) elementwise (NaN and -0 pass through); x 1-D
+                            contiguous, 2-D row-major or 4-D channels-last, y likewise; no
+                            parameters.  Forward through ms_relu_forward() only           */
 } ms_kind;
 
 typedef struct {
@@ -99,8 +102,11 @@ typedef struct {
 /* Opaque saved-tensor record (the AD tape entry of one layer call). */
 typedef struct ms_record ms_record;
 
-/* Bits of ms_account.borrowed: which caller tensors a record keeps. */
-enum { MS_SAVED_X = 1u, MS_SAVED_W = 2u, MS_SAVED_MEAN = 4u, MS_SAVED_VAR = 8u };
+/* Bits of ms_account.borrowed: which caller tensors a record keeps.
+ * MS_SAVED_BITS: a ReLU's 1-bit mask; MS_SAVED_Y (policy accounting only):
+ * the layer output, which stock PyTorch's ReLU keeps. */
+enum { MS_SAVED_X = 1u, MS_SAVED_W = 2u, MS_SAVED_MEAN = 4u, MS_SAVED_VAR = 8u, MS_SAVED_BITS = 16u,
+       MS_SAVED_Y = 32u };
 
 /* Bits of ms_account.kernels: what the record's backward will launch. */
 enum { MS_K_DGRAD = 1u, MS_K_WGRAD = 2u, MS_K_BGRAD = 4u };
@@ -143,6 +149,35 @@ enum {
 ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_tensor *W,
                            const ms_tensor *b, uint32_t mask, const ms_tensor *y,
                            ms_record **rec, void *stream);
+
+/*
+ * ms_relu_mask_bytes -- size of the mask ms_relu_forward() writes for an
+ * n-element tensor: 4 * ceil(n / 32) bytes (0 for n <= 0).  Bit i of the
+ * mask (bit i % 8 of byte i / 8) belongs to element i in memory order.
+ */
+uint64_t ms_relu_mask_bytes(int64_t n);
+
+/*
+ * ms_relu_forward -- y = max(x, 0), keeping one bit per element for backward.
+ *
+ * Sec. 2.2.2: an activation that stores its output keeps the next linear
+ * layer's input alive whatever that layer's mask, which cancels the saving
+ * of Sec. 2.2.1; the input gradient of ReLU needs only which outputs are
+ * positive.  The paper's ReLU keeps a one-byte boolean per element and names
+ * one-bit booleans as the next step; this one keeps one bit.
+ * mask: 0 or MS_RG_INPUT (MS_E_MASK otherwise).  x and y: same shape, dtype
+ * and layout (see MS_RELU); y is fully overwritten.  With INPUT set, `bits`
+ * is caller-allocated device memory of ms_relu_mask_bytes(numel) bytes,
+ * 4-byte aligned (MS_E_ARG otherwise), fully overwritten, and borrowed by
+ * *rec (it is the record's saved_activation_bytes) until backward or
+ * ms_record_free(); neither x nor y is kept.  With mask 0, bits may be NULL
+ * and *rec = NULL.  Backward is ms_layer_backward(rec, grad_y, grad_x, NULL,
+ * NULL, stream): grad_x[i] = bit i ? grad_y[i] : 0, where bit i = !(y_i <= 0)
+ * (a NaN output passes its gradient, as PyTorch's ReLU does).  ms_layer_forward()
+ * rejects MS_RELU (MS_E_ARG).
+ */
+ms_status ms_relu_forward(const ms_tensor *x, const ms_tensor *y, void *bits, uint32_t mask, ms_record **rec,
+                          void *stream);
 
 /*
  * ms_layer_backward -- write exactly the requested gradients for grad_y.
@@ -189,13 +224,14 @@ ms_status ms_policy_account(const ms_layer *layer, const ms_tensor *x, const ms_
  *   MS_PROF_DGRAD input-gradient GEMM
  *   MS_PROF_WGRAD weight-gradient GEMM (its split-K partial launch)
  *   MS_PROF_BN    BN-eval forward kernel
+ *   MS_PROF_ACT   ReLU forward and backward kernels
  * ms_profile_start() discards earlier records and arms `kinds` (0 disarms);
  * at most 65536 launches per kind are recorded.  ms_profile_read() waits
  * for the recorded events and returns the number of launches of one kind and
  * their summed duration in milliseconds.  Calls from several threads or
  * streams at once are serialised internally.
  */
-enum { MS_PROF_FWD = 1u, MS_PROF_DGRAD = 2u, MS_PROF_WGRAD = 4u, MS_PROF_BN = 8u };
+enum { MS_PROF_FWD = 1u, MS_PROF_DGRAD = 2u, MS_PROF_WGRAD = 4u, MS_PROF_BN = 8u, MS_PROF_ACT = 16u };
 ms_status ms_profile_start(uint32_t kinds);
 ms_status ms_profile_read(uint32_t kind, uint64_t *launches, double *total_ms);
 

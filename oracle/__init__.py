@@ -25,6 +25,7 @@ __all__ = [
     "linear_forward", "linear_forward_at", "linear_input_grad", "linear_input_grad_at",
     "linear_weight_grad", "linear_weight_grad_at", "linear_bias_grad",
     "bn_eval_forward", "bn_eval_backward", "avgpool_forward", "avgpool_backward",
+    "relu_forward", "relu_mask_bits", "relu_backward", "relu_mask_nbytes", "memory_order",
     "round_to", "rel_err",
 ]
 
@@ -262,6 +263,57 @@ def avgpool_backward(dy, x_shape):
 
 
 # ----------------------------------------------------------------- rounding, error
+# ---------------------------------------------------------------- ReLU (Sec. 2.2.2)
+# The activation whose stored output would keep the next linear layer's input
+# alive; its input gradient needs only which outputs are positive, so the
+# paper's version keeps a boolean mask of the output instead (one bit per
+# element here).  Written element by element from the definition:
+#   y = x if x >= 0 else 0      (a NaN stays NaN, as torch.relu keeps it)
+#   bit i = not (y_i <= 0)      in memory order, 8 per byte, bit e of byte j
+#                                is element 8 j + e; 4 * ceil(n / 32) bytes
+#   dx_i = dy_i if bit i else 0
+# (The paper does not treat NaN; a NaN output passes its gradient, as
+# PyTorch's ReLU backward does, whose layer this one replaces.)
+def relu_forward(x):
+    """y = max(x, 0) elementwise, exact (no rounding: y is a copy of x or 0)."""
+    x = np.asarray(x, dtype=np.float64)
+    y = x.copy()
+    y[x < 0] = 0.0
+    return y
+
+
+def memory_order(a, layout: str = "plain"):
+    """The elements of a logical-order array in the library's memory order:
+    "nhwc" for 4-D channels-last activations, "plain" for row-major."""
+    a = np.asarray(a)
+    if layout == "nhwc":
+        return np.transpose(a, (0, 2, 3, 1)).reshape(-1)
+    return a.reshape(-1)
+
+
+def relu_mask_nbytes(n: int) -> int:
+    return 4 * ((int(n) + 31) // 32) if n > 0 else 0
+
+
+def relu_mask_bits(x_mem):
+    """The 1-bit mask of a ReLU over the 1-D memory-order elements x_mem,
+    as uint8 bytes (bit e of byte j = not (relu(x)[8 j + e] <= 0))."""
+    x_mem = np.asarray(x_mem, dtype=np.float64).reshape(-1)
+    n = x_mem.size
+    out = np.zeros(relu_mask_nbytes(n), dtype=np.uint8)
+    pos = ~(relu_forward(x_mem) <= 0)
+    for i in np.nonzero(pos)[0]:
+        out[i // 8] |= np.uint8(1 << (int(i) % 8))
+    return out
+
+
+def relu_backward(dy, x):
+    """dx = dy where not relu(x) <= 0, else 0 (same logical shape as x)."""
+    dy = np.asarray(dy, dtype=np.float64)
+    pos = ~(relu_forward(x) <= 0)
+    return np.where(pos, dy, 0.0)
+
+
 def round_to(a, dtype):
     """Round float64 values once to 'f32' or 'bf16' (ties to even); float64 out."""
     a = np.array(a, dtype=np.float64, copy=True, order="C")

@@ -20,6 +20,12 @@ Comparison policies:
 Only non-parameter tensors count as retained activation bytes; parameters
 and running statistics are resident anyway and are reported separately.
 A mask of 0 creates no record at all (no node is recorded).
+
+ReLU (Sec. 2.2.2): stock PyTorch keeps the output, which may be the next
+linear layer's input; the paper's ReLU keeps a boolean mask of the output
+instead, one byte per element, and this library one bit per element (4-byte
+words: 4 * ceil(n / 32) bytes).  It has no parameters, so ALL_TRUE is its
+INPUT mask.
 """
 from __future__ import annotations
 
@@ -54,20 +60,33 @@ def saved_tensors(kind: str, mask: int, policy: int = SELECTIVE,
                 "running_var": i or w}
     if kind == "avgpool":
         return {"x": False}
+    if kind == "relu":
+        if policy == PYTORCH_DEFAULT:
+            return {"x": False, "y": i, "bits": False}
+        return {"x": False, "y": False, "bits": i}
     raise ValueError(kind)
+
+
+def relu_mask_bytes(numel: int) -> int:
+    """Bytes of a ReLU record's 1-bit mask."""
+    return 4 * ((int(numel) + 31) // 32) if numel > 0 else 0
 
 
 def saved_activation_bytes(kind: str, mask: int, x_numel: int, dtype: str,
                            policy: int = SELECTIVE, has_weight: bool = True,
                            has_bias: bool = True) -> int:
     st = saved_tensors(kind, mask, policy, has_weight, has_bias)
+    if kind == "relu":
+        if st["y"]:
+            return int(x_numel) * ELT[dtype]
+        return relu_mask_bytes(x_numel) if st["bits"] else 0
     return int(x_numel) * ELT[dtype] if st["x"] else 0
 
 
 def launched(kind: str, mask: int) -> Dict[str, bool]:
     """Backward launch plan: the input-, weight- and bias-gradient work runs
     exactly when its flag is set (Sec. 2.2.1)."""
-    if kind == "avgpool":
+    if kind in ("avgpool", "relu"):
         return {"dgrad": bool(mask & MASK_INPUT), "wgrad": False, "bgrad": False}
     return {"dgrad": bool(mask & MASK_INPUT), "wgrad": bool(mask & MASK_WEIGHT),
             "bgrad": bool(mask & MASK_BIAS)}

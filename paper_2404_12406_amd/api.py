@@ -18,9 +18,9 @@ from typing import Optional, Tuple
 import torch
 
 from . import _lib
-from ._lib import (MS_AVGPOOL, MS_BN_EVAL, MS_CONV2D, MS_LINEAR, MS_RG_BIAS, MS_RG_INPUT,
-                   MS_RG_WEIGHT, MS_SAVED_MEAN, MS_SAVED_VAR, MS_SAVED_W, MS_SAVED_X, MsAccount,
-                   MsLayer, MsTensor, check)
+from ._lib import (MS_AVGPOOL, MS_BN_EVAL, MS_CONV2D, MS_LINEAR, MS_RELU, MS_RG_BIAS, MS_RG_INPUT,
+                   MS_RG_WEIGHT, MS_SAVED_BITS, MS_SAVED_MEAN, MS_SAVED_VAR, MS_SAVED_W, MS_SAVED_X,
+                   MsAccount, MsLayer, MsTensor, check)
 
 MASK_INPUT, MASK_WEIGHT, MASK_BIAS = MS_RG_INPUT, MS_RG_WEIGHT, MS_RG_BIAS
 POLICY_SELECTIVE, POLICY_PYTORCH_DEFAULT, POLICY_ALL_TRUE = 0, 1, 2
@@ -52,6 +52,11 @@ class BatchNormEval:
 @dataclass(frozen=True)
 class AvgPool:
     """Global average pool x[N, C, H, W] -> y[N, C]."""
+
+
+@dataclass(frozen=True)
+class ReLU:
+    """y = max(x, 0); its record keeps one bit per element (y > 0), not y."""
 
 
 def _pair(v):
@@ -103,6 +108,8 @@ class _LayerDesc:
             self.layer.running_var = ctypes.pointer(self.var)
         elif isinstance(spec, AvgPool):
             self.layer.kind = MS_AVGPOOL
+        elif isinstance(spec, ReLU):
+            self.layer.kind = MS_RELU
         else:
             raise TypeError(f"unknown layer spec {spec!r}")
 
@@ -125,6 +132,8 @@ def output_shape(spec, x: torch.Tensor, W: Optional[torch.Tensor]):
         return tuple(x.shape)
     if isinstance(spec, AvgPool):
         return (x.shape[0], x.shape[1])
+    if isinstance(spec, ReLU):
+        return tuple(x.shape)
     raise TypeError(spec)
 
 
@@ -142,13 +151,15 @@ class Record:
     the tensors it borrows (so the caching allocator sees the same retained
     bytes as the ledger)."""
 
-    def __init__(self, handle: ctypes.c_void_p, desc: _LayerDesc, x, W, b, y_shape, y_like):
+    def __init__(self, handle: ctypes.c_void_p, desc: _LayerDesc, x, W, b, y_shape, y_like, bits=None):
         self._h = handle
         self._desc = desc
         acct = self.account()
         self.mask = acct["mask"]
         bor = acct["borrowed"]
         self._keep = {}
+        if bor & MS_SAVED_BITS:
+            self._keep["bits"] = bits
         if bor & MS_SAVED_X:
             self._keep["x"] = x
         if bor & MS_SAVED_W:
@@ -203,11 +214,42 @@ def _on_gpu(*ts):
         torch.cuda.set_device(dev)
 
 
+def relu_mask_bytes(numel: int) -> int:
+    """Bytes of the 1-bit mask a ReLU record keeps for `numel` elements."""
+    return int(_lib.load().ms_relu_mask_bytes(int(numel)))
+
+
+def relu_mask_buffer(x: torch.Tensor) -> torch.Tensor:
+    """A device buffer for the 1-bit mask of a ReLU over x (int32 words)."""
+    return torch.empty(relu_mask_bytes(x.numel()) // 4, dtype=torch.int32, device=x.device)
+
+
+def _relu_forward(lib, x, y, bits, mask):
+    h = ctypes.c_void_p()
+    st = lib.ms_relu_forward(_ptr(tensor_desc(x)), _ptr(tensor_desc(y)),
+                             ctypes.c_void_p(bits.data_ptr() if bits is not None and bits.numel() else None),
+                             int(mask), ctypes.byref(h), _stream(x.device))
+    check(st, "ms_relu_forward")
+    return h
+
+
 def layer_forward(spec, x: torch.Tensor, W: Optional[torch.Tensor] = None, b: Optional[torch.Tensor] = None,
                   mask: int = 0, y: Optional[torch.Tensor] = None):
     """Run the layer's forward kernel on the current stream; return (y, record).
-    record is None when mask == 0 (nothing is saved)."""
+    record is None when mask == 0 (nothing is saved).  A ReLU with the INPUT
+    bit gets a fresh 1-bit mask buffer, owned by its record."""
     lib = _lib.load()
+    if isinstance(spec, ReLU):
+        if W is not None or b is not None:
+            raise TypeError("ReLU takes no W or b")
+        _on_gpu(x, y)
+        if y is None:
+            y = empty_like_layout(tuple(x.shape), x)
+        bits = relu_mask_buffer(x) if mask & MASK_INPUT else None
+        h = _relu_forward(lib, x, y, bits, mask)
+        if not h.value:
+            return y, None
+        return y, Record(h, _LayerDesc(spec), x, None, None, tuple(y.shape), y, bits)
     desc = _LayerDesc(spec)
     extra = (spec.running_mean, spec.running_var) if isinstance(spec, BatchNormEval) else ()
     _on_gpu(x, W, b, y, *extra)
@@ -267,7 +309,7 @@ def ledger_reset():
     check(_lib.load().ms_ledger_reset(), "ms_ledger_reset")
 
 
-PROF_FWD, PROF_DGRAD, PROF_WGRAD, PROF_BN = 1, 2, 4, 8
+PROF_FWD, PROF_DGRAD, PROF_WGRAD, PROF_BN, PROF_ACT = 1, 2, 4, 8, 16
 
 
 def profile_start(kinds: int):
@@ -306,6 +348,9 @@ class PreparedLayer:
         self.tensors = (x, W, b, y, grad_y, grad_x, grad_W, grad_b)
         self.y = y
         self.mask = int(mask)
+        self.relu = isinstance(spec, ReLU)
+        # a ReLU's 1-bit mask lives as long as this object (reused by every forward)
+        self.bits = relu_mask_buffer(x) if self.relu and self.mask & MASK_INPUT else None
         self._d = [tensor_desc(t) for t in self.tensors]
         self._fa = (ctypes.byref(self.desc.layer),) + tuple(_ptr(d) for d in self._d[:3])
         self._fy = _ptr(self._d[3])
@@ -319,6 +364,11 @@ class PreparedLayer:
         if self._h.value:
             self._free(self._h)
             self._h.value = None
+        if self.relu:
+            bits = ctypes.c_void_p(self.bits.data_ptr() if self.bits is not None and self.bits.numel() else None)
+            check(self.lib.ms_relu_forward(self._fa[1], self._fy, bits, self.mask, self._hp, self._stream),
+                  "ms_relu_forward")
+            return
         check(self.lib.ms_layer_forward(*self._fa, self.mask, self._fy, self._hp, self._stream),
               "ms_layer_forward")
 

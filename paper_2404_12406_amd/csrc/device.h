@@ -58,6 +58,12 @@ int launch_bn_bwd(int dtype, const void *dy, const void *x, const void *mean,
                   const void *var, const void *gamma, float eps, int64_t rows, int C,
                   void *dx, void *dgamma, void *dbeta, void *ws, void *stream);
 
+// ReLU over n elements in memory order: y = x < 0 ? 0 : x and its 1-bit mask
+// (bit i = !(y_i <= 0), 8 elements per byte, little-endian; bytes ceil(n/8) ..
+// bits_bytes - 1 are zeroed); backward dx_i = bit i ? dy_i : 0.
+int launch_relu_fwd(int dtype, const void *x, int64_t n, void *y, void *bits, int64_t bits_bytes, void *stream);
+int launch_relu_bwd(int dtype, const void *dy, const void *bits, int64_t n, void *dx, void *stream);
+
 // Global average pool x[N][L][C] -> y[N][C] and its adjoint.
 int launch_avgpool_fwd(int dtype, const void *x, int N, int L, int C, void *y, void *stream);
 int launch_avgpool_bwd(int dtype, const void *dy, int N, int L, int C, void *dx, void *stream);
@@ -72,7 +78,7 @@ int device_last_error();  // hipGetLastError()
 
 // Kernel timing (profile.hip): prof_mark(kind, stream, true) before a launch
 // and (.., false) after it record an event pair when `kind` is armed.
-enum ProfKind : unsigned { kProfFwd = 1u, kProfDgrad = 2u, kProfWgrad = 4u, kProfBn = 8u };
+enum ProfKind : unsigned { kProfFwd = 1u, kProfDgrad = 2u, kProfWgrad = 4u, kProfBn = 8u, kProfAct = 16u };
 void prof_mark(unsigned kind, void *stream, bool begin);
 int prof_start(unsigned kinds);
 int prof_read(unsigned kind, uint64_t *launches, double *total_ms);

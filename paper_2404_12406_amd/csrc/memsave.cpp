@@ -8,7 +8,9 @@
 // that backward will apply need.  BN in evaluation mode follows the same
 // pattern with gamma as the weight (its input gradient needs gamma and the
 // running variance, its gamma gradient needs x, the running mean and
-// variance).  Nothing in this file touches the device except through the
+// variance).  ReLU (Sec. 2.2.2) keeps one bit per element instead of its
+// output, so the next linear layer's input is not kept alive by it.
+// Nothing in this file touches the device except through the
 // launchers of device.h, and every check runs before the first launch.
 #include <algorithm>
 #include <atomic>
@@ -126,7 +128,19 @@ struct Plan {
     int Nb = 0;            // avgpool batch
     bool has_w = false, has_b = false;
     uint64_t x_bytes = 0, w_bytes = 0, stat_bytes = 0;
+    int64_t n = 0;                           // ReLU: elements
+    uint64_t bits_bytes = 0, y_bytes = 0;    // ReLU: 1-bit mask, output
 };
+
+uint64_t relu_mask_bytes(int64_t n) { return n > 0 ? (uint64_t)((n + 31) / 32) * 4u : 0u; }
+
+// Dense layouts an elementwise layer accepts: 1-D contiguous, 2-D row-major,
+// 4-D channels-last.
+bool dense_layout(const ms_tensor *t) {
+    if (t->ndim == 4) return is_nhwc(t);
+    if (t->ndim == 2) return is_rowmajor2(t);
+    return is_contig1(t);
+}
 
 ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_tensor *W,
                            const ms_tensor *b, uint32_t mask, const ms_tensor *y, bool need_data,
@@ -270,6 +284,27 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
         pl->x_bytes = (uint64_t)numel(x) * elt_size(x->dtype);
         return MS_OK;
     }
+    case MS_RELU: {
+        if (W || b) return fail(MS_E_ARG, "ReLU takes no W or b");
+        if (mask & ~(uint32_t)MS_RG_INPUT) return fail(MS_E_MASK, "ReLU has no parameters");
+        if (!x) return fail(MS_E_NULL, "x is NULL");
+        const int nd = x->ndim;
+        if (nd != 1 && nd != 2 && nd != 4) return fail(MS_E_SHAPE, "ReLU x must have 1, 2 or 4 dims");
+        if ((st = check_tensor(x, "x", nd, need_data))) return st;
+        if (!dense_layout(x)) return fail(MS_E_LAYOUT, "x must be contiguous, row-major or channels-last");
+        if (y) {
+            if ((st = check_tensor(y, "y", nd, need_data))) return st;
+            if (y->dtype != x->dtype) return fail(MS_E_DTYPE, "y dtype differs from x");
+            if (!same_shape(x, y)) return fail(MS_E_SHAPE, "y must have the shape of x");
+            if (!dense_layout(y)) return fail(MS_E_LAYOUT, "y must be in the layout of x");
+        }
+        pl->dtype = x->dtype;
+        pl->n = numel(x);
+        pl->x_bytes = (uint64_t)pl->n * elt_size(x->dtype);
+        pl->y_bytes = pl->x_bytes;
+        pl->bits_bytes = relu_mask_bytes(pl->n);
+        return MS_OK;
+    }
     default:
         return fail(MS_E_ARG, "unknown layer kind %d", layer->kind);
     }
@@ -292,6 +327,9 @@ uint32_t borrowed_bits(int32_t kind, uint32_t mask, int32_t policy, bool has_w, 
             return MS_SAVED_X | (has_w ? (uint32_t)MS_SAVED_W : 0u) | MS_SAVED_MEAN | MS_SAVED_VAR;
         return (w ? (uint32_t)(MS_SAVED_X | MS_SAVED_MEAN) : 0u) | (in && has_w ? (uint32_t)MS_SAVED_W : 0u) |
                ((in || w) ? (uint32_t)MS_SAVED_VAR : 0u);
+    case MS_RELU:   // stock PyTorch keeps the output; this library one bit per element
+        if (!in) return 0;
+        return policy == MS_POLICY_PYTORCH_DEFAULT ? (uint32_t)MS_SAVED_Y : (uint32_t)MS_SAVED_BITS;
     default:
         return 0;
     }
@@ -325,7 +363,9 @@ ms_account make_account(const Plan &pl, uint32_t mask, uint32_t borrowed, uint32
     a.mask = mask;
     a.borrowed = borrowed;
     a.kernels = kernels;
-    a.saved_activation_bytes = (borrowed & MS_SAVED_X) ? pl.x_bytes : 0;
+    a.saved_activation_bytes = ((borrowed & MS_SAVED_X) ? pl.x_bytes : 0) +
+                               ((borrowed & MS_SAVED_BITS) ? pl.bits_bytes : 0) +
+                               ((borrowed & MS_SAVED_Y) ? pl.y_bytes : 0);
     uint64_t pb = 0;
     if (borrowed & MS_SAVED_W) pb += pl.w_bytes;
     if (borrowed & MS_SAVED_MEAN) pb += pl.stat_bytes;
@@ -346,6 +386,7 @@ struct ms_record {
     Plan plan;
     float eps;
     ms_tensor x, W, b, mean, var, y;   // data non-NULL only for borrowed tensors
+    void *bits;                         // ReLU: the borrowed 1-bit mask
     ms_account acct;
     bool consumed;
     bool released;
@@ -361,6 +402,7 @@ void release(ms_record *r) {
         r->W.data = nullptr;
         r->mean.data = nullptr;
         r->var.data = nullptr;
+        r->bits = nullptr;
     }
 }
 
@@ -387,6 +429,7 @@ ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
     if (!rec) return fail(MS_E_NULL, "rec is NULL");
     *rec = nullptr;
     if (!y) return fail(MS_E_NULL, "y is NULL");
+    if (layer && layer->kind == MS_RELU) return fail(MS_E_ARG, "ReLU runs through ms_relu_forward()");
     Plan pl;
     ms_status st = validate_forward(layer, x, W, b, mask, y, true, &pl);
     if (st) return st;
@@ -434,6 +477,7 @@ ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
     r->eps = layer->eps;
     r->x = shape_only(x);
     r->y = shape_only(y);
+    r->bits = nullptr;
     std::memset(&r->W, 0, sizeof r->W);
     std::memset(&r->b, 0, sizeof r->b);
     std::memset(&r->mean, 0, sizeof r->mean);
@@ -511,10 +555,64 @@ ms_status ms_layer_backward(ms_record *r, const ms_tensor *grad_y, const ms_tens
     case MS_AVGPOOL:
         if (kernels & MS_K_DGRAD) err = ms::launch_avgpool_bwd(pl.dtype, dy, pl.Nb, pl.L, pl.C, grad_x->data, stream);
         break;
+    case MS_RELU:
+        if (kernels & MS_K_DGRAD) err = ms::launch_relu_bwd(pl.dtype, dy, r->bits, pl.n, grad_x->data, stream);
+        break;
     }
     if (err) return hip_fail(err, "backward launch");
     r->consumed = true;
     release(r);
+    return MS_OK;
+}
+
+uint64_t ms_relu_mask_bytes(int64_t n) { return relu_mask_bytes(n); }
+
+ms_status ms_relu_forward(const ms_tensor *x, const ms_tensor *y, void *bits, uint32_t mask, ms_record **rec,
+                          void *stream) {
+    clear_err();
+    if (!rec) return fail(MS_E_NULL, "rec is NULL");
+    *rec = nullptr;
+    if (!y) return fail(MS_E_NULL, "y is NULL");
+    ms_layer layer{};
+    layer.kind = MS_RELU;
+    Plan pl;
+    ms_status st = validate_forward(&layer, x, nullptr, nullptr, mask, y, true, &pl);
+    if (st) return st;
+    const bool keep = mask & MS_RG_INPUT;
+    if (keep && pl.bits_bytes > 0 && !bits) return fail(MS_E_NULL, "bits is NULL but the INPUT bit is set");
+    if (keep && (reinterpret_cast<uintptr_t>(bits) & 3u)) return fail(MS_E_ARG, "bits must be 4-byte aligned");
+    ms_record *r = nullptr;
+    if (keep) {
+        r = new (std::nothrow) ms_record();
+        if (!r) return fail(MS_E_NOMEM, "record allocation failed");
+    }
+    // without a record the mask is not needed: the forward writes y only
+    const int err = pl.n == 0 && !keep ? 0
+                    : ms::launch_relu_fwd(pl.dtype, x->data, pl.n, y->data, keep ? bits : nullptr,
+                                          keep ? (int64_t)pl.bits_bytes : 0, stream);
+    if (err) {
+        delete r;
+        return hip_fail(err, "forward launch");
+    }
+    if (!r) return MS_OK;
+    const uint32_t borrowed = borrowed_bits(MS_RELU, mask, MS_POLICY_SELECTIVE, false, false);
+    const uint32_t kernels = kernel_bits(MS_RELU, mask);
+    r->magic = kMagic;
+    r->plan = pl;
+    r->eps = 0.f;
+    r->x = shape_only(x);
+    r->y = shape_only(y);
+    std::memset(&r->W, 0, sizeof r->W);
+    std::memset(&r->b, 0, sizeof r->b);
+    std::memset(&r->mean, 0, sizeof r->mean);
+    std::memset(&r->var, 0, sizeof r->var);
+    r->bits = bits;
+    r->acct = make_account(pl, mask, borrowed, kernels);
+    r->consumed = false;
+    r->released = false;
+    ledger_add(r->acct.saved_activation_bytes);
+    g_records.fetch_add(1);
+    *rec = r;
     return MS_OK;
 }
 
@@ -568,7 +666,7 @@ ms_status ms_policy_account(const ms_layer *layer, const ms_tensor *x, const ms_
 
 ms_status ms_profile_start(uint32_t kinds) {
     clear_err();
-    if (kinds & ~15u) return fail(MS_E_ARG, "unknown profile kinds 0x%x", kinds);
+    if (kinds & ~31u) return fail(MS_E_ARG, "unknown profile kinds 0x%x", kinds);
     const int err = ms::prof_start(kinds);
     return err ? hip_fail(err, "ms_profile_start") : MS_OK;
 }
@@ -576,7 +674,8 @@ ms_status ms_profile_start(uint32_t kinds) {
 ms_status ms_profile_read(uint32_t kind, uint64_t *launches, double *total_ms) {
     clear_err();
     if (!launches || !total_ms) return fail(MS_E_NULL, "NULL argument");
-    if (kind != MS_PROF_FWD && kind != MS_PROF_DGRAD && kind != MS_PROF_WGRAD && kind != MS_PROF_BN)
+    if (kind != MS_PROF_FWD && kind != MS_PROF_DGRAD && kind != MS_PROF_WGRAD && kind != MS_PROF_BN &&
+        kind != MS_PROF_ACT)
         return fail(MS_E_ARG, "read one kind at a time");
     const int err = ms::prof_read(kind, launches, total_ms);
     return err ? hip_fail(err, "ms_profile_read") : MS_OK;

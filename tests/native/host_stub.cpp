@@ -128,6 +128,19 @@ int launch_bn_bwd(int, const void *dy, const void *x, const void *mean, const vo
     return e;
 }
 
+int launch_relu_fwd(int, const void *x, int64_t n, void *y, void *bits, int64_t bits_bytes, void *) {
+    log(bits ? "relu_fwd+bits" : "relu_fwd");
+    int e = 0;
+    if (n > 0) e |= need(x && y, "relu_fwd:x,y");
+    if (bits_bytes > 0) e |= need(bits, "relu_fwd:bits");
+    return e;
+}
+
+int launch_relu_bwd(int, const void *dy, const void *bits, int64_t n, void *dx, void *) {
+    log("relu_bwd");
+    return n > 0 ? need(dy && bits && dx, "relu_bwd:dy,bits,dx") : 0;
+}
+
 int launch_avgpool_fwd(int, const void *x, int N, int, int C, void *y, void *) {
     log("avgpool_fwd");
     return (N > 0 && C > 0) ? need(x && y, "avgpool_fwd:x,y") : 0;

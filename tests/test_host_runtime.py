@@ -409,9 +409,99 @@ def test_real_library_planners_on_edge_shapes(spec, dtype):
 def test_profile_api_validates_arguments(stub):
     n, t = ctypes.c_uint64(), ctypes.c_double()
     stub.ms_profile_start.argtypes = [ctypes.c_uint32]
-    assert stub.ms_profile_start(16) == L.MS_E_ARG
+    assert stub.ms_profile_start(32) == L.MS_E_ARG
     assert stub.ms_profile_start(L.MS_PROF_FWD | L.MS_PROF_DGRAD) == 0
     assert stub.ms_profile_read(L.MS_PROF_FWD | L.MS_PROF_DGRAD, ctypes.byref(n), ctypes.byref(t)) == L.MS_E_ARG
     assert stub.ms_profile_read(L.MS_PROF_FWD, None, ctypes.byref(t)) == L.MS_E_NULL
     assert stub.ms_profile_read(L.MS_PROF_BN, ctypes.byref(n), ctypes.byref(t)) == 0
     assert stub.ms_profile_start(0) == 0
+
+
+# ------------------------------------------------------------------ ReLU (Sec. 2.2.2)
+def _relu_forward(stub, x, y, bits, mask):
+    h = ctypes.c_void_p()
+    st = stub.ms_relu_forward(ref(x), ref(y), ctypes.c_void_p(bits) if bits is not None else None, mask,
+                              ctypes.byref(h), None)
+    return st, h
+
+
+@pytest.mark.parametrize("shape", [(1000,), (1,), (33, 7), (2, 16, 5, 7), (64, 64, 112, 112), (0,), (4, 0)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_relu_record_keeps_one_bit_per_element(stub, shape, dtype):
+    n = _numel(shape)
+    x, y = tdesc(shape, dtype), tdesc(shape, dtype)
+    stub.stub_reset()
+    live0, peak0 = ctypes.c_uint64(), ctypes.c_uint64()
+    stub.ms_ledger_read(ctypes.byref(live0), ctypes.byref(peak0))
+    st, h = _relu_forward(stub, x, y, FAKE + 4096, L.MS_RG_INPUT)
+    assert st == 0, stub.ms_last_error()
+    assert stub.stub_violations().decode() == ""
+    assert stub.ms_relu_mask_bytes(n) == P.relu_mask_bytes(n) == (4 * ((n + 31) // 32) if n else 0)
+    acct = L.MsAccount()
+    stub.ms_record_account(h, ctypes.byref(acct))
+    assert acct.saved_activation_bytes == P.saved_activation_bytes("relu", 1, n, dtype, P.SELECTIVE)
+    assert acct.borrowed == L.MS_SAVED_BITS and acct.kernels == L.MS_K_DGRAD
+    assert acct.referenced_param_bytes == 0
+    live = ctypes.c_uint64()
+    stub.ms_ledger_read(ctypes.byref(live), ctypes.byref(peak0))
+    assert live.value - live0.value == acct.saved_activation_bytes
+    stub.stub_reset()
+    gy, gx = tdesc(shape, dtype), tdesc(shape, dtype)
+    assert stub.ms_layer_backward(h, ref(gy), ref(gx), None, None, None) == 0, stub.ms_last_error()
+    assert stub.stub_log().decode() == "relu_bwd;"
+    assert stub.stub_violations().decode() == ""
+    stub.ms_ledger_read(ctypes.byref(live), ctypes.byref(peak0))
+    assert live.value == live0.value
+    assert stub.ms_layer_backward(h, ref(gy), ref(gx), None, None, None) == L.MS_E_CONSUMED
+    stub.ms_record_free(h)
+    # mask 0: y only, no mask buffer needed, no record
+    stub.stub_reset()
+    st, h = _relu_forward(stub, x, y, None, 0)
+    assert st == 0 and not h.value
+    assert stub.stub_log().decode() in ("relu_fwd;", "")
+    assert stub.ms_testing_live_records() == 0
+
+
+def test_relu_validation_errors_launch_nothing(stub):
+    x, y = tdesc((8, 16), "bf16"), tdesc((8, 16), "bf16")
+    cases = [
+        (x, y, FAKE, L.MS_RG_WEIGHT, L.MS_E_MASK),
+        (x, y, FAKE, L.MS_RG_INPUT | L.MS_RG_BIAS, L.MS_E_MASK),
+        (x, y, None, L.MS_RG_INPUT, L.MS_E_NULL),
+        (x, y, FAKE + 2, L.MS_RG_INPUT, L.MS_E_ARG),
+        (x, tdesc((8, 17), "bf16"), FAKE, L.MS_RG_INPUT, L.MS_E_SHAPE),
+        (x, tdesc((8, 16), "f32"), FAKE, L.MS_RG_INPUT, L.MS_E_DTYPE),
+        (tdesc((2, 3, 4), "bf16"), tdesc((2, 3, 4), "bf16"), FAKE, L.MS_RG_INPUT, L.MS_E_SHAPE),
+        (tdesc((2, 3, 4, 5), "bf16", "nchw"), tdesc((2, 3, 4, 5), "bf16", "nchw"), FAKE, 1, L.MS_E_LAYOUT),
+        (tdesc((2, 3, 4, 5), "bf16"), tdesc((2, 3, 4, 5), "bf16", "nchw"), FAKE, 1, L.MS_E_LAYOUT),
+        (None, y, FAKE, L.MS_RG_INPUT, L.MS_E_NULL),
+        (x, None, FAKE, L.MS_RG_INPUT, L.MS_E_NULL),
+    ]
+    for xi, yi, bits, mask, want in cases:
+        stub.stub_reset()
+        st, h = _relu_forward(stub, xi, yi, bits, mask)
+        assert st == want, (mask, want, st, stub.ms_last_error())
+        assert not h.value and stub.stub_log().decode() == ""
+    # the generic entry point refuses ReLU (it has no slot for the mask buffer)
+    layer = L.MsLayer()
+    layer.kind = L.MS_RELU
+    h = ctypes.c_void_p()
+    assert stub.ms_layer_forward(ctypes.byref(layer), ref(x), None, None, 1, ref(y), ctypes.byref(h), None) == L.MS_E_ARG
+    assert stub.ms_testing_live_records() == 0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_relu_policy_account(stub, dtype):
+    shape = (64, 64, 56, 56)
+    n = _numel(shape)
+    layer = L.MsLayer()
+    layer.kind = L.MS_RELU
+    x = tdesc(shape, dtype, data=False)
+    for policy in (P.SELECTIVE, P.PYTORCH_DEFAULT, P.ALL_TRUE):
+        for mask in (0, 1):
+            a = L.MsAccount()
+            assert stub.ms_policy_account(ctypes.byref(layer), ref(x), None, None, mask, policy, ctypes.byref(a)) == 0
+            assert a.saved_activation_bytes == P.saved_activation_bytes("relu", mask, n, dtype, policy)
+    a = L.MsAccount()
+    assert stub.ms_policy_account(ctypes.byref(layer), ref(x), ref(tdesc((4,), dtype)), None, 1, 0,
+                                  ctypes.byref(a)) == L.MS_E_ARG
