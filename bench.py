@@ -361,6 +361,52 @@ def relu_bandwidth(steps, warmup):
     return out
 
 
+def fig1_probe(depth: int = 16):
+    """The synthetic deep CNN of Sec. 2.1 (Fig. 1) at the paper's shape:
+    `depth` bias-free 3x3 convs with 8 channels on x = (256, 8, 256, 256)
+    fp32 (512 MiB per layer input), in three cases -- every layer and the
+    input differentiable, layers 4+ differentiable, only layer 4
+    differentiable -- built from torch.nn and converted to the library's
+    layers, and the same model with stock PyTorch layers for context.
+    Reported: bytes the allocator holds after the forward pass (beyond the
+    input and the output) and its forward peak, in MiB."""
+    import torch
+    from torch import nn
+    from paper_2404_12406_amd import autograd as msa
+    xs = (256, 8, 256, 256)
+    per_input = 256 * 8 * 256 * 256 * 4
+    out = {"shape": list(xs), "depth": depth, "dtype": "f32", "layer_input_MiB": per_input / 2 ** 20}
+    for impl in ("library", "stock_pytorch"):
+        res = {}
+        for case in ("all", "layers_4_plus", "layer_4_only"):
+            torch.manual_seed(0)
+            convs = [nn.Conv2d(8, 8, 3, padding=1, bias=False).cuda() for _ in range(depth)]
+            for i, c in enumerate(convs):
+                layer = i + 1
+                c.weight.requires_grad_(case == "all" or (case == "layers_4_plus" and layer >= 4)
+                                        or (case == "layer_4_only" and layer == 4))
+                if impl == "stock_pytorch":
+                    c.weight.data = c.weight.data.contiguous(memory_format=torch.channels_last)
+            net = nn.Sequential(*convs)
+            if impl == "library":
+                msa.convert(net)
+            x = torch.randn(xs, device="cuda").contiguous(memory_format=torch.channels_last)
+            x.requires_grad_(case == "all")
+            torch.cuda.synchronize()
+            torch.cuda.reset_peak_memory_stats()
+            base = torch.cuda.memory_allocated()
+            y = net(x)
+            torch.cuda.synchronize()
+            held = torch.cuda.memory_allocated() - base - y.numel() * y.element_size()
+            peak = torch.cuda.max_memory_allocated() - base
+            res[case] = {"held_MiB": round(held / 2 ** 20, 1), "held_layer_inputs": round(held / per_input, 3),
+                         "peak_MiB": round(peak / 2 ** 20, 1)}
+            del y, net, convs, x
+            torch.cuda.empty_cache()
+        out[impl] = res
+    return out
+
+
 def extras(steps, warmup):
     from synth import workloads as wl
     out = {}
@@ -380,6 +426,9 @@ def extras(steps, warmup):
     t0 = time.time()
     out["bn_eval_forward_resnet18_shaped"] = bn = bn_bandwidth(steps, warmup)
     log(f"[bench] bn: stack {bn['stack']['GBs']} GB/s, largest layer {bn['largest_layer']} ({time.time() - t0:.1f}s)")
+    t0 = time.time()
+    out["fig1_synthetic_cnn_memory"] = f1 = fig1_probe()
+    log(f"[bench] fig1 probe: library {f1['library']}, stock {f1['stock_pytorch']} ({time.time() - t0:.1f}s)")
     t0 = time.time()
     out["relu_bitmask_stem_output"] = rl = relu_bandwidth(steps, warmup)
     log(f"[bench] relu: forward {rl['forward']}, backward {rl['backward']}, saved {rl['saved_bytes']} "

@@ -1,0 +1,168 @@
+"""PyTorch autograd adapter: the library's layers as torch.autograd.Functions
+and nn.Modules, and a converter that swaps them into an existing model
+(Sec. 2.2: the method is a drop-in replacement whose forward decides what to
+keep from which of its inputs require grad, and whose backward computes only
+the gradients autograd asks for).
+
+Each Function derives its mask from ctx.needs_input_grad, runs the forward
+through the C ABI and keeps the library's record on ctx -- the record holds
+references to exactly the tensors the save rule borrows, so PyTorch's
+allocator retains what the ledger reports and nothing else.  Backward hands
+grad_y to ms_layer_backward and returns only the requested gradients.
+
+Layout: 4-D activations and conv weights are channels-last; the modules keep
+their weights that way and convert an input that is not (the converted copy
+is what a record would then borrow).
+"""
+from __future__ import annotations
+
+from typing import Optional
+
+import torch
+from torch import nn
+
+from . import api
+from .api import MASK_BIAS, MASK_INPUT, MASK_WEIGHT
+
+__all__ = ["MSConv2d", "MSLinear", "MSBatchNorm2dEval", "MSReLU", "convert"]
+
+
+def _cl(t: Optional[torch.Tensor]) -> Optional[torch.Tensor]:
+    if t is None or t.dim() != 4:
+        return t
+    return t if t.is_contiguous(memory_format=torch.channels_last) else t.contiguous(memory_format=torch.channels_last)
+
+
+def _mask(ctx, ix: int, iw: Optional[int] = None, ib: Optional[int] = None) -> int:
+    need = ctx.needs_input_grad
+    m = MASK_INPUT if need[ix] else 0
+    if iw is not None and need[iw]:
+        m |= MASK_WEIGHT
+    if ib is not None and need[ib]:
+        m |= MASK_BIAS
+    return m
+
+
+class _LayerFn(torch.autograd.Function):
+    """y = layer(x; W, b) through the C ABI; inputs (spec, x, W, b)."""
+
+    @staticmethod
+    def forward(ctx, spec, x, W, b):
+        mask = _mask(ctx, 1, 2 if W is not None else None, 3 if b is not None else None)
+        y, rec = api.layer_forward(spec, x, W, b, mask)
+        ctx.rec = rec
+        ctx.has = (W is not None, b is not None)
+        return y
+
+    @staticmethod
+    def backward(ctx, grad_y):
+        rec = ctx.rec
+        ctx.rec = None
+        if rec is None:
+            return None, None, None, None
+        gx, gw, gb = api.layer_backward(rec, _cl(grad_y.contiguous() if grad_y.dim() != 4 else grad_y))
+        rec.free()
+        return None, gx, gw, gb
+
+
+class _ReLUFn(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, x):
+        y, rec = api.layer_forward(api.ReLU(), x, mask=_mask(ctx, 0))
+        ctx.rec = rec
+        return y
+
+    @staticmethod
+    def backward(ctx, grad_y):
+        rec = ctx.rec
+        ctx.rec = None
+        if rec is None:
+            return None
+        gx, _, _ = api.layer_backward(rec, _cl(grad_y.contiguous() if grad_y.dim() != 4 else grad_y))
+        rec.free()
+        return gx
+
+
+class MSConv2d(nn.Module):
+    """Conv2d (cross-correlation, zero padding, dilation 1, groups 1) with a
+    channels-last weight [K, C, R, S] and optional bias [K]."""
+
+    def __init__(self, weight: torch.Tensor, bias: Optional[torch.Tensor], stride=1, padding=0):
+        super().__init__()
+        self.weight = weight if isinstance(weight, nn.Parameter) else nn.Parameter(weight)
+        self.bias = bias if (bias is None or isinstance(bias, nn.Parameter)) else nn.Parameter(bias)
+        with torch.no_grad():
+            if not self.weight.is_contiguous(memory_format=torch.channels_last):
+                self.weight.data = self.weight.data.contiguous(memory_format=torch.channels_last)
+        self.spec = api.Conv2d(stride, padding)
+
+    def forward(self, x):
+        return _LayerFn.apply(self.spec, _cl(x), self.weight, self.bias)
+
+
+class MSLinear(nn.Module):
+    """y = x W^T + b for x[M, K_in] (leading dims are flattened into M)."""
+
+    def __init__(self, weight: torch.Tensor, bias: Optional[torch.Tensor]):
+        super().__init__()
+        self.weight = weight if isinstance(weight, nn.Parameter) else nn.Parameter(weight)
+        self.bias = bias if (bias is None or isinstance(bias, nn.Parameter)) else nn.Parameter(bias)
+        self.spec = api.Linear()
+
+    def forward(self, x):
+        lead = x.shape[:-1]
+        y = _LayerFn.apply(self.spec, x.reshape(-1, x.shape[-1]).contiguous(), self.weight, self.bias)
+        return y.reshape(*lead, y.shape[-1])
+
+
+class MSBatchNorm2dEval(nn.Module):
+    """BatchNorm in evaluation mode: fixed running statistics, optional
+    affine gamma (weight) and beta (bias)."""
+
+    def __init__(self, weight, bias, running_mean, running_var, eps=1e-5):
+        super().__init__()
+        self.weight = weight if (weight is None or isinstance(weight, nn.Parameter)) else nn.Parameter(weight)
+        self.bias = bias if (bias is None or isinstance(bias, nn.Parameter)) else nn.Parameter(bias)
+        self.register_buffer("running_mean", running_mean)
+        self.register_buffer("running_var", running_var)
+        self.eps = float(eps)
+
+    def forward(self, x):
+        spec = api.BatchNormEval(self.running_mean, self.running_var, self.eps)
+        return _LayerFn.apply(spec, _cl(x), self.weight, self.bias)
+
+
+class MSReLU(nn.Module):
+    """ReLU whose backward keeps one bit per element (Sec. 2.2.2)."""
+
+    def forward(self, x):
+        return _ReLUFn.apply(_cl(x) if x.dim() == 4 else x.contiguous())
+
+
+def _convertible_conv(m: nn.Conv2d) -> bool:
+    pad = m.padding
+    return (m.groups == 1 and tuple(m.dilation) == (1, 1) and m.padding_mode == "zeros"
+            and not isinstance(pad, str) and m.weight.dtype in (torch.float32, torch.bfloat16))
+
+
+def convert(module: nn.Module) -> nn.Module:
+    """Replace, in place, every nn.Conv2d (groups 1, dilation 1, zero
+    padding), nn.Linear, nn.BatchNorm2d in evaluation mode and nn.ReLU of
+    `module` by the library's layers, sharing their parameters and buffers;
+    returns the module.  A BatchNorm2d still in training mode is left as it
+    is (its batch statistics make it non-linear in x)."""
+    for name, child in list(module.named_children()):
+        new = None
+        if isinstance(child, nn.Conv2d) and _convertible_conv(child):
+            new = MSConv2d(child.weight, child.bias, tuple(child.stride), tuple(child.padding))
+        elif isinstance(child, nn.Linear):
+            new = MSLinear(child.weight, child.bias)
+        elif isinstance(child, nn.BatchNorm2d) and not child.training and child.track_running_stats:
+            new = MSBatchNorm2dEval(child.weight, child.bias, child.running_mean, child.running_var, child.eps)
+        elif isinstance(child, nn.ReLU):
+            new = MSReLU()
+        if new is not None:
+            setattr(module, name, new)
+        else:
+            convert(child)
+    return module
