@@ -22,6 +22,8 @@ from . import build as _build
 __all__ = [
     "conv2d_forward", "conv2d_forward_at", "conv2d_input_grad", "conv2d_input_grad_at",
     "conv2d_weight_grad", "conv2d_weight_grad_at", "conv2d_bias_grad", "conv_out_hw",
+    "convt2d_out_hw", "convt2d_forward", "convt2d_forward_at", "convt2d_input_grad", "convt2d_input_grad_at",
+    "convt2d_weight_grad", "convt2d_weight_grad_at", "convt2d_bias_grad",
     "linear_forward", "linear_forward_at", "linear_input_grad", "linear_input_grad_at",
     "linear_weight_grad", "linear_weight_grad_at", "linear_bias_grad",
     "bn_eval_forward", "bn_eval_backward", "avgpool_forward", "avgpool_backward",
@@ -73,6 +75,93 @@ def _conv_args(x_shape, w_shape, stride, pad):
     if C2 != C:
         raise ValueError("channel mismatch")
     return [_I(v) for v in (N, C, H, W, K, R, S, stride[0], stride[1], pad[0], pad[1])]
+
+
+# ----------------------------------------------------------------- conv_transpose2d
+def convt2d_out_hw(H, W, R, S, stride, pad, out_pad=(0, 0)):
+    """Output extent of the transposed convolution (torch.nn.ConvTranspose2d,
+    dilation 1): (H-1) stride - 2 pad + R + out_pad."""
+    if not (0 <= out_pad[0] < stride[0] and 0 <= out_pad[1] < stride[1]):
+        raise ValueError("output padding must satisfy 0 <= out_pad < stride")
+    Ho = (H - 1) * stride[0] - 2 * pad[0] + R + out_pad[0]
+    Wo = (W - 1) * stride[1] - 2 * pad[1] + S + out_pad[1]
+    if Ho < 1 or Wo < 1:
+        raise ValueError("transposed convolution output would be empty")
+    return Ho, Wo
+
+
+def _convt_args(x_shape, w_shape, stride, pad, out_pad):
+    N, Ci, H, W = x_shape
+    Ci2, Co, R, S = w_shape
+    if Ci2 != Ci:
+        raise ValueError("channel mismatch")
+    Ho, Wo = convt2d_out_hw(H, W, R, S, stride, pad, out_pad)
+    return [_I(v) for v in (N, Ci, H, W, Co, R, S, stride[0], stride[1], pad[0], pad[1])], (Ho, Wo)
+
+
+def convt2d_forward(x, w, b=None, stride=(1, 1), pad=(0, 0), out_pad=(0, 0)):
+    """Transposed convolution, x[N,Ci,H,W], W[Ci,Co,R,S]: every input pixel
+    scatters x W through each tap to the output pixel h*stride - pad + r
+    (Sec. 2.2.1 names the layer; App. B lists it)."""
+    x, w, b = _d(x), _d(w), _d(b)
+    args, (Ho, Wo) = _convt_args(x.shape, w.shape, stride, pad, out_pad)
+    y = np.empty((x.shape[0], w.shape[1], Ho, Wo), np.float64)
+    _load().orc_convt2d_forward(_p(x), _p(w), _p(b), _p(y), *args, _I(Ho), _I(Wo))
+    return y
+
+
+def convt2d_forward_at(x, w, b, stride, pad, out_pad, idx):
+    """Forward values at sampled (n, o, h', w') coordinates, gathered."""
+    x, w, b = _d(x), _d(w), _d(b)
+    args, _ = _convt_args(x.shape, w.shape, stride, pad, out_pad)
+    ia, n = _idx(idx, 4)
+    out = np.empty(n, np.float64)
+    _load().orc_convt2d_forward_at(_p(x), _p(w), _p(b), *args,
+                                   ia.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), _I(n), _p(out))
+    return out
+
+
+def convt2d_input_grad(dy, w, x_shape, stride=(1, 1), pad=(0, 0), out_pad=(0, 0)):
+    """dx[n,i,h,w] = sum_{o,r,s} W[i,o,r,s] dy[n,o,h*sh-ph+r,w*sw-pw+s] (needs W only)."""
+    dy, w = _d(dy), _d(w)
+    args, (Ho, Wo) = _convt_args(x_shape, w.shape, stride, pad, out_pad)
+    dx = np.empty(tuple(x_shape), np.float64)
+    _load().orc_convt2d_input_grad(_p(dy), _p(w), _p(dx), *args, _I(Ho), _I(Wo))
+    return dx
+
+
+def convt2d_input_grad_at(dy, w, x_shape, stride, pad, out_pad, idx):
+    dy, w = _d(dy), _d(w)
+    args, (Ho, Wo) = _convt_args(x_shape, w.shape, stride, pad, out_pad)
+    ia, n = _idx(idx, 4)
+    out = np.empty(n, np.float64)
+    _load().orc_convt2d_input_grad_at(_p(dy), _p(w), *args, _I(Ho), _I(Wo),
+                                      ia.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), _I(n), _p(out))
+    return out
+
+
+def convt2d_weight_grad(dy, x, w_shape, stride=(1, 1), pad=(0, 0), out_pad=(0, 0)):
+    """dW[i,o,r,s] = sum_{n,h,w} x[n,i,h,w] dy[n,o,h*sh-ph+r,w*sw-pw+s] (needs x only)."""
+    dy, x = _d(dy), _d(x)
+    args, (Ho, Wo) = _convt_args(x.shape, w_shape, stride, pad, out_pad)
+    dw = np.empty(tuple(w_shape), np.float64)
+    _load().orc_convt2d_weight_grad(_p(dy), _p(x), _p(dw), *args, _I(Ho), _I(Wo))
+    return dw
+
+
+def convt2d_weight_grad_at(dy, x, w_shape, stride, pad, out_pad, idx):
+    dy, x = _d(dy), _d(x)
+    args, (Ho, Wo) = _convt_args(x.shape, w_shape, stride, pad, out_pad)
+    ia, n = _idx(idx, 4)
+    out = np.empty(n, np.float64)
+    _load().orc_convt2d_weight_grad_at(_p(dy), _p(x), *args, _I(Ho), _I(Wo),
+                                       ia.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), _I(n), _p(out))
+    return out
+
+
+def convt2d_bias_grad(dy):
+    """db[o] = sum over (n, h', w') of dy: the same column sum as any bias."""
+    return conv2d_bias_grad(dy)
 
 
 # ----------------------------------------------------------------- conv2d

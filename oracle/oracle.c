@@ -6,7 +6,8 @@
  * layers that are linear in both their input and their parameters
  * (Sec. 2.2.1: convolution Z = W * X + b, the fully-connected layer
  * y = W x + b of App. C, and batch normalisation in evaluation mode,
- * y = W (x - mu_hat) / sqrt(sigma_hat^2 + eps) + b of App. C), plus the
+ * y = W (x - mu_hat) / sqrt(sigma_hat^2 + eps) + b of App. C), the
+ * transposed convolution that Sec. 2.2.1 and App. B name beside them, plus the
  * parameter-free global average pool used to shape the ResNet-18-like stack.
  *
  * Only tests/, __graft_entry__.smoke() and the cpu_baseline leg of bench.py
@@ -212,6 +213,164 @@ void orc_conv2d_bias_grad(const double *dy, double *db, i64 N, i64 K, i64 P, i64
                     acc += dy[IDX4(n, k, p, q, K, P, Q)];
         db[k] = acc;
     }
+}
+
+/* ---------------------------------------------------------------------------
+ * Transposed convolution (the (transpose) convolution of Sec. 2.2.1 and the
+ * ConvTransposeNd of App. B), as torch.nn.ConvTranspose2d defines it with
+ * dilation 1 and groups 1: x[N,Ci,H,W], W[Ci,Co,R,S], output
+ * [N,Co,Ho,Wo] with Ho = (H-1) sh - 2 ph + R + oph (likewise Wo).  Every
+ * input pixel (h,w) scatters x[n,i,h,w] W[i,o,r,s] to the output pixel
+ * (h sh - ph + r, w sw - pw + s) when that lies inside the output:
+ *   y[n,o,h',w'] = b[o] + sum over (i,h,w,r,s) with h sh - ph + r = h' and
+ *                  w sw - pw + s = w' of x[n,i,h,w] W[i,o,r,s].
+ * The layer is linear in x and in W, so the rule of Sec. 2.2.1 applies: the
+ * input gradient needs W only, the weight gradient x only.
+ * ------------------------------------------------------------------------- */
+void orc_convt2d_forward(const double *x, const double *w, const double *b, double *y,
+                         i64 N, i64 Ci, i64 H, i64 W, i64 Co, i64 R, i64 S,
+                         i64 sh, i64 sw, i64 ph, i64 pw, i64 Ho, i64 Wo)
+{
+#pragma omp parallel for schedule(static)
+    for (i64 n = 0; n < N; ++n) {
+        double *yn = y + n * Co * Ho * Wo;
+        for (i64 o = 0; o < Co; ++o)
+            for (i64 t = 0; t < Ho * Wo; ++t)
+                yn[o * Ho * Wo + t] = b ? b[o] : 0.0;
+        for (i64 i = 0; i < Ci; ++i)
+            for (i64 h = 0; h < H; ++h)
+                for (i64 ww = 0; ww < W; ++ww) {
+                    double xv = x[IDX4(n, i, h, ww, Ci, H, W)];
+                    for (i64 o = 0; o < Co; ++o)
+                        for (i64 r = 0; r < R; ++r) {
+                            i64 oh = h * sh - ph + r;
+                            if (oh < 0 || oh >= Ho) continue;
+                            for (i64 s = 0; s < S; ++s) {
+                                i64 ow = ww * sw - pw + s;
+                                if (ow < 0 || ow >= Wo) continue;
+                                yn[(o * Ho + oh) * Wo + ow] += xv * w[IDX4(i, o, r, s, Co, R, S)];
+                            }
+                        }
+                }
+    }
+}
+
+/* One output entry y[n,o,h',w'], gathered: the taps (r,s) and input pixels
+ * (h,w) with h sh - ph + r = h' (h an integer in [0,H)), likewise for w. */
+void orc_convt2d_forward_at(const double *x, const double *w, const double *b,
+                            i64 N, i64 Ci, i64 H, i64 W, i64 Co, i64 R, i64 S,
+                            i64 sh, i64 sw, i64 ph, i64 pw,
+                            const i64 *idx, i64 count, double *out)
+{
+    (void)N;
+#pragma omp parallel for schedule(static)
+    for (i64 k = 0; k < count; ++k) {
+        i64 n = idx[4 * k], o = idx[4 * k + 1], oh = idx[4 * k + 2], ow = idx[4 * k + 3];
+        double acc = 0.0;
+        for (i64 i = 0; i < Ci; ++i)
+            for (i64 r = 0; r < R; ++r) {
+                i64 th = oh + ph - r;
+                if (th < 0 || th % sh != 0 || th / sh >= H) continue;
+                for (i64 s = 0; s < S; ++s) {
+                    i64 tw = ow + pw - s;
+                    if (tw < 0 || tw % sw != 0 || tw / sw >= W) continue;
+                    acc += x[IDX4(n, i, th / sh, tw / sw, Ci, H, W)] * w[IDX4(i, o, r, s, Co, R, S)];
+                }
+            }
+        out[k] = acc + (b ? b[o] : 0.0);
+    }
+}
+
+/* Input gradient: each scattered product x[n,i,h,w] W[i,o,r,s] sends
+ * W[i,o,r,s] dy[n,o,h',w'] back to x[n,i,h,w], so
+ *   dx[n,i,h,w] = sum_{o,r,s} W[i,o,r,s] dy[n,o, h sh - ph + r, w sw - pw + s]
+ * over the output pixels inside [0,Ho) x [0,Wo). */
+static double convt_dgrad_one(const double *dy, const double *w, i64 n, i64 i, i64 h, i64 ww,
+                              i64 Co, i64 R, i64 S, i64 sh, i64 sw, i64 ph, i64 pw, i64 Ho, i64 Wo)
+{
+    double acc = 0.0;
+    for (i64 o = 0; o < Co; ++o)
+        for (i64 r = 0; r < R; ++r) {
+            i64 oh = h * sh - ph + r;
+            if (oh < 0 || oh >= Ho) continue;
+            for (i64 s = 0; s < S; ++s) {
+                i64 ow = ww * sw - pw + s;
+                if (ow < 0 || ow >= Wo) continue;
+                acc += w[IDX4(i, o, r, s, Co, R, S)] * dy[IDX4(n, o, oh, ow, Co, Ho, Wo)];
+            }
+        }
+    return acc;
+}
+
+void orc_convt2d_input_grad(const double *dy, const double *w, double *dx,
+                            i64 N, i64 Ci, i64 H, i64 W, i64 Co, i64 R, i64 S,
+                            i64 sh, i64 sw, i64 ph, i64 pw, i64 Ho, i64 Wo)
+{
+#pragma omp parallel for collapse(2) schedule(static)
+    for (i64 n = 0; n < N; ++n)
+        for (i64 i = 0; i < Ci; ++i)
+            for (i64 h = 0; h < H; ++h)
+                for (i64 ww = 0; ww < W; ++ww)
+                    dx[IDX4(n, i, h, ww, Ci, H, W)] =
+                        convt_dgrad_one(dy, w, n, i, h, ww, Co, R, S, sh, sw, ph, pw, Ho, Wo);
+}
+
+void orc_convt2d_input_grad_at(const double *dy, const double *w,
+                               i64 N, i64 Ci, i64 H, i64 W, i64 Co, i64 R, i64 S,
+                               i64 sh, i64 sw, i64 ph, i64 pw, i64 Ho, i64 Wo,
+                               const i64 *idx, i64 count, double *out)
+{
+    (void)N; (void)Ci; (void)H; (void)W;
+#pragma omp parallel for schedule(static)
+    for (i64 k = 0; k < count; ++k)
+        out[k] = convt_dgrad_one(dy, w, idx[4 * k], idx[4 * k + 1], idx[4 * k + 2], idx[4 * k + 3],
+                                 Co, R, S, sh, sw, ph, pw, Ho, Wo);
+}
+
+/* Weight gradient:
+ *   dW[i,o,r,s] = sum_{n,h,w} x[n,i,h,w] dy[n,o, h sh - ph + r, w sw - pw + s]
+ * over the output pixels inside [0,Ho) x [0,Wo). */
+static double convt_wgrad_one(const double *dy, const double *x, i64 i, i64 o, i64 r, i64 s,
+                              i64 N, i64 Ci, i64 H, i64 W, i64 Co,
+                              i64 sh, i64 sw, i64 ph, i64 pw, i64 Ho, i64 Wo)
+{
+    double acc = 0.0;
+    for (i64 n = 0; n < N; ++n)
+        for (i64 h = 0; h < H; ++h) {
+            i64 oh = h * sh - ph + r;
+            if (oh < 0 || oh >= Ho) continue;
+            for (i64 ww = 0; ww < W; ++ww) {
+                i64 ow = ww * sw - pw + s;
+                if (ow < 0 || ow >= Wo) continue;
+                acc += x[IDX4(n, i, h, ww, Ci, H, W)] * dy[IDX4(n, o, oh, ow, Co, Ho, Wo)];
+            }
+        }
+    return acc;
+}
+
+void orc_convt2d_weight_grad(const double *dy, const double *x, double *dw,
+                             i64 N, i64 Ci, i64 H, i64 W, i64 Co, i64 R, i64 S,
+                             i64 sh, i64 sw, i64 ph, i64 pw, i64 Ho, i64 Wo)
+{
+#pragma omp parallel for collapse(2) schedule(static)
+    for (i64 i = 0; i < Ci; ++i)
+        for (i64 o = 0; o < Co; ++o)
+            for (i64 r = 0; r < R; ++r)
+                for (i64 s = 0; s < S; ++s)
+                    dw[IDX4(i, o, r, s, Co, R, S)] =
+                        convt_wgrad_one(dy, x, i, o, r, s, N, Ci, H, W, Co, sh, sw, ph, pw, Ho, Wo);
+}
+
+void orc_convt2d_weight_grad_at(const double *dy, const double *x,
+                                i64 N, i64 Ci, i64 H, i64 W, i64 Co, i64 R, i64 S,
+                                i64 sh, i64 sw, i64 ph, i64 pw, i64 Ho, i64 Wo,
+                                const i64 *idx, i64 count, double *out)
+{
+    (void)R; (void)S;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (i64 k = 0; k < count; ++k)
+        out[k] = convt_wgrad_one(dy, x, idx[4 * k], idx[4 * k + 1], idx[4 * k + 2], idx[4 * k + 3],
+                                 N, Ci, H, W, Co, sh, sw, ph, pw, Ho, Wo);
 }
 
 /* ---------------------------------------------------------------------------

@@ -6,12 +6,14 @@ Jacobian needs nothing; the layer checks which of W, X (and b) require grad
 and stores only what the Jacobians that will be applied need.  The same holds
 for batch normalisation in evaluation mode with gamma in the role of W:
 the input gradient needs gamma and sigma_hat^2, the gamma gradient needs x,
-mu_hat and sigma_hat^2 (App. C).
+mu_hat and sigma_hat^2 (App. C).  The transposed convolution is linear in x
+and in W as well (Sec. 2.2.1 names it beside the convolution) and follows the
+convolution's rule.
 
 Comparison policies:
   SELECTIVE        the rule above;
-  PYTORCH_DEFAULT  what stock PyTorch saves under the same mask: convolution
-                   and BN-eval store their input whenever the node exists,
+  PYTORCH_DEFAULT  what stock PyTorch saves under the same mask: convolution,
+                   its transpose and BN-eval store their input whenever the node exists,
                    i.e. whenever any parent requires grad (Fig. 2, Sec. 2.1,
                    App. B); the fully-connected layer is already agnostic
                    (App. B), so it follows SELECTIVE;
@@ -48,8 +50,8 @@ def saved_tensors(kind: str, mask: int, policy: int = SELECTIVE,
     i = bool(mask & MASK_INPUT)
     w = bool(mask & MASK_WEIGHT)
     any_flag = mask != 0
-    if kind in ("conv2d", "linear"):
-        if policy == PYTORCH_DEFAULT and kind == "conv2d":
+    if kind in ("conv2d", "conv_transpose2d", "linear"):
+        if policy == PYTORCH_DEFAULT and kind != "linear":
             return {"x": any_flag, "W": any_flag}
         return {"x": w, "W": i}
     if kind == "bn_eval":
