@@ -50,6 +50,12 @@ def layer_flops(spec, mask: int) -> dict:
         _, k, p, q = spec.out_shape()
         r, s = spec.ksize
         f = 2 * n * p * q * k * c * r * s
+    elif spec.kind == "conv_transpose2d":
+        # the convolution it is the adjoint of: every input pixel meets every
+        # tap and every (C_in, C_out) pair
+        n, ci, h, w = spec.in_shape
+        r, s = spec.ksize
+        f = 2 * n * h * w * ci * spec.out_ch * r * s
     elif spec.kind == "linear":
         m, kin = spec.in_shape
         f = 2 * m * kin * spec.out_ch
@@ -238,8 +244,10 @@ def run_workload(w, steps, warmup, backward=True):
         for c in chains:
             c.backward()
     torch.cuda.synchronize()
-    out = {"ms_per_step": round(ms_step, 4), "gflop": round(flop / 1e9, 3),
-           "tflops": round(flop / (ms_step * 1e-3) / 1e12, 2), "saved_selective": sel}
+    tflops = flop / (ms_step * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_TFLOPS
+    out = {"ms_per_step": round(ms_step, 4), "gflop": round(flop / 1e9, 3), "tflops": round(tflops, 2),
+           "frac_of_peak": round(tflops / peak, 4), "saved_selective": sel}
     del chains
     torch.cuda.empty_cache()
     return out
@@ -361,36 +369,49 @@ def relu_bandwidth(steps, warmup):
     return out
 
 
-def fig1_probe(depth: int = 16):
-    """The synthetic deep CNN of Sec. 2.1 (Fig. 1) at the paper's shape:
-    `depth` bias-free 3x3 convs with 8 channels on x = (256, 8, 256, 256)
-    fp32 (512 MiB per layer input), in three cases -- every layer and the
-    input differentiable, layers 4+ differentiable, only layer 4
-    differentiable -- built from torch.nn and converted to the library's
-    layers, and the same model with stock PyTorch layers for context.
-    Reported: bytes the allocator holds after the forward pass (beyond the
-    input and the output) and its forward peak, in MiB."""
+PROBE_SHAPES = {"conv2d": (256, 8, 256, 256), "conv_transpose2d": (256, 8, 256, 256),
+                "conv1d": (4096, 8, 4096), "conv_transpose1d": (4096, 8, 4096)}
+
+
+def memory_probe(kind: str = "conv2d", depth: int = 16):
+    """The synthetic deep CNN of Sec. 2.1 (Fig. 1) at the paper's shape, and
+    its App. B repetitions with the other layers linear in input and weight:
+    `depth` bias-free size-preserving layers with 8 channels and kernel 3
+    (conv2d / conv_transpose2d on (256, 8, 256, 256), conv1d /
+    conv_transpose1d on (4096, 8, 4096); fp32, 512 MiB per layer input), in
+    three cases -- every layer and the input differentiable, layers 4+
+    differentiable, only layer 4 differentiable -- built from torch.nn and
+    converted to the library's layers, and the same model with stock PyTorch
+    layers for context.  Reported: bytes the allocator holds after the
+    forward pass (beyond the input and the output) and its forward peak, in
+    MiB."""
     import torch
     from torch import nn
     from paper_2404_12406_amd import autograd as msa
-    xs = (256, 8, 256, 256)
-    per_input = 256 * 8 * 256 * 256 * 4
-    out = {"shape": list(xs), "depth": depth, "dtype": "f32", "layer_input_MiB": per_input / 2 ** 20}
+    xs = PROBE_SHAPES[kind]
+    per_input = numel(xs) * 4
+    make = {"conv2d": lambda: nn.Conv2d(8, 8, 3, padding=1, bias=False),
+            "conv_transpose2d": lambda: nn.ConvTranspose2d(8, 8, 3, padding=1, bias=False),
+            "conv1d": lambda: nn.Conv1d(8, 8, 3, padding=1, bias=False),
+            "conv_transpose1d": lambda: nn.ConvTranspose1d(8, 8, 3, padding=1, bias=False)}[kind]
+    out = {"layer": kind, "shape": list(xs), "depth": depth, "dtype": "f32", "layer_input_MiB": per_input / 2 ** 20}
     for impl in ("library", "stock_pytorch"):
         res = {}
         for case in ("all", "layers_4_plus", "layer_4_only"):
             torch.manual_seed(0)
-            convs = [nn.Conv2d(8, 8, 3, padding=1, bias=False).cuda() for _ in range(depth)]
+            convs = [make().cuda() for _ in range(depth)]
             for i, c in enumerate(convs):
                 layer = i + 1
                 c.weight.requires_grad_(case == "all" or (case == "layers_4_plus" and layer >= 4)
                                         or (case == "layer_4_only" and layer == 4))
-                if impl == "stock_pytorch":
+                if impl == "stock_pytorch" and len(xs) == 4:
                     c.weight.data = c.weight.data.contiguous(memory_format=torch.channels_last)
             net = nn.Sequential(*convs)
             if impl == "library":
                 msa.convert(net)
-            x = torch.randn(xs, device="cuda").contiguous(memory_format=torch.channels_last)
+            x = torch.randn(xs, device="cuda")
+            x = (x.contiguous(memory_format=torch.channels_last) if len(xs) == 4
+                 else x.transpose(1, 2).contiguous().transpose(1, 2))
             x.requires_grad_(case == "all")
             torch.cuda.synchronize()
             torch.cuda.reset_peak_memory_stats()
@@ -415,7 +436,8 @@ def extras(steps, warmup):
     jobs = [("single_conv2d_f32", wl.single_conv_f32(), True),
             ("resnet18_shaped_bf16", wl.resnet18_shaped_bf16(), True),
             ("resnet18_shaped_bf16_input", wl.resnet18_shaped_bf16(input_requires_grad=True), True),
-            ("encoder_linears_bf16", wl.encoder_linears_bf16(), True)]
+            ("encoder_linears_bf16", wl.encoder_linears_bf16(), True),
+            ("decoder_convt_bf16", wl.decoder_convt_bf16(), True)]
     for mk in ("00", "10", "01", "11"):
         jobs.append((f"conv_sweep_3x3_{mk}", wl.conv_sweep_bf16(mk), True))
         jobs.append((f"conv_sweep_1x1_{mk}", wl.conv_sweep_bf16(mk, pointwise=True), True))
@@ -427,8 +449,14 @@ def extras(steps, warmup):
     out["bn_eval_forward_resnet18_shaped"] = bn = bn_bandwidth(steps, warmup)
     log(f"[bench] bn: stack {bn['stack']['GBs']} GB/s, largest layer {bn['largest_layer']} ({time.time() - t0:.1f}s)")
     t0 = time.time()
-    out["fig1_synthetic_cnn_memory"] = f1 = fig1_probe()
+    out["fig1_synthetic_cnn_memory"] = f1 = memory_probe("conv2d")
     log(f"[bench] fig1 probe: library {f1['library']}, stock {f1['stock_pytorch']} ({time.time() - t0:.1f}s)")
+    out["appB_layer_memory"] = {}
+    for kind in ("conv_transpose2d", "conv1d", "conv_transpose1d"):
+        t0 = time.time()
+        out["appB_layer_memory"][kind] = pr = memory_probe(kind)
+        log(f"[bench] App. B probe {kind}: library {pr['library']}, stock {pr['stock_pytorch']} "
+            f"({time.time() - t0:.1f}s)")
     t0 = time.time()
     out["relu_bitmask_stem_output"] = rl = relu_bandwidth(steps, warmup)
     log(f"[bench] relu: forward {rl['forward']}, backward {rl['backward']}, saved {rl['saved_bytes']} "

@@ -2,8 +2,10 @@
  * memsave.h -- C ABI of the MI355X (gfx950) selective-differentiation layers.
  *
  * The library implements the forward and backward pass of the layers that
- * are linear in both their input and their parameters -- Conv2d, Linear and
- * BatchNorm in evaluation mode -- driven by a differentiability mask
+ * are linear in both their input and their parameters -- Conv2d, its
+ * transpose, Linear and BatchNorm in evaluation mode (Sec. 2.2.1 names the
+ * transposed convolution beside the others; App. B lists ConvTransposeNd
+ * among the layers it covers) -- driven by a differentiability mask
  * (Sec. 2.2.1 of "Lowering PyTorch's Memory Consumption for Selective
  * Differentiation", arXiv 2404.12406).  The input Jacobian of such a layer
  * needs only the weight, the weight Jacobian needs only the input and the
@@ -85,9 +87,24 @@ typedef enum {
                             x[N,C,H,W] (channels-last) or x[N,C]; W = gamma[C], b = beta[C]
                             (both NULL for affine=False); running stats are fixed buffers  */
     MS_AVGPOOL = 3,      /* global average pool x[N,C,H,W] -> y[N,C]; no parameters        */
-    MS_RELU = 4          /* y = max(x, 0) elementwise (NaN and -0 pass through); x 1-D
+    MS_RELU = 4,         /* y = max(x, 0) elementwise (NaN and -0 pass through); x 1-D
                             contiguous, 2-D row-major or 4-D channels-last, y likewise; no
                             parameters.  Forward through ms_relu_forward() only           */
+    MS_CONV_TRANSPOSE2D = 5 /* y = transposed convolution of x (torch.nn.ConvTranspose2d with
+                            dilation 1, groups 1): x[N,C_in,H,W], W[C_in,C_out,R,S]
+                            (channels-last: memory [C_in][R][S][C_out]), b[C_out] or NULL,
+                            y[N,C_out,H_out,W_out], H_out = (H-1) stride_h - 2 pad_h + R
+                            + out_pad_h (likewise W_out), 0 <= out_pad < stride:
+                              y[n,o,h',w'] = b[o] + sum of x[n,i,h,w] W[i,o,r,s]
+                              over h stride_h - pad_h + r = h', w stride_w - pad_w + s = w'.
+                            It is the adjoint of the convolution that maps [N,C_out,H_out,
+                            W_out] to [N,C_in,H,W] with filter W, stride and pad: its
+                            forward runs that convolution's input-gradient kernel (plus
+                            the bias), its input gradient that convolution's forward
+                            kernel, its weight gradient that convolution's weight-gradient
+                            kernel with x in the role of the output gradient.  The save
+                            rule is the convolution's.  A 1-D (transposed) convolution is
+                            the 2-D one with H = R = 1, stride_h = 1, pad_h = 0.          */
 } ms_kind;
 
 typedef struct {
@@ -97,6 +114,8 @@ typedef struct {
     float eps;                  /* BN-eval: epsilon (> 0) */
     const ms_tensor *running_mean;  /* BN-eval: mu_hat[C]; never differentiable */
     const ms_tensor *running_var;   /* BN-eval: sigma_hat^2[C]; never differentiable */
+    int32_t out_pad[2];         /* transposed conv: output padding (h, w), 0 <= out_pad < stride;
+                                   ignored by the other kinds */
 } ms_layer;
 
 /* Opaque saved-tensor record (the AD tape entry of one layer call). */
@@ -219,7 +238,9 @@ ms_status ms_policy_account(const ms_layer *layer, const ms_tensor *x, const ms_
  * launch of the selected kernel kinds with a pair of HIP events recorded on
  * the launch stream, so the caller can read the kernels' own GPU time over a
  * region of its choice.  Only the contraction kernel itself is bracketed
- * (not the weight transpose or reduction kernels around it).
+ * (not the weight transpose or reduction kernels around it).  Kinds name
+ * the contraction, not the layer's pass: a transposed convolution's forward
+ * is an input-gradient GEMM and its input gradient a forward GEMM.
  *   MS_PROF_FWD   forward convolution / linear GEMM
  *   MS_PROF_DGRAD input-gradient GEMM
  *   MS_PROF_WGRAD weight-gradient GEMM (its split-K partial launch)

@@ -12,7 +12,7 @@ MS_OK, MS_E_NULL, MS_E_MASK, MS_E_SHAPE, MS_E_DTYPE, MS_E_LAYOUT = 0, 1, 2, 3, 4
 MS_E_UNSUPPORTED, MS_E_CONSUMED, MS_E_NOMEM, MS_E_HIP, MS_E_ARG = 6, 7, 8, 9, 10
 MS_RG_INPUT, MS_RG_WEIGHT, MS_RG_BIAS = 1, 2, 4
 MS_F32, MS_BF16 = 0, 1
-MS_CONV2D, MS_LINEAR, MS_BN_EVAL, MS_AVGPOOL, MS_RELU = 0, 1, 2, 3, 4
+MS_CONV2D, MS_LINEAR, MS_BN_EVAL, MS_AVGPOOL, MS_RELU, MS_CONV_TRANSPOSE2D = 0, 1, 2, 3, 4, 5
 MS_SAVED_X, MS_SAVED_W, MS_SAVED_MEAN, MS_SAVED_VAR, MS_SAVED_BITS, MS_SAVED_Y = 1, 2, 4, 8, 16, 32
 MS_K_DGRAD, MS_K_WGRAD, MS_K_BGRAD = 1, 2, 4
 MS_POLICY_SELECTIVE, MS_POLICY_PYTORCH_DEFAULT, MS_POLICY_ALL_TRUE = 0, 1, 2
@@ -35,7 +35,7 @@ class MsTensor(ctypes.Structure):
 class MsLayer(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("stride", ctypes.c_int32 * 2), ("pad", ctypes.c_int32 * 2),
                 ("eps", ctypes.c_float), ("running_mean", ctypes.POINTER(MsTensor)),
-                ("running_var", ctypes.POINTER(MsTensor))]
+                ("running_var", ctypes.POINTER(MsTensor)), ("out_pad", ctypes.c_int32 * 2)]
 
 
 class MsAccount(ctypes.Structure):

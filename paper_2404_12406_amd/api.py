@@ -18,7 +18,8 @@ from typing import Optional, Tuple
 import torch
 
 from . import _lib
-from ._lib import (MS_AVGPOOL, MS_BN_EVAL, MS_CONV2D, MS_LINEAR, MS_RELU, MS_RG_BIAS, MS_RG_INPUT,
+from ._lib import (MS_AVGPOOL, MS_BN_EVAL, MS_CONV2D, MS_CONV_TRANSPOSE2D, MS_LINEAR, MS_RELU, MS_RG_BIAS,
+                   MS_RG_INPUT,
                    MS_RG_WEIGHT, MS_SAVED_BITS, MS_SAVED_MEAN, MS_SAVED_VAR, MS_SAVED_W, MS_SAVED_X,
                    MsAccount, MsLayer, MsTensor, check)
 
@@ -34,6 +35,16 @@ class Conv2d:
     """y = W * x + b (cross-correlation, zero padding, dilation 1, groups 1)."""
     stride: Tuple[int, int] | int = 1
     pad: Tuple[int, int] | int = 0
+
+
+@dataclass(frozen=True)
+class ConvTranspose2d:
+    """Transposed convolution (torch.nn.ConvTranspose2d, dilation 1, groups 1)
+    with W[C_in, C_out, R, S]: the adjoint of the convolution with that filter,
+    stride and pad; out_pad (< stride) extends the output on the high side."""
+    stride: Tuple[int, int] | int = 1
+    pad: Tuple[int, int] | int = 0
+    out_pad: Tuple[int, int] | int = 0
 
 
 @dataclass(frozen=True)
@@ -97,6 +108,12 @@ class _LayerDesc:
             s, p = _pair(spec.stride), _pair(spec.pad)
             self.layer.stride[0], self.layer.stride[1] = s
             self.layer.pad[0], self.layer.pad[1] = p
+        elif isinstance(spec, ConvTranspose2d):
+            self.layer.kind = MS_CONV_TRANSPOSE2D
+            s, p, o = _pair(spec.stride), _pair(spec.pad), _pair(spec.out_pad)
+            self.layer.stride[0], self.layer.stride[1] = s
+            self.layer.pad[0], self.layer.pad[1] = p
+            self.layer.out_pad[0], self.layer.out_pad[1] = o
         elif isinstance(spec, Linear):
             self.layer.kind = MS_LINEAR
         elif isinstance(spec, BatchNormEval):
@@ -126,6 +143,11 @@ def output_shape(spec, x: torch.Tensor, W: Optional[torch.Tensor]):
         K, _, R, S = W.shape
         (sh, sw), (ph, pw) = _pair(spec.stride), _pair(spec.pad)
         return (N, K, (H + 2 * ph - R) // sh + 1, (Wd + 2 * pw - S) // sw + 1)
+    if isinstance(spec, ConvTranspose2d):
+        N, _, H, Wd = x.shape
+        _, Co, R, S = W.shape
+        (sh, sw), (ph, pw), (oh, ow) = _pair(spec.stride), _pair(spec.pad), _pair(spec.out_pad)
+        return (N, Co, (H - 1) * sh - 2 * ph + R + oh, (Wd - 1) * sw - 2 * pw + S + ow)
     if isinstance(spec, Linear):
         return (x.shape[0], W.shape[0])
     if isinstance(spec, BatchNormEval):

@@ -12,7 +12,10 @@ grad_y to ms_layer_backward and returns only the requested gradients.
 
 Layout: 4-D activations and conv weights are channels-last; the modules keep
 their weights that way and convert an input that is not (the converted copy
-is what a record would then borrow).
+is what a record would then borrow).  The 1-D layers run as the 2-D ones
+with H = 1: their activations [N, C, L] and weights [K, C, R] are kept with
+the channel index innermost ([N][L][C], [K][R][C] in memory), so the 4-D
+views the library sees are channels-last without a copy.
 """
 from __future__ import annotations
 
@@ -24,7 +27,8 @@ from torch import nn
 from . import api
 from .api import MASK_BIAS, MASK_INPUT, MASK_WEIGHT
 
-__all__ = ["MSConv2d", "MSLinear", "MSBatchNorm2dEval", "MSReLU", "convert"]
+__all__ = ["MSConv2d", "MSConvTranspose2d", "MSConv1d", "MSConvTranspose1d", "MSLinear", "MSBatchNorm2dEval",
+           "MSReLU", "convert"]
 
 
 def _cl(t: Optional[torch.Tensor]) -> Optional[torch.Tensor]:
@@ -100,6 +104,66 @@ class MSConv2d(nn.Module):
         return _LayerFn.apply(self.spec, _cl(x), self.weight, self.bias)
 
 
+class MSConvTranspose2d(nn.Module):
+    """ConvTranspose2d (dilation 1, groups 1) with a channels-last weight
+    [C_in, C_out, R, S], optional bias [C_out] and output padding < stride."""
+
+    def __init__(self, weight: torch.Tensor, bias: Optional[torch.Tensor], stride=1, padding=0,
+                 output_padding=0):
+        super().__init__()
+        self.weight = weight if isinstance(weight, nn.Parameter) else nn.Parameter(weight)
+        self.bias = bias if (bias is None or isinstance(bias, nn.Parameter)) else nn.Parameter(bias)
+        with torch.no_grad():
+            if not self.weight.is_contiguous(memory_format=torch.channels_last):
+                self.weight.data = self.weight.data.contiguous(memory_format=torch.channels_last)
+        self.spec = api.ConvTranspose2d(stride, padding, output_padding)
+
+    def forward(self, x):
+        return _LayerFn.apply(self.spec, _cl(x), self.weight, self.bias)
+
+
+def _channels_inner(t: torch.Tensor) -> torch.Tensor:
+    """[A, C, L] with C innermost in memory ([A][L][C])."""
+    if t.stride(1) == 1 and t.stride(2) == t.shape[1]:
+        return t
+    return t.transpose(1, 2).contiguous().transpose(1, 2)
+
+
+def _first(v):
+    return int(v[0]) if isinstance(v, (tuple, list)) else int(v)
+
+
+class _Conv1dBase(nn.Module):
+    def __init__(self, weight, bias):
+        super().__init__()
+        self.weight = weight if isinstance(weight, nn.Parameter) else nn.Parameter(weight)
+        self.bias = bias if (bias is None or isinstance(bias, nn.Parameter)) else nn.Parameter(bias)
+        with torch.no_grad():
+            self.weight.data = _channels_inner(self.weight.data)
+
+    def forward(self, x):
+        y = _LayerFn.apply(self.spec, _cl(_channels_inner(x).unsqueeze(2)), self.weight.unsqueeze(2), self.bias)
+        return y.squeeze(2)
+
+
+class MSConv1d(_Conv1dBase):
+    """Conv1d (zero padding, dilation 1, groups 1) as the 2-D convolution
+    with H = R = 1: x[N, C, L], weight [K, C, R]."""
+
+    def __init__(self, weight, bias, stride=1, padding=0):
+        super().__init__(weight, bias)
+        self.spec = api.Conv2d((1, _first(stride)), (0, _first(padding)))
+
+
+class MSConvTranspose1d(_Conv1dBase):
+    """ConvTranspose1d (dilation 1, groups 1) as the 2-D transposed
+    convolution with H = R = 1: x[N, C_in, L], weight [C_in, C_out, R]."""
+
+    def __init__(self, weight, bias, stride=1, padding=0, output_padding=0):
+        super().__init__(weight, bias)
+        self.spec = api.ConvTranspose2d((1, _first(stride)), (0, _first(padding)), (0, _first(output_padding)))
+
+
 class MSLinear(nn.Module):
     """y = x W^T + b for x[M, K_in] (leading dims are flattened into M)."""
 
@@ -139,22 +203,31 @@ class MSReLU(nn.Module):
         return _ReLUFn.apply(_cl(x) if x.dim() == 4 else x.contiguous())
 
 
-def _convertible_conv(m: nn.Conv2d) -> bool:
-    pad = m.padding
-    return (m.groups == 1 and tuple(m.dilation) == (1, 1) and m.padding_mode == "zeros"
-            and not isinstance(pad, str) and m.weight.dtype in (torch.float32, torch.bfloat16))
+def _convertible_conv(m) -> bool:
+    """groups 1, dilation 1, zero padding given as numbers, fp32 or bf16."""
+    return (m.groups == 1 and all(d == 1 for d in m.dilation) and m.padding_mode == "zeros"
+            and not isinstance(m.padding, str) and m.weight.dtype in (torch.float32, torch.bfloat16))
 
 
 def convert(module: nn.Module) -> nn.Module:
-    """Replace, in place, every nn.Conv2d (groups 1, dilation 1, zero
-    padding), nn.Linear, nn.BatchNorm2d in evaluation mode and nn.ReLU of
-    `module` by the library's layers, sharing their parameters and buffers;
-    returns the module.  A BatchNorm2d still in training mode is left as it
-    is (its batch statistics make it non-linear in x)."""
+    """Replace, in place, every nn.Conv2d, nn.ConvTranspose2d, nn.Conv1d and
+    nn.ConvTranspose1d (groups 1, dilation 1, zero padding), nn.Linear,
+    nn.BatchNorm2d in evaluation mode and nn.ReLU of `module` by the
+    library's layers, sharing their parameters and buffers; returns the
+    module (Sec. 4: one call swaps every supported layer).  A BatchNorm2d
+    still in training mode is left as it is (its batch statistics make it
+    non-linear in x); so is any layer outside those limits."""
     for name, child in list(module.named_children()):
         new = None
         if isinstance(child, nn.Conv2d) and _convertible_conv(child):
             new = MSConv2d(child.weight, child.bias, tuple(child.stride), tuple(child.padding))
+        elif isinstance(child, nn.ConvTranspose2d) and _convertible_conv(child):
+            new = MSConvTranspose2d(child.weight, child.bias, tuple(child.stride), tuple(child.padding),
+                                    tuple(child.output_padding))
+        elif isinstance(child, nn.Conv1d) and _convertible_conv(child):
+            new = MSConv1d(child.weight, child.bias, child.stride, child.padding)
+        elif isinstance(child, nn.ConvTranspose1d) and _convertible_conv(child):
+            new = MSConvTranspose1d(child.weight, child.bias, child.stride, child.padding, child.output_padding)
         elif isinstance(child, nn.Linear):
             new = MSLinear(child.weight, child.bias)
         elif isinstance(child, nn.BatchNorm2d) and not child.training and child.track_running_stats:

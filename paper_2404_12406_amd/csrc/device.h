@@ -27,11 +27,13 @@ size_t conv_fwd_workspace(int dtype, const ConvGeom &g);
 int launch_conv_fwd(int dtype, const ConvGeom &g, const void *x, const void *w,
                     const void *bias, void *y, void *ws, void *stream);
 
-// dx = input gradient of the convolution for grad dy (needs w only).  May
-// use conv_dgrad_workspace() bytes of workspace (a transposed copy of w).
+// dx = input gradient of the convolution for grad dy (needs w only), plus
+// bias[c] per channel when bias is non-null (the forward of a transposed
+// convolution is this contraction).  May use conv_dgrad_workspace() bytes of
+// workspace (a transposed copy of w, zero-padded channel copies).
 size_t conv_dgrad_workspace(int dtype, const ConvGeom &g);
 int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *w,
-                      void *dx, void *ws, void *stream);
+                      const void *bias, void *dx, void *ws, void *stream);
 
 // dw = weight gradient for grad dy and input x.  Needs conv_wgrad_workspace()
 // bytes of device workspace (may be 0).  When db is non-null the launcher may

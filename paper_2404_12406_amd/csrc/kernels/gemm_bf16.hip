@@ -58,7 +58,8 @@ struct Args {
     float *part;          // split-K partials: part_stride floats per split (nullptr: splits == 1)
     float *dbpart;        // WGRAD fused bias-gradient partials [splits][M] (nullptr: off)
     int64_t part_stride;  // FWD/WGRAD: M*N; DGRAD: N*H*W*C (partials indexed by dx pixel)
-    const bf16 *bias;     // FWD bias (nullptr: none)
+    const bf16 *bias;     // FWD / DGRAD per-column bias (nullptr: none; DGRAD: the
+                          // transposed convolution's forward)
     ConvGeom g;
     int M, N, K;          // GEMM extents (DGRAD: bounds over phases)
     int ntm, ntn;
@@ -763,9 +764,10 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
     constexpr int SEG = G::WN / 8;                   // 16-byte segments per staged row
     constexpr int ROWS_PER_PASS = 64 / SEG;
     typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-    // forward bias: the lane's output columns are the same for every row it
-    // holds, so its bias values are read once and added in fp32 before the
-    // single rounding to bf16
+    // bias: the lane's output columns are the same for every row it holds,
+    // so its bias values are read once and added in fp32 before the single
+    // rounding to bf16 (forward: staged in LDS; input gradient, i.e. the
+    // forward of a transposed convolution: read from global memory)
     float bcol[TN][4][4];
 #pragma unroll
     for (int j = 0; j < TN; ++j)
@@ -773,7 +775,7 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
         for (int q = 0; q < 4; ++q)
 #pragma unroll
             for (int v = 0; v < 4; ++v) bcol[j][q][v] = 0.f;
-    if constexpr (MODE == kFwd) {
+    if constexpr (MODE != kWgrad) {
         if (bias_lds) {
             // the bias area is past every stage and the staging rows; its
             // DMA completed before the barrier above
@@ -1342,25 +1344,31 @@ size_t dgrad_core_workspace(const ConvGeom &g) {
 size_t dgrad_workspace(const ConvGeom &g) {
     if (g.K % 8 != 0) return 0;
     if (g.C % 8 != 0) {
-        // padded W, padded dx, then the workspace of the padded contraction
+        // padded W, padded bias, padded dx, then the workspace of the padded
+        // contraction
         const ConvGeom g8 = padded(g);
-        return al256((size_t)g.K * g.R * g.S * g8.C * 2) + al256((size_t)g.N * g.H * g.W * g8.C * 2) +
-               dgrad_core_workspace(g8);
+        return al256((size_t)g.K * g.R * g.S * g8.C * 2) + al256((size_t)g8.C * 2) +
+               al256((size_t)g.N * g.H * g.W * g8.C * 2) + dgrad_core_workspace(g8);
     }
     return dgrad_core_workspace(g);
 }
 
-int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, void *ws, hipStream_t st) {
+// dx = input gradient (+ bias[c] per channel when bias is non-null: the
+// forward of a transposed convolution runs this contraction).
+int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bias, void *dx, void *ws,
+               hipStream_t st) {
     if (g.K % 8 != 0) return -1;
     if (g.C % 8 != 0) {
         if (!ws || !al16(ws)) return -1;
         const ConvGeom g8 = padded(g);
         char *wp = static_cast<char *>(ws);
-        char *dxp = wp + al256((size_t)g.K * g.R * g.S * g8.C * 2);
+        char *bp = wp + al256((size_t)g.K * g.R * g.S * g8.C * 2);
+        char *dxp = bp + al256((size_t)g8.C * 2);
         char *ws2 = dxp + al256((size_t)g.N * g.H * g.W * g8.C * 2);
         int err = pad_channels(w, (int64_t)g.K * g.R * g.S, g.C, wp, st);
+        if (!err && bias) err = pad_channels(bias, 1, g.C, bp, st);
         if (err) return err;
-        err = conv_dgrad(g8, dy, wp, dxp, ws2, st);
+        err = conv_dgrad(g8, dy, wp, bias ? bp : nullptr, dxp, ws2, st);
         if (err) return err;   // -1: not applicable (the caller falls back), else a HIP error
         return crop_channels(dxp, (int64_t)g.N * g.H * g.W, g.C, dx, st);
     }
@@ -1375,6 +1383,7 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, void 
     if (p.splits > 1) part = reinterpret_cast<float *>(wsc + (direct ? 0 : al256((size_t)g.K * g.R * g.S * g.C * sizeof(bf16))));
     Args a{};
     a.a = (const bf16 *)dy; a.b = direct ? (const bf16 *)w : wt; a.c = (bf16 *)dx; a.g = g;
+    a.bias = (const bf16 *)bias;
     const int Hb = (g.H + g.sh - 1) / g.sh, Wb = (g.W + g.sw - 1) / g.sw;
     a.M = g.N * Hb * Wb; a.N = g.C;
     a.K = ((g.R + g.sh - 1) / g.sh) * ((g.S + g.sw - 1) / g.sw) * g.K;
@@ -1398,7 +1407,7 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, void 
     const dim3 grid(a.ntm * a.ntn, 1, g.sh * g.sw * p.splits);
     int err = direct ? go_mode<kDgradN>(p.t, a, grid, unit_geom(g), st) : go_mode<kDgrad>(p.t, a, grid, unit_geom(g), st);
     if (err || p.splits <= 1) return err;
-    return reduce_partials(part, p.splits, n, a.part_stride, (bf16 *)dx, nullptr, 1, st);
+    return reduce_partials(part, p.splits, n, a.part_stride, (bf16 *)dx, (const bf16 *)bias, g.C, st);
 }
 
 bool wgrad_applies(const ConvGeom &g) { return g.K % 8 == 0; }

@@ -36,7 +36,8 @@ namespace g2 {
 size_t fwd_workspace(const ConvGeom &g);
 int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, void *y, void *ws, hipStream_t st);
 size_t dgrad_workspace(const ConvGeom &g);
-int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, void *dx, void *ws, hipStream_t st);
+int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bias, void *dx, void *ws,
+               hipStream_t st);
 bool wgrad_applies(const ConvGeom &g);
 size_t wgrad_workspace(const ConvGeom &g, bool with_db);
 int conv_wgrad(const ConvGeom &g, const void *dy, const void *x, void *dw, void *db, void *ws, hipStream_t st);
@@ -104,7 +105,10 @@ struct Igemm {
     static_assert(BK % KI == 0, "BK must be a multiple of the MFMA k");
 };
 
-template <typename T, int MODE, int BM, int BN, int BK, bool VEC_OK, bool UNIT>
+// BIAS (DGRAD only): add bias[c] to the input gradient -- the forward of a
+// transposed convolution; a variant of its own so that the plain input
+// gradient keeps its register budget.
+template <typename T, int MODE, int BM, int BN, int BK, bool VEC_OK, bool UNIT, bool BIAS = false>
 __global__ __launch_bounds__(256) void igemm_kernel(IgemmParams prm) {
     using G = Igemm<T, MODE, BM, BN, BK, VEC_OK, UNIT>;
     constexpr int VEC = G::VEC, LDK = G::LDK, NVA = G::NVA, NVB = G::NVB;
@@ -488,6 +492,7 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgemmParams prm) {
         }
     } else if constexpr (MODE == kDgrad) {
         T *DX = static_cast<T *>(prm.c);
+        const T *bias = static_cast<const T *>(prm.bias);
         const int HW = f.Hp * f.Wp;
 #pragma unroll
         for (int i = 0; i < TM; ++i)
@@ -506,7 +511,9 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgemmParams prm) {
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
                     const int c = n0 + wn0 + j * 16 + ec;
-                    if (c < Ng) DX[pix * g.C + c] = from_f32<T>(acc[i][j][v]);
+                    if (c >= Ng) continue;
+                    if constexpr (BIAS) DX[pix * g.C + c] = from_f32<T>(acc[i][j][v] + to_f32(bias[c]));
+                    else DX[pix * g.C + c] = from_f32<T>(acc[i][j][v]);
                 }
             }
     } else {
@@ -572,7 +579,11 @@ int launch_t(const IgemmParams &prm, dim3 grid, hipStream_t st) {
     constexpr int BK = bk_of<T>();
     const unsigned pk = MODE == kFwd ? kProfFwd : MODE == kDgrad ? kProfDgrad : kProfWgrad;
     prof_mark(pk, st, true);
-    hipLaunchKernelGGL((igemm_kernel<T, MODE, kBM, kBN, BK, VEC_OK, UNIT>), grid, dim3(256), 0, st, prm);
+    if (MODE == kDgrad && prm.bias)
+        hipLaunchKernelGGL((igemm_kernel<T, MODE, kBM, kBN, BK, VEC_OK, UNIT, MODE == kDgrad>), grid, dim3(256), 0, st,
+                           prm);
+    else
+        hipLaunchKernelGGL((igemm_kernel<T, MODE, kBM, kBN, BK, VEC_OK, UNIT>), grid, dim3(256), 0, st, prm);
     const int err = (int)hipGetLastError();
     prof_mark(pk, st, false);
     return err;
@@ -650,14 +661,14 @@ size_t conv_dgrad_workspace(int dtype, const ConvGeom &g) {
     return dtype == kBF16 ? g2::dgrad_workspace(g) : 0;
 }
 
-int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *w, void *dx,
-                      void *ws, void *stream) {
+int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *w, const void *bias,
+                      void *dx, void *ws, void *stream) {
     if (dtype == kBF16) {
-        const int r = g2::conv_dgrad(g, dy, w, dx, ws, (hipStream_t)stream);
+        const int r = g2::conv_dgrad(g, dy, w, bias, dx, ws, (hipStream_t)stream);
         if (r >= 0) return r;
     }
     IgemmParams prm{};
-    prm.a = dy; prm.b = w; prm.c = dx; prm.g = g;
+    prm.a = dy; prm.b = w; prm.c = dx; prm.bias = bias; prm.g = g;
     // bounds over phases: ceil(H / sh) rows, ceil(R / sh) taps
     const int Hb = (g.H + g.sh - 1) / g.sh, Wb = (g.W + g.sw - 1) / g.sw;
     prm.M = g.N * Hb * Wb;

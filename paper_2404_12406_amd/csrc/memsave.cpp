@@ -8,8 +8,10 @@
 // that backward will apply need.  BN in evaluation mode follows the same
 // pattern with gamma as the weight (its input gradient needs gamma and the
 // running variance, its gamma gradient needs x, the running mean and
-// variance).  ReLU (Sec. 2.2.2) keeps one bit per element instead of its
-// output, so the next linear layer's input is not kept alive by it.
+// variance).  A transposed convolution is the adjoint of a convolution and
+// keeps what a convolution keeps.  ReLU (Sec. 2.2.2) keeps one bit per
+// element instead of its output, so the next linear layer's input is not
+// kept alive by it.
 // Nothing in this file touches the device except through the
 // launchers of device.h, and every check runs before the first launch.
 #include <algorithm>
@@ -121,7 +123,7 @@ ms_tensor shape_only(const ms_tensor *t) {
 struct Plan {
     int32_t kind = 0;
     int32_t dtype = 0;
-    ms::ConvGeom g{};      // conv / linear
+    ms::ConvGeom g{};      // conv / linear; transposed conv: the convolution it is the adjoint of
     int64_t rows = 0;      // BN / avgpool: pixels; conv/linear bias grad rows
     int C = 0;             // BN / avgpool channels
     int L = 0;             // avgpool pixels per sample
@@ -192,6 +194,57 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
                              layer->stride[0], layer->stride[1], layer->pad[0], layer->pad[1]};
         if (N * P * Q * K > kMaxElems) return fail(MS_E_UNSUPPORTED, "output has more than 2^31-1 elements");
         pl->rows = N * P * Q;
+        pl->x_bytes = (uint64_t)numel(x) * elt_size(x->dtype);
+        pl->w_bytes = (uint64_t)numel(W) * elt_size(W->dtype);
+        return MS_OK;
+    }
+    case MS_CONV_TRANSPOSE2D: {
+        if ((st = check_tensor(x, "x", 4, need_data))) return st;
+        if (!W) return fail(MS_E_NULL, "conv_transpose2d needs W");
+        if ((st = check_tensor(W, "W", 4, need_data))) return st;
+        if (x->dtype != W->dtype) return fail(MS_E_DTYPE, "x and W dtypes differ");
+        if (!is_nhwc(x)) return fail(MS_E_LAYOUT, "x must be channels-last (NHWC)");
+        if (!is_nhwc(W)) return fail(MS_E_LAYOUT, "W must be channels-last (memory [C_in][R][S][C_out])");
+        const int64_t N = x->shape[0], Ci = x->shape[1], H = x->shape[2], Wd = x->shape[3];
+        const int64_t Co = W->shape[1], R = W->shape[2], S = W->shape[3];
+        if (W->shape[0] != Ci) return fail(MS_E_SHAPE, "W has %lld input channels, x has %lld",
+                                           (long long)W->shape[0], (long long)Ci);
+        if (layer->stride[0] < 1 || layer->stride[1] < 1) return fail(MS_E_ARG, "stride must be >= 1");
+        if (layer->pad[0] < 0 || layer->pad[1] < 0) return fail(MS_E_ARG, "pad must be >= 0");
+        for (int i = 0; i < 2; ++i)
+            if (layer->out_pad[i] < 0 || layer->out_pad[i] >= layer->stride[i])
+                return fail(MS_E_ARG, "out_pad must satisfy 0 <= out_pad < stride");
+        if (Ci < 1 || Co < 1 || R < 1 || S < 1 || H < 1 || Wd < 1)
+            return fail(MS_E_SHAPE, "conv_transpose2d extents C_in, C_out, R, S, H, W must be >= 1");
+        const int64_t Ho = (H - 1) * layer->stride[0] - 2 * (int64_t)layer->pad[0] + R + layer->out_pad[0];
+        const int64_t Wo = (Wd - 1) * layer->stride[1] - 2 * (int64_t)layer->pad[1] + S + layer->out_pad[1];
+        if (Ho < 1 || Wo < 1) return fail(MS_E_SHAPE, "output would be empty");
+        if (Ho + 2 * (int64_t)layer->pad[0] > kMaxElems || Wo + 2 * (int64_t)layer->pad[1] > kMaxElems)
+            return fail(MS_E_UNSUPPORTED, "output extent too large");
+        if (b) {
+            if ((st = check_tensor(b, "b", 1, need_data))) return st;
+            if (b->dtype != x->dtype) return fail(MS_E_DTYPE, "b dtype differs from x");
+            if (b->shape[0] != Co) return fail(MS_E_SHAPE, "b must have C_out elements");
+            if (!is_contig1(b)) return fail(MS_E_LAYOUT, "b must be contiguous");
+        }
+        if (y) {
+            if ((st = check_tensor(y, "y", 4, need_data))) return st;
+            if (y->dtype != x->dtype) return fail(MS_E_DTYPE, "y dtype differs from x");
+            if (y->shape[0] != N || y->shape[1] != Co || y->shape[2] != Ho || y->shape[3] != Wo)
+                return fail(MS_E_SHAPE, "y must be [%lld,%lld,%lld,%lld]", (long long)N, (long long)Co,
+                            (long long)Ho, (long long)Wo);
+            if (!is_nhwc(y)) return fail(MS_E_LAYOUT, "y must be channels-last (NHWC)");
+        }
+        if (N * Ho * Wo * Co > kMaxElems) return fail(MS_E_UNSUPPORTED, "output has more than 2^31-1 elements");
+        pl->dtype = x->dtype;
+        // the convolution y -> x with filter W: input [N,C_out,H_out,W_out], K = C_in filters,
+        // output [N,C_in,H,W]; out_pad < stride makes its output extent exactly H x W
+        pl->g = ms::ConvGeom{(int)N, (int)Co, (int)Ho, (int)Wo, (int)Ci, (int)R, (int)S, (int)H, (int)Wd,
+                             layer->stride[0], layer->stride[1], layer->pad[0], layer->pad[1]};
+        if ((Ho + 2 * layer->pad[0] - R) / layer->stride[0] + 1 != H ||
+            (Wo + 2 * layer->pad[1] - S) / layer->stride[1] + 1 != Wd)
+            return fail(MS_E_ARG, "inconsistent transposed-convolution geometry");
+        pl->rows = N * Ho * Wo;
         pl->x_bytes = (uint64_t)numel(x) * elt_size(x->dtype);
         pl->w_bytes = (uint64_t)numel(W) * elt_size(W->dtype);
         return MS_OK;
@@ -318,6 +371,7 @@ uint32_t borrowed_bits(int32_t kind, uint32_t mask, int32_t policy, bool has_w, 
     const bool in = mask & MS_RG_INPUT, w = mask & MS_RG_WEIGHT;
     switch (kind) {
     case MS_CONV2D:
+    case MS_CONV_TRANSPOSE2D:   // stock PyTorch keeps both for either (Fig. 2, App. B)
         if (policy == MS_POLICY_PYTORCH_DEFAULT) return MS_SAVED_X | MS_SAVED_W;
         return (w ? (uint32_t)MS_SAVED_X : 0u) | (in ? (uint32_t)MS_SAVED_W : 0u);
     case MS_LINEAR:   // PyTorch's Linear is already selective (App. B)
@@ -352,6 +406,10 @@ size_t backward_workspace(const Plan &pl, uint32_t kernels) {
         if (kernels & MS_K_WGRAD)
             ws = std::max(ws, ms::conv_wgrad_workspace(pl.dtype, pl.g, (kernels & MS_K_BGRAD) != 0));
         if (kernels & MS_K_BGRAD) ws = std::max(ws, ms::colsum_workspace(pl.dtype, pl.rows, pl.g.K));
+    } else if (pl.kind == MS_CONV_TRANSPOSE2D) {
+        if (kernels & MS_K_DGRAD) ws = std::max(ws, ms::conv_fwd_workspace(pl.dtype, pl.g));
+        if (kernels & MS_K_WGRAD) ws = std::max(ws, ms::conv_wgrad_workspace(pl.dtype, pl.g, false));
+        if (kernels & MS_K_BGRAD) ws = std::max(ws, ms::colsum_workspace(pl.dtype, pl.rows, pl.g.C));
     } else if (pl.kind == MS_BN_EVAL) {
         if (kernels & (MS_K_WGRAD | MS_K_BGRAD)) ws = ms::bn_bwd_workspace(pl.dtype, pl.rows, pl.C);
     }
@@ -438,8 +496,9 @@ ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
     // transient forward workspace (zero-padded channel copies for channel
     // counts that are not a multiple of 8), taken before anything is launched
     void *fws = nullptr;
-    if (pl.kind == MS_CONV2D || pl.kind == MS_LINEAR) {
-        const size_t fb = ms::conv_fwd_workspace(pl.dtype, pl.g);
+    if (pl.kind == MS_CONV2D || pl.kind == MS_LINEAR || pl.kind == MS_CONV_TRANSPOSE2D) {
+        const size_t fb = pl.kind == MS_CONV_TRANSPOSE2D ? ms::conv_dgrad_workspace(pl.dtype, pl.g)
+                                                         : ms::conv_fwd_workspace(pl.dtype, pl.g);
         if (fb) {
             int werr = 0;
             fws = ms::workspace_get(stream, fb, &werr);
@@ -457,6 +516,10 @@ ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
     case MS_CONV2D:
     case MS_LINEAR:
         err = ms::launch_conv_fwd(pl.dtype, pl.g, x->data, W->data, b ? b->data : nullptr, y->data, fws, stream);
+        break;
+    case MS_CONV_TRANSPOSE2D:   // the input-gradient contraction of the convolution y -> x, plus b
+        err = ms::launch_conv_dgrad(pl.dtype, pl.g, x->data, W->data, b ? b->data : nullptr, y->data, fws,
+                                    stream);
         break;
     case MS_BN_EVAL:
         err = ms::launch_bn_fwd(pl.dtype, x->data, layer->running_mean->data, layer->running_var->data,
@@ -537,12 +600,27 @@ ms_status ms_layer_backward(ms_record *r, const ms_tensor *grad_y, const ms_tens
     case MS_LINEAR:
     {
         bool db_done = false;
-        if (!err && (kernels & MS_K_DGRAD)) err = ms::launch_conv_dgrad(pl.dtype, pl.g, dy, r->W.data, grad_x->data, ws, stream);
+        if (!err && (kernels & MS_K_DGRAD))
+            err = ms::launch_conv_dgrad(pl.dtype, pl.g, dy, r->W.data, nullptr, grad_x->data, ws, stream);
         if (!err && (kernels & MS_K_WGRAD))
             err = ms::launch_conv_wgrad(pl.dtype, pl.g, dy, r->x.data, grad_W->data,
                                         (kernels & MS_K_BGRAD) ? grad_b->data : nullptr, ws, stream, &db_done);
         if (!err && (kernels & MS_K_BGRAD) && !db_done)
             err = ms::launch_colsum(pl.dtype, dy, pl.rows, pl.g.K, grad_b->data, ws, stream);
+    }
+        break;
+    case MS_CONV_TRANSPOSE2D:
+    {
+        // adjoint of the convolution g (input y-shaped, output x-shaped): the
+        // input gradient is g's forward of grad_y; the weight gradient is g's
+        // weight gradient with x as its output gradient and grad_y as its input
+        bool db_unused = false;
+        if (kernels & MS_K_DGRAD)
+            err = ms::launch_conv_fwd(pl.dtype, pl.g, dy, r->W.data, nullptr, grad_x->data, ws, stream);
+        if (!err && (kernels & MS_K_WGRAD))
+            err = ms::launch_conv_wgrad(pl.dtype, pl.g, r->x.data, dy, grad_W->data, nullptr, ws, stream, &db_unused);
+        if (!err && (kernels & MS_K_BGRAD))
+            err = ms::launch_colsum(pl.dtype, dy, pl.rows, pl.g.C, grad_b->data, ws, stream);
     }
         break;
     case MS_BN_EVAL:

@@ -29,6 +29,8 @@ def layer_call(la, dtype: str) -> LayerCall:
     s = la.spec
     if s.kind == "conv2d":
         spec = ms.Conv2d(s.stride, s.pad)
+    elif s.kind == "conv_transpose2d":
+        spec = ms.ConvTranspose2d(s.stride, s.pad, s.out_pad)
     elif s.kind == "linear":
         spec = ms.Linear()
     elif s.kind == "bn_eval":

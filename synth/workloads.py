@@ -21,13 +21,14 @@ MASK_INPUT, MASK_WEIGHT, MASK_BIAS = 1, 2, 4
 
 @dataclass
 class LayerSpec:
-    kind: str                      # "conv2d" | "linear" | "bn_eval" | "avgpool"
+    kind: str                      # "conv2d" | "conv_transpose2d" | "linear" | "bn_eval" | "avgpool"
     name: str
     in_shape: Tuple[int, ...]      # conv/bn/avgpool: logical (N, C, H, W); linear: (M, K_in)
-    out_ch: int = 0                # conv: K; linear: N_out
+    out_ch: int = 0                # conv: K; transposed conv: C_out; linear: N_out
     ksize: Tuple[int, int] = (1, 1)
     stride: Tuple[int, int] = (1, 1)
     pad: Tuple[int, int] = (0, 0)
+    out_pad: Tuple[int, int] = (0, 0)   # transposed conv only
     has_bias: bool = False
     mask: int = 0
     eps: float = 1e-5
@@ -43,6 +44,12 @@ class LayerSpec:
             p = (h + 2 * self.pad[0] - r) // self.stride[0] + 1
             q = (w + 2 * self.pad[1] - s) // self.stride[1] + 1
             return (n, self.out_ch, p, q)
+        if self.kind == "conv_transpose2d":
+            n, _, h, w = self.in_shape
+            r, s = self.ksize
+            ho = (h - 1) * self.stride[0] - 2 * self.pad[0] + r + self.out_pad[0]
+            wo = (w - 1) * self.stride[1] - 2 * self.pad[1] + s + self.out_pad[1]
+            return (n, self.out_ch, ho, wo)
         if self.kind == "linear":
             return (self.in_shape[0], self.out_ch)
         if self.kind == "bn_eval":
@@ -54,6 +61,8 @@ class LayerSpec:
     def weight_shape(self) -> Optional[Tuple[int, ...]]:
         if self.kind == "conv2d":
             return (self.out_ch, self.in_shape[1], self.ksize[0], self.ksize[1])
+        if self.kind == "conv_transpose2d":
+            return (self.in_shape[1], self.out_ch, self.ksize[0], self.ksize[1])
         if self.kind == "linear":
             return (self.out_ch, self.in_shape[1])
         if self.kind == "bn_eval":
@@ -93,6 +102,20 @@ def _conv(name, in_shape, k, r, stride, pad, mask, seeds, bias, bias_law=None):
         init["b"] = bias_law or ("kaiming", (fan_in,))
         sd["b"] = seeds()
     return LayerSpec("conv2d", name, tuple(in_shape), out_ch=k, ksize=(r, r),
+                     stride=(stride, stride), pad=(pad, pad), has_bias=bias,
+                     mask=mask, init=init, seeds=sd)
+
+
+def _convt(name, in_shape, c_out, r, stride, pad, mask, seeds, bias):
+    """Transposed conv with PyTorch's default init law: the fan-in of a
+    ConvTranspose weight [C_in, C_out, R, S] is C_out * R * S."""
+    fan_in = c_out * r * r
+    init = {"W": ("kaiming", (fan_in,))}
+    sd = {"W": seeds()}
+    if bias:
+        init["b"] = ("kaiming", (fan_in,))
+        sd["b"] = seeds()
+    return LayerSpec("conv_transpose2d", name, tuple(in_shape), out_ch=c_out, ksize=(r, r),
                      stride=(stride, stride), pad=(pad, pad), has_bias=bias,
                      mask=mask, init=init, seeds=sd)
 
@@ -237,10 +260,29 @@ def encoder_linears_bf16(layers: int = 12, tokens: int = 16 * 512) -> Workload:
     return w
 
 
+def decoder_convt_bf16(batch: int = 32, mask: int = MASK_INPUT | MASK_WEIGHT | MASK_BIAS) -> Workload:
+    """The upsampling path of an image decoder: three bf16 ConvTranspose2d
+    layers with bias, 512x14x14 -> 256x28x28 (4x4, stride 2, pad 1) ->
+    128x56x56 (4x4, stride 2, pad 1) -> 64x112x112 (2x2, stride 2), every
+    layer trained (mask I, W, B by default)."""
+    s = _Seeds(6)
+    x_seed = s()
+    layers = []
+    shape = (batch, 512, 14, 14)
+    for name, cout, r, pad in (("up1", 256, 4, 1), ("up2", 128, 4, 1), ("up3", 64, 2, 0)):
+        layers.append(_convt(name, shape, cout, r, 2, pad, mask, s, bias=True))
+        shape = layers[-1].out_shape()
+    w = Workload(6, "decoder_convt_bf16", "bf16", layers, input_seed=x_seed,
+                 note=f"x[{batch},512,14,14], ConvTranspose2d 4x4/s2/p1 512->256, 4x4/s2/p1 256->128, "
+                      f"2x2/s2 128->64")
+    w.grad_seed = s()
+    return w
+
+
 def all_workloads() -> Dict[str, Workload]:
     d = {"1": single_conv_f32(), "2": linear_stack_bf16(),
          "3": resnet18_shaped_bf16(), "3b": resnet18_shaped_bf16(input_requires_grad=True),
-         "5": encoder_linears_bf16()}
+         "5": encoder_linears_bf16(), "6": decoder_convt_bf16()}
     for mk in CONV_SWEEP_MASKS:
         d[f"4_3x3_{mk}"] = conv_sweep_bf16(mk)
         d[f"4_1x1_{mk}"] = conv_sweep_bf16(mk, pointwise=True)

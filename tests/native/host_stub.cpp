@@ -69,8 +69,9 @@ size_t conv_dgrad_workspace(int dtype, const ConvGeom &g) {
     return dtype == kBF16 ? (size_t)g.K * g.R * g.S * g.C * 2 : 0;
 }
 
-int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *w, void *dx, void *ws, void *) {
-    log("conv_dgrad");
+int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *w, const void *bias, void *dx,
+                      void *ws, void *) {
+    log(bias ? "conv_dgrad+bias" : "conv_dgrad");
     if (conv_dgrad_workspace(dtype, g) > 0 && !ws) return need(false, "conv_dgrad:ws");
     const long long out = (long long)g.N * g.H * g.W * g.C;
     int e = 0;

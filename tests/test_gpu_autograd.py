@@ -174,3 +174,114 @@ def test_synthetic_deep_cnn_retains_exactly_the_saved_inputs(case):
     # the first record borrows x, which `base` already includes
     assert held == want - (nbytes if case == "all" else 0)
     y.backward(torch.ones_like(y))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("flags", list(itertools.product([False, True], repeat=3)))
+def test_conv_transpose2d_function_masks(dtype, flags):
+    rx, rw, rb = flags
+    xs, ws, st, pd, op = (2, 16, 5, 6), (16, 8, 4, 3), (2, 2), (1, 1), (1, 0)
+    x = synth.normal(xs, 9830, dtype=dtype)
+    w = synth.kaiming_uniform(ws, 9831, 8 * 12, dtype=dtype)
+    b = synth.normal((8,), 9832, 0.1, dtype=dtype)
+    xt = _leaf(x, dtype, rx)
+    m = msa.MSConvTranspose2d(nn.Parameter(dev(w, dtype), requires_grad=rw),
+                              nn.Parameter(dev(b, dtype), requires_grad=rb), st, pd, op)
+    y = m(xt)
+    assert oracle.rel_err(host(y), oracle.convt2d_forward(x, w, b, st, pd, op)) <= TOL[dtype]
+    if not (rx or rw or rb):
+        assert y.grad_fn is None
+        return
+    gy = synth.normal(tuple(y.shape), 9833, dtype=dtype)
+    y.backward(dev(gy, dtype))
+    if rx:
+        assert oracle.rel_err(host(xt.grad), oracle.convt2d_input_grad(gy, w, xs, st, pd, op)) <= TOL[dtype]
+    if rw:
+        assert oracle.rel_err(host(m.weight.grad), oracle.convt2d_weight_grad(gy, x, ws, st, pd, op)) <= TOL[dtype]
+    if rb:
+        assert oracle.rel_err(host(m.bias.grad), oracle.convt2d_bias_grad(gy)) <= TOL[dtype]
+    assert (xt.grad is None) == (not rx) and (m.weight.grad is None) == (not rw) and (m.bias.grad is None) == (not rb)
+
+
+@pytest.mark.parametrize("transposed", [False, True])
+@pytest.mark.parametrize("flags", [(True, True, True), (True, False, False), (False, True, True)])
+def test_one_dimensional_layers(transposed, flags):
+    """Conv1d / ConvTranspose1d from torch.nn, converted, against the oracle
+    of the 2-D layer with H = R = 1 (a plain [N, C, L] input that is not
+    channels-inner is converted on the way in)."""
+    rx, rw, rb = flags
+    torch.manual_seed(3)
+    if transposed:
+        ref = nn.ConvTranspose1d(8, 16, 4, stride=2, padding=1, output_padding=1).cuda()
+    else:
+        ref = nn.Conv1d(8, 16, 3, stride=2, padding=1).cuda()
+    w = ref.weight.detach().cpu().numpy().astype(np.float64)
+    b = ref.bias.detach().cpu().numpy().astype(np.float64)
+    ref.weight.requires_grad_(rw)
+    ref.bias.requires_grad_(rb)
+    net = msa.convert(nn.Sequential(ref))
+    assert isinstance(net[0], msa.MSConvTranspose1d if transposed else msa.MSConv1d)
+    x = synth.normal((3, 8, 21), 9840)
+    xt = torch.from_numpy(x.astype(np.float32)).cuda().requires_grad_(rx)
+    y = net(xt)
+    x4, w4 = x[:, :, None, :], w[:, :, None, :]
+    if transposed:
+        want = oracle.convt2d_forward(x4, w4, b, (1, 2), (0, 1), (0, 1))[:, :, 0, :]
+    else:
+        want = oracle.conv2d_forward(x4, w4, b, (1, 2), (0, 1))[:, :, 0, :]
+    assert tuple(y.shape) == want.shape
+    assert oracle.rel_err(host(y), want) <= TOL["f32"]
+    gy = synth.normal(want.shape, 9841)
+    y.backward(torch.from_numpy(gy.astype(np.float32)).cuda())
+    g4 = gy[:, :, None, :]
+    if transposed:
+        gx = oracle.convt2d_input_grad(g4, w4, x4.shape, (1, 2), (0, 1), (0, 1))
+        gw = oracle.convt2d_weight_grad(g4, x4, w4.shape, (1, 2), (0, 1), (0, 1))
+    else:
+        gx = oracle.conv2d_input_grad(g4, w4, x4.shape, (1, 2), (0, 1))
+        gw = oracle.conv2d_weight_grad(g4, x4, w4.shape, (1, 2), (0, 1))
+    if rx:
+        assert oracle.rel_err(host(xt.grad), gx[:, :, 0, :]) <= TOL["f32"]
+    if rw:
+        assert oracle.rel_err(host(net[0].weight.grad), gw[:, :, 0, :]) <= TOL["f32"]
+    if rb:
+        assert oracle.rel_err(host(net[0].bias.grad), oracle.conv2d_bias_grad(g4)) <= TOL["f32"]
+    assert (net[0].weight.grad is None) == (not rw)
+
+
+@pytest.mark.parametrize("kind", ["conv_transpose2d", "conv1d", "conv_transpose1d"])
+@pytest.mark.parametrize("case", ["all", "layers_4_plus", "layer_4_only"])
+def test_appendix_b_layers_retain_exactly_the_saved_inputs(kind, case):
+    """App. B repeats the Fig. 1 experiment with the other layers that are
+    linear in input and weight; at test size, a stack of 8 size-preserving
+    layers with 8 channels and kernel 3, fp32: after the forward pass the
+    allocator holds exactly the inputs the save rule keeps."""
+    from oracle import policy as P
+    depth = 8
+    xs = (4, 8, 64, 64) if kind == "conv_transpose2d" else (16, 8, 1024)
+    nel = int(np.prod(xs))
+    torch.manual_seed(2)
+    mk = {"conv_transpose2d": lambda: nn.ConvTranspose2d(8, 8, 3, padding=1, bias=False),
+          "conv1d": lambda: nn.Conv1d(8, 8, 3, padding=1, bias=False),
+          "conv_transpose1d": lambda: nn.ConvTranspose1d(8, 8, 3, padding=1, bias=False)}[kind]
+    layers = [mk().cuda() for _ in range(depth)]
+    for i, c in enumerate(layers):
+        layer = i + 1
+        c.weight.requires_grad_(case == "all" or (case == "layers_4_plus" and layer >= 4)
+                                or (case == "layer_4_only" and layer == 4))
+    net = msa.convert(nn.Sequential(*layers))
+    x = torch.randn(xs, device="cuda")
+    x = x.contiguous(memory_format=torch.channels_last) if len(xs) == 4 else x.transpose(1, 2).contiguous().transpose(1, 2)
+    x.requires_grad_(case == "all")
+    torch.cuda.synchronize()
+    base = torch.cuda.memory_allocated()
+    y = net(x)
+    torch.cuda.synchronize()
+    held = torch.cuda.memory_allocated() - base - y.numel() * 4
+    kind2 = "conv2d" if kind == "conv1d" else "conv_transpose2d"
+    masks = P.propagate([2 if c.weight.requires_grad else 0 for c in layers], case == "all")
+    want = P.stack_saved_bytes([(kind2, m, nel, "f32", True, False) for m in masks])
+    assert want == {"all": 8, "layers_4_plus": 5, "layer_4_only": 1}[case] * nel * 4
+    assert held == want - (nel * 4 if case == "all" else 0)
+    y.backward(torch.ones_like(y))
+    assert (layers[3].weight.grad is not None) and (layers[0].weight.grad is None) == (case != "all")

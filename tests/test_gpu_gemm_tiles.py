@@ -177,3 +177,43 @@ def test_linear_tiles_split(tile, shape, splits):
     assert gw is None
     check("dX", host(gx), oracle.linear_input_grad(gy, w), "bf16")
     check("db", host(gb), oracle.linear_bias_grad(gy), "bf16")
+
+
+CONVT_CASES = [
+    # x shape, C_out, (R, S), stride, pad, out_pad
+    ((2, 24, 7, 6), 40, (4, 4), (2, 2), (1, 1), (1, 0)),
+    ((2, 64, 5, 5), 264, (3, 3), (1, 1), (1, 1), (0, 0)),    # several 256-wide tiles, ragged
+    ((1, 16, 9, 8), 12, (2, 2), (2, 2), (0, 0), (0, 0)),     # 12 output channels: padded, bias padded
+]
+
+
+def _convt_case(case, seed):
+    xs, co, k, st, pd, op = CONVT_CASES[case]
+    ws = (xs[1], co, k[0], k[1])
+    x = synth.normal(xs, seed, dtype="bf16")
+    w = synth.kaiming_uniform(ws, seed + 1, co * k[0] * k[1], dtype="bf16")
+    b = synth.normal((co,), seed + 2, 0.1, dtype="bf16")
+    y, rec = ms.layer_forward(ms.ConvTranspose2d(st, pd, op), dev(x, "bf16"), dev(w, "bf16"), dev(b, "bf16"), 7)
+    check("y", host(y), oracle.convt2d_forward(x, w, b, st, pd, op), "bf16")
+    gy = synth.normal(tuple(y.shape), seed + 3, dtype="bf16")
+    gx, gw, gb = ms.layer_backward(rec, dev(gy, "bf16"))
+    check("dx", host(gx), oracle.convt2d_input_grad(gy, w, xs, st, pd, op), "bf16")
+    check("dW", host(gw), oracle.convt2d_weight_grad(gy, x, ws, st, pd, op), "bf16")
+    check("db", host(gb), oracle.convt2d_bias_grad(gy), "bf16")
+
+
+@pytest.mark.parametrize("tile", TILES, indirect=True)
+@pytest.mark.parametrize("case", range(len(CONVT_CASES)))
+def test_conv_transpose_tiles(tile, case, dgrad_variant):
+    """The transposed convolution on every tile and input-gradient variant:
+    its forward is the input-gradient contraction with the bias added in the
+    epilogue, its input gradient the forward contraction."""
+    _convt_case(case, 8800 + 10 * case)
+
+
+@pytest.mark.parametrize("splits", ["3"], indirect=True)
+@pytest.mark.parametrize("tile", TILES, indirect=True)
+@pytest.mark.parametrize("case", range(len(CONVT_CASES)))
+def test_conv_transpose_tiles_split(tile, case, splits):
+    """Split reductions: the bias is added once, by the reduce pass."""
+    _convt_case(case, 8900 + 10 * case)

@@ -37,6 +37,8 @@ def oracle_chain(ca, dtype, rows=None, want_grads=True):
         a = acts[-1]
         if s.kind == "conv2d":
             y = oracle.conv2d_forward(a, la.W, la.b, s.stride, s.pad)
+        elif s.kind == "conv_transpose2d":
+            y = oracle.convt2d_forward(a, la.W, la.b, s.stride, s.pad, s.out_pad)
         elif s.kind == "linear":
             y = oracle.linear_forward(a, la.W, la.b)
         elif s.kind == "bn_eval":
@@ -61,6 +63,13 @@ def oracle_chain(ca, dtype, rows=None, want_grads=True):
                 gw = oracle.conv2d_weight_grad(g, a, la.W.shape, s.stride, s.pad)
             if m & 4:
                 gb = oracle.conv2d_bias_grad(g)
+        elif s.kind == "conv_transpose2d":
+            if m & 1:
+                gx = oracle.convt2d_input_grad(g, la.W, a.shape, s.stride, s.pad, s.out_pad)
+            if m & 2:
+                gw = oracle.convt2d_weight_grad(g, a, la.W.shape, s.stride, s.pad, s.out_pad)
+            if m & 4:
+                gb = oracle.convt2d_bias_grad(g)
         elif s.kind == "linear":
             if m & 1:
                 gx = oracle.linear_input_grad(g, la.W)
@@ -294,4 +303,59 @@ def test_resnet18_shaped_bn_and_head_full_size():
             _, gw, gb = ms.layer_backward(rec, gpu.dev(gy, "bf16"))
             check("fc dW", host(gw), oracle.linear_weight_grad(gy, x), "bf16")
             check("fc db", host(gb), oracle.linear_bias_grad(gy), "bf16")
+        torch.cuda.empty_cache()
+
+
+# ------------------------------------------------------------------ transposed convolutions
+def test_decoder_convt_stack_reduced():
+    """The three-layer ConvTranspose2d decoder at batch 2, every element of
+    every activation and gradient, and the ledger against the closed form."""
+    w = wl.decoder_convt_bf16(batch=2)
+    ca = draw.chains(w)[0]
+    chain, peak = run_gpu_chain(ca, "bf16")
+    acts, grads = oracle_chain(ca, "bf16")
+    compare_chain(chain, acts, grads, "bf16")
+    assert peak == P.stack_saved_bytes(_layers_bytes(w), P.SELECTIVE)
+
+
+def _convt_layer_full(spec, dtype, seed, samples=2048):
+    import synth
+    la = draw.layer_arrays(spec, dtype)
+    x = synth.normal(spec.in_shape, seed, dtype=dtype)
+    gy = synth.normal(spec.out_shape(), seed + 1, dtype=dtype)
+    st, pd, op = spec.stride, spec.pad, spec.out_pad
+    y, rec = ms.layer_forward(ms.ConvTranspose2d(st, pd, op), gpu.dev(x, dtype), gpu.dev(la.W, dtype),
+                              gpu.dev(la.b, dtype), spec.mask)
+    yh = host(y)
+    rng = np.random.default_rng(seed)
+    dims = yh.shape
+    idx = np.stack([rng.integers(0, d, samples) for d in dims], 1)
+    idx = np.concatenate([idx, [[0, 0, 0, 0], [d - 1 for d in dims], [0, dims[1] - 1, 0, dims[3] - 1],
+                                [dims[0] - 1, 0, dims[2] - 1, 0]]])
+    check("y@", yh[tuple(idx.T)], oracle.convt2d_forward_at(x, la.W, la.b, st, pd, op, idx), dtype)
+    if rec is None:
+        return
+    gx, gw, gb = ms.layer_backward(rec, gpu.dev(gy, dtype))
+    if gx is not None:
+        gxh = host(gx)
+        idx = np.stack([rng.integers(0, d, samples) for d in gxh.shape], 1)
+        idx = np.concatenate([idx, [[0, 0, 0, 0], [d - 1 for d in gxh.shape]]])
+        check("dx@", gxh[tuple(idx.T)], oracle.convt2d_input_grad_at(gy, la.W, spec.in_shape, st, pd, op, idx),
+              dtype)
+    if gw is not None:
+        gwh = host(gw)
+        idx = np.stack([rng.integers(0, d, 512) for d in gwh.shape], 1)
+        idx = np.concatenate([idx, [[0, 0, 0, 0], [d - 1 for d in gwh.shape]]])
+        check("dW@", gwh[tuple(idx.T)], oracle.convt2d_weight_grad_at(gy, x, la.W.shape, st, pd, op, idx), dtype)
+    if gb is not None:
+        check("db", host(gb), oracle.convt2d_bias_grad(gy), dtype)
+
+
+def test_decoder_convt_layers_full_size():
+    """Every layer of the decoder at the benchmark's batch of 32, with every
+    gradient requested, at sampled entries (corners included); the bias
+    gradient in full."""
+    w = wl.decoder_convt_bf16()
+    for i, spec in enumerate(w.layers):
+        _convt_layer_full(spec, "bf16", 4600 + 10 * i)
         torch.cuda.empty_cache()

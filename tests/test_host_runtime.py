@@ -20,7 +20,8 @@ NATIVE = os.path.join(ROOT, "tests", "native")
 BUILD = os.path.join(NATIVE, "_build")
 STUB_SO = os.path.join(BUILD, "libmemsave_hoststub.so")
 DT = {"f32": L.MS_F32, "bf16": L.MS_BF16}
-KIND = {"conv2d": L.MS_CONV2D, "linear": L.MS_LINEAR, "bn_eval": L.MS_BN_EVAL, "avgpool": L.MS_AVGPOOL}
+KIND = {"conv2d": L.MS_CONV2D, "linear": L.MS_LINEAR, "bn_eval": L.MS_BN_EVAL, "avgpool": L.MS_AVGPOOL,
+        "conv_transpose2d": L.MS_CONV_TRANSPOSE2D}
 FAKE = 0x7f0000000000  # a 256-byte aligned address nobody dereferences
 
 
@@ -77,6 +78,7 @@ class LayerArgs:
         self.layer.kind = KIND[spec.kind]
         self.layer.stride[0], self.layer.stride[1] = spec.stride
         self.layer.pad[0], self.layer.pad[1] = spec.pad
+        self.layer.out_pad[0], self.layer.out_pad[1] = spec.out_pad
         self.layer.eps = spec.eps
         self.x = tdesc(spec.in_shape, dtype, data=data, addr=addr)
         ws = spec.weight_shape()
@@ -186,7 +188,8 @@ def _grads(a, mask):
 def test_forward_backward_plan(stub, label, spec, dtype):
     a = LayerArgs(spec, dtype)
     masks = [0, 1] if spec.kind == "avgpool" else range(8)
-    fwd_name = {"conv2d": "conv_fwd", "linear": "conv_fwd", "bn_eval": "bn_fwd", "avgpool": "avgpool_fwd"}[spec.kind]
+    fwd_name = {"conv2d": "conv_fwd", "linear": "conv_fwd", "bn_eval": "bn_fwd", "avgpool": "avgpool_fwd",
+                "conv_transpose2d": "conv_dgrad+bias" if spec.has_bias else "conv_dgrad"}[spec.kind]
     for mask in masks:
         if (mask & 4) and a.b is None:
             continue
@@ -224,6 +227,9 @@ def test_forward_backward_plan(stub, label, spec, dtype):
             fused = "conv_wgrad+db" in log
             assert (("colsum" in log) or fused) == plan["bgrad"]
             assert not (fused and "colsum" in log)
+        elif spec.kind == "conv_transpose2d":
+            assert log == [n for n, f in (("conv_fwd", "dgrad"), ("conv_wgrad", "wgrad"), ("colsum", "bgrad"))
+                           if plan[f]]
         elif spec.kind == "bn_eval":
             assert log == ["bn_bwd"]
         else:
@@ -505,3 +511,118 @@ def test_relu_policy_account(stub, dtype):
     a = L.MsAccount()
     assert stub.ms_policy_account(ctypes.byref(layer), ref(x), ref(tdesc((4,), dtype)), None, 1, 0,
                                   ctypes.byref(a)) == L.MS_E_ARG
+
+
+# ------------------------------------------------------------------ transposed convolution
+class ConvTArgs:
+    """MsLayer + tensors of a transposed convolution x[N,Ci,H,W], W[Ci,Co,R,S]."""
+
+    def __init__(self, x_shape, Co, k, stride, pad, out_pad, dtype="bf16", bias=True, data=True):
+        N, Ci, H, W = x_shape
+        self.layer = L.MsLayer()
+        self.layer.kind = L.MS_CONV_TRANSPOSE2D
+        self.layer.stride[0], self.layer.stride[1] = stride
+        self.layer.pad[0], self.layer.pad[1] = pad
+        self.layer.out_pad[0], self.layer.out_pad[1] = out_pad
+        Ho = (H - 1) * stride[0] - 2 * pad[0] + k[0] + out_pad[0]
+        Wo = (W - 1) * stride[1] - 2 * pad[1] + k[1] + out_pad[1]
+        self.x_shape, self.w_shape, self.y_shape = x_shape, (Ci, Co, k[0], k[1]), (N, Co, Ho, Wo)
+        self.x = tdesc(x_shape, dtype, data=data)
+        self.W = tdesc(self.w_shape, dtype, data=data)
+        self.b = tdesc((Co,), dtype, data=data) if bias else None
+        self.y = tdesc(self.y_shape, dtype, data=data)
+        self.dtype = dtype
+
+
+CONVT = [
+    ((2, 16, 5, 7), 8, (4, 4), (2, 2), (1, 1), (0, 0)),
+    ((1, 12, 6, 6), 3, (3, 3), (2, 2), (1, 1), (1, 1)),
+    ((3, 8, 4, 5), 24, (2, 2), (2, 2), (0, 0), (0, 0)),
+    ((1, 8, 1, 40), 8, (1, 3), (1, 1), (0, 1), (0, 0)),     # a 1-D transposed convolution
+]
+
+
+@pytest.mark.parametrize("case", range(len(CONVT)))
+def test_conv_transpose_policy_matches_closed_form(stub, case):
+    a = ConvTArgs(*CONVT[case], data=False)
+    numel = _numel(a.x_shape)
+    for mask in range(8):
+        for pol in (P.SELECTIVE, P.PYTORCH_DEFAULT, P.ALL_TRUE):
+            acct = L.MsAccount()
+            st = stub.ms_policy_account(ctypes.byref(a.layer), ref(a.x), ref(a.W), ref(a.b), mask, pol,
+                                        ctypes.byref(acct))
+            assert st == 0, stub.ms_last_error()
+            assert acct.saved_activation_bytes == P.saved_activation_bytes("conv_transpose2d", mask, numel,
+                                                                           a.dtype, pol)
+            sv = P.saved_tensors("conv_transpose2d", mask, pol)
+            assert bool(acct.borrowed & L.MS_SAVED_X) == sv["x"]
+            assert bool(acct.borrowed & L.MS_SAVED_W) == sv["W"]
+
+
+@pytest.mark.parametrize("case", range(len(CONVT)))
+def test_conv_transpose_forward_backward_plan(stub, case):
+    """Forward: the input-gradient contraction (with the bias when there is
+    one).  Backward: the forward contraction for dx, the weight-gradient
+    contraction for dW (never with a fused bias: its column sums would be
+    those of x), a column sum of grad_y for db -- each only under its flag."""
+    for bias in (True, False):
+        a = ConvTArgs(*CONVT[case], bias=bias)
+        for mask in range(8):
+            if (mask & 4) and not bias:
+                continue
+            stub.stub_reset()
+            h = ctypes.c_void_p()
+            st = stub.ms_layer_forward(ctypes.byref(a.layer), ref(a.x), ref(a.W), ref(a.b), mask, ref(a.y),
+                                       ctypes.byref(h), None)
+            assert st == 0, stub.ms_last_error()
+            assert stub.stub_log().decode() == ("conv_dgrad+bias;" if bias else "conv_dgrad;")
+            assert stub.stub_violations().decode() == ""
+            if mask == 0:
+                assert not h.value
+                continue
+            stub.stub_reset()
+            gy = tdesc(a.y_shape)
+            gx = tdesc(a.x_shape) if mask & 1 else None
+            gw = tdesc(a.w_shape) if mask & 2 else None
+            gb = tdesc((a.w_shape[1],)) if mask & 4 else None
+            assert stub.ms_layer_backward(h, ref(gy), ref(gx), ref(gw), ref(gb), None) == 0, stub.ms_last_error()
+            assert stub.stub_violations().decode() == ""
+            want = [n for n, f in (("conv_fwd", 1), ("conv_wgrad", 2), ("colsum", 4)) if mask & f]
+            assert stub.stub_log().decode().split(";")[:-1] == want
+            stub.ms_record_free(h)
+    assert stub.ms_testing_live_records() == 0
+
+
+def test_conv_transpose_validation(stub):
+    def fwd(a, mask=7, x=None, W=None, b="keep", y=None):
+        h = ctypes.c_void_p()
+        stub.stub_reset()
+        st = stub.ms_layer_forward(ctypes.byref(a.layer), ref(x or a.x), ref(W or a.W),
+                                   ref(a.b if b == "keep" else b), mask, ref(y or a.y), ctypes.byref(h), None)
+        assert stub.stub_log().decode() == "" and not h.value
+        return st
+
+    a = ConvTArgs((2, 16, 5, 7), 8, (4, 4), (2, 2), (1, 1), (1, 0))
+    assert fwd(a, y=tdesc((2, 8, 10, 14))) == L.MS_E_SHAPE        # out_pad ignored in y
+    assert fwd(a, W=tdesc((8, 16, 4, 4))) == L.MS_E_SHAPE          # W given as [Co, Ci, R, S]
+    assert fwd(a, W=tdesc(a.w_shape, layout="nchw")) == L.MS_E_LAYOUT
+    assert fwd(a, x=tdesc(a.x_shape, layout="nchw")) == L.MS_E_LAYOUT
+    assert fwd(a, b=tdesc((16,))) == L.MS_E_SHAPE                  # bias has C_out entries
+    assert fwd(a, x=tdesc(a.x_shape, "f32")) == L.MS_E_DTYPE
+    a.layer.out_pad[0] = 2                                          # out_pad >= stride
+    assert fwd(a) == L.MS_E_ARG
+    a.layer.out_pad[0] = -1
+    assert fwd(a) == L.MS_E_ARG
+    a.layer.out_pad[0] = 1
+    a.layer.stride[1] = 0
+    assert fwd(a) == L.MS_E_ARG
+    a.layer.stride[1] = 2
+    # an output that would be empty: H = 1, R = 1, pad 1
+    e = ConvTArgs((1, 8, 1, 4), 8, (1, 3), (1, 1), (0, 0), (0, 0))
+    e.layer.pad[0] = 1
+    assert fwd(e, y=tdesc((1, 8, 1, 6))) == L.MS_E_SHAPE
+    # the forward is valid once everything matches
+    h = ctypes.c_void_p()
+    assert stub.ms_layer_forward(ctypes.byref(a.layer), ref(a.x), ref(a.W), ref(a.b), 7, ref(a.y),
+                                 ctypes.byref(h), None) == 0, stub.ms_last_error()
+    stub.ms_record_free(h)
