@@ -13,6 +13,7 @@ any float dtype are widened to float64, outputs are float64.
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 
 import numpy as np
@@ -28,6 +29,8 @@ __all__ = [
     "linear_weight_grad", "linear_weight_grad_at", "linear_bias_grad",
     "bn_eval_forward", "bn_eval_backward", "avgpool_forward", "avgpool_backward",
     "relu_forward", "relu_mask_bits", "relu_backward", "relu_mask_nbytes", "memory_order",
+    "philox4x32_10", "dropout_threshold", "dropout_scale", "dropout_words", "dropout_keep", "dropout_forward",
+    "dropout_backward",
     "round_to", "rel_err",
 ]
 
@@ -432,3 +435,73 @@ def rel_err(got, ref):
 def threads() -> int:
     """OpenMP threads the oracle's loops use."""
     return int(_load().orc_threads())
+
+
+# ----------------------------------------------------------------- dropout
+_U32 = ctypes.POINTER(ctypes.c_uint32)
+
+
+def philox4x32_10(ctr, key):
+    """One Philox4x32-10 block (Salmon et al., SC 2011): 4 counter words and
+    2 key words in, 4 words out."""
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    assert c.shape == (4,) and k.shape == (2,)
+    out = np.empty(4, np.uint32)
+    _load().orc_philox4x32_10(c.ctypes.data_as(_U32), k.ctypes.data_as(_U32), out.ctypes.data_as(_U32))
+    return out
+
+
+def dropout_threshold(p):
+    """(thresh, drop_all) of drop probability p taken as a float32: an element
+    is kept iff its stream word is >= floor(p * 2^32); p = 1 drops every
+    element (Sec. 2.2.2 leaves the generator and the draw to the
+    implementation)."""
+    p32 = float(np.float32(p))
+    if not (0.0 <= p32 <= 1.0):
+        raise ValueError("p must lie in [0, 1]")
+    if p32 == 1.0:
+        return 0, True
+    return int(math.floor(p32 * 4294967296.0)), False
+
+
+def dropout_scale(p):
+    """1 / (1 - p) for p taken as a float32, rounded to float32 (0 when p = 1)."""
+    p32 = float(np.float32(p))
+    return 0.0 if p32 == 1.0 else float(np.float32(1.0 / (1.0 - p32)))
+
+
+def dropout_words(n, seed, offset=0):
+    """The n stream words of one call (element i: word i mod 4 of block
+    offset + i // 4 under key `seed`)."""
+    u = np.empty(int(n), np.uint32)
+    if n > 0:
+        _load().orc_dropout_words(_I(int(n)), ctypes.c_uint64(int(seed)), ctypes.c_uint64(int(offset)),
+                                  u.ctypes.data_as(_U32))
+    return u
+
+
+def dropout_keep(n, p, seed, offset=0):
+    """Which of n elements (memory order) are kept."""
+    t, drop_all = dropout_threshold(p)
+    if drop_all:
+        return np.zeros(int(n), bool)
+    return dropout_words(n, seed, offset) >= np.uint32(t)
+
+
+def dropout_forward(x_mem, p, seed, offset=0):
+    """y = x * m / (1 - p) over a flat array in memory order, m the kept
+    mask: each element is multiplied by 1/(1-p) (float32) when kept and by 0
+    when dropped; p = 1 gives zeros."""
+    x = np.asarray(x_mem, dtype=np.float64).reshape(-1)
+    t, drop_all = dropout_threshold(p)
+    if drop_all:
+        return np.zeros_like(x)
+    s = np.where(dropout_keep(x.size, p, seed, offset), dropout_scale(p), 0.0)
+    return x * s
+
+
+def dropout_backward(dy_mem, p, seed, offset=0):
+    """dx = dy * m / (1 - p) with the mask drawn again from the same counters
+    (the forward map is linear with that diagonal Jacobian)."""
+    return dropout_forward(dy_mem, p, seed, offset)

@@ -7,7 +7,8 @@
  * (Sec. 2.2.1: convolution Z = W * X + b, the fully-connected layer
  * y = W x + b of App. C, and batch normalisation in evaluation mode,
  * y = W (x - mu_hat) / sqrt(sigma_hat^2 + eps) + b of App. C), the
- * transposed convolution that Sec. 2.2.1 and App. B name beside them, plus the
+ * transposed convolution that Sec. 2.2.1 and App. B name beside them, the
+ * dropout of Sec. 2.2.2 with its counter-based generator, plus the
  * parameter-free global average pool used to shape the ResNet-18-like stack.
  *
  * Only tests/, __graft_entry__.smoke() and the cpu_baseline leg of bench.py
@@ -371,6 +372,59 @@ void orc_convt2d_weight_grad_at(const double *dy, const double *x,
     for (i64 k = 0; k < count; ++k)
         out[k] = convt_wgrad_one(dy, x, idx[4 * k], idx[4 * k + 1], idx[4 * k + 2], idx[4 * k + 3],
                                  N, Ci, H, W, Co, sh, sw, ph, pw, Ho, Wo);
+}
+
+/* ---------------------------------------------------------------------------
+ * Dropout that regenerates its mask (Sec. 2.2.2): instead of the mask, the
+ * layer keeps the state of a counter-based generator and draws the mask
+ * again in backward.  The generator is Philox4x32 with 10 rounds (Salmon,
+ * Moraes, Dror and Shaw, "Parallel random numbers: as easy as 1, 2, 3",
+ * SC 2011): a 128-bit counter c0..c3 and a 64-bit key k0, k1; each round
+ * multiplies c0 and c2 by two fixed 32-bit constants, mixes the high halves
+ * of the products with the other two words and the key, and the key is
+ * bumped by two Weyl constants between rounds.
+ *
+ * The stream of a call: element i (memory order) takes word i mod 4 of the
+ * block with counter (b mod 2^32, b div 2^32, 0, 0), b = offset + floor(i/4),
+ * key (seed mod 2^32, seed div 2^32).  It is kept iff that word is >= thresh.
+ * ------------------------------------------------------------------------- */
+static uint32_t mulhi32(uint32_t a, uint32_t b, uint32_t *lo)
+{
+    uint64_t p = (uint64_t)a * (uint64_t)b;
+    *lo = (uint32_t)p;
+    return (uint32_t)(p >> 32);
+}
+
+void orc_philox4x32_10(const uint32_t *ctr, const uint32_t *key, uint32_t *out)
+{
+    const uint32_t mul0 = 0xD2511F53u, mul1 = 0xCD9E8D57u;      /* round multipliers */
+    const uint32_t weyl0 = 0x9E3779B9u, weyl1 = 0xBB67AE85u;    /* key increments    */
+    uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; ++round) {
+        uint32_t lo0, lo1;
+        uint32_t hi0 = mulhi32(mul0, c0, &lo0);
+        uint32_t hi1 = mulhi32(mul1, c2, &lo1);
+        uint32_t n0 = hi1 ^ c1 ^ k0, n1 = lo1, n2 = hi0 ^ c3 ^ k1, n3 = lo0;
+        c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+        k0 += weyl0;
+        k1 += weyl1;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* The stream words u_i of a call, i < n. */
+void orc_dropout_words(i64 n, uint64_t seed, uint64_t offset, uint32_t *u)
+{
+    const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+#pragma omp parallel for schedule(static)
+    for (i64 blk = 0; blk < (n + 3) / 4; ++blk) {
+        uint64_t b = offset + (uint64_t)blk;
+        const uint32_t ctr[4] = {(uint32_t)b, (uint32_t)(b >> 32), 0u, 0u};
+        uint32_t w[4];
+        orc_philox4x32_10(ctr, key, w);
+        for (int j = 0; j < 4 && 4 * blk + j < n; ++j) u[4 * blk + j] = w[j];
+    }
 }
 
 /* ---------------------------------------------------------------------------

@@ -28,6 +28,10 @@ linear layer's input; the paper's ReLU keeps a boolean mask of the output
 instead, one byte per element, and this library one bit per element (4-byte
 words: 4 * ceil(n / 32) bytes).  It has no parameters, so ALL_TRUE is its
 INPUT mask.
+
+Dropout (Sec. 2.2.2): stock PyTorch keeps its one-byte boolean mask; the
+paper's dropout, and this library's, keeps the random state and draws the
+mask again in backward, so it keeps no activation bytes.
 """
 from __future__ import annotations
 
@@ -66,6 +70,10 @@ def saved_tensors(kind: str, mask: int, policy: int = SELECTIVE,
         if policy == PYTORCH_DEFAULT:
             return {"x": False, "y": i, "bits": False}
         return {"x": False, "y": False, "bits": i}
+    if kind == "dropout":
+        # stock PyTorch keeps a one-byte boolean mask; this library the
+        # generator's key and counter (no device memory)
+        return {"x": False, "mask8": i and policy == PYTORCH_DEFAULT, "rng_state": i and policy != PYTORCH_DEFAULT}
     raise ValueError(kind)
 
 
@@ -82,13 +90,15 @@ def saved_activation_bytes(kind: str, mask: int, x_numel: int, dtype: str,
         if st["y"]:
             return int(x_numel) * ELT[dtype]
         return relu_mask_bytes(x_numel) if st["bits"] else 0
+    if kind == "dropout":
+        return int(x_numel) if st["mask8"] else 0
     return int(x_numel) * ELT[dtype] if st["x"] else 0
 
 
 def launched(kind: str, mask: int) -> Dict[str, bool]:
     """Backward launch plan: the input-, weight- and bias-gradient work runs
     exactly when its flag is set (Sec. 2.2.1)."""
-    if kind in ("avgpool", "relu"):
+    if kind in ("avgpool", "relu", "dropout"):
         return {"dgrad": bool(mask & MASK_INPUT), "wgrad": False, "bgrad": False}
     return {"dgrad": bool(mask & MASK_INPUT), "wgrad": bool(mask & MASK_WEIGHT),
             "bgrad": bool(mask & MASK_BIAS)}
