@@ -369,6 +369,67 @@ def relu_bandwidth(steps, warmup):
     return out
 
 
+def dropout_bandwidth(steps, warmup):
+    """Dropout that draws its mask again in backward (Sec. 2.2.2) on the
+    stem-output tensor of the ResNet-18-shaped stack (64 x 64 x 112 x 112
+    bf16, channels-last) and on the FFN hidden activation of the encoder
+    (8192 x 3072 bf16), p = 0.1.
+
+    HBM bytes per launch: read the input, write the output (2 * 2 * n); no
+    mask is read or written.  ALU work per launch: one Philox4x32-10 block
+    per 4 elements.  Each launch is timed by the library's HIP events after a
+    512 MiB read sweep evicts the cache.  Retained bytes: this library keeps
+    the generator state (0 bytes), stock PyTorch a one-byte mask (n)."""
+    import torch
+    import paper_2404_12406_amd as ms
+    big = torch.ones(1 << 27, dtype=torch.float32, device="cuda")
+    out = {}
+    for name, shape in (("stem_output", (64, 64, 112, 112)), ("ffn_hidden", (8192, 3072))):
+        n = numel(shape)
+        g = torch.Generator(device="cuda").manual_seed(4343)
+        x = torch.randn(shape, generator=g, device="cuda").to(torch.bfloat16)
+        if len(shape) == 4:
+            x = x.contiguous(memory_format=torch.channels_last)
+        gy = torch.randn_like(x)
+        gx = torch.empty_like(x)
+        p = ms.PreparedLayer(ms.Dropout(0.1, 0x5EED, 0), x, mask=ms.MASK_INPUT, grad_y=gy, grad_x=gx)
+        for _ in range(max(1, warmup)):
+            p.forward()
+            p.backward()
+        torch.cuda.synchronize()
+        nbytes = 2 * 2 * n
+        res = {"shape": list(shape), "dtype": "bf16", "p": 0.1, "bytes_per_launch": nbytes,
+               "philox_blocks_per_launch": ms.dropout_blocks(n)}
+        ms.profile_start(ms.PROF_ACT)
+        for _ in range(steps):
+            big.sum()
+            p.forward()
+        torch.cuda.synchronize()
+        cnt, t_fwd = ms.profile_read(ms.PROF_ACT)
+        assert cnt == steps, (cnt, steps)
+        ms.profile_start(ms.PROF_ACT)
+        for _ in range(steps):
+            big.sum()
+            p.forward()
+            big.sum()
+            p.backward()
+        torch.cuda.synchronize()
+        cnt, t_both = ms.profile_read(ms.PROF_ACT)
+        ms.profile_start(0)
+        assert cnt == 2 * steps, (cnt, steps)
+        for pas, ms_tot in (("forward", t_fwd), ("backward", t_both - t_fwd)):
+            us = ms_tot / steps * 1e3
+            res[pas] = {"us": round(us, 2), "GBs": round(nbytes / (us * 1e-6) / 1e9, 1),
+                        "frac_of_hbm": round(nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                        "G_elements_per_s": round(n / (us * 1e-6) / 1e9, 1)}
+        res["saved_bytes"] = {"generator_state": 0, "stock_one_byte_mask": n}
+        out[name] = res
+        del p, x, gy, gx
+    del big
+    torch.cuda.empty_cache()
+    return out
+
+
 PROBE_SHAPES = {"conv2d": (256, 8, 256, 256), "conv_transpose2d": (256, 8, 256, 256),
                 "conv1d": (4096, 8, 4096), "conv_transpose1d": (4096, 8, 4096)}
 
@@ -457,6 +518,10 @@ def extras(steps, warmup):
         out["appB_layer_memory"][kind] = pr = memory_probe(kind)
         log(f"[bench] App. B probe {kind}: library {pr['library']}, stock {pr['stock_pytorch']} "
             f"({time.time() - t0:.1f}s)")
+    t0 = time.time()
+    out["dropout_regenerated_mask"] = dr = dropout_bandwidth(steps, warmup)
+    log(f"[bench] dropout: " + ", ".join(f"{k} fwd {v['forward']} bwd {v['backward']}" for k, v in dr.items())
+        + f" ({time.time() - t0:.1f}s)")
     t0 = time.time()
     out["relu_bitmask_stem_output"] = rl = relu_bandwidth(steps, warmup)
     log(f"[bench] relu: forward {rl['forward']}, backward {rl['backward']}, saved {rl['saved_bytes']} "

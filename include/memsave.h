@@ -90,7 +90,7 @@ typedef enum {
     MS_RELU = 4,         /* y = max(x, 0) elementwise (NaN and -0 pass through); x 1-D
                             contiguous, 2-D row-major or 4-D channels-last, y likewise; no
                             parameters.  Forward through ms_relu_forward() only           */
-    MS_CONV_TRANSPOSE2D = 5 /* y = transposed convolution of x (torch.nn.ConvTranspose2d with
+    MS_CONV_TRANSPOSE2D = 5, /* y = transposed convolution of x (torch.nn.ConvTranspose2d with
                             dilation 1, groups 1): x[N,C_in,H,W], W[C_in,C_out,R,S]
                             (channels-last: memory [C_in][R][S][C_out]), b[C_out] or NULL,
                             y[N,C_out,H_out,W_out], H_out = (H-1) stride_h - 2 pad_h + R
@@ -105,6 +105,8 @@ typedef enum {
                             kernel with x in the role of the output gradient.  The save
                             rule is the convolution's.  A 1-D (transposed) convolution is
                             the 2-D one with H = R = 1, stride_h = 1, pad_h = 0.          */
+    MS_DROPOUT = 6       /* y = x * m / (1 - p), m a random keep mask; layouts as MS_RELU;
+                            no parameters.  Forward through ms_dropout_forward() only    */
 } ms_kind;
 
 typedef struct {
@@ -123,9 +125,11 @@ typedef struct ms_record ms_record;
 
 /* Bits of ms_account.borrowed: which caller tensors a record keeps.
  * MS_SAVED_BITS: a ReLU's 1-bit mask; MS_SAVED_Y (policy accounting only):
- * the layer output, which stock PyTorch's ReLU keeps. */
+ * the layer output, which stock PyTorch's ReLU keeps; MS_SAVED_MASK8 (policy
+ * accounting only): the one-byte-per-element mask stock PyTorch's dropout
+ * keeps. */
 enum { MS_SAVED_X = 1u, MS_SAVED_W = 2u, MS_SAVED_MEAN = 4u, MS_SAVED_VAR = 8u, MS_SAVED_BITS = 16u,
-       MS_SAVED_Y = 32u };
+       MS_SAVED_Y = 32u, MS_SAVED_MASK8 = 64u };
 
 /* Bits of ms_account.kernels: what the record's backward will launch. */
 enum { MS_K_DGRAD = 1u, MS_K_WGRAD = 2u, MS_K_BGRAD = 4u };
@@ -199,6 +203,38 @@ ms_status ms_relu_forward(const ms_tensor *x, const ms_tensor *y, void *bits, ui
                           void *stream);
 
 /*
+ * ms_dropout_blocks -- generator blocks one ms_dropout_forward() call over n
+ * elements consumes: ceil(n / 4) (0 for n <= 0).  Calls whose offsets are at
+ * least this far apart under one seed draw disjoint parts of the stream.
+ */
+uint64_t ms_dropout_blocks(int64_t n);
+
+/*
+ * ms_dropout_forward -- y = x * m / (1 - p), keeping the generator state
+ * instead of m for backward.
+ *
+ * Sec. 2.2.2: a dropout that stores its mask (or its output) keeps
+ * activation memory alive for backward whatever the next linear layer's
+ * mask says; the paper's dropout keeps the random state and draws the mask
+ * again in backward, for some extra compute.  The draw is Philox4x32 with 10
+ * rounds (Salmon, Moraes, Dror, Shaw, SC 2011): element i (memory order)
+ * takes word i mod 4 of the block with counter (b mod 2^32, b div 2^32, 0,
+ * 0), b = offset + floor(i / 4), under key (seed mod 2^32, seed div 2^32),
+ * and is kept iff that word is >= floor(p * 2^32).  Kept elements are
+ * multiplied by (float)(1 / (1 - p)), dropped ones by 0 (so a dropped Inf or
+ * NaN gives NaN, as in PyTorch); p = 1 writes zeros.
+ * p: finite, 0 <= p <= 1 (MS_E_ARG otherwise).  mask: 0 or MS_RG_INPUT
+ * (MS_E_MASK otherwise).  x and y: same shape, dtype and layout (see
+ * MS_RELU); y is fully overwritten.  With INPUT set, *rec keeps (seed,
+ * offset, p) and no device memory (saved_activation_bytes = 0); with mask 0,
+ * *rec = NULL.  Backward is ms_layer_backward(rec, grad_y, grad_x, NULL,
+ * NULL, stream): grad_x = grad_y * m / (1 - p) with m drawn again.
+ * ms_layer_forward() rejects MS_DROPOUT (MS_E_ARG).
+ */
+ms_status ms_dropout_forward(const ms_tensor *x, const ms_tensor *y, float p, uint64_t seed, uint64_t offset,
+                             uint32_t mask, ms_record **rec, void *stream);
+
+/*
  * ms_layer_backward -- write exactly the requested gradients for grad_y.
  *
  * grad_x / grad_W / grad_b must be non-NULL exactly for the INPUT / WEIGHT /
@@ -245,7 +281,7 @@ ms_status ms_policy_account(const ms_layer *layer, const ms_tensor *x, const ms_
  *   MS_PROF_DGRAD input-gradient GEMM
  *   MS_PROF_WGRAD weight-gradient GEMM (its split-K partial launch)
  *   MS_PROF_BN    BN-eval forward kernel
- *   MS_PROF_ACT   ReLU forward and backward kernels
+ *   MS_PROF_ACT   ReLU and dropout forward and backward kernels
  * ms_profile_start() discards earlier records and arms `kinds` (0 disarms);
  * at most 65536 launches per kind are recorded.  ms_profile_read() waits
  * for the recorded events and returns the number of launches of one kind and

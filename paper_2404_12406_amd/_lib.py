@@ -12,8 +12,8 @@ MS_OK, MS_E_NULL, MS_E_MASK, MS_E_SHAPE, MS_E_DTYPE, MS_E_LAYOUT = 0, 1, 2, 3, 4
 MS_E_UNSUPPORTED, MS_E_CONSUMED, MS_E_NOMEM, MS_E_HIP, MS_E_ARG = 6, 7, 8, 9, 10
 MS_RG_INPUT, MS_RG_WEIGHT, MS_RG_BIAS = 1, 2, 4
 MS_F32, MS_BF16 = 0, 1
-MS_CONV2D, MS_LINEAR, MS_BN_EVAL, MS_AVGPOOL, MS_RELU, MS_CONV_TRANSPOSE2D = 0, 1, 2, 3, 4, 5
-MS_SAVED_X, MS_SAVED_W, MS_SAVED_MEAN, MS_SAVED_VAR, MS_SAVED_BITS, MS_SAVED_Y = 1, 2, 4, 8, 16, 32
+MS_CONV2D, MS_LINEAR, MS_BN_EVAL, MS_AVGPOOL, MS_RELU, MS_CONV_TRANSPOSE2D, MS_DROPOUT = 0, 1, 2, 3, 4, 5, 6
+MS_SAVED_X, MS_SAVED_W, MS_SAVED_MEAN, MS_SAVED_VAR, MS_SAVED_BITS, MS_SAVED_Y, MS_SAVED_MASK8 = 1, 2, 4, 8, 16, 32, 64
 MS_K_DGRAD, MS_K_WGRAD, MS_K_BGRAD = 1, 2, 4
 MS_POLICY_SELECTIVE, MS_POLICY_PYTORCH_DEFAULT, MS_POLICY_ALL_TRUE = 0, 1, 2
 
@@ -23,6 +23,7 @@ EXPORTS = (
     "ms_ledger_read", "ms_ledger_reset", "ms_policy_account", "ms_status_str",
     "ms_last_error", "ms_version", "ms_testing_fail_next_workspace", "ms_testing_live_records",
     "ms_profile_start", "ms_profile_read", "ms_relu_mask_bytes", "ms_relu_forward",
+    "ms_dropout_blocks", "ms_dropout_forward",
 )
 MS_PROF_FWD, MS_PROF_DGRAD, MS_PROF_WGRAD, MS_PROF_BN, MS_PROF_ACT = 1, 2, 4, 8, 16
 
@@ -94,6 +95,11 @@ def configure(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.ms_relu_forward.argtypes = [_T, _T, ctypes.c_void_p, ctypes.c_uint32, ctypes.POINTER(ctypes.c_void_p),
                                     ctypes.c_void_p]
     lib.ms_relu_forward.restype = ctypes.c_int
+    lib.ms_dropout_blocks.argtypes = [ctypes.c_int64]
+    lib.ms_dropout_blocks.restype = ctypes.c_uint64
+    lib.ms_dropout_forward.argtypes = [_T, _T, ctypes.c_float, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint32,
+                                       ctypes.POINTER(ctypes.c_void_p), ctypes.c_void_p]
+    lib.ms_dropout_forward.restype = ctypes.c_int
     return lib
 
 

@@ -18,7 +18,7 @@ from typing import Optional, Tuple
 import torch
 
 from . import _lib
-from ._lib import (MS_AVGPOOL, MS_BN_EVAL, MS_CONV2D, MS_CONV_TRANSPOSE2D, MS_LINEAR, MS_RELU, MS_RG_BIAS,
+from ._lib import (MS_AVGPOOL, MS_BN_EVAL, MS_CONV2D, MS_CONV_TRANSPOSE2D, MS_DROPOUT, MS_LINEAR, MS_RELU, MS_RG_BIAS,
                    MS_RG_INPUT,
                    MS_RG_WEIGHT, MS_SAVED_BITS, MS_SAVED_MEAN, MS_SAVED_VAR, MS_SAVED_W, MS_SAVED_X,
                    MsAccount, MsLayer, MsTensor, check)
@@ -68,6 +68,16 @@ class AvgPool:
 @dataclass(frozen=True)
 class ReLU:
     """y = max(x, 0); its record keeps one bit per element (y > 0), not y."""
+
+
+@dataclass(frozen=True)
+class Dropout:
+    """y = x * m / (1 - p) with the keep mask m drawn from Philox4x32-10
+    under key `seed`, starting at block `offset`; its record keeps
+    (seed, offset, p), not m, and backward draws m again."""
+    p: float = 0.5
+    seed: int = 0
+    offset: int = 0
 
 
 def _pair(v):
@@ -127,6 +137,8 @@ class _LayerDesc:
             self.layer.kind = MS_AVGPOOL
         elif isinstance(spec, ReLU):
             self.layer.kind = MS_RELU
+        elif isinstance(spec, Dropout):
+            self.layer.kind = MS_DROPOUT
         else:
             raise TypeError(f"unknown layer spec {spec!r}")
 
@@ -154,7 +166,7 @@ def output_shape(spec, x: torch.Tensor, W: Optional[torch.Tensor]):
         return tuple(x.shape)
     if isinstance(spec, AvgPool):
         return (x.shape[0], x.shape[1])
-    if isinstance(spec, ReLU):
+    if isinstance(spec, (ReLU, Dropout)):
         return tuple(x.shape)
     raise TypeError(spec)
 
@@ -255,6 +267,19 @@ def _relu_forward(lib, x, y, bits, mask):
     return h
 
 
+def dropout_blocks(numel: int) -> int:
+    """Generator blocks one dropout call over `numel` elements consumes."""
+    return int(_lib.load().ms_dropout_blocks(int(numel)))
+
+
+def _dropout_forward(lib, spec, x, y, mask):
+    h = ctypes.c_void_p()
+    st = lib.ms_dropout_forward(_ptr(tensor_desc(x)), _ptr(tensor_desc(y)), float(spec.p), int(spec.seed),
+                                int(spec.offset), int(mask), ctypes.byref(h), _stream(x.device))
+    check(st, "ms_dropout_forward")
+    return h
+
+
 def layer_forward(spec, x: torch.Tensor, W: Optional[torch.Tensor] = None, b: Optional[torch.Tensor] = None,
                   mask: int = 0, y: Optional[torch.Tensor] = None):
     """Run the layer's forward kernel on the current stream; return (y, record).
@@ -272,6 +297,16 @@ def layer_forward(spec, x: torch.Tensor, W: Optional[torch.Tensor] = None, b: Op
         if not h.value:
             return y, None
         return y, Record(h, _LayerDesc(spec), x, None, None, tuple(y.shape), y, bits)
+    if isinstance(spec, Dropout):
+        if W is not None or b is not None:
+            raise TypeError("dropout takes no W or b")
+        _on_gpu(x, y)
+        if y is None:
+            y = empty_like_layout(tuple(x.shape), x)
+        h = _dropout_forward(lib, spec, x, y, mask)
+        if not h.value:
+            return y, None
+        return y, Record(h, _LayerDesc(spec), x, None, None, tuple(y.shape), y)
     desc = _LayerDesc(spec)
     extra = (spec.running_mean, spec.running_var) if isinstance(spec, BatchNormEval) else ()
     _on_gpu(x, W, b, y, *extra)
@@ -371,6 +406,7 @@ class PreparedLayer:
         self.y = y
         self.mask = int(mask)
         self.relu = isinstance(spec, ReLU)
+        self.dropout = spec if isinstance(spec, Dropout) else None
         # a ReLU's 1-bit mask lives as long as this object (reused by every forward)
         self.bits = relu_mask_buffer(x) if self.relu and self.mask & MASK_INPUT else None
         self._d = [tensor_desc(t) for t in self.tensors]
@@ -390,6 +426,11 @@ class PreparedLayer:
             bits = ctypes.c_void_p(self.bits.data_ptr() if self.bits is not None and self.bits.numel() else None)
             check(self.lib.ms_relu_forward(self._fa[1], self._fy, bits, self.mask, self._hp, self._stream),
                   "ms_relu_forward")
+            return
+        if self.dropout is not None:
+            d = self.dropout
+            check(self.lib.ms_dropout_forward(self._fa[1], self._fy, float(d.p), int(d.seed), int(d.offset),
+                                              self.mask, self._hp, self._stream), "ms_dropout_forward")
             return
         check(self.lib.ms_layer_forward(*self._fa, self.mask, self._fy, self._hp, self._stream),
               "ms_layer_forward")

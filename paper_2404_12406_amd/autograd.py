@@ -28,7 +28,7 @@ from . import api
 from .api import MASK_BIAS, MASK_INPUT, MASK_WEIGHT
 
 __all__ = ["MSConv2d", "MSConvTranspose2d", "MSConv1d", "MSConvTranspose1d", "MSLinear", "MSBatchNorm2dEval",
-           "MSReLU", "convert"]
+           "MSReLU", "MSDropout", "convert"]
 
 
 def _cl(t: Optional[torch.Tensor]) -> Optional[torch.Tensor]:
@@ -85,6 +85,25 @@ class _ReLUFn(torch.autograd.Function):
         gx, _, _ = api.layer_backward(rec, _cl(grad_y.contiguous() if grad_y.dim() != 4 else grad_y))
         rec.free()
         return gx
+
+
+class _DropoutFn(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, x, p, seed):
+        y, rec = api.layer_forward(api.Dropout(p, seed, 0), x, mask=_mask(ctx, 0))
+        ctx.rec = rec
+        return y
+
+    @staticmethod
+    def backward(ctx, grad_y):
+        rec = ctx.rec
+        ctx.rec = None
+        if rec is None:
+            return None, None, None
+        g = _cl(grad_y) if grad_y.dim() == 4 else grad_y.contiguous()
+        gx, _, _ = api.layer_backward(rec, g)
+        rec.free()
+        return gx, None, None
 
 
 class MSConv2d(nn.Module):
@@ -203,6 +222,32 @@ class MSReLU(nn.Module):
         return _ReLUFn.apply(_cl(x) if x.dim() == 4 else x.contiguous())
 
 
+class MSDropout(nn.Module):
+    """Dropout that keeps its generator state, not its mask, and draws the
+    mask again in backward (Sec. 2.2.2).  In training mode each call takes a
+    fresh 64-bit key from torch's default CPU generator (so torch.manual_seed
+    makes runs repeatable; `last_seed` holds the key of the latest call); in
+    evaluation mode, or with p = 0, it is the identity.  Inputs other than
+    channels-last 4-D tensors are processed as one flat contiguous array."""
+
+    def __init__(self, p: float = 0.5):
+        super().__init__()
+        if not 0.0 <= p <= 1.0:
+            raise ValueError("dropout probability must lie in [0, 1]")
+        self.p = float(p)
+        self.last_seed = None
+
+    def forward(self, x):
+        if not self.training or self.p == 0.0:
+            return x
+        seed = int(torch.randint(0, 2 ** 63 - 1, (), dtype=torch.int64))
+        self.last_seed = seed
+        if x.dim() == 4 and x.is_contiguous(memory_format=torch.channels_last):
+            return _DropoutFn.apply(x, self.p, seed)
+        flat = x.contiguous().view(-1)
+        return _DropoutFn.apply(flat, self.p, seed).view(x.shape)
+
+
 def _convertible_conv(m) -> bool:
     """groups 1, dilation 1, zero padding given as numbers, fp32 or bf16."""
     return (m.groups == 1 and all(d == 1 for d in m.dilation) and m.padding_mode == "zeros"
@@ -214,7 +259,8 @@ def convert(module: nn.Module) -> nn.Module:
     nn.ConvTranspose1d (groups 1, dilation 1, zero padding), nn.Linear,
     nn.BatchNorm2d in evaluation mode and nn.ReLU of `module` by the
     library's layers, sharing their parameters and buffers; returns the
-    module (Sec. 4: one call swaps every supported layer).  A BatchNorm2d
+    module (Sec. 4: one call swaps every supported layer); nn.Dropout
+    becomes MSDropout with the same p and mode.  A BatchNorm2d
     still in training mode is left as it is (its batch statistics make it
     non-linear in x); so is any layer outside those limits."""
     for name, child in list(module.named_children()):
@@ -234,6 +280,9 @@ def convert(module: nn.Module) -> nn.Module:
             new = MSBatchNorm2dEval(child.weight, child.bias, child.running_mean, child.running_var, child.eps)
         elif isinstance(child, nn.ReLU):
             new = MSReLU()
+        elif isinstance(child, nn.Dropout):
+            new = MSDropout(child.p)
+            new.train(child.training)
         if new is not None:
             setattr(module, name, new)
         else:

@@ -66,6 +66,13 @@ int launch_bn_bwd(int dtype, const void *dy, const void *x, const void *mean,
 int launch_relu_fwd(int dtype, const void *x, int64_t n, void *y, void *bits, int64_t bits_bytes, void *stream);
 int launch_relu_bwd(int dtype, const void *dy, const void *bits, int64_t n, void *dx, void *stream);
 
+// Dropout over n elements in memory order, forward (in = x) or backward
+// (in = dy): out_i = in_i * (u_i >= thresh ? scale : 0), or 0 when drop_all;
+// u_i is word i mod 4 of the Philox4x32-10 block with counter
+// (b mod 2^32, b div 2^32, 0, 0), b = offset + floor(i / 4), key = seed.
+int launch_dropout(int dtype, const void *in, int64_t n, void *out, uint64_t seed, uint64_t offset, uint32_t thresh,
+                   float scale, int drop_all, void *stream);
+
 // Global average pool x[N][L][C] -> y[N][C] and its adjoint.
 int launch_avgpool_fwd(int dtype, const void *x, int N, int L, int C, void *y, void *stream);
 int launch_avgpool_bwd(int dtype, const void *dy, int N, int L, int C, void *dx, void *stream);

@@ -50,6 +50,43 @@ __device__ __forceinline__ Vec16<T> zero16() {
     return v;
 }
 
+// Eight consecutive elements of an elementwise pass (one 16-byte vector of
+// bf16, two of fp32).  With VEC the whole group is read or written with
+// 16-byte accesses when it lies inside [0, n) (the caller guarantees 16-byte
+// alignment of the base); otherwise element by element, and elements past n
+// read as zero and are not written.
+template <typename T>
+struct Group8 {
+    T e[8];
+};
+
+template <typename T, bool VEC>
+__device__ __forceinline__ Group8<T> load_group8(const T *__restrict__ p, int64_t i0, int64_t n) {
+    Group8<T> g;
+    if (VEC && i0 + 8 <= n) {
+        const u32x4 *q = reinterpret_cast<const u32x4 *>(p + i0);
+#pragma unroll
+        for (int h = 0; h < (int)(8 * sizeof(T) / 16); ++h) reinterpret_cast<u32x4 *>(g.e)[h] = q[h];
+    } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) g.e[e] = i0 + e < n ? p[i0 + e] : (T)0.f;
+    }
+    return g;
+}
+
+template <typename T, bool VEC>
+__device__ __forceinline__ void store_group8(T *__restrict__ p, int64_t i0, int64_t n, const Group8<T> &g) {
+    if (VEC && i0 + 8 <= n) {
+        u32x4 *q = reinterpret_cast<u32x4 *>(p + i0);
+#pragma unroll
+        for (int h = 0; h < (int)(8 * sizeof(T) / 16); ++h) q[h] = reinterpret_cast<const u32x4 *>(g.e)[h];
+    } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            if (i0 + e < n) p[i0 + e] = g.e[e];
+    }
+}
+
 // Map a hardware block index to a logical tile index so that each of the 8
 // XCDs (which receive blocks round-robin, block b -> XCD b % 8) owns one
 // contiguous range of logical tiles: neighbouring tiles then share an L2.

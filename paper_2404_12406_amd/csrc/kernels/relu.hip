@@ -24,38 +24,6 @@ namespace {
 
 constexpr int kU = 4;   // groups per thread per pass
 
-template <typename T>
-struct Group {
-    T e[8];
-};
-
-template <typename T, bool VEC>
-__device__ __forceinline__ Group<T> load_group(const T *__restrict__ p, int64_t i0, int64_t n) {
-    Group<T> g;
-    if (VEC && i0 + 8 <= n) {
-        const u32x4 *q = reinterpret_cast<const u32x4 *>(p + i0);
-#pragma unroll
-        for (int h = 0; h < (int)(8 * sizeof(T) / 16); ++h) reinterpret_cast<u32x4 *>(g.e)[h] = q[h];
-    } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) g.e[e] = i0 + e < n ? p[i0 + e] : (T)0.f;
-    }
-    return g;
-}
-
-template <typename T, bool VEC>
-__device__ __forceinline__ void store_group(T *__restrict__ p, int64_t i0, int64_t n, const Group<T> &g) {
-    if (VEC && i0 + 8 <= n) {
-        u32x4 *q = reinterpret_cast<u32x4 *>(p + i0);
-#pragma unroll
-        for (int h = 0; h < (int)(8 * sizeof(T) / 16); ++h) q[h] = reinterpret_cast<const u32x4 *>(g.e)[h];
-    } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-            if (i0 + e < n) p[i0 + e] = g.e[e];
-    }
-}
-
 // ngroups = ceil(n / 8) mask bytes carry bits; the bytes after them up to
 // nbytes (the word-rounded mask size) are written as zeros.  bits == nullptr
 // (nbytes == 0): y only.
@@ -65,10 +33,10 @@ __global__ __launch_bounds__(256) void relu_fwd_kernel(const T *__restrict__ x, 
                                                        int64_t nbytes) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t v0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; v0 < ngroups; v0 += kU * stride) {
-        Group<T> g[kU];
+        Group8<T> g[kU];
 #pragma unroll
         for (int u = 0; u < kU; ++u)
-            if (v0 + u * stride < ngroups) g[u] = load_group<T, VEC>(x, (v0 + u * stride) * 8, n);
+            if (v0 + u * stride < ngroups) g[u] = load_group8<T, VEC>(x, (v0 + u * stride) * 8, n);
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
             const int64_t v = v0 + u * stride;
@@ -80,7 +48,7 @@ __global__ __launch_bounds__(256) void relu_fwd_kernel(const T *__restrict__ x, 
                 if (f < 0.f) g[u].e[e] = (T)0.f;
                 byte |= (f <= 0.f ? 0u : 1u) << e;
             }
-            store_group<T, VEC>(y, v * 8, n, g[u]);
+            store_group8<T, VEC>(y, v * 8, n, g[u]);
             if (bits) bits[v] = (uint8_t)byte;   // no mask without a record
         }
     }
@@ -92,14 +60,14 @@ __global__ __launch_bounds__(256) void relu_bwd_kernel(const T *__restrict__ dy,
                                                        T *__restrict__ dx, int64_t n, int64_t ngroups) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t v0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; v0 < ngroups; v0 += kU * stride) {
-        Group<T> g[kU];
+        Group8<T> g[kU];
         uint32_t byte[kU];
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
             const int64_t v = v0 + u * stride;
             byte[u] = 0;
             if (v < ngroups) {
-                g[u] = load_group<T, VEC>(dy, v * 8, n);
+                g[u] = load_group8<T, VEC>(dy, v * 8, n);
                 byte[u] = bits[v];
             }
         }
@@ -110,7 +78,7 @@ __global__ __launch_bounds__(256) void relu_bwd_kernel(const T *__restrict__ dy,
 #pragma unroll
             for (int e = 0; e < 8; ++e)
                 if (!((byte[u] >> e) & 1u)) g[u].e[e] = (T)0.f;
-            store_group<T, VEC>(dx, v * 8, n, g[u]);
+            store_group8<T, VEC>(dx, v * 8, n, g[u]);
         }
     }
 }

@@ -11,7 +11,8 @@
 // variance).  A transposed convolution is the adjoint of a convolution and
 // keeps what a convolution keeps.  ReLU (Sec. 2.2.2) keeps one bit per
 // element instead of its output, so the next linear layer's input is not
-// kept alive by it.
+// kept alive by it; dropout (Sec. 2.2.2 too) keeps its generator's key and
+// counter and draws the mask again in backward.
 // Nothing in this file touches the device except through the
 // launchers of device.h, and every check runs before the first launch.
 #include <algorithm>
@@ -130,8 +131,9 @@ struct Plan {
     int Nb = 0;            // avgpool batch
     bool has_w = false, has_b = false;
     uint64_t x_bytes = 0, w_bytes = 0, stat_bytes = 0;
-    int64_t n = 0;                           // ReLU: elements
+    int64_t n = 0;                           // ReLU / dropout: elements
     uint64_t bits_bytes = 0, y_bytes = 0;    // ReLU: 1-bit mask, output
+    uint64_t mask8_bytes = 0;                // dropout: stock PyTorch's one-byte mask
 };
 
 uint64_t relu_mask_bytes(int64_t n) { return n > 0 ? (uint64_t)((n + 31) / 32) * 4u : 0u; }
@@ -337,12 +339,14 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
         pl->x_bytes = (uint64_t)numel(x) * elt_size(x->dtype);
         return MS_OK;
     }
-    case MS_RELU: {
-        if (W || b) return fail(MS_E_ARG, "ReLU takes no W or b");
-        if (mask & ~(uint32_t)MS_RG_INPUT) return fail(MS_E_MASK, "ReLU has no parameters");
+    case MS_RELU:
+    case MS_DROPOUT: {
+        const char *nm = layer->kind == MS_RELU ? "ReLU" : "dropout";
+        if (W || b) return fail(MS_E_ARG, "%s takes no W or b", nm);
+        if (mask & ~(uint32_t)MS_RG_INPUT) return fail(MS_E_MASK, "%s has no parameters", nm);
         if (!x) return fail(MS_E_NULL, "x is NULL");
         const int nd = x->ndim;
-        if (nd != 1 && nd != 2 && nd != 4) return fail(MS_E_SHAPE, "ReLU x must have 1, 2 or 4 dims");
+        if (nd != 1 && nd != 2 && nd != 4) return fail(MS_E_SHAPE, "%s x must have 1, 2 or 4 dims", nm);
         if ((st = check_tensor(x, "x", nd, need_data))) return st;
         if (!dense_layout(x)) return fail(MS_E_LAYOUT, "x must be contiguous, row-major or channels-last");
         if (y) {
@@ -356,6 +360,7 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
         pl->x_bytes = (uint64_t)pl->n * elt_size(x->dtype);
         pl->y_bytes = pl->x_bytes;
         pl->bits_bytes = relu_mask_bytes(pl->n);
+        pl->mask8_bytes = (uint64_t)pl->n;
         return MS_OK;
     }
     default:
@@ -384,6 +389,8 @@ uint32_t borrowed_bits(int32_t kind, uint32_t mask, int32_t policy, bool has_w, 
     case MS_RELU:   // stock PyTorch keeps the output; this library one bit per element
         if (!in) return 0;
         return policy == MS_POLICY_PYTORCH_DEFAULT ? (uint32_t)MS_SAVED_Y : (uint32_t)MS_SAVED_BITS;
+    case MS_DROPOUT:   // stock PyTorch keeps a one-byte mask; this library the generator state
+        return in && policy == MS_POLICY_PYTORCH_DEFAULT ? (uint32_t)MS_SAVED_MASK8 : 0u;
     default:
         return 0;
     }
@@ -423,7 +430,8 @@ ms_account make_account(const Plan &pl, uint32_t mask, uint32_t borrowed, uint32
     a.kernels = kernels;
     a.saved_activation_bytes = ((borrowed & MS_SAVED_X) ? pl.x_bytes : 0) +
                                ((borrowed & MS_SAVED_BITS) ? pl.bits_bytes : 0) +
-                               ((borrowed & MS_SAVED_Y) ? pl.y_bytes : 0);
+                               ((borrowed & MS_SAVED_Y) ? pl.y_bytes : 0) +
+                               ((borrowed & MS_SAVED_MASK8) ? pl.mask8_bytes : 0);
     uint64_t pb = 0;
     if (borrowed & MS_SAVED_W) pb += pl.w_bytes;
     if (borrowed & MS_SAVED_MEAN) pb += pl.stat_bytes;
@@ -445,6 +453,10 @@ struct ms_record {
     float eps;
     ms_tensor x, W, b, mean, var, y;   // data non-NULL only for borrowed tensors
     void *bits;                         // ReLU: the borrowed 1-bit mask
+    uint64_t seed, offset;              // dropout: generator key and first block
+    uint32_t thresh;                    // dropout: keep iff word >= thresh
+    float scale;                        // dropout: 1 / (1 - p) (0 when p = 1)
+    int drop_all;                       // dropout: p = 1
     ms_account acct;
     bool consumed;
     bool released;
@@ -488,6 +500,7 @@ ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
     *rec = nullptr;
     if (!y) return fail(MS_E_NULL, "y is NULL");
     if (layer && layer->kind == MS_RELU) return fail(MS_E_ARG, "ReLU runs through ms_relu_forward()");
+    if (layer && layer->kind == MS_DROPOUT) return fail(MS_E_ARG, "dropout runs through ms_dropout_forward()");
     Plan pl;
     ms_status st = validate_forward(layer, x, W, b, mask, y, true, &pl);
     if (st) return st;
@@ -636,6 +649,11 @@ ms_status ms_layer_backward(ms_record *r, const ms_tensor *grad_y, const ms_tens
     case MS_RELU:
         if (kernels & MS_K_DGRAD) err = ms::launch_relu_bwd(pl.dtype, dy, r->bits, pl.n, grad_x->data, stream);
         break;
+    case MS_DROPOUT:   // the mask is drawn again from the record's key and counter
+        if (kernels & MS_K_DGRAD)
+            err = ms::launch_dropout(pl.dtype, dy, pl.n, grad_x->data, r->seed, r->offset, r->thresh, r->scale,
+                                     r->drop_all, stream);
+        break;
     }
     if (err) return hip_fail(err, "backward launch");
     r->consumed = true;
@@ -686,6 +704,61 @@ ms_status ms_relu_forward(const ms_tensor *x, const ms_tensor *y, void *bits, ui
     std::memset(&r->var, 0, sizeof r->var);
     r->bits = bits;
     r->acct = make_account(pl, mask, borrowed, kernels);
+    r->consumed = false;
+    r->released = false;
+    ledger_add(r->acct.saved_activation_bytes);
+    g_records.fetch_add(1);
+    *rec = r;
+    return MS_OK;
+}
+
+uint64_t ms_dropout_blocks(int64_t n) { return n > 0 ? (uint64_t)((n + 3) / 4) : 0u; }
+
+ms_status ms_dropout_forward(const ms_tensor *x, const ms_tensor *y, float p, uint64_t seed, uint64_t offset,
+                             uint32_t mask, ms_record **rec, void *stream) {
+    clear_err();
+    if (!rec) return fail(MS_E_NULL, "rec is NULL");
+    *rec = nullptr;
+    if (!y) return fail(MS_E_NULL, "y is NULL");
+    if (!(p >= 0.f && p <= 1.f)) return fail(MS_E_ARG, "p must be finite and in [0, 1]");
+    ms_layer layer{};
+    layer.kind = MS_DROPOUT;
+    Plan pl;
+    ms_status st = validate_forward(&layer, x, nullptr, nullptr, mask, y, true, &pl);
+    if (st) return st;
+    // keep iff the element's word >= floor(p * 2^32); p < 1 keeps that below 2^32
+    const int drop_all = p == 1.f;
+    const uint32_t thresh = drop_all ? 0u : (uint32_t)std::floor((double)p * 4294967296.0);
+    const float scale = drop_all ? 0.f : (float)(1.0 / (1.0 - (double)p));
+    const bool keep = mask & MS_RG_INPUT;
+    ms_record *r = nullptr;
+    if (keep) {
+        r = new (std::nothrow) ms_record();
+        if (!r) return fail(MS_E_NOMEM, "record allocation failed");
+    }
+    const int err = ms::launch_dropout(pl.dtype, x->data, pl.n, y->data, seed, offset, thresh, scale, drop_all, stream);
+    if (err) {
+        delete r;
+        return hip_fail(err, "forward launch");
+    }
+    if (!r) return MS_OK;
+    r->magic = kMagic;
+    r->plan = pl;
+    r->eps = 0.f;
+    r->x = shape_only(x);
+    r->y = shape_only(y);
+    std::memset(&r->W, 0, sizeof r->W);
+    std::memset(&r->b, 0, sizeof r->b);
+    std::memset(&r->mean, 0, sizeof r->mean);
+    std::memset(&r->var, 0, sizeof r->var);
+    r->bits = nullptr;
+    r->seed = seed;
+    r->offset = offset;
+    r->thresh = thresh;
+    r->scale = scale;
+    r->drop_all = drop_all;
+    r->acct = make_account(pl, mask, borrowed_bits(MS_DROPOUT, mask, MS_POLICY_SELECTIVE, false, false),
+                           kernel_bits(MS_DROPOUT, mask));
     r->consumed = false;
     r->released = false;
     ledger_add(r->acct.saved_activation_bytes);

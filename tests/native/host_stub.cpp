@@ -137,6 +137,13 @@ int launch_relu_fwd(int, const void *x, int64_t n, void *y, void *bits, int64_t 
     return e;
 }
 
+int launch_dropout(int, const void *in, int64_t n, void *out, uint64_t, uint64_t, uint32_t, float, int drop_all,
+                   void *) {
+    log(drop_all ? "dropout(all)" : "dropout");
+    if (n > 0) return need(in && out, "dropout:in,out");
+    return 0;
+}
+
 int launch_relu_bwd(int, const void *dy, const void *bits, int64_t n, void *dx, void *) {
     log("relu_bwd");
     return n > 0 ? need(dy && bits && dx, "relu_bwd:dy,bits,dx") : 0;

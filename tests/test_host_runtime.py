@@ -626,3 +626,84 @@ def test_conv_transpose_validation(stub):
     assert stub.ms_layer_forward(ctypes.byref(a.layer), ref(a.x), ref(a.W), ref(a.b), 7, ref(a.y),
                                  ctypes.byref(h), None) == 0, stub.ms_last_error()
     stub.ms_record_free(h)
+
+
+# ------------------------------------------------------------------ dropout
+def _dropout_forward(lib, x, y, p, mask, seed=5, offset=0):
+    h = ctypes.c_void_p()
+    st = lib.ms_dropout_forward(ref(x), ref(y), p, seed, offset, mask, ctypes.byref(h), None)
+    return st, h
+
+
+@pytest.mark.parametrize("shape", [(1000,), (8, 16), (2, 3, 4, 5), (0, 7)])
+@pytest.mark.parametrize("p", [0.0, 0.3, 1.0])
+def test_dropout_record_keeps_no_device_memory(stub, shape, p):
+    """Sec. 2.2.2: the record holds the generator state; backward launches
+    the same pass on grad_y (all-zero output when p = 1)."""
+    x, y = tdesc(shape, "bf16"), tdesc(shape, "bf16")
+    live0, pk = ctypes.c_uint64(), ctypes.c_uint64()
+    stub.ms_ledger_read(ctypes.byref(live0), ctypes.byref(pk))
+    stub.stub_reset()
+    st, h = _dropout_forward(stub, x, y, p, L.MS_RG_INPUT)
+    assert st == 0, stub.ms_last_error()
+    name = "dropout(all)" if p == 1.0 else "dropout"
+    assert stub.stub_log().decode() == name + ";" and stub.stub_violations().decode() == ""
+    a = L.MsAccount()
+    stub.ms_record_account(h, ctypes.byref(a))
+    assert a.saved_activation_bytes == 0 and a.borrowed == 0 and a.kernels == L.MS_K_DGRAD
+    live, _ = ctypes.c_uint64(), ctypes.c_uint64()
+    stub.ms_ledger_read(ctypes.byref(live), ctypes.byref(pk))
+    assert live.value == live0.value
+    stub.stub_reset()
+    gy, gx = tdesc(shape, "bf16"), tdesc(shape, "bf16")
+    assert stub.ms_layer_backward(h, ref(gy), ref(gx), None, None, None) == 0
+    assert stub.stub_log().decode() == name + ";"
+    stub.ms_record_free(h)
+    # mask 0: the forward only, no record
+    stub.stub_reset()
+    st, h = _dropout_forward(stub, x, y, p, 0)
+    assert st == 0 and not h.value
+    assert stub.stub_log().decode() == name + ";"
+    assert stub.ms_testing_live_records() == 0
+
+
+def test_dropout_validation_errors_launch_nothing(stub):
+    x, y = tdesc((8, 16), "bf16"), tdesc((8, 16), "bf16")
+    cases = [
+        (x, y, 0.5, L.MS_RG_WEIGHT, L.MS_E_MASK),
+        (x, y, -0.1, 1, L.MS_E_ARG),
+        (x, y, 1.5, 1, L.MS_E_ARG),
+        (x, y, float("nan"), 1, L.MS_E_ARG),
+        (x, y, float("inf"), 1, L.MS_E_ARG),
+        (x, tdesc((8, 17), "bf16"), 0.5, 1, L.MS_E_SHAPE),
+        (x, tdesc((8, 16), "f32"), 0.5, 1, L.MS_E_DTYPE),
+        (tdesc((2, 3, 4, 5), "bf16", "nchw"), tdesc((2, 3, 4, 5), "bf16", "nchw"), 0.5, 1, L.MS_E_LAYOUT),
+        (None, y, 0.5, 1, L.MS_E_NULL),
+        (x, None, 0.5, 1, L.MS_E_NULL),
+    ]
+    for xi, yi, p, mask, want in cases:
+        stub.stub_reset()
+        st, h = _dropout_forward(stub, xi, yi, p, mask)
+        assert st == want, (p, mask, want, st, stub.ms_last_error())
+        assert not h.value and stub.stub_log().decode() == ""
+    layer = L.MsLayer()
+    layer.kind = L.MS_DROPOUT
+    h = ctypes.c_void_p()
+    assert stub.ms_layer_forward(ctypes.byref(layer), ref(x), None, None, 1, ref(y), ctypes.byref(h), None) == L.MS_E_ARG
+    assert stub.ms_dropout_blocks(0) == 0 and stub.ms_dropout_blocks(4) == 1 and stub.ms_dropout_blocks(9) == 3
+    assert stub.ms_testing_live_records() == 0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_dropout_policy_account(stub, dtype):
+    shape = (8192, 3072)
+    n = _numel(shape)
+    layer = L.MsLayer()
+    layer.kind = L.MS_DROPOUT
+    x = tdesc(shape, dtype, data=False)
+    for policy in (P.SELECTIVE, P.PYTORCH_DEFAULT, P.ALL_TRUE):
+        for mask in (0, 1):
+            a = L.MsAccount()
+            assert stub.ms_policy_account(ctypes.byref(layer), ref(x), None, None, mask, policy, ctypes.byref(a)) == 0
+            assert a.saved_activation_bytes == P.saved_activation_bytes("dropout", mask, n, dtype, policy)
+            assert bool(a.borrowed & L.MS_SAVED_MASK8) == (policy == P.PYTORCH_DEFAULT and mask == 1)
