@@ -30,7 +30,8 @@ __all__ = [
     "bn_eval_forward", "bn_eval_backward", "avgpool_forward", "avgpool_backward",
     "relu_forward", "relu_mask_bits", "relu_backward", "relu_mask_nbytes", "memory_order",
     "philox4x32_10", "dropout_threshold", "dropout_scale", "dropout_words", "dropout_keep", "dropout_forward",
-    "dropout_backward",
+    "dropout_backward", "conv3d_out", "conv3d_forward", "conv3d_input_grad", "conv3d_weight_grad", "bias_grad5",
+    "convt3d_out", "convt3d_forward", "convt3d_input_grad", "convt3d_weight_grad",
     "round_to", "rel_err",
 ]
 
@@ -505,3 +506,110 @@ def dropout_backward(dy_mem, p, seed, offset=0):
     """dx = dy * m / (1 - p) with the mask drawn again from the same counters
     (the forward map is linear with that diagonal Jacobian)."""
     return dropout_forward(dy_mem, p, seed, offset)
+
+
+# ----------------------------------------------------------------- 3-D convolution and its transpose
+def _g3(N, C, D, H, W, K, T, R, S, Do, P, Q, stride, pad):
+    return np.array([N, C, D, H, W, K, T, R, S, Do, P, Q, stride[0], stride[1], stride[2],
+                     pad[0], pad[1], pad[2]], np.int64)
+
+
+def _gp(g):
+    return g.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))
+
+
+def conv3d_out(D, H, W, T, R, S, stride, pad):
+    out = tuple((e + 2 * p - k) // s + 1 for e, k, s, p in zip((D, H, W), (T, R, S), stride, pad))
+    if min(out) < 1:
+        raise ValueError("convolution output would be empty")
+    return out
+
+
+def conv3d_forward(x, w, b=None, stride=(1, 1, 1), pad=(0, 0, 0)):
+    """3-D cross-correlation with zero padding (torch.nn.Conv3d, App. B):
+    x[N,C,D,H,W], W[K,C,T,R,S]."""
+    x, w, b = _d(x), _d(w), _d(b)
+    N, C, D, H, W = x.shape
+    K, C2, T, R, S = w.shape
+    if C2 != C:
+        raise ValueError("channel mismatch")
+    Do, P, Q = conv3d_out(D, H, W, T, R, S, stride, pad)
+    g = _g3(N, C, D, H, W, K, T, R, S, Do, P, Q, stride, pad)
+    y = np.empty((N, K, Do, P, Q), np.float64)
+    _load().orc_conv3d_forward(_p(x), _p(w), _p(b), _p(y), _gp(g))
+    return y
+
+
+def conv3d_input_grad(dy, w, x_shape, stride=(1, 1, 1), pad=(0, 0, 0)):
+    dy, w = _d(dy), _d(w)
+    N, C, D, H, W = x_shape
+    K, _, T, R, S = w.shape
+    Do, P, Q = conv3d_out(D, H, W, T, R, S, stride, pad)
+    g = _g3(N, C, D, H, W, K, T, R, S, Do, P, Q, stride, pad)
+    dx = np.empty(tuple(x_shape), np.float64)
+    _load().orc_conv3d_input_grad(_p(dy), _p(w), _p(dx), _gp(g))
+    return dx
+
+
+def conv3d_weight_grad(dy, x, w_shape, stride=(1, 1, 1), pad=(0, 0, 0)):
+    dy, x = _d(dy), _d(x)
+    N, C, D, H, W = x.shape
+    K, _, T, R, S = w_shape
+    Do, P, Q = conv3d_out(D, H, W, T, R, S, stride, pad)
+    g = _g3(N, C, D, H, W, K, T, R, S, Do, P, Q, stride, pad)
+    dw = np.empty(tuple(w_shape), np.float64)
+    _load().orc_conv3d_weight_grad(_p(dy), _p(x), _p(dw), _gp(g))
+    return dw
+
+
+def bias_grad5(dy):
+    """db[k] = sum over (n, d, h, w) of dy[n, k, d, h, w]."""
+    dy = _d(dy)
+    N, K = dy.shape[:2]
+    db = np.empty(K, np.float64)
+    _load().orc_bias_grad5(_p(dy), _p(db), _I(N), _I(K), _I(int(np.prod(dy.shape[2:]))))
+    return db
+
+
+def convt3d_out(D, H, W, T, R, S, stride, pad, out_pad=(0, 0, 0)):
+    if not all(0 <= o < s for o, s in zip(out_pad, stride)):
+        raise ValueError("output padding must satisfy 0 <= out_pad < stride")
+    out = tuple((e - 1) * s - 2 * p + k + o for e, k, s, p, o in zip((D, H, W), (T, R, S), stride, pad, out_pad))
+    if min(out) < 1:
+        raise ValueError("transposed convolution output would be empty")
+    return out
+
+
+def _convt3d_g(x_shape, w_shape, stride, pad, out_pad):
+    N, Ci, D, H, W = x_shape
+    Ci2, Co, T, R, S = w_shape
+    if Ci2 != Ci:
+        raise ValueError("channel mismatch")
+    Do, Ho, Wo = convt3d_out(D, H, W, T, R, S, stride, pad, out_pad)
+    return _g3(N, Ci, D, H, W, Co, T, R, S, Do, Ho, Wo, stride, pad), (N, Co, Do, Ho, Wo)
+
+
+def convt3d_forward(x, w, b=None, stride=(1, 1, 1), pad=(0, 0, 0), out_pad=(0, 0, 0)):
+    """Transposed 3-D convolution (torch.nn.ConvTranspose3d, App. B):
+    x[N,Ci,D,H,W], W[Ci,Co,T,R,S], each input voxel scatters through each tap."""
+    x, w, b = _d(x), _d(w), _d(b)
+    g, ys = _convt3d_g(x.shape, w.shape, stride, pad, out_pad)
+    y = np.empty(ys, np.float64)
+    _load().orc_convt3d_forward(_p(x), _p(w), _p(b), _p(y), _gp(g))
+    return y
+
+
+def convt3d_input_grad(dy, w, x_shape, stride=(1, 1, 1), pad=(0, 0, 0), out_pad=(0, 0, 0)):
+    dy, w = _d(dy), _d(w)
+    g, _ = _convt3d_g(x_shape, w.shape, stride, pad, out_pad)
+    dx = np.empty(tuple(x_shape), np.float64)
+    _load().orc_convt3d_input_grad(_p(dy), _p(w), _p(dx), _gp(g))
+    return dx
+
+
+def convt3d_weight_grad(dy, x, w_shape, stride=(1, 1, 1), pad=(0, 0, 0), out_pad=(0, 0, 0)):
+    dy, x = _d(dy), _d(x)
+    g, _ = _convt3d_g(x.shape, w_shape, stride, pad, out_pad)
+    dw = np.empty(tuple(w_shape), np.float64)
+    _load().orc_convt3d_weight_grad(_p(dy), _p(x), _p(dw), _gp(g))
+    return dw

@@ -7,7 +7,8 @@
  * (Sec. 2.2.1: convolution Z = W * X + b, the fully-connected layer
  * y = W x + b of App. C, and batch normalisation in evaluation mode,
  * y = W (x - mu_hat) / sqrt(sigma_hat^2 + eps) + b of App. C), the
- * transposed convolution that Sec. 2.2.1 and App. B name beside them, the
+ * transposed convolution that Sec. 2.2.1 and App. B name beside them (in 2-D
+ * and 3-D), the
  * dropout of Sec. 2.2.2 with its counter-based generator, plus the
  * parameter-free global average pool used to shape the ResNet-18-like stack.
  *
@@ -372,6 +373,223 @@ void orc_convt2d_weight_grad_at(const double *dy, const double *x,
     for (i64 k = 0; k < count; ++k)
         out[k] = convt_wgrad_one(dy, x, idx[4 * k], idx[4 * k + 1], idx[4 * k + 2], idx[4 * k + 3],
                                  N, Ci, H, W, Co, sh, sw, ph, pw, Ho, Wo);
+}
+
+/* ---------------------------------------------------------------------------
+ * 3-D convolution and its transpose (App. B probes torch.nn.Conv3d and
+ * torch.nn.ConvTranspose3d): the 2-D definitions with a depth axis added.
+ * Arrays are dense in logical order: x[N,C,D,H,W], conv weight W[K,C,T,R,S],
+ * transposed weight W[Ci,Co,T,R,S].  g3 packs the geometry:
+ *   g3 = {N, C, D, H, W, K, T, R, S, Do, P, Q, sd, sh, sw, pd, ph, pw}
+ * where (Do, P, Q) is the convolution's output extent (the transposed
+ * layer's input extent is (D, H, W) of its adjoint convolution's output).
+ * ------------------------------------------------------------------------- */
+#define IDX5(a, b, c, d, e, B, C, D, E) (((((a) * (B) + (b)) * (C) + (c)) * (D) + (d)) * (E) + (e))
+
+/* y[n,k,o,p,q] = b[k] + sum_{c,t,r,s} W[k,c,t,r,s] x[n,c,o sd-pd+t, p sh-ph+r, q sw-pw+s] */
+static double conv3d_fwd_one(const double *x, const double *w, const double *b, const i64 *g,
+                             i64 n, i64 k, i64 o, i64 p, i64 q)
+{
+    i64 C = g[1], D = g[2], H = g[3], W = g[4], T = g[6], R = g[7], S = g[8];
+    double acc = 0.0;
+    for (i64 c = 0; c < C; ++c)
+        for (i64 t = 0; t < T; ++t) {
+            i64 id = o * g[12] - g[15] + t;
+            if (id < 0 || id >= D) continue;
+            for (i64 r = 0; r < R; ++r) {
+                i64 ih = p * g[13] - g[16] + r;
+                if (ih < 0 || ih >= H) continue;
+                for (i64 s = 0; s < S; ++s) {
+                    i64 iw = q * g[14] - g[17] + s;
+                    if (iw < 0 || iw >= W) continue;
+                    acc += w[IDX5(k, c, t, r, s, C, T, R, S)] * x[IDX5(n, c, id, ih, iw, C, D, H, W)];
+                }
+            }
+        }
+    return acc + (b ? b[k] : 0.0);
+}
+
+void orc_conv3d_forward(const double *x, const double *w, const double *b, double *y, const i64 *g)
+{
+    i64 N = g[0], K = g[5], Do = g[9], P = g[10], Q = g[11];
+#pragma omp parallel for collapse(2) schedule(static)
+    for (i64 n = 0; n < N; ++n)
+        for (i64 k = 0; k < K; ++k)
+            for (i64 o = 0; o < Do; ++o)
+                for (i64 p = 0; p < P; ++p)
+                    for (i64 q = 0; q < Q; ++q)
+                        y[IDX5(n, k, o, p, q, K, Do, P, Q)] = conv3d_fwd_one(x, w, b, g, n, k, o, p, q);
+}
+
+/* dx[n,c,d,h,w] = sum over (k,t,r,s) and output positions (o,p,q) with
+ * o sd-pd+t = d, p sh-ph+r = h, q sw-pw+s = w of W[k,c,t,r,s] dy[n,k,o,p,q] */
+void orc_conv3d_input_grad(const double *dy, const double *w, double *dx, const i64 *g)
+{
+    i64 N = g[0], C = g[1], D = g[2], H = g[3], W = g[4], K = g[5], T = g[6], R = g[7], S = g[8];
+    i64 Do = g[9], P = g[10], Q = g[11];
+#pragma omp parallel for collapse(2) schedule(static)
+    for (i64 n = 0; n < N; ++n)
+        for (i64 c = 0; c < C; ++c)
+            for (i64 d = 0; d < D; ++d)
+                for (i64 h = 0; h < H; ++h)
+                    for (i64 ww = 0; ww < W; ++ww) {
+                        double acc = 0.0;
+                        for (i64 k = 0; k < K; ++k)
+                            for (i64 t = 0; t < T; ++t) {
+                                i64 td = d + g[15] - t;
+                                if (td < 0 || td % g[12] != 0 || td / g[12] >= Do) continue;
+                                for (i64 r = 0; r < R; ++r) {
+                                    i64 th = h + g[16] - r;
+                                    if (th < 0 || th % g[13] != 0 || th / g[13] >= P) continue;
+                                    for (i64 s = 0; s < S; ++s) {
+                                        i64 tw = ww + g[17] - s;
+                                        if (tw < 0 || tw % g[14] != 0 || tw / g[14] >= Q) continue;
+                                        acc += w[IDX5(k, c, t, r, s, C, T, R, S)] *
+                                               dy[IDX5(n, k, td / g[12], th / g[13], tw / g[14], K, Do, P, Q)];
+                                    }
+                                }
+                            }
+                        dx[IDX5(n, c, d, h, ww, C, D, H, W)] = acc;
+                    }
+}
+
+/* dW[k,c,t,r,s] = sum_{n,o,p,q} dy[n,k,o,p,q] x[n,c,o sd-pd+t, p sh-ph+r, q sw-pw+s] */
+void orc_conv3d_weight_grad(const double *dy, const double *x, double *dw, const i64 *g)
+{
+    i64 N = g[0], C = g[1], D = g[2], H = g[3], W = g[4], K = g[5], T = g[6], R = g[7], S = g[8];
+    i64 Do = g[9], P = g[10], Q = g[11];
+#pragma omp parallel for collapse(2) schedule(static)
+    for (i64 k = 0; k < K; ++k)
+        for (i64 c = 0; c < C; ++c)
+            for (i64 t = 0; t < T; ++t)
+                for (i64 r = 0; r < R; ++r)
+                    for (i64 s = 0; s < S; ++s) {
+                        double acc = 0.0;
+                        for (i64 n = 0; n < N; ++n)
+                            for (i64 o = 0; o < Do; ++o) {
+                                i64 id = o * g[12] - g[15] + t;
+                                if (id < 0 || id >= D) continue;
+                                for (i64 p = 0; p < P; ++p) {
+                                    i64 ih = p * g[13] - g[16] + r;
+                                    if (ih < 0 || ih >= H) continue;
+                                    for (i64 q = 0; q < Q; ++q) {
+                                        i64 iw = q * g[14] - g[17] + s;
+                                        if (iw < 0 || iw >= W) continue;
+                                        acc += dy[IDX5(n, k, o, p, q, K, Do, P, Q)] * x[IDX5(n, c, id, ih, iw, C, D, H, W)];
+                                    }
+                                }
+                            }
+                        dw[IDX5(k, c, t, r, s, C, T, R, S)] = acc;
+                    }
+}
+
+/* Transposed 3-D convolution, x[N,Ci,D,H,W], W[Ci,Co,T,R,S], output
+ * [N,Co,Do,Ho,Wo]: every input voxel scatters x W through each tap to the
+ * output voxel (d sd-pd+t, h sh-ph+r, w sw-pw+s) when that lies inside.
+ * Here g3 = {N, Ci, D, H, W, Co, T, R, S, Do, Ho, Wo, sd, sh, sw, pd, ph, pw}. */
+void orc_convt3d_forward(const double *x, const double *w, const double *b, double *y, const i64 *g)
+{
+    i64 N = g[0], Ci = g[1], D = g[2], H = g[3], W = g[4], Co = g[5], T = g[6], R = g[7], S = g[8];
+    i64 Do = g[9], Ho = g[10], Wo = g[11];
+#pragma omp parallel for schedule(static)
+    for (i64 n = 0; n < N; ++n) {
+        double *yn = y + n * Co * Do * Ho * Wo;
+        for (i64 o = 0; o < Co; ++o)
+            for (i64 v = 0; v < Do * Ho * Wo; ++v)
+                yn[o * Do * Ho * Wo + v] = b ? b[o] : 0.0;
+        for (i64 i = 0; i < Ci; ++i)
+            for (i64 d = 0; d < D; ++d)
+                for (i64 h = 0; h < H; ++h)
+                    for (i64 ww = 0; ww < W; ++ww) {
+                        double xv = x[IDX5(n, i, d, h, ww, Ci, D, H, W)];
+                        for (i64 o = 0; o < Co; ++o)
+                            for (i64 t = 0; t < T; ++t) {
+                                i64 od = d * g[12] - g[15] + t;
+                                if (od < 0 || od >= Do) continue;
+                                for (i64 r = 0; r < R; ++r) {
+                                    i64 oh = h * g[13] - g[16] + r;
+                                    if (oh < 0 || oh >= Ho) continue;
+                                    for (i64 s = 0; s < S; ++s) {
+                                        i64 ow = ww * g[14] - g[17] + s;
+                                        if (ow < 0 || ow >= Wo) continue;
+                                        yn[((o * Do + od) * Ho + oh) * Wo + ow] += xv * w[IDX5(i, o, t, r, s, Co, T, R, S)];
+                                    }
+                                }
+                            }
+                    }
+    }
+}
+
+/* dx[n,i,d,h,w] = sum_{o,t,r,s} W[i,o,t,r,s] dy[n,o, d sd-pd+t, h sh-ph+r, w sw-pw+s] */
+void orc_convt3d_input_grad(const double *dy, const double *w, double *dx, const i64 *g)
+{
+    i64 N = g[0], Ci = g[1], D = g[2], H = g[3], W = g[4], Co = g[5], T = g[6], R = g[7], S = g[8];
+    i64 Do = g[9], Ho = g[10], Wo = g[11];
+#pragma omp parallel for collapse(2) schedule(static)
+    for (i64 n = 0; n < N; ++n)
+        for (i64 i = 0; i < Ci; ++i)
+            for (i64 d = 0; d < D; ++d)
+                for (i64 h = 0; h < H; ++h)
+                    for (i64 ww = 0; ww < W; ++ww) {
+                        double acc = 0.0;
+                        for (i64 o = 0; o < Co; ++o)
+                            for (i64 t = 0; t < T; ++t) {
+                                i64 od = d * g[12] - g[15] + t;
+                                if (od < 0 || od >= Do) continue;
+                                for (i64 r = 0; r < R; ++r) {
+                                    i64 oh = h * g[13] - g[16] + r;
+                                    if (oh < 0 || oh >= Ho) continue;
+                                    for (i64 s = 0; s < S; ++s) {
+                                        i64 ow = ww * g[14] - g[17] + s;
+                                        if (ow < 0 || ow >= Wo) continue;
+                                        acc += w[IDX5(i, o, t, r, s, Co, T, R, S)] * dy[IDX5(n, o, od, oh, ow, Co, Do, Ho, Wo)];
+                                    }
+                                }
+                            }
+                        dx[IDX5(n, i, d, h, ww, Ci, D, H, W)] = acc;
+                    }
+}
+
+/* dW[i,o,t,r,s] = sum_{n,d,h,w} x[n,i,d,h,w] dy[n,o, d sd-pd+t, h sh-ph+r, w sw-pw+s] */
+void orc_convt3d_weight_grad(const double *dy, const double *x, double *dw, const i64 *g)
+{
+    i64 N = g[0], Ci = g[1], D = g[2], H = g[3], W = g[4], Co = g[5], T = g[6], R = g[7], S = g[8];
+    i64 Do = g[9], Ho = g[10], Wo = g[11];
+#pragma omp parallel for collapse(2) schedule(static)
+    for (i64 i = 0; i < Ci; ++i)
+        for (i64 o = 0; o < Co; ++o)
+            for (i64 t = 0; t < T; ++t)
+                for (i64 r = 0; r < R; ++r)
+                    for (i64 s = 0; s < S; ++s) {
+                        double acc = 0.0;
+                        for (i64 n = 0; n < N; ++n)
+                            for (i64 d = 0; d < D; ++d) {
+                                i64 od = d * g[12] - g[15] + t;
+                                if (od < 0 || od >= Do) continue;
+                                for (i64 h = 0; h < H; ++h) {
+                                    i64 oh = h * g[13] - g[16] + r;
+                                    if (oh < 0 || oh >= Ho) continue;
+                                    for (i64 ww = 0; ww < W; ++ww) {
+                                        i64 ow = ww * g[14] - g[17] + s;
+                                        if (ow < 0 || ow >= Wo) continue;
+                                        acc += x[IDX5(n, i, d, h, ww, Ci, D, H, W)] * dy[IDX5(n, o, od, oh, ow, Co, Do, Ho, Wo)];
+                                    }
+                                }
+                            }
+                        dw[IDX5(i, o, t, r, s, Co, T, R, S)] = acc;
+                    }
+}
+
+/* Bias gradient of a 5-D output: db[k] = sum over (n, o, p, q) of dy. */
+void orc_bias_grad5(const double *dy, double *db, i64 N, i64 K, i64 V)
+{
+#pragma omp parallel for schedule(static)
+    for (i64 k = 0; k < K; ++k) {
+        double acc = 0.0;
+        for (i64 n = 0; n < N; ++n)
+            for (i64 v = 0; v < V; ++v) acc += dy[(n * K + k) * V + v];
+        db[k] = acc;
+    }
 }
 
 /* ---------------------------------------------------------------------------

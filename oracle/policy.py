@@ -54,7 +54,7 @@ def saved_tensors(kind: str, mask: int, policy: int = SELECTIVE,
     i = bool(mask & MASK_INPUT)
     w = bool(mask & MASK_WEIGHT)
     any_flag = mask != 0
-    if kind in ("conv2d", "conv_transpose2d", "linear"):
+    if kind in ("conv2d", "conv_transpose2d", "conv3d", "conv_transpose3d", "linear"):
         if policy == PYTORCH_DEFAULT and kind != "linear":
             return {"x": any_flag, "W": any_flag}
         return {"x": w, "W": i}
