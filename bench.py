@@ -430,8 +430,55 @@ def dropout_bandwidth(steps, warmup):
     return out
 
 
+def conv3d_throughput(steps, warmup):
+    """One training step (forward, input and weight gradients, bias
+    gradient) of a bf16 Conv3d 64 -> 64, 3x3x3, pad 1 on
+    x = (8, 64, 16, 56, 56), and of a bf16 ConvTranspose3d 128 -> 64,
+    2x2x2, stride 2 on x = (8, 128, 8, 28, 28) (the 3-D layers run as the
+    2-D GEMMs on depth-folded inputs).  FLOP: 3 x 2 N Do P Q K C T R S."""
+    import torch
+    import paper_2404_12406_amd as ms
+    out = {}
+    cases = (("conv3d_64x64_3x3x3", ms.Conv3d(1, 1), (8, 64, 16, 56, 56), (64, 64, 3, 3, 3)),
+             ("conv_transpose3d_128x64_2x2x2_s2", ms.ConvTranspose3d(2, 0), (8, 128, 8, 28, 28), (128, 64, 2, 2, 2)))
+    for name, spec, xs, ws in cases:
+        g = torch.Generator(device="cuda").manual_seed(4545)
+        cl = torch.channels_last_3d
+        x = torch.randn(xs, generator=g, device="cuda").to(torch.bfloat16).contiguous(memory_format=cl)
+        w = (0.05 * torch.randn(ws, generator=g, device="cuda")).to(torch.bfloat16).contiguous(memory_format=cl)
+        cy = ws[1] if isinstance(spec, ms.ConvTranspose3d) else ws[0]
+        b = torch.zeros(cy, device="cuda", dtype=torch.bfloat16)
+        yshape = ms.output_shape(spec, x, w)
+        gy = torch.randn(yshape, generator=g, device="cuda").to(torch.bfloat16).contiguous(memory_format=cl)
+        p = ms.PreparedLayer(spec, x, w, b, mask=7, grad_y=gy, grad_x=torch.empty_like(x),
+                             grad_W=torch.empty_like(w), grad_b=torch.empty_like(b))
+        if isinstance(spec, ms.ConvTranspose3d):
+            f = 2 * numel(xs) * ws[1] * ws[2] * ws[3] * ws[4]
+        else:
+            f = 2 * numel(yshape) * ws[1] * ws[2] * ws[3] * ws[4]
+        for _ in range(max(1, warmup)):
+            p.forward()
+            p.backward()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            p.forward()
+            p.backward()
+        e1.record()
+        torch.cuda.synchronize()
+        step_ms = e0.elapsed_time(e1) / steps
+        tf = 3 * f / (step_ms * 1e-3) / 1e12
+        out[name] = {"x": list(xs), "W": list(ws), "ms_per_step": round(step_ms, 4), "gflop": round(3 * f / 1e9, 2),
+                     "tflops": round(tf, 1), "frac_of_peak": round(tf / PEAK_BF16_TFLOPS, 4)}
+        del p, x, w, gy
+    torch.cuda.empty_cache()
+    return out
+
+
 PROBE_SHAPES = {"conv2d": (256, 8, 256, 256), "conv_transpose2d": (256, 8, 256, 256),
-                "conv1d": (4096, 8, 4096), "conv_transpose1d": (4096, 8, 4096)}
+                "conv1d": (4096, 8, 4096), "conv_transpose1d": (4096, 8, 4096),
+                "conv3d": (64, 8, 64, 64, 64), "conv_transpose3d": (64, 8, 64, 64, 64)}
 
 
 def memory_probe(kind: str = "conv2d", depth: int = 16):
@@ -439,7 +486,8 @@ def memory_probe(kind: str = "conv2d", depth: int = 16):
     its App. B repetitions with the other layers linear in input and weight:
     `depth` bias-free size-preserving layers with 8 channels and kernel 3
     (conv2d / conv_transpose2d on (256, 8, 256, 256), conv1d /
-    conv_transpose1d on (4096, 8, 4096); fp32, 512 MiB per layer input), in
+    conv_transpose1d on (4096, 8, 4096), conv3d / conv_transpose3d on
+    (64, 8, 64, 64, 64); fp32, 512 MiB per layer input), in
     three cases -- every layer and the input differentiable, layers 4+
     differentiable, only layer 4 differentiable -- built from torch.nn and
     converted to the library's layers, and the same model with stock PyTorch
@@ -454,7 +502,9 @@ def memory_probe(kind: str = "conv2d", depth: int = 16):
     make = {"conv2d": lambda: nn.Conv2d(8, 8, 3, padding=1, bias=False),
             "conv_transpose2d": lambda: nn.ConvTranspose2d(8, 8, 3, padding=1, bias=False),
             "conv1d": lambda: nn.Conv1d(8, 8, 3, padding=1, bias=False),
-            "conv_transpose1d": lambda: nn.ConvTranspose1d(8, 8, 3, padding=1, bias=False)}[kind]
+            "conv_transpose1d": lambda: nn.ConvTranspose1d(8, 8, 3, padding=1, bias=False),
+            "conv3d": lambda: nn.Conv3d(8, 8, 3, padding=1, bias=False),
+            "conv_transpose3d": lambda: nn.ConvTranspose3d(8, 8, 3, padding=1, bias=False)}[kind]
     out = {"layer": kind, "shape": list(xs), "depth": depth, "dtype": "f32", "layer_input_MiB": per_input / 2 ** 20}
     for impl in ("library", "stock_pytorch"):
         res = {}
@@ -465,14 +515,19 @@ def memory_probe(kind: str = "conv2d", depth: int = 16):
                 layer = i + 1
                 c.weight.requires_grad_(case == "all" or (case == "layers_4_plus" and layer >= 4)
                                         or (case == "layer_4_only" and layer == 4))
-                if impl == "stock_pytorch" and len(xs) == 4:
-                    c.weight.data = c.weight.data.contiguous(memory_format=torch.channels_last)
+                if impl == "stock_pytorch" and len(xs) >= 4:
+                    c.weight.data = c.weight.data.contiguous(
+                        memory_format=torch.channels_last if len(xs) == 4 else torch.channels_last_3d)
             net = nn.Sequential(*convs)
             if impl == "library":
                 msa.convert(net)
             x = torch.randn(xs, device="cuda")
-            x = (x.contiguous(memory_format=torch.channels_last) if len(xs) == 4
-                 else x.transpose(1, 2).contiguous().transpose(1, 2))
+            if len(xs) == 4:
+                x = x.contiguous(memory_format=torch.channels_last)
+            elif len(xs) == 5:
+                x = x.contiguous(memory_format=torch.channels_last_3d)
+            else:
+                x = x.transpose(1, 2).contiguous().transpose(1, 2)
             x.requires_grad_(case == "all")
             torch.cuda.synchronize()
             torch.cuda.reset_peak_memory_stats()
@@ -512,8 +567,11 @@ def extras(steps, warmup):
     t0 = time.time()
     out["fig1_synthetic_cnn_memory"] = f1 = memory_probe("conv2d")
     log(f"[bench] fig1 probe: library {f1['library']}, stock {f1['stock_pytorch']} ({time.time() - t0:.1f}s)")
+    t0 = time.time()
+    out["conv3d_training_step_bf16"] = c3 = conv3d_throughput(steps, warmup)
+    log(f"[bench] 3-D convolutions: {c3} ({time.time() - t0:.1f}s)")
     out["appB_layer_memory"] = {}
-    for kind in ("conv_transpose2d", "conv1d", "conv_transpose1d"):
+    for kind in ("conv_transpose2d", "conv1d", "conv_transpose1d", "conv3d", "conv_transpose3d"):
         t0 = time.time()
         out["appB_layer_memory"][kind] = pr = memory_probe(kind)
         log(f"[bench] App. B probe {kind}: library {pr['library']}, stock {pr['stock_pytorch']} "

@@ -22,7 +22,8 @@
  *    frees or copies caller memory.  `ms_tensor.data` is a device pointer.
  *  - Shapes are given in logical PyTorch order, strides in elements.
  *    4-D activations and conv weights must be channels-last (NHWC / KRSC
- *    memory order, i.e. torch.channels_last); 2-D tensors row-major; 1-D
+ *    memory order, i.e. torch.channels_last), 5-D ones channels-last too
+ *    (NDHWC / KTRSC, torch.channels_last_3d); 2-D tensors row-major; 1-D
  *    tensors contiguous.  Anything else returns MS_E_LAYOUT.
  *  - dtypes: MS_F32 or MS_BF16; all tensors of one call share one dtype.
  *    Products are accumulated in fp32 and rounded once to the output dtype
@@ -73,9 +74,9 @@ typedef enum { MS_F32 = 0, MS_BF16 = 1 } ms_dtype;
 typedef struct {
     void *data;
     int32_t dtype;       /* ms_dtype */
-    int32_t ndim;        /* 1, 2 or 4 */
-    int64_t shape[4];
-    int64_t stride[4];   /* in elements */
+    int32_t ndim;        /* 1, 2, 4 or 5 */
+    int64_t shape[5];
+    int64_t stride[5];   /* in elements */
 } ms_tensor;
 
 typedef enum {
@@ -105,8 +106,18 @@ typedef enum {
                             kernel with x in the role of the output gradient.  The save
                             rule is the convolution's.  A 1-D (transposed) convolution is
                             the 2-D one with H = R = 1, stride_h = 1, pad_h = 0.          */
-    MS_DROPOUT = 6       /* y = x * m / (1 - p), m a random keep mask; layouts as MS_RELU;
+    MS_DROPOUT = 6,      /* y = x * m / (1 - p), m a random keep mask; layouts as MS_RELU;
                             no parameters.  Forward through ms_dropout_forward() only    */
+    MS_CONV3D = 7,       /* 3-D MS_CONV2D (torch.nn.Conv3d, dilation 1, groups 1):
+                            x[N,C,D,H,W], W[K,C,T,R,S], b[K] or NULL, y[N,K,Do,P,Q],
+                            Do = (D + 2 pad_d - T) / stride_d + 1; channels-last 5-D.
+                            Runs the 2-D kernels on the input with its T depth taps
+                            folded into the channels (transient workspace of T / stride_d
+                            times x in the forward and weight gradient)                  */
+    MS_CONV_TRANSPOSE3D = 8 /* 3-D MS_CONV_TRANSPOSE2D: x[N,C_in,D,H,W], W[C_in,C_out,T,R,S],
+                            b[C_out] or NULL, y[N,C_out,Do,Ho,Wo], Do = (D-1) stride_d
+                            - 2 pad_d + T + out_pad_d; the adjoint of the MS_CONV3D with
+                            filter W read as [K = C_in, C = C_out, T, R, S]               */
 } ms_kind;
 
 typedef struct {
@@ -118,6 +129,8 @@ typedef struct {
     const ms_tensor *running_var;   /* BN-eval: sigma_hat^2[C]; never differentiable */
     int32_t out_pad[2];         /* transposed conv: output padding (h, w), 0 <= out_pad < stride;
                                    ignored by the other kinds */
+    int32_t stride_d, pad_d, out_pad_d; /* 3-D kinds: the depth axis's stride (>= 1), pad
+                                   (>= 0) and output padding (transposed, < stride_d) */
 } ms_layer;
 
 /* Opaque saved-tensor record (the AD tape entry of one layer call). */

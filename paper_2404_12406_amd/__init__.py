@@ -9,7 +9,7 @@ The compute lives in libmemsave.so (hand-written HIP kernels, C ABI in
 include/memsave.h); this package is its Python binding.  Build the library
 with `python -m paper_2404_12406_amd.build`.
 """
-from .api import (AvgPool, BatchNormEval, Conv2d, ConvTranspose2d, Dropout, Linear, MASK_BIAS, MASK_INPUT, MASK_WEIGHT,
+from .api import (AvgPool, BatchNormEval, Conv2d, Conv3d, ConvTranspose2d, ConvTranspose3d, Dropout, Linear, MASK_BIAS, MASK_INPUT, MASK_WEIGHT,
                   POLICY_ALL_TRUE, POLICY_PYTORCH_DEFAULT, POLICY_SELECTIVE, PreparedLayer, Record, ReLU,
                   empty_like_layout, layer_backward, layer_forward, ledger_read, ledger_reset, output_shape,
                   policy_account, profile_read, profile_start, PROF_ACT, PROF_BN, PROF_DGRAD, PROF_FWD, PROF_WGRAD,
@@ -17,7 +17,7 @@ from .api import (AvgPool, BatchNormEval, Conv2d, ConvTranspose2d, Dropout, Line
 from ._lib import MemsaveError
 
 __all__ = [
-    "AvgPool", "BatchNormEval", "Conv2d", "ConvTranspose2d", "Dropout", "Linear", "MASK_BIAS", "MASK_INPUT", "MASK_WEIGHT",
+    "AvgPool", "BatchNormEval", "Conv2d", "Conv3d", "ConvTranspose2d", "ConvTranspose3d", "Dropout", "Linear", "MASK_BIAS", "MASK_INPUT", "MASK_WEIGHT",
     "POLICY_ALL_TRUE", "POLICY_PYTORCH_DEFAULT", "POLICY_SELECTIVE", "PreparedLayer", "Record", "ReLU",
     "MemsaveError", "PROF_ACT", "relu_mask_bytes", "dropout_blocks",
     "empty_like_layout", "layer_backward", "layer_forward", "ledger_read", "ledger_reset",

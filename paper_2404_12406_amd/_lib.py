@@ -13,6 +13,7 @@ MS_E_UNSUPPORTED, MS_E_CONSUMED, MS_E_NOMEM, MS_E_HIP, MS_E_ARG = 6, 7, 8, 9, 10
 MS_RG_INPUT, MS_RG_WEIGHT, MS_RG_BIAS = 1, 2, 4
 MS_F32, MS_BF16 = 0, 1
 MS_CONV2D, MS_LINEAR, MS_BN_EVAL, MS_AVGPOOL, MS_RELU, MS_CONV_TRANSPOSE2D, MS_DROPOUT = 0, 1, 2, 3, 4, 5, 6
+MS_CONV3D, MS_CONV_TRANSPOSE3D = 7, 8
 MS_SAVED_X, MS_SAVED_W, MS_SAVED_MEAN, MS_SAVED_VAR, MS_SAVED_BITS, MS_SAVED_Y, MS_SAVED_MASK8 = 1, 2, 4, 8, 16, 32, 64
 MS_K_DGRAD, MS_K_WGRAD, MS_K_BGRAD = 1, 2, 4
 MS_POLICY_SELECTIVE, MS_POLICY_PYTORCH_DEFAULT, MS_POLICY_ALL_TRUE = 0, 1, 2
@@ -30,13 +31,14 @@ MS_PROF_FWD, MS_PROF_DGRAD, MS_PROF_WGRAD, MS_PROF_BN, MS_PROF_ACT = 1, 2, 4, 8,
 
 class MsTensor(ctypes.Structure):
     _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32), ("ndim", ctypes.c_int32),
-                ("shape", ctypes.c_int64 * 4), ("stride", ctypes.c_int64 * 4)]
+                ("shape", ctypes.c_int64 * 5), ("stride", ctypes.c_int64 * 5)]
 
 
 class MsLayer(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("stride", ctypes.c_int32 * 2), ("pad", ctypes.c_int32 * 2),
                 ("eps", ctypes.c_float), ("running_mean", ctypes.POINTER(MsTensor)),
-                ("running_var", ctypes.POINTER(MsTensor)), ("out_pad", ctypes.c_int32 * 2)]
+                ("running_var", ctypes.POINTER(MsTensor)), ("out_pad", ctypes.c_int32 * 2),
+                ("stride_d", ctypes.c_int32), ("pad_d", ctypes.c_int32), ("out_pad_d", ctypes.c_int32)]
 
 
 class MsAccount(ctypes.Structure):

@@ -18,7 +18,8 @@ from typing import Optional, Tuple
 import torch
 
 from . import _lib
-from ._lib import (MS_AVGPOOL, MS_BN_EVAL, MS_CONV2D, MS_CONV_TRANSPOSE2D, MS_DROPOUT, MS_LINEAR, MS_RELU, MS_RG_BIAS,
+from ._lib import (MS_AVGPOOL, MS_BN_EVAL, MS_CONV2D, MS_CONV3D, MS_CONV_TRANSPOSE2D, MS_CONV_TRANSPOSE3D, MS_DROPOUT,
+                   MS_LINEAR, MS_RELU, MS_RG_BIAS,
                    MS_RG_INPUT,
                    MS_RG_WEIGHT, MS_SAVED_BITS, MS_SAVED_MEAN, MS_SAVED_VAR, MS_SAVED_W, MS_SAVED_X,
                    MsAccount, MsLayer, MsTensor, check)
@@ -45,6 +46,21 @@ class ConvTranspose2d:
     stride: Tuple[int, int] | int = 1
     pad: Tuple[int, int] | int = 0
     out_pad: Tuple[int, int] | int = 0
+
+
+@dataclass(frozen=True)
+class Conv3d:
+    """3-D Conv2d: x[N,C,D,H,W], W[K,C,T,R,S]; stride and pad are (d, h, w)."""
+    stride: Tuple[int, int, int] | int = 1
+    pad: Tuple[int, int, int] | int = 0
+
+
+@dataclass(frozen=True)
+class ConvTranspose3d:
+    """3-D ConvTranspose2d: x[N,C_in,D,H,W], W[C_in,C_out,T,R,S]; (d, h, w) triples."""
+    stride: Tuple[int, int, int] | int = 1
+    pad: Tuple[int, int, int] | int = 0
+    out_pad: Tuple[int, int, int] | int = 0
 
 
 @dataclass(frozen=True)
@@ -84,14 +100,18 @@ def _pair(v):
     return (int(v), int(v)) if isinstance(v, int) else (int(v[0]), int(v[1]))
 
 
+def _triple(v):
+    return (int(v),) * 3 if isinstance(v, int) else (int(v[0]), int(v[1]), int(v[2]))
+
+
 def tensor_desc(t: Optional[torch.Tensor]) -> Optional[MsTensor]:
     """Describe a torch tensor for the C ABI (pointer, dtype, shape, strides)."""
     if t is None:
         return None
     if t.dtype not in _DT:
         raise TypeError(f"unsupported dtype {t.dtype}; use float32 or bfloat16")
-    if t.dim() > 4 or t.dim() < 1:
-        raise ValueError("tensors must have 1 to 4 dims")
+    if t.dim() > 5 or t.dim() < 1:
+        raise ValueError("tensors must have 1 to 5 dims")
     d = MsTensor()
     d.data = t.data_ptr() if t.numel() > 0 else None
     d.dtype = _DT[t.dtype]
@@ -124,6 +144,14 @@ class _LayerDesc:
             self.layer.stride[0], self.layer.stride[1] = s
             self.layer.pad[0], self.layer.pad[1] = p
             self.layer.out_pad[0], self.layer.out_pad[1] = o
+        elif isinstance(spec, (Conv3d, ConvTranspose3d)):
+            tr = isinstance(spec, ConvTranspose3d)
+            self.layer.kind = MS_CONV_TRANSPOSE3D if tr else MS_CONV3D
+            s, p = _triple(spec.stride), _triple(spec.pad)
+            o = _triple(spec.out_pad) if tr else (0, 0, 0)
+            self.layer.stride_d, self.layer.stride[0], self.layer.stride[1] = s
+            self.layer.pad_d, self.layer.pad[0], self.layer.pad[1] = p
+            self.layer.out_pad_d, self.layer.out_pad[0], self.layer.out_pad[1] = o
         elif isinstance(spec, Linear):
             self.layer.kind = MS_LINEAR
         elif isinstance(spec, BatchNormEval):
@@ -160,6 +188,17 @@ def output_shape(spec, x: torch.Tensor, W: Optional[torch.Tensor]):
         _, Co, R, S = W.shape
         (sh, sw), (ph, pw), (oh, ow) = _pair(spec.stride), _pair(spec.pad), _pair(spec.out_pad)
         return (N, Co, (H - 1) * sh - 2 * ph + R + oh, (Wd - 1) * sw - 2 * pw + S + ow)
+    if isinstance(spec, Conv3d):
+        N, _, D, H, Wd = x.shape
+        K, _, T, R, S = W.shape
+        s, p = _triple(spec.stride), _triple(spec.pad)
+        return (N, K) + tuple((e + 2 * pp - k) // ss + 1 for e, k, ss, pp in zip((D, H, Wd), (T, R, S), s, p))
+    if isinstance(spec, ConvTranspose3d):
+        N, _, D, H, Wd = x.shape
+        _, Co, T, R, S = W.shape
+        s, p, o = _triple(spec.stride), _triple(spec.pad), _triple(spec.out_pad)
+        return (N, Co) + tuple((e - 1) * ss - 2 * pp + k + oo
+                               for e, k, ss, pp, oo in zip((D, H, Wd), (T, R, S), s, p, o))
     if isinstance(spec, Linear):
         return (x.shape[0], W.shape[0])
     if isinstance(spec, BatchNormEval):
@@ -173,9 +212,11 @@ def output_shape(spec, x: torch.Tensor, W: Optional[torch.Tensor]):
 
 def empty_like_layout(shape, like: torch.Tensor) -> torch.Tensor:
     """Uninitialised tensor of `shape` on like's device in the layout the
-    library requires (channels-last for 4-D)."""
+    library requires (channels-last for 4-D and 5-D)."""
     if len(shape) == 4:
         return torch.empty(shape, dtype=like.dtype, device=like.device, memory_format=torch.channels_last)
+    if len(shape) == 5:
+        return torch.empty(shape, dtype=like.dtype, device=like.device, memory_format=torch.channels_last_3d)
     return torch.empty(shape, dtype=like.dtype, device=like.device)
 
 

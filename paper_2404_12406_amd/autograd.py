@@ -27,14 +27,16 @@ from torch import nn
 from . import api
 from .api import MASK_BIAS, MASK_INPUT, MASK_WEIGHT
 
-__all__ = ["MSConv2d", "MSConvTranspose2d", "MSConv1d", "MSConvTranspose1d", "MSLinear", "MSBatchNorm2dEval",
-           "MSReLU", "MSDropout", "convert"]
+__all__ = ["MSConv2d", "MSConvTranspose2d", "MSConv1d", "MSConvTranspose1d", "MSConv3d", "MSConvTranspose3d",
+           "MSLinear", "MSBatchNorm2dEval", "MSReLU", "MSDropout", "convert"]
 
 
 def _cl(t: Optional[torch.Tensor]) -> Optional[torch.Tensor]:
-    if t is None or t.dim() != 4:
+    """Channels-last for 4-D and 5-D tensors (a copy only when needed)."""
+    if t is None or t.dim() not in (4, 5):
         return t
-    return t if t.is_contiguous(memory_format=torch.channels_last) else t.contiguous(memory_format=torch.channels_last)
+    fmt = torch.channels_last if t.dim() == 4 else torch.channels_last_3d
+    return t if t.is_contiguous(memory_format=fmt) else t.contiguous(memory_format=fmt)
 
 
 def _mask(ctx, ix: int, iw: Optional[int] = None, ib: Optional[int] = None) -> int:
@@ -64,7 +66,7 @@ class _LayerFn(torch.autograd.Function):
         ctx.rec = None
         if rec is None:
             return None, None, None, None
-        gx, gw, gb = api.layer_backward(rec, _cl(grad_y.contiguous() if grad_y.dim() != 4 else grad_y))
+        gx, gw, gb = api.layer_backward(rec, _cl(grad_y.contiguous() if grad_y.dim() < 4 else grad_y))
         rec.free()
         return None, gx, gw, gb
 
@@ -139,6 +141,36 @@ class MSConvTranspose2d(nn.Module):
 
     def forward(self, x):
         return _LayerFn.apply(self.spec, _cl(x), self.weight, self.bias)
+
+
+class _Conv3dBase(nn.Module):
+    def __init__(self, weight, bias):
+        super().__init__()
+        self.weight = weight if isinstance(weight, nn.Parameter) else nn.Parameter(weight)
+        self.bias = bias if (bias is None or isinstance(bias, nn.Parameter)) else nn.Parameter(bias)
+        with torch.no_grad():
+            self.weight.data = _cl(self.weight.data)
+
+    def forward(self, x):
+        return _LayerFn.apply(self.spec, _cl(x), self.weight, self.bias)
+
+
+class MSConv3d(_Conv3dBase):
+    """Conv3d (zero padding, dilation 1, groups 1), channels-last 3-D
+    weight [K, C, T, R, S]."""
+
+    def __init__(self, weight, bias, stride=1, padding=0):
+        super().__init__(weight, bias)
+        self.spec = api.Conv3d(stride, padding)
+
+
+class MSConvTranspose3d(_Conv3dBase):
+    """ConvTranspose3d (dilation 1, groups 1), channels-last 3-D weight
+    [C_in, C_out, T, R, S]."""
+
+    def __init__(self, weight, bias, stride=1, padding=0, output_padding=0):
+        super().__init__(weight, bias)
+        self.spec = api.ConvTranspose3d(stride, padding, output_padding)
 
 
 def _channels_inner(t: torch.Tensor) -> torch.Tensor:
@@ -255,8 +287,8 @@ def _convertible_conv(m) -> bool:
 
 
 def convert(module: nn.Module) -> nn.Module:
-    """Replace, in place, every nn.Conv2d, nn.ConvTranspose2d, nn.Conv1d and
-    nn.ConvTranspose1d (groups 1, dilation 1, zero padding), nn.Linear,
+    """Replace, in place, every nn.Conv1d/2d/3d and nn.ConvTranspose1d/2d/3d
+    (groups 1, dilation 1, zero padding), nn.Linear,
     nn.BatchNorm2d in evaluation mode and nn.ReLU of `module` by the
     library's layers, sharing their parameters and buffers; returns the
     module (Sec. 4: one call swaps every supported layer); nn.Dropout
@@ -274,6 +306,11 @@ def convert(module: nn.Module) -> nn.Module:
             new = MSConv1d(child.weight, child.bias, child.stride, child.padding)
         elif isinstance(child, nn.ConvTranspose1d) and _convertible_conv(child):
             new = MSConvTranspose1d(child.weight, child.bias, child.stride, child.padding, child.output_padding)
+        elif isinstance(child, nn.Conv3d) and _convertible_conv(child):
+            new = MSConv3d(child.weight, child.bias, tuple(child.stride), tuple(child.padding))
+        elif isinstance(child, nn.ConvTranspose3d) and _convertible_conv(child):
+            new = MSConvTranspose3d(child.weight, child.bias, tuple(child.stride), tuple(child.padding),
+                                    tuple(child.output_padding))
         elif isinstance(child, nn.Linear):
             new = MSLinear(child.weight, child.bias)
         elif isinstance(child, nn.BatchNorm2d) and not child.training and child.track_running_stats:

@@ -43,6 +43,29 @@ size_t conv_wgrad_workspace(int dtype, const ConvGeom &g, bool with_db);
 int launch_conv_wgrad(int dtype, const ConvGeom &g, const void *dy, const void *x,
                       void *dw, void *db, void *ws, void *stream, bool *db_done);
 
+// 3-D convolution u[N][Din][H][W][C] -> v[N][Do][P][Q][K], filter
+// W[K][T][R][S][C] (depth taps T, depth stride sd, depth pad pd), run as the
+// 2-D convolution g over N*Do images of the depth-folded input
+// [N*Do][H][W][T*C] with the filter regrouped to [K][R][S][T*C]
+// (conv3d.hip).  g.N = N*Do, g.C = T*C; g's other fields are the 3-D
+// convolution's (H, W, K, R, S, P, Q, strides and pads).
+struct Conv3dGeom {
+    ConvGeom g;
+    int N, C, Din, Do, T, sd, pd;
+};
+// v = conv(u) + bias (bias may be null)
+size_t conv3d_fwd_workspace(int dtype, const Conv3dGeom &q);
+int launch_conv3d_fwd(int dtype, const Conv3dGeom &q, const void *u, const void *w, const void *bias, void *v,
+                      void *ws, void *stream);
+// du = input gradient for dv (+ bias[c] when non-null: the transposed layer's forward)
+size_t conv3d_dgrad_workspace(int dtype, const Conv3dGeom &q);
+int launch_conv3d_dgrad(int dtype, const Conv3dGeom &q, const void *dv, const void *w, const void *bias, void *du,
+                        void *ws, void *stream);
+// dw = weight gradient for dv and u; db as launch_conv_wgrad
+size_t conv3d_wgrad_workspace(int dtype, const Conv3dGeom &q, bool with_db);
+int launch_conv3d_wgrad(int dtype, const Conv3dGeom &q, const void *dv, const void *u, void *dw, void *db, void *ws,
+                        void *stream, bool *db_done);
+
 // out[j] = sum_i in[i][j] for a dense row-major [rows][cols] matrix (bias
 // gradient of conv over N*P*Q rows, of linear over M rows).
 size_t colsum_workspace(int dtype, int64_t rows, int cols);

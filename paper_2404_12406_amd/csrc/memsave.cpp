@@ -98,6 +98,16 @@ bool is_nhwc(const ms_tensor *t) {
     return true;
 }
 
+// Channels-last 5-D: memory order N, D, H, W, C.
+bool is_ndhwc(const ms_tensor *t) {
+    if (numel(t) == 0) return true;
+    const int64_t C = t->shape[1], D = t->shape[2], H = t->shape[3], W = t->shape[4];
+    const int64_t want[5] = {D * H * W * C, 1, H * W * C, W * C, C};
+    for (int i = 0; i < 5; ++i)
+        if (t->shape[i] > 1 && t->stride[i] != want[i]) return false;
+    return true;
+}
+
 bool is_rowmajor2(const ms_tensor *t) {
     if (numel(t) == 0) return true;
     if (t->shape[1] > 1 && t->stride[1] != 1) return false;
@@ -125,6 +135,7 @@ struct Plan {
     int32_t kind = 0;
     int32_t dtype = 0;
     ms::ConvGeom g{};      // conv / linear; transposed conv: the convolution it is the adjoint of
+    ms::Conv3dGeom q{};    // 3-D kinds: the (adjoint) 3-D convolution; g = q.g
     int64_t rows = 0;      // BN / avgpool: pixels; conv/linear bias grad rows
     int C = 0;             // BN / avgpool channels
     int L = 0;             // avgpool pixels per sample
@@ -247,6 +258,85 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
             (Wo + 2 * layer->pad[1] - S) / layer->stride[1] + 1 != Wd)
             return fail(MS_E_ARG, "inconsistent transposed-convolution geometry");
         pl->rows = N * Ho * Wo;
+        pl->x_bytes = (uint64_t)numel(x) * elt_size(x->dtype);
+        pl->w_bytes = (uint64_t)numel(W) * elt_size(W->dtype);
+        return MS_OK;
+    }
+    case MS_CONV3D:
+    case MS_CONV_TRANSPOSE3D: {
+        const bool tr = layer->kind == MS_CONV_TRANSPOSE3D;
+        if ((st = check_tensor(x, "x", 5, need_data))) return st;
+        if (!W) return fail(MS_E_NULL, "3-D convolution needs W");
+        if ((st = check_tensor(W, "W", 5, need_data))) return st;
+        if (x->dtype != W->dtype) return fail(MS_E_DTYPE, "x and W dtypes differ");
+        if (!is_ndhwc(x)) return fail(MS_E_LAYOUT, "x must be channels-last (NDHWC)");
+        if (!is_ndhwc(W)) return fail(MS_E_LAYOUT, "W must be channels-last (memory [W0][T][R][S][W1])");
+        const int64_t N = x->shape[0], Cx = x->shape[1], D = x->shape[2], H = x->shape[3], Wd = x->shape[4];
+        const int64_t T = W->shape[2], R = W->shape[3], S = W->shape[4];
+        const int64_t Cw = tr ? W->shape[0] : W->shape[1];   // W's extent that must match x's channels
+        const int64_t Cy = tr ? W->shape[1] : W->shape[0];   // output channels
+        if (Cw != Cx) return fail(MS_E_SHAPE, "W has %lld input channels, x has %lld", (long long)Cw, (long long)Cx);
+        const int32_t sd = layer->stride_d, pd = layer->pad_d, od = layer->out_pad_d;
+        if (layer->stride[0] < 1 || layer->stride[1] < 1 || sd < 1) return fail(MS_E_ARG, "stride must be >= 1");
+        if (layer->pad[0] < 0 || layer->pad[1] < 0 || pd < 0) return fail(MS_E_ARG, "pad must be >= 0");
+        if (tr && (od < 0 || od >= sd || layer->out_pad[0] < 0 || layer->out_pad[0] >= layer->stride[0] ||
+                   layer->out_pad[1] < 0 || layer->out_pad[1] >= layer->stride[1]))
+            return fail(MS_E_ARG, "out_pad must satisfy 0 <= out_pad < stride");
+        if (Cx < 1 || Cy < 1 || T < 1 || R < 1 || S < 1 || D < 1 || H < 1 || Wd < 1)
+            return fail(MS_E_SHAPE, "3-D convolution extents must be >= 1");
+        int64_t o[3];
+        const int64_t in[3] = {D, H, Wd}, k[3] = {T, R, S};
+        const int64_t sv[3] = {sd, layer->stride[0], layer->stride[1]}, pv[3] = {pd, layer->pad[0], layer->pad[1]};
+        const int64_t ov[3] = {od, layer->out_pad[0], layer->out_pad[1]};
+        for (int i = 0; i < 3; ++i) {
+            if (in[i] + 2 * pv[i] > kMaxElems) return fail(MS_E_UNSUPPORTED, "padding too large");
+            if (tr) {
+                o[i] = (in[i] - 1) * sv[i] - 2 * pv[i] + k[i] + ov[i];
+                if (o[i] < 1) return fail(MS_E_SHAPE, "output would be empty");
+                if (o[i] + 2 * pv[i] > kMaxElems) return fail(MS_E_UNSUPPORTED, "output extent too large");
+            } else {
+                if (in[i] + 2 * pv[i] < k[i]) return fail(MS_E_SHAPE, "kernel larger than the padded input");
+                o[i] = (in[i] + 2 * pv[i] - k[i]) / sv[i] + 1;
+            }
+        }
+        if (b) {
+            if ((st = check_tensor(b, "b", 1, need_data))) return st;
+            if (b->dtype != x->dtype) return fail(MS_E_DTYPE, "b dtype differs from x");
+            if (b->shape[0] != Cy) return fail(MS_E_SHAPE, "b must have %lld elements", (long long)Cy);
+            if (!is_contig1(b)) return fail(MS_E_LAYOUT, "b must be contiguous");
+        }
+        if (y) {
+            if ((st = check_tensor(y, "y", 5, need_data))) return st;
+            if (y->dtype != x->dtype) return fail(MS_E_DTYPE, "y dtype differs from x");
+            if (y->shape[0] != N || y->shape[1] != Cy || y->shape[2] != o[0] || y->shape[3] != o[1] ||
+                y->shape[4] != o[2])
+                return fail(MS_E_SHAPE, "y must be [%lld,%lld,%lld,%lld,%lld]", (long long)N, (long long)Cy,
+                            (long long)o[0], (long long)o[1], (long long)o[2]);
+            if (!is_ndhwc(y)) return fail(MS_E_LAYOUT, "y must be channels-last (NDHWC)");
+        }
+        if (N * o[0] * o[1] * o[2] * Cy > kMaxElems) return fail(MS_E_UNSUPPORTED, "output has more than 2^31-1 elements");
+        // the 3-D convolution u -> v this layer runs (itself, or the one it is the adjoint of)
+        const int64_t Cu = tr ? Cy : Cx, Cv = tr ? Cx : Cy;
+        const int64_t *du = tr ? o : in, *dv = tr ? in : o;
+        const int64_t folded = N * dv[0] * du[1] * du[2] * T * Cu;   // [N*Dv][Hu][Wu][T*Cu]
+        if (folded > kMaxElems || T * Cu > kMaxElems || N * dv[0] > kMaxElems)
+            return fail(MS_E_UNSUPPORTED, "depth-folded input has more than 2^31-1 elements");
+        pl->dtype = x->dtype;
+        pl->q.N = (int)N;
+        pl->q.C = (int)Cu;
+        pl->q.Din = (int)du[0];
+        pl->q.Do = (int)dv[0];
+        pl->q.T = (int)T;
+        pl->q.sd = sd;
+        pl->q.pd = pd;
+        pl->q.g = ms::ConvGeom{(int)(N * dv[0]), (int)(T * Cu), (int)du[1], (int)du[2], (int)Cv, (int)R, (int)S,
+                               (int)dv[1], (int)dv[2], layer->stride[0], layer->stride[1], layer->pad[0], layer->pad[1]};
+        if ((du[1] + 2 * layer->pad[0] - R) / layer->stride[0] + 1 != dv[1] ||
+            (du[2] + 2 * layer->pad[1] - S) / layer->stride[1] + 1 != dv[2] || (du[0] + 2 * pd - T) / sd + 1 != dv[0])
+            return fail(MS_E_ARG, "inconsistent 3-D convolution geometry");
+        pl->g = pl->q.g;
+        pl->rows = N * o[0] * o[1] * o[2];   // bias-gradient rows of the output
+        pl->C = (int)Cy;
         pl->x_bytes = (uint64_t)numel(x) * elt_size(x->dtype);
         pl->w_bytes = (uint64_t)numel(W) * elt_size(W->dtype);
         return MS_OK;
@@ -377,6 +467,8 @@ uint32_t borrowed_bits(int32_t kind, uint32_t mask, int32_t policy, bool has_w, 
     switch (kind) {
     case MS_CONV2D:
     case MS_CONV_TRANSPOSE2D:   // stock PyTorch keeps both for either (Fig. 2, App. B)
+    case MS_CONV3D:
+    case MS_CONV_TRANSPOSE3D:
         if (policy == MS_POLICY_PYTORCH_DEFAULT) return MS_SAVED_X | MS_SAVED_W;
         return (w ? (uint32_t)MS_SAVED_X : 0u) | (in ? (uint32_t)MS_SAVED_W : 0u);
     case MS_LINEAR:   // PyTorch's Linear is already selective (App. B)
@@ -417,6 +509,15 @@ size_t backward_workspace(const Plan &pl, uint32_t kernels) {
         if (kernels & MS_K_DGRAD) ws = std::max(ws, ms::conv_fwd_workspace(pl.dtype, pl.g));
         if (kernels & MS_K_WGRAD) ws = std::max(ws, ms::conv_wgrad_workspace(pl.dtype, pl.g, false));
         if (kernels & MS_K_BGRAD) ws = std::max(ws, ms::colsum_workspace(pl.dtype, pl.rows, pl.g.C));
+    } else if (pl.kind == MS_CONV3D) {
+        if (kernels & MS_K_DGRAD) ws = std::max(ws, ms::conv3d_dgrad_workspace(pl.dtype, pl.q));
+        if (kernels & MS_K_WGRAD)
+            ws = std::max(ws, ms::conv3d_wgrad_workspace(pl.dtype, pl.q, (kernels & MS_K_BGRAD) != 0));
+        if (kernels & MS_K_BGRAD) ws = std::max(ws, ms::colsum_workspace(pl.dtype, pl.rows, pl.C));
+    } else if (pl.kind == MS_CONV_TRANSPOSE3D) {
+        if (kernels & MS_K_DGRAD) ws = std::max(ws, ms::conv3d_fwd_workspace(pl.dtype, pl.q));
+        if (kernels & MS_K_WGRAD) ws = std::max(ws, ms::conv3d_wgrad_workspace(pl.dtype, pl.q, false));
+        if (kernels & MS_K_BGRAD) ws = std::max(ws, ms::colsum_workspace(pl.dtype, pl.rows, pl.C));
     } else if (pl.kind == MS_BN_EVAL) {
         if (kernels & (MS_K_WGRAD | MS_K_BGRAD)) ws = ms::bn_bwd_workspace(pl.dtype, pl.rows, pl.C);
     }
@@ -482,6 +583,7 @@ ms_status check_grad(const ms_tensor *g, const ms_tensor *primal, const char *na
     if (g->dtype != primal->dtype) return fail(MS_E_DTYPE, "%s dtype must match its primal", name);
     if (!same_shape(g, primal)) return fail(MS_E_SHAPE, "%s shape must match its primal", name);
     if (g->ndim == 4 && !is_nhwc(g)) return fail(MS_E_LAYOUT, "%s must be channels-last", name);
+    if (g->ndim == 5 && !is_ndhwc(g)) return fail(MS_E_LAYOUT, "%s must be channels-last", name);
     if (g->ndim == 2 && !is_rowmajor2(g)) return fail(MS_E_LAYOUT, "%s must be row-major", name);
     if (g->ndim == 1 && !is_contig1(g)) return fail(MS_E_LAYOUT, "%s must be contiguous", name);
     (void)kind;
@@ -509,9 +611,12 @@ ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
     // transient forward workspace (zero-padded channel copies for channel
     // counts that are not a multiple of 8), taken before anything is launched
     void *fws = nullptr;
-    if (pl.kind == MS_CONV2D || pl.kind == MS_LINEAR || pl.kind == MS_CONV_TRANSPOSE2D) {
-        const size_t fb = pl.kind == MS_CONV_TRANSPOSE2D ? ms::conv_dgrad_workspace(pl.dtype, pl.g)
-                                                         : ms::conv_fwd_workspace(pl.dtype, pl.g);
+    if (pl.kind == MS_CONV2D || pl.kind == MS_LINEAR || pl.kind == MS_CONV_TRANSPOSE2D || pl.kind == MS_CONV3D ||
+        pl.kind == MS_CONV_TRANSPOSE3D) {
+        const size_t fb = pl.kind == MS_CONV_TRANSPOSE2D    ? ms::conv_dgrad_workspace(pl.dtype, pl.g)
+                          : pl.kind == MS_CONV3D            ? ms::conv3d_fwd_workspace(pl.dtype, pl.q)
+                          : pl.kind == MS_CONV_TRANSPOSE3D ? ms::conv3d_dgrad_workspace(pl.dtype, pl.q)
+                                                            : ms::conv_fwd_workspace(pl.dtype, pl.g);
         if (fb) {
             int werr = 0;
             fws = ms::workspace_get(stream, fb, &werr);
@@ -533,6 +638,12 @@ ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
     case MS_CONV_TRANSPOSE2D:   // the input-gradient contraction of the convolution y -> x, plus b
         err = ms::launch_conv_dgrad(pl.dtype, pl.g, x->data, W->data, b ? b->data : nullptr, y->data, fws,
                                     stream);
+        break;
+    case MS_CONV3D:
+        err = ms::launch_conv3d_fwd(pl.dtype, pl.q, x->data, W->data, b ? b->data : nullptr, y->data, fws, stream);
+        break;
+    case MS_CONV_TRANSPOSE3D:
+        err = ms::launch_conv3d_dgrad(pl.dtype, pl.q, x->data, W->data, b ? b->data : nullptr, y->data, fws, stream);
         break;
     case MS_BN_EVAL:
         err = ms::launch_bn_fwd(pl.dtype, x->data, layer->running_mean->data, layer->running_var->data,
@@ -634,6 +745,30 @@ ms_status ms_layer_backward(ms_record *r, const ms_tensor *grad_y, const ms_tens
             err = ms::launch_conv_wgrad(pl.dtype, pl.g, r->x.data, dy, grad_W->data, nullptr, ws, stream, &db_unused);
         if (!err && (kernels & MS_K_BGRAD))
             err = ms::launch_colsum(pl.dtype, dy, pl.rows, pl.g.C, grad_b->data, ws, stream);
+    }
+        break;
+    case MS_CONV3D:
+    {
+        bool db_done = false;
+        if (kernels & MS_K_DGRAD)
+            err = ms::launch_conv3d_dgrad(pl.dtype, pl.q, dy, r->W.data, nullptr, grad_x->data, ws, stream);
+        if (!err && (kernels & MS_K_WGRAD))
+            err = ms::launch_conv3d_wgrad(pl.dtype, pl.q, dy, r->x.data, grad_W->data,
+                                          (kernels & MS_K_BGRAD) ? grad_b->data : nullptr, ws, stream, &db_done);
+        if (!err && (kernels & MS_K_BGRAD) && !db_done)
+            err = ms::launch_colsum(pl.dtype, dy, pl.rows, pl.C, grad_b->data, ws, stream);
+    }
+        break;
+    case MS_CONV_TRANSPOSE3D:
+    {
+        // adjoint of the 3-D convolution q (input y-shaped, output x-shaped)
+        bool db_unused = false;
+        if (kernels & MS_K_DGRAD)
+            err = ms::launch_conv3d_fwd(pl.dtype, pl.q, dy, r->W.data, nullptr, grad_x->data, ws, stream);
+        if (!err && (kernels & MS_K_WGRAD))
+            err = ms::launch_conv3d_wgrad(pl.dtype, pl.q, r->x.data, dy, grad_W->data, nullptr, ws, stream, &db_unused);
+        if (!err && (kernels & MS_K_BGRAD))
+            err = ms::launch_colsum(pl.dtype, dy, pl.rows, pl.C, grad_b->data, ws, stream);
     }
         break;
     case MS_BN_EVAL:

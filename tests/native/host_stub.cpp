@@ -98,6 +98,35 @@ int launch_conv_wgrad(int dtype, const ConvGeom &g, const void *dy, const void *
     return e;
 }
 
+size_t conv3d_fwd_workspace(int, const Conv3dGeom &q) { return (size_t)q.g.N * q.g.H * q.g.W * q.g.C * 2 + 256; }
+size_t conv3d_dgrad_workspace(int, const Conv3dGeom &q) { return (size_t)q.g.N * q.g.H * q.g.W * q.g.C * 2 + 512; }
+size_t conv3d_wgrad_workspace(int, const Conv3dGeom &q, bool) { return (size_t)q.g.N * q.g.H * q.g.W * q.g.C * 2 + 768; }
+
+int launch_conv3d_fwd(int, const Conv3dGeom &q, const void *u, const void *w, const void *, void *v, void *ws,
+                      void *) {
+    log("conv3d_fwd");
+    int e = need(ws, "conv3d_fwd:ws");
+    if ((long long)q.g.N * q.g.P * q.g.Q * q.g.K > 0) e |= need(u && w && v, "conv3d_fwd:u,w,v");
+    return e;
+}
+
+int launch_conv3d_dgrad(int, const Conv3dGeom &q, const void *dv, const void *w, const void *bias, void *du,
+                        void *ws, void *) {
+    log(bias ? "conv3d_dgrad+bias" : "conv3d_dgrad");
+    int e = need(ws, "conv3d_dgrad:ws");
+    if ((long long)q.N * q.Din * q.g.H * q.g.W * q.C > 0) e |= need(dv && w && du, "conv3d_dgrad:dv,w,du");
+    return e;
+}
+
+int launch_conv3d_wgrad(int dtype, const Conv3dGeom &q, const void *dv, const void *u, void *dw, void *db, void *ws,
+                        void *, bool *db_done) {
+    log(db && dtype == kBF16 ? "conv3d_wgrad+db" : "conv3d_wgrad");
+    *db_done = db != nullptr && dtype == kBF16;
+    int e = need(ws && dw, "conv3d_wgrad:ws,dw");
+    if ((long long)q.g.N * q.g.P * q.g.Q > 0) e |= need(dv && u, "conv3d_wgrad:dv,u");
+    return e;
+}
+
 size_t colsum_workspace(int, int64_t, int cols) { return (size_t)cols * 4 * 8; }
 
 int launch_colsum(int, const void *in, int64_t rows, int cols, void *out, void *ws, void *) {

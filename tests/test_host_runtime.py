@@ -54,6 +54,9 @@ def tdesc(shape, dtype="bf16", layout="auto", data=True, addr=FAKE):
     if len(shape) == 4 and layout in ("auto", "nhwc"):
         N, C, H, W = shape
         st = (H * W * C, 1, W * C, C)
+    elif len(shape) == 5 and layout in ("auto", "nhwc"):
+        N, C, D, H, W = shape
+        st = (D * H * W * C, 1, H * W * C, W * C, C)
     else:
         st, acc = [], 1
         for s in reversed(shape):
@@ -707,3 +710,99 @@ def test_dropout_policy_account(stub, dtype):
             assert stub.ms_policy_account(ctypes.byref(layer), ref(x), None, None, mask, policy, ctypes.byref(a)) == 0
             assert a.saved_activation_bytes == P.saved_activation_bytes("dropout", mask, n, dtype, policy)
             assert bool(a.borrowed & L.MS_SAVED_MASK8) == (policy == P.PYTORCH_DEFAULT and mask == 1)
+
+
+# ------------------------------------------------------------------ 3-D convolutions
+class Conv3dArgs:
+    def __init__(self, x_shape, c_out, k, stride, pad, out_pad=None, dtype="bf16", bias=True, data=True):
+        tr = out_pad is not None
+        N, C, D, H, W = x_shape
+        self.layer = L.MsLayer()
+        self.layer.kind = L.MS_CONV_TRANSPOSE3D if tr else L.MS_CONV3D
+        self.layer.stride_d, self.layer.stride[0], self.layer.stride[1] = stride
+        self.layer.pad_d, self.layer.pad[0], self.layer.pad[1] = pad
+        if tr:
+            self.layer.out_pad_d, self.layer.out_pad[0], self.layer.out_pad[1] = out_pad
+            out = [(e - 1) * s - 2 * p + kk + o for e, kk, s, p, o in zip((D, H, W), k, stride, pad, out_pad)]
+            self.w_shape = (C, c_out) + tuple(k)
+        else:
+            out = [(e + 2 * p - kk) // s + 1 for e, kk, s, p in zip((D, H, W), k, stride, pad)]
+            self.w_shape = (c_out, C) + tuple(k)
+        self.x_shape, self.y_shape = x_shape, (N, c_out) + tuple(out)
+        self.x = tdesc(x_shape, dtype, data=data)
+        self.W = tdesc(self.w_shape, dtype, data=data)
+        self.b = tdesc((c_out,), dtype, data=data) if bias else None
+        self.y = tdesc(self.y_shape, dtype, data=data)
+        self.dtype, self.tr = dtype, tr
+
+
+CONV3D = [
+    ((2, 8, 6, 7, 5), 16, (3, 3, 3), (1, 1, 1), (1, 1, 1), None),
+    ((1, 3, 5, 8, 8), 8, (3, 1, 2), (2, 1, 2), (1, 0, 1), None),
+    ((2, 16, 3, 4, 4), 8, (2, 4, 4), (2, 2, 2), (0, 1, 1), (1, 0, 1)),
+    ((1, 8, 4, 5, 3), 3, (3, 3, 3), (1, 2, 1), (1, 1, 1), (0, 1, 0)),
+]
+
+
+@pytest.mark.parametrize("case", range(len(CONV3D)))
+def test_conv3d_policy_and_plan(stub, case):
+    a = Conv3dArgs(*CONV3D[case])
+    kind = "conv_transpose3d" if a.tr else "conv3d"
+    numel = _numel(a.x_shape)
+    for mask in range(8):
+        for pol in (P.SELECTIVE, P.PYTORCH_DEFAULT, P.ALL_TRUE):
+            acct = L.MsAccount()
+            assert stub.ms_policy_account(ctypes.byref(a.layer), ref(a.x), ref(a.W), ref(a.b), mask, pol,
+                                          ctypes.byref(acct)) == 0, stub.ms_last_error()
+            assert acct.saved_activation_bytes == P.saved_activation_bytes(kind, mask, numel, a.dtype, pol)
+        stub.stub_reset()
+        h = ctypes.c_void_p()
+        assert stub.ms_layer_forward(ctypes.byref(a.layer), ref(a.x), ref(a.W), ref(a.b), mask, ref(a.y),
+                                     ctypes.byref(h), None) == 0, stub.ms_last_error()
+        assert stub.stub_log().decode() == ("conv3d_dgrad+bias;" if a.tr else "conv3d_fwd;")
+        if mask == 0:
+            assert not h.value
+            continue
+        stub.stub_reset()
+        gy = tdesc(a.y_shape)
+        gx = tdesc(a.x_shape) if mask & 1 else None
+        gw = tdesc(a.w_shape) if mask & 2 else None
+        gb = tdesc((a.y_shape[1],)) if mask & 4 else None
+        assert stub.ms_layer_backward(h, ref(gy), ref(gx), ref(gw), ref(gb), None) == 0, stub.ms_last_error()
+        assert stub.stub_violations().decode() == ""
+        log = stub.stub_log().decode().split(";")[:-1]
+        if a.tr:
+            want = [n for n, f in (("conv3d_fwd", 1), ("conv3d_wgrad", 2), ("colsum", 4)) if mask & f]
+        else:
+            want = [n for n, f in (("conv3d_dgrad", 1), ("conv3d_wgrad+db" if mask & 4 else "conv3d_wgrad", 2))
+                    if mask & f]
+            if mask & 4 and not mask & 2:
+                want.append("colsum")
+        assert log == want, (mask, log)
+        stub.ms_record_free(h)
+    assert stub.ms_testing_live_records() == 0
+
+
+def test_conv3d_validation(stub):
+    def fwd(a, x=None, W=None, y=None):
+        h = ctypes.c_void_p()
+        stub.stub_reset()
+        st = stub.ms_layer_forward(ctypes.byref(a.layer), ref(x or a.x), ref(W or a.W), ref(a.b), 7,
+                                   ref(y or a.y), ctypes.byref(h), None)
+        assert stub.stub_log().decode() == "" and not h.value
+        return st
+
+    a = Conv3dArgs((2, 8, 6, 7, 5), 16, (3, 3, 3), (1, 1, 1), (1, 1, 1))
+    assert fwd(a, x=tdesc(a.x_shape, layout="ncdhw")) == L.MS_E_LAYOUT
+    assert fwd(a, W=tdesc((16, 8, 3, 3, 2))) == L.MS_E_SHAPE       # y no longer matches
+    assert fwd(a, W=tdesc((16, 4, 3, 3, 3))) == L.MS_E_SHAPE
+    assert fwd(a, x=tdesc((2, 8, 6, 7))) == L.MS_E_SHAPE            # 4-D x
+    a.layer.stride_d = 0
+    assert fwd(a) == L.MS_E_ARG
+    a.layer.stride_d = 1
+    a.layer.pad_d = -1
+    assert fwd(a) == L.MS_E_ARG
+    a.layer.pad_d = 1
+    t = Conv3dArgs((2, 16, 3, 4, 4), 8, (2, 4, 4), (2, 2, 2), (0, 1, 1), (1, 0, 1))
+    t.layer.out_pad_d = 2                                           # out_pad >= stride
+    assert fwd(t) == L.MS_E_ARG
