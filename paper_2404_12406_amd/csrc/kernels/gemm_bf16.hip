@@ -999,6 +999,18 @@ constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 // beats that one by ~5% on the forward and input gradient of 4096 x 1024
 // outputs with K = 4096 (38.7 -> 36.3 us)
 constexpr bool kAuto[kNumTiles] = {true, true, true, true, false, true, true, true};
+// tiles the planner chooses from for the input gradient of convolutions
+// that are not 1x1 / stride 1 (implicit-GEMM gathers): on the
+// ResNet-18-shaped stack's layers and the conv sweep the 2-stage 128 x 128
+// tile (128 x 64 for 64 channels) was fastest or within 2% of it, and the
+// 8-wave, 4-stage and k-group tiles lost by up to 35% (14 x 14 x 256: k-group
+// 45 us against 33); that input gradient goes through the transposed filter
+// (the in-place variant wants an 8-wave tile).  Whole steps on one box: the
+// input-variant stack 2.32 -> 2.27 ms, the 3x3 conv sweep (input mask)
+// 0.121 -> 0.116 ms.  The forward keeps the general set: restricted the same
+// way it took split reductions whose extra pass made the frozen stack 6%
+// slower.
+constexpr bool kAutoConv[kNumTiles] = {true, false, true, false, false, false, false, true};
 
 // MEMSAVE_GEMM_TILE=<name> forces one tile shape (a debugging and testing
 // knob); returns its index or -1.
@@ -1058,20 +1070,25 @@ struct GemmPlan {
     int splits, k_split;
 };
 
+// Use of the k-group tile: by the planner, only when forced by the testing
+// knob, or never (the weight gradient has no k-group instantiation).
+enum KgUse { kKgNever = 0, kKgForced = 1, kKgAuto = 2 };
+
 // Tile and split count for the forward or weight gradient (z = 1) or the input gradient (z stride
 // phases) with at most max_splits splits of at least 4 BK steps each.
 GemmPlan plan_gemm(long M, long N, long K, int z, int split_cap = 16, bool allow_256x256 = true,
-                   bool allow_kgroups = true) {
+                   int kgroups = kKgAuto, const bool *auto_set = kAuto) {
     int forced = forced_tile();
+    if (forced >= 0 && kTiles[forced].kg > 1 && kgroups == kKgNever) forced = -1;   // not built: plan as usual
     if (forced == 0 && !allow_256x256) forced = 1;   // the next widest tile (256 x 128)
     const int fs = split_cap > 1 ? forced_splits() : 0;
     const int max_splits = (int)std::max<long>(1, std::min<long>(split_cap, K / (4 * BK)));
     double best = 1e300;
     GemmPlan bp{kTiles[0], 1, (int)K};
     for (int ti = 0; ti < kNumTiles; ++ti) {
-        if (forced >= 0 ? ti != forced : !kAuto[ti]) continue;
+        if (forced >= 0 ? ti != forced : !auto_set[ti]) continue;
         if (ti == 0 && !allow_256x256) continue;
-        if (kTiles[ti].kg > 1 && !allow_kgroups) continue;
+        if (kTiles[ti].kg > 1 && (kgroups == kKgNever || (kgroups == kKgForced && forced < 0))) continue;
         for (int sp = 1; sp <= (fs ? 1 : max_splits); ++sp) {
             const int splits = fs ? fs : sp;
             const double us = est_us(kTiles[ti], M, N, K, z, splits);
@@ -1184,7 +1201,8 @@ Tile pick_conv_wgrad(long M, long N, long K, int splits_allowed, int *splits_out
     double best = 1e300;
     Tile bt = kTiles[0];
     int bs = 1;
-    const int forced = forced_tile();
+    int forced = forced_tile();
+    if (forced >= 0 && kTiles[forced].kg > 1) forced = -1;   // no k-group weight gradient: plan as usual
     for (int ti = 0; ti < kNumTiles; ++ti) {
         if (forced >= 0 ? ti != forced : !kAuto[ti]) continue;
         const Tile &t = kTiles[ti];
@@ -1217,7 +1235,7 @@ WgradPlan wgrad_plan(const ConvGeom &g) {
     const long M = g.K, N = (long)g.R * g.S * g.C, K = (long)g.N * g.P * g.Q;
     if (unit_geom(g)) {
         // (the weight gradient has no k-group tile)
-        const GemmPlan p = plan_gemm(M, N, K, 1, 16, true, false);
+        const GemmPlan p = plan_gemm(M, N, K, 1, 16, true, kKgNever);
         return {p.t, p.splits, p.k_split};
     }
     int splits = 1;
@@ -1321,13 +1339,17 @@ DgradChoice dgrad_choice(const ConvGeom &g) {
     const long Kb = (long)((g.R + g.sh - 1) / g.sh) * ((g.S + g.sw - 1) / g.sw) * g.K;
     const long M = (long)g.N * Hb * Wb;
     const int z = g.sh * g.sw;
+    const bool unit = unit_geom(g);
+    const int kg = unit ? kKgAuto : kKgForced;
+    const bool *set = unit ? kAuto : kAutoConv;
     const char *e = getenv("MEMSAVE_DGRAD");
     if (e && *e) {
         const bool direct = e[0] == 'd';
-        return {direct, plan_gemm(M, g.C, Kb, z, direct ? 1 : 16, direct || unit_geom(g))};
+        return {direct, plan_gemm(M, g.C, Kb, z, direct ? 1 : 16, direct || unit, kg, set)};
     }
-    const GemmPlan pd = plan_gemm(M, g.C, Kb, z, 1, true);
-    const GemmPlan pt = plan_gemm(M, g.C, Kb, z, 16, unit_geom(g));
+    const GemmPlan pt = plan_gemm(M, g.C, Kb, z, 16, unit, kg, set);
+    if (!unit) return {false, pt};
+    const GemmPlan pd = plan_gemm(M, g.C, Kb, z, 1, true, kg);
     if (pd.t.wr * pd.t.wc * pd.t.kg == 8 && pt.splits == 1) return {true, pd};
     return {false, pt};
 }
