@@ -33,71 +33,82 @@ int blocks_for(int64_t work) {
     return (int)std::max<int64_t>(1, std::min<int64_t>((work + 255) / 256, 65536));
 }
 
-// fold: out[(n*Do + o)*HW + hw][t*C + c] = in[(n*Din + o*sd - pd + t)*HW + hw][c] or 0.
-// V elements per thread step (16 bytes when C is a multiple of V).
+// V consecutive channels: one 16-byte vector when V * sizeof(T) == 16.
 template <typename T, int V>
-__global__ __launch_bounds__(256) void depth_fold_kernel(const T *__restrict__ in, T *__restrict__ out, int64_t N,
-                                                         int64_t Din, int64_t Do, int64_t HW, int64_t C, int64_t Tt,
-                                                         int64_t sd, int64_t pd) {
-    const int64_t cv = C / V;                      // vectors per channel run
-    const int64_t total = N * Do * HW * Tt * cv;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-        int64_t r = i;
-        const int64_t c0 = (r % cv) * V;
-        r /= cv;
-        const int64_t t = r % Tt;
-        r /= Tt;
-        const int64_t hw = r % HW;
-        r /= HW;
-        const int64_t o = r % Do;
-        const int64_t n = r / Do;
-        const int64_t d = o * sd - pd + t;
-        T *dst = out + ((n * Do + o) * HW + hw) * (Tt * C) + t * C + c0;
+struct Chan {
+    T e[V];
+    __device__ __forceinline__ void load(const T *p) {
+        if constexpr (V * sizeof(T) == 16) *reinterpret_cast<u32x4 *>(e) = *reinterpret_cast<const u32x4 *>(p);
+        else
+#pragma unroll
+            for (int k = 0; k < V; ++k) e[k] = p[k];
+    }
+    __device__ __forceinline__ void store(T *p) const {
+        if constexpr (V * sizeof(T) == 16) *reinterpret_cast<u32x4 *>(p) = *reinterpret_cast<const u32x4 *>(e);
+        else
+#pragma unroll
+            for (int k = 0; k < V; ++k) p[k] = e[k];
+    }
+};
+
+// fold: out[(n*Do + o)*HW + hw][t*C + c] = in[(n*Din + o*sd - pd + t)*HW + hw][c] or 0.
+// A thread moves V channels (16 bytes when C is a multiple of V) of one
+// (output pixel, tap); indices are 32-bit (every buffer has fewer than 2^31
+// elements).
+template <typename T, int V>
+__global__ __launch_bounds__(256) void depth_fold_kernel(const T *__restrict__ in, T *__restrict__ out, int N,
+                                                         int Din, int Do, int HW, int C, int Tt, int sd, int pd) {
+    const uint32_t cv = (uint32_t)(C / V);                  // vectors per channel run
+    const uint32_t per_pix = (uint32_t)Tt * cv;             // vectors per folded pixel row
+    const uint32_t total = (uint32_t)N * Do * HW * per_pix;
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+        const uint32_t pix = i / per_pix, j = i - pix * per_pix;   // pix = (n*Do + o)*HW + hw
+        const uint32_t t = j / cv, c0 = (j - t * cv) * V;
+        const uint32_t img = pix / (uint32_t)HW, hw = pix - img * (uint32_t)HW;
+        const uint32_t n = img / (uint32_t)Do, o = img - n * (uint32_t)Do;
+        const int d = (int)o * sd - pd + (int)t;
+        Chan<T, V> v;
         if (d >= 0 && d < Din) {
-            const T *src = in + ((n * Din + d) * HW + hw) * C + c0;
-            if constexpr (V * sizeof(T) == 16) {
-                *reinterpret_cast<u32x4 *>(dst) = *reinterpret_cast<const u32x4 *>(src);
-            } else {
-#pragma unroll
-                for (int e = 0; e < V; ++e) dst[e] = src[e];
-            }
+            v.load(in + ((size_t)(n * (uint32_t)Din + (uint32_t)d) * HW + hw) * C + c0);
         } else {
-            if constexpr (V * sizeof(T) == 16) {
-                *reinterpret_cast<u32x4 *>(dst) = u32x4{0u, 0u, 0u, 0u};
-            } else {
 #pragma unroll
-                for (int e = 0; e < V; ++e) dst[e] = (T)0.f;
-            }
+            for (int k = 0; k < V; ++k) v.e[k] = (T)0.f;
         }
+        v.store(out + (size_t)pix * (Tt * C) + t * C + c0);
     }
 }
 
 // unfold_sum: out[(n*Dout + d)*HW + hw][c] = bias[c] + sum over t with
 // o = (d + pd - t) / sd an integer in [0, Dc) of in[(n*Dc + o)*HW + hw][t*C + c],
-// summed in fp32 and rounded once.
-template <typename T>
+// summed in fp32 and rounded once.  A thread owns V channels of one output
+// pixel.
+template <typename T, int V>
 __global__ __launch_bounds__(256) void depth_unfold_sum_kernel(const T *__restrict__ in, T *__restrict__ out,
-                                                               const T *__restrict__ bias, int64_t N, int64_t Dc,
-                                                               int64_t Dout, int64_t HW, int64_t C, int64_t Tt,
-                                                               int64_t sd, int64_t pd) {
-    const int64_t total = N * Dout * HW * C;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-        int64_t r = i;
-        const int64_t c = r % C;
-        r /= C;
-        const int64_t hw = r % HW;
-        r /= HW;
-        const int64_t d = r % Dout;
-        const int64_t n = r / Dout;
-        float acc = bias ? to_f32(bias[c]) : 0.f;
-        for (int64_t t = 0; t < Tt; ++t) {
-            const int64_t q = d + pd - t;
+                                                               const T *__restrict__ bias, int N, int Dc, int Dout,
+                                                               int HW, int C, int Tt, int sd, int pd) {
+    const uint32_t cv = (uint32_t)(C / V);
+    const uint32_t total = (uint32_t)N * Dout * HW * cv;
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+        const uint32_t pix = i / cv, c0 = (i - pix * cv) * V;      // pix = (n*Dout + d)*HW + hw
+        const uint32_t img = pix / (uint32_t)HW, hw = pix - img * (uint32_t)HW;
+        const uint32_t n = img / (uint32_t)Dout, d = img - n * (uint32_t)Dout;
+        float acc[V];
+#pragma unroll
+        for (int k = 0; k < V; ++k) acc[k] = bias ? to_f32(bias[c0 + k]) : 0.f;
+        for (int t = 0; t < Tt; ++t) {
+            const int q = (int)d + pd - t;
             if (q < 0 || q % sd != 0) continue;
-            const int64_t o = q / sd;
+            const int o = q / sd;
             if (o >= Dc) continue;
-            acc += to_f32(in[((n * Dc + o) * HW + hw) * (Tt * C) + t * C + c]);
+            Chan<T, V> v;
+            v.load(in + ((size_t)(n * (uint32_t)Dc + (uint32_t)o) * HW + hw) * (Tt * C) + t * C + c0);
+#pragma unroll
+            for (int k = 0; k < V; ++k) acc[k] += to_f32(v.e[k]);
         }
-        out[i] = from_f32<T>(acc);
+        Chan<T, V> r;
+#pragma unroll
+        for (int k = 0; k < V; ++k) r.e[k] = from_f32<T>(acc[k]);
+        r.store(out + (size_t)pix * C + c0);
     }
 }
 
@@ -121,33 +132,37 @@ __global__ __launch_bounds__(256) void regroup_taps_kernel(const T *__restrict__
     }
 }
 
+bool al16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
 template <typename T>
 int fold_t(const Conv3dGeom &q, const void *u, void *out, hipStream_t st) {
-    const int64_t HW = (int64_t)q.g.H * q.g.W;
+    const int HW = q.g.H * q.g.W;
     constexpr int V = 16 / sizeof(T);
-    const bool vec = q.C % V == 0 && (reinterpret_cast<uintptr_t>(u) & 15u) == 0 &&
-                     (reinterpret_cast<uintptr_t>(out) & 15u) == 0;
+    const bool vec = q.C % V == 0 && al16(u) && al16(out);
     const int64_t work = (int64_t)q.N * q.Do * HW * q.T * (vec ? q.C / V : q.C);
     if (work == 0) return 0;
     if (vec)
         hipLaunchKernelGGL((depth_fold_kernel<T, V>), dim3(blocks_for(work)), dim3(256), 0, st, (const T *)u, (T *)out,
-                           (int64_t)q.N, (int64_t)q.Din, (int64_t)q.Do, HW, (int64_t)q.C, (int64_t)q.T, (int64_t)q.sd,
-                           (int64_t)q.pd);
+                           q.N, q.Din, q.Do, HW, q.C, q.T, q.sd, q.pd);
     else
         hipLaunchKernelGGL((depth_fold_kernel<T, 1>), dim3(blocks_for(work)), dim3(256), 0, st, (const T *)u, (T *)out,
-                           (int64_t)q.N, (int64_t)q.Din, (int64_t)q.Do, HW, (int64_t)q.C, (int64_t)q.T, (int64_t)q.sd,
-                           (int64_t)q.pd);
+                           q.N, q.Din, q.Do, HW, q.C, q.T, q.sd, q.pd);
     return (int)hipGetLastError();
 }
 
 template <typename T>
 int unfold_t(const Conv3dGeom &q, const void *in, const void *bias, void *out, hipStream_t st) {
-    const int64_t HW = (int64_t)q.g.H * q.g.W;
-    const int64_t work = (int64_t)q.N * q.Din * HW * q.C;
+    const int HW = q.g.H * q.g.W;
+    constexpr int V = 16 / sizeof(T);
+    const bool vec = q.C % V == 0 && al16(in) && al16(out);
+    const int64_t work = (int64_t)q.N * q.Din * HW * (vec ? q.C / V : q.C);
     if (work == 0) return 0;
-    hipLaunchKernelGGL((depth_unfold_sum_kernel<T>), dim3(blocks_for(work)), dim3(256), 0, st, (const T *)in, (T *)out,
-                       (const T *)bias, (int64_t)q.N, (int64_t)q.Do, (int64_t)q.Din, HW, (int64_t)q.C, (int64_t)q.T,
-                       (int64_t)q.sd, (int64_t)q.pd);
+    if (vec)
+        hipLaunchKernelGGL((depth_unfold_sum_kernel<T, V>), dim3(blocks_for(work)), dim3(256), 0, st, (const T *)in,
+                           (T *)out, (const T *)bias, q.N, q.Do, q.Din, HW, q.C, q.T, q.sd, q.pd);
+    else
+        hipLaunchKernelGGL((depth_unfold_sum_kernel<T, 1>), dim3(blocks_for(work)), dim3(256), 0, st, (const T *)in,
+                           (T *)out, (const T *)bias, q.N, q.Do, q.Din, HW, q.C, q.T, q.sd, q.pd);
     return (int)hipGetLastError();
 }
 
