@@ -244,8 +244,9 @@ __global__ __launch_bounds__(256) void rowcol_reduce_kernel(
 }
 
 // out[c] = sum_y part[y][c], rounded once to T.  A block owns 16 columns;
-// its 16 thread rows split the partial rows (each keeps several loads in
-// flight) and meet in LDS in a fixed order.
+// its 16 thread rows split the partial rows and meet in LDS in a fixed
+// order.  The first 128 partial rows (all of them for the usual plans) are
+// loaded at once, so the pass costs one memory round trip.
 template <typename T>
 __global__ __launch_bounds__(256) void finalize_kernel(const float *__restrict__ part, int gy, int C,
                                                        T *__restrict__ out) {
@@ -254,13 +255,14 @@ __global__ __launch_bounds__(256) void finalize_kernel(const float *__restrict__
     const int c = blockIdx.x * 16 + cl;
     float s = 0.f;
     if (c < C) {
-        int y = yg;
-        for (; y + 48 < gy; y += 64) {
-            const float a0 = part[(int64_t)y * C + c], a1 = part[(int64_t)(y + 16) * C + c];
-            const float a2 = part[(int64_t)(y + 32) * C + c], a3 = part[(int64_t)(y + 48) * C + c];
-            s += (a0 + a1) + (a2 + a3);
+        float a[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int y = yg + 16 * k;
+            a[k] = y < gy ? part[(int64_t)y * C + c] : 0.f;
         }
-        for (; y < gy; y += 16) s += part[(int64_t)y * C + c];
+        s = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
+        for (int y = yg + 128; y < gy; y += 16) s += part[(int64_t)y * C + c];
     }
     red[yg][cl] = s;
     __syncthreads();
