@@ -913,6 +913,75 @@ __global__ __launch_bounds__(256) void pad_channels_kernel(const bf16 *__restric
     }
 }
 
+// Pair packing for narrow inputs with a stride-2 width (the 3-channel stem):
+// each 8-channel pixel u of the packed input holds the columns 2u - pw and
+// 2u + 1 - pw of up to 4 channels (zeros past C and outside the width), so the
+// stride-2 convolution over W becomes a stride-1 convolution over pixel pairs
+// with ceil(S / 2) taps and no width padding.
+//   xq[row][u][4t + c] = x[row][2u + t - pw][c]        (row = (n, h))
+//   wq[kr][j][4t + c]  = w[kr][2j + t][c]   (0 for 2j + t >= S)  (kr = (k, r))
+__global__ __launch_bounds__(256) void pack_pairs_kernel(const bf16 *__restrict__ x, int64_t rows, int W, int C,
+                                                         int Wq, int pw, bf16 *__restrict__ xq) {
+    const int64_t total = rows * Wq;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = i / Wq;
+        const int u = (int)(i - row * Wq);
+        Vec16<bf16> v;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int c = e & 3, w = 2 * u + (e >> 2) - pw;
+            v.e[e] = c < C && w >= 0 && w < W ? x[(row * W + w) * C + c] : (bf16)0.f;
+        }
+        store16(xq + i * 8, v);
+    }
+}
+
+__global__ __launch_bounds__(256) void pack_pair_filter_kernel(const bf16 *__restrict__ w, int64_t KR, int S, int C,
+                                                               int Sq, bf16 *__restrict__ wq) {
+    const int64_t total = KR * Sq;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t kr = i / Sq;
+        const int j = (int)(i - kr * Sq);
+        Vec16<bf16> v;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int c = e & 3, s = 2 * j + (e >> 2);
+            v.e[e] = c < C && s < S ? w[(kr * S + s) * C + c] : (bf16)0.f;
+        }
+        store16(wq + i * 8, v);
+    }
+}
+
+// the adjoints of the packings: dx[row][w][c] = dxq[row][(w + pw) / 2][4 ((w + pw) % 2) + c],
+// dw[kr][s][c] = dwq[kr][s / 2][4 (s % 2) + c]
+__global__ __launch_bounds__(256) void unpack_pairs_kernel(const bf16 *__restrict__ dxq, int64_t rows, int W, int C,
+                                                           int Wq, int pw, bf16 *__restrict__ dx) {
+    const int64_t total = rows * W * C;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t rw = i / C;
+        const int c = (int)(i - rw * C);
+        const int64_t row = rw / W;
+        const int w = (int)(rw - row * W) + pw;
+        dx[i] = dxq[(row * Wq + w / 2) * 8 + 4 * (w & 1) + c];
+    }
+}
+
+__global__ __launch_bounds__(256) void unpack_pair_filter_kernel(const bf16 *__restrict__ dwq, int64_t KR, int S,
+                                                                 int C, int Sq, bf16 *__restrict__ dw) {
+    const int64_t total = KR * S * C;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t ks = i / C;
+        const int c = (int)(i - ks * C);
+        const int64_t kr = ks / S;
+        const int s = (int)(ks - kr * S);
+        dw[i] = dwq[(kr * Sq + s / 2) * 8 + 4 * (s & 1) + c];
+    }
+}
+
 // dst[row][c] = src[row][c] for c < C (drops the padding channels).
 __global__ __launch_bounds__(256) void crop_channels_kernel(const bf16 *__restrict__ src, int64_t rows, int C8, int C,
                                                             bf16 *__restrict__ dst) {
@@ -1179,6 +1248,60 @@ int crop_channels(const void *src, int64_t rows, int C, void *dst, hipStream_t s
     return (int)hipGetLastError();
 }
 
+// Pair packing applies to inputs of at most 4 channels with a stride-2
+// width whose packed output width equals the original (true unless the
+// padded width is odd and S even).
+int pair_width(const ConvGeom &g) { return (g.W + 2 * g.pw + 1) / 2; }
+bool pair_applies(const ConvGeom &g) {
+    return g.C <= 4 && g.sw == 2 && pair_width(g) - (g.S + 1) / 2 + 1 == g.Q;
+}
+ConvGeom paired(const ConvGeom &g) {
+    ConvGeom q = g;
+    q.C = 8;
+    q.W = pair_width(g);
+    q.S = (g.S + 1) / 2;
+    q.sw = 1;
+    q.pw = 0;
+    return q;
+}
+
+int launch_grid(int64_t work) { return (int)std::max<int64_t>(1, std::min<int64_t>((work + 255) / 256, 8192)); }
+
+int pack_pairs(const ConvGeom &g, const void *x, void *xq, hipStream_t st) {
+    const int64_t rows = (int64_t)g.N * g.H, work = rows * pair_width(g);
+    if (work == 0) return 0;
+    hipLaunchKernelGGL(pack_pairs_kernel, dim3(launch_grid(work)), dim3(256), 0, st, (const bf16 *)x, rows, g.W, g.C,
+                       pair_width(g), g.pw, (bf16 *)xq);
+    return (int)hipGetLastError();
+}
+
+int pack_pair_filter(const ConvGeom &g, const void *w, void *wq, hipStream_t st) {
+    const int64_t KR = (int64_t)g.K * g.R, work = KR * ((g.S + 1) / 2);
+    if (work == 0) return 0;
+    hipLaunchKernelGGL(pack_pair_filter_kernel, dim3(launch_grid(work)), dim3(256), 0, st, (const bf16 *)w, KR, g.S,
+                       g.C, (g.S + 1) / 2, (bf16 *)wq);
+    return (int)hipGetLastError();
+}
+
+int unpack_pairs(const ConvGeom &g, const void *dxq, void *dx, hipStream_t st) {
+    const int64_t rows = (int64_t)g.N * g.H, work = rows * g.W * g.C;
+    if (work == 0) return 0;
+    hipLaunchKernelGGL(unpack_pairs_kernel, dim3(launch_grid(work)), dim3(256), 0, st, (const bf16 *)dxq, rows, g.W,
+                       g.C, pair_width(g), g.pw, (bf16 *)dx);
+    return (int)hipGetLastError();
+}
+
+int unpack_pair_filter(const ConvGeom &g, const void *dwq, void *dw, hipStream_t st) {
+    const int64_t KR = (int64_t)g.K * g.R, work = KR * g.S * g.C;
+    if (work == 0) return 0;
+    hipLaunchKernelGGL(unpack_pair_filter_kernel, dim3(launch_grid(work)), dim3(256), 0, st, (const bf16 *)dwq, KR,
+                       g.S, g.C, (g.S + 1) / 2, (bf16 *)dw);
+    return (int)hipGetLastError();
+}
+
+size_t pair_x_bytes(const ConvGeom &g) { return al256((size_t)g.N * g.H * pair_width(g) * 8 * 2); }
+size_t pair_w_bytes(const ConvGeom &g) { return al256((size_t)g.K * g.R * ((g.S + 1) / 2) * 8 * 2); }
+
 // The geometry with C padded to a multiple of 8.
 ConvGeom padded(const ConvGeom &g) {
     ConvGeom g8 = g;
@@ -1278,12 +1401,23 @@ size_t fwd_split_bytes(const ConvGeom &g) {
 // the padded contraction (split-K partials).
 size_t fwd_workspace(const ConvGeom &g) {
     if (g.C % 8 == 0) return fwd_split_bytes(g);
+    if (pair_applies(g)) return pair_x_bytes(g) + pair_w_bytes(g) + fwd_split_bytes(paired(g));
     const int C8 = pad8(g.C);
     return al256((size_t)g.N * g.H * g.W * C8 * 2) + al256((size_t)g.K * g.R * g.S * C8 * 2) +
            fwd_split_bytes(padded(g));
 }
 
 int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, void *y, void *ws, hipStream_t st) {
+    if (g.C % 8 != 0 && pair_applies(g)) {
+        if (!ws || !al16(ws) || !al16(y)) return -1;
+        char *xq = static_cast<char *>(ws);
+        char *wq = xq + pair_x_bytes(g);
+        char *ws2 = wq + pair_w_bytes(g);
+        int err = pack_pairs(g, x, xq, st);
+        if (!err) err = pack_pair_filter(g, w, wq, st);
+        if (err) return err;
+        return conv_fwd(paired(g), xq, wq, bias, y, ws2, st);
+    }
     if (g.C % 8 != 0) {
         if (!ws || !al16(ws) || !al16(y)) return -1;
         const ConvGeom g8 = padded(g);
@@ -1366,11 +1500,13 @@ size_t dgrad_core_workspace(const ConvGeom &g) {
 size_t dgrad_workspace(const ConvGeom &g) {
     if (g.K % 8 != 0) return 0;
     if (g.C % 8 != 0) {
+        // pair packing (without a bias) or channel padding, whichever is larger
+        const size_t pq = pair_applies(g) ? pair_w_bytes(g) + pair_x_bytes(g) + dgrad_core_workspace(paired(g)) : 0;
         // padded W, padded bias, padded dx, then the workspace of the padded
         // contraction
         const ConvGeom g8 = padded(g);
-        return al256((size_t)g.K * g.R * g.S * g8.C * 2) + al256((size_t)g8.C * 2) +
-               al256((size_t)g.N * g.H * g.W * g8.C * 2) + dgrad_core_workspace(g8);
+        return std::max(pq, al256((size_t)g.K * g.R * g.S * g8.C * 2) + al256((size_t)g8.C * 2) +
+                                al256((size_t)g.N * g.H * g.W * g8.C * 2) + dgrad_core_workspace(g8));
     }
     return dgrad_core_workspace(g);
 }
@@ -1380,6 +1516,17 @@ size_t dgrad_workspace(const ConvGeom &g) {
 int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bias, void *dx, void *ws,
                hipStream_t st) {
     if (g.K % 8 != 0) return -1;
+    if (g.C % 8 != 0 && pair_applies(g) && !bias) {
+        if (!ws || !al16(ws)) return -1;
+        char *wq = static_cast<char *>(ws);
+        char *dxq = wq + pair_w_bytes(g);
+        char *ws2 = dxq + pair_x_bytes(g);
+        int err = pack_pair_filter(g, w, wq, st);
+        if (err) return err;
+        err = conv_dgrad(paired(g), dy, wq, nullptr, dxq, ws2, st);
+        if (err) return err;   // -1: not applicable (the caller falls back), else a HIP error
+        return unpack_pairs(g, dxq, dx, st);
+    }
     if (g.C % 8 != 0) {
         if (!ws || !al16(ws)) return -1;
         const ConvGeom g8 = padded(g);
@@ -1435,6 +1582,8 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bia
 bool wgrad_applies(const ConvGeom &g) { return g.K % 8 == 0; }
 
 size_t wgrad_workspace(const ConvGeom &g, bool with_db) {
+    if (g.C % 8 != 0 && pair_applies(g))
+        return pair_x_bytes(g) + pair_w_bytes(g) + wgrad_workspace(paired(g), with_db);
     if (g.C % 8 != 0) {
         // padded x, padded dW, then the workspace of the padded contraction
         const ConvGeom g8 = padded(g);
@@ -1450,6 +1599,17 @@ size_t wgrad_workspace(const ConvGeom &g, bool with_db) {
 
 int conv_wgrad(const ConvGeom &g, const void *dy, const void *x, void *dw, void *db, void *ws, hipStream_t st) {
     if (!wgrad_applies(g)) return -1;
+    if (g.C % 8 != 0 && pair_applies(g)) {
+        if (!ws || !al16(ws) || !al16(dy)) return -1;
+        char *xq = static_cast<char *>(ws);
+        char *dwq = xq + pair_x_bytes(g);
+        char *ws2 = dwq + pair_w_bytes(g);
+        int err = pack_pairs(g, x, xq, st);
+        if (err) return err;
+        err = conv_wgrad(paired(g), dy, xq, dwq, db, ws2, st);
+        if (err) return err;   // -1: not applicable (the caller falls back), else a HIP error
+        return unpack_pair_filter(g, dwq, dw, st);
+    }
     if (g.C % 8 != 0) {
         if (!ws || !al16(ws) || !al16(dy)) return -1;
         const ConvGeom g8 = padded(g);

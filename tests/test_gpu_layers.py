@@ -276,3 +276,35 @@ def test_kernel_timing_counts_launches():
     assert tf > 0 and td > 0 and tw == 0
     y, rec = ms.layer_forward(ms.Conv2d((1, 1), (1, 1)), X, Wt, B, 0)
     assert ms.profile_read(ms.PROF_FWD) == (0, 0.0)
+
+
+NARROW_CASES = [
+    # x shape, w shape, stride, pad: at most 4 channels with a stride-2 width run
+    # as a stride-1 convolution over packed column pairs (the stem's path)
+    ((2, 3, 30, 29), (16, 3, 7, 7), (2, 2), (3, 3)),     # padded width odd, S odd
+    ((2, 3, 28, 28), (24, 3, 7, 7), (2, 2), (3, 3)),     # padded width even, S odd
+    ((1, 4, 17, 30), (8, 4, 3, 4), (1, 2), (1, 1)),      # width even, S even
+    ((2, 1, 9, 21), (16, 1, 5, 5), (2, 2), (0, 2)),      # one channel
+    ((1, 2, 12, 13), (8, 2, 3, 3), (2, 2), (1, 1)),
+    ((1, 3, 10, 11), (8, 3, 3, 4), (2, 2), (1, 1)),      # padded width odd, S even: channel padding instead
+]
+
+
+@pytest.mark.parametrize("case", range(len(NARROW_CASES)))
+@pytest.mark.parametrize("mask", [0, 7, 1, 2])
+def test_narrow_inputs_with_stride_two_width(case, mask):
+    xs, ws, stride, pad = NARROW_CASES[case]
+    seed = 9970 + 10 * case
+    x, w, b = _conv_inputs(seed, xs, ws, "bf16")
+    y, rec = ms.layer_forward(ms.Conv2d(stride, pad), dev(x, "bf16"), dev(w, "bf16"), dev(b, "bf16"), mask)
+    check("y", host(y), oracle.conv2d_forward(x, w, b, stride, pad), "bf16")
+    if rec is None:
+        return
+    gy = synth.normal(tuple(y.shape), seed + 3, dtype="bf16")
+    gx, gw, gb = ms.layer_backward(rec, dev(gy, "bf16"))
+    if gx is not None:
+        check("dx", host(gx), oracle.conv2d_input_grad(gy, w, xs, stride, pad), "bf16")
+    if gw is not None:
+        check("dW", host(gw), oracle.conv2d_weight_grad(gy, x, ws, stride, pad), "bf16")
+    if gb is not None:
+        check("db", host(gb), oracle.conv2d_bias_grad(gy), "bf16")
