@@ -1059,6 +1059,7 @@ constexpr Tile kTiles[] = {
     {"128x128w8s4", 128, 128, 2, 4, 4, 1, 0.90f, 0.90f},  // 8 waves of 64 x 32, 4 stages (128 KB)
     {"128x128k2", 128, 128, 2, 2, 4, 1, 0.95f, 0.95f, 2},  // 2 k-groups of 4 waves of 64 x 64, 4 stages
     {"128x64", 128, 64, 2, 2, 2, 3, 0.75f, 0.75f},        // 4 waves of 64 x 32, 48 KB, three blocks per CU
+    {"256x32", 256, 32, 4, 1, 2, 2, 0.70f, 0.70f},        // 4 waves of 64 x 32, 72 KB, two blocks per CU
 };
 constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 // tiles the planner chooses from
@@ -1067,7 +1068,14 @@ constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 // (weight gradient 4096 x 1024 x 4096: 57 -> 46 us), and the k-group tile
 // beats that one by ~5% on the forward and input gradient of 4096 x 1024
 // outputs with K = 4096 (38.7 -> 36.3 us)
-constexpr bool kAuto[kNumTiles] = {true, true, true, true, false, true, true, true};
+constexpr bool kAuto[kNumTiles] = {true, true, true, true, false, true, true, true, false};
+// the narrow 256 x 32 tile is for thin outputs (N <= 32, e.g. the input
+// gradient of a 3-channel image) and exists only for the contractions whose
+// operands are both k-contiguous (forward, input gradient through the
+// transposed filter): the transposing reads' swizzle assumes rows of at
+// least 8 slots
+constexpr bool narrow_tile(const Tile &t) { return t.bn < 64; }
+constexpr bool kAutoKc[kNumTiles] = {true, true, true, true, false, true, true, true, true};
 // tiles the planner chooses from for the input gradient of convolutions
 // that are not 1x1 / stride 1 (implicit-GEMM gathers): on the
 // ResNet-18-shaped stack's layers and the conv sweep the 2-stage 128 x 128
@@ -1079,7 +1087,7 @@ constexpr bool kAuto[kNumTiles] = {true, true, true, true, false, true, true, tr
 // 0.121 -> 0.116 ms.  The forward keeps the general set: restricted the same
 // way it took split reductions whose extra pass made the frozen stack 6%
 // slower.
-constexpr bool kAutoConv[kNumTiles] = {true, false, true, false, false, false, false, true};
+constexpr bool kAutoConv[kNumTiles] = {true, false, true, false, false, false, false, true, true};
 
 // MEMSAVE_GEMM_TILE=<name> forces one tile shape (a debugging and testing
 // knob); returns its index or -1.
@@ -1148,7 +1156,8 @@ enum KgUse { kKgNever = 0, kKgForced = 1, kKgAuto = 2 };
 GemmPlan plan_gemm(long M, long N, long K, int z, int split_cap = 16, bool allow_256x256 = true,
                    int kgroups = kKgAuto, const bool *auto_set = kAuto) {
     int forced = forced_tile();
-    if (forced >= 0 && kTiles[forced].kg > 1 && kgroups == kKgNever) forced = -1;   // not built: plan as usual
+    // not built for the weight gradient: plan as usual
+    if (forced >= 0 && (kTiles[forced].kg > 1 || narrow_tile(kTiles[forced])) && kgroups == kKgNever) forced = -1;
     if (forced == 0 && !allow_256x256) forced = 1;   // the next widest tile (256 x 128)
     const int fs = split_cap > 1 ? forced_splits() : 0;
     const int max_splits = (int)std::max<long>(1, std::min<long>(split_cap, K / (4 * BK)));
@@ -1205,6 +1214,10 @@ int go_tile(const Tile &t, const Args &a, dim3 grid, hipStream_t st) {
         if constexpr (MODE != kWgrad) {
             if (t.bm == 128 && t.bn == 128) return go<MODE, 128, 128, 2, 2, 4, 1, UNIT, 2>(a, grid, st);
         }
+        return (int)hipErrorInvalidValue;
+    }
+    if (t.bn == 32) {
+        if constexpr (MODE == kFwd || MODE == kDgrad) return go<MODE, 256, 32, 4, 1, 2, 2, UNIT>(a, grid, st);
         return (int)hipErrorInvalidValue;
     }
     if (t.bm == 128 && t.bn == 128 && t.wc == 4 && t.stages == 4) return go<MODE, 128, 128, 2, 4, 4, 1, UNIT>(a, grid, st);
@@ -1325,11 +1338,12 @@ Tile pick_conv_wgrad(long M, long N, long K, int splits_allowed, int *splits_out
     Tile bt = kTiles[0];
     int bs = 1;
     int forced = forced_tile();
-    if (forced >= 0 && kTiles[forced].kg > 1) forced = -1;   // no k-group weight gradient: plan as usual
+    // no k-group or narrow weight gradient: plan as usual
+    if (forced >= 0 && (kTiles[forced].kg > 1 || narrow_tile(kTiles[forced]))) forced = -1;
     for (int ti = 0; ti < kNumTiles; ++ti) {
         if (forced >= 0 ? ti != forced : !kAuto[ti]) continue;
         const Tile &t = kTiles[ti];
-        if (t.kg > 1) continue;   // no k-group tile for the weight gradient
+        if (t.kg > 1 || narrow_tile(t)) continue;   // neither is built for the weight gradient
         const long tiles = ((M + t.bm - 1) / t.bm) * ((N + t.bn - 1) / t.bn) * z;
         int splits = 1;
         if (splits_allowed > 1) {
@@ -1388,7 +1402,7 @@ int reduce_partials(const float *part, int splits, int64_t n, int64_t pstride, b
 }
 
 GemmPlan fwd_plan(const ConvGeom &g) {
-    return plan_gemm((long)g.N * g.P * g.Q, g.K, (long)g.R * g.S * g.C, 1);
+    return plan_gemm((long)g.N * g.P * g.Q, g.K, (long)g.R * g.S * g.C, 1, 16, true, kKgAuto, kAutoKc);
 }
 
 size_t fwd_split_bytes(const ConvGeom &g) {
@@ -1475,16 +1489,20 @@ DgradChoice dgrad_choice(const ConvGeom &g) {
     const int z = g.sh * g.sw;
     const bool unit = unit_geom(g);
     const int kg = unit ? kKgAuto : kKgForced;
-    const bool *set = unit ? kAuto : kAutoConv;
+    const bool *set = unit ? kAutoKc : kAutoConv;
     const char *e = getenv("MEMSAVE_DGRAD");
-    if (e && *e) {
+    const int forced = forced_tile();
+    // the narrow tile reads W through the transposed copy only
+    const bool narrow_forced = forced >= 0 && narrow_tile(kTiles[forced]);
+    if (e && *e && !narrow_forced) {
         const bool direct = e[0] == 'd';
-        return {direct, plan_gemm(M, g.C, Kb, z, direct ? 1 : 16, direct || unit, kg, set)};
+        return {direct, plan_gemm(M, g.C, Kb, z, direct ? 1 : 16, direct || unit, kg, direct ? kAuto : set)};
     }
     const GemmPlan pt = plan_gemm(M, g.C, Kb, z, 16, unit, kg, set);
     if (!unit) return {false, pt};
+    if (narrow_tile(pt.t)) return {false, pt};
     const GemmPlan pd = plan_gemm(M, g.C, Kb, z, 1, true, kg);
-    if (pd.t.wr * pd.t.wc * pd.t.kg == 8 && pt.splits == 1) return {true, pd};
+    if (pd.t.wr * pd.t.wc * pd.t.kg == 8 && pt.splits == 1 && !narrow_tile(pd.t)) return {true, pd};
     return {false, pt};
 }
 
