@@ -16,6 +16,7 @@
 // Nothing in this file touches the device except through the
 // launchers of device.h, and every check runs before the first launch.
 #include <algorithm>
+#include <initializer_list>
 #include <atomic>
 #include <cmath>
 #include <cstdarg>
@@ -61,6 +62,10 @@ void ledger_sub(uint64_t n) { g_live.fetch_sub(n); }
 constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
 constexpr uint32_t kMagic = 0x4d53524bu;  // "MSRK"
 
+// Product of non-negative extents, saturated just above kMaxElems (the
+// limit checks below must not be fooled by an int64 overflow).
+int64_t capped_product(std::initializer_list<int64_t> f);
+
 int64_t numel(const ms_tensor *t) {
     int64_t n = 1;
     for (int i = 0; i < t->ndim; ++i) n *= t->shape[i];
@@ -68,6 +73,16 @@ int64_t numel(const ms_tensor *t) {
 }
 
 size_t elt_size(int32_t dt) { return dt == MS_BF16 ? 2 : 4; }
+
+int64_t capped_product(std::initializer_list<int64_t> f) {
+    int64_t p = 1;
+    for (int64_t v : f) {
+        if (v == 0) return 0;
+        if (p > (kMaxElems + 1) / v) p = kMaxElems + 1;
+        else p = std::min<int64_t>(p * v, kMaxElems + 1);
+    }
+    return p;
+}
 
 bool dtype_ok(int32_t dt) { return dt == MS_F32 || dt == MS_BF16; }
 
@@ -205,7 +220,7 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
         pl->dtype = x->dtype;
         pl->g = ms::ConvGeom{(int)N, (int)C, (int)H, (int)Wd, (int)K, (int)R, (int)S, (int)P, (int)Q,
                              layer->stride[0], layer->stride[1], layer->pad[0], layer->pad[1]};
-        if (N * P * Q * K > kMaxElems) return fail(MS_E_UNSUPPORTED, "output has more than 2^31-1 elements");
+        if (capped_product({N, P, Q, K}) > kMaxElems) return fail(MS_E_UNSUPPORTED, "output has more than 2^31-1 elements");
         pl->rows = N * P * Q;
         pl->x_bytes = (uint64_t)numel(x) * elt_size(x->dtype);
         pl->w_bytes = (uint64_t)numel(W) * elt_size(W->dtype);
@@ -248,7 +263,8 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
                             (long long)Ho, (long long)Wo);
             if (!is_nhwc(y)) return fail(MS_E_LAYOUT, "y must be channels-last (NHWC)");
         }
-        if (N * Ho * Wo * Co > kMaxElems) return fail(MS_E_UNSUPPORTED, "output has more than 2^31-1 elements");
+        if (capped_product({N, Ho, Wo, Co}) > kMaxElems)
+            return fail(MS_E_UNSUPPORTED, "output has more than 2^31-1 elements");
         pl->dtype = x->dtype;
         // the convolution y -> x with filter W: input [N,C_out,H_out,W_out], K = C_in filters,
         // output [N,C_in,H,W]; out_pad < stride makes its output extent exactly H x W
@@ -314,11 +330,12 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
                             (long long)o[0], (long long)o[1], (long long)o[2]);
             if (!is_ndhwc(y)) return fail(MS_E_LAYOUT, "y must be channels-last (NDHWC)");
         }
-        if (N * o[0] * o[1] * o[2] * Cy > kMaxElems) return fail(MS_E_UNSUPPORTED, "output has more than 2^31-1 elements");
+        if (capped_product({N, o[0], o[1], o[2], Cy}) > kMaxElems)
+            return fail(MS_E_UNSUPPORTED, "output has more than 2^31-1 elements");
         // the 3-D convolution u -> v this layer runs (itself, or the one it is the adjoint of)
         const int64_t Cu = tr ? Cy : Cx, Cv = tr ? Cx : Cy;
         const int64_t *du = tr ? o : in, *dv = tr ? in : o;
-        const int64_t folded = N * dv[0] * du[1] * du[2] * T * Cu;   // [N*Dv][Hu][Wu][T*Cu]
+        const int64_t folded = capped_product({N, dv[0], du[1], du[2], T, Cu});   // [N*Dv][Hu][Wu][T*Cu]
         if (folded > kMaxElems || T * Cu > kMaxElems || N * dv[0] > kMaxElems)
             return fail(MS_E_UNSUPPORTED, "depth-folded input has more than 2^31-1 elements");
         pl->dtype = x->dtype;

@@ -806,3 +806,23 @@ def test_conv3d_validation(stub):
     t = Conv3dArgs((2, 16, 3, 4, 4), 8, (2, 4, 4), (2, 2, 2), (0, 1, 1), (1, 0, 1))
     t.layer.out_pad_d = 2                                           # out_pad >= stride
     assert fwd(t) == L.MS_E_ARG
+
+
+def test_output_size_limits_hold_for_extreme_padding(stub):
+    """Pads near 2^30 make output extents near 2^31: the element-count
+    checks must reject them (a plain int64 product of the extents would
+    overflow) for the accounting call, which takes no y."""
+    big = 1 << 30
+    layer = L.MsLayer()
+    layer.kind = L.MS_CONV2D
+    layer.stride[0] = layer.stride[1] = 1
+    layer.pad[0] = layer.pad[1] = big - 1
+    x, w = tdesc((1, 1, 1, 1), data=False), tdesc((3, 1, 1, 1), data=False)
+    a = L.MsAccount()
+    assert stub.ms_policy_account(ctypes.byref(layer), ref(x), ref(w), None, 1, 0, ctypes.byref(a)) == L.MS_E_UNSUPPORTED
+    l3 = L.MsLayer()
+    l3.kind = L.MS_CONV3D
+    l3.stride_d = l3.stride[0] = l3.stride[1] = 1
+    l3.pad_d = l3.pad[0] = l3.pad[1] = big - 1
+    x3, w3 = tdesc((1, 1, 1, 1, 1), data=False), tdesc((2, 1, 1, 1, 1), data=False)
+    assert stub.ms_policy_account(ctypes.byref(l3), ref(x3), ref(w3), None, 1, 0, ctypes.byref(a)) == L.MS_E_UNSUPPORTED
