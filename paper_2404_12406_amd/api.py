@@ -432,6 +432,9 @@ class PreparedLayer:
 
     forward() enqueues ms_layer_forward on the current stream and keeps the
     raw record; backward() enqueues ms_layer_backward for it and frees it.
+    A Dropout spec's seed and offset are part of the prepared call, so every
+    forward draws the same mask (prepare a new call, or use layer_forward,
+    to draw another).
     The object holds references to every tensor it describes, so nothing it
     points to can be freed while it exists."""
 
