@@ -226,7 +226,12 @@ def headline(steps, warmup):
                      "traffic": recorded_traffic(dom["key"]),
                      "kernel": f"ms::g2::gemm_kernel ({dom['name']} GEMM of the Linear layers)",
                      "flop_per_launch": dom["flop"] // dom["launches"], "avg_launch_us": round(avg_ms * 1e3, 2),
-                     "launches": dom["launches"], "pass_ms_per_step": round(ms_step_profiled, 4)},
+                     "launches": dom["launches"], "pass_ms_per_step": round(ms_step_profiled, 4),
+                     # the input-gradient launches also take the layer's bias
+                     # gradient along: each block adds its share of dy's
+                     # columns (dy read a second time) after the contraction
+                     "fused": ("bias-gradient column sums of dy (8 or 32 MiB re-read per launch, no FLOP counted)"
+                               if dom["key"] == "dgrad" else None)},
         "saved": {"selective": sel, "all_true": allb},
     }
 

@@ -30,10 +30,15 @@ int launch_conv_fwd(int dtype, const ConvGeom &g, const void *x, const void *w,
 // dx = input gradient of the convolution for grad dy (needs w only), plus
 // bias[c] per channel when bias is non-null (the forward of a transposed
 // convolution is this contraction).  May use conv_dgrad_workspace() bytes of
-// workspace (a transposed copy of w, zero-padded channel copies).
-size_t conv_dgrad_workspace(int dtype, const ConvGeom &g);
+// workspace (a transposed copy of w, zero-padded channel copies).  When db
+// is non-null the launcher may also produce the bias gradient db[k] = sum
+// over pixels of dy[.][k] (bf16 unit geometry: the contraction's blocks add
+// dy's columns as they finish) and sets *db_done; with_db sizes the
+// workspace for that.
+size_t conv_dgrad_workspace(int dtype, const ConvGeom &g, bool with_db = false);
 int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *w,
-                      const void *bias, void *dx, void *ws, void *stream);
+                      const void *bias, void *dx, void *ws, void *stream, void *db = nullptr,
+                      bool *db_done = nullptr);
 
 // dw = weight gradient for grad dy and input x.  Needs conv_wgrad_workspace()
 // bytes of device workspace (may be 0).  When db is non-null the launcher may
@@ -69,6 +74,9 @@ int launch_conv3d_wgrad(int dtype, const Conv3dGeom &q, const void *dv, const vo
 // out[j] = sum_i in[i][j] for a dense row-major [rows][cols] matrix (bias
 // gradient of conv over N*P*Q rows, of linear over M rows).
 size_t colsum_workspace(int dtype, int64_t rows, int cols);
+// out[j] = sum_i part[i][j] over `rows` fp32 partial rows (fixed order),
+// rounded once to dtype.
+int launch_colsum_finalize(int dtype, const float *part, int rows, int cols, void *out, void *stream);
 int launch_colsum(int dtype, const void *in, int64_t rows, int cols, void *out,
                   void *ws, void *stream);
 

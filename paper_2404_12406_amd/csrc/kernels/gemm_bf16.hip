@@ -57,6 +57,9 @@ struct Args {
     bf16 *c;              // output (or nullptr when the output is fp32 partials)
     float *part;          // split-K partials: part_stride floats per split (nullptr: splits == 1)
     float *dbpart;        // WGRAD fused bias-gradient partials [splits][M] (nullptr: off)
+    float *cspart;        // unit-geometry DGRAD: column sums of dy (the bias gradient),
+                          // one partial row per (row tile, summing wave) (nullptr: off)
+    int cs_cw;            // columns of dy per block column (a multiple of 8)
     int64_t part_stride;  // FWD/WGRAD: M*N; DGRAD: N*H*W*C (partials indexed by dx pixel)
     const bf16 *bias;     // FWD / DGRAD per-column bias (nullptr: none; DGRAD: the
                           // transposed convolution's forward)
@@ -188,6 +191,81 @@ __device__ __forceinline__ bf16x8 frag_kc(const char *base, int row, int sub, in
     const int off = row * (BK * 2) + ((chunk ^ swz_k(row)) << 4);
     return *reinterpret_cast<const bf16x8 *>(base + off);
 }
+
+// Column sums of dy for the bias gradient, taken by a unit-geometry input
+// gradient (there A = dy: row m holds the K output channels of pixel m).
+// Block (tm, tn) adds rows m0 .. m0+BM-1 for columns [tn*cw, tn*cw + cw) of
+// K; nwc waves take part, wave w writing partial row tm*nwc + w of part
+// ([rows][K] fp32).  Lane t = 64w + l of the nwc*64 owns column vector
+// t % cvp (8 channels) of each pass of 8*cvp columns and walks the rows
+// t / cvp + i * rgs (rgs = nwc*64 / cvp), NB loads in flight; the lanes of a
+// wave that share a column vector meet by shuffles.  Loads go through the
+// buffer descriptor of dy with out-of-range rows and columns sent past its
+// end, so they read zeros.  The data was read by this block's main loop
+// moments earlier.  issue() may be called first (the first batch of the
+// first pass, e.g. before an epilogue); run() then starts from it.
+template <int NB>
+struct DyColumnSums {
+    __amdgpu_buffer_rsrc_t ra;
+    int M, K, m0, BM, kb, ncv, cvp, cvl, rg, rgs;
+    bool on;
+    u32x4 v[NB];
+
+    __device__ __forceinline__ DyColumnSums(__amdgpu_buffer_rsrc_t ra_, int M_, int K_, int m0_, int BM_, int tn,
+                                            int cw, int w, int nwc, int lane)
+        : ra(ra_), M(M_), K(K_), m0(m0_), BM(BM_) {
+        kb = tn * cw;
+        on = kb < K;   // uniform over the block
+        ncv = on ? (min(cw, K - kb) + 7) / 8 : 0;
+        cvp = 1;
+        while (cvp < ncv && cvp < 64) cvp <<= 1;
+        const int t = w * 64 + lane;
+        cvl = t % cvp;
+        rg = t / cvp;
+        rgs = nwc * 64 / cvp;
+    }
+    __device__ __forceinline__ void issue(int c0, int r0) {
+        const int k = kb + (c0 + cvl) * 8;
+        const bool kin = c0 + cvl < ncv && k < K;
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int r = r0 + i * rgs, m = m0 + r;
+            const bool ok = kin && r < BM && m < M;
+            const uint32_t off = ok ? ((uint32_t)m * (uint32_t)K + (uint32_t)k) * 2u : kOOB;
+            v[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, (int)off, 0, 0);
+        }
+    }
+    __device__ __forceinline__ void add(float (&acc)[8]) const {
+#pragma unroll
+        for (int i = 0; i < NB; ++i)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                acc[2 * q] += __uint_as_float(v[i][q] << 16);
+                acc[2 * q + 1] += __uint_as_float(v[i][q] & 0xffff0000u);
+            }
+    }
+    __device__ __forceinline__ void run(bool issued, int w, int nwc, int tm, int lane, float *__restrict__ part) {
+        if (!on) return;
+        for (int c0 = 0; c0 < ncv; c0 += cvp) {
+            float acc[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+            for (int r0 = rg; r0 < BM; r0 += NB * rgs) {
+                if (!(issued && c0 == 0 && r0 == rg)) issue(c0, r0);
+                add(acc);
+            }
+            for (int sh = cvp; sh < 64; sh <<= 1)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], sh);
+            const int k = kb + (c0 + cvl) * 8;
+            if (lane < cvp && c0 + cvl < ncv && k < K) {
+                float *dst = part + (size_t)(tm * nwc + w) * K + k;
+                *reinterpret_cast<floatx4 *>(dst) = floatx4{acc[0], acc[1], acc[2], acc[3]};
+                *reinterpret_cast<floatx4 *>(dst + 4) = floatx4{acc[4], acc[5], acc[6], acc[7]};
+            }
+        }
+    }
+};
 
 // KG k-groups of WR x WC waves: group g computes the whole block tile from
 // the 16-k slices 2g and 2g+1 of every BK step (KG = 2), and the groups add
@@ -708,7 +786,16 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
                     for (int v = 0; v < 16; ++v) acc[i][j][v] += red[(((wl * TM + i) * TN + j) * 16 + v) * 64 + lane];
         }
         __syncthreads();   // the partials are read before the epilogue reuses LDS
-        if (kg == 1) return;
+        if (kg == 1) {
+            // group 1 sums dy's columns while group 0 writes the output tile
+            if constexpr (DG && UNIT) {
+                if (P.cspart) {
+                    DyColumnSums<16> cs(ra, M, Kg, m0, BM, tn, P.cs_cw, wl, WR * WC, lane);
+                    cs.run(false, wl, WR * WC, tm, lane, P.cspart);
+                }
+            }
+            return;
+        }
     }
 
     // ------------------------------------------------ fused bias-gradient partials
@@ -758,6 +845,12 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
                 }
         }
         return;
+    }
+    // KG == 1: the column sums' first loads are issued here, so they land
+    // while the output tile is written
+    DyColumnSums<8> cs(ra, M, Kg, m0, BM, tn, P.cs_cw, wave, G::NW, lane);
+    if constexpr (DG && UNIT && KG == 1) {
+        if (P.cspart && cs.on) cs.issue(0, cs.rg);
     }
     if constexpr (KG == 1) __syncthreads();   // every wave is done with the operand stages
     bf16 *stage = reinterpret_cast<bf16 *>(smem) + wave * G::EPI_ROWS * G::EPI_PITCH;
@@ -844,6 +937,9 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
         }
         wait_lgkm0();   // reads done before the next pass overwrites
         __builtin_amdgcn_wave_barrier();
+    }
+    if constexpr (DG && UNIT && KG == 1) {
+        if (P.cspart) cs.run(true, wave, G::NW, tm, lane, P.cspart);
     }
 }
 
@@ -1506,33 +1602,47 @@ DgradChoice dgrad_choice(const ConvGeom &g) {
     return {false, pt};
 }
 
-// transposed filter (when used), then split-K partials indexed by dx pixel
-size_t dgrad_core_workspace(const ConvGeom &g) {
+// The bias gradient rides on a unit-geometry input gradient that does not
+// split its reduction: every block also adds its share of dy's columns
+// (dy_column_sums), leaving one partial row per (row tile, summing wave).
+bool colsum_rides(const ConvGeom &g, const GemmPlan &p) { return unit_geom(g) && p.splits == 1; }
+int colsum_waves(const Tile &t) { return t.wr * t.wc; }   // k-groups: the second group's waves
+int64_t colsum_rows(const ConvGeom &g, const Tile &t) {
+    return (((int64_t)g.N * g.H * g.W + t.bm - 1) / t.bm) * colsum_waves(t);
+}
+
+// transposed filter (when used), then split-K partials indexed by dx pixel,
+// then (with_db, when the column sums ride along) their partial rows
+size_t dgrad_core_workspace(const ConvGeom &g, bool with_db) {
     const DgradChoice dc = dgrad_choice(g);
     const GemmPlan &p = dc.p;
     size_t ws = dc.direct ? 0 : al256((size_t)g.K * g.R * g.S * g.C * sizeof(bf16));
     if (p.splits > 1) ws += al256((size_t)p.splits * part_stride((int64_t)g.N * g.H * g.W * g.C) * sizeof(float));
+    if (with_db && colsum_rides(g, p)) ws += al256((size_t)colsum_rows(g, p.t) * g.K * sizeof(float));
     return ws;
 }
 
-size_t dgrad_workspace(const ConvGeom &g) {
+size_t dgrad_workspace(const ConvGeom &g, bool with_db) {
     if (g.K % 8 != 0) return 0;
     if (g.C % 8 != 0) {
         // pair packing (without a bias) or channel padding, whichever is larger
-        const size_t pq = pair_applies(g) ? pair_w_bytes(g) + pair_x_bytes(g) + dgrad_core_workspace(paired(g)) : 0;
+        const size_t pq = pair_applies(g) ? pair_w_bytes(g) + pair_x_bytes(g) + dgrad_core_workspace(paired(g), false) : 0;
         // padded W, padded bias, padded dx, then the workspace of the padded
         // contraction
         const ConvGeom g8 = padded(g);
         return std::max(pq, al256((size_t)g.K * g.R * g.S * g8.C * 2) + al256((size_t)g8.C * 2) +
-                                al256((size_t)g.N * g.H * g.W * g8.C * 2) + dgrad_core_workspace(g8));
+                                al256((size_t)g.N * g.H * g.W * g8.C * 2) + dgrad_core_workspace(g8, false));
     }
-    return dgrad_core_workspace(g);
+    return dgrad_core_workspace(g, with_db);
 }
 
 // dx = input gradient (+ bias[c] per channel when bias is non-null: the
-// forward of a transposed convolution runs this contraction).
+// forward of a transposed convolution runs this contraction).  With db
+// non-null the contraction may also produce db[k] = sum of dy's column k
+// (the layer's bias gradient); *db_done says whether it did.
 int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bias, void *dx, void *ws,
-               hipStream_t st) {
+               hipStream_t st, void *db, bool *db_done) {
+    if (db_done) *db_done = false;
     if (g.K % 8 != 0) return -1;
     if (g.C % 8 != 0 && pair_applies(g) && !bias) {
         if (!ws || !al16(ws)) return -1;
@@ -1541,7 +1651,7 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bia
         char *ws2 = dxq + pair_x_bytes(g);
         int err = pack_pair_filter(g, w, wq, st);
         if (err) return err;
-        err = conv_dgrad(paired(g), dy, wq, nullptr, dxq, ws2, st);
+        err = conv_dgrad(paired(g), dy, wq, nullptr, dxq, ws2, st, nullptr, nullptr);
         if (err) return err;   // -1: not applicable (the caller falls back), else a HIP error
         return unpack_pairs(g, dxq, dx, st);
     }
@@ -1555,7 +1665,7 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bia
         int err = pad_channels(w, (int64_t)g.K * g.R * g.S, g.C, wp, st);
         if (!err && bias) err = pad_channels(bias, 1, g.C, bp, st);
         if (err) return err;
-        err = conv_dgrad(g8, dy, wp, bias ? bp : nullptr, dxp, ws2, st);
+        err = conv_dgrad(g8, dy, wp, bias ? bp : nullptr, dxp, ws2, st, nullptr, nullptr);
         if (err) return err;   // -1: not applicable (the caller falls back), else a HIP error
         return crop_channels(dxp, (int64_t)g.N * g.H * g.W, g.C, dx, st);
     }
@@ -1591,9 +1701,21 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bia
         a.part_stride = part_stride(n);
         a.c = nullptr;
     }
+    const bool cs = db && !bias && colsum_rides(g, p);
+    if (cs) {
+        a.cspart = reinterpret_cast<float *>(wsc + (direct ? 0 : al256((size_t)g.K * g.R * g.S * g.C * sizeof(bf16))));
+        a.cs_cw = (g.K + a.ntn - 1) / a.ntn;
+        a.cs_cw = (a.cs_cw + 7) / 8 * 8;
+    }
     const dim3 grid(a.ntm * a.ntn, 1, g.sh * g.sw * p.splits);
     int err = direct ? go_mode<kDgradN>(p.t, a, grid, unit_geom(g), st) : go_mode<kDgrad>(p.t, a, grid, unit_geom(g), st);
-    if (err || p.splits <= 1) return err;
+    if (err) return err;
+    if (cs) {
+        err = launch_colsum_finalize(kBF16, a.cspart, (int)colsum_rows(g, p.t), g.K, db, st);
+        if (!err && db_done) *db_done = true;
+        return err;
+    }
+    if (p.splits <= 1) return err;
     return reduce_partials(part, p.splits, n, a.part_stride, (bf16 *)dx, (const bf16 *)bias, g.C, st);
 }
 

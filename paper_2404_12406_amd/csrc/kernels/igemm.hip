@@ -35,9 +35,9 @@ namespace ms {
 namespace g2 {
 size_t fwd_workspace(const ConvGeom &g);
 int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, void *y, void *ws, hipStream_t st);
-size_t dgrad_workspace(const ConvGeom &g);
+size_t dgrad_workspace(const ConvGeom &g, bool with_db);
 int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bias, void *dx, void *ws,
-               hipStream_t st);
+               hipStream_t st, void *db, bool *db_done);
 bool wgrad_applies(const ConvGeom &g);
 size_t wgrad_workspace(const ConvGeom &g, bool with_db);
 int conv_wgrad(const ConvGeom &g, const void *dy, const void *x, void *dw, void *db, void *ws, hipStream_t st);
@@ -657,14 +657,15 @@ int launch_conv_fwd(int dtype, const ConvGeom &g, const void *x, const void *w, 
     return launch_dtype<kFwd>(dtype, prm, grid, vec_ok, is_unit(g), (hipStream_t)stream);
 }
 
-size_t conv_dgrad_workspace(int dtype, const ConvGeom &g) {
-    return dtype == kBF16 ? g2::dgrad_workspace(g) : 0;
+size_t conv_dgrad_workspace(int dtype, const ConvGeom &g, bool with_db) {
+    return dtype == kBF16 ? g2::dgrad_workspace(g, with_db) : 0;
 }
 
 int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *w, const void *bias,
-                      void *dx, void *ws, void *stream) {
+                      void *dx, void *ws, void *stream, void *db, bool *db_done) {
+    if (db_done) *db_done = false;
     if (dtype == kBF16) {
-        const int r = g2::conv_dgrad(g, dy, w, bias, dx, ws, (hipStream_t)stream);
+        const int r = g2::conv_dgrad(g, dy, w, bias, dx, ws, (hipStream_t)stream, db, db_done);
         if (r >= 0) return r;
     }
     IgemmParams prm{};

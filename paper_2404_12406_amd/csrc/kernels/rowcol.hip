@@ -458,6 +458,11 @@ size_t colsum_workspace(int dtype, int64_t rows, int C) {
     return (size_t)std::max(p1.gy, p0.gy) * C * sizeof(float);
 }
 
+int launch_colsum_finalize(int dtype, const float *part, int rows, int cols, void *out, void *stream) {
+    if (cols == 0) return 0;
+    return finalize(dtype, part, rows, cols, out, (hipStream_t)stream);
+}
+
 int launch_colsum(int dtype, const void *in, int64_t rows, int C, void *out, void *ws, void *stream) {
     if (C == 0) return 0;
     hipStream_t st = (hipStream_t)stream;

@@ -518,7 +518,10 @@ uint32_t kernel_bits(int32_t kind, uint32_t mask) {
 size_t backward_workspace(const Plan &pl, uint32_t kernels) {
     size_t ws = 0;
     if (pl.kind == MS_CONV2D || pl.kind == MS_LINEAR) {
-        if (kernels & MS_K_DGRAD) ws = std::max(ws, ms::conv_dgrad_workspace(pl.dtype, pl.g));
+        // without a weight gradient, the bias gradient may ride on the input gradient
+        if (kernels & MS_K_DGRAD)
+            ws = std::max(ws, ms::conv_dgrad_workspace(pl.dtype, pl.g,
+                                                       (kernels & MS_K_BGRAD) && !(kernels & MS_K_WGRAD)));
         if (kernels & MS_K_WGRAD)
             ws = std::max(ws, ms::conv_wgrad_workspace(pl.dtype, pl.g, (kernels & MS_K_BGRAD) != 0));
         if (kernels & MS_K_BGRAD) ws = std::max(ws, ms::colsum_workspace(pl.dtype, pl.rows, pl.g.K));
@@ -740,9 +743,13 @@ ms_status ms_layer_backward(ms_record *r, const ms_tensor *grad_y, const ms_tens
     case MS_CONV2D:
     case MS_LINEAR:
     {
+        // the bias gradient rides on the weight gradient when there is one,
+        // else (where it can) on the input gradient
         bool db_done = false;
+        void *db_dgrad = (kernels & MS_K_BGRAD) && !(kernels & MS_K_WGRAD) ? grad_b->data : nullptr;
         if (!err && (kernels & MS_K_DGRAD))
-            err = ms::launch_conv_dgrad(pl.dtype, pl.g, dy, r->W.data, nullptr, grad_x->data, ws, stream);
+            err = ms::launch_conv_dgrad(pl.dtype, pl.g, dy, r->W.data, nullptr, grad_x->data, ws, stream, db_dgrad,
+                                        &db_done);
         if (!err && (kernels & MS_K_WGRAD))
             err = ms::launch_conv_wgrad(pl.dtype, pl.g, dy, r->x.data, grad_W->data,
                                         (kernels & MS_K_BGRAD) ? grad_b->data : nullptr, ws, stream, &db_done);

@@ -65,12 +65,14 @@ int launch_conv_fwd(int, const ConvGeom &g, const void *x, const void *w, const 
     return e;
 }
 
-size_t conv_dgrad_workspace(int dtype, const ConvGeom &g) {
+size_t conv_dgrad_workspace(int dtype, const ConvGeom &g, bool) {
     return dtype == kBF16 ? (size_t)g.K * g.R * g.S * g.C * 2 : 0;
 }
 
+// never takes the bias gradient along: the runtime then launches the column sum
 int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *w, const void *bias, void *dx,
-                      void *ws, void *) {
+                      void *ws, void *, void *, bool *db_done) {
+    if (db_done) *db_done = false;
     log(bias ? "conv_dgrad+bias" : "conv_dgrad");
     if (conv_dgrad_workspace(dtype, g) > 0 && !ws) return need(false, "conv_dgrad:ws");
     const long long out = (long long)g.N * g.H * g.W * g.C;

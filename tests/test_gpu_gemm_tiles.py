@@ -87,12 +87,15 @@ def test_linear_tiles(tile, shape, dgrad_variant):
 
 
 @pytest.mark.parametrize("tile", TILES, indirect=True)
-@pytest.mark.parametrize("shape", [(300, 72, 136), (520, 264, 392), (1000, 520, 64), (4100, 64, 1032)])
+@pytest.mark.parametrize("shape", [(300, 72, 136), (520, 264, 392), (1000, 520, 64), (4100, 64, 1032),
+                                   (300, 72, 4200), (700, 1032, 40)])
 def test_linear_tiles_bias_without_weight_gradient(tile, shape, dgrad_variant):
     """Mask input + bias (weight frozen, the fine-tuning mask): the input
-    gradient on every tile next to the separate bias column sum, with rows
-    ragged against every block height and reductions ragged against the
-    64-deep step."""
+    gradient on every tile, the bias gradient taken along by its blocks
+    (dy's columns shared out over the block columns; several 512-column
+    passes when the output is narrow, block columns with no share when it is
+    wide), with rows ragged against every block height and reductions ragged
+    against the 64-deep step."""
     M, Kin, Nout = shape
     seed = 7700 + M
     x = synth.normal((M, Kin), seed, dtype="bf16")
