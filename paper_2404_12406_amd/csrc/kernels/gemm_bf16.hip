@@ -1078,6 +1078,51 @@ __global__ __launch_bounds__(256) void unpack_pair_filter_kernel(const bf16 *__r
     }
 }
 
+// 2 x 2 pixel blocks, for the input gradient of a layer with at most 4
+// input channels and stride 2 in both dimensions: with the padded input cut
+// into 2 x 2 blocks, xq[n][i][j][8a + 4b + c] = x[n][2i + a - ph][2j + b - pw][c],
+// the layer is a stride-1 convolution of xq with the filter
+// wq[k][r'][s'][8a + 4b + c] = w[k][2r' + a][2s' + b][c] (zeros past R, S, C).
+// Its input gradient has 16 columns (pairs along W alone give 8 and two
+// stride phases).  One thread writes the 16 channels of one (k, r', s').
+__global__ __launch_bounds__(256) void pack_block_filter_kernel(const bf16 *__restrict__ w, int K, int R, int S, int C,
+                                                                int Rq, int Sq, bf16 *__restrict__ wq) {
+    const int64_t total = (int64_t)K * Rq * Sq;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t k = i / (Rq * Sq);
+        const int rs = (int)(i - k * (Rq * Sq));
+        const int rq = rs / Sq, sq = rs - rq * Sq;
+        Vec16<bf16> v[2];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int a = e >> 3, b = (e >> 2) & 1, c = e & 3;
+            const int r = 2 * rq + a, s = 2 * sq + b;
+            v[e >> 3].e[e & 7] = c < C && r < R && s < S ? w[((k * R + r) * S + s) * C + c] : (bf16)0.f;
+        }
+        store16(wq + i * 16, v[0]);
+        store16(wq + i * 16 + 8, v[1]);
+    }
+}
+
+// the adjoint of the input packing:
+// dx[n][h][w][c] = dxq[n][(h + ph) / 2][(w + pw) / 2][8 ((h + ph) % 2) + 4 ((w + pw) % 2) + c]
+__global__ __launch_bounds__(256) void unpack_blocks_kernel(const bf16 *__restrict__ dxq, int64_t NH, int H, int W,
+                                                            int C, int Hq, int Wq, int ph, int pw,
+                                                            bf16 *__restrict__ dx) {
+    const int64_t total = NH * W * C;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t pix = i / C;
+        const int c = (int)(i - pix * C);
+        const int64_t nh = pix / W;
+        const int w = (int)(pix - nh * W) + pw;
+        const int64_t n = nh / H;
+        const int h = (int)(nh - n * H) + ph;
+        dx[i] = dxq[((n * Hq + h / 2) * Wq + w / 2) * 16 + 8 * (h & 1) + 4 * (w & 1) + c];
+    }
+}
+
 // dst[row][c] = src[row][c] for c < C (drops the padding channels).
 __global__ __launch_bounds__(256) void crop_channels_kernel(const bf16 *__restrict__ src, int64_t rows, int C8, int C,
                                                             bf16 *__restrict__ dst) {
@@ -1408,6 +1453,44 @@ int unpack_pair_filter(const ConvGeom &g, const void *dwq, void *dw, hipStream_t
     return (int)hipGetLastError();
 }
 
+// 2 x 2 block packing (input gradient only): applies to inputs of at most 4
+// channels with stride 2 in both dimensions whose packed output extents
+// equal the original ones.
+int block_height(const ConvGeom &g) { return (g.H + 2 * g.ph + 1) / 2; }
+bool block_applies(const ConvGeom &g) {
+    return g.C <= 4 && g.sh == 2 && g.sw == 2 && block_height(g) - (g.R + 1) / 2 + 1 == g.P &&
+           pair_width(g) - (g.S + 1) / 2 + 1 == g.Q;
+}
+ConvGeom blocked(const ConvGeom &g) {
+    ConvGeom q = g;
+    q.C = 16;
+    q.H = block_height(g);
+    q.W = pair_width(g);
+    q.R = (g.R + 1) / 2;
+    q.S = (g.S + 1) / 2;
+    q.sh = q.sw = 1;
+    q.ph = q.pw = 0;
+    return q;
+}
+size_t block_x_bytes(const ConvGeom &g) { return al256((size_t)g.N * block_height(g) * pair_width(g) * 16 * 2); }
+size_t block_w_bytes(const ConvGeom &g) { return al256((size_t)g.K * ((g.R + 1) / 2) * ((g.S + 1) / 2) * 16 * 2); }
+
+int pack_block_filter(const ConvGeom &g, const void *w, void *wq, hipStream_t st) {
+    const int64_t work = (int64_t)g.K * ((g.R + 1) / 2) * ((g.S + 1) / 2);
+    if (work == 0) return 0;
+    hipLaunchKernelGGL(pack_block_filter_kernel, dim3(launch_grid(work)), dim3(256), 0, st, (const bf16 *)w, g.K, g.R,
+                       g.S, g.C, (g.R + 1) / 2, (g.S + 1) / 2, (bf16 *)wq);
+    return (int)hipGetLastError();
+}
+
+int unpack_blocks(const ConvGeom &g, const void *dxq, void *dx, hipStream_t st) {
+    const int64_t NH = (int64_t)g.N * g.H, work = NH * g.W * g.C;
+    if (work == 0) return 0;
+    hipLaunchKernelGGL(unpack_blocks_kernel, dim3(launch_grid(work)), dim3(256), 0, st, (const bf16 *)dxq, NH, g.H,
+                       g.W, g.C, block_height(g), pair_width(g), g.ph, g.pw, (bf16 *)dx);
+    return (int)hipGetLastError();
+}
+
 size_t pair_x_bytes(const ConvGeom &g) { return al256((size_t)g.N * g.H * pair_width(g) * 8 * 2); }
 size_t pair_w_bytes(const ConvGeom &g) { return al256((size_t)g.K * g.R * ((g.S + 1) / 2) * 8 * 2); }
 
@@ -1625,8 +1708,9 @@ size_t dgrad_core_workspace(const ConvGeom &g, bool with_db) {
 size_t dgrad_workspace(const ConvGeom &g, bool with_db) {
     if (g.K % 8 != 0) return 0;
     if (g.C % 8 != 0) {
-        // pair packing (without a bias) or channel padding, whichever is larger
-        const size_t pq = pair_applies(g) ? pair_w_bytes(g) + pair_x_bytes(g) + dgrad_core_workspace(paired(g), false) : 0;
+        // block or pair packing (without a bias) or channel padding, whichever is larger
+        const size_t bq = block_applies(g) ? block_w_bytes(g) + block_x_bytes(g) + dgrad_core_workspace(blocked(g), false) : 0;
+        const size_t pq = std::max(bq, pair_applies(g) ? pair_w_bytes(g) + pair_x_bytes(g) + dgrad_core_workspace(paired(g), false) : 0);
         // padded W, padded bias, padded dx, then the workspace of the padded
         // contraction
         const ConvGeom g8 = padded(g);
@@ -1644,6 +1728,17 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bia
                hipStream_t st, void *db, bool *db_done) {
     if (db_done) *db_done = false;
     if (g.K % 8 != 0) return -1;
+    if (g.C % 8 != 0 && block_applies(g) && !bias) {
+        if (!ws || !al16(ws)) return -1;
+        char *wq = static_cast<char *>(ws);
+        char *dxq = wq + block_w_bytes(g);
+        char *ws2 = dxq + block_x_bytes(g);
+        int err = pack_block_filter(g, w, wq, st);
+        if (err) return err;
+        err = conv_dgrad(blocked(g), dy, wq, nullptr, dxq, ws2, st, nullptr, nullptr);
+        if (err) return err;   // -1: not applicable (the caller falls back), else a HIP error
+        return unpack_blocks(g, dxq, dx, st);
+    }
     if (g.C % 8 != 0 && pair_applies(g) && !bias) {
         if (!ws || !al16(ws)) return -1;
         char *wq = static_cast<char *>(ws);

@@ -280,13 +280,15 @@ def test_kernel_timing_counts_launches():
 
 NARROW_CASES = [
     # x shape, w shape, stride, pad: at most 4 channels with a stride-2 width run
-    # as a stride-1 convolution over packed column pairs (the stem's path)
+    # as a stride-1 convolution over packed column pairs (the stem's path); with
+    # stride 2 in both dimensions the input gradient packs 2 x 2 pixel blocks
     ((2, 3, 30, 29), (16, 3, 7, 7), (2, 2), (3, 3)),     # padded width odd, S odd
     ((2, 3, 28, 28), (24, 3, 7, 7), (2, 2), (3, 3)),     # padded width even, S odd
     ((1, 4, 17, 30), (8, 4, 3, 4), (1, 2), (1, 1)),      # width even, S even
     ((2, 1, 9, 21), (16, 1, 5, 5), (2, 2), (0, 2)),      # one channel
     ((1, 2, 12, 13), (8, 2, 3, 3), (2, 2), (1, 1)),
     ((1, 3, 10, 11), (8, 3, 3, 4), (2, 2), (1, 1)),      # padded width odd, S even: channel padding instead
+    ((1, 3, 11, 12), (8, 3, 4, 3), (2, 2), (1, 1)),      # blocks do not fit the height: pairs, two phases
 ]
 
 
