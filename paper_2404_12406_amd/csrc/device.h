@@ -80,7 +80,8 @@ int launch_colsum_finalize(int dtype, const float *part, int rows, int cols, voi
 int launch_colsum(int dtype, const void *in, int64_t rows, int cols, void *out,
                   void *ws, void *stream);
 
-// BN-eval over x[rows][C] (NHWC pixels x channels).  gamma/beta may be null.
+// BN-eval over x[rows][C] (NHWC pixels x channels).  gamma/beta may be null,
+// and so may mean (read as zeros: the input gradient dy * gamma / sqrt(var + eps)).
 int launch_bn_fwd(int dtype, const void *x, const void *mean, const void *var,
                   const void *gamma, const void *beta, float eps, int64_t rows, int C,
                   void *y, void *stream);

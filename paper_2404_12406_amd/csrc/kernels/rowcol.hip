@@ -99,7 +99,7 @@ __global__ __launch_bounds__(256) void bn_fwd_flat_kernel(const T *__restrict__ 
                               : (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int c0 = (int)(i0 % nvc) * V;
     VecT<T, V> pm, pv, pg, pb;
-    pm.load(mean + c0);
+    if (mean) pm.load(mean + c0);
     pv.load(var + c0);
     if (gamma) pg.load(gamma + c0);
     if (beta) pb.load(beta + c0);
@@ -108,8 +108,9 @@ __global__ __launch_bounds__(256) void bn_fwd_flat_kernel(const T *__restrict__ 
     for (int e = 0; e < V; ++e) {
         const float g = gamma ? to_f32(pg.e[e]) : 1.f;
         const float b = beta ? to_f32(pb.e[e]) : 0.f;
+        const float m = mean ? to_f32(pm.e[e]) : 0.f;
         s[e] = g * rsqrtf(to_f32(pv.e[e]) + eps);
-        t[e] = b - to_f32(pm.e[e]) * s[e];
+        t[e] = b - m * s[e];
     }
     for (int64_t i = i0; i < nvec; i += contig ? nvec : kBnU * stride) {
         VecT<T, V> v[kBnU];
@@ -423,6 +424,9 @@ int launch_bn_bwd(int dtype, const void *dy, const void *x, const void *mean, co
     // pointers the requested outputs need (the host runtime guarantees them)
     if ((dx || dgamma) && !var) return (int)hipErrorInvalidValue;
     if (dgamma && (!x || !mean)) return (int)hipErrorInvalidValue;
+    // dx alone (frozen gamma and beta) is the forward's per-channel sweep
+    // with a zero mean and no shift: dx = dy * gamma / sqrt(var + eps)
+    if (dx && !dgamma && !dbeta) return launch_bn_fwd(dtype, dy, nullptr, var, gamma, nullptr, eps, rows, C, dx, stream);
     hipStream_t st = (hipStream_t)stream;
     const int V = dtype == kBF16 ? 8 : 4;
     const bool vec = C % V == 0 && al16(dy) && (!x || al16(x)) && (!dx || al16(dx));
