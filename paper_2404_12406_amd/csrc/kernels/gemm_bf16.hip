@@ -767,6 +767,12 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
     // ------------------------------------------------ k-groups: add group 1's accumulators to group 0's
     if constexpr (KG == 2) {
         float *red = reinterpret_cast<float *>(smem);
+        // group 1 also sums dy's columns; its first loads go out now, so they
+        // land during the exchange below
+        DyColumnSums<16> cs(ra, M, Kg, m0, BM, tn, P.cs_cw, wl, WR * WC, lane);
+        if constexpr (DG && UNIT) {
+            if (kg == 1 && P.cspart && cs.on) cs.issue(0, cs.rg);
+        }
         __syncthreads();   // every wave is done with the operand stages
         if (kg == 1) {
 #pragma unroll
@@ -789,10 +795,7 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
         if (kg == 1) {
             // group 1 sums dy's columns while group 0 writes the output tile
             if constexpr (DG && UNIT) {
-                if (P.cspart) {
-                    DyColumnSums<16> cs(ra, M, Kg, m0, BM, tn, P.cs_cw, wl, WR * WC, lane);
-                    cs.run(false, wl, WR * WC, tm, lane, P.cspart);
-                }
+                if (P.cspart) cs.run(true, wl, WR * WC, tm, lane, P.cspart);
             }
             return;
         }
