@@ -262,6 +262,33 @@ ms_status ms_dropout_forward(const ms_tensor *x, const ms_tensor *y, float p, ui
 ms_status ms_layer_backward(ms_record *rec, const ms_tensor *grad_y, const ms_tensor *grad_x,
                             const ms_tensor *grad_W, const ms_tensor *grad_b, void *stream);
 
+/*
+ * ms_layer_backward_noalloc -- ms_layer_backward() for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Same arguments, checks, kernels,
+ * results and record semantics as ms_layer_backward(); the only difference
+ * is where the transient workspace (split-K partials, bias-gradient partial
+ * rows, transposed or channel-padded copies) lives: in one fixed scratch
+ * array of ms_noalloc_scratch_bytes() bytes per GPU, a static device array
+ * the library holds on every GPU it runs on until the process ends.  The
+ * call allocates nothing (no hipMalloc, hipFree or allocating library
+ * routine) and records no profiling events.
+ * A backward whose workspace (ms_account.transient_workspace_bytes of the
+ * record) exceeds the scratch returns MS_E_UNSUPPORTED before anything is
+ * launched; the record is then not consumed and may go to
+ * ms_layer_backward() instead.
+ * Every call on one GPU uses the same scratch bytes, which keep the last
+ * call's contents (no kernel reads scratch it has not written in the same
+ * call): calls that may overlap on one GPU -- on different streams, or from
+ * several threads without ordering between their streams -- race.  Order
+ * them on one stream.
+ */
+ms_status ms_layer_backward_noalloc(ms_record *rec, const ms_tensor *grad_y, const ms_tensor *grad_x,
+                                    const ms_tensor *grad_W, const ms_tensor *grad_b, void *stream);
+
+/* Size in bytes of the fixed scratch of ms_layer_backward_noalloc() (per GPU). */
+uint64_t ms_noalloc_scratch_bytes(void);
+
 /* Copy a record's accounting into *out. */
 ms_status ms_record_account(const ms_record *rec, ms_account *out);
 

@@ -24,7 +24,7 @@ EXPORTS = (
     "ms_ledger_read", "ms_ledger_reset", "ms_policy_account", "ms_status_str",
     "ms_last_error", "ms_version", "ms_testing_fail_next_workspace", "ms_testing_live_records",
     "ms_profile_start", "ms_profile_read", "ms_relu_mask_bytes", "ms_relu_forward",
-    "ms_dropout_blocks", "ms_dropout_forward",
+    "ms_dropout_blocks", "ms_dropout_forward", "ms_layer_backward_noalloc", "ms_noalloc_scratch_bytes",
 )
 MS_PROF_FWD, MS_PROF_DGRAD, MS_PROF_WGRAD, MS_PROF_BN, MS_PROF_ACT = 1, 2, 4, 8, 16
 
@@ -67,6 +67,10 @@ def configure(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.ms_layer_forward.restype = ctypes.c_int
     lib.ms_layer_backward.argtypes = [ctypes.c_void_p, _T, _T, _T, _T, ctypes.c_void_p]
     lib.ms_layer_backward.restype = ctypes.c_int
+    lib.ms_layer_backward_noalloc.argtypes = [ctypes.c_void_p, _T, _T, _T, _T, ctypes.c_void_p]
+    lib.ms_layer_backward_noalloc.restype = ctypes.c_int
+    lib.ms_noalloc_scratch_bytes.argtypes = []
+    lib.ms_noalloc_scratch_bytes.restype = ctypes.c_uint64
     lib.ms_record_account.argtypes = [ctypes.c_void_p, ctypes.POINTER(MsAccount)]
     lib.ms_record_account.restype = ctypes.c_int
     lib.ms_record_free.argtypes = [ctypes.c_void_p]

@@ -115,12 +115,23 @@ void *workspace_get(void *stream, size_t bytes, int *err);
 // Test hook: make the next `n` workspace growths fail.
 void workspace_fail_next(int n);
 
+// Fixed scratch of the no-allocation backward (workspace.hip): a static
+// device array of kScratchBytes per GPU.  scratch_get returns its device
+// address on the current device (looked up once per device) or null with
+// *err = 1 when `bytes` exceeds kScratchBytes, 2 on a HIP error.  Every
+// caller on one device shares the same bytes.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+void *scratch_get(size_t bytes, int *err);
+
 int device_last_error();  // hipGetLastError()
 
 // Kernel timing (profile.hip): prof_mark(kind, stream, true) before a launch
 // and (.., false) after it record an event pair when `kind` is armed.
 enum ProfKind : unsigned { kProfFwd = 1u, kProfDgrad = 2u, kProfWgrad = 4u, kProfBn = 8u, kProfAct = 16u };
 void prof_mark(unsigned kind, void *stream, bool begin);
+// Skip prof_mark on the calling thread while `off` (the no-allocation
+// backward records no events).
+void prof_thread_off(bool off);
 int prof_start(unsigned kinds);
 int prof_read(unsigned kind, uint64_t *launches, double *total_ms);
 

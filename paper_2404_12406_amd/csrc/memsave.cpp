@@ -708,8 +708,16 @@ ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
     return MS_OK;
 }
 
-ms_status ms_layer_backward(ms_record *r, const ms_tensor *grad_y, const ms_tensor *grad_x,
-                            const ms_tensor *grad_W, const ms_tensor *grad_b, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// Backward of a record.  The transient workspace comes from the per-stream
+// pool (which may allocate) or, with fixed_scratch, from the library's
+// static scratch array (which never does; requests beyond its size fail
+// before anything is launched).
+ms_status backward_impl(ms_record *r, const ms_tensor *grad_y, const ms_tensor *grad_x,
+                        const ms_tensor *grad_W, const ms_tensor *grad_b, void *stream, bool fixed_scratch) {
     clear_err();
     if (!r) return fail(MS_E_NULL, "record is NULL");
     if (r->magic != kMagic) return fail(MS_E_ARG, "not a live record");
@@ -731,7 +739,13 @@ ms_status ms_layer_backward(ms_record *r, const ms_tensor *grad_y, const ms_tens
     const uint32_t kernels = r->acct.kernels;
     void *ws = nullptr;
     const size_t ws_bytes = backward_workspace(pl, kernels);
-    if (ws_bytes) {
+    if (ws_bytes && fixed_scratch) {
+        int werr = 0;
+        ws = ms::scratch_get(ws_bytes, &werr);
+        if (!ws) return werr == 1 ? fail(MS_E_UNSUPPORTED, "backward needs %zu bytes of scratch; the fixed scratch "
+                                                           "holds %zu", ws_bytes, ms::kScratchBytes)
+                                  : hip_fail(ms::device_last_error(), "scratch lookup");
+    } else if (ws_bytes) {
         int werr = 0;
         ws = ms::workspace_get(stream, ws_bytes, &werr);
         if (!ws) return werr == 1 ? fail(MS_E_NOMEM, "workspace of %zu bytes unavailable", ws_bytes)
@@ -819,6 +833,29 @@ ms_status ms_layer_backward(ms_record *r, const ms_tensor *grad_y, const ms_tens
     release(r);
     return MS_OK;
 }
+
+// Profiling events stay off for the calling thread while one lives.
+struct ProfOff {
+    ProfOff() { ms::prof_thread_off(true); }
+    ~ProfOff() { ms::prof_thread_off(false); }
+};
+
+}  // namespace
+
+extern "C" {
+
+ms_status ms_layer_backward(ms_record *r, const ms_tensor *grad_y, const ms_tensor *grad_x,
+                            const ms_tensor *grad_W, const ms_tensor *grad_b, void *stream) {
+    return backward_impl(r, grad_y, grad_x, grad_W, grad_b, stream, false);
+}
+
+ms_status ms_layer_backward_noalloc(ms_record *r, const ms_tensor *grad_y, const ms_tensor *grad_x,
+                                    const ms_tensor *grad_W, const ms_tensor *grad_b, void *stream) {
+    ProfOff off;
+    return backward_impl(r, grad_y, grad_x, grad_W, grad_b, stream, true);
+}
+
+uint64_t ms_noalloc_scratch_bytes(void) { return ms::kScratchBytes; }
 
 uint64_t ms_relu_mask_bytes(int64_t n) { return relu_mask_bytes(n); }
 

@@ -52,8 +52,14 @@ void recycle(KindLog &l) {
 }
 }  // namespace
 
+namespace {
+thread_local bool t_off = false;
+}  // namespace
+
+void prof_thread_off(bool off) { t_off = off; }
+
 void prof_mark(unsigned kind, void *stream, bool begin) {
-    if (!(g_armed & kind)) return;   // unarmed fast path (racy read is harmless)
+    if (t_off || !(g_armed & kind)) return;   // unarmed fast path (racy read is harmless)
     std::lock_guard<std::mutex> lk(g_mu);
     if (!(g_armed & kind)) return;
     const int k = kind_index(kind);

@@ -48,6 +48,11 @@ void stub_reset() {
     g_log.clear();
     g_violation.clear();
 }
+// workspace growths (allocations) since the library was loaded
+long stub_workspace_allocations() {
+    std::lock_guard<std::mutex> lk(g_mu);
+    return (long)g_ws.size();
+}
 }
 
 namespace ms {
@@ -209,9 +214,20 @@ void workspace_fail_next(int n) {
     g_fail_next = n;
 }
 
+// the stub launchers never dereference workspace: any distinct non-null
+// address stands in for the fixed scratch array
+void *scratch_get(size_t bytes, int *err) {
+    static char stand_in[256];
+    *err = bytes > kScratchBytes ? 1 : 0;
+    if (*err) return nullptr;
+    log("scratch");
+    return stand_in;
+}
+
 int device_last_error() { return 0; }
 
 void prof_mark(unsigned, void *, bool) {}
+void prof_thread_off(bool) {}
 int prof_start(unsigned) { return 0; }
 int prof_read(unsigned, uint64_t *launches, double *total_ms) {
     *launches = 0;

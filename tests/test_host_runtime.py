@@ -338,6 +338,59 @@ def test_workspace_failure_leaves_record_and_ledger_intact(stub):
     stub.ms_record_free(None)
 
 
+def test_noalloc_backward_launches_the_same_plan_from_the_fixed_scratch(stub):
+    """The no-allocation backward runs the launch plan of ms_layer_backward
+    with its workspace taken from the fixed scratch (never the allocating
+    pool), rejects a workspace larger than the scratch before launching
+    anything, and leaves that record usable by ms_layer_backward."""
+    stub.stub_workspace_allocations.restype = ctypes.c_long
+    cap = stub.ms_noalloc_scratch_bytes()
+    assert cap == 64 << 20
+    for spec, mask in ((wl.conv_sweep_bf16("01").layers[0], 6), (wl.linear_stack_bf16().layers[0], 5),
+                       (wl.conv_sweep_bf16("11", pointwise=True).layers[0], 7)):
+        a = LayerArgs(spec, "bf16")
+        logs = []
+        for entry in (stub.ms_layer_backward, stub.ms_layer_backward_noalloc):
+            h = ctypes.c_void_p()
+            assert stub.ms_layer_forward(ctypes.byref(a.layer), ref(a.x), ref(a.W), ref(a.b), mask, ref(a.y),
+                                         ctypes.byref(h), None) == 0
+            gy = tdesc(spec.out_shape())
+            gx, gw, gb = _grads(a, mask)
+            n_alloc = stub.stub_workspace_allocations()
+            stub.stub_reset()
+            assert entry(h, ref(gy), ref(gx), ref(gw), ref(gb), None) == 0, stub.ms_last_error()
+            assert stub.stub_violations().decode() == ""
+            logs.append(stub.stub_log().decode())
+            if entry is stub.ms_layer_backward_noalloc:
+                assert stub.stub_workspace_allocations() == n_alloc
+            stub.ms_record_free(h)
+        acct_ws = logs[1].startswith("scratch;")
+        assert logs[1] == ("scratch;" if acct_ws else "") + logs[0], logs
+    # a backward whose workspace exceeds the scratch: the weight gradient of
+    # a 4096 x 4096 Linear over 8192 rows (split-K partials)
+    big = wl.LayerSpec("linear", "big", (8192, 4096), out_ch=4096, has_bias=True)
+    a = LayerArgs(big, "bf16")
+    h = ctypes.c_void_p()
+    assert stub.ms_layer_forward(ctypes.byref(a.layer), ref(a.x), ref(a.W), ref(a.b), 6, ref(a.y),
+                                 ctypes.byref(h), None) == 0
+    acct = L.MsAccount()
+    stub.ms_record_account(h, ctypes.byref(acct))
+    assert acct.transient_workspace_bytes > cap
+    live1, pk = ctypes.c_uint64(), ctypes.c_uint64()
+    stub.ms_ledger_read(ctypes.byref(live1), ctypes.byref(pk))
+    gy = tdesc(big.out_shape())
+    _, gw, gb = _grads(a, 6)
+    stub.stub_reset()
+    assert stub.ms_layer_backward_noalloc(h, ref(gy), None, ref(gw), ref(gb), None) == L.MS_E_UNSUPPORTED
+    assert "scratch" in stub.ms_last_error().decode()
+    assert stub.stub_log().decode() == ""
+    live2 = ctypes.c_uint64()
+    stub.ms_ledger_read(ctypes.byref(live2), ctypes.byref(pk))
+    assert live2.value == live1.value
+    assert stub.ms_layer_backward(h, ref(gy), None, ref(gw), ref(gb), None) == 0
+    stub.ms_record_free(h)
+
+
 def test_ledger_peak_over_a_stack(stub):
     """Peak retained bytes of the ResNet-18-shaped stack in its 'Input'
     variant equal the closed form: convs and BN keep nothing, the final
