@@ -322,13 +322,19 @@ ms_status ms_policy_account(const ms_layer *layer, const ms_tensor *x, const ms_
  *   MS_PROF_WGRAD weight-gradient GEMM (its split-K partial launch)
  *   MS_PROF_BN    BN-eval forward kernel
  *   MS_PROF_ACT   ReLU and dropout forward and backward kernels
+ *   MS_PROF_RED   the reduction passes: a BN-eval backward (its dx-only
+ *                 sweep, or its reduction kernel and the finalize kernels
+ *                 of dgamma / dbeta, bracketed together) and a bias
+ *                 gradient's column sum with its finalize kernel (or the
+ *                 finalize alone when the sums rode on the input gradient)
  * ms_profile_start() discards earlier records and arms `kinds` (0 disarms);
  * at most 65536 launches per kind are recorded.  ms_profile_read() waits
  * for the recorded events and returns the number of launches of one kind and
  * their summed duration in milliseconds.  Calls from several threads or
  * streams at once are serialised internally.
  */
-enum { MS_PROF_FWD = 1u, MS_PROF_DGRAD = 2u, MS_PROF_WGRAD = 4u, MS_PROF_BN = 8u, MS_PROF_ACT = 16u };
+enum { MS_PROF_FWD = 1u, MS_PROF_DGRAD = 2u, MS_PROF_WGRAD = 4u, MS_PROF_BN = 8u, MS_PROF_ACT = 16u,
+       MS_PROF_RED = 32u };
 ms_status ms_profile_start(uint32_t kinds);
 ms_status ms_profile_read(uint32_t kind, uint64_t *launches, double *total_ms);
 

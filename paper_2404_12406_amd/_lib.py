@@ -26,7 +26,7 @@ EXPORTS = (
     "ms_profile_start", "ms_profile_read", "ms_relu_mask_bytes", "ms_relu_forward",
     "ms_dropout_blocks", "ms_dropout_forward", "ms_layer_backward_noalloc", "ms_noalloc_scratch_bytes",
 )
-MS_PROF_FWD, MS_PROF_DGRAD, MS_PROF_WGRAD, MS_PROF_BN, MS_PROF_ACT = 1, 2, 4, 8, 16
+MS_PROF_FWD, MS_PROF_DGRAD, MS_PROF_WGRAD, MS_PROF_BN, MS_PROF_ACT, MS_PROF_RED = 1, 2, 4, 8, 16, 32
 
 
 class MsTensor(ctypes.Structure):

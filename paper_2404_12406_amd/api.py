@@ -407,7 +407,8 @@ def ledger_reset():
     check(_lib.load().ms_ledger_reset(), "ms_ledger_reset")
 
 
-PROF_FWD, PROF_DGRAD, PROF_WGRAD, PROF_BN, PROF_ACT = 1, 2, 4, 8, 16
+PROF_FWD, PROF_DGRAD, PROF_WGRAD, PROF_BN, PROF_ACT, PROF_RED = 1, 2, 4, 8, 16, 32
+PROF_ALL = 63
 
 
 def profile_start(kinds: int):

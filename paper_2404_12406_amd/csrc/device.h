@@ -127,7 +127,9 @@ int device_last_error();  // hipGetLastError()
 
 // Kernel timing (profile.hip): prof_mark(kind, stream, true) before a launch
 // and (.., false) after it record an event pair when `kind` is armed.
-enum ProfKind : unsigned { kProfFwd = 1u, kProfDgrad = 2u, kProfWgrad = 4u, kProfBn = 8u, kProfAct = 16u };
+enum ProfKind : unsigned {
+    kProfFwd = 1u, kProfDgrad = 2u, kProfWgrad = 4u, kProfBn = 8u, kProfAct = 16u, kProfRed = 32u
+};
 void prof_mark(unsigned kind, void *stream, bool begin);
 // Skip prof_mark on the calling thread while `off` (the no-allocation
 // backward records no events).

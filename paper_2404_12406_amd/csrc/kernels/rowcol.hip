@@ -358,8 +358,11 @@ int finalize(int dtype, const float *part, int gy, int C, void *out, hipStream_t
 
 }  // namespace
 
-int launch_bn_fwd(int dtype, const void *x, const void *mean, const void *var, const void *gamma,
-                  const void *beta, float eps, int64_t rows, int C, void *y, void *stream) {
+namespace {
+// The flat per-channel sweep y = x * s_c + t_c; `pk` is the profiling kind
+// its launch counts as (the BN forward, or a BN backward that wants dx only).
+int bn_sweep(int dtype, const void *x, const void *mean, const void *var, const void *gamma, const void *beta,
+             float eps, int64_t rows, int C, void *y, void *stream, unsigned pk) {
     if (rows == 0 || C == 0) return 0;
     const int V = dtype == kBF16 ? 8 : 4;
     // 16-byte vectors of x, y and of the per-channel parameters
@@ -381,7 +384,7 @@ int launch_bn_fwd(int dtype, const void *x, const void *mean, const void *var, c
     const bool contig = 256 % nvc == 0;
     if (!contig) blocks = (blocks + q - 1) / q * q;
     hipStream_t st = (hipStream_t)stream;
-    prof_mark(kProfBn, st, true);
+    prof_mark(pk, st, true);
     if (dtype == kBF16) {
         if (vec)
             hipLaunchKernelGGL((bn_fwd_flat_kernel<bf16, 8>), dim3((unsigned)blocks), dim3(256), 0, st, (const bf16 *)x,
@@ -402,8 +405,14 @@ int launch_bn_fwd(int dtype, const void *x, const void *mean, const void *var, c
                                nvec, nvc, contig, (float *)y);
     }
     const int err = (int)hipGetLastError();
-    prof_mark(kProfBn, st, false);
+    prof_mark(pk, st, false);
     return err;
+}
+}  // namespace
+
+int launch_bn_fwd(int dtype, const void *x, const void *mean, const void *var, const void *gamma,
+                  const void *beta, float eps, int64_t rows, int C, void *y, void *stream) {
+    return bn_sweep(dtype, x, mean, var, gamma, beta, eps, rows, C, y, stream, kProfBn);
 }
 
 static RowColPlan bn_bwd_plan(int dtype, int64_t rows, int C, bool vec) {
@@ -426,8 +435,9 @@ int launch_bn_bwd(int dtype, const void *dy, const void *x, const void *mean, co
     if (dgamma && (!x || !mean)) return (int)hipErrorInvalidValue;
     // dx alone (frozen gamma and beta) is the forward's per-channel sweep
     // with a zero mean and no shift: dx = dy * gamma / sqrt(var + eps)
-    if (dx && !dgamma && !dbeta) return launch_bn_fwd(dtype, dy, nullptr, var, gamma, nullptr, eps, rows, C, dx, stream);
+    if (dx && !dgamma && !dbeta) return bn_sweep(dtype, dy, nullptr, var, gamma, nullptr, eps, rows, C, dx, stream, kProfRed);
     hipStream_t st = (hipStream_t)stream;
+    prof_mark(kProfRed, st, true);
     const int V = dtype == kBF16 ? 8 : 4;
     const bool vec = C % V == 0 && al16(dy) && (!x || al16(x)) && (!dx || al16(dx));
     RowColPlan p = bn_bwd_plan(dtype, rows, C, vec);
@@ -453,6 +463,7 @@ int launch_bn_bwd(int dtype, const void *dy, const void *x, const void *mean, co
         int err = finalize(dtype, part1, gy, C, dbeta, st);
         if (err) return err;
     }
+    prof_mark(kProfRed, st, false);
     return 0;
 }
 
@@ -464,7 +475,10 @@ size_t colsum_workspace(int dtype, int64_t rows, int C) {
 
 int launch_colsum_finalize(int dtype, const float *part, int rows, int cols, void *out, void *stream) {
     if (cols == 0) return 0;
-    return finalize(dtype, part, rows, cols, out, (hipStream_t)stream);
+    prof_mark(kProfRed, stream, true);
+    const int err = finalize(dtype, part, rows, cols, out, (hipStream_t)stream);
+    prof_mark(kProfRed, stream, false);
+    return err;
 }
 
 int launch_colsum(int dtype, const void *in, int64_t rows, int C, void *out, void *ws, void *stream) {
@@ -474,6 +488,7 @@ int launch_colsum(int dtype, const void *in, int64_t rows, int C, void *out, voi
     const bool vec = C % V == 0 && al16(in);
     RowColPlan p = plan_rowcol(dtype, rows, C, vec, kTargetBlocks);
     float *part = static_cast<float *>(ws);
+    prof_mark(kProfRed, st, true);
     if (rows > 0) {
         int err;
         if (dtype == kBF16)
@@ -484,7 +499,9 @@ int launch_colsum(int dtype, const void *in, int64_t rows, int C, void *out, voi
                       : reduce_t<float, 1, 0>(p, in, nullptr, nullptr, nullptr, nullptr, 0.f, rows, C, nullptr, false, true, part, nullptr, st);
         if (err) return err;
     }
-    return finalize(dtype, part, rows > 0 ? p.gy : 0, C, out, st);
+    const int err = finalize(dtype, part, rows > 0 ? p.gy : 0, C, out, st);
+    prof_mark(kProfRed, st, false);
+    return err;
 }
 
 int launch_avgpool_fwd(int dtype, const void *x, int N, int L, int C, void *y, void *stream) {

@@ -1013,7 +1013,7 @@ ms_status ms_policy_account(const ms_layer *layer, const ms_tensor *x, const ms_
 
 ms_status ms_profile_start(uint32_t kinds) {
     clear_err();
-    if (kinds & ~31u) return fail(MS_E_ARG, "unknown profile kinds 0x%x", kinds);
+    if (kinds & ~63u) return fail(MS_E_ARG, "unknown profile kinds 0x%x", kinds);
     const int err = ms::prof_start(kinds);
     return err ? hip_fail(err, "ms_profile_start") : MS_OK;
 }
@@ -1022,7 +1022,7 @@ ms_status ms_profile_read(uint32_t kind, uint64_t *launches, double *total_ms) {
     clear_err();
     if (!launches || !total_ms) return fail(MS_E_NULL, "NULL argument");
     if (kind != MS_PROF_FWD && kind != MS_PROF_DGRAD && kind != MS_PROF_WGRAD && kind != MS_PROF_BN &&
-        kind != MS_PROF_ACT)
+        kind != MS_PROF_ACT && kind != MS_PROF_RED)
         return fail(MS_E_ARG, "read one kind at a time");
     const int err = ms::prof_read(kind, launches, total_ms);
     return err ? hip_fail(err, "ms_profile_read") : MS_OK;

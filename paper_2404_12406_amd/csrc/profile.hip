@@ -11,7 +11,7 @@
 namespace ms {
 
 namespace {
-constexpr int kKinds = 5;
+constexpr int kKinds = 6;
 constexpr size_t kMaxLaunches = 65536;
 
 struct KindLog {
@@ -22,7 +22,7 @@ std::mutex g_mu;
 unsigned g_armed = 0;
 KindLog g_log[kKinds];
 std::vector<hipEvent_t> g_pool;           // events reusable across sessions
-bool g_open[kKinds] = {false, false, false, false, false};
+bool g_open[kKinds] = {false, false, false, false, false, false};
 
 int kind_index(unsigned kind) {
     for (int i = 0; i < kKinds; ++i)

@@ -31,12 +31,14 @@ def round_bf16(a: np.ndarray) -> np.ndarray:
     Inputs here are finite draws; NaN/Inf are passed through unchanged.
     """
     a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    r = ((u + 0x7FFF + lsb) & 0xFFFF0000).astype(np.uint32)
+    u = a.view(np.uint32)
+    # 32-bit arithmetic: a finite value's bits are at most 0xFF7FFFFF, so
+    # adding 0x8000 cannot wrap (only NaN payloads could, and NaN/Inf take
+    # the np.where branch)
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) & np.uint32(0xFFFF0000)
     out = r.view(np.float32).reshape(a.shape)
     finite = np.isfinite(a)
-    return np.where(finite, out, a).astype(np.float32)
+    return np.where(finite, out, a).astype(np.float32, copy=False)
 
 
 def cast(a: np.ndarray, dtype: str) -> np.ndarray:

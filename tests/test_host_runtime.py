@@ -471,7 +471,9 @@ def test_real_library_planners_on_edge_shapes(spec, dtype):
 def test_profile_api_validates_arguments(stub):
     n, t = ctypes.c_uint64(), ctypes.c_double()
     stub.ms_profile_start.argtypes = [ctypes.c_uint32]
-    assert stub.ms_profile_start(32) == L.MS_E_ARG
+    assert stub.ms_profile_start(64) == L.MS_E_ARG
+    assert stub.ms_profile_start(L.MS_PROF_RED) == 0
+    assert stub.ms_profile_read(L.MS_PROF_RED, ctypes.byref(n), ctypes.byref(t)) == 0
     assert stub.ms_profile_start(L.MS_PROF_FWD | L.MS_PROF_DGRAD) == 0
     assert stub.ms_profile_read(L.MS_PROF_FWD | L.MS_PROF_DGRAD, ctypes.byref(n), ctypes.byref(t)) == L.MS_E_ARG
     assert stub.ms_profile_read(L.MS_PROF_FWD, None, ctypes.byref(t)) == L.MS_E_NULL
