@@ -300,7 +300,7 @@ def timing(chains, steps, warmup, flush, backward=True, clock=None):
                      "p90_ms": round(pct(cold, 90), 4)}, "clock": clk}
 
 
-def per_layer_roofline(chains, w, reps, flush):
+def per_layer_roofline(chains, w, reps, flush, order=None):
     """Each layer's timed kernels, cache evicted before every launch: the
     layer's forward, then its backward, `reps` times, with every profiling
     kind armed (a layer's forward and backward kernels are of distinct
@@ -317,6 +317,8 @@ def per_layer_roofline(chains, w, reps, flush):
             if not passes or key in seen:
                 continue
             seen.add(key)
+            if order is not None:
+                order.append({"layer": spec.name, "mask": p.mask, "reps": reps})
             ms.profile_start(ms.PROF_ALL)
             for _ in range(reps):
                 flush()
@@ -974,8 +976,11 @@ def main():
     ap.add_argument("--no-extra", action="store_true", help="skip the other workloads")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle timings")
     ap.add_argument("--workload", default=None,
-                    help="measure this one workload only (warm and cold steps, per-layer kernels) and print "
-                         "its record; for kernel traces and counters")
+                    help="measure these workloads only (comma-separated names: warm and cold steps, per-layer "
+                         "kernels) and print one record each; for kernel traces and counters")
+    ap.add_argument("--per-layer-only", action="store_true",
+                    help="with --workload: one untimed step, then only the per-layer kernel timings (every "
+                         "layer call preceded by a cache-evicting sweep, so a kernel trace splits at the sweeps)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run three plain 256 MiB device copies, the known-size reference "
                          "for hardware byte counters (FETCH_SIZE / WRITE_SIZE) of the same process")
@@ -995,9 +1000,19 @@ def main():
         copy_calibration()
     flush = Flusher()
     if args.workload:
-        w = workload_by_name(args.workload)
-        rec = measure(w, args.steps, args.warmup, flush)
-        print(json.dumps({"workload": args.workload, **rec}), flush=True)
+        for name in args.workload.split(","):
+            w = workload_by_name(name)
+            if args.per_layer_only:
+                _, chains = build(w)
+                run_steps(chains, 1)
+                torch.cuda.synchronize()
+                order = []
+                rec = {"per_layer": per_layer_roofline(chains, w, args.steps, flush, order), "measured": order}
+                del chains
+                torch.cuda.empty_cache()
+            else:
+                rec = measure(w, args.steps, args.warmup, flush)
+            print(json.dumps({"workload": name, **rec}), flush=True)
         return
     h = headline(args.steps, args.warmup, flush)
     w = h["workload"]
