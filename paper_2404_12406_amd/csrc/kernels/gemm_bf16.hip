@@ -296,6 +296,9 @@ struct Cfg {
     static_assert(SMEM_BYTES <= 160 * 1024, "LDS");
     static_assert(BN * 2 <= 64 * 16, "bias columns fit the bias area");
     static_assert(KG == 1 || (KG == 2 && STAGES >= 3 && MODE != kWgrad), "k-groups: spread pipeline, no weight gradient");
+    // block widths that are not a power of two (192) only with both operands
+    // k-contiguous: the transposing reads' slot swizzle needs 2^n slots a row
+    static_assert((BN & (BN - 1)) == 0 || (A_KC && B_KC), "a 192-wide tile reads k-contiguous operands only");
     static_assert(KG == 1 || (WR * WC) * (WM / 32) * (WN / 32) * 16 * 64 * 4 <= LDS_BYTES, "k-group partials fit LDS");
 };
 
@@ -858,7 +861,8 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
     if constexpr (KG == 1) __syncthreads();   // every wave is done with the operand stages
     bf16 *stage = reinterpret_cast<bf16 *>(smem) + wave * G::EPI_ROWS * G::EPI_PITCH;
     constexpr int SEG = G::WN / 8;                   // 16-byte segments per staged row
-    constexpr int ROWS_PER_PASS = 64 / SEG;
+    constexpr int ROWS_PER_PASS = 64 / SEG;          // rows a wave stores per pass (lanes past
+                                                     // ROWS_PER_PASS * SEG idle when SEG does not divide 64)
     typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
     // bias: the lane's output columns are the same for every row it holds,
     // so its bias values are read once and added in fp32 before the single
@@ -914,6 +918,7 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
             const int cl = (lane % SEG) * 8;
             const int m = m0 + wm0 + i * 32 + rl;
             const int n = n0 + wn0 + cl;
+            if ((64 % SEG != 0 && lane >= ROWS_PER_PASS * SEG) || rl >= G::EPI_ROWS) continue;
             Vec16<bf16> v;
             v.u = *reinterpret_cast<const u32x4 *>(stage + rl * G::EPI_PITCH + cl);
             if (m >= M || n >= N) continue;
@@ -1204,6 +1209,7 @@ constexpr Tile kTiles[] = {
     {"128x128k2", 128, 128, 2, 2, 4, 1, 0.95f, 0.95f, 2},  // 2 k-groups of 4 waves of 64 x 64, 4 stages
     {"128x64", 128, 64, 2, 2, 2, 3, 0.75f, 0.75f},        // 4 waves of 64 x 32, 48 KB, three blocks per CU
     {"256x32", 256, 32, 4, 1, 2, 2, 0.70f, 0.70f},        // 4 waves of 64 x 32, 72 KB, two blocks per CU
+    {"128x192k2", 128, 192, 2, 2, 3, 1, 0.82f, 0.82f, 2},  // 2 k-groups of 4 waves of 64 x 96, 3 stages (120 KB)
 };
 constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 // tiles the planner chooses from
@@ -1212,14 +1218,19 @@ constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 // (weight gradient 4096 x 1024 x 4096: 57 -> 46 us), and the k-group tile
 // beats that one by ~5% on the forward and input gradient of 4096 x 1024
 // outputs with K = 4096 (38.7 -> 36.3 us)
-constexpr bool kAuto[kNumTiles] = {true, true, true, true, false, true, true, true, false};
+constexpr bool kAuto[kNumTiles] = {true, true, true, true, false, true, true, true, false, false};
 // the narrow 256 x 32 tile is for thin outputs (N <= 32, e.g. the input
 // gradient of a 3-channel image) and exists only for the contractions whose
 // operands are both k-contiguous (forward, input gradient through the
 // transposed filter): the transposing reads' swizzle assumes rows of at
 // least 8 slots
 constexpr bool narrow_tile(const Tile &t) { return t.bn < 64; }
-constexpr bool kAutoKc[kNumTiles] = {true, true, true, true, false, true, true, true, true};
+// The 128 x 192 tile (two k-groups) also exists only for those contractions:
+// its block width is not a power of two.  On 8192-row outputs it makes every
+// encoder shape a whole number of waves (8192 x 768: 256 tiles, where
+// 256 x 128 leaves 64 CUs idle).
+constexpr bool kc_only(const Tile &t) { return narrow_tile(t) || t.bn == 192; }
+constexpr bool kAutoKc[kNumTiles] = {true, true, true, true, false, true, true, true, true, true};
 // tiles the planner chooses from for the input gradient of convolutions
 // that are not 1x1 / stride 1 (implicit-GEMM gathers): on the
 // ResNet-18-shaped stack's layers and the conv sweep the 2-stage 128 x 128
@@ -1231,7 +1242,7 @@ constexpr bool kAutoKc[kNumTiles] = {true, true, true, true, false, true, true, 
 // 0.121 -> 0.116 ms.  The forward keeps the general set: restricted the same
 // way it took split reductions whose extra pass made the frozen stack 6%
 // slower.
-constexpr bool kAutoConv[kNumTiles] = {true, false, true, false, false, false, false, true, true};
+constexpr bool kAutoConv[kNumTiles] = {true, false, true, false, false, false, false, true, true, false};
 
 // MEMSAVE_GEMM_TILE=<name> forces one tile shape (a debugging and testing
 // knob); returns its index or -1.
@@ -1301,7 +1312,9 @@ GemmPlan plan_gemm(long M, long N, long K, int z, int split_cap = 16, bool allow
                    int kgroups = kKgAuto, const bool *auto_set = kAuto) {
     int forced = forced_tile();
     // not built for the weight gradient: plan as usual
-    if (forced >= 0 && (kTiles[forced].kg > 1 || narrow_tile(kTiles[forced])) && kgroups == kKgNever) forced = -1;
+    if (forced >= 0 && (kTiles[forced].kg > 1 || kc_only(kTiles[forced])) && kgroups == kKgNever) forced = -1;
+    // the in-place input gradient (its set is kAuto) has no k-contiguous-only tile: plan as usual
+    if (forced >= 0 && kc_only(kTiles[forced]) && auto_set == kAuto) forced = -1;
     if (forced == 0 && !allow_256x256) forced = 1;   // the next widest tile (256 x 128)
     const int fs = split_cap > 1 ? forced_splits() : 0;
     const int max_splits = (int)std::max<long>(1, std::min<long>(split_cap, K / (4 * BK)));
@@ -1311,6 +1324,11 @@ GemmPlan plan_gemm(long M, long N, long K, int z, int split_cap = 16, bool allow
         if (forced >= 0 ? ti != forced : !auto_set[ti]) continue;
         if (ti == 0 && !allow_256x256) continue;
         if (kTiles[ti].kg > 1 && (kgroups == kKgNever || (kgroups == kKgForced && forced < 0))) continue;
+        // the 192-wide tile pays off only where it fills the CUs in one wave
+        // (encoder shapes, 8192 x {768, 2304, 3072} outputs: 34 against 38 us
+        // at K = 2304 in one wave, 49 against 44 us in three waves at K = 768)
+        if (forced < 0 && kTiles[ti].bn == 192 &&
+            ((M + 127) / 128) * ((N + 191) / 192) * z > (long)kCUs * kTiles[ti].per_cu) continue;
         for (int sp = 1; sp <= (fs ? 1 : max_splits); ++sp) {
             const int splits = fs ? fs : sp;
             const double us = est_us(kTiles[ti], M, N, K, z, splits);
@@ -1357,6 +1375,9 @@ int go_tile(const Tile &t, const Args &a, dim3 grid, hipStream_t st) {
     if (t.kg == 2) {
         if constexpr (MODE != kWgrad) {
             if (t.bm == 128 && t.bn == 128) return go<MODE, 128, 128, 2, 2, 4, 1, UNIT, 2>(a, grid, st);
+        }
+        if constexpr (MODE == kFwd || MODE == kDgrad) {
+            if (t.bm == 128 && t.bn == 192) return go<MODE, 128, 192, 2, 2, 3, 1, UNIT, 2>(a, grid, st);
         }
         return (int)hipErrorInvalidValue;
     }
@@ -1674,17 +1695,25 @@ DgradChoice dgrad_choice(const ConvGeom &g) {
     const bool *set = unit ? kAutoKc : kAutoConv;
     const char *e = getenv("MEMSAVE_DGRAD");
     const int forced = forced_tile();
-    // the narrow tile reads W through the transposed copy only
-    const bool narrow_forced = forced >= 0 && narrow_tile(kTiles[forced]);
-    if (e && *e && !narrow_forced) {
+    // the narrow and 192-wide tiles read W through the transposed copy only
+    const bool kc_forced = forced >= 0 && kc_only(kTiles[forced]);
+    if (e && *e && !kc_forced) {
         const bool direct = e[0] == 'd';
         return {direct, plan_gemm(M, g.C, Kb, z, direct ? 1 : 16, direct || unit, kg, direct ? kAuto : set)};
     }
     const GemmPlan pt = plan_gemm(M, g.C, Kb, z, 16, unit, kg, set);
     if (!unit) return {false, pt};
-    if (narrow_tile(pt.t)) return {false, pt};
+    if (narrow_tile(pt.t) || kc_forced) return {false, pt};
     const GemmPlan pd = plan_gemm(M, g.C, Kb, z, 1, true, kg);
-    if (pd.t.wr * pd.t.wc * pd.t.kg == 8 && pt.splits == 1 && !narrow_tile(pd.t)) return {true, pd};
+    const bool pd_ok = pd.t.wr * pd.t.wc * pd.t.kg == 8 && pt.splits == 1 && !kc_only(pd.t);
+    if (kc_only(pt.t)) {
+        // the 192-wide tile pays the transposed copy (read and write W once
+        // plus a launch); the in-place variant pays nothing extra
+        const double tr_us = 1.0 + 4.0 * (double)g.K * g.R * g.S * g.C / kBytesPerUs;
+        if (pd_ok && est_us(pd.t, M, g.C, Kb, z, 1) <= est_us(pt.t, M, g.C, Kb, z, pt.splits) + tr_us) return {true, pd};
+        return {false, pt};
+    }
+    if (pd_ok) return {true, pd};
     return {false, pt};
 }
 

@@ -14,7 +14,8 @@ from _gpu import check, dev, host
 
 pytestmark = pytest.mark.gpu
 
-TILES = ["256x256", "256x128", "128x128", "128x128w8", "128x128s4", "128x128w8s4", "128x128k2", "128x64", "256x32"]
+TILES = ["256x256", "256x128", "128x128", "128x128w8", "128x128s4", "128x128w8s4", "128x128k2", "128x64", "256x32",
+         "128x192k2"]
 
 CASES = [
     # x shape, w shape, stride, pad
