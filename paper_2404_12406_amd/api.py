@@ -6,8 +6,12 @@ memory (tensors the caller or this module allocates) and the stream.
     y, rec = layer_forward(Conv2d(stride=1, pad=1), x, W, b, mask=MASK_INPUT)
     gx, gW, gb = layer_backward(rec, grad_y)     # gW, gb are None here
 
-4-D activations and conv weights must be channels-last (torch.channels_last);
-2-D tensors row-major; 1-D tensors contiguous; dtypes float32 or bfloat16.
+4-D and 2-D tensors may have any strides: channels-last (torch.channels_last)
+activations and conv weights and row-major matrices are used in place, any
+other layout (NCHW, slices, transposed views) is staged by the library
+through transient workspace.  5-D tensors must be channels-last-3d, 1-D
+tensors contiguous; ReLU and dropout take any dense layout, with gradients
+in the layout of x.  dtypes float32 or bfloat16.
 """
 from __future__ import annotations
 
@@ -241,7 +245,8 @@ class Record:
             self._keep["W"] = W
         if bor & (MS_SAVED_MEAN | MS_SAVED_VAR):
             self._keep["stats"] = (desc.spec.running_mean, desc.spec.running_var)
-        self._x_meta = (tuple(x.shape), x.dtype, x.device)
+        self._x_meta = (tuple(x.shape), x.dtype, x.device, tuple(x.stride()))
+        self._elementwise = isinstance(desc.spec, (ReLU, Dropout))
         self._w_meta = (tuple(W.shape), W.dtype) if W is not None else None
         self._b_meta = (tuple(b.shape), b.dtype) if b is not None else None
         self.y_shape = y_shape
@@ -332,7 +337,7 @@ def layer_forward(spec, x: torch.Tensor, W: Optional[torch.Tensor] = None, b: Op
             raise TypeError("ReLU takes no W or b")
         _on_gpu(x, y)
         if y is None:
-            y = empty_like_layout(tuple(x.shape), x)
+            y = torch.empty_like(x)   # x's (dense) layout: the mask runs in memory order
         bits = relu_mask_buffer(x) if mask & MASK_INPUT else None
         h = _relu_forward(lib, x, y, bits, mask)
         if not h.value:
@@ -343,7 +348,7 @@ def layer_forward(spec, x: torch.Tensor, W: Optional[torch.Tensor] = None, b: Op
             raise TypeError("dropout takes no W or b")
         _on_gpu(x, y)
         if y is None:
-            y = empty_like_layout(tuple(x.shape), x)
+            y = torch.empty_like(x)   # x's (dense) layout: the mask runs in memory order
         h = _dropout_forward(lib, spec, x, y, mask)
         if not h.value:
             return y, None
@@ -372,7 +377,10 @@ def layer_backward(rec: Record, grad_y: torch.Tensor, grad_x: Optional[torch.Ten
     _on_gpu(grad_y, grad_x, grad_W, grad_b)
     m = rec.mask
     if m & MASK_INPUT and grad_x is None:
-        grad_x = empty_like_layout(rec._x_meta[0], grad_y)
+        if rec._elementwise:   # memory order: the gradient in x's layout
+            grad_x = torch.empty_strided(rec._x_meta[0], rec._x_meta[3], dtype=grad_y.dtype, device=grad_y.device)
+        else:
+            grad_x = empty_like_layout(rec._x_meta[0], grad_y)
     if m & MASK_WEIGHT and grad_W is None:
         grad_W = empty_like_layout(rec._w_meta[0], grad_y)
     if m & MASK_BIAS and grad_b is None:
@@ -446,7 +454,7 @@ class PreparedLayer:
         self.lib = _lib.load()
         self.desc = _LayerDesc(spec)
         if y is None:
-            y = empty_like_layout(output_shape(spec, x, W), x)
+            y = torch.empty_like(x) if isinstance(spec, (ReLU, Dropout)) else empty_like_layout(output_shape(spec, x, W), x)
         self.tensors = (x, W, b, y, grad_y, grad_x, grad_W, grad_b)
         self.y = y
         self.mask = int(mask)

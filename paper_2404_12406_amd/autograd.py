@@ -10,9 +10,14 @@ references to exactly the tensors the save rule borrows, so PyTorch's
 allocator retains what the ledger reports and nothing else.  Backward hands
 grad_y to ms_layer_backward and returns only the requested gradients.
 
-Layout: 4-D activations and conv weights are channels-last; the modules keep
-their weights that way and convert an input that is not (the converted copy
-is what a record would then borrow).  The 1-D layers run as the 2-D ones
+Layout: the 2-D layers take activations in any layout (NCHW, channels-last,
+strided views): the library stages what is not channels-last through
+transient workspace, and a record borrows the caller's own input.  The
+modules keep their weights channels-last (no staging) and return
+channels-last outputs, so only the first layer of a stack fed NCHW tensors
+pays the staging.  ReLU and dropout work in memory order and take any dense
+layout as it is.  The 3-D layers need channels-last-3d tensors and convert an
+input that is not (the converted copy is what a record then borrows).  The 1-D layers run as the 2-D ones
 with H = 1: their activations [N, C, L] and weights [K, C, R] are kept with
 the channel index innermost ([N][L][C], [K][R][C] in memory), so the 4-D
 views the library sees are channels-last without a copy.
@@ -37,6 +42,23 @@ def _cl(t: Optional[torch.Tensor]) -> Optional[torch.Tensor]:
         return t
     fmt = torch.channels_last if t.dim() == 4 else torch.channels_last_3d
     return t if t.is_contiguous(memory_format=fmt) else t.contiguous(memory_format=fmt)
+
+
+def _dense(t: torch.Tensor) -> torch.Tensor:
+    """t itself when its elements form one dense block (row-major or
+    channels-last), else a contiguous copy (for the elementwise layers)."""
+    if t.is_contiguous() or (t.dim() == 4 and t.is_contiguous(memory_format=torch.channels_last)):
+        return t
+    return t.contiguous()
+
+
+def _as_layout_of(g: torch.Tensor, like) -> torch.Tensor:
+    """g with the strides of a tensor of stride `like` (a copy only when they differ)."""
+    if g.stride() == tuple(like):
+        return g
+    out = torch.empty_strided(g.shape, like, dtype=g.dtype, device=g.device)
+    out.copy_(g)
+    return out
 
 
 def _mask(ctx, ix: int, iw: Optional[int] = None, ib: Optional[int] = None) -> int:
@@ -66,7 +88,8 @@ class _LayerFn(torch.autograd.Function):
         ctx.rec = None
         if rec is None:
             return None, None, None, None
-        gx, gw, gb = api.layer_backward(rec, _cl(grad_y.contiguous() if grad_y.dim() < 4 else grad_y))
+        gy = grad_y if grad_y.dim() in (2, 4) else _cl(grad_y.contiguous() if grad_y.dim() < 4 else grad_y)
+        gx, gw, gb = api.layer_backward(rec, gy)
         rec.free()
         return None, gx, gw, gb
 
@@ -76,6 +99,7 @@ class _ReLUFn(torch.autograd.Function):
     def forward(ctx, x):
         y, rec = api.layer_forward(api.ReLU(), x, mask=_mask(ctx, 0))
         ctx.rec = rec
+        ctx.stride = y.stride()
         return y
 
     @staticmethod
@@ -84,7 +108,7 @@ class _ReLUFn(torch.autograd.Function):
         ctx.rec = None
         if rec is None:
             return None
-        gx, _, _ = api.layer_backward(rec, _cl(grad_y.contiguous() if grad_y.dim() != 4 else grad_y))
+        gx, _, _ = api.layer_backward(rec, _as_layout_of(grad_y, ctx.stride))
         rec.free()
         return gx
 
@@ -94,6 +118,7 @@ class _DropoutFn(torch.autograd.Function):
     def forward(ctx, x, p, seed):
         y, rec = api.layer_forward(api.Dropout(p, seed, 0), x, mask=_mask(ctx, 0))
         ctx.rec = rec
+        ctx.stride = y.stride()
         return y
 
     @staticmethod
@@ -102,8 +127,7 @@ class _DropoutFn(torch.autograd.Function):
         ctx.rec = None
         if rec is None:
             return None, None, None
-        g = _cl(grad_y) if grad_y.dim() == 4 else grad_y.contiguous()
-        gx, _, _ = api.layer_backward(rec, g)
+        gx, _, _ = api.layer_backward(rec, _as_layout_of(grad_y, ctx.stride))
         rec.free()
         return gx, None, None
 
@@ -122,7 +146,7 @@ class MSConv2d(nn.Module):
         self.spec = api.Conv2d(stride, padding)
 
     def forward(self, x):
-        return _LayerFn.apply(self.spec, _cl(x), self.weight, self.bias)
+        return _LayerFn.apply(self.spec, x, self.weight, self.bias)
 
 
 class MSConvTranspose2d(nn.Module):
@@ -140,7 +164,7 @@ class MSConvTranspose2d(nn.Module):
         self.spec = api.ConvTranspose2d(stride, padding, output_padding)
 
     def forward(self, x):
-        return _LayerFn.apply(self.spec, _cl(x), self.weight, self.bias)
+        return _LayerFn.apply(self.spec, x, self.weight, self.bias)
 
 
 class _Conv3dBase(nn.Module):
@@ -226,7 +250,7 @@ class MSLinear(nn.Module):
 
     def forward(self, x):
         lead = x.shape[:-1]
-        y = _LayerFn.apply(self.spec, x.reshape(-1, x.shape[-1]).contiguous(), self.weight, self.bias)
+        y = _LayerFn.apply(self.spec, x.reshape(-1, x.shape[-1]), self.weight, self.bias)
         return y.reshape(*lead, y.shape[-1])
 
 
@@ -244,14 +268,14 @@ class MSBatchNorm2dEval(nn.Module):
 
     def forward(self, x):
         spec = api.BatchNormEval(self.running_mean, self.running_var, self.eps)
-        return _LayerFn.apply(spec, _cl(x), self.weight, self.bias)
+        return _LayerFn.apply(spec, x, self.weight, self.bias)
 
 
 class MSReLU(nn.Module):
     """ReLU whose backward keeps one bit per element (Sec. 2.2.2)."""
 
     def forward(self, x):
-        return _ReLUFn.apply(_cl(x) if x.dim() == 4 else x.contiguous())
+        return _ReLUFn.apply(_dense(x))
 
 
 class MSDropout(nn.Module):
@@ -259,8 +283,9 @@ class MSDropout(nn.Module):
     mask again in backward (Sec. 2.2.2).  In training mode each call takes a
     fresh 64-bit key from torch's default CPU generator (so torch.manual_seed
     makes runs repeatable; `last_seed` holds the key of the latest call); in
-    evaluation mode, or with p = 0, it is the identity.  Inputs other than
-    channels-last 4-D tensors are processed as one flat contiguous array."""
+    evaluation mode, or with p = 0, it is the identity.  A dense input (any
+    order of its dims) is used as it is, any other one through a contiguous
+    copy; the mask is drawn in memory order."""
 
     def __init__(self, p: float = 0.5):
         super().__init__()
@@ -274,10 +299,7 @@ class MSDropout(nn.Module):
             return x
         seed = int(torch.randint(0, 2 ** 63 - 1, (), dtype=torch.int64))
         self.last_seed = seed
-        if x.dim() == 4 and x.is_contiguous(memory_format=torch.channels_last):
-            return _DropoutFn.apply(x, self.p, seed)
-        flat = x.contiguous().view(-1)
-        return _DropoutFn.apply(flat, self.p, seed).view(x.shape)
+        return _DropoutFn.apply(_dense(x), self.p, seed)
 
 
 def _convertible_conv(m) -> bool:

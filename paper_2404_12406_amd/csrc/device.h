@@ -109,6 +109,13 @@ int launch_dropout(int dtype, const void *in, int64_t n, void *out, uint64_t see
 int launch_avgpool_fwd(int dtype, const void *x, int N, int L, int C, void *y, void *stream);
 int launch_avgpool_bwd(int dtype, const void *dy, int N, int L, int C, void *dx, void *stream);
 
+// dst[i] = src[i] over a 4-D index space of extents ext, each side with its
+// own element strides (layout.hip): the staging of a caller tensor into (or
+// out of) the dense layout the kernels read.  dst must not overlap itself
+// or src.
+int launch_copy4(int dtype, const void *src, const int64_t ext[4], const int64_t sstride[4], void *dst,
+                 const int64_t dstride[4], void *stream);
+
 // Per-stream transient workspace (workspace.hip).  Returns null and sets
 // *err on failure.
 void *workspace_get(void *stream, size_t bytes, int *err);

@@ -1,0 +1,134 @@
+// Strided copies between a caller's tensor layout and the dense
+// channels-last layout the layer kernels read (NHWC activations, KRSC
+// filters, row-major matrices).  A layer call whose tensors are in another
+// layout -- NCHW, a strided slice, a transposed view -- runs its kernels on
+// staged copies in transient workspace; the staging moves every byte once in
+// and once out, HBM-bound.
+//
+// A copy is described over a 4-D index space with each side's own element
+// strides.  When the unit-stride dimension of the destination differs from
+// the source's (NCHW <-> NHWC: w against c), 64 x 64 tiles over those two
+// dimensions pass through LDS, so that the reads run along the source's unit
+// stride and the writes along the destination's; the other two dimensions
+// index the tiles' batch.  Otherwise (the same fastest dimension on both
+// sides, e.g. a channel slice) elements are copied in the order of that
+// dimension, coalesced on both sides.
+#include "common.h"
+
+#include <algorithm>
+
+#include "../device.h"
+
+namespace ms {
+
+namespace {
+
+struct Copy4 {
+    int64_t ext[4];
+    int64_t ss[4], ds[4];
+    int ia, ib;        // tiled path: the destination's and the source's unit-stride dims
+    int o0, o1;        // tiled path: the batch dims (o1 varies fastest)
+    int64_t ta, tb;    // tiled path: tiles along ia and ib
+    int p[4];          // flat path: dims from fastest to slowest
+};
+
+constexpr int kT = 64;   // tile edge
+
+template <typename T>
+__global__ __launch_bounds__(256) void copy4_tiled_kernel(const T *__restrict__ src, T *__restrict__ dst, const Copy4 c) {
+    __shared__ T tile[kT][kT + 1];
+    int64_t blk = blockIdx.x;
+    const int64_t tbi = blk % c.tb;
+    blk /= c.tb;
+    const int64_t tai = blk % c.ta;
+    const int64_t bat = blk / c.ta;
+    const int64_t j1 = bat % c.ext[c.o1], j0 = bat / c.ext[c.o1];
+    const int64_t sbase = j0 * c.ss[c.o0] + j1 * c.ss[c.o1];
+    const int64_t dbase = j0 * c.ds[c.o0] + j1 * c.ds[c.o1];
+    const int64_t a0 = tai * kT, b0 = tbi * kT;
+    const int64_t ea = c.ext[c.ia], eb = c.ext[c.ib];
+    const int lx = threadIdx.x & (kT - 1), ly = threadIdx.x >> 6;
+    // read along the source's unit stride (lanes over b)
+    for (int r = ly; r < kT; r += 4) {
+        const int64_t a = a0 + r, b = b0 + lx;
+        if (a < ea && b < eb) tile[r][lx] = src[sbase + a * c.ss[c.ia] + b * c.ss[c.ib]];
+    }
+    __syncthreads();
+    // write along the destination's unit stride (lanes over a)
+    for (int r = ly; r < kT; r += 4) {
+        const int64_t a = a0 + lx, b = b0 + r;
+        if (a < ea && b < eb) dst[dbase + a * c.ds[c.ia] + b * c.ds[c.ib]] = tile[lx][r];
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void copy4_flat_kernel(const T *__restrict__ src, T *__restrict__ dst, const Copy4 c,
+                                                         int64_t total) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+        int64_t r = i, so = 0, dso = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int d = c.p[k];
+            const int64_t e = c.ext[d];
+            const int64_t idx = r % e;
+            r /= e;
+            so += idx * c.ss[d];
+            dso += idx * c.ds[d];
+        }
+        dst[dso] = src[so];
+    }
+}
+
+template <typename T>
+int copy4(const T *src, T *dst, Copy4 c, hipStream_t st) {
+    int64_t total = 1;
+    for (int d = 0; d < 4; ++d) total *= c.ext[d];
+    if (total == 0) return 0;
+    // unit-stride (smallest-stride) dims of each side among the dims that vary
+    int ia = -1, ib = -1;
+    for (int d = 0; d < 4; ++d) {
+        if (c.ext[d] <= 1) continue;
+        if (ia < 0 || c.ds[d] < c.ds[ia]) ia = d;
+        if (ib < 0 || c.ss[d] < c.ss[ib]) ib = d;
+    }
+    if (ia >= 0 && ib >= 0 && ia != ib && c.ext[ia] * c.ext[ib] >= 1024) {
+        c.ia = ia;
+        c.ib = ib;
+        int o[2], k = 0;
+        for (int d = 0; d < 4; ++d)
+            if (d != ia && d != ib) o[k++] = d;
+        // the batch's faster dim: the one with the smaller destination stride
+        c.o0 = c.ds[o[0]] >= c.ds[o[1]] ? o[0] : o[1];
+        c.o1 = c.o0 == o[0] ? o[1] : o[0];
+        c.ta = (c.ext[ia] + kT - 1) / kT;
+        c.tb = (c.ext[ib] + kT - 1) / kT;
+        const int64_t blocks = c.ta * c.tb * c.ext[c.o0] * c.ext[c.o1];
+        if (blocks > INT32_MAX) return (int)hipErrorInvalidValue;
+        hipLaunchKernelGGL(copy4_tiled_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, st, src, dst, c);
+        return (int)hipGetLastError();
+    }
+    // flat: destination's fastest dim first, the rest by decreasing stride order
+    int p[4] = {0, 1, 2, 3};
+    std::sort(p, p + 4, [&](int a, int b) { return c.ds[a] < c.ds[b] || (c.ds[a] == c.ds[b] && a > b); });
+    for (int k = 0; k < 4; ++k) c.p[k] = p[k];
+    const int blocks = (int)std::min<int64_t>((total + 255) / 256, 65536);
+    hipLaunchKernelGGL(copy4_flat_kernel<T>, dim3(blocks), dim3(256), 0, st, src, dst, c, total);
+    return (int)hipGetLastError();
+}
+
+}  // namespace
+
+int launch_copy4(int dtype, const void *src, const int64_t ext[4], const int64_t sstride[4], void *dst,
+                 const int64_t dstride[4], void *stream) {
+    Copy4 c{};
+    for (int d = 0; d < 4; ++d) {
+        c.ext[d] = ext[d];
+        c.ss[d] = sstride[d];
+        c.ds[d] = dstride[d];
+    }
+    hipStream_t st = (hipStream_t)stream;
+    return dtype == kBF16 ? copy4(static_cast<const bf16 *>(src), static_cast<bf16 *>(dst), c, st)
+                          : copy4(static_cast<const float *>(src), static_cast<float *>(dst), c, st);
+}
+
+}  // namespace ms

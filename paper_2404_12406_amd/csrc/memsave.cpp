@@ -132,6 +132,63 @@ bool is_rowmajor2(const ms_tensor *t) {
 
 bool is_contig1(const ms_tensor *t) { return t->shape[0] <= 1 || t->stride[0] == 1; }
 
+// Any layout of an input: strides of the varying dims must be >= 0.
+bool strides_ok(const ms_tensor *t) {
+    for (int i = 0; i < t->ndim; ++i)
+        if (t->shape[i] > 1 && t->stride[i] < 0) return false;
+    return true;
+}
+
+// No two elements share an address: with the varying dims sorted by stride,
+// each stride is at least the span of the faster ones (a strided sub-array
+// of a dense array).  Outputs must satisfy this.
+bool non_overlapping(const ms_tensor *t) {
+    if (!strides_ok(t)) return false;
+    if (numel(t) == 0) return true;
+    int d[5], k = 0;
+    for (int i = 0; i < t->ndim; ++i)
+        if (t->shape[i] > 1) d[k++] = i;
+    std::sort(d, d + k, [&](int a, int b) { return t->stride[a] < t->stride[b]; });
+    int64_t span = 1;
+    for (int i = 0; i < k; ++i) {
+        if (t->stride[d[i]] < span) return false;
+        span = t->stride[d[i]] * t->shape[d[i]];
+    }
+    return true;
+}
+
+// Every element of a dense block of numel(t) elements, in some order of the
+// dims (channels-last, NCHW, a transposed matrix, ...).
+bool dense_any_order(const ms_tensor *t) {
+    if (!non_overlapping(t)) return false;
+    if (numel(t) == 0) return true;
+    int64_t lo_span = 1;
+    int d[5], k = 0;
+    for (int i = 0; i < t->ndim; ++i)
+        if (t->shape[i] > 1) d[k++] = i;
+    std::sort(d, d + k, [&](int a, int b) { return t->stride[a] < t->stride[b]; });
+    for (int i = 0; i < k; ++i) {
+        if (t->stride[d[i]] != lo_span) return false;
+        lo_span *= t->shape[d[i]];
+    }
+    return true;
+}
+
+bool same_strides(const ms_tensor *a, const ms_tensor *b) {
+    for (int i = 0; i < a->ndim; ++i)
+        if (a->shape[i] > 1 && a->stride[i] != b->stride[i]) return false;
+    return true;
+}
+
+// The dense layout the kernels read and write: channels-last for 4-D
+// tensors (NHWC activations, KRSC filters), row-major for matrices.
+bool canonical(const ms_tensor *t) {
+    if (t->ndim == 4) return is_nhwc(t);
+    if (t->ndim == 2) return is_rowmajor2(t);
+    if (t->ndim == 5) return is_ndhwc(t);
+    return is_contig1(t);
+}
+
 bool same_shape(const ms_tensor *a, const ms_tensor *b) {
     if (a->ndim != b->ndim) return false;
     for (int i = 0; i < a->ndim; ++i)
@@ -160,21 +217,50 @@ struct Plan {
     int64_t n = 0;                           // ReLU / dropout: elements
     uint64_t bits_bytes = 0, y_bytes = 0;    // ReLU: 1-bit mask, output
     uint64_t mask8_bytes = 0;                // dropout: stock PyTorch's one-byte mask
+    // layouts that are not the kernels' (staged through transient workspace)
+    bool st_x = false, st_w = false, st_y = false;
+    uint64_t out_bytes = 0;                  // bytes of y
 };
+
+bool stageable(int32_t kind) {
+    return kind == MS_CONV2D || kind == MS_CONV_TRANSPOSE2D || kind == MS_LINEAR || kind == MS_BN_EVAL ||
+           kind == MS_AVGPOOL;
+}
+
+// Staging flags and the output size, once the kind's checks have passed.
+void plan_layouts(Plan *pl, const ms_tensor *x, const ms_tensor *W, const ms_tensor *y) {
+    if (!stageable(pl->kind)) return;
+    pl->st_x = !canonical(x);
+    pl->st_w = W && W->ndim >= 2 && !canonical(W);
+    pl->st_y = y && !canonical(y);
+    const uint64_t e = elt_size(pl->dtype);
+    switch (pl->kind) {
+    case MS_CONV2D: pl->out_bytes = (uint64_t)pl->g.N * pl->g.P * pl->g.Q * pl->g.K * e; break;
+    case MS_CONV_TRANSPOSE2D: pl->out_bytes = (uint64_t)pl->g.N * pl->g.H * pl->g.W * pl->g.C * e; break;
+    case MS_LINEAR: pl->out_bytes = (uint64_t)pl->g.N * pl->g.K * e; break;
+    case MS_BN_EVAL: pl->out_bytes = pl->x_bytes; break;
+    case MS_AVGPOOL: pl->out_bytes = (uint64_t)pl->Nb * pl->C * e; break;
+    }
+}
 
 uint64_t relu_mask_bytes(int64_t n) { return n > 0 ? (uint64_t)((n + 31) / 32) * 4u : 0u; }
 
-// Dense layouts an elementwise layer accepts: 1-D contiguous, 2-D row-major,
-// 4-D channels-last.
-bool dense_layout(const ms_tensor *t) {
-    if (t->ndim == 4) return is_nhwc(t);
-    if (t->ndim == 2) return is_rowmajor2(t);
-    return is_contig1(t);
-}
+
+ms_status validate_forward_kind(const ms_layer *layer, const ms_tensor *x, const ms_tensor *W,
+                                const ms_tensor *b, uint32_t mask, const ms_tensor *y, bool need_data,
+                                Plan *pl);
 
 ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_tensor *W,
                            const ms_tensor *b, uint32_t mask, const ms_tensor *y, bool need_data,
                            Plan *pl) {
+    const ms_status st = validate_forward_kind(layer, x, W, b, mask, y, need_data, pl);
+    if (st == MS_OK) plan_layouts(pl, x, W, y);
+    return st;
+}
+
+ms_status validate_forward_kind(const ms_layer *layer, const ms_tensor *x, const ms_tensor *W,
+                                const ms_tensor *b, uint32_t mask, const ms_tensor *y, bool need_data,
+                                Plan *pl) {
     if (!layer) return fail(MS_E_NULL, "layer is NULL");
     if (mask & ~7u) return fail(MS_E_MASK, "mask 0x%x has bits outside INPUT|WEIGHT|BIAS", mask);
     pl->kind = layer->kind;
@@ -189,8 +275,7 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
         if (!W) return fail(MS_E_NULL, "conv2d needs W");
         if ((st = check_tensor(W, "W", 4, need_data))) return st;
         if (x->dtype != W->dtype) return fail(MS_E_DTYPE, "x and W dtypes differ");
-        if (!is_nhwc(x)) return fail(MS_E_LAYOUT, "x must be channels-last (NHWC)");
-        if (!is_nhwc(W)) return fail(MS_E_LAYOUT, "W must be channels-last (KRSC)");
+        if (!strides_ok(x) || !strides_ok(W)) return fail(MS_E_LAYOUT, "x and W need non-negative strides");
         const int64_t N = x->shape[0], C = x->shape[1], H = x->shape[2], Wd = x->shape[3];
         const int64_t K = W->shape[0], R = W->shape[2], S = W->shape[3];
         if (W->shape[1] != C) return fail(MS_E_SHAPE, "W has %lld input channels, x has %lld",
@@ -215,7 +300,7 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
             if (y->shape[0] != N || y->shape[1] != K || y->shape[2] != P || y->shape[3] != Q)
                 return fail(MS_E_SHAPE, "y must be [%lld,%lld,%lld,%lld]", (long long)N, (long long)K,
                             (long long)P, (long long)Q);
-            if (!is_nhwc(y)) return fail(MS_E_LAYOUT, "y must be channels-last (NHWC)");
+            if (!non_overlapping(y)) return fail(MS_E_LAYOUT, "y must not overlap itself");
         }
         pl->dtype = x->dtype;
         pl->g = ms::ConvGeom{(int)N, (int)C, (int)H, (int)Wd, (int)K, (int)R, (int)S, (int)P, (int)Q,
@@ -231,8 +316,7 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
         if (!W) return fail(MS_E_NULL, "conv_transpose2d needs W");
         if ((st = check_tensor(W, "W", 4, need_data))) return st;
         if (x->dtype != W->dtype) return fail(MS_E_DTYPE, "x and W dtypes differ");
-        if (!is_nhwc(x)) return fail(MS_E_LAYOUT, "x must be channels-last (NHWC)");
-        if (!is_nhwc(W)) return fail(MS_E_LAYOUT, "W must be channels-last (memory [C_in][R][S][C_out])");
+        if (!strides_ok(x) || !strides_ok(W)) return fail(MS_E_LAYOUT, "x and W need non-negative strides");
         const int64_t N = x->shape[0], Ci = x->shape[1], H = x->shape[2], Wd = x->shape[3];
         const int64_t Co = W->shape[1], R = W->shape[2], S = W->shape[3];
         if (W->shape[0] != Ci) return fail(MS_E_SHAPE, "W has %lld input channels, x has %lld",
@@ -261,7 +345,7 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
             if (y->shape[0] != N || y->shape[1] != Co || y->shape[2] != Ho || y->shape[3] != Wo)
                 return fail(MS_E_SHAPE, "y must be [%lld,%lld,%lld,%lld]", (long long)N, (long long)Co,
                             (long long)Ho, (long long)Wo);
-            if (!is_nhwc(y)) return fail(MS_E_LAYOUT, "y must be channels-last (NHWC)");
+            if (!non_overlapping(y)) return fail(MS_E_LAYOUT, "y must not overlap itself");
         }
         if (capped_product({N, Ho, Wo, Co}) > kMaxElems)
             return fail(MS_E_UNSUPPORTED, "output has more than 2^31-1 elements");
@@ -363,8 +447,7 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
         if (!W) return fail(MS_E_NULL, "linear needs W");
         if ((st = check_tensor(W, "W", 2, need_data))) return st;
         if (x->dtype != W->dtype) return fail(MS_E_DTYPE, "x and W dtypes differ");
-        if (!is_rowmajor2(x)) return fail(MS_E_LAYOUT, "x must be row-major");
-        if (!is_rowmajor2(W)) return fail(MS_E_LAYOUT, "W must be row-major");
+        if (!strides_ok(x) || !strides_ok(W)) return fail(MS_E_LAYOUT, "x and W need non-negative strides");
         const int64_t M = x->shape[0], Kin = x->shape[1], Nout = W->shape[0];
         if (W->shape[1] != Kin) return fail(MS_E_SHAPE, "W has %lld input features, x has %lld",
                                             (long long)W->shape[1], (long long)Kin);
@@ -378,7 +461,7 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
             if ((st = check_tensor(y, "y", 2, need_data))) return st;
             if (y->dtype != x->dtype) return fail(MS_E_DTYPE, "y dtype differs from x");
             if (y->shape[0] != M || y->shape[1] != Nout) return fail(MS_E_SHAPE, "y must be [M, N_out]");
-            if (!is_rowmajor2(y)) return fail(MS_E_LAYOUT, "y must be row-major");
+            if (!non_overlapping(y)) return fail(MS_E_LAYOUT, "y must not overlap itself");
         }
         pl->dtype = x->dtype;
         pl->g = ms::ConvGeom{(int)M, (int)Kin, 1, 1, (int)Nout, 1, 1, 1, 1, 1, 1, 0, 0};
@@ -392,8 +475,7 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
         const int nd = x->ndim;
         if (nd != 2 && nd != 4) return fail(MS_E_SHAPE, "BN-eval x must be [N,C] or [N,C,H,W]");
         if ((st = check_tensor(x, "x", nd, need_data))) return st;
-        if (nd == 4 && !is_nhwc(x)) return fail(MS_E_LAYOUT, "x must be channels-last (NHWC)");
-        if (nd == 2 && !is_rowmajor2(x)) return fail(MS_E_LAYOUT, "x must be row-major");
+        if (!strides_ok(x)) return fail(MS_E_LAYOUT, "x needs non-negative strides");
         const int64_t C = x->shape[1];
         if (C < 1) return fail(MS_E_SHAPE, "BN-eval needs C >= 1");
         const ms_tensor *mean = layer->running_mean, *var = layer->running_var;
@@ -414,8 +496,7 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
             if ((st = check_tensor(y, "y", nd, need_data))) return st;
             if (y->dtype != x->dtype) return fail(MS_E_DTYPE, "y dtype differs from x");
             if (!same_shape(x, y)) return fail(MS_E_SHAPE, "y must have the shape of x");
-            if (nd == 4 && !is_nhwc(y)) return fail(MS_E_LAYOUT, "y must be channels-last (NHWC)");
-            if (nd == 2 && !is_rowmajor2(y)) return fail(MS_E_LAYOUT, "y must be row-major");
+            if (!non_overlapping(y)) return fail(MS_E_LAYOUT, "y must not overlap itself");
         }
         pl->dtype = x->dtype;
         pl->C = (int)C;
@@ -429,14 +510,14 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
         if (W || b) return fail(MS_E_ARG, "avgpool takes no W or b");
         if (mask & ~(uint32_t)MS_RG_INPUT) return fail(MS_E_MASK, "avgpool has no parameters");
         if ((st = check_tensor(x, "x", 4, need_data))) return st;
-        if (!is_nhwc(x)) return fail(MS_E_LAYOUT, "x must be channels-last (NHWC)");
+        if (!strides_ok(x)) return fail(MS_E_LAYOUT, "x needs non-negative strides");
         const int64_t N = x->shape[0], C = x->shape[1], L = x->shape[2] * x->shape[3];
         if (C < 1 || L < 1) return fail(MS_E_SHAPE, "avgpool needs C, H, W >= 1");
         if (y) {
             if ((st = check_tensor(y, "y", 2, need_data))) return st;
             if (y->dtype != x->dtype) return fail(MS_E_DTYPE, "y dtype differs from x");
             if (y->shape[0] != N || y->shape[1] != C) return fail(MS_E_SHAPE, "y must be [N, C]");
-            if (!is_rowmajor2(y)) return fail(MS_E_LAYOUT, "y must be row-major");
+            if (!non_overlapping(y)) return fail(MS_E_LAYOUT, "y must not overlap itself");
         }
         pl->dtype = x->dtype;
         pl->C = (int)C;
@@ -455,12 +536,12 @@ ms_status validate_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
         const int nd = x->ndim;
         if (nd != 1 && nd != 2 && nd != 4) return fail(MS_E_SHAPE, "%s x must have 1, 2 or 4 dims", nm);
         if ((st = check_tensor(x, "x", nd, need_data))) return st;
-        if (!dense_layout(x)) return fail(MS_E_LAYOUT, "x must be contiguous, row-major or channels-last");
+        if (!dense_any_order(x)) return fail(MS_E_LAYOUT, "x must be dense (any order of its dims)");
         if (y) {
             if ((st = check_tensor(y, "y", nd, need_data))) return st;
             if (y->dtype != x->dtype) return fail(MS_E_DTYPE, "y dtype differs from x");
             if (!same_shape(x, y)) return fail(MS_E_SHAPE, "y must have the shape of x");
-            if (!dense_layout(y)) return fail(MS_E_LAYOUT, "y must be in the layout of x");
+            if (!dense_any_order(y) || !same_strides(x, y)) return fail(MS_E_LAYOUT, "y must be in the layout of x");
         }
         pl->dtype = x->dtype;
         pl->n = numel(x);
@@ -544,6 +625,8 @@ size_t backward_workspace(const Plan &pl, uint32_t kernels) {
     return ws;
 }
 
+uint64_t backward_staging(const Plan &pl, uint32_t kernels);
+
 ms_account make_account(const Plan &pl, uint32_t mask, uint32_t borrowed, uint32_t kernels) {
     ms_account a{};
     a.mask = mask;
@@ -558,12 +641,81 @@ ms_account make_account(const Plan &pl, uint32_t mask, uint32_t borrowed, uint32
     if (borrowed & MS_SAVED_MEAN) pb += pl.stat_bytes;
     if (borrowed & MS_SAVED_VAR) pb += pl.stat_bytes;
     a.referenced_param_bytes = pb;
-    a.transient_workspace_bytes = backward_workspace(pl, kernels);
+    a.transient_workspace_bytes = backward_workspace(pl, kernels) + backward_staging(pl, kernels);
     return a;
 }
 
 ms_status hip_fail(int err, const char *what) {
     return fail(MS_E_HIP, "%s failed with HIP error %d", what, err);
+}
+
+// ------------------------------------------------------------------ layout staging
+// A caller tensor that is not in the kernels' layout (NCHW, a strided
+// slice, a transposed matrix) is copied into a dense channels-last (or
+// row-major) stand-in in transient workspace before the launch, and an
+// output is written to such a stand-in and copied out after it.  The record
+// still borrows the caller's own tensor.
+constexpr size_t kNoStage = ~size_t(0);
+
+size_t al256(size_t n) { return (n + 255) / 256 * 256; }
+
+struct Stager {
+    size_t bytes = 0;
+    // Offset of t's stand-in, or kNoStage when t is used in place.
+    size_t add(const ms_tensor *t) {
+        if (!t || !t->data || numel(t) == 0 || canonical(t)) return kNoStage;
+        const size_t off = bytes;
+        bytes += al256((size_t)numel(t) * elt_size(t->dtype));
+        return off;
+    }
+};
+
+// The copy between t's layout and its dense stand-in, over (n, h, w, c) for
+// 4-D tensors and (m, -, -, k) for matrices.
+void copy_desc(const ms_tensor *t, int64_t ext[4], int64_t s[4], int64_t dense[4]) {
+    if (t->ndim == 4) {
+        const int64_t N = t->shape[0], C = t->shape[1], H = t->shape[2], W = t->shape[3];
+        const int64_t e[4] = {N, H, W, C}, st[4] = {t->stride[0], t->stride[2], t->stride[3], t->stride[1]},
+                      d[4] = {H * W * C, W * C, C, 1};
+        for (int i = 0; i < 4; ++i) ext[i] = e[i], s[i] = st[i], dense[i] = d[i];
+    } else {
+        const int64_t e[4] = {t->shape[0], 1, 1, t->shape[1]}, st[4] = {t->stride[0], 0, 0, t->stride[1]},
+                      d[4] = {t->shape[1], 0, 0, 1};
+        for (int i = 0; i < 4; ++i) ext[i] = e[i], s[i] = st[i], dense[i] = d[i];
+    }
+}
+
+int stage_in(const ms_tensor *t, char *base, size_t off, void *stream) {
+    if (off == kNoStage) return 0;
+    int64_t ext[4], s[4], d[4];
+    copy_desc(t, ext, s, d);
+    return ms::launch_copy4(t->dtype, t->data, ext, s, base + off, d, stream);
+}
+
+int stage_out(const ms_tensor *t, char *base, size_t off, void *stream) {
+    if (off == kNoStage) return 0;
+    int64_t ext[4], s[4], d[4];
+    copy_desc(t, ext, s, d);
+    return ms::launch_copy4(t->dtype, base + off, ext, d, t->data, s, stream);
+}
+
+// Data pointer the kernels use for t: its stand-in or the caller's memory.
+void *kptr(const ms_tensor *t, char *base, size_t off) {
+    if (!t) return nullptr;
+    return off == kNoStage ? t->data : base + off;
+}
+
+// Staging bytes a backward with `kernels` needs, taking the output
+// gradient in y's layout and the input and weight gradients in x's and W's.
+uint64_t backward_staging(const Plan &pl, uint32_t kernels) {
+    if (!stageable(pl.kind)) return 0;
+    const bool wg = kernels & MS_K_WGRAD, dg = kernels & MS_K_DGRAD;
+    uint64_t b = pl.st_y ? al256(pl.out_bytes) : 0;               // grad_y
+    if (pl.st_x && wg && pl.kind != MS_AVGPOOL) b += al256(pl.x_bytes);   // x read by the weight gradient
+    if (pl.st_w && dg) b += al256(pl.w_bytes);                      // W read by the input gradient
+    if (pl.st_x && dg) b += al256(pl.x_bytes);                      // grad_x
+    if (pl.st_w && wg) b += al256(pl.w_bytes);                      // grad_W
+    return b;
 }
 
 }  // namespace
@@ -597,16 +749,19 @@ void release(ms_record *r) {
     }
 }
 
-ms_status check_grad(const ms_tensor *g, const ms_tensor *primal, const char *name, int32_t kind) {
+ms_status check_grad(const ms_tensor *g, const ms_tensor *primal, const char *name, int32_t kind, bool output) {
     ms_status st = check_tensor(g, name, primal->ndim, true);
     if (st) return st;
     if (g->dtype != primal->dtype) return fail(MS_E_DTYPE, "%s dtype must match its primal", name);
     if (!same_shape(g, primal)) return fail(MS_E_SHAPE, "%s shape must match its primal", name);
-    if (g->ndim == 4 && !is_nhwc(g)) return fail(MS_E_LAYOUT, "%s must be channels-last", name);
     if (g->ndim == 5 && !is_ndhwc(g)) return fail(MS_E_LAYOUT, "%s must be channels-last", name);
-    if (g->ndim == 2 && !is_rowmajor2(g)) return fail(MS_E_LAYOUT, "%s must be row-major", name);
     if (g->ndim == 1 && !is_contig1(g)) return fail(MS_E_LAYOUT, "%s must be contiguous", name);
-    (void)kind;
+    if (kind == MS_RELU || kind == MS_DROPOUT) {
+        // elementwise in memory order: the layout of the forward's tensors
+        if (!dense_any_order(g) || !same_strides(g, primal)) return fail(MS_E_LAYOUT, "%s must be in the layout of x", name);
+    } else if (output ? !non_overlapping(g) : !strides_ok(g)) {
+        return fail(MS_E_LAYOUT, output ? "%s must not overlap itself" : "%s needs non-negative strides", name);
+    }
     return MS_OK;
 }
 
@@ -628,36 +783,44 @@ ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
     if (st) return st;
     const uint32_t borrowed = borrowed_bits(pl.kind, mask, MS_POLICY_SELECTIVE, pl.has_w, pl.has_b);
     const uint32_t kernels = kernel_bits(pl.kind, mask);
-    // transient forward workspace (zero-padded channel copies for channel
-    // counts that are not a multiple of 8), taken before anything is launched
-    void *fws = nullptr;
+    // transient forward workspace: stand-ins of tensors in other layouts,
+    // then the kernels' own (zero-padded channel copies for channel counts
+    // that are not a multiple of 8), taken before anything is launched
+    Stager sg;
+    const size_t ox = stageable(pl.kind) ? sg.add(x) : kNoStage;
+    const size_t ow = stageable(pl.kind) && W && W->ndim >= 2 ? sg.add(W) : kNoStage;
+    const size_t oy = stageable(pl.kind) ? sg.add(y) : kNoStage;
+    size_t fb = 0;
     if (pl.kind == MS_CONV2D || pl.kind == MS_LINEAR || pl.kind == MS_CONV_TRANSPOSE2D || pl.kind == MS_CONV3D ||
-        pl.kind == MS_CONV_TRANSPOSE3D) {
-        const size_t fb = pl.kind == MS_CONV_TRANSPOSE2D    ? ms::conv_dgrad_workspace(pl.dtype, pl.g)
-                          : pl.kind == MS_CONV3D            ? ms::conv3d_fwd_workspace(pl.dtype, pl.q)
-                          : pl.kind == MS_CONV_TRANSPOSE3D ? ms::conv3d_dgrad_workspace(pl.dtype, pl.q)
-                                                            : ms::conv_fwd_workspace(pl.dtype, pl.g);
-        if (fb) {
-            int werr = 0;
-            fws = ms::workspace_get(stream, fb, &werr);
-            if (!fws) return werr == 1 ? fail(MS_E_NOMEM, "workspace of %zu bytes unavailable", fb)
-                                       : hip_fail(ms::device_last_error(), "workspace");
-        }
+        pl.kind == MS_CONV_TRANSPOSE3D)
+        fb = pl.kind == MS_CONV_TRANSPOSE2D    ? ms::conv_dgrad_workspace(pl.dtype, pl.g)
+             : pl.kind == MS_CONV3D            ? ms::conv3d_fwd_workspace(pl.dtype, pl.q)
+             : pl.kind == MS_CONV_TRANSPOSE3D ? ms::conv3d_dgrad_workspace(pl.dtype, pl.q)
+                                               : ms::conv_fwd_workspace(pl.dtype, pl.g);
+    char *base = nullptr;
+    if (sg.bytes + fb) {
+        int werr = 0;
+        base = static_cast<char *>(ms::workspace_get(stream, sg.bytes + fb, &werr));
+        if (!base) return werr == 1 ? fail(MS_E_NOMEM, "workspace of %zu bytes unavailable", sg.bytes + fb)
+                                    : hip_fail(ms::device_last_error(), "workspace");
     }
+    void *fws = fb ? base + sg.bytes : nullptr;
     ms_record *r = nullptr;
     if (mask != 0) {
         r = new (std::nothrow) ms_record();
         if (!r) return fail(MS_E_NOMEM, "record allocation failed");
     }
-    int err = 0;
-    switch (pl.kind) {
+    int err = stage_in(x, base, ox, stream);
+    if (!err && ow != kNoStage) err = stage_in(W, base, ow, stream);
+    const void *xk = kptr(x, base, ox), *wk = ow != kNoStage ? base + ow : (W ? W->data : nullptr);
+    void *yk = kptr(y, base, oy);
+    if (!err) switch (pl.kind) {
     case MS_CONV2D:
     case MS_LINEAR:
-        err = ms::launch_conv_fwd(pl.dtype, pl.g, x->data, W->data, b ? b->data : nullptr, y->data, fws, stream);
+        err = ms::launch_conv_fwd(pl.dtype, pl.g, xk, wk, b ? b->data : nullptr, yk, fws, stream);
         break;
     case MS_CONV_TRANSPOSE2D:   // the input-gradient contraction of the convolution y -> x, plus b
-        err = ms::launch_conv_dgrad(pl.dtype, pl.g, x->data, W->data, b ? b->data : nullptr, y->data, fws,
-                                    stream);
+        err = ms::launch_conv_dgrad(pl.dtype, pl.g, xk, wk, b ? b->data : nullptr, yk, fws, stream);
         break;
     case MS_CONV3D:
         err = ms::launch_conv3d_fwd(pl.dtype, pl.q, x->data, W->data, b ? b->data : nullptr, y->data, fws, stream);
@@ -666,14 +829,14 @@ ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
         err = ms::launch_conv3d_dgrad(pl.dtype, pl.q, x->data, W->data, b ? b->data : nullptr, y->data, fws, stream);
         break;
     case MS_BN_EVAL:
-        err = ms::launch_bn_fwd(pl.dtype, x->data, layer->running_mean->data, layer->running_var->data,
-                                W ? W->data : nullptr, b ? b->data : nullptr, layer->eps, pl.rows, pl.C,
-                                y->data, stream);
+        err = ms::launch_bn_fwd(pl.dtype, xk, layer->running_mean->data, layer->running_var->data,
+                                W ? W->data : nullptr, b ? b->data : nullptr, layer->eps, pl.rows, pl.C, yk, stream);
         break;
     case MS_AVGPOOL:
-        err = ms::launch_avgpool_fwd(pl.dtype, x->data, pl.Nb, pl.L, pl.C, y->data, stream);
+        err = ms::launch_avgpool_fwd(pl.dtype, xk, pl.Nb, pl.L, pl.C, yk, stream);
         break;
     }
+    if (!err) err = stage_out(y, base, oy, stream);
     if (err) {
         delete r;
         return hip_fail(err, "forward launch");
@@ -730,30 +893,47 @@ ms_status backward_impl(ms_record *r, const ms_tensor *grad_y, const ms_tensor *
         return fail(MS_E_MASK, "grad_W must be given exactly when the WEIGHT bit is set");
     if ((grad_b != nullptr) != bool(mask & MS_RG_BIAS))
         return fail(MS_E_MASK, "grad_b must be given exactly when the BIAS bit is set");
-    ms_status st = check_grad(grad_y, &r->y, "grad_y", pl.kind);
+    ms_status st = check_grad(grad_y, &r->y, "grad_y", pl.kind, false);
     if (st) return st;
-    if (grad_x && (st = check_grad(grad_x, &r->x, "grad_x", pl.kind))) return st;
-    if (grad_W && (st = check_grad(grad_W, &r->W, "grad_W", pl.kind))) return st;
-    if (grad_b && (st = check_grad(grad_b, &r->b, "grad_b", pl.kind))) return st;
+    if (grad_x && (st = check_grad(grad_x, &r->x, "grad_x", pl.kind, true))) return st;
+    if (grad_W && (st = check_grad(grad_W, &r->W, "grad_W", pl.kind, true))) return st;
+    if (grad_b && (st = check_grad(grad_b, &r->b, "grad_b", pl.kind, true))) return st;
 
     const uint32_t kernels = r->acct.kernels;
-    void *ws = nullptr;
-    const size_t ws_bytes = backward_workspace(pl, kernels);
+    // stand-ins of tensors in other layouts, then the kernels' workspace
+    Stager sg;
+    const bool stg = stageable(pl.kind);
+    const bool x_read = (kernels & MS_K_WGRAD) && pl.kind != MS_AVGPOOL;   // weight gradient (BN: dgamma)
+    const bool w_read = (kernels & MS_K_DGRAD) && pl.kind != MS_BN_EVAL && pl.kind != MS_AVGPOOL;
+    const size_t ody = stg ? sg.add(grad_y) : kNoStage;
+    const size_t ox = stg && x_read ? sg.add(&r->x) : kNoStage;
+    const size_t ow = stg && w_read ? sg.add(&r->W) : kNoStage;
+    const size_t ogx = stg && grad_x ? sg.add(grad_x) : kNoStage;
+    const size_t ogw = stg && grad_W && grad_W->ndim >= 2 ? sg.add(grad_W) : kNoStage;
+    const size_t kb = backward_workspace(pl, kernels);
+    const size_t ws_bytes = sg.bytes + kb;
+    char *base = nullptr;
     if (ws_bytes && fixed_scratch) {
         int werr = 0;
-        ws = ms::scratch_get(ws_bytes, &werr);
-        if (!ws) return werr == 1 ? fail(MS_E_UNSUPPORTED, "backward needs %zu bytes of scratch; the fixed scratch "
-                                                           "holds %zu", ws_bytes, ms::kScratchBytes)
-                                  : hip_fail(ms::device_last_error(), "scratch lookup");
+        base = static_cast<char *>(ms::scratch_get(ws_bytes, &werr));
+        if (!base) return werr == 1 ? fail(MS_E_UNSUPPORTED, "backward needs %zu bytes of scratch; the fixed scratch "
+                                                             "holds %zu", ws_bytes, ms::kScratchBytes)
+                                    : hip_fail(ms::device_last_error(), "scratch lookup");
     } else if (ws_bytes) {
         int werr = 0;
-        ws = ms::workspace_get(stream, ws_bytes, &werr);
-        if (!ws) return werr == 1 ? fail(MS_E_NOMEM, "workspace of %zu bytes unavailable", ws_bytes)
-                                  : hip_fail(ms::device_last_error(), "workspace");
+        base = static_cast<char *>(ms::workspace_get(stream, ws_bytes, &werr));
+        if (!base) return werr == 1 ? fail(MS_E_NOMEM, "workspace of %zu bytes unavailable", ws_bytes)
+                                    : hip_fail(ms::device_last_error(), "workspace");
     }
-    int err = 0;
-    const void *dy = grad_y->data;
-    switch (pl.kind) {
+    void *ws = kb ? base + sg.bytes : nullptr;
+    int err = stage_in(grad_y, base, ody, stream);
+    if (!err) err = stage_in(&r->x, base, ox, stream);
+    if (!err) err = stage_in(&r->W, base, ow, stream);
+    const void *dy = kptr(grad_y, base, ody);
+    const void *xk = ox != kNoStage ? base + ox : r->x.data;
+    const void *wk = ow != kNoStage ? base + ow : r->W.data;
+    void *gx = kptr(grad_x, base, ogx), *gw = kptr(grad_W, base, ogw);
+    if (!err) switch (pl.kind) {
     case MS_CONV2D:
     case MS_LINEAR:
     {
@@ -762,11 +942,10 @@ ms_status backward_impl(ms_record *r, const ms_tensor *grad_y, const ms_tensor *
         bool db_done = false;
         void *db_dgrad = (kernels & MS_K_BGRAD) && !(kernels & MS_K_WGRAD) ? grad_b->data : nullptr;
         if (!err && (kernels & MS_K_DGRAD))
-            err = ms::launch_conv_dgrad(pl.dtype, pl.g, dy, r->W.data, nullptr, grad_x->data, ws, stream, db_dgrad,
-                                        &db_done);
+            err = ms::launch_conv_dgrad(pl.dtype, pl.g, dy, wk, nullptr, gx, ws, stream, db_dgrad, &db_done);
         if (!err && (kernels & MS_K_WGRAD))
-            err = ms::launch_conv_wgrad(pl.dtype, pl.g, dy, r->x.data, grad_W->data,
-                                        (kernels & MS_K_BGRAD) ? grad_b->data : nullptr, ws, stream, &db_done);
+            err = ms::launch_conv_wgrad(pl.dtype, pl.g, dy, xk, gw, (kernels & MS_K_BGRAD) ? grad_b->data : nullptr, ws,
+                                        stream, &db_done);
         if (!err && (kernels & MS_K_BGRAD) && !db_done)
             err = ms::launch_colsum(pl.dtype, dy, pl.rows, pl.g.K, grad_b->data, ws, stream);
     }
@@ -777,10 +956,9 @@ ms_status backward_impl(ms_record *r, const ms_tensor *grad_y, const ms_tensor *
         // input gradient is g's forward of grad_y; the weight gradient is g's
         // weight gradient with x as its output gradient and grad_y as its input
         bool db_unused = false;
-        if (kernels & MS_K_DGRAD)
-            err = ms::launch_conv_fwd(pl.dtype, pl.g, dy, r->W.data, nullptr, grad_x->data, ws, stream);
+        if (kernels & MS_K_DGRAD) err = ms::launch_conv_fwd(pl.dtype, pl.g, dy, wk, nullptr, gx, ws, stream);
         if (!err && (kernels & MS_K_WGRAD))
-            err = ms::launch_conv_wgrad(pl.dtype, pl.g, r->x.data, dy, grad_W->data, nullptr, ws, stream, &db_unused);
+            err = ms::launch_conv_wgrad(pl.dtype, pl.g, xk, dy, gw, nullptr, ws, stream, &db_unused);
         if (!err && (kernels & MS_K_BGRAD))
             err = ms::launch_colsum(pl.dtype, dy, pl.rows, pl.g.C, grad_b->data, ws, stream);
     }
@@ -810,14 +988,13 @@ ms_status backward_impl(ms_record *r, const ms_tensor *grad_y, const ms_tensor *
     }
         break;
     case MS_BN_EVAL:
-        err = ms::launch_bn_bwd(pl.dtype, dy, (kernels & MS_K_WGRAD) ? r->x.data : nullptr,
+        err = ms::launch_bn_bwd(pl.dtype, dy, (kernels & MS_K_WGRAD) ? xk : nullptr,
                                 (kernels & MS_K_WGRAD) ? r->mean.data : nullptr, r->var.data,
                                 (kernels & MS_K_DGRAD) ? r->W.data : nullptr, r->eps, pl.rows, pl.C,
-                                grad_x ? grad_x->data : nullptr, grad_W ? grad_W->data : nullptr,
-                                grad_b ? grad_b->data : nullptr, ws, stream);
+                                gx, grad_W ? grad_W->data : nullptr, grad_b ? grad_b->data : nullptr, ws, stream);
         break;
     case MS_AVGPOOL:
-        if (kernels & MS_K_DGRAD) err = ms::launch_avgpool_bwd(pl.dtype, dy, pl.Nb, pl.L, pl.C, grad_x->data, stream);
+        if (kernels & MS_K_DGRAD) err = ms::launch_avgpool_bwd(pl.dtype, dy, pl.Nb, pl.L, pl.C, gx, stream);
         break;
     case MS_RELU:
         if (kernels & MS_K_DGRAD) err = ms::launch_relu_bwd(pl.dtype, dy, r->bits, pl.n, grad_x->data, stream);
@@ -828,6 +1005,8 @@ ms_status backward_impl(ms_record *r, const ms_tensor *grad_y, const ms_tensor *
                                      r->drop_all, stream);
         break;
     }
+    if (!err) err = stage_out(grad_x, base, ogx, stream);
+    if (!err) err = stage_out(grad_W, base, ogw, stream);
     if (err) return hip_fail(err, "backward launch");
     r->consumed = true;
     release(r);

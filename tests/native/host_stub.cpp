@@ -214,6 +214,12 @@ void workspace_fail_next(int n) {
     g_fail_next = n;
 }
 
+int launch_copy4(int, const void *src, const int64_t ext[4], const int64_t *, void *dst, const int64_t *, void *) {
+    log("copy4");
+    const long long n = (long long)ext[0] * ext[1] * ext[2] * ext[3];
+    return n > 0 ? need(src && dst, "copy4:src,dst") : 0;
+}
+
 // the stub launchers never dereference workspace: any distinct non-null
 // address stands in for the fixed scratch array
 void *scratch_get(size_t bytes, int *err) {

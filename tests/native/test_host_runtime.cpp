@@ -99,8 +99,11 @@ int main() {
     CHECK(ms_layer_forward(&conv, &x, &W, &b, 9, &y, &r, nullptr) == MS_E_MASK);
     CHECK(ms_layer_forward(&conv, &x, &W, &b, 1, &y, nullptr, nullptr) == MS_E_NULL);
     ms_tensor xbad = x;
-    xbad.stride[1] = 28 * 28;
+    xbad.stride[1] = -1;   // any layout is staged, but strides must not be negative
     CHECK(ms_layer_forward(&conv, &xbad, &W, &b, 1, &y, &r, nullptr) == MS_E_LAYOUT);
+    ms_tensor ybad = y;
+    ybad.stride[2] = 0;    // an output may not overlap itself
+    CHECK(ms_layer_forward(&conv, &x, &W, &b, 1, &ybad, &r, nullptr) == MS_E_LAYOUT);
     CHECK(ms_layer_backward(nullptr, &y, nullptr, nullptr, nullptr, nullptr) == MS_E_NULL);
     ms_account acct;
     CHECK(ms_policy_account(&conv, &x, &W, &b, 1, 7, &acct) == MS_E_ARG);

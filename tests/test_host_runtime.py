@@ -266,7 +266,8 @@ def test_backward_rejects_grad_sets_that_contradict_the_mask(stub):
         if gx is not None:
             bad = tdesc((1, 2, 3, 4))
             assert stub.ms_layer_backward(h, ref(gy), ref(bad), ref(gw), ref(gb), None) == L.MS_E_SHAPE
-            badl = tdesc(spec.in_shape, layout="nchw")
+            badl = tdesc(spec.in_shape)
+            badl.stride[2] = 0                             # rows of dx would share memory
             assert stub.ms_layer_backward(h, ref(gy), ref(badl), ref(gw), ref(gb), None) == L.MS_E_LAYOUT
             badd = tdesc(spec.in_shape, "f32")
             assert stub.ms_layer_backward(h, ref(gy), ref(badd), ref(gw), ref(gb), None) == L.MS_E_DTYPE
@@ -291,7 +292,12 @@ def test_forward_validation_errors_launch_nothing(stub):
     assert fwd(a, 8) == L.MS_E_MASK
     assert fwd(a, 2, W=None) == L.MS_E_MASK
     assert fwd(a, 4, b=None) == L.MS_E_MASK
-    assert fwd(a, 1, x=tdesc(spec.in_shape, layout="nchw")) == L.MS_E_LAYOUT
+    negx = tdesc(spec.in_shape)
+    negx.stride[3] = -negx.stride[3]
+    assert fwd(a, 1, x=negx) == L.MS_E_LAYOUT
+    ovy = tdesc(spec.out_shape())
+    ovy.stride[0] = 1                                  # images would overlap
+    assert fwd(a, 1, y=ovy) == L.MS_E_LAYOUT
     assert fwd(a, 1, x=tdesc(spec.in_shape, "f32")) == L.MS_E_DTYPE
     assert fwd(a, 1, x=tdesc((32, 128, 28, 28))) == L.MS_E_SHAPE
     assert fwd(a, 1, y=tdesc((32, 256, 27, 28))) == L.MS_E_SHAPE
@@ -314,6 +320,101 @@ def test_forward_validation_errors_launch_nothing(stub):
     live = ctypes.c_uint64()
     stub.ms_ledger_read(ctypes.byref(live), ctypes.byref(pk))
     assert live.value == live0.value
+
+
+def _nchw(shape, dtype="bf16"):
+    return tdesc(shape, dtype, layout="nchw")
+
+
+def test_tensors_in_other_layouts_are_staged_around_the_kernels(stub):
+    """NCHW (any strides) at the boundary: every 4-D tensor that is not
+    channels-last, and every matrix that is not row-major, is copied into a
+    dense stand-in before the kernels run and copied out after them; the
+    record still borrows the caller's own x, so its bytes are unchanged, and
+    the accounting counts the stand-ins as transient workspace."""
+    spec = wl.conv_sweep_bf16("11").layers[0]
+    a = LayerArgs(spec, "bf16")
+    xn, wn, yn = _nchw(spec.in_shape), _nchw(spec.weight_shape()), _nchw(spec.out_shape())
+    for mask in range(8):
+        h = ctypes.c_void_p()
+        stub.stub_reset()
+        assert stub.ms_layer_forward(ctypes.byref(a.layer), ref(xn), ref(wn), ref(a.b), mask, ref(yn),
+                                     ctypes.byref(h), None) == 0, stub.ms_last_error()
+        assert stub.stub_log().decode() == "copy4;copy4;conv_fwd;copy4;"
+        if mask == 0:
+            continue
+        acct = L.MsAccount()
+        stub.ms_record_account(h, ctypes.byref(acct))
+        assert acct.saved_activation_bytes == P.saved_activation_bytes("conv2d", mask, _numel(spec.in_shape), "bf16")
+        hc = ctypes.c_void_p()
+        assert stub.ms_layer_forward(ctypes.byref(a.layer), ref(a.x), ref(a.W), ref(a.b), mask, ref(a.y),
+                                     ctypes.byref(hc), None) == 0
+        accc = L.MsAccount()
+        stub.ms_record_account(hc, ctypes.byref(accc))
+        e = 2
+        stage = (_numel(spec.out_shape()) * e                                    # grad_y
+                 + ((mask >> 1) & 1) * (_numel(spec.in_shape) * e)                # x for the weight gradient
+                 + (mask & 1) * (_numel(spec.weight_shape()) * e)                 # W for the input gradient
+                 + (mask & 1) * (_numel(spec.in_shape) * e)                       # grad_x
+                 + ((mask >> 1) & 1) * (_numel(spec.weight_shape()) * e))         # grad_W
+        assert acct.transient_workspace_bytes - accc.transient_workspace_bytes == stage, mask
+        stub.ms_record_free(hc)
+        gy = _nchw(spec.out_shape())
+        gx = _nchw(spec.in_shape) if mask & 1 else None
+        gw = _nchw(spec.weight_shape()) if mask & 2 else None
+        gb = tdesc((spec.out_ch,)) if mask & 4 else None
+        stub.stub_reset()
+        assert stub.ms_layer_backward(h, ref(gy), ref(gx), ref(gw), ref(gb), None) == 0, stub.ms_last_error()
+        assert stub.stub_violations().decode() == ""
+        log = stub.stub_log().decode().split(";")[:-1]
+        n_in = 1 + ((mask >> 1) & 1) + (mask & 1)          # grad_y, x, W
+        n_out = (mask & 1) + ((mask >> 1) & 1)             # grad_x, grad_W
+        assert log[:n_in] == ["copy4"] * n_in and log[len(log) - n_out:] == ["copy4"] * n_out, log
+        assert "copy4" not in log[n_in:len(log) - n_out]
+        stub.ms_record_free(h)
+    # a transposed matrix (Linear input [M, K] stored as K x M), BN-eval in NCHW
+    lin = LayerArgs(wl.linear_stack_bf16(m=256).layers[0], "bf16")
+    xt = tdesc((256, 1024))
+    xt.stride[0], xt.stride[1] = 1, 256
+    h = ctypes.c_void_p()
+    stub.stub_reset()
+    assert stub.ms_layer_forward(ctypes.byref(lin.layer), ref(xt), ref(lin.W), ref(lin.b), 5, ref(lin.y),
+                                 ctypes.byref(h), None) == 0
+    assert stub.stub_log().decode() == "copy4;conv_fwd;"
+    stub.ms_record_free(h)
+    bn = LayerArgs(wl.resnet18_shaped_bf16(batch=2, image=32).layers[1], "bf16")
+    xb = _nchw(bn.spec.in_shape)
+    stub.stub_reset()
+    yb = _nchw(bn.spec.in_shape)
+    assert stub.ms_layer_forward(ctypes.byref(bn.layer), ref(xb), ref(bn.W), ref(bn.b), 3, ref(yb), ctypes.byref(h),
+                                 None) == 0
+    assert stub.stub_log().decode() == "copy4;bn_fwd;copy4;"
+    stub.stub_reset()
+    gb = _nchw(bn.spec.in_shape)
+    assert stub.ms_layer_backward(h, ref(gb), ref(_nchw(bn.spec.in_shape)), ref(tdesc((bn.spec.in_shape[1],))), None,
+                                  None) == 0, stub.ms_last_error()
+    assert stub.stub_log().decode() == "copy4;copy4;bn_bwd;copy4;"   # grad_y, x (dgamma); grad_x out
+    stub.ms_record_free(h)
+    # the 3-D kinds stay channels-last only
+    assert stub.ms_testing_live_records() == 0
+
+
+def test_elementwise_layers_take_any_dense_layout(stub):
+    """ReLU and dropout work in memory order: any dense layout (NCHW too) is
+    taken as is, with y (and the gradients) in x's layout."""
+    shape = (2, 16, 5, 7)
+    x, y = _nchw(shape), _nchw(shape)
+    h = ctypes.c_void_p()
+    stub.stub_reset()
+    assert stub.ms_relu_forward(ref(x), ref(y), FAKE, 1, ctypes.byref(h), None) == 0, stub.ms_last_error()
+    assert stub.stub_log().decode() == "relu_fwd+bits;"
+    assert stub.ms_layer_backward(h, ref(_nchw(shape)), ref(tdesc(shape)), None, None, None) == L.MS_E_LAYOUT
+    assert stub.ms_layer_backward(h, ref(_nchw(shape)), ref(_nchw(shape)), None, None, None) == 0
+    stub.ms_record_free(h)
+    assert stub.ms_relu_forward(ref(x), ref(tdesc(shape)), FAKE, 1, ctypes.byref(h), None) == L.MS_E_LAYOUT
+    sl = _nchw(shape)
+    sl.stride[0] *= 2                                  # every other image of a larger tensor: not dense
+    assert stub.ms_dropout_forward(ref(sl), ref(sl), ctypes.c_float(0.5), 1, 0, 1, ctypes.byref(h), None) == L.MS_E_LAYOUT
 
 
 def test_workspace_failure_leaves_record_and_ledger_intact(stub):
@@ -526,6 +627,12 @@ def test_relu_record_keeps_one_bit_per_element(stub, shape, dtype):
     assert stub.ms_testing_live_records() == 0
 
 
+def _sliced(shape):
+    t = tdesc(shape, "bf16", "nchw")
+    t.stride[0] *= 2
+    return t
+
+
 def test_relu_validation_errors_launch_nothing(stub):
     x, y = tdesc((8, 16), "bf16"), tdesc((8, 16), "bf16")
     cases = [
@@ -536,7 +643,7 @@ def test_relu_validation_errors_launch_nothing(stub):
         (x, tdesc((8, 17), "bf16"), FAKE, L.MS_RG_INPUT, L.MS_E_SHAPE),
         (x, tdesc((8, 16), "f32"), FAKE, L.MS_RG_INPUT, L.MS_E_DTYPE),
         (tdesc((2, 3, 4), "bf16"), tdesc((2, 3, 4), "bf16"), FAKE, L.MS_RG_INPUT, L.MS_E_SHAPE),
-        (tdesc((2, 3, 4, 5), "bf16", "nchw"), tdesc((2, 3, 4, 5), "bf16", "nchw"), FAKE, 1, L.MS_E_LAYOUT),
+        (_sliced((2, 3, 4, 5)), _sliced((2, 3, 4, 5)), FAKE, 1, L.MS_E_LAYOUT),   # not dense
         (tdesc((2, 3, 4, 5), "bf16"), tdesc((2, 3, 4, 5), "bf16", "nchw"), FAKE, 1, L.MS_E_LAYOUT),
         (None, y, FAKE, L.MS_RG_INPUT, L.MS_E_NULL),
         (x, None, FAKE, L.MS_RG_INPUT, L.MS_E_NULL),
@@ -663,8 +770,12 @@ def test_conv_transpose_validation(stub):
     a = ConvTArgs((2, 16, 5, 7), 8, (4, 4), (2, 2), (1, 1), (1, 0))
     assert fwd(a, y=tdesc((2, 8, 10, 14))) == L.MS_E_SHAPE        # out_pad ignored in y
     assert fwd(a, W=tdesc((8, 16, 4, 4))) == L.MS_E_SHAPE          # W given as [Co, Ci, R, S]
-    assert fwd(a, W=tdesc(a.w_shape, layout="nchw")) == L.MS_E_LAYOUT
-    assert fwd(a, x=tdesc(a.x_shape, layout="nchw")) == L.MS_E_LAYOUT
+    negw = tdesc(a.w_shape)
+    negw.stride[2] = -negw.stride[2]
+    assert fwd(a, W=negw) == L.MS_E_LAYOUT          # other layouts are staged; negative strides are refused
+    ovx = tdesc(a.y_shape)
+    ovx.stride[0] = 0
+    assert fwd(a, y=ovx) == L.MS_E_LAYOUT
     assert fwd(a, b=tdesc((16,))) == L.MS_E_SHAPE                  # bias has C_out entries
     assert fwd(a, x=tdesc(a.x_shape, "f32")) == L.MS_E_DTYPE
     a.layer.out_pad[0] = 2                                          # out_pad >= stride
@@ -735,7 +846,7 @@ def test_dropout_validation_errors_launch_nothing(stub):
         (x, y, float("inf"), 1, L.MS_E_ARG),
         (x, tdesc((8, 17), "bf16"), 0.5, 1, L.MS_E_SHAPE),
         (x, tdesc((8, 16), "f32"), 0.5, 1, L.MS_E_DTYPE),
-        (tdesc((2, 3, 4, 5), "bf16", "nchw"), tdesc((2, 3, 4, 5), "bf16", "nchw"), 0.5, 1, L.MS_E_LAYOUT),
+        (_sliced((2, 3, 4, 5)), _sliced((2, 3, 4, 5)), 0.5, 1, L.MS_E_LAYOUT),
         (None, y, 0.5, 1, L.MS_E_NULL),
         (x, None, 0.5, 1, L.MS_E_NULL),
     ]
