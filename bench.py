@@ -369,7 +369,8 @@ def measure(w, steps, warmup, flush, per_layer=True, reps=None):
 
 # ------------------------------------------------------------------ recorded counters
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_encoder_linears_bf16_hbm_counters.md")
-GEMM_SOURCES = ("paper_2404_12406_amd/csrc/kernels/gemm_bf16.hip", "paper_2404_12406_amd/csrc/kernels/common.h")
+GEMM_SOURCES = ("paper_2404_12406_amd/csrc/kernels/gemm_bf16.hip", "paper_2404_12406_amd/csrc/kernels/common.h",
+                "paper_2404_12406_amd/csrc/kernels/limits.h")
 
 
 def gemm_sources_sha256():
@@ -547,6 +548,70 @@ def reduction_bandwidth(steps, warmup, flush):
             out.append(e)
             log(f"[bench] {name} on {label}: {us:.1f} us, {e['GBs']} GB/s")
         del cases, p
+    torch.cuda.empty_cache()
+    return out
+
+
+def layout_staging_cost(steps, warmup, flush):
+    """What a caller's NCHW tensors cost against channels-last ones: the
+    conv sweep's 3x3 layer x[32,256,28,28] with every flag set (forward,
+    input, weight and bias gradients) and the BN-eval forward on the stage-1
+    tensor [64,64,56,56], bf16, each call after a cache eviction.  For the
+    conv in NCHW the library stages x, W, y (and grad_y, grad_x, grad_W)
+    through transient workspace with its strided-copy kernel, whose bytes
+    (each staged tensor read and written once) are reported beside the
+    times; BN-eval sweeps a plain NCHW tensor in place."""
+    import torch
+    import paper_2404_12406_amd as ms
+    out = {}
+    g = torch.Generator(device="cuda").manual_seed(4646)
+    cl = torch.channels_last
+    cases = []
+    x = torch.randn(32, 256, 28, 28, generator=g, device="cuda").to(torch.bfloat16)
+    w = (0.02 * torch.randn(256, 256, 3, 3, generator=g, device="cuda")).to(torch.bfloat16)
+    b = torch.zeros(256, device="cuda", dtype=torch.bfloat16)
+    gy = torch.randn(32, 256, 28, 28, generator=g, device="cuda").to(torch.bfloat16)
+    # staged tensors, each read and written once: x (forward and weight
+    # gradient), y, grad_y, grad_x; W (forward and input gradient), grad_W
+    staged = 2 * 2 * (5 * x.numel() + 3 * w.numel())
+    for fmt in ("channels_last", "nchw"):
+        conv = (lambda t: t.contiguous(memory_format=cl)) if fmt == "channels_last" else (lambda t: t.contiguous())
+        X, W, GY = conv(x), conv(w), conv(gy)
+        p = ms.PreparedLayer(ms.Conv2d(1, 1), X, W, b, 7, y=conv(torch.empty_like(x)), grad_y=GY,
+                             grad_x=conv(torch.empty_like(x)), grad_W=conv(torch.empty_like(w)),
+                             grad_b=torch.empty_like(b))
+        cases.append(("conv3x3_256_all_flags", fmt, p, staged))
+    xb = torch.randn(64, 64, 56, 56, generator=g, device="cuda").to(torch.bfloat16)
+    C = 64
+    mu, var = torch.zeros(C, device="cuda", dtype=torch.bfloat16), torch.ones(C, device="cuda", dtype=torch.bfloat16)
+    ga, be = torch.ones(C, device="cuda", dtype=torch.bfloat16), torch.zeros(C, device="cuda", dtype=torch.bfloat16)
+    for fmt in ("channels_last", "nchw"):
+        X = xb.contiguous(memory_format=cl) if fmt == "channels_last" else xb.contiguous()
+        p = ms.PreparedLayer(ms.BatchNormEval(mu, var, 1e-5), X, ga, be, 0, y=torch.empty_like(X))
+        cases.append(("bn_eval_forward_stage1", fmt, p, 0))   # plain NCHW: swept in place, nothing staged
+    for name, fmt, p, sbytes in cases:
+        for _ in range(max(1, warmup)):
+            p.forward()
+            if p.mask:
+                p.backward()
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        for a, c in ev:
+            flush()
+            a.record()
+            p.forward()
+            if p.mask:
+                p.backward()
+            c.record()
+        torch.cuda.synchronize()
+        t = statistics.median(a.elapsed_time(c) for a, c in ev)
+        out.setdefault(name, {})[fmt] = {"median_ms": round(t, 4)}
+        if fmt == "nchw":
+            base = out[name]["channels_last"]["median_ms"]
+            out[name]["nchw"].update({"overhead_ms": round(t - base, 4), "staged_bytes": sbytes})
+            if sbytes:
+                out[name]["nchw"]["staging_GBs"] = round(sbytes / max(t - base, 1e-6) / 1e6, 1)
+        log(f"[bench] layout {name} {fmt}: {t:.4f} ms")
     torch.cuda.empty_cache()
     return out
 
@@ -787,6 +852,9 @@ def extras(steps, warmup, flush):
     t0 = time.time()
     out["reduction_passes"] = reduction_bandwidth(steps, warmup, flush)
     log(f"[bench] reduction passes ({time.time() - t0:.1f}s)")
+    t0 = time.time()
+    out["layout_staging"] = layout_staging_cost(min(steps, 20), warmup, flush)
+    log(f"[bench] layout staging ({time.time() - t0:.1f}s)")
     t0 = time.time()
     out["fig1_synthetic_cnn_memory"] = f1 = memory_probe("conv2d")
     log(f"[bench] fig1 probe: library {f1['library']}, stock {f1['stock_pytorch']} ({time.time() - t0:.1f}s)")

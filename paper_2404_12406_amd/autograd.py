@@ -61,6 +61,26 @@ def _as_layout_of(g: torch.Tensor, like) -> torch.Tensor:
     return out
 
 
+def _versions(rec):
+    """(tensor, version counter) of every tensor a record borrows."""
+    if rec is None:
+        return ()
+    out = []
+    for v in rec.saved.values():
+        for t in (v if isinstance(v, tuple) else (v,)):
+            if isinstance(t, torch.Tensor):
+                out.append((t, t._version))
+    return tuple(out)
+
+
+def _check_versions(versions):
+    for t, v in versions:
+        if t._version != v:
+            raise RuntimeError("a tensor that the layer's record borrows for backward has been modified by an "
+                               f"inplace operation (version {t._version}, expected {v}); the gradient would be "
+                               "computed from the modified values")
+
+
 def _mask(ctx, ix: int, iw: Optional[int] = None, ib: Optional[int] = None) -> int:
     need = ctx.needs_input_grad
     m = MASK_INPUT if need[ix] else 0
@@ -80,6 +100,9 @@ class _LayerFn(torch.autograd.Function):
         y, rec = api.layer_forward(spec, x, W, b, mask)
         ctx.rec = rec
         ctx.has = (W is not None, b is not None)
+        # the record borrows these tensors: like autograd's saved tensors,
+        # they must not be modified in place before backward
+        ctx.versions = _versions(rec)
         return y
 
     @staticmethod
@@ -88,6 +111,7 @@ class _LayerFn(torch.autograd.Function):
         ctx.rec = None
         if rec is None:
             return None, None, None, None
+        _check_versions(ctx.versions)
         gy = grad_y if grad_y.dim() in (2, 4) else _cl(grad_y.contiguous() if grad_y.dim() < 4 else grad_y)
         gx, gw, gb = api.layer_backward(rec, gy)
         rec.free()

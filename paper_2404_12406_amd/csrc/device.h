@@ -85,6 +85,12 @@ int launch_colsum(int dtype, const void *in, int64_t rows, int cols, void *out,
 int launch_bn_fwd(int dtype, const void *x, const void *mean, const void *var,
                   const void *gamma, const void *beta, float eps, int64_t rows, int C,
                   void *y, void *stream);
+// BN-eval over a plain row-major [N, C, H, W] tensor (HW = H * W), in the
+// same layout: the forward, or (mean and beta null) a backward that wants dx
+// alone, dx = dy * gamma / sqrt(var + eps).  `backward` picks the profiling
+// kind the launch counts as.
+int launch_bn_nchw(int dtype, const void *x, const void *mean, const void *var, const void *gamma, const void *beta,
+                   float eps, int64_t N, int C, int64_t HW, void *y, void *stream, bool backward);
 size_t bn_bwd_workspace(int dtype, int64_t rows, int C);
 // Any of dx, dgamma, dbeta may be null (not requested); x and mean are read
 // only when dgamma is requested.

@@ -34,6 +34,7 @@
 #include <cstring>
 
 #include "common.h"
+#include "limits.h"
 #include "../device.h"
 
 namespace ms {
@@ -48,7 +49,6 @@ typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
 // M/N-contiguous operand (no copy, transposing LDS reads).
 enum Mode { kFwd = 0, kDgrad = 1, kWgrad = 2, kDgradN = 3 };
 
-constexpr uint32_t kOOB = 0xFFFFFFF0u;   // byte offset beyond any buffer: loads return 0
 constexpr int BK = 64;                   // reduction step (elements)
 
 struct Args {
@@ -1403,6 +1403,8 @@ bool unit_geom(const ConvGeom &g) {
     return g.R == 1 && g.S == 1 && g.sh == 1 && g.sw == 1 && g.ph == 0 && g.pw == 0 && g.P == g.H && g.Q == g.W;
 }
 
+// Byte size of an operand for its buffer descriptor; callers have checked
+// operand_fits, so the size and every row base fit 32 bits.
 uint32_t bytes_of(long elems) { return (uint32_t)(elems * 2); }
 
 int pad8(int c) { return (c + 7) / 8 * 8; }
@@ -1647,6 +1649,7 @@ int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, 
         return conv_fwd(g8, xp, wp, bias, y, ws2, st);
     }
     if (!al16(x) || !al16(w) || !al16(y)) return -1;
+    if (!operand_fits((long)g.N * g.H * g.W * g.C) || !operand_fits((long)g.K * g.R * g.S * g.C)) return -1;
     Args a{};
     a.a = (const bf16 *)x; a.b = (const bf16 *)w; a.c = (bf16 *)y; a.g = g;
     a.M = g.N * g.P * g.Q; a.N = g.K; a.K = g.R * g.S * g.C;
@@ -1797,6 +1800,7 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bia
         return crop_channels(dxp, (int64_t)g.N * g.H * g.W, g.C, dx, st);
     }
     if (!al16(dy) || !al16(w) || !al16(dx)) return -1;
+    if (!operand_fits((long)g.N * g.P * g.Q * g.K) || !operand_fits((long)g.K * g.R * g.S * g.C)) return -1;
     const DgradChoice dc = dgrad_choice(g);
     const bool direct = dc.direct;
     const GemmPlan &p = dc.p;
@@ -1890,6 +1894,7 @@ int conv_wgrad(const ConvGeom &g, const void *dy, const void *x, void *dw, void 
         return crop_channels(dwp, (int64_t)g.K * g.R * g.S, g.C, dw, st);
     }
     if (!al16(dy) || !al16(x) || !al16(dw)) return -1;
+    if (!operand_fits((long)g.N * g.P * g.Q * g.K) || !operand_fits((long)g.N * g.H * g.W * g.C)) return -1;
     WgradPlan p = wgrad_plan(g);
     Args a{};
     a.a = (const bf16 *)dy; a.b = (const bf16 *)x; a.g = g;

@@ -34,9 +34,19 @@ struct Copy4 {
 
 constexpr int kT = 64;   // tile edge
 
-template <typename T>
+// Raw vector of B bytes (B = 4, 8 or 16).
+template <int B> struct Raw;
+template <> struct Raw<4> { typedef uint32_t type; };
+template <> struct Raw<8> { typedef uint64_t type; };
+template <> struct Raw<16> { typedef u32x4 type; };
+
+// RB / WB: bytes per access of a source row (along ib) / destination row
+// (along ia); 0 = element by element.  The caller checked unit stride,
+// extent and alignment for the vector widths it picked.
+template <typename T, int RB, int WB>
 __global__ __launch_bounds__(256) void copy4_tiled_kernel(const T *__restrict__ src, T *__restrict__ dst, const Copy4 c) {
-    __shared__ T tile[kT][kT + 1];
+    constexpr int PITCH = kT + 16 / (int)sizeof(T);   // 16-byte aligned rows, shifted banks
+    __shared__ __attribute__((aligned(16))) T tile[kT][PITCH];
     int64_t blk = blockIdx.x;
     const int64_t tbi = blk % c.tb;
     blk /= c.tb;
@@ -47,18 +57,60 @@ __global__ __launch_bounds__(256) void copy4_tiled_kernel(const T *__restrict__ 
     const int64_t dbase = j0 * c.ds[c.o0] + j1 * c.ds[c.o1];
     const int64_t a0 = tai * kT, b0 = tbi * kT;
     const int64_t ea = c.ext[c.ia], eb = c.ext[c.ib];
-    const int lx = threadIdx.x & (kT - 1), ly = threadIdx.x >> 6;
-    // read along the source's unit stride (lanes over b)
-    for (int r = ly; r < kT; r += 4) {
-        const int64_t a = a0 + r, b = b0 + lx;
-        if (a < ea && b < eb) tile[r][lx] = src[sbase + a * c.ss[c.ia] + b * c.ss[c.ib]];
+    const int t = threadIdx.x;
+    // read along the source's unit stride: tile[a][b]
+    if constexpr (RB > 0) {
+        typedef typename Raw<RB>::type V;
+        constexpr int E = RB / (int)sizeof(T), VPR = kT / E, RPP = 256 / VPR;   // rows per pass
+        const int cv = t % VPR;
+        for (int r = t / VPR; r < kT; r += RPP) {
+            const int64_t a = a0 + r, b = b0 + cv * E;
+            if (a < ea && b < eb)
+                *reinterpret_cast<V *>(&tile[r][cv * E]) = *reinterpret_cast<const V *>(src + sbase + a * c.ss[c.ia] + b);
+        }
+    } else {
+        const int lx = t & (kT - 1);
+        for (int r = t >> 6; r < kT; r += 4) {
+            const int64_t a = a0 + r, b = b0 + lx;
+            if (a < ea && b < eb) tile[r][lx] = src[sbase + a * c.ss[c.ia] + b * c.ss[c.ib]];
+        }
     }
     __syncthreads();
-    // write along the destination's unit stride (lanes over a)
-    for (int r = ly; r < kT; r += 4) {
-        const int64_t a = a0 + lx, b = b0 + r;
-        if (a < ea && b < eb) dst[dbase + a * c.ds[c.ia] + b * c.ds[c.ib]] = tile[lx][r];
+    // write along the destination's unit stride
+    if constexpr (WB > 0) {
+        typedef typename Raw<WB>::type V;
+        constexpr int E = WB / (int)sizeof(T), VPR = kT / E, RPP = 256 / VPR;
+        const int av = t % VPR;
+        for (int r = t / VPR; r < kT; r += RPP) {
+            const int64_t a = a0 + av * E, b = b0 + r;
+            if (a < ea && b < eb) {
+                union {
+                    V v;
+                    T e[E];
+                } u;
+#pragma unroll
+                for (int e = 0; e < E; ++e) u.e[e] = tile[av * E + e][r];
+                *reinterpret_cast<V *>(dst + dbase + b * c.ds[c.ib] + a) = u.v;
+            }
+        }
+    } else {
+        const int lx = t & (kT - 1);
+        for (int r = t >> 6; r < kT; r += 4) {
+            const int64_t a = a0 + lx, b = b0 + r;
+            if (a < ea && b < eb) dst[dbase + a * c.ds[c.ia] + b * c.ds[c.ib]] = tile[lx][r];
+        }
     }
+}
+
+template <typename T, int RB>
+int launch_tiled(int wb, const T *src, T *dst, const Copy4 &c, dim3 grid, hipStream_t st) {
+    switch (wb) {
+    case 16: hipLaunchKernelGGL((copy4_tiled_kernel<T, RB, 16>), grid, dim3(256), 0, st, src, dst, c); break;
+    case 8: hipLaunchKernelGGL((copy4_tiled_kernel<T, RB, 8>), grid, dim3(256), 0, st, src, dst, c); break;
+    case 4: hipLaunchKernelGGL((copy4_tiled_kernel<T, RB, (sizeof(T) <= 4 ? 4 : 0)>), grid, dim3(256), 0, st, src, dst, c); break;
+    default: hipLaunchKernelGGL((copy4_tiled_kernel<T, RB, 0>), grid, dim3(256), 0, st, src, dst, c); break;
+    }
+    return (int)hipGetLastError();
 }
 
 template <typename T>
@@ -104,8 +156,29 @@ int copy4(const T *src, T *dst, Copy4 c, hipStream_t st) {
         c.tb = (c.ext[ib] + kT - 1) / kT;
         const int64_t blocks = c.ta * c.tb * c.ext[c.o0] * c.ext[c.o1];
         if (blocks > INT32_MAX) return (int)hipErrorInvalidValue;
-        hipLaunchKernelGGL(copy4_tiled_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, st, src, dst, c);
-        return (int)hipGetLastError();
+        // the widest vector (16, 8 or 4 bytes) that a side's unit-stride
+        // dim allows: its extent and every other stride of the side whole
+        // vectors, the base aligned to one
+        auto width = [&](const int64_t *str, int unit, const void *p) {
+            if (str[unit] != 1) return 0;
+            for (int B = 16; B >= 4; B /= 2) {
+                const int E = B / (int)sizeof(T);
+                if (E < 2 || reinterpret_cast<uintptr_t>(p) % B != 0 || c.ext[unit] % E != 0) continue;
+                bool ok = true;
+                for (int d = 0; d < 4; ++d)
+                    if (d != unit && c.ext[d] > 1 && str[d] % E != 0) ok = false;
+                if (ok) return B;
+            }
+            return 0;
+        };
+        const int rb = width(c.ss, ib, src), wb = width(c.ds, ia, dst);
+        const dim3 grid((unsigned)blocks);
+        switch (rb) {
+        case 16: return launch_tiled<T, 16>(wb, src, dst, c, grid, st);
+        case 8: return launch_tiled<T, 8>(wb, src, dst, c, grid, st);
+        case 4: return launch_tiled<T, (sizeof(T) <= 2 ? 4 : 0)>(wb, src, dst, c, grid, st);
+        default: return launch_tiled<T, 0>(wb, src, dst, c, grid, st);
+        }
     }
     // flat: destination's fastest dim first, the rest by decreasing stride order
     int p[4] = {0, 1, 2, 3};

@@ -128,6 +128,39 @@ __global__ __launch_bounds__(256) void bn_fwd_flat_kernel(const T *__restrict__ 
     }
 }
 
+// BN-eval over a logical-NCHW tensor stored plane by plane (the plain
+// row-major layout of [N, C, H, W]): vector i of V elements lies in plane
+// i / vpp (vpp = HW / V vectors per plane), whose channel is plane % C.  A
+// block streams 256 * kBnU consecutive vectors, each thread kBnU of them with
+// all loads in flight; the per-channel scale and shift are formed per vector
+// from the (cached) parameter arrays.
+template <typename T, int V>
+__global__ __launch_bounds__(256) void bn_nchw_kernel(const T *__restrict__ x, const T *__restrict__ mean,
+                                                      const T *__restrict__ var, const T *__restrict__ gamma,
+                                                      const T *__restrict__ beta, float eps, uint32_t nvec,
+                                                      uint32_t vpp, uint32_t C, T *__restrict__ y) {
+    const uint32_t i0 = blockIdx.x * 256u * kBnU + threadIdx.x;
+    VecT<T, V> v[kBnU];
+#pragma unroll
+    for (int u = 0; u < kBnU; ++u) {
+        const uint32_t i = i0 + u * 256u;
+        if (i < nvec) v[u].load(x + (size_t)i * V);
+    }
+#pragma unroll
+    for (int u = 0; u < kBnU; ++u) {
+        const uint32_t i = i0 + u * 256u;
+        if (i >= nvec) continue;
+        const uint32_t c = (i / vpp) % C;
+        const float g = gamma ? to_f32(gamma[c]) : 1.f;
+        const float b = beta ? to_f32(beta[c]) : 0.f;
+        const float m = mean ? to_f32(mean[c]) : 0.f;
+        const float sc = g * rsqrtf(to_f32(var[c]) + eps), sh = b - m * sc;
+#pragma unroll
+        for (int e = 0; e < V; ++e) v[u].e[e] = from_f32<T>(fmaf(to_f32(v[u].e[e]), sc, sh));
+        v[u].store(y + (size_t)i * V);
+    }
+}
+
 // One row vector of the reduction.  x comes as a value with a flag and the
 // dgamma term is accumulated without a branch: a pointer to x that may be
 // null, or a conditional update inside the unrolled loop, left the
@@ -413,6 +446,39 @@ int bn_sweep(int dtype, const void *x, const void *mean, const void *var, const 
 int launch_bn_fwd(int dtype, const void *x, const void *mean, const void *var, const void *gamma,
                   const void *beta, float eps, int64_t rows, int C, void *y, void *stream) {
     return bn_sweep(dtype, x, mean, var, gamma, beta, eps, rows, C, y, stream, kProfBn);
+}
+
+int launch_bn_nchw(int dtype, const void *x, const void *mean, const void *var, const void *gamma, const void *beta,
+                   float eps, int64_t N, int C, int64_t HW, void *y, void *stream, bool backward) {
+    const int64_t n = N * C * HW;
+    if (n == 0) return 0;
+    const int V = dtype == kBF16 ? 8 : 4;
+    const bool vec = HW % V == 0 && al16(x) && al16(y);
+    const int Ve = vec ? V : 1;
+    const int64_t nvec = n / Ve;
+    const unsigned blocks = (unsigned)((nvec + 256 * kBnU - 1) / (256 * kBnU));
+    hipStream_t st = (hipStream_t)stream;
+    const unsigned pk = backward ? kProfRed : kProfBn;
+    prof_mark(pk, st, true);
+    const uint32_t vpp = (uint32_t)(HW / Ve);
+    if (dtype == kBF16) {
+        if (vec) hipLaunchKernelGGL((bn_nchw_kernel<bf16, 8>), dim3(blocks), dim3(256), 0, st, (const bf16 *)x, (const bf16 *)mean,
+                                    (const bf16 *)var, (const bf16 *)gamma, (const bf16 *)beta, eps, (uint32_t)nvec, vpp,
+                                    (uint32_t)C, (bf16 *)y);
+        else hipLaunchKernelGGL((bn_nchw_kernel<bf16, 1>), dim3(blocks), dim3(256), 0, st, (const bf16 *)x, (const bf16 *)mean,
+                                (const bf16 *)var, (const bf16 *)gamma, (const bf16 *)beta, eps, (uint32_t)nvec, vpp,
+                                (uint32_t)C, (bf16 *)y);
+    } else {
+        if (vec) hipLaunchKernelGGL((bn_nchw_kernel<float, 4>), dim3(blocks), dim3(256), 0, st, (const float *)x,
+                                    (const float *)mean, (const float *)var, (const float *)gamma, (const float *)beta, eps,
+                                    (uint32_t)nvec, vpp, (uint32_t)C, (float *)y);
+        else hipLaunchKernelGGL((bn_nchw_kernel<float, 1>), dim3(blocks), dim3(256), 0, st, (const float *)x,
+                                (const float *)mean, (const float *)var, (const float *)gamma, (const float *)beta, eps,
+                                (uint32_t)nvec, vpp, (uint32_t)C, (float *)y);
+    }
+    const int err = (int)hipGetLastError();
+    prof_mark(pk, st, false);
+    return err;
 }
 
 static RowColPlan bn_bwd_plan(int dtype, int64_t rows, int C, bool vec) {

@@ -174,6 +174,16 @@ bool dense_any_order(const ms_tensor *t) {
     return true;
 }
 
+// Plain row-major [N, C, H, W] (PyTorch's default contiguous layout).
+bool is_nchw(const ms_tensor *t) {
+    if (t->ndim != 4) return false;
+    const int64_t C = t->shape[1], H = t->shape[2], W = t->shape[3];
+    const int64_t want[4] = {C * H * W, H * W, W, 1};
+    for (int i = 0; i < 4; ++i)
+        if (t->shape[i] > 1 && t->stride[i] != want[i]) return false;
+    return true;
+}
+
 bool same_strides(const ms_tensor *a, const ms_tensor *b) {
     for (int i = 0; i < a->ndim; ++i)
         if (a->shape[i] > 1 && a->stride[i] != b->stride[i]) return false;
@@ -220,6 +230,8 @@ struct Plan {
     // layouts that are not the kernels' (staged through transient workspace)
     bool st_x = false, st_w = false, st_y = false;
     uint64_t out_bytes = 0;                  // bytes of y
+    bool bn_nchw = false;                    // BN-eval on plain NCHW tensors: its sweeps run in place
+    int64_t hw = 0;                          // BN-eval: H * W of a 4-D x
 };
 
 bool stageable(int32_t kind) {
@@ -233,6 +245,10 @@ void plan_layouts(Plan *pl, const ms_tensor *x, const ms_tensor *W, const ms_ten
     pl->st_x = !canonical(x);
     pl->st_w = W && W->ndim >= 2 && !canonical(W);
     pl->st_y = y && !canonical(y);
+    if (pl->kind == MS_BN_EVAL && x->ndim == 4) {
+        pl->hw = x->shape[2] * x->shape[3];
+        pl->bn_nchw = pl->st_x && is_nchw(x) && (!y || (pl->st_y && is_nchw(y)));
+    }
     const uint64_t e = elt_size(pl->dtype);
     switch (pl->kind) {
     case MS_CONV2D: pl->out_bytes = (uint64_t)pl->g.N * pl->g.P * pl->g.Q * pl->g.K * e; break;
@@ -709,6 +725,7 @@ void *kptr(const ms_tensor *t, char *base, size_t off) {
 // gradient in y's layout and the input and weight gradients in x's and W's.
 uint64_t backward_staging(const Plan &pl, uint32_t kernels) {
     if (!stageable(pl.kind)) return 0;
+    if (pl.bn_nchw && kernels == MS_K_DGRAD) return 0;   // dx alone: the in-place NCHW sweep
     const bool wg = kernels & MS_K_WGRAD, dg = kernels & MS_K_DGRAD;
     uint64_t b = pl.st_y ? al256(pl.out_bytes) : 0;               // grad_y
     if (pl.st_x && wg && pl.kind != MS_AVGPOOL) b += al256(pl.x_bytes);   // x read by the weight gradient
@@ -787,9 +804,10 @@ ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
     // then the kernels' own (zero-padded channel copies for channel counts
     // that are not a multiple of 8), taken before anything is launched
     Stager sg;
-    const size_t ox = stageable(pl.kind) ? sg.add(x) : kNoStage;
-    const size_t ow = stageable(pl.kind) && W && W->ndim >= 2 ? sg.add(W) : kNoStage;
-    const size_t oy = stageable(pl.kind) ? sg.add(y) : kNoStage;
+    const bool stg = stageable(pl.kind) && !pl.bn_nchw;   // BN-eval sweeps plain NCHW tensors in place
+    const size_t ox = stg ? sg.add(x) : kNoStage;
+    const size_t ow = stg && W && W->ndim >= 2 ? sg.add(W) : kNoStage;
+    const size_t oy = stg ? sg.add(y) : kNoStage;
     size_t fb = 0;
     if (pl.kind == MS_CONV2D || pl.kind == MS_LINEAR || pl.kind == MS_CONV_TRANSPOSE2D || pl.kind == MS_CONV3D ||
         pl.kind == MS_CONV_TRANSPOSE3D)
@@ -829,8 +847,13 @@ ms_status ms_layer_forward(const ms_layer *layer, const ms_tensor *x, const ms_t
         err = ms::launch_conv3d_dgrad(pl.dtype, pl.q, x->data, W->data, b ? b->data : nullptr, y->data, fws, stream);
         break;
     case MS_BN_EVAL:
-        err = ms::launch_bn_fwd(pl.dtype, xk, layer->running_mean->data, layer->running_var->data,
-                                W ? W->data : nullptr, b ? b->data : nullptr, layer->eps, pl.rows, pl.C, yk, stream);
+        if (pl.bn_nchw)
+            err = ms::launch_bn_nchw(pl.dtype, x->data, layer->running_mean->data, layer->running_var->data,
+                                     W ? W->data : nullptr, b ? b->data : nullptr, layer->eps, x->shape[0], pl.C, pl.hw,
+                                     y->data, stream, false);
+        else
+            err = ms::launch_bn_fwd(pl.dtype, xk, layer->running_mean->data, layer->running_var->data,
+                                    W ? W->data : nullptr, b ? b->data : nullptr, layer->eps, pl.rows, pl.C, yk, stream);
         break;
     case MS_AVGPOOL:
         err = ms::launch_avgpool_fwd(pl.dtype, xk, pl.Nb, pl.L, pl.C, yk, stream);
@@ -902,7 +925,10 @@ ms_status backward_impl(ms_record *r, const ms_tensor *grad_y, const ms_tensor *
     const uint32_t kernels = r->acct.kernels;
     // stand-ins of tensors in other layouts, then the kernels' workspace
     Stager sg;
-    const bool stg = stageable(pl.kind);
+    // BN-eval wanting dx alone on plain NCHW tensors: the in-place sweep
+    const bool bn_native = pl.kind == MS_BN_EVAL && kernels == MS_K_DGRAD && grad_y->ndim == 4 && !canonical(grad_y) &&
+                           is_nchw(grad_y) && !canonical(grad_x) && is_nchw(grad_x);
+    const bool stg = stageable(pl.kind) && !bn_native;
     const bool x_read = (kernels & MS_K_WGRAD) && pl.kind != MS_AVGPOOL;   // weight gradient (BN: dgamma)
     const bool w_read = (kernels & MS_K_DGRAD) && pl.kind != MS_BN_EVAL && pl.kind != MS_AVGPOOL;
     const size_t ody = stg ? sg.add(grad_y) : kNoStage;
@@ -988,6 +1014,11 @@ ms_status backward_impl(ms_record *r, const ms_tensor *grad_y, const ms_tensor *
     }
         break;
     case MS_BN_EVAL:
+        if (bn_native) {
+            err = ms::launch_bn_nchw(pl.dtype, dy, nullptr, r->var.data, r->W.data, nullptr, r->eps, r->x.shape[0], pl.C,
+                                     pl.hw, gx, stream, true);
+            break;
+        }
         err = ms::launch_bn_bwd(pl.dtype, dy, (kernels & MS_K_WGRAD) ? xk : nullptr,
                                 (kernels & MS_K_WGRAD) ? r->mean.data : nullptr, r->var.data,
                                 (kernels & MS_K_DGRAD) ? r->W.data : nullptr, r->eps, pl.rows, pl.C,

@@ -26,9 +26,19 @@ def host(t: torch.Tensor) -> np.ndarray:
     return t.detach().float().cpu().numpy().astype(np.float64)
 
 
+# (test id, output name, observed error, bar) of every check, for the
+# session's margin report (tests/conftest.py)
+MARGINS = []
+
+
 def check(name, got, ref, dtype, tol=None):
+    """Normwise relative error of `got` against the oracle's `ref` (both in
+    logical order), asserted against the bar; the observed error is logged."""
+    import os
     tol = TOL[dtype] if tol is None else tol
     err = oracle.rel_err(got, ref)
+    MARGINS.append((os.environ.get("PYTEST_CURRENT_TEST", "?").split(" ")[0], name, err, tol))
+    print(f"[parity] {name}: normwise rel err {err:.3e} (bar {tol:.0e})")
     assert err <= tol, f"{name}: normwise rel err {err:.3e} > {tol:.0e}"
     return err
 

@@ -285,3 +285,25 @@ def test_appendix_b_layers_retain_exactly_the_saved_inputs(kind, case):
     assert held == want - (nel * 4 if case == "all" else 0)
     y.backward(torch.ones_like(y))
     assert (layers[3].weight.grad is not None) and (layers[0].weight.grad is None) == (case != "all")
+
+
+def test_inplace_change_of_a_borrowed_input_is_refused():
+    """A conv whose weight trains borrows its input; writing that input in
+    place before backward would give a wrong weight gradient, so backward
+    raises (as stock autograd does for its saved tensors).  An input the
+    record does not borrow (frozen weight) may be changed freely."""
+    from paper_2404_12406_amd import autograd as msa
+    torch.manual_seed(0)
+    conv = msa.convert(torch.nn.Sequential(torch.nn.Conv2d(8, 16, 3, padding=1))).cuda()
+    x = torch.randn(2, 8, 6, 6, device="cuda")
+    y = conv(x)
+    x.add_(1.0)
+    with pytest.raises(RuntimeError, match="inplace"):
+        y.sum().backward()
+    conv[0].weight.requires_grad_(False)
+    xi = torch.randn(2, 8, 6, 6, device="cuda", requires_grad=True)
+    xx = xi * 1.0
+    y = conv(xx)
+    xx.add_(1.0)                      # not borrowed: the input gradient needs W only
+    y.sum().backward()
+    assert xi.grad is not None

@@ -12,7 +12,7 @@ import paper_2404_12406_amd as ms
 import synth
 from oracle import policy as P
 
-from _gpu import check, dev, guarded_empty, guards_intact, host
+from _gpu import TOL, check, dev, guarded_empty, guards_intact, host
 
 pytestmark = pytest.mark.gpu
 
@@ -23,7 +23,7 @@ def _conv_inputs(seed, shape_x, shape_w, dtype, bias=True):
     x = synth.normal(shape_x, seed, dtype=dtype)
     fan_in = shape_w[1] * shape_w[2] * shape_w[3]
     w = synth.kaiming_uniform(shape_w, seed + 1, fan_in, dtype=dtype)
-    b = synth.normal((shape_w[0],), seed + 2, 0.1, dtype=dtype) if bias else None
+    b = synth.normal((shape_w[0],), seed + 2, 1.0, dtype=dtype) if bias else None   # output scale: a dropped bias fails
     return x, w, b
 
 
@@ -49,6 +49,7 @@ def test_conv2d_all_masks(case, mask):
     seed = 100 + 10 * case
     x, w, b = _conv_inputs(seed, xs, ws, dt)
     y_ref = oracle.round_to(oracle.conv2d_forward(x, w, b, stride, pad), dt)
+    assert oracle.rel_err(oracle.conv2d_forward(x, w, None, stride, pad), y_ref) > 10 * TOL[dt]
     gy = synth.normal(y_ref.shape, seed + 3, dtype=dt)
     X, Wt, B = dev(x, dt), dev(w, dt), dev(b, dt)
     y, rec = ms.layer_forward(ms.Conv2d(stride, pad), X, Wt, B, mask)
@@ -87,10 +88,12 @@ def test_linear_all_masks(case, mask):
     seed = 300 + 10 * case
     x = synth.normal((M, Kin), seed, dtype=dt)
     w = synth.normal((Nout, Kin), seed + 1, 0.05, dtype=dt)
-    b = synth.normal((Nout,), seed + 2, 0.02, dtype=dt)
+    b = synth.normal((Nout,), seed + 2, 1.0, dtype=dt)     # output scale: a dropped bias fails the bar
     gy = synth.normal((M, Nout), seed + 3, dtype=dt)
     y, rec = ms.layer_forward(ms.Linear(), dev(x, dt), dev(w, dt), dev(b, dt), mask)
-    check("y", host(y), oracle.linear_forward(x, w, b), dt)
+    y_ref = oracle.linear_forward(x, w, b)
+    assert oracle.rel_err(oracle.linear_forward(x, w, None), y_ref) > 10 * TOL[dt]
+    check("y", host(y), y_ref, dt)
     if mask == 0:
         assert rec is None
         return

@@ -388,13 +388,27 @@ def test_tensors_in_other_layouts_are_staged_around_the_kernels(stub):
     yb = _nchw(bn.spec.in_shape)
     assert stub.ms_layer_forward(ctypes.byref(bn.layer), ref(xb), ref(bn.W), ref(bn.b), 3, ref(yb), ctypes.byref(h),
                                  None) == 0
-    assert stub.stub_log().decode() == "copy4;bn_fwd;copy4;"
+    assert stub.stub_log().decode() == "bn_nchw;"          # plain NCHW: swept in place
     stub.stub_reset()
     gb = _nchw(bn.spec.in_shape)
     assert stub.ms_layer_backward(h, ref(gb), ref(_nchw(bn.spec.in_shape)), ref(tdesc((bn.spec.in_shape[1],))), None,
                                   None) == 0, stub.ms_last_error()
-    assert stub.stub_log().decode() == "copy4;copy4;bn_bwd;copy4;"   # grad_y, x (dgamma); grad_x out
+    assert stub.stub_log().decode() == "copy4;copy4;bn_bwd;copy4;"   # the reduction: grad_y, x (dgamma); grad_x out
     stub.ms_record_free(h)
+    assert stub.ms_layer_forward(ctypes.byref(bn.layer), ref(xb), ref(bn.W), ref(bn.b), 1, ref(yb), ctypes.byref(h),
+                                 None) == 0
+    acct = L.MsAccount()
+    stub.ms_record_account(h, ctypes.byref(acct))
+    stub.stub_reset()
+    assert stub.ms_layer_backward(h, ref(gb), ref(_nchw(bn.spec.in_shape)), None, None, None) == 0
+    assert stub.stub_log().decode() == "bn_nchw_bwd;"      # dx alone: the same in-place sweep
+    stub.ms_record_free(h)
+    sl = _nchw(bn.spec.in_shape)
+    sl.stride[0] *= 2                                       # a slice: staged
+    stub.stub_reset()
+    assert stub.ms_layer_forward(ctypes.byref(bn.layer), ref(sl), ref(bn.W), ref(bn.b), 0, ref(yb), ctypes.byref(h),
+                                 None) == 0
+    assert stub.stub_log().decode() == "copy4;bn_fwd;copy4;"
     # the 3-D kinds stay channels-last only
     assert stub.ms_testing_live_records() == 0
 
@@ -516,6 +530,31 @@ def test_ledger_peak_over_a_stack(stub):
         stub.ms_record_free(h)
     stub.ms_ledger_read(ctypes.byref(live), ctypes.byref(peak))
     assert live.value == live0.value
+
+
+def test_fast_path_operand_limit():
+    """The bf16 GEMM fast path takes an operand only while its byte size stays
+    below the out-of-range offset its loads use (and its row bases fit 32
+    bits); larger operands -- e.g. the 8-channel padded copy of a 3-channel
+    image of 2^28 pixels -- go to the general kernel."""
+    src = os.path.join(BUILD, "limits_check.cpp")
+    exe = os.path.join(BUILD, "limits_check")
+    os.makedirs(BUILD, exist_ok=True)
+    with open(src, "w") as f:
+        f.write('#include "kernels/limits.h"\n#include <cstdio>\nusing namespace ms::g2;\n'
+                "int main() {\n"
+                "  const long long v[] = {0, 1, 2147483632LL, 2147483633LL, 2147483647LL, (1LL << 28) * 8, 64LL * 224 * 115 * 8, -1};\n"
+                '  for (long long e : v) printf("%lld %d\\n", e, (int)operand_fits(e));\n'
+                "  return 0;\n}\n")
+    subprocess.run(["g++", "-std=c++17", "-I", os.path.join(ROOT, "paper_2404_12406_amd", "csrc"), src, "-o", exe],
+                   check=True)
+    out = dict(tuple(map(int, l.split())) for l in subprocess.run([exe], capture_output=True, text=True,
+                                                                   check=True).stdout.split("\n") if l)
+    # the largest operand whose last byte stays below 0xFFFFFFF0 with 8 elements of slack
+    assert out[2147483632] == 1 and out[2147483633] == 0
+    assert out[2147483647] == 0 and out[(1 << 28) * 8] == 0 and out[-1] == 0
+    assert out[0] == 1 and out[64 * 224 * 115 * 8] == 1       # the stem's packed input
+    assert 2147483632 * 2 + 16 <= 0xFFFFFFF0
 
 
 def test_native_driver_under_sanitizers():
