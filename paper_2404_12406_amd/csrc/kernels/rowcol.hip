@@ -252,60 +252,111 @@ __global__ __launch_bounds__(256) void rowcol_reduce_kernel(
     const bool need_b = MODE == 0 || want_b;
     const bool need_g = MODE == 1 && want_g;
     if (!need_b && !need_g) return;   // uniform over the block
+    // Combine the row groups in a fixed order.  With TC a power of two
+    // (every vectorized channel count that is a multiple of 8 or 16 up to
+    // 512 channels per block column) first inside each wave, by butterfly
+    // shuffles over the lanes that share a channel vector (lane = rg * TC +
+    // tc, so they are TC apart), then the four waves' sums through LDS.
+    // Otherwise through LDS, one thread per (channel vector, element) adding
+    // the row groups in order.  (The first version let TC threads add all
+    // RG * V sums serially out of LDS: a tail of several microseconds per
+    // block that dominated the smaller tensors.)
+    const int64_t orow = (int64_t)blockIdx.y * C;
+    auto put = [&](int c, float sb, float sg) {
+        if (MODE == 0) {
+            part0[orow + c] = sb;
+        } else {
+            if (need_g) part0[orow + c] = sg;
+            if (want_b) part1[orow + c] = sb;
+        }
+    };
+    if ((TC & (TC - 1)) == 0) {
+        const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+        for (int off = TC; off < 64; off <<= 1) {
 #pragma unroll
-    for (int e = 0; e < V; ++e) {
-        red[0][threadIdx.x * V + e] = acc_b[e];
-        red[1][threadIdx.x * V + e] = acc_g[e];
-    }
-    __syncthreads();
-    if (rg == 0 && active) {
+            for (int e = 0; e < V; ++e) {
+                acc_b[e] += __shfl_xor(acc_b[e], off);
+                if (MODE == 1) acc_g[e] += __shfl_xor(acc_g[e], off);
+            }
+        }
+        // lanes 0 .. TC-1 of each wave now hold the wave's sums for tc = lane
+        if (lane < TC) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+                red[0][(wave * TC + lane) * V + e] = acc_b[e];
+                red[1][(wave * TC + lane) * V + e] = acc_g[e];
+            }
+        }
+        __syncthreads();
+        if (threadIdx.x < TC && cv * V < C) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+                float sb = 0.f, sg = 0.f;
+#pragma unroll
+                for (int w = 0; w < 4; ++w) {
+                    sb += red[0][(w * TC + tc) * V + e];
+                    sg += red[1][(w * TC + tc) * V + e];
+                }
+                put(c0 + e, sb, sg);
+            }
+        }
+    } else {
 #pragma unroll
         for (int e = 0; e < V; ++e) {
+            red[0][threadIdx.x * V + e] = acc_b[e];
+            red[1][threadIdx.x * V + e] = acc_g[e];
+        }
+        __syncthreads();
+        for (int j = threadIdx.x; j < TC * V; j += 256) {
+            const int tcj = j / V, e = j - tcj * V;
+            const int c = (blockIdx.x * TC + tcj) * V + e;
+            if (c >= C) continue;
             float sb = 0.f, sg = 0.f;
             for (int q = 0; q < RG; ++q) {
-                sb += red[0][(q * TC + tc) * V + e];
-                sg += red[1][(q * TC + tc) * V + e];
+                sb += red[0][(q * TC + tcj) * V + e];
+                sg += red[1][(q * TC + tcj) * V + e];
             }
-            const int64_t o = (int64_t)blockIdx.y * C + c0 + e;
-            if (MODE == 0) {
-                part0[o] = sb;
-            } else {
-                if (need_g) part0[o] = sg;
-                if (want_b) part1[o] = sb;
-            }
+            put(c, sb, sg);
         }
     }
 }
 
-// out[c] = sum_y part[y][c], rounded once to T.  A block owns 16 columns;
-// its 16 thread rows split the partial rows and meet in LDS in a fixed
-// order.  The first 128 partial rows (all of them for the usual plans) are
-// loaded at once, so the pass costs one memory round trip.
+// out[c] = sum_y part[y][c], rounded once to T, for up to two (part, out)
+// pairs (grid y).  A block owns 4 columns; its 64 thread rows split the
+// partial rows, each issuing 16 loads at once (one memory round trip per
+// 1024 partial rows), and meet in LDS in a fixed tree order.
 template <typename T>
-__global__ __launch_bounds__(256) void finalize_kernel(const float *__restrict__ part, int gy, int C,
-                                                       T *__restrict__ out) {
-    __shared__ float red[16][16];
-    const int cl = threadIdx.x & 15, yg = threadIdx.x >> 4;
-    const int c = blockIdx.x * 16 + cl;
+__global__ __launch_bounds__(256) void finalize_kernel(const float *__restrict__ part0, T *__restrict__ out0,
+                                                       const float *__restrict__ part1, T *__restrict__ out1, int gy,
+                                                       int C) {
+    __shared__ float red[64][5];
+    const float *__restrict__ part = blockIdx.y ? part1 : part0;
+    T *__restrict__ out = blockIdx.y ? out1 : out0;
+    const int cl = threadIdx.x & 3, yg = threadIdx.x >> 2;
+    const int c = blockIdx.x * 4 + cl;
     float s = 0.f;
     if (c < C) {
-        float a[8];
+        for (int y0 = yg; y0 < gy; y0 += 64 * 16) {
+            float a[16];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int y = yg + 16 * k;
-            a[k] = y < gy ? part[(int64_t)y * C + c] : 0.f;
+            for (int k = 0; k < 16; ++k) {
+                const int y = y0 + 64 * k;
+                a[k] = y < gy ? part[(int64_t)y * C + c] : 0.f;
+            }
+#pragma unroll
+            for (int w = 8; w >= 1; w >>= 1)
+#pragma unroll
+                for (int k = 0; k < w; ++k) a[k] += a[k + w];
+            s += a[0];
         }
-        s = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
-        for (int y = yg + 128; y < gy; y += 16) s += part[(int64_t)y * C + c];
     }
     red[yg][cl] = s;
     __syncthreads();
-    if (yg == 0 && c < C) {
-        float t = 0.f;
-#pragma unroll
-        for (int q = 0; q < 16; ++q) t += red[q][cl];
-        out[c] = from_f32<T>(t);
+    for (int off = 32; off >= 1; off >>= 1) {
+        if (yg < off) red[yg][cl] += red[yg + off][cl];
+        __syncthreads();
     }
+    if (yg == 0 && c < C) out[c] = from_f32<T>(red[0][cl]);
 }
 
 // ---------------------------------------------------------------- avgpool
@@ -379,14 +430,18 @@ int reduce_t(const RowColPlan &p, const void *a, const void *x, const void *mean
     return (int)hipGetLastError();
 }
 
+// One launch for one or two column reductions (part1 / out1 may be null).
 template <typename T>
-int finalize_t(const float *part, int gy, int C, void *out, hipStream_t st) {
-    hipLaunchKernelGGL(finalize_kernel<T>, dim3((C + 15) / 16), dim3(256), 0, st, part, gy, C, (T *)out);
+int finalize_t(const float *part0, void *out0, const float *part1, void *out1, int gy, int C, hipStream_t st) {
+    hipLaunchKernelGGL(finalize_kernel<T>, dim3((C + 3) / 4, out1 ? 2 : 1), dim3(256), 0, st, part0, (T *)out0, part1,
+                       (T *)out1, gy, C);
     return (int)hipGetLastError();
 }
 
-int finalize(int dtype, const float *part, int gy, int C, void *out, hipStream_t st) {
-    return dtype == kBF16 ? finalize_t<bf16>(part, gy, C, out, st) : finalize_t<float>(part, gy, C, out, st);
+int finalize(int dtype, const float *part0, void *out0, const float *part1, void *out1, int gy, int C,
+             hipStream_t st) {
+    return dtype == kBF16 ? finalize_t<bf16>(part0, out0, part1, out1, gy, C, st)
+                          : finalize_t<float>(part0, out0, part1, out1, gy, C, st);
 }
 
 }  // namespace
@@ -521,12 +576,10 @@ int launch_bn_bwd(int dtype, const void *dy, const void *x, const void *mean, co
         if (err) return err;
     }
     const int gy = rows > 0 ? p.gy : 0;
-    if (want_g) {
-        int err = finalize(dtype, part0, gy, C, dgamma, st);
-        if (err) return err;
-    }
-    if (want_b) {
-        int err = finalize(dtype, part1, gy, C, dbeta, st);
+    if (want_g || want_b) {
+        // dgamma and dbeta in one finalize launch
+        const int err = want_g ? finalize(dtype, part0, dgamma, want_b ? part1 : nullptr, dbeta, gy, C, st)
+                               : finalize(dtype, part1, dbeta, nullptr, nullptr, gy, C, st);
         if (err) return err;
     }
     prof_mark(kProfRed, st, false);
@@ -542,7 +595,7 @@ size_t colsum_workspace(int dtype, int64_t rows, int C) {
 int launch_colsum_finalize(int dtype, const float *part, int rows, int cols, void *out, void *stream) {
     if (cols == 0) return 0;
     prof_mark(kProfRed, stream, true);
-    const int err = finalize(dtype, part, rows, cols, out, (hipStream_t)stream);
+    const int err = finalize(dtype, part, out, nullptr, nullptr, rows, cols, (hipStream_t)stream);
     prof_mark(kProfRed, stream, false);
     return err;
 }
@@ -565,7 +618,7 @@ int launch_colsum(int dtype, const void *in, int64_t rows, int C, void *out, voi
                       : reduce_t<float, 1, 0>(p, in, nullptr, nullptr, nullptr, nullptr, 0.f, rows, C, nullptr, false, true, part, nullptr, st);
         if (err) return err;
     }
-    const int err = finalize(dtype, part, rows > 0 ? p.gy : 0, C, out, st);
+    const int err = finalize(dtype, part, out, nullptr, nullptr, rows > 0 ? p.gy : 0, C, st);
     prof_mark(kProfRed, st, false);
     return err;
 }
