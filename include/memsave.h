@@ -21,10 +21,20 @@
  *  - Every buffer is caller-allocated device memory; the library never
  *    frees or copies caller memory.  `ms_tensor.data` is a device pointer.
  *  - Shapes are given in logical PyTorch order, strides in elements.
- *    4-D activations and conv weights must be channels-last (NHWC / KRSC
- *    memory order, i.e. torch.channels_last), 5-D ones channels-last too
- *    (NDHWC / KTRSC, torch.channels_last_3d); 2-D tensors row-major; 1-D
- *    tensors contiguous.  Anything else returns MS_E_LAYOUT.
+ *    The kernels read dense channels-last tensors (NHWC activations, KRSC
+ *    filters, row-major matrices).  For MS_CONV2D, MS_CONV_TRANSPOSE2D,
+ *    MS_LINEAR, MS_BN_EVAL and MS_AVGPOOL any non-negative strides are
+ *    accepted (NCHW, strided slices, transposed views, broadcast inputs);
+ *    output and gradient buffers must not overlap themselves.  Tensors in
+ *    another layout are staged: copied into the kernels' layout in transient
+ *    workspace before the launch and back after it, on the same stream
+ *    (counted in ms_account.transient_workspace_bytes).  The record still
+ *    borrows the caller's own x, never a staged copy.  BN-eval on a plain
+ *    NCHW tensor runs in place, without staging.  5-D tensors (the 3-D
+ *    kinds) must be channels-last (NDHWC / KTRSC, torch.channels_last_3d);
+ *    MS_RELU and MS_DROPOUT take x dense in any order of its dims with y and
+ *    the gradients in x's strides; 1-D tensors (biases, BN statistics) are
+ *    contiguous.  Anything else returns MS_E_LAYOUT.
  *  - dtypes: MS_F32 or MS_BF16; all tensors of one call share one dtype.
  *    Products are accumulated in fp32 and rounded once to the output dtype
  *    (round to nearest even).
@@ -85,15 +95,15 @@ typedef enum {
                             P = (H + 2 pad_h - R) / stride_h + 1 (likewise Q)              */
     MS_LINEAR = 1,       /* y = x W^T + b: x[M,K_in], W[N_out,K_in], b[N_out] or NULL, y[M,N_out] */
     MS_BN_EVAL = 2,      /* y = gamma (x - mean) / sqrt(var + eps) + beta per channel,
-                            x[N,C,H,W] (channels-last) or x[N,C]; W = gamma[C], b = beta[C]
+                            x[N,C,H,W] or x[N,C]; W = gamma[C], b = beta[C]
                             (both NULL for affine=False); running stats are fixed buffers  */
     MS_AVGPOOL = 3,      /* global average pool x[N,C,H,W] -> y[N,C]; no parameters        */
-    MS_RELU = 4,         /* y = max(x, 0) elementwise (NaN and -0 pass through); x 1-D
-                            contiguous, 2-D row-major or 4-D channels-last, y likewise; no
+    MS_RELU = 4,         /* y = max(x, 0) elementwise (NaN and -0 pass through); x dense
+                            in any order of its dims, y in the strides of x; no
                             parameters.  Forward through ms_relu_forward() only           */
     MS_CONV_TRANSPOSE2D = 5, /* y = transposed convolution of x (torch.nn.ConvTranspose2d with
                             dilation 1, groups 1): x[N,C_in,H,W], W[C_in,C_out,R,S]
-                            (channels-last: memory [C_in][R][S][C_out]), b[C_out] or NULL,
+                            (kernel layout: memory [C_in][R][S][C_out]), b[C_out] or NULL,
                             y[N,C_out,H_out,W_out], H_out = (H-1) stride_h - 2 pad_h + R
                             + out_pad_h (likewise W_out), 0 <= out_pad < stride:
                               y[n,o,h',w'] = b[o] + sum of x[n,i,h,w] W[i,o,r,s]
@@ -289,10 +299,14 @@ ms_status ms_layer_backward_noalloc(ms_record *rec, const ms_tensor *grad_y, con
 /* Size in bytes of the fixed scratch of ms_layer_backward_noalloc() (per GPU). */
 uint64_t ms_noalloc_scratch_bytes(void);
 
-/* Copy a record's accounting into *out. */
+/* Copy a record's accounting into *out: the bytes of the tensors the
+ * forward call kept for the backward (the saved tensors of the autograd
+ * primitive, Sec. 2.2) and the transient workspace it used. */
 ms_status ms_record_account(const ms_record *rec, ms_account *out);
 
-/* Release a record (and its borrowed bytes if backward did not run).  NULL is a no-op. */
+/* Release a record (and its borrowed bytes if backward did not run): the
+ * saved tensors of a graph that is never differentiated are dropped, as
+ * Sec. 2.2's primitive frees its context.  NULL is a no-op. */
 void ms_record_free(ms_record *rec);
 
 /* Process-wide ledger of borrowed activation bytes: current and peak since
@@ -305,6 +319,11 @@ ms_status ms_ledger_reset(void);
  * ms_policy_account -- the accounting a forward call would produce under
  * `policy` (MS_POLICY_*), without launching anything or touching the ledger.
  * Tensors are validated like ms_layer_forward (data pointers may be NULL).
+ * The policies are the comparison of Fig. 2 and App. B: the selective rule
+ * of Sec. 2.2.1, stock PyTorch's rule (convolutions and BN-eval keep the
+ * input whenever any flag is set; Linear already saves selectively) and the
+ * every-parent-differentiable case.  The saved bytes of a forward pass under
+ * each policy are what Sec. 2 compares through the forward-peak proxy.
  */
 ms_status ms_policy_account(const ms_layer *layer, const ms_tensor *x, const ms_tensor *W,
                             const ms_tensor *b, uint32_t mask, int32_t policy, ms_account *out);
