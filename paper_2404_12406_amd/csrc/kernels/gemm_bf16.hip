@@ -66,6 +66,8 @@ struct Args {
     ConvGeom g;
     int M, N, K;          // GEMM extents (DGRAD: bounds over phases)
     int ntm, ntn;
+    int ldc;              // bf16 output row stride in elements (0: N); a launch that covers
+                          // a column range of a wider output passes the full width
     int k_split, splits;  // reduction range per split (a multiple of BK) and split count
     uint32_t a_bytes, b_bytes;
 };
@@ -930,7 +932,7 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
                 const int pix = (nimg * g.H + f.h0 + i2 * g.sh) * g.W + f.w0 + j2 * g.sw;
                 dst = P.c + (size_t)pix * g.C + n;
             } else {
-                dst = P.c + (size_t)m * N + n;
+                dst = P.c + (size_t)m * (P.ldc > 0 ? P.ldc : N) + n;
             }
             if (n + 8 <= N) {
                 *reinterpret_cast<u32x4 *>(dst) = v.u;
@@ -1347,6 +1349,51 @@ GemmPlan plan_gemm(long M, long N, long K, int z, int split_cap = 16, bool allow
     return bp;
 }
 
+// Column split of a one-split, unit-geometry contraction whose tiles leave
+// its last wave of blocks partly empty (an 8192 x 3072 output is 384 tiles
+// of 256 x 256: one and a half waves of 256 CUs, so the second wave runs at
+// half occupancy for as long as the first).  The first launch takes the
+// leading n1 columns, the tile columns that fill whole waves on the plan's
+// tile; the second covers the remaining columns with the tile the planner
+// picks for that narrower output (8192 x 1024: 256 tiles of 256 x 128).  The
+// two launches write disjoint column ranges of one output (row stride = the
+// full width) and neither needs workspace.  The split is taken when the
+// estimate of the two launches plus the gap between them beats the one.
+// MEMSAVE_GEMM_TAIL=off disables it and =on takes it wherever it applies
+// (testing knobs).
+struct ColSplit {
+    int n1 = 0;     // columns of the first launch (0: no split)
+    GemmPlan p2{};  // plan of the remaining columns
+};
+constexpr double kGapUs = 1.5;   // dispatch gap between two launches on one stream
+
+int tail_mode() {
+    const char *e = getenv("MEMSAVE_GEMM_TAIL");
+    if (!e || !*e) return 1;
+    if (strcmp(e, "off") == 0) return 0;
+    if (strcmp(e, "on") == 0) return 2;
+    return 1;
+}
+
+ColSplit col_split(const GemmPlan &p, long M, long N, long K, const bool *set) {
+    ColSplit cs;
+    const int mode = tail_mode();
+    if (mode == 0 || p.splits != 1 || forced_tile() >= 0) return cs;
+    const long ntm = (M + p.t.bm - 1) / p.t.bm, ntn = (N + p.t.bn - 1) / p.t.bn;
+    const long conc = (long)kCUs * p.t.per_cu, tiles = ntm * ntn;
+    if (tiles <= conc || tiles % conc == 0 || ntm > conc) return cs;
+    const long c1 = (tiles / conc) * conc / ntm;   // tile columns of the whole waves
+    if (c1 < 1 || c1 >= ntn) return cs;
+    const long n1 = c1 * p.t.bn;
+    const GemmPlan p2 = plan_gemm(M, N - n1, K, 1, 1, true, kKgAuto, set);
+    const double one = est_us(p.t, M, N, K, 1, 1);
+    const double two = est_us(p.t, M, n1, K, 1, 1) + est_us(p2.t, M, N - n1, K, 1, 1) + kGapUs;
+    if (mode == 1 && two >= one) return cs;
+    cs.n1 = (int)n1;
+    cs.p2 = p2;
+    return cs;
+}
+
 // floats of one split's partials (a multiple of 4: 16-byte aligned splits)
 int64_t part_stride(int64_t elems) { return (elems + 3) / 4 * 4; }
 
@@ -1668,6 +1715,26 @@ int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, 
     } else {
         a.bias = (const bf16 *)bias;
     }
+    const ColSplit cs = unit_geom(g) ? col_split(p, a.M, a.N, a.K, kAutoKc) : ColSplit{};
+    if (cs.n1 > 0) {
+        // filter rows and output columns [0, n1), then [n1, K)
+        Args a2 = a;
+        a.N = cs.n1;
+        a.ldc = g.K;
+        a.ntn = (a.N + p.t.bn - 1) / p.t.bn;
+        int err = go_mode<kFwd>(p.t, a, dim3(a.ntm * a.ntn), true, st);
+        if (err) return err;
+        a2.b += (size_t)cs.n1 * a2.K;
+        a2.c += cs.n1;
+        if (a2.bias) a2.bias += cs.n1;
+        a2.N = g.K - cs.n1;
+        a2.ldc = g.K;
+        a2.b_bytes = bytes_of((long)a2.N * a2.K);
+        a2.ntm = (a2.M + cs.p2.t.bm - 1) / cs.p2.t.bm;
+        a2.ntn = (a2.N + cs.p2.t.bn - 1) / cs.p2.t.bn;
+        a2.k_split = cs.p2.k_split;
+        return go_mode<kFwd>(cs.p2.t, a2, dim3(a2.ntm * a2.ntn), true, st);
+    }
     int err = go_mode<kFwd>(p.t, a, dim3(a.ntm * a.ntn, 1, p.splits), unit_geom(g), st);
     if (err || p.splits <= 1) return err;
     return reduce_partials(a.part, p.splits, n, a.part_stride, (bf16 *)y, (const bf16 *)bias, a.N, st);
@@ -1837,6 +1904,29 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bia
         a.cspart = reinterpret_cast<float *>(wsc + (direct ? 0 : al256((size_t)g.K * g.R * g.S * g.C * sizeof(bf16))));
         a.cs_cw = (g.K + a.ntn - 1) / a.ntn;
         a.cs_cw = (a.cs_cw + 7) / 8 * 8;
+    }
+    const ColSplit tsp = !cs && unit_geom(g) ? col_split(p, a.M, a.N, a.K, direct ? kAuto : kAutoKc) : ColSplit{};
+    if (tsp.n1 > 0) {
+        // dx columns [0, n1), then [n1, C): W in place is [K][C] (columns
+        // along its rows), the transposed copy [C][K] (one row per column)
+        Args a2 = a;
+        a.N = tsp.n1;
+        a.ldc = g.C;
+        a.ntn = (a.N + p.t.bn - 1) / p.t.bn;
+        int err = direct ? go_mode<kDgradN>(p.t, a, dim3(a.ntm * a.ntn), true, st)
+                         : go_mode<kDgrad>(p.t, a, dim3(a.ntm * a.ntn), true, st);
+        if (err) return err;
+        a2.b += direct ? (size_t)tsp.n1 : (size_t)tsp.n1 * g.K;
+        a2.c += tsp.n1;
+        if (a2.bias) a2.bias += tsp.n1;
+        a2.N = g.C - tsp.n1;
+        a2.ldc = g.C;
+        a2.b_bytes = direct ? bytes_of((long)g.K * g.C - tsp.n1) : bytes_of((long)a2.N * g.K);
+        a2.ntm = (a2.M + tsp.p2.t.bm - 1) / tsp.p2.t.bm;
+        a2.ntn = (a2.N + tsp.p2.t.bn - 1) / tsp.p2.t.bn;
+        a2.k_split = tsp.p2.k_split;
+        return direct ? go_mode<kDgradN>(tsp.p2.t, a2, dim3(a2.ntm * a2.ntn), true, st)
+                      : go_mode<kDgrad>(tsp.p2.t, a2, dim3(a2.ntm * a2.ntn), true, st);
     }
     const dim3 grid(a.ntm * a.ntn, 1, g.sh * g.sw * p.splits);
     int err = direct ? go_mode<kDgradN>(p.t, a, grid, unit_geom(g), st) : go_mode<kDgrad>(p.t, a, grid, unit_geom(g), st);

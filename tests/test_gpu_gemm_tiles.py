@@ -225,3 +225,42 @@ def test_conv_transpose_tiles(tile, case, dgrad_variant):
 def test_conv_transpose_tiles_split(tile, case, splits):
     """Split reductions: the bias is added once, by the reduce pass."""
     _convt_case(case, 8900 + 10 * case)
+
+
+@pytest.fixture
+def tail_split():
+    """Take the column split wherever it applies (MEMSAVE_GEMM_TAIL=on): the
+    output's leading tile columns that fill whole waves of 256 CUs in one
+    launch, the rest with another tile in a second launch."""
+    old = os.environ.get("MEMSAVE_GEMM_TAIL")
+    os.environ["MEMSAVE_GEMM_TAIL"] = "on"
+    yield
+    if old is None:
+        del os.environ["MEMSAVE_GEMM_TAIL"]
+    else:
+        os.environ["MEMSAVE_GEMM_TAIL"] = old
+
+
+@pytest.mark.parametrize("shape", [(8200, 136, 2312), (8192, 64, 3072), (8192, 72, 2304),
+                                   (8200, 2312, 136), (8192, 3072, 64), (8192, 2304, 72)])
+def test_linear_column_split(shape, dgrad_variant, tail_split):
+    """Outputs of more than one wave of 256 x 256 tiles with a partial last
+    wave: the forward (wide N_out; the bias added past the split column) and
+    the input gradient (wide K_in; W read in place, or through the transposed
+    copy), with remainders on the 256 x 128, 128 x 128 k-group and 128 x 192
+    tiles, one row from every 64-row band and the last rows, every column."""
+    M, Kin, Nout = shape
+    seed = 7300 + M + Nout
+    x = synth.normal((M, Kin), seed, dtype="bf16")
+    w = synth.normal((Nout, Kin), seed + 1, 0.05, dtype="bf16")
+    b = synth.normal((Nout,), seed + 2, 1.0, dtype="bf16")
+    y, rec = ms.layer_forward(ms.Linear(), dev(x, "bf16"), dev(w, "bf16"), dev(b, "bf16"), 1)
+    rng = np.random.default_rng(seed)
+    rows = np.unique(np.concatenate([np.arange(0, M, 64) + rng.integers(0, 64, (M + 63) // 64), [M - 2, M - 1]]))
+    rows = rows[rows < M]
+    yr = oracle.linear_forward(x[rows], w, b)
+    assert oracle.rel_err(oracle.linear_forward(x[rows], w, None), yr) > 0.2
+    check("y", host(y)[rows], yr, "bf16")
+    gy = synth.normal((M, Nout), seed + 3, dtype="bf16")
+    (gx,) = [g for g in ms.layer_backward(rec, dev(gy, "bf16")) if g is not None]
+    check("dX", host(gx)[rows], oracle.linear_input_grad(gy[rows], w), "bf16")
