@@ -34,6 +34,13 @@ struct RowColPlan {
 };
 
 constexpr int kRowsPerThread = 8;   // the unroll of the reduction's row loop
+// The BN-eval backward holds a batch of dy and x rows (two vectors per row):
+// eight rows took 200 VGPRs, so only two blocks fit on a CU and a stage-1
+// tensor's 784 blocks ran in two rounds; four rows take 128 (every block
+// resident at once; the mask-7 backward of 64 x 64 x 56 x 56 went from 31.2
+// to 27.4 us, the stem-sized one unchanged).  Each thread still walks
+// kRowsPerThread rows of its chunk, in two batches.
+constexpr int kRowsPerThreadBn = 4;
 
 RowColPlan plan_rowcol(int dtype, int64_t rows, int C, bool vec_ok, int target_blocks) {
     RowColPlan p;
@@ -228,7 +235,7 @@ __global__ __launch_bounds__(256) void rowcol_reduce_kernel(
         const int64_t r0 = (int64_t)blockIdx.y * chunk;
         const int64_t r1 = min(rows, r0 + chunk);
         int64_t r = r0 + rg;
-        constexpr int U = kRowsPerThread;
+        constexpr int U = MODE == 1 ? kRowsPerThreadBn : kRowsPerThread;
         const bool use_x = MODE == 1 && want_g;
         for (; r + (U - 1) * RG < r1; r += U * RG) {
             VecT<T, V> va[U], vx[U] = {};
