@@ -189,6 +189,31 @@ int copy4(const T *src, T *dst, Copy4 c, hipStream_t st) {
     return (int)hipGetLastError();
 }
 
+// Dimensions a and b are one dimension on both sides when a step of a lands
+// where a walk over all of b ends: s[a] == s[b] * ext[b] for the source and
+// the destination strides alike.  Merging them (extent ext[a] * ext[b], b's
+// strides) leaves the same element map in fewer dimensions: the H x W plane
+// of an NCHW <-> NHWC copy becomes one dimension, and the tiled path gets
+// whole 64 x 64 tiles instead of 64 x W ones (a 28-wide plane left more than
+// half of every tile empty).
+void merge_dims(Copy4 &c) {
+    for (bool changed = true; changed;) {
+        changed = false;
+        for (int a = 0; a < 4 && !changed; ++a) {
+            if (c.ext[a] <= 1) continue;
+            for (int b = 0; b < 4; ++b) {
+                if (b == a || c.ext[b] <= 1) continue;
+                if (c.ss[a] == c.ss[b] * c.ext[b] && c.ds[a] == c.ds[b] * c.ext[b]) {
+                    c.ext[b] *= c.ext[a];
+                    c.ext[a] = 1;
+                    changed = true;
+                    break;
+                }
+            }
+        }
+    }
+}
+
 }  // namespace
 
 int launch_copy4(int dtype, const void *src, const int64_t ext[4], const int64_t sstride[4], void *dst,
@@ -199,6 +224,7 @@ int launch_copy4(int dtype, const void *src, const int64_t ext[4], const int64_t
         c.ss[d] = sstride[d];
         c.ds[d] = dstride[d];
     }
+    merge_dims(c);
     hipStream_t st = (hipStream_t)stream;
     return dtype == kBF16 ? copy4(static_cast<const bf16 *>(src), static_cast<bf16 *>(dst), c, st)
                           : copy4(static_cast<const float *>(src), static_cast<float *>(dst), c, st);
