@@ -25,6 +25,7 @@ EXPORTS = (
     "ms_last_error", "ms_version", "ms_testing_fail_next_workspace", "ms_testing_live_records",
     "ms_profile_start", "ms_profile_read", "ms_relu_mask_bytes", "ms_relu_forward",
     "ms_dropout_blocks", "ms_dropout_forward", "ms_layer_backward_noalloc", "ms_noalloc_scratch_bytes",
+    "ms_testing_gemm_plan",
 )
 MS_PROF_FWD, MS_PROF_DGRAD, MS_PROF_WGRAD, MS_PROF_BN, MS_PROF_ACT, MS_PROF_RED = 1, 2, 4, 8, 16, 32
 
@@ -92,6 +93,8 @@ def configure(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.ms_testing_fail_next_workspace.restype = None
     lib.ms_testing_live_records.argtypes = []
     lib.ms_testing_live_records.restype = ctypes.c_int64
+    lib.ms_testing_gemm_plan.argtypes = [ctypes.c_int32, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]
+    lib.ms_testing_gemm_plan.restype = ctypes.c_int32
     lib.ms_profile_start.argtypes = [ctypes.c_uint32]
     lib.ms_profile_start.restype = ctypes.c_int
     lib.ms_profile_read.argtypes = [ctypes.c_uint32, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_double)]

@@ -40,6 +40,15 @@ int launch_conv_dgrad(int dtype, const ConvGeom &g, const void *dy, const void *
                       const void *bias, void *dx, void *ws, void *stream, void *db = nullptr,
                       bool *db_done = nullptr);
 
+// The bf16 GEMM planner's decision for one contraction of a convolution
+// (testing and diagnostics; launches nothing): pass 0 forward, 1 input
+// gradient, 2 weight gradient.  out[0..9] = tile rows, tile columns, waves,
+// LDS stages, k-groups, splits, input gradient reading W in place (1) or its
+// transposed copy (0), columns of the first launch of a column split (0:
+// none), the second launch's tile rows and columns.  Returns 0, or -1 when
+// the fast path does not take the contraction.
+int gemm_plan_info(int pass, const ConvGeom &g, int out[10]);
+
 // dw = weight gradient for grad dy and input x.  Needs conv_wgrad_workspace()
 // bytes of device workspace (may be 0).  When db is non-null the launcher may
 // also produce the bias gradient db[k] = sum over pixels of dy[.][k] from the

@@ -1353,8 +1353,9 @@ GemmPlan plan_gemm(long M, long N, long K, int z, int split_cap = 16, bool allow
 // its last wave of blocks partly empty (an 8192 x 3072 output is 384 tiles
 // of 256 x 256: one and a half waves of 256 CUs, so the second wave runs at
 // half occupancy for as long as the first).  The first launch takes the
-// leading n1 columns, the tile columns that fill whole waves on the plan's
-// tile; the second covers the remaining columns with the tile the planner
+// leading n1 columns, as many whole tile columns as fit in the waves the
+// plan's tiles fill completely; the second covers the remaining columns with
+// the tile the planner
 // picks for that narrower output (8192 x 1024: 256 tiles of 256 x 128).  The
 // two launches write disjoint column ranges of one output (row stride = the
 // full width) and neither needs workspace.  The split is taken when the
@@ -2018,4 +2019,40 @@ int conv_wgrad(const ConvGeom &g, const void *dy, const void *x, void *dw, void 
 }
 
 }  // namespace g2
+
+int gemm_plan_info(int pass, const ConvGeom &g, int out[10]) {
+    for (int i = 0; i < 10; ++i) out[i] = 0;
+    if (g.C % 8 != 0 || g.K % 8 != 0 || pass < 0 || pass > 2) return -1;
+    auto put = [&](const g2::Tile &t, int splits) {
+        out[0] = t.bm;
+        out[1] = t.bn;
+        out[2] = t.wr * t.wc * t.kg;
+        out[3] = t.stages;
+        out[4] = t.kg;
+        out[5] = splits;
+    };
+    auto put2 = [&](const g2::ColSplit &c) {
+        out[7] = c.n1;
+        if (c.n1 > 0) {
+            out[8] = c.p2.t.bm;
+            out[9] = c.p2.t.bn;
+        }
+    };
+    const bool unit = g2::unit_geom(g);
+    if (pass == 0) {
+        const g2::GemmPlan p = g2::fwd_plan(g);
+        put(p.t, p.splits);
+        if (unit) put2(g2::col_split(p, (long)g.N * g.P * g.Q, g.K, (long)g.R * g.S * g.C, g2::kAutoKc));
+    } else if (pass == 1) {
+        const g2::DgradChoice d = g2::dgrad_choice(g);
+        put(d.p.t, d.p.splits);
+        out[6] = d.direct ? 1 : 0;
+        if (unit) put2(g2::col_split(d.p, (long)g.N * g.H * g.W, g.C, g.K, d.direct ? g2::kAuto : g2::kAutoKc));
+    } else {
+        const g2::WgradPlan w = g2::wgrad_plan(g);
+        put(w.t, w.splits);
+    }
+    return 0;
+}
+
 }  // namespace ms

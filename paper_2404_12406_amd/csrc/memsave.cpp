@@ -1263,4 +1263,14 @@ void ms_testing_fail_next_workspace(int32_t n) { ms::workspace_fail_next(n); }
 
 int64_t ms_testing_live_records(void) { return g_records.load(); }
 
+int32_t ms_testing_gemm_plan(int32_t pass, const int32_t geom[13], int32_t out[10]) {
+    if (!geom || !out) return -1;
+    const ms::ConvGeom g{geom[0], geom[1], geom[2], geom[3], geom[4], geom[5], geom[6],
+                         geom[7], geom[8], geom[9], geom[10], geom[11], geom[12]};
+    int o[10];
+    const int r = ms::gemm_plan_info(pass, g, o);
+    for (int i = 0; i < 10; ++i) out[i] = o[i];
+    return r;
+}
+
 }  // extern "C"

@@ -236,6 +236,11 @@ void *scratch_get(size_t bytes, int *err) {
     return stand_in;
 }
 
+int gemm_plan_info(int, const ConvGeom &, int out[10]) {
+    for (int i = 0; i < 10; ++i) out[i] = 0;
+    return -1;
+}
+
 int device_last_error() { return 0; }
 
 void prof_mark(unsigned, void *, bool) {}
