@@ -329,11 +329,15 @@ ms_status ms_policy_account(const ms_layer *layer, const ms_tensor *x, const ms_
                             const ms_tensor *b, uint32_t mask, int32_t policy, ms_account *out);
 
 /*
- * Kernel timing (diagnostics).  While armed, the library brackets every
- * launch of the selected kernel kinds with a pair of HIP events recorded on
- * the launch stream, so the caller can read the kernels' own GPU time over a
- * region of its choice.  Only the contraction kernel itself is bracketed
- * (not the weight transpose or reduction kernels around it).  Kinds name
+ * Kernel timing (diagnostics).  While armed, the library times every
+ * launch of the selected kernel kinds with a pair of HIP events, so the
+ * caller can read the kernels' own GPU time over a region of its choice.
+ * The bf16 GEMM launches record their pair themselves, stamped at the
+ * dispatch's start and end (the kernel alone); the other kernels' pairs are
+ * recorded on the launch stream around the launch (they also span its
+ * dispatch latency).  A contraction whose output is split over two launches
+ * records two pairs.  Only the contraction kernel itself is timed (not the
+ * weight transpose or reduction kernels around it).  Kinds name
  * the contraction, not the layer's pass: a transposed convolution's forward
  * is an input-gradient GEMM and its input gradient a forward GEMM.
  *   MS_PROF_FWD   forward convolution / linear GEMM

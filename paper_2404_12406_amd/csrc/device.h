@@ -153,8 +153,15 @@ enum ProfKind : unsigned {
     kProfFwd = 1u, kProfDgrad = 2u, kProfWgrad = 4u, kProfBn = 8u, kProfAct = 16u, kProfRed = 32u
 };
 void prof_mark(unsigned kind, void *stream, bool begin);
-// Skip prof_mark on the calling thread while `off` (the no-allocation
-// backward records no events).
+// For a launch that records its own events (hipExtLaunchKernelGGL stamps the
+// dispatch's start and end, so the pair spans the kernel alone, not the
+// dispatch latency around it): prof_pair hands out a pair (hipEvent_t) when
+// `kind` is armed, and prof_pair_done files it after the launch (or returns
+// it to the pool when the launch failed).
+bool prof_pair(unsigned kind, void **begin, void **end);
+void prof_pair_done(unsigned kind, void *begin, void *end, bool launched);
+// Skip prof_mark and prof_pair on the calling thread while `off` (the
+// no-allocation backward records no events).
 void prof_thread_off(bool off);
 int prof_start(unsigned kinds);
 int prof_read(unsigned kind, uint64_t *launches, double *total_ms);

@@ -33,6 +33,8 @@
 #include <cstdlib>
 #include <cstring>
 
+#include <hip/hip_ext.h>
+
 #include "common.h"
 #include "limits.h"
 #include "../device.h"
@@ -1398,13 +1400,17 @@ ColSplit col_split(const GemmPlan &p, long M, long N, long K, const bool *set) {
 // floats of one split's partials (a multiple of 4: 16-byte aligned splits)
 int64_t part_stride(int64_t elems) { return (elems + 3) / 4 * 4; }
 
+// The launch records the profiling events itself when its kind is armed, so
+// a pair spans this kernel's execution alone.
 template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int OCC, bool UNIT, int KG = 1>
 int go(const Args &a, dim3 grid, hipStream_t st) {
     const unsigned pk = MODE == kFwd ? kProfFwd : MODE == kWgrad ? kProfWgrad : kProfDgrad;
-    prof_mark(pk, st, true);
-    hipLaunchKernelGGL((gemm_kernel<MODE, BM, BN, WR, WC, STAGES, OCC, UNIT, KG>), grid, dim3(WR * WC * KG * 64), 0, st, a);
+    void *eb = nullptr, *ee = nullptr;
+    const bool timed = prof_pair(pk, &eb, &ee);
+    hipExtLaunchKernelGGL((gemm_kernel<MODE, BM, BN, WR, WC, STAGES, OCC, UNIT, KG>), grid, dim3(WR * WC * KG * 64), 0,
+                          st, (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
     const int err = (int)hipGetLastError();
-    prof_mark(pk, st, false);
+    if (timed) prof_pair_done(pk, eb, ee, err == 0);
     return err;
 }
 

@@ -86,6 +86,36 @@ void prof_mark(unsigned kind, void *stream, bool begin) {
     }
 }
 
+bool prof_pair(unsigned kind, void **begin, void **end) {
+    *begin = *end = nullptr;
+    if (t_off || !(g_armed & kind)) return false;
+    std::lock_guard<std::mutex> lk(g_mu);
+    const int k = kind_index(kind);
+    if (k < 0 || !(g_armed & kind) || g_log[k].begin.size() >= kMaxLaunches) return false;
+    hipEvent_t b = take_event();
+    if (!b) return false;
+    hipEvent_t e = take_event();
+    if (!e) {
+        g_pool.push_back(b);
+        return false;
+    }
+    *begin = b;
+    *end = e;
+    return true;
+}
+
+void prof_pair_done(unsigned kind, void *begin, void *end, bool launched) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    const int k = kind_index(kind);
+    if (k >= 0 && launched && (g_armed & kind)) {
+        g_log[k].begin.push_back((hipEvent_t)begin);
+        g_log[k].end.push_back((hipEvent_t)end);
+    } else {
+        g_pool.push_back((hipEvent_t)begin);
+        g_pool.push_back((hipEvent_t)end);
+    }
+}
+
 int prof_start(unsigned kinds) {
     std::lock_guard<std::mutex> lk(g_mu);
     for (int i = 0; i < kKinds; ++i) {
