@@ -955,6 +955,250 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
     }
 }
 
+// ---------------------------------------------------------------- halo convolution
+// A stride-1 convolution of a 64-channel input whose filter fits in LDS: the
+// 3x3 64 -> 64 layers of a ResNet stage 1 (forward, and input gradient as the
+// correlation of dy with the flipped, transposed filter) and the stride-1
+// 4x4 form of the 3-channel stem's input gradient (2x2 pixel blocks).  The
+// implicit GEMM streams every input pixel through L2 once per tap (9 to 16
+// times the tensor), which is what bounds those layers.  Here a persistent
+// block keeps the whole filter in LDS and loads each output tile's input
+// neighbourhood (the tile plus R-1 rows and S-1 columns of halo) once, with
+// the next tile's halo loading into a second buffer while the current tile's
+// MFMAs run; every tap's A fragments are read from that copy.
+//
+// in[n][h][w][64] (NHWC); filt[NO][TAPS][64]: row n of tap t holds output
+// channel n's weights over the 64 input channels (flip: output tap t reads
+// filter tap TAPS-1-t); out[n][p][q][NO], out[p][q] = bias + sum over taps
+// (r, s) of filt . in[p - ph + r][q - pw + s], zero outside the input.
+// A block is 8 waves in two k-groups of four (two waves per SIMD, so one
+// wave's MFMAs cover the other's LDS reads).  The tile is TH x TW <= 256
+// output pixels (8 MFMA row tiles) by NP >= NO output channels (NP / 32
+// column tiles); wave w of a group owns row tiles 2w and 2w+1 and every
+// column tile, and group g takes the 16-deep slices g, g+2, ... of the
+// reduction (taps x 64 channels), so each wave reads one fragment per MFMA
+// (four reads for four MFMAs per slice).  Group 1 adds its sums into group
+// 0's through LDS, and group 0 writes the tile.  Pixels past TH x TW, past the image or past NO
+// channels are computed on zeros or clamped rows and never stored.
+struct HaloArgs {
+    const bf16 *in, *filt, *bias;
+    bf16 *out;
+    int H, W, P, Q;              // input and output extents
+    int R, S, ph, pw;            // taps, zero padding
+    int NO, flip;                // output channels stored; flipped taps
+    int TH, TW, tiles_w, tiles_img, tiles;
+    uint32_t in_bytes, filt_bytes, out_bytes;
+};
+
+constexpr int kHaloMaxPx = 320;                     // halo pixels per buffer (40 KB)
+
+template <int NP, int TAPS_MAX>
+__global__ __launch_bounds__(512, 1) void halo_conv_kernel(const HaloArgs A) {
+    constexpr int NW = 8;                           // waves: two k-groups of four
+    constexpr int FILT_BYTES = TAPS_MAX * NP * 128;
+    constexpr int HALO_BYTES = kHaloMaxPx * 128;
+    constexpr int TN = NP / 32;
+    constexpr int TM = 2;                           // row tiles per wave
+    constexpr int EPI_PITCH = NP + 8;               // staged row, bf16 elements
+    static_assert(FILT_BYTES + 2 * HALO_BYTES <= 160 * 1024, "LDS");
+    static_assert(4 * 32 * EPI_PITCH * 2 <= HALO_BYTES, "epilogue staging fits a halo buffer");
+    static_assert(4 * TN * 16 * 64 * 4 <= HALO_BYTES, "one row tile of group 1's sums fits a halo buffer");
+    __shared__ __attribute__((aligned(1024))) char smem[FILT_BYTES + 2 * HALO_BYTES];
+    char *const sF = smem;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int kg = wave >> 2, wl = wave & 3;          // k-group, wave within it
+    const int taps = A.R * A.S;
+    const int HWW = A.TW + A.S - 1;                   // halo row length
+    const int HP = (A.TH + A.R - 1) * HWW;            // halo pixels
+    const __amdgpu_buffer_rsrc_t rin = rsrc(A.in, A.in_bytes);
+    const __amdgpu_buffer_rsrc_t rf = rsrc(A.filt, A.filt_bytes);
+    const __amdgpu_buffer_rsrc_t ro = rsrc(A.out, A.out_bytes);
+    // the lane's 16-byte slot of a 128-byte row, and the logical k chunk it
+    // holds in row `row` (the chunk swizzle of frag_kc)
+    const int slot = lane & 7;
+    auto chunk_of = [&](int row) { return slot ^ swz_k(row); };
+
+    // bias of the lane's output columns (added in fp32 before the rounding),
+    // read before any LDS load is in flight
+    const int fr = lane & 31, fh = lane >> 5;
+    float bcol[TN][4][4];
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int n = j * 32 + 8 * q + 4 * fh + v;
+                bcol[j][q][v] = A.bias && n < A.NO ? (float)A.bias[n] : 0.f;
+            }
+
+    // ---- the filter, once: LDS row t * NP + n = output channel n at tap t
+    {
+        const int rows = taps * NP, ninstr = (rows + 7) / 8;
+        for (int j = wave; j < ninstr; j += NW) {
+            const int L = j * 8 + (lane >> 3);
+            const int t = L / NP, n = L - t * NP;
+            const int ts = A.flip ? taps - 1 - t : t;
+            const bool ok = t < taps && n < A.NO;
+            const uint32_t off = ok ? (uint32_t)((n * taps + ts) * 64 + chunk_of(n) * 8) * 2u : kOOB;
+            dma16<false>(rf, sF + j * 1024, off);
+        }
+    }
+    // ---- the halo of tile `tile` into buffer `b`
+    auto load_halo = [&](int tile, int b) {
+        char *dst = smem + FILT_BYTES + b * HALO_BYTES;
+        const int img = tile / A.tiles_img, rem = tile - img * A.tiles_img;
+        const int ty = rem / A.tiles_w, tx = rem - ty * A.tiles_w;
+        const int iy0 = ty * A.TH - A.ph, ix0 = tx * A.TW - A.pw;
+        const int ninstr = (HP + 7) / 8;
+        for (int j = wave; j < ninstr; j += NW) {
+            const int hp = j * 8 + (lane >> 3);
+            const int hy = hp / HWW, hx = hp - hy * HWW;
+            const int iy = iy0 + hy, ix = ix0 + hx;
+            const bool ok = hp < HP && (unsigned)iy < (unsigned)A.H && (unsigned)ix < (unsigned)A.W;
+            // element index below 2^31 (operand_fits), byte offset below kOOB
+            const uint32_t off = ok ? (uint32_t)(((img * A.H + iy) * A.W + ix) * 64 + chunk_of(hp) * 8) * 2u : kOOB;
+            dma16<false>(rin, dst + j * 1024, off);
+        }
+    };
+
+    // per-lane halo rows of the wave's row tiles (tap (0, 0))
+    const int npx = A.TH * A.TW;
+    int base[TM];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+        const int p = (TM * wl + i) * 32 + fr;
+        const int pp = p < npx ? p : 0;
+        const int oy = pp / A.TW;
+        base[i] = oy * HWW + (pp - oy * A.TW);
+    }
+    // output stores per wave and tile: a fixed count (masked lanes store past
+    // the output's buffer range, which the hardware drops), so the wait for a
+    // halo can leave the previous tile's stores in flight
+    constexpr int NPASS = NP / 16;                  // 32 rows x NP/8 pieces over 64 lanes
+    int tile = blockIdx.x;
+    if (tile < A.tiles) load_halo(tile, 0);
+    for (int it = 0; tile < A.tiles; ++it, tile += gridDim.x) {
+        const int b = it & 1;
+        const char *sH = smem + FILT_BYTES + b * HALO_BYTES;
+        // this wave's loads of the filter and of this halo landed (group 0's
+        // stores issued after them may still be in flight)
+        if (it == 0 || kg == 1) wait_vmcnt<0>();
+        else wait_vmcnt<TM * NPASS>();
+        wait_lgkm0();
+        __syncthreads();        // every wave's loads landed; the other buffer is free
+        const int next = tile + gridDim.x;
+        if (next < A.tiles) load_halo(next, b ^ 1);   // lands while this tile computes
+
+        floatx16 acc[TM][TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+        bf16x8 fa[2][TM], fb[2][TN];
+        // fragments of one slice: the row tiles' halo rows at tap (r, s) and
+        // the filter rows of tap t, chunk pair `sub`
+        auto read = [&](int r, int s, int t, int sub, int buf) {
+            const int shift = r * HWW + s;
+#pragma unroll
+            for (int i = 0; i < TM; ++i) fa[buf][i] = frag_kc(sH, base[i] + shift, sub, lane);
+            const char *sFt = sF + t * NP * 128;
+#pragma unroll
+            for (int j = 0; j < TN; ++j) fb[buf][j] = frag_kc(sFt, j * 32 + fr, sub, lane);
+        };
+        auto mfma = [&](int buf) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[buf][j], fa[buf][i], acc[i][j], 0, 0, 0);
+        };
+        // group kg takes slices kg and kg + 2 of every tap; the next slice's
+        // fragments are read while a slice's MFMAs run
+        read(0, 0, 0, kg, 0);
+        for (int t = 0, r = 0, s = 0; t < taps; ++t) {
+            int r1 = r, s1 = s + 1;                 // the next tap
+            if (s1 == A.S) {
+                s1 = 0;
+                ++r1;
+            }
+            read(r, s, t, kg + 2, 1);
+            mfma(0);
+            if (t + 1 < taps) read(r1, s1, t + 1, kg, 0);
+            mfma(1);
+            r = r1;
+            s = s1;
+        }
+
+        // ---- group 1's sums into group 0's, one row tile at a time, through
+        // this tile's halo buffer (every wave is done reading it after the
+        // first barrier)
+        float *red = reinterpret_cast<float *>(smem + FILT_BYTES + b * HALO_BYTES);
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            wait_lgkm0();
+            __syncthreads();
+            if (kg == 1) {
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) red[((wl * TN + j) * 16 + v) * 64 + lane] = acc[i][j][v];
+            }
+            __syncthreads();
+            if (kg == 0) {
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) acc[i][j][v] += red[((wl * TN + j) * 16 + v) * 64 + lane];
+            }
+        }
+        wait_lgkm0();
+        __syncthreads();   // the sums are read before the staging reuses the buffer
+        if (kg == 1) continue;
+
+        // ---- epilogue (group 0): stage 32 rows per wave in this tile's halo
+        // buffer, 16-byte stores
+        const int img = tile / A.tiles_img, rem = tile - img * A.tiles_img;
+        const int ty0 = (rem / A.tiles_w) * A.TH, tx0 = (rem - (rem / A.tiles_w) * A.tiles_w) * A.TW;
+        bf16 *stage = reinterpret_cast<bf16 *>(smem + FILT_BYTES + b * HALO_BYTES) + wl * 32 * EPI_PITCH;
+        constexpr int SEG = NP / 8;                 // 16-byte pieces of a staged pixel row
+        typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    bf16x4 o;
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) o[v] = (bf16)(acc[i][j][4 * q + v] + bcol[j][q][v]);
+                    *reinterpret_cast<bf16x4 *>(stage + fr * EPI_PITCH + j * 32 + 8 * q + 4 * fh) = o;
+                }
+            wait_lgkm0();
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int ps = 0; ps < NPASS; ++ps) {
+                const int lin = ps * 64 + lane;
+                const int rl = lin / SEG, cl = (lin % SEG) * 8;
+                const int p = (TM * wl + i) * 32 + rl;
+                const int oy = p / A.TW, ox = p - oy * A.TW;
+                const int y = ty0 + oy, x = tx0 + ox;
+                const u32x4 v = *reinterpret_cast<const u32x4 *>(stage + rl * EPI_PITCH + cl);
+                const bool ok = cl < A.NO && p < npx && y < A.P && x < A.Q;
+                // element index below 2^31 (operand_fits on the output)
+                const uint32_t off = ok ? (uint32_t)(((img * A.P + y) * A.Q + x) * A.NO + cl) * 2u : kOOB;
+                __builtin_amdgcn_raw_buffer_store_b128(v, ro, (int)off, 0, 0);
+            }
+            wait_lgkm0();
+            __builtin_amdgcn_wave_barrier();
+        }
+    }
+    wait_vmcnt<0>();   // no load of this block is still writing LDS when it ends
+}
+
 // Wt[c][rs][k] = W[k][rs][c]: the input gradient reads the (frozen) filter
 // with its reduction index k contiguous.  A block moves a 64 (k) x 64 (c)
 // tile of one tap rs through LDS; global reads and writes are 16-byte
@@ -1660,6 +1904,83 @@ int reduce_partials(const float *part, int splits, int64_t n, int64_t pstride, b
     return (int)hipGetLastError();
 }
 
+// ---------------------------------------------------------------- halo convolution (host)
+// MEMSAVE_CONV_HALO=off turns the halo kernel off (testing knob: the tests run
+// both paths).
+bool halo_enabled() {
+    const char *e = getenv("MEMSAVE_CONV_HALO");
+    return !(e && strcmp(e, "off") == 0);
+}
+
+// Output tile of the halo kernel for an output of P x Q pixels with R x S
+// taps: the width split into the fewest column tiles of at most 32, then as
+// many rows as fit both 256 pixels and a halo of at most kHaloMaxPx pixels.
+// False when no tile fits.
+bool halo_tile(int Q, int R, int S, int *TH, int *TW) {
+    if (Q <= 0) return false;
+    const int ntw = (Q + 31) / 32;
+    const int tw = (Q + ntw - 1) / ntw;
+    const int th = std::min(256 / tw, kHaloMaxPx / (tw + S - 1) - (R - 1));
+    if (th < 1) return false;
+    *TH = th;
+    *TW = tw;
+    return true;
+}
+
+// The halo kernel's instantiations: up to 64 output channels with up to 9
+// taps, or up to 32 with up to 16.
+bool halo_shape_ok(int NO, int taps) {
+    return NO % 8 == 0 && NO > 0 && ((NO <= 32 && taps <= 16) || (NO <= 64 && taps <= 9));
+}
+
+// in[N][H][W][64] -> out[N][P][Q][NO] (see halo_conv_kernel).
+int run_halo(const bf16 *in, int N, int H, int W, const bf16 *filt, const bf16 *bias, int NO, int R, int S, int ph,
+             int pw, bool flip, bf16 *out, int P, int Q, hipStream_t st) {
+    HaloArgs a{};
+    a.in = in; a.filt = filt; a.bias = bias; a.out = out;
+    a.H = H; a.W = W; a.P = P; a.Q = Q; a.R = R; a.S = S; a.ph = ph; a.pw = pw;
+    a.NO = NO; a.flip = flip ? 1 : 0;
+    if (!halo_tile(Q, R, S, &a.TH, &a.TW)) return (int)hipErrorInvalidValue;
+    const int tiles_h = (P + a.TH - 1) / a.TH;
+    a.tiles_w = (Q + a.TW - 1) / a.TW;
+    a.tiles_img = tiles_h * a.tiles_w;
+    const long tiles = (long)N * a.tiles_img;
+    if (tiles == 0) return 0;
+    if (tiles > INT32_MAX) return (int)hipErrorInvalidValue;
+    a.tiles = (int)tiles;
+    a.in_bytes = bytes_of((long)N * H * W * 64);
+    a.filt_bytes = bytes_of((long)NO * R * S * 64);
+    if (!operand_fits((long)N * P * Q * NO)) return (int)hipErrorInvalidValue;
+    a.out_bytes = bytes_of((long)N * P * Q * NO);
+    const dim3 grid((unsigned)std::min<long>(tiles, kCUs));
+    const unsigned pk = flip ? kProfDgrad : kProfFwd;
+    void *eb = nullptr, *ee = nullptr;
+    const bool timed = prof_pair(pk, &eb, &ee);
+    if (NO <= 32)
+        hipExtLaunchKernelGGL((halo_conv_kernel<32, 16>), grid, dim3(512), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
+    else
+        hipExtLaunchKernelGGL((halo_conv_kernel<64, 9>), grid, dim3(512), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
+    const int err = (int)hipGetLastError();
+    if (timed) prof_pair_done(pk, eb, ee, err == 0);
+    return err;
+}
+
+// Forward: stride 1, 64 input channels, the filter within the kernel's
+// instantiations, more than one tap.
+bool halo_fwd_applies(const ConvGeom &g) {
+    return halo_enabled() && g.C == 64 && g.sh == 1 && g.sw == 1 && g.R * g.S > 1 && halo_shape_ok(g.K, g.R * g.S) &&
+           g.P > 0 && g.Q > 0 && operand_fits((long)g.N * g.P * g.Q * g.K) &&
+           [&] { int th, tw; return halo_tile(g.Q, g.R, g.S, &th, &tw); }();
+}
+
+// Input gradient: the correlation of dy (64 channels) with the flipped,
+// transposed filter and padding R - 1 - ph (stride 1).
+bool halo_dgrad_applies(const ConvGeom &g) {
+    return halo_enabled() && g.K == 64 && g.sh == 1 && g.sw == 1 && g.R * g.S > 1 && halo_shape_ok(g.C, g.R * g.S) &&
+           g.ph <= g.R - 1 && g.pw <= g.S - 1 && g.H > 0 && g.W > 0 && operand_fits((long)g.N * g.H * g.W * g.C) &&
+           [&] { int th, tw; return halo_tile(g.W, g.R, g.S, &th, &tw); }();
+}
+
 GemmPlan fwd_plan(const ConvGeom &g) {
     return plan_gemm((long)g.N * g.P * g.Q, g.K, (long)g.R * g.S * g.C, 1, 16, true, kKgAuto, kAutoKc);
 }
@@ -1704,6 +2025,9 @@ int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, 
     }
     if (!al16(x) || !al16(w) || !al16(y)) return -1;
     if (!operand_fits((long)g.N * g.H * g.W * g.C) || !operand_fits((long)g.K * g.R * g.S * g.C)) return -1;
+    if (halo_fwd_applies(g))
+        return run_halo((const bf16 *)x, g.N, g.H, g.W, (const bf16 *)w, (const bf16 *)bias, g.K, g.R, g.S, g.ph, g.pw,
+                        false, (bf16 *)y, g.P, g.Q, st);
     Args a{};
     a.a = (const bf16 *)x; a.b = (const bf16 *)w; a.c = (bf16 *)y; a.g = g;
     a.M = g.N * g.P * g.Q; a.N = g.K; a.K = g.R * g.S * g.C;
@@ -1806,6 +2130,7 @@ int64_t colsum_rows(const ConvGeom &g, const Tile &t) {
 // transposed filter (when used), then split-K partials indexed by dx pixel,
 // then (with_db, when the column sums ride along) their partial rows
 size_t dgrad_core_workspace(const ConvGeom &g, bool with_db) {
+    if (halo_dgrad_applies(g)) return al256((size_t)g.K * g.R * g.S * g.C * sizeof(bf16));   // the transposed filter
     const DgradChoice dc = dgrad_choice(g);
     const GemmPlan &p = dc.p;
     size_t ws = dc.direct ? 0 : al256((size_t)g.K * g.R * g.S * g.C * sizeof(bf16));
@@ -1875,6 +2200,17 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bia
     }
     if (!al16(dy) || !al16(w) || !al16(dx)) return -1;
     if (!operand_fits((long)g.N * g.P * g.Q * g.K) || !operand_fits((long)g.K * g.R * g.S * g.C)) return -1;
+    if (halo_dgrad_applies(g)) {
+        // the correlation of dy with the flipped, transposed filter Wt[c][r][s][k]
+        if (!ws || !al16(ws)) return -1;
+        bf16 *wt = reinterpret_cast<bf16 *>(ws);
+        hipLaunchKernelGGL(transpose_krsc_kernel, dim3((g.C + 63) / 64, (g.K + 63) / 64, g.R * g.S), dim3(256), 0, st,
+                           (const bf16 *)w, wt, g.K, g.R * g.S, g.C);
+        const int err = (int)hipGetLastError();
+        if (err) return err;
+        return run_halo((const bf16 *)dy, g.N, g.P, g.Q, wt, (const bf16 *)bias, g.C, g.R, g.S, g.R - 1 - g.ph,
+                        g.S - 1 - g.pw, true, (bf16 *)dx, g.H, g.W, st);
+    }
     const DgradChoice dc = dgrad_choice(g);
     const bool direct = dc.direct;
     const GemmPlan &p = dc.p;
