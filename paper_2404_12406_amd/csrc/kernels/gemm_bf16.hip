@@ -1914,8 +1914,9 @@ bool halo_enabled() {
 
 // Output tile of the halo kernel for an output of P x Q pixels with R x S
 // taps: the width split into the fewest column tiles of at most 32, then as
-// many rows as fit both 256 pixels and a halo of at most kHaloMaxPx pixels.
-// False when no tile fits.
+// many rows as fit both 256 pixels and a halo of at most kHaloMaxPx pixels
+// (a tile always computes 256 rows of MFMA tiles, so the largest tile is the
+// cheapest per pixel).  False when no tile fits.
 bool halo_tile(int Q, int R, int S, int *TH, int *TW) {
     if (Q <= 0) return false;
     const int ntw = (Q + 31) / 32;
