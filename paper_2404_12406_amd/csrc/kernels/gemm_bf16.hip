@@ -1019,19 +1019,31 @@ __global__ __launch_bounds__(512, 1) void halo_conv_kernel(const HaloArgs A) {
     const int slot = lane & 7;
     auto chunk_of = [&](int row) { return slot ^ swz_k(row); };
 
-    // bias of the lane's output columns (added in fp32 before the rounding),
-    // read before any LDS load is in flight
+    // bias of the lane's output columns (added in fp32 before the rounding):
+    // 4 consecutive channels per load through a descriptor of NO entries
+    // (none without a bias), so columns past NO read zeros and every load is
+    // in flight at once
     const int fr = lane & 31, fh = lane >> 5;
     float bcol[TN][4][4];
+    {
+        const __amdgpu_buffer_rsrc_t rb = rsrc(A.bias, A.bias ? (uint32_t)A.NO * 2u : 0u);
+        typedef unsigned v2u32 __attribute__((ext_vector_type(2)));
+        v2u32 bv[TN][4];
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+        for (int j = 0; j < TN; ++j)
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
+            for (int q = 0; q < 4; ++q)
+                bv[j][q] = __builtin_amdgcn_raw_buffer_load_b64(rb, (j * 32 + 8 * q + 4 * fh) * 2, 0, 0);
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int n = j * 32 + 8 * q + 4 * fh + v;
-                bcol[j][q][v] = A.bias && n < A.NO ? (float)A.bias[n] : 0.f;
-            }
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const uint32_t w = bv[j][q][v >> 1];
+                    bcol[j][q][v] = __uint_as_float((v & 1) ? (w & 0xffff0000u) : (w << 16));
+                }
+    }
 
     // ---- the filter, once: LDS row t * NP + n = output channel n at tap t
     {
@@ -1087,7 +1099,7 @@ __global__ __launch_bounds__(512, 1) void halo_conv_kernel(const HaloArgs A) {
         if (it == 0 || kg == 1) wait_vmcnt<0>();
         else wait_vmcnt<TM * NPASS>();
         wait_lgkm0();
-        __syncthreads();        // every wave's loads landed; the other buffer is free
+        block_sync<true>();     // every wave's loads landed; the other buffer is free
         const int next = tile + gridDim.x;
         if (next < A.tiles) load_halo(next, b ^ 1);   // lands while this tile computes
 
@@ -1140,14 +1152,15 @@ __global__ __launch_bounds__(512, 1) void halo_conv_kernel(const HaloArgs A) {
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
             wait_lgkm0();
-            __syncthreads();
+            block_sync<true>();
             if (kg == 1) {
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
 #pragma unroll
                     for (int v = 0; v < 16; ++v) red[((wl * TN + j) * 16 + v) * 64 + lane] = acc[i][j][v];
             }
-            __syncthreads();
+            wait_lgkm0();
+            block_sync<true>();
             if (kg == 0) {
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
@@ -1156,7 +1169,7 @@ __global__ __launch_bounds__(512, 1) void halo_conv_kernel(const HaloArgs A) {
             }
         }
         wait_lgkm0();
-        __syncthreads();   // the sums are read before the staging reuses the buffer
+        block_sync<true>();   // the sums are read before the staging reuses the buffer
         if (kg == 1) continue;
 
         // ---- epilogue (group 0): stage 32 rows per wave in this tile's halo
