@@ -892,6 +892,28 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
 #pragma unroll
                     for (int v = 0; v < 4; ++v) bcol[j][q][v] = (float)b4[v];
                 }
+        } else if (P.bias && (N & 3) == 0) {
+            // 4 consecutive columns per load through a descriptor of N entries
+            // (a load is wholly in range or past it and reads zeros), every
+            // load in flight at once: element-wise loads behind a range test
+            // each waited for the one before
+            typedef unsigned v2u32 __attribute__((ext_vector_type(2)));
+            const __amdgpu_buffer_rsrc_t rbias = rsrc(P.bias, (uint32_t)N * 2u);
+            v2u32 bv[TN][4];
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    bv[j][q] = __builtin_amdgcn_raw_buffer_load_b64(rbias, (n0 + wn0 + j * 32 + 8 * q + 4 * fh) * 2, 0, 0);
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const uint32_t w = bv[j][q][v >> 1];
+                        bcol[j][q][v] = __uint_as_float((v & 1) ? (w & 0xffff0000u) : (w << 16));
+                    }
         } else if (P.bias) {
 #pragma unroll
             for (int j = 0; j < TN; ++j)
