@@ -80,6 +80,32 @@ template <typename T> struct VecT<T, 16 / sizeof(T)> {
     __device__ __forceinline__ void store(T *p) const { *reinterpret_cast<u32x4 *>(p) = u; }
 };
 
+// Per-channel parameters (BN statistics, gamma, beta; any may be absent)
+// read through a buffer descriptor of n elements, or of none when the array
+// is absent, so a read past the end or of an absent array returns zeros and
+// is issued without a branch.  Element-wise reads behind a null test each
+// sat in its own branch, and every one waited for the one before.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t param_rsrc(const void *p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, p ? (int)bytes : 0, 0x00020000);
+}
+template <typename T>
+__device__ __forceinline__ float param_at(__amdgpu_buffer_rsrc_t r, uint32_t i) {
+    if constexpr (sizeof(T) == 2) return __uint_as_float((uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)(i * 2), 0, 0) << 16);
+    else return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)(i * 4), 0, 0));
+}
+// V consecutive parameters starting at element i (16 bytes when V > 1)
+template <typename T, int V>
+__device__ __forceinline__ void params_at(__amdgpu_buffer_rsrc_t r, uint32_t i, float (&out)[V]) {
+    if constexpr (V == 1) {
+        out[0] = param_at<T>(r, i);
+    } else {
+        VecT<T, V> v;
+        v.u = __builtin_amdgcn_raw_buffer_load_b128(r, (int)(i * sizeof(T)), 0, 0);
+#pragma unroll
+        for (int e = 0; e < V; ++e) out[e] = to_f32(v.e[e]);
+    }
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------- BN-eval fwd
@@ -147,21 +173,26 @@ __global__ __launch_bounds__(256) void bn_nchw_kernel(const T *__restrict__ x, c
                                                       const T *__restrict__ beta, float eps, uint32_t nvec,
                                                       uint32_t vpp, uint32_t C, T *__restrict__ y) {
     const uint32_t i0 = blockIdx.x * 256u * kBnU + threadIdx.x;
+    const __amdgpu_buffer_rsrc_t rm = param_rsrc(mean, C * sizeof(T)), rv = param_rsrc(var, C * sizeof(T));
+    const __amdgpu_buffer_rsrc_t rg = param_rsrc(gamma, C * sizeof(T)), rb = param_rsrc(beta, C * sizeof(T));
     VecT<T, V> v[kBnU];
+    float pm[kBnU], pv[kBnU], pg[kBnU], pb[kBnU];
 #pragma unroll
     for (int u = 0; u < kBnU; ++u) {
         const uint32_t i = i0 + u * 256u;
         if (i < nvec) v[u].load(x + (size_t)i * V);
+        const uint32_t c = ((i < nvec ? i : 0) / vpp) % C;
+        pm[u] = param_at<T>(rm, c);
+        pv[u] = param_at<T>(rv, c);
+        pg[u] = param_at<T>(rg, c);
+        pb[u] = param_at<T>(rb, c);
     }
 #pragma unroll
     for (int u = 0; u < kBnU; ++u) {
         const uint32_t i = i0 + u * 256u;
         if (i >= nvec) continue;
-        const uint32_t c = (i / vpp) % C;
-        const float g = gamma ? to_f32(gamma[c]) : 1.f;
-        const float b = beta ? to_f32(beta[c]) : 0.f;
-        const float m = mean ? to_f32(mean[c]) : 0.f;
-        const float sc = g * rsqrtf(to_f32(var[c]) + eps), sh = b - m * sc;
+        const float g = gamma ? pg[u] : 1.f;
+        const float sc = g * rsqrtf(pv[u] + eps), sh = pb[u] - pm[u] * sc;
 #pragma unroll
         for (int e = 0; e < V; ++e) v[u].e[e] = from_f32<T>(fmaf(to_f32(v[u].e[e]), sc, sh));
         v[u].store(y + (size_t)i * V);
@@ -224,11 +255,15 @@ __global__ __launch_bounds__(256) void rowcol_reduce_kernel(
             // var is read only when dx or dgamma is requested: a beta-only
             // record does not keep the running statistics (var == nullptr).
             if (dx || want_g) {
+                float pv[V], pg[V], pm[V];
+                params_at<T, V>(param_rsrc(var, C * sizeof(T)), c0, pv);
+                params_at<T, V>(param_rsrc(gamma, C * sizeof(T)), c0, pg);
+                params_at<T, V>(param_rsrc(want_g ? mean : nullptr, C * sizeof(T)), c0, pm);
 #pragma unroll
                 for (int e = 0; e < V; ++e) {
-                    inv[e] = 1.f / sqrtf(to_f32(var[c0 + e]) + eps);
-                    s[e] = (gamma ? to_f32(gamma[c0 + e]) : 1.f) * inv[e];
-                    mu[e] = want_g ? to_f32(mean[c0 + e]) : 0.f;
+                    inv[e] = 1.f / sqrtf(pv[e] + eps);
+                    s[e] = (gamma ? pg[e] : 1.f) * inv[e];
+                    mu[e] = pm[e];
                 }
             }
         }
