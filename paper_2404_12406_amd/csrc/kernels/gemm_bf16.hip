@@ -915,13 +915,17 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
                         bcol[j][q][v] = __uint_as_float((v & 1) ? (w & 0xffff0000u) : (w << 16));
                     }
         } else if (P.bias) {
+            // N not a multiple of 4: one column per load, through the same
+            // kind of descriptor, so every load is still issued at once
+            const __amdgpu_buffer_rsrc_t rbias = rsrc(P.bias, (uint32_t)N * 2u);
 #pragma unroll
             for (int j = 0; j < TN; ++j)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     const int n = n0 + wn0 + j * 32 + 8 * q + 4 * fh;
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) bcol[j][q][v] = n + v < N ? (float)P.bias[n + v] : 0.f;
+                    for (int v = 0; v < 4; ++v)
+                        bcol[j][q][v] = __uint_as_float((uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rbias, (n + v) * 2, 0, 0) << 16);
                 }
         }
     }
