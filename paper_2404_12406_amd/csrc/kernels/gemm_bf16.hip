@@ -1402,19 +1402,28 @@ __global__ __launch_bounds__(256) void pack_block_filter_kernel(const bf16 *__re
 
 // the adjoint of the input packing:
 // dx[n][h][w][c] = dxq[n][(h + ph) / 2][(w + pw) / 2][8 ((h + ph) % 2) + 4 ((w + pw) % 2) + c]
-__global__ __launch_bounds__(256) void unpack_blocks_kernel(const bf16 *__restrict__ dxq, int64_t NH, int H, int W,
+// One thread per (image row n, h; block column j): the 16-byte half of block
+// (n, (h + ph) / 2, j) that holds row h carries both of its columns,
+// w = 2j - pw and 2j + 1 - pw, so each output pixel is written exactly once.
+// 32-bit indices: the host checks that the rows x block columns fit.
+__global__ __launch_bounds__(256) void unpack_blocks_kernel(const bf16 *__restrict__ dxq, uint32_t NH, int H, int W,
                                                             int C, int Hq, int Wq, int ph, int pw,
                                                             bf16 *__restrict__ dx) {
-    const int64_t total = NH * W * C;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t pix = i / C;
-        const int c = (int)(i - pix * C);
-        const int64_t nh = pix / W;
-        const int w = (int)(pix - nh * W) + pw;
-        const int64_t n = nh / H;
-        const int h = (int)(nh - n * H) + ph;
-        dx[i] = dxq[((n * Hq + h / 2) * Wq + w / 2) * 16 + 8 * (h & 1) + 4 * (w & 1) + c];
+    const uint32_t total = NH * (uint32_t)Wq;
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+        const uint32_t nh = i / (uint32_t)Wq, j = i - nh * (uint32_t)Wq;
+        const uint32_t n = nh / (uint32_t)H, h = nh - n * (uint32_t)H;
+        const uint32_t hp = h + (uint32_t)ph;
+        const Vec16<bf16> v = load16(dxq + (((size_t)n * Hq + hp / 2) * Wq + j) * 16 + 8 * (hp & 1));
+        bf16 *row = dx + (size_t)nh * W * C;
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const int w = 2 * (int)j + b - pw;
+            if (w < 0 || w >= W) continue;
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                if (c < C) row[w * C + c] = v.e[4 * b + c];
+        }
     }
 }
 
@@ -1847,10 +1856,11 @@ int pack_block_filter(const ConvGeom &g, const void *w, void *wq, hipStream_t st
 }
 
 int unpack_blocks(const ConvGeom &g, const void *dxq, void *dx, hipStream_t st) {
-    const int64_t NH = (int64_t)g.N * g.H, work = NH * g.W * g.C;
+    const int64_t NH = (int64_t)g.N * g.H, work = NH * pair_width(g);
     if (work == 0) return 0;
-    hipLaunchKernelGGL(unpack_blocks_kernel, dim3(launch_grid(work)), dim3(256), 0, st, (const bf16 *)dxq, NH, g.H,
-                       g.W, g.C, block_height(g), pair_width(g), g.ph, g.pw, (bf16 *)dx);
+    if (work > INT32_MAX) return (int)hipErrorInvalidValue;
+    hipLaunchKernelGGL(unpack_blocks_kernel, dim3(launch_grid(work)), dim3(256), 0, st, (const bf16 *)dxq,
+                       (uint32_t)NH, g.H, g.W, g.C, block_height(g), pair_width(g), g.ph, g.pw, (bf16 *)dx);
     return (int)hipGetLastError();
 }
 
