@@ -997,14 +997,16 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
 // channel n's weights over the 64 input channels (flip: output tap t reads
 // filter tap TAPS-1-t); out[n][p][q][NO], out[p][q] = bias + sum over taps
 // (r, s) of filt . in[p - ph + r][q - pw + s], zero outside the input.
-// A block is 8 waves in two k-groups of four (two waves per SIMD, so one
-// wave's MFMAs cover the other's LDS reads).  The tile is TH x TW <= 256
-// output pixels (8 MFMA row tiles) by NP >= NO output channels (NP / 32
-// column tiles); wave w of a group owns row tiles 2w and 2w+1 and every
-// column tile, and group g takes the 16-deep slices g, g+2, ... of the
-// reduction (taps x 64 channels), so each wave reads one fragment per MFMA
-// (four reads for four MFMAs per slice).  Group 1 adds its sums into group
-// 0's through LDS, and group 0 writes the tile.  Pixels past TH x TW, past the image or past NO
+// A block is KG k-groups of four waves.  The tile is TH x TW <= 256 output
+// pixels (8 MFMA row tiles) by NP >= NO output channels (NP / 32 column
+// tiles); wave w of a group owns row tiles 2w and 2w+1 and every column
+// tile.  With 64 columns (KG = 1) the four waves, one per SIMD, each run
+// every 16-deep slice of the reduction (taps x 64 channels) and write their
+// own rows: four fragment reads per four MFMAs.  With 32 columns (KG = 2,
+// the stem's 16-tap input gradient) that would be three reads per two MFMAs,
+// so group g takes the slices g, g+2, ... instead (two waves per SIMD, one
+// fragment per MFMA), group 1 adds its sums into group 0's through LDS, and
+// group 0 writes the tile.  Pixels past TH x TW, past the image or past NO
 // channels are computed on zeros or clamped rows and never stored.
 struct HaloArgs {
     const bf16 *in, *filt, *bias;
@@ -1018,9 +1020,9 @@ struct HaloArgs {
 
 constexpr int kHaloMaxPx = 320;                     // halo pixels per buffer (40 KB)
 
-template <int NP, int TAPS_MAX>
-__global__ __launch_bounds__(512, 1) void halo_conv_kernel(const HaloArgs A) {
-    constexpr int NW = 8;                           // waves: two k-groups of four
+template <int NP, int TAPS_MAX, int KG>
+__global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A) {
+    constexpr int NW = 4 * KG;                      // waves: KG k-groups of four
     constexpr int FILT_BYTES = TAPS_MAX * NP * 128;
     constexpr int HALO_BYTES = kHaloMaxPx * 128;
     constexpr int TN = NP / 32;
@@ -1028,12 +1030,12 @@ __global__ __launch_bounds__(512, 1) void halo_conv_kernel(const HaloArgs A) {
     constexpr int EPI_PITCH = NP + 8;               // staged row, bf16 elements
     static_assert(FILT_BYTES + 2 * HALO_BYTES <= 160 * 1024, "LDS");
     static_assert(4 * 32 * EPI_PITCH * 2 <= HALO_BYTES, "epilogue staging fits a halo buffer");
-    static_assert(4 * TN * 16 * 64 * 4 <= HALO_BYTES, "one row tile of group 1's sums fits a halo buffer");
+    static_assert(KG == 1 || 4 * TN * 16 * 64 * 4 <= HALO_BYTES, "one row tile of group 1's sums fits a halo buffer");
     __shared__ __attribute__((aligned(1024))) char smem[FILT_BYTES + 2 * HALO_BYTES];
     char *const sF = smem;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int kg = wave >> 2, wl = wave & 3;          // k-group, wave within it
+    const int kg = KG == 2 ? wave >> 2 : 0, wl = wave & 3;   // k-group, wave within it
     const int taps = A.R * A.S;
     const int HWW = A.TW + A.S - 1;                   // halo row length
     const int HP = (A.TH + A.R - 1) * HWW;            // halo pixels
@@ -1154,8 +1156,8 @@ __global__ __launch_bounds__(512, 1) void halo_conv_kernel(const HaloArgs A) {
                 for (int j = 0; j < TN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[buf][j], fa[buf][i], acc[i][j], 0, 0, 0);
         };
-        // group kg takes slices kg and kg + 2 of every tap; the next slice's
-        // fragments are read while a slice's MFMAs run
+        // group kg takes slices kg and kg + 2 of every tap (one group: all
+        // four); the next slice's fragments are read while a slice's MFMAs run
         read(0, 0, 0, kg, 0);
         for (int t = 0, r = 0, s = 0; t < taps; ++t) {
             int r1 = r, s1 = s + 1;                 // the next tap
@@ -1163,8 +1165,17 @@ __global__ __launch_bounds__(512, 1) void halo_conv_kernel(const HaloArgs A) {
                 s1 = 0;
                 ++r1;
             }
-            read(r, s, t, kg + 2, 1);
-            mfma(0);
+            if constexpr (KG == 2) {
+                read(r, s, t, kg + 2, 1);
+                mfma(0);
+            } else {
+                read(r, s, t, 1, 1);
+                mfma(0);
+                read(r, s, t, 2, 0);
+                mfma(1);
+                read(r, s, t, 3, 1);
+                mfma(0);
+            }
             if (t + 1 < taps) read(r1, s1, t + 1, kg, 0);
             mfma(1);
             r = r1;
@@ -1176,7 +1187,7 @@ __global__ __launch_bounds__(512, 1) void halo_conv_kernel(const HaloArgs A) {
         // first barrier)
         float *red = reinterpret_cast<float *>(smem + FILT_BYTES + b * HALO_BYTES);
 #pragma unroll
-        for (int i = 0; i < TM; ++i) {
+        for (int i = 0; i < (KG == 2 ? TM : 0); ++i) {
             wait_lgkm0();
             block_sync<true>();
             if (kg == 1) {
@@ -1195,7 +1206,7 @@ __global__ __launch_bounds__(512, 1) void halo_conv_kernel(const HaloArgs A) {
             }
         }
         wait_lgkm0();
-        block_sync<true>();   // the sums are read before the staging reuses the buffer
+        block_sync<true>();   // the halo (and the sums) are read before the staging reuses the buffer
         if (kg == 1) continue;
 
         // ---- epilogue (group 0): stage 32 rows per wave in this tile's halo
@@ -2007,9 +2018,10 @@ int run_halo(const bf16 *in, int N, int H, int W, const bf16 *filt, const bf16 *
     void *eb = nullptr, *ee = nullptr;
     const bool timed = prof_pair(pk, &eb, &ee);
     if (NO <= 32)
-        hipExtLaunchKernelGGL((halo_conv_kernel<32, 16>), grid, dim3(512), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
+        hipExtLaunchKernelGGL((halo_conv_kernel<32, 16, 2>), grid, dim3(512), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
     else
-        hipExtLaunchKernelGGL((halo_conv_kernel<64, 9>), grid, dim3(512), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
+        hipExtLaunchKernelGGL((halo_conv_kernel<64, 9, 1>), grid, dim3(256), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0,
+                              a);
     const int err = (int)hipGetLastError();
     if (timed) prof_pair_done(pk, eb, ee, err == 0);
     return err;
