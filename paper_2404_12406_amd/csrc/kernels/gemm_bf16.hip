@@ -1020,7 +1020,7 @@ struct HaloArgs {
 
 constexpr int kHaloMaxPx = 320;                     // halo pixels per buffer (40 KB)
 
-template <int NP, int TAPS_MAX, int KG>
+template <int NP, int TAPS_MAX, int KG, bool EXACT = false>
 __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A) {
     constexpr int NW = 4 * KG;                      // waves: KG k-groups of four
     constexpr int FILT_BYTES = TAPS_MAX * NP * 128;
@@ -1085,20 +1085,36 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
             dma16<false>(rf, sF + j * 1024, off);
         }
     }
-    // ---- the halo of tile `tile` into buffer `b`
+    // ---- the halo of tile `tile` into buffer `b`.  Load instruction
+    // j = wave + NW jj carries halo pixels 8 j .. 8 j + 7, the same ones for
+    // every tile: their rows, columns and element offsets within the halo
+    // are worked out once (rows past the halo are sent out of range).
+    constexpr int HJ = (kHaloMaxPx / 8 + NW - 1) / NW;
+    const int ninstr = (HP + 7) / 8;
+    int h_y[HJ], h_x[HJ];
+    uint32_t h_c[HJ];
+#pragma unroll
+    for (int jj = 0; jj < HJ; ++jj) {
+        const int hp = (wave + jj * NW) * 8 + (lane >> 3);
+        const int hy = hp / HWW, hx = hp - hy * HWW;
+        h_y[jj] = hp < HP ? hy : -(1 << 20);
+        h_x[jj] = hx;
+        h_c[jj] = ((uint32_t)hy * (uint32_t)A.W + (uint32_t)hx) * 64u + (uint32_t)chunk_of(hp) * 8u;
+    }
     auto load_halo = [&](int tile, int b) {
         char *dst = smem + FILT_BYTES + b * HALO_BYTES;
         const int img = tile / A.tiles_img, rem = tile - img * A.tiles_img;
         const int ty = rem / A.tiles_w, tx = rem - ty * A.tiles_w;
         const int iy0 = ty * A.TH - A.ph, ix0 = tx * A.TW - A.pw;
-        const int ninstr = (HP + 7) / 8;
-        for (int j = wave; j < ninstr; j += NW) {
-            const int hp = j * 8 + (lane >> 3);
-            const int hy = hp / HWW, hx = hp - hy * HWW;
-            const int iy = iy0 + hy, ix = ix0 + hx;
-            const bool ok = hp < HP && (unsigned)iy < (unsigned)A.H && (unsigned)ix < (unsigned)A.W;
+        const int gbase = ((img * A.H + iy0) * A.W + ix0) * 64;
+#pragma unroll
+        for (int jj = 0; jj < HJ; ++jj) {
+            const int j = wave + jj * NW;
+            if (j >= ninstr) break;
+            const int iy = iy0 + h_y[jj], ix = ix0 + h_x[jj];
+            const bool ok = (unsigned)iy < (unsigned)A.H && (unsigned)ix < (unsigned)A.W;
             // element index below 2^31 (operand_fits), byte offset below kOOB
-            const uint32_t off = ok ? (uint32_t)(((img * A.H + iy) * A.W + ix) * 64 + chunk_of(hp) * 8) * 2u : kOOB;
+            const uint32_t off = ok ? ((uint32_t)gbase + h_c[jj]) * 2u : kOOB;
             dma16<false>(rin, dst + j * 1024, off);
         }
     };
@@ -1117,6 +1133,29 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
     // the output's buffer range, which the hardware drops), so the wait for a
     // halo can leave the previous tile's stores in flight
     constexpr int NPASS = NP / 16;                  // 32 rows x NP/8 pieces over 64 lanes
+    constexpr int SEG = NP / 8;                     // 16-byte pieces of a staged pixel row
+    // the output pixel (row, column within the tile) and element offset of
+    // each of the lane's stores, the same for every tile
+    int e_y[TM][NPASS], e_x[TM][NPASS], e_c[TM][NPASS];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int ps = 0; ps < NPASS; ++ps) {
+            const int lin = ps * 64 + lane;
+            const int rl = lin / SEG, cl = (lin % SEG) * 8;
+            const int p = (TM * wl + i) * 32 + rl;
+            const int oy = p / A.TW, ox = p - oy * A.TW;
+            const bool ok = cl < A.NO && p < npx;
+            e_y[i][ps] = ok ? oy : (1 << 20);
+            e_x[i][ps] = ox;
+            e_c[i][ps] = (oy * A.Q + ox) * A.NO + cl;
+        }
+    int tap_r[TAPS_MAX], tap_s[TAPS_MAX];           // (r, s) of tap t
+#pragma unroll
+    for (int t = 0; t < TAPS_MAX; ++t) {
+        tap_r[t] = t / A.S;
+        tap_s[t] = t - tap_r[t] * A.S;
+    }
     int tile = blockIdx.x;
     if (tile < A.tiles) load_halo(tile, 0);
     for (int it = 0; tile < A.tiles; ++it, tile += gridDim.x) {
@@ -1138,7 +1177,7 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
             for (int j = 0; j < TN; ++j)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-        bf16x8 fa[2][TM], fb[2][TN];
+        bf16x8 fa[3][TM], fb[3][TN];
         // fragments of one slice: the row tiles' halo rows at tap (r, s) and
         // the filter rows of tap t, chunk pair `sub`
         auto read = [&](int r, int s, int t, int sub, int buf) {
@@ -1156,30 +1195,47 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
                 for (int j = 0; j < TN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[buf][j], fa[buf][i], acc[i][j], 0, 0, 0);
         };
-        // group kg takes slices kg and kg + 2 of every tap (one group: all
-        // four); the next slice's fragments are read while a slice's MFMAs run
-        read(0, 0, 0, kg, 0);
-        for (int t = 0, r = 0, s = 0; t < taps; ++t) {
-            int r1 = r, s1 = s + 1;                 // the next tap
-            if (s1 == A.S) {
-                s1 = 0;
-                ++r1;
+        if constexpr (EXACT && KG == 1) {
+            // exactly TAPS_MAX taps: every slice (t, sub) unrolled, fragments
+            // read two slices ahead, slice k in buffer k mod 3
+            constexpr int NSL = 4 * TAPS_MAX;
+            auto rd = [&](int k) {
+                const int t = k >> 2, sub = k & 3;
+                read(tap_r[t], tap_s[t], t, sub, k % 3);
+            };
+            rd(0);
+            rd(1);
+#pragma unroll
+            for (int k = 0; k < NSL; ++k) {
+                if (k + 2 < NSL) rd(k + 2);
+                mfma(k % 3);
             }
-            if constexpr (KG == 2) {
-                read(r, s, t, kg + 2, 1);
-                mfma(0);
-            } else {
-                read(r, s, t, 1, 1);
-                mfma(0);
-                read(r, s, t, 2, 0);
+        } else {
+            // group kg takes slices kg and kg + 2 of every tap (one group: all
+            // four); the next slice's fragments are read while a slice's MFMAs run
+            read(0, 0, 0, kg, 0);
+            for (int t = 0, r = 0, s = 0; t < taps; ++t) {
+                int r1 = r, s1 = s + 1;                 // the next tap
+                if (s1 == A.S) {
+                    s1 = 0;
+                    ++r1;
+                }
+                if constexpr (KG == 2) {
+                    read(r, s, t, kg + 2, 1);
+                    mfma(0);
+                } else {
+                    read(r, s, t, 1, 1);
+                    mfma(0);
+                    read(r, s, t, 2, 0);
+                    mfma(1);
+                    read(r, s, t, 3, 1);
+                    mfma(0);
+                }
+                if (t + 1 < taps) read(r1, s1, t + 1, kg, 0);
                 mfma(1);
-                read(r, s, t, 3, 1);
-                mfma(0);
+                r = r1;
+                s = s1;
             }
-            if (t + 1 < taps) read(r1, s1, t + 1, kg, 0);
-            mfma(1);
-            r = r1;
-            s = s1;
         }
 
         // ---- group 1's sums into group 0's, one row tile at a time, through
@@ -1213,8 +1269,8 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
         // buffer, 16-byte stores
         const int img = tile / A.tiles_img, rem = tile - img * A.tiles_img;
         const int ty0 = (rem / A.tiles_w) * A.TH, tx0 = (rem - (rem / A.tiles_w) * A.tiles_w) * A.TW;
+        const int obase = ((img * A.P + ty0) * A.Q + tx0) * A.NO;
         bf16 *stage = reinterpret_cast<bf16 *>(smem + FILT_BYTES + b * HALO_BYTES) + wl * 32 * EPI_PITCH;
-        constexpr int SEG = NP / 8;                 // 16-byte pieces of a staged pixel row
         typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
@@ -1233,13 +1289,10 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
             for (int ps = 0; ps < NPASS; ++ps) {
                 const int lin = ps * 64 + lane;
                 const int rl = lin / SEG, cl = (lin % SEG) * 8;
-                const int p = (TM * wl + i) * 32 + rl;
-                const int oy = p / A.TW, ox = p - oy * A.TW;
-                const int y = ty0 + oy, x = tx0 + ox;
                 const u32x4 v = *reinterpret_cast<const u32x4 *>(stage + rl * EPI_PITCH + cl);
-                const bool ok = cl < A.NO && p < npx && y < A.P && x < A.Q;
+                const bool ok = ty0 + e_y[i][ps] < A.P && tx0 + e_x[i][ps] < A.Q;
                 // element index below 2^31 (operand_fits on the output)
-                const uint32_t off = ok ? (uint32_t)(((img * A.P + y) * A.Q + x) * A.NO + cl) * 2u : kOOB;
+                const uint32_t off = ok ? (uint32_t)(obase + e_c[i][ps]) * 2u : kOOB;
                 __builtin_amdgcn_raw_buffer_store_b128(v, ro, (int)off, 0, 0);
             }
             wait_lgkm0();
@@ -2019,9 +2072,10 @@ int run_halo(const bf16 *in, int N, int H, int W, const bf16 *filt, const bf16 *
     const bool timed = prof_pair(pk, &eb, &ee);
     if (NO <= 32)
         hipExtLaunchKernelGGL((halo_conv_kernel<32, 16, 2>), grid, dim3(512), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
+    else if (R * S == 9)   // 3 x 3: the unrolled schedule
+        hipExtLaunchKernelGGL((halo_conv_kernel<64, 9, 1, true>), grid, dim3(256), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
     else
-        hipExtLaunchKernelGGL((halo_conv_kernel<64, 9, 1>), grid, dim3(256), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0,
-                              a);
+        hipExtLaunchKernelGGL((halo_conv_kernel<64, 9, 1>), grid, dim3(256), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
     const int err = (int)hipGetLastError();
     if (timed) prof_pair_done(pk, eb, ee, err == 0);
     return err;

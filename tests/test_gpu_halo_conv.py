@@ -26,6 +26,8 @@ CASES = [
     ((1, 64, 56, 56), (64, 64, 3, 3), (1, 1), (1, 1)),     # the ResNet stage-1 tile shape
     ((2, 64, 10, 12), (32, 64, 3, 3), (1, 1), (0, 2)),     # 32 outputs: the 16-tap kernel; asymmetric pad
     ((2, 64, 11, 9), (24, 64, 2, 3), (1, 1), (1, 0)),      # 24 outputs (not a power of two), 2 x 3 taps
+    ((2, 64, 10, 9), (48, 64, 2, 3), (1, 1), (1, 1)),      # 48 outputs, 2 x 3 taps: the generic 64-column loop
+    ((2, 40, 9, 11), (64, 40, 2, 2), (1, 1), (1, 1)),      # input gradient of 40 channels, 2 x 2 taps
     ((1, 16, 12, 14), (64, 16, 4, 4), (1, 1), (0, 3)),     # input gradient only: 16 channels, 4 x 4 taps
     ((2, 3, 37, 41), (64, 3, 7, 7), (2, 2), (3, 3)),       # stem: input gradient through 2 x 2 blocks
 ]
