@@ -306,7 +306,7 @@ struct Cfg {
     static_assert(KG == 1 || (WR * WC) * (WM / 32) * (WN / 32) * 16 * 64 * 4 <= LDS_BYTES, "k-group partials fit LDS");
 };
 
-template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int OCC, bool UNIT, int KG = 1>
+template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int OCC, bool UNIT, int KG = 1, bool TS = false>
 __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args P) {
     using G = Cfg<MODE, BM, BN, WR, WC, STAGES, KG>;
     constexpr int NIA = G::NIA, NIB = G::NIB, TM = G::TM, TN = G::TN, NSUB = G::NSUB;
@@ -444,64 +444,137 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
         }
     }
 
+    // Convolution forward with C a multiple of BK and at most 32 taps (TS,
+    // checked by the host): a BK-deep step is the channels c0 .. c0 + 63 of
+    // one tap t = (r, s), the same for every lane.  Each A load's pixel
+    // offset (with its chunk) and whether its pixel lies inside the image at
+    // tap t (bit t) are worked out once, so a step costs a bit test, an add
+    // and a select per load instead of dividing every lane's k by C and S.
+    constexpr bool TAPSTEP = TS && MODE == kFwd && !UNIT && G::A_KC;
+    constexpr bool tapstep = TAPSTEP;
+    uint32_t a_pixb[TAPSTEP ? NIA : 1], a_tmask[TAPSTEP ? NIA : 1];
+    if constexpr (TAPSTEP) {
+#pragma unroll
+        for (int j = 0; j < NIA; ++j) {
+            const int v = (wave * NIA + j) & 1;
+            // element offset of the pixel at tap (0, 0); negative in the
+            // padding, where no tap that reads it is inside the image
+            a_pixb[j] = (uint32_t)(a_base[j] + (a_y[j] * g.W + a_x[j]) * g.C + (kc0 ^ v) * 8) * 2u;
+            uint32_t m = 0;
+            if (tapstep && a_ok[j]) {
+                for (int t = 0, r = 0, sx = 0; t < g.R * g.S; ++t) {
+                    if ((unsigned)(a_y[j] + r) < (unsigned)g.H && (unsigned)(a_x[j] + sx) < (unsigned)g.W) m |= 1u << t;
+                    if (++sx == g.S) {
+                        sx = 0;
+                        ++r;
+                    }
+                }
+            }
+            a_tmask[j] = m;
+        }
+    }
+    // Tap cursor of the last step issued (uniform).  The steps are issued in
+    // order, each BK past the one before (the prologue's STAGES steps from
+    // k_begin, then one refill per step), so the cursor advances by a
+    // channel block, or to the next tap, without dividing.
+    int ts_k0 = k_begin, ts_t = 0, ts_r = 0, ts_s = 0, ts_c0 = 0;
+    if constexpr (TAPSTEP) {
+        if (tapstep) {
+            ts_t = k_begin / g.C;
+            ts_c0 = k_begin - ts_t * g.C;
+            ts_r = ts_t / g.S;
+            ts_s = ts_t - ts_r * g.S;
+        }
+    }
+    uint32_t ts_off = (uint32_t)((ts_r * g.W + ts_s) * g.C + ts_c0) * 2u;
+
     // ------------------------------------------------ issue the loads of one tile
     // Loads j of A are instructions j, loads j of B are NIA + j; issue_range
     // issues those in [lo, hi).
     auto issue_range = [&](int stage, int k0, int lo, int hi) {
         char *sA = smem + stage * G::STAGE_BYTES;
         char *sB = sA + G::A_BYTES;
-        // ---- A
-        if constexpr (G::A_KC) {
-            // the two chunk variants of this lane: (tap, channel offset) of each
-            int dr[2] = {0, 0}, ds[2] = {0, 0}, off_k[2];
-            bool kin[2];
+        bool a_done = false;
+        if constexpr (TAPSTEP) {
+            if (tapstep) {
+                if (k0 != ts_k0) {   // the next step
+                    ts_k0 = k0;
+                    ts_c0 += BK;
+                    if (ts_c0 == g.C) {
+                        ts_c0 = 0;
+                        ++ts_t;
+                        if (++ts_s == g.S) {
+                            ts_s = 0;
+                            ++ts_r;
+                        }
+                    }
+                    ts_off = (uint32_t)((ts_r * g.W + ts_s) * g.C + ts_c0) * 2u;
+                }
+                // steps past the end of the reduction (refills nobody reads) load zeros
+                const bool live = k0 < k_end;
 #pragma unroll
-            for (int v = 0; v < 2; ++v) {
-                const int kk = k0 + (kc0 ^ v) * 8;
-                kin[v] = kk < k_end;
-                off_k[v] = kk;
-                if constexpr (!UNIT) {
-                    if constexpr (MODE == kFwd) {
-                        const int rs = kk / g.C;
-                        off_k[v] = kk - rs * g.C;
-                        dr[v] = rs / g.S;
-                        ds[v] = rs - dr[v] * g.S;
-                    } else {
-                        const int t = kk / g.K;
-                        off_k[v] = kk - t * g.K;
-                        const int tr = f.Sp > 0 ? t / f.Sp : 0;
-                        dr[v] = -tr;
-                        ds[v] = -(t - tr * f.Sp);
+                for (int j = 0; j < NIA; ++j) {
+                    const bool ok = live && ((a_tmask[j] >> (ts_t & 31)) & 1u);
+                    const uint32_t boff = ok ? a_pixb[j] + ts_off : kOOB;
+                    if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
+                }
+                a_done = true;
+            }
+        }
+        // ---- A
+        if (!a_done) {
+            if constexpr (G::A_KC) {
+                // the two chunk variants of this lane: (tap, channel offset) of each
+                int dr[2] = {0, 0}, ds[2] = {0, 0}, off_k[2];
+                bool kin[2];
+    #pragma unroll
+                for (int v = 0; v < 2; ++v) {
+                    const int kk = k0 + (kc0 ^ v) * 8;
+                    kin[v] = kk < k_end;
+                    off_k[v] = kk;
+                    if constexpr (!UNIT) {
+                        if constexpr (MODE == kFwd) {
+                            const int rs = kk / g.C;
+                            off_k[v] = kk - rs * g.C;
+                            dr[v] = rs / g.S;
+                            ds[v] = rs - dr[v] * g.S;
+                        } else {
+                            const int t = kk / g.K;
+                            off_k[v] = kk - t * g.K;
+                            const int tr = f.Sp > 0 ? t / f.Sp : 0;
+                            dr[v] = -tr;
+                            ds[v] = -(t - tr * f.Sp);
+                        }
                     }
                 }
-            }
-#pragma unroll
-            for (int j = 0; j < NIA; ++j) {
-                const int v = (wave * NIA + j) & 1;
-                bool ok = kin[v] && a_ok[j];
-                int off;
-                if constexpr (UNIT) {
-                    off = a_base[j] + off_k[v];
-                } else if constexpr (MODE == kFwd) {
-                    const int ih = a_y[j] + dr[v], iw = a_x[j] + ds[v];
-                    ok = ok && (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
-                    off = a_base[j] + (ih * g.W + iw) * g.C + off_k[v];
-                } else {
-                    const int p = a_y[j] + dr[v], q = a_x[j] + ds[v];
-                    ok = ok && (unsigned)p < (unsigned)g.P && (unsigned)q < (unsigned)g.Q;
-                    off = a_base[j] + (p * g.Q + q) * g.K + off_k[v];
+    #pragma unroll
+                for (int j = 0; j < NIA; ++j) {
+                    const int v = (wave * NIA + j) & 1;
+                    bool ok = kin[v] && a_ok[j];
+                    int off;
+                    if constexpr (UNIT) {
+                        off = a_base[j] + off_k[v];
+                    } else if constexpr (MODE == kFwd) {
+                        const int ih = a_y[j] + dr[v], iw = a_x[j] + ds[v];
+                        ok = ok && (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
+                        off = a_base[j] + (ih * g.W + iw) * g.C + off_k[v];
+                    } else {
+                        const int p = a_y[j] + dr[v], q = a_x[j] + ds[v];
+                        ok = ok && (unsigned)p < (unsigned)g.P && (unsigned)q < (unsigned)g.Q;
+                        off = a_base[j] + (p * g.Q + q) * g.K + off_k[v];
+                    }
+                    const uint32_t boff = ok ? (uint32_t)off * 2u : kOOB;
+                    if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
                 }
-                const uint32_t boff = ok ? (uint32_t)off * 2u : kOOB;
-                if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
-            }
-        } else {
-            constexpr int SPR = BM / 8, KPI = 64 / SPR;
-#pragma unroll
-            for (int j = 0; j < NIA; ++j) {
-                const int kk = k0 + (wave * NIA + j) * KPI + lane / SPR;
-                const bool ok = a_ok[j] && kk < k_end;
-                const uint32_t boff = ok ? ((uint32_t)kk * (uint32_t)g.K + a_mn_off[j]) * 2u : kOOB;
-                if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
+            } else {
+                constexpr int SPR = BM / 8, KPI = 64 / SPR;
+    #pragma unroll
+                for (int j = 0; j < NIA; ++j) {
+                    const int kk = k0 + (wave * NIA + j) * KPI + lane / SPR;
+                    const bool ok = a_ok[j] && kk < k_end;
+                    const uint32_t boff = ok ? ((uint32_t)kk * (uint32_t)g.K + a_mn_off[j]) * 2u : kOOB;
+                    if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
+                }
             }
         }
         // ---- B
@@ -1758,13 +1831,13 @@ int64_t part_stride(int64_t elems) { return (elems + 3) / 4 * 4; }
 
 // The launch records the profiling events itself when its kind is armed, so
 // a pair spans this kernel's execution alone.
-template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int OCC, bool UNIT, int KG = 1>
+template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int OCC, bool UNIT, int KG = 1, bool TS = false>
 int go(const Args &a, dim3 grid, hipStream_t st) {
     const unsigned pk = MODE == kFwd ? kProfFwd : MODE == kWgrad ? kProfWgrad : kProfDgrad;
     void *eb = nullptr, *ee = nullptr;
     const bool timed = prof_pair(pk, &eb, &ee);
-    hipExtLaunchKernelGGL((gemm_kernel<MODE, BM, BN, WR, WC, STAGES, OCC, UNIT, KG>), grid, dim3(WR * WC * KG * 64), 0,
-                          st, (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
+    hipExtLaunchKernelGGL((gemm_kernel<MODE, BM, BN, WR, WC, STAGES, OCC, UNIT, KG, TS>), grid,
+                          dim3(WR * WC * KG * 64), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
     const int err = (int)hipGetLastError();
     if (timed) prof_pair_done(pk, eb, ee, err == 0);
     return err;
@@ -1775,36 +1848,42 @@ int go(const Args &a, dim3 grid, hipStream_t st) {
 template <int MODE, bool UNIT>
 constexpr bool has_256x256() { return !(MODE == kDgrad && !UNIT); }
 
-template <int MODE, bool UNIT>
+template <int MODE, bool UNIT, bool TS = false>
 int go_tile(const Tile &t, const Args &a, dim3 grid, hipStream_t st) {
     if (t.bm == 256 && t.bn == 256) {
-        if constexpr (has_256x256<MODE, UNIT>()) return go<MODE, 256, 256, 2, 4, 2, 1, UNIT>(a, grid, st);
+        if constexpr (has_256x256<MODE, UNIT>()) return go<MODE, 256, 256, 2, 4, 2, 1, UNIT, 1, TS>(a, grid, st);
         else return (int)hipErrorInvalidValue;
     }
-    if (t.bm == 256 && t.bn == 128) return go<MODE, 256, 128, 2, 4, 3, 1, UNIT>(a, grid, st);
+    if (t.bm == 256 && t.bn == 128) return go<MODE, 256, 128, 2, 4, 3, 1, UNIT, 1, TS>(a, grid, st);
     if (t.kg == 2) {
         if constexpr (MODE != kWgrad) {
-            if (t.bm == 128 && t.bn == 128) return go<MODE, 128, 128, 2, 2, 4, 1, UNIT, 2>(a, grid, st);
+            if (t.bm == 128 && t.bn == 128) return go<MODE, 128, 128, 2, 2, 4, 1, UNIT, 2, TS>(a, grid, st);
         }
         if constexpr (MODE == kFwd || MODE == kDgrad) {
-            if (t.bm == 128 && t.bn == 192) return go<MODE, 128, 192, 2, 2, 3, 1, UNIT, 2>(a, grid, st);
+            if (t.bm == 128 && t.bn == 192) return go<MODE, 128, 192, 2, 2, 3, 1, UNIT, 2, TS>(a, grid, st);
         }
         return (int)hipErrorInvalidValue;
     }
     if (t.bn == 32) {
-        if constexpr (MODE == kFwd || MODE == kDgrad) return go<MODE, 256, 32, 4, 1, 2, 2, UNIT>(a, grid, st);
+        if constexpr (MODE == kFwd || MODE == kDgrad) return go<MODE, 256, 32, 4, 1, 2, 2, UNIT, 1, TS>(a, grid, st);
         return (int)hipErrorInvalidValue;
     }
-    if (t.bm == 128 && t.bn == 128 && t.wc == 4 && t.stages == 4) return go<MODE, 128, 128, 2, 4, 4, 1, UNIT>(a, grid, st);
-    if (t.bm == 128 && t.bn == 128 && t.wc == 4) return go<MODE, 128, 128, 2, 4, 2, 2, UNIT>(a, grid, st);
-    if (t.bm == 128 && t.bn == 128 && t.stages == 4) return go<MODE, 128, 128, 2, 2, 4, 1, UNIT>(a, grid, st);
-    if (t.bm == 128 && t.bn == 128) return go<MODE, 128, 128, 2, 2, 2, 2, UNIT>(a, grid, st);
-    return go<MODE, 128, 64, 2, 2, 2, 3, UNIT>(a, grid, st);
+    if (t.bm == 128 && t.bn == 128 && t.wc == 4 && t.stages == 4) return go<MODE, 128, 128, 2, 4, 4, 1, UNIT, 1, TS>(a, grid, st);
+    if (t.bm == 128 && t.bn == 128 && t.wc == 4) return go<MODE, 128, 128, 2, 4, 2, 2, UNIT, 1, TS>(a, grid, st);
+    if (t.bm == 128 && t.bn == 128 && t.stages == 4) return go<MODE, 128, 128, 2, 2, 4, 1, UNIT, 1, TS>(a, grid, st);
+    if (t.bm == 128 && t.bn == 128) return go<MODE, 128, 128, 2, 2, 2, 2, UNIT, 1, TS>(a, grid, st);
+    return go<MODE, 128, 64, 2, 2, 2, 3, UNIT, 1, TS>(a, grid, st);
 }
 
+// ts: a convolution forward whose steps each lie in one tap (C a multiple
+// of BK, at most 32 taps), built with the tap-cursor operand loads
 template <int MODE>
-int go_mode(const Tile &t, const Args &a, dim3 grid, bool unit, hipStream_t st) {
-    return unit ? go_tile<MODE, true>(t, a, grid, st) : go_tile<MODE, false>(t, a, grid, st);
+int go_mode(const Tile &t, const Args &a, dim3 grid, bool unit, hipStream_t st, bool ts = false) {
+    if (unit) return go_tile<MODE, true>(t, a, grid, st);
+    if constexpr (MODE == kFwd) {
+        if (ts) return go_tile<MODE, false, true>(t, a, grid, st);
+    }
+    return go_tile<MODE, false>(t, a, grid, st);
 }
 
 bool al16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -2182,7 +2261,8 @@ int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, 
         a2.k_split = cs.p2.k_split;
         return go_mode<kFwd>(cs.p2.t, a2, dim3(a2.ntm * a2.ntn), true, st);
     }
-    int err = go_mode<kFwd>(p.t, a, dim3(a.ntm * a.ntn, 1, p.splits), unit_geom(g), st);
+    const bool ts = g.C % BK == 0 && g.R * g.S <= 32;
+    int err = go_mode<kFwd>(p.t, a, dim3(a.ntm * a.ntn, 1, p.splits), unit_geom(g), st, ts);
     if (err || p.splits <= 1) return err;
     return reduce_partials(a.part, p.splits, n, a.part_stride, (bf16 *)y, (const bf16 *)bias, a.N, st);
 }
