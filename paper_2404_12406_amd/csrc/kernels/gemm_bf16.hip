@@ -444,33 +444,50 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
         }
     }
 
-    // Convolution forward with C a multiple of BK and at most 32 taps (TS,
-    // checked by the host): a BK-deep step is the channels c0 .. c0 + 63 of
-    // one tap t = (r, s), the same for every lane.  Each A load's pixel
-    // offset (with its chunk) and whether its pixel lies inside the image at
-    // tap t (bit t) are worked out once, so a step costs a bit test, an add
-    // and a select per load instead of dividing every lane's k by C and S.
-    constexpr bool TAPSTEP = TS && MODE == kFwd && !UNIT && G::A_KC;
-    constexpr bool tapstep = TAPSTEP;
-    uint32_t a_pixb[TAPSTEP ? NIA : 1], a_tmask[TAPSTEP ? NIA : 1];
+    // Tap steps (TS, checked by the host): the convolution forward with C a
+    // multiple of BK, or the input gradient through the transposed filter
+    // with K a multiple of BK, with at most 32 taps (of the stride phase).
+    // A BK-deep step is then the channels c0 .. c0 + 63 of one tap t = (r, s),
+    // the same for every lane.  Each A load's pixel offset (with its chunk)
+    // and whether its pixel lies inside the image at tap t (bit t) are worked
+    // out once, as is each B load's row offset, so a step costs a bit test,
+    // an add and a select per load instead of dividing every lane's k.  The
+    // forward's pixel at tap (r, s) is (y + r, x + s) in the H x W input;
+    // the input gradient's is (y - r, x - s) in the P x Q output gradient.
+    constexpr bool TAPSTEP = TS && !UNIT && G::A_KC && G::B_KC && (MODE == kFwd || MODE == kDgrad);
+    constexpr int TSIGN = MODE == kFwd ? 1 : -1;
+    int ts_ch = 1, ts_gh = 1, ts_gw = 1, ts_nr = 1, ts_ns = 1;   // channels, pixel grid, taps
+    uint32_t a_pixb[TAPSTEP ? NIA : 1], a_tmask[TAPSTEP ? NIA : 1], b_rowb[TAPSTEP ? NIB : 1];
     if constexpr (TAPSTEP) {
+        if constexpr (MODE == kFwd) {
+            ts_ch = g.C; ts_gh = g.H; ts_gw = g.W; ts_nr = g.R; ts_ns = g.S;
+        } else {
+            // (an empty phase, Sp = 0, has no steps: its cursor is never read)
+            ts_ch = g.K; ts_gh = g.P; ts_gw = g.Q; ts_nr = f.Rp; ts_ns = f.Sp > 0 ? f.Sp : 1;
+        }
 #pragma unroll
         for (int j = 0; j < NIA; ++j) {
             const int v = (wave * NIA + j) & 1;
-            // element offset of the pixel at tap (0, 0); negative in the
-            // padding, where no tap that reads it is inside the image
-            a_pixb[j] = (uint32_t)(a_base[j] + (a_y[j] * g.W + a_x[j]) * g.C + (kc0 ^ v) * 8) * 2u;
+            // element offset of the pixel at tap (0, 0), which may lie in the
+            // padding, where only taps inside the image read from it
+            a_pixb[j] = (uint32_t)(a_base[j] + (a_y[j] * ts_gw + a_x[j]) * ts_ch + (kc0 ^ v) * 8) * 2u;
             uint32_t m = 0;
-            if (tapstep && a_ok[j]) {
-                for (int t = 0, r = 0, sx = 0; t < g.R * g.S; ++t) {
-                    if ((unsigned)(a_y[j] + r) < (unsigned)g.H && (unsigned)(a_x[j] + sx) < (unsigned)g.W) m |= 1u << t;
-                    if (++sx == g.S) {
+            if (a_ok[j]) {
+                for (int t = 0, r = 0, sx = 0; t < ts_nr * ts_ns; ++t) {
+                    if ((unsigned)(a_y[j] + TSIGN * r) < (unsigned)ts_gh && (unsigned)(a_x[j] + TSIGN * sx) < (unsigned)ts_gw)
+                        m |= 1u << t;
+                    if (++sx == ts_ns) {
                         sx = 0;
                         ++r;
                     }
                 }
             }
             a_tmask[j] = m;
+        }
+#pragma unroll
+        for (int j = 0; j < NIB; ++j) {
+            const int v = (wave * NIB + j) & 1;
+            b_rowb[j] = (uint32_t)(b_base[j] + (kc0 ^ v) * 8) * 2u;
         }
     }
     // Tap cursor of the last step issued (uniform).  The steps are issued in
@@ -479,14 +496,20 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
     // channel block, or to the next tap, without dividing.
     int ts_k0 = k_begin, ts_t = 0, ts_r = 0, ts_s = 0, ts_c0 = 0;
     if constexpr (TAPSTEP) {
-        if (tapstep) {
-            ts_t = k_begin / g.C;
-            ts_c0 = k_begin - ts_t * g.C;
-            ts_r = ts_t / g.S;
-            ts_s = ts_t - ts_r * g.S;
-        }
+        ts_t = k_begin / ts_ch;
+        ts_c0 = k_begin - ts_t * ts_ch;
+        ts_r = ts_t / ts_ns;
+        ts_s = ts_t - ts_r * ts_ns;
     }
-    uint32_t ts_off = (uint32_t)((ts_r * g.W + ts_s) * g.C + ts_c0) * 2u;
+    // byte offsets of the cursor's step: into A (relative to the pixel at
+    // tap (0, 0)) and into B's rows
+    uint32_t ts_aoff = 0, ts_boff = 0;
+    auto ts_offsets = [&]() {
+        ts_aoff = (uint32_t)(TSIGN * (ts_r * ts_gw + ts_s) * ts_ch + ts_c0) * 2u;
+        if constexpr (MODE == kFwd) ts_boff = (uint32_t)((ts_r * g.S + ts_s) * g.C + ts_c0) * 2u;
+        else ts_boff = (uint32_t)(((f.fh + ts_r * g.sh) * g.S + f.fw + ts_s * g.sw) * g.K + ts_c0) * 2u;
+    };
+    if constexpr (TAPSTEP) ts_offsets();
 
     // ------------------------------------------------ issue the loads of one tile
     // Loads j of A are instructions j, loads j of B are NIA + j; issue_range
@@ -494,87 +517,88 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
     auto issue_range = [&](int stage, int k0, int lo, int hi) {
         char *sA = smem + stage * G::STAGE_BYTES;
         char *sB = sA + G::A_BYTES;
-        bool a_done = false;
         if constexpr (TAPSTEP) {
-            if (tapstep) {
-                if (k0 != ts_k0) {   // the next step
-                    ts_k0 = k0;
-                    ts_c0 += BK;
-                    if (ts_c0 == g.C) {
-                        ts_c0 = 0;
-                        ++ts_t;
-                        if (++ts_s == g.S) {
-                            ts_s = 0;
-                            ++ts_r;
-                        }
+            if (k0 != ts_k0) {   // the next step
+                ts_k0 = k0;
+                ts_c0 += BK;
+                if (ts_c0 == ts_ch) {
+                    ts_c0 = 0;
+                    ++ts_t;
+                    if (++ts_s == ts_ns) {
+                        ts_s = 0;
+                        ++ts_r;
                     }
-                    ts_off = (uint32_t)((ts_r * g.W + ts_s) * g.C + ts_c0) * 2u;
                 }
-                // steps past the end of the reduction (refills nobody reads) load zeros
-                const bool live = k0 < k_end;
-#pragma unroll
-                for (int j = 0; j < NIA; ++j) {
-                    const bool ok = live && ((a_tmask[j] >> (ts_t & 31)) & 1u);
-                    const uint32_t boff = ok ? a_pixb[j] + ts_off : kOOB;
-                    if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
-                }
-                a_done = true;
+                ts_offsets();
             }
+            // steps past the end of the reduction (refills nobody reads) load zeros
+            const bool live = k0 < k_end;
+#pragma unroll
+            for (int j = 0; j < NIA; ++j) {
+                const bool ok = live && ((a_tmask[j] >> (ts_t & 31)) & 1u);
+                const uint32_t boff = ok ? a_pixb[j] + ts_aoff : kOOB;
+                if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
+            }
+#pragma unroll
+            for (int j = 0; j < NIB; ++j) {
+                const bool ok = live && b_ok[j];
+                const uint32_t boff = ok ? b_rowb[j] + ts_boff : kOOB;
+                if (NIA + j >= lo && NIA + j < hi) dma16<ASM_DMA>(rb, sB + (wave * NIB + j) * 1024, boff);
+            }
+            return;
         }
         // ---- A
-        if (!a_done) {
-            if constexpr (G::A_KC) {
-                // the two chunk variants of this lane: (tap, channel offset) of each
-                int dr[2] = {0, 0}, ds[2] = {0, 0}, off_k[2];
-                bool kin[2];
-    #pragma unroll
-                for (int v = 0; v < 2; ++v) {
-                    const int kk = k0 + (kc0 ^ v) * 8;
-                    kin[v] = kk < k_end;
-                    off_k[v] = kk;
-                    if constexpr (!UNIT) {
-                        if constexpr (MODE == kFwd) {
-                            const int rs = kk / g.C;
-                            off_k[v] = kk - rs * g.C;
-                            dr[v] = rs / g.S;
-                            ds[v] = rs - dr[v] * g.S;
-                        } else {
-                            const int t = kk / g.K;
-                            off_k[v] = kk - t * g.K;
-                            const int tr = f.Sp > 0 ? t / f.Sp : 0;
-                            dr[v] = -tr;
-                            ds[v] = -(t - tr * f.Sp);
-                        }
-                    }
-                }
-    #pragma unroll
-                for (int j = 0; j < NIA; ++j) {
-                    const int v = (wave * NIA + j) & 1;
-                    bool ok = kin[v] && a_ok[j];
-                    int off;
-                    if constexpr (UNIT) {
-                        off = a_base[j] + off_k[v];
-                    } else if constexpr (MODE == kFwd) {
-                        const int ih = a_y[j] + dr[v], iw = a_x[j] + ds[v];
-                        ok = ok && (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
-                        off = a_base[j] + (ih * g.W + iw) * g.C + off_k[v];
+        if constexpr (G::A_KC) {
+            // the two chunk variants of this lane: (tap, channel offset) of each
+            int dr[2] = {0, 0}, ds[2] = {0, 0}, off_k[2];
+            bool kin[2];
+#pragma unroll
+            for (int v = 0; v < 2; ++v) {
+                const int kk = k0 + (kc0 ^ v) * 8;
+                kin[v] = kk < k_end;
+                off_k[v] = kk;
+                if constexpr (!UNIT) {
+                    if constexpr (MODE == kFwd) {
+                        const int rs = kk / g.C;
+                        off_k[v] = kk - rs * g.C;
+                        dr[v] = rs / g.S;
+                        ds[v] = rs - dr[v] * g.S;
                     } else {
-                        const int p = a_y[j] + dr[v], q = a_x[j] + ds[v];
-                        ok = ok && (unsigned)p < (unsigned)g.P && (unsigned)q < (unsigned)g.Q;
-                        off = a_base[j] + (p * g.Q + q) * g.K + off_k[v];
+                        const int t = kk / g.K;
+                        off_k[v] = kk - t * g.K;
+                        const int tr = f.Sp > 0 ? t / f.Sp : 0;
+                        dr[v] = -tr;
+                        ds[v] = -(t - tr * f.Sp);
                     }
-                    const uint32_t boff = ok ? (uint32_t)off * 2u : kOOB;
-                    if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
                 }
-            } else {
-                constexpr int SPR = BM / 8, KPI = 64 / SPR;
-    #pragma unroll
-                for (int j = 0; j < NIA; ++j) {
-                    const int kk = k0 + (wave * NIA + j) * KPI + lane / SPR;
-                    const bool ok = a_ok[j] && kk < k_end;
-                    const uint32_t boff = ok ? ((uint32_t)kk * (uint32_t)g.K + a_mn_off[j]) * 2u : kOOB;
-                    if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
+            }
+#pragma unroll
+            for (int j = 0; j < NIA; ++j) {
+                const int v = (wave * NIA + j) & 1;
+                bool ok = kin[v] && a_ok[j];
+                int off;
+                if constexpr (UNIT) {
+                    off = a_base[j] + off_k[v];
+                } else if constexpr (MODE == kFwd) {
+                    const int ih = a_y[j] + dr[v], iw = a_x[j] + ds[v];
+                    ok = ok && (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
+                    off = a_base[j] + (ih * g.W + iw) * g.C + off_k[v];
+                } else {
+                    const int p = a_y[j] + dr[v], q = a_x[j] + ds[v];
+                    ok = ok && (unsigned)p < (unsigned)g.P && (unsigned)q < (unsigned)g.Q;
+                    off = a_base[j] + (p * g.Q + q) * g.K + off_k[v];
                 }
+                const uint32_t boff = ok ? (uint32_t)off * 2u : kOOB;
+                if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
+            }
+        } else {
+            constexpr int SPR = BM / 8, KPI = 64 / SPR;
+#pragma unroll
+            for (int j = 0; j < NIA; ++j) {
+                const int kk = k0 + (wave * NIA + j) * KPI + lane / SPR;
+                const bool ok = a_ok[j] && kk < k_end;
+                const uint32_t boff = ok ? ((uint32_t)kk * (uint32_t)g.K + a_mn_off[j]) * 2u : kOOB;
+                if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
             }
         }
         // ---- B
@@ -1875,12 +1899,14 @@ int go_tile(const Tile &t, const Args &a, dim3 grid, hipStream_t st) {
     return go<MODE, 128, 64, 2, 2, 2, 3, UNIT, 1, TS>(a, grid, st);
 }
 
-// ts: a convolution forward whose steps each lie in one tap (C a multiple
-// of BK, at most 32 taps), built with the tap-cursor operand loads
+// ts: a convolution forward, or input gradient through the transposed
+// filter, whose steps each lie in one tap (channels of the reduction a
+// multiple of BK, at most 32 taps per stride phase): the tap-cursor operand
+// loads
 template <int MODE>
 int go_mode(const Tile &t, const Args &a, dim3 grid, bool unit, hipStream_t st, bool ts = false) {
     if (unit) return go_tile<MODE, true>(t, a, grid, st);
-    if constexpr (MODE == kFwd) {
+    if constexpr (MODE == kFwd || MODE == kDgrad) {
         if (ts) return go_tile<MODE, false, true>(t, a, grid, st);
     }
     return go_tile<MODE, false>(t, a, grid, st);
@@ -2468,7 +2494,9 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bia
                       : go_mode<kDgrad>(tsp.p2.t, a2, dim3(a2.ntm * a2.ntn), true, st);
     }
     const dim3 grid(a.ntm * a.ntn, 1, g.sh * g.sw * p.splits);
-    int err = direct ? go_mode<kDgradN>(p.t, a, grid, unit_geom(g), st) : go_mode<kDgrad>(p.t, a, grid, unit_geom(g), st);
+    const bool ts = g.K % BK == 0 && ((g.R + g.sh - 1) / g.sh) * ((g.S + g.sw - 1) / g.sw) <= 32;
+    int err = direct ? go_mode<kDgradN>(p.t, a, grid, unit_geom(g), st)
+                     : go_mode<kDgrad>(p.t, a, grid, unit_geom(g), st, ts);
     if (err) return err;
     if (cs) {
         err = launch_colsum_finalize(kBF16, a.cspart, (int)colsum_rows(g, p.t), g.K, db, st);
