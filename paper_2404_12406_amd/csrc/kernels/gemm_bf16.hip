@@ -511,6 +511,67 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
     };
     if constexpr (TAPSTEP) ts_offsets();
 
+    // Weight gradient by pixel steps (TS, checked by the host): a BK-deep
+    // step is 64 consecutive output pixels, and each lane's k-rows (the same
+    // offsets within every step) move by the same 64 pixels = (dn, dp, dq) in
+    // (image, row, column) from step to step, with at most one carry from q
+    // into p and from p into n.  Each B load keeps its pixel's input row and
+    // column at tap (0, 0) and its element offset, advanced without dividing;
+    // A's rows (dy^T, k-rows = pixels) move by 64 K-element rows.
+    constexpr bool WSTEP = TS && !UNIT && MODE == kWgrad;
+    int w_ih0[WSTEP ? NIB : 1], w_iw0[WSTEP ? NIB : 1], w_pix[WSTEP ? NIB : 1], w_tap[WSTEP ? NIB : 1];
+    int w_krb[WSTEP ? NIB : 1], w_kra[WSTEP ? NIA : 1];
+    uint32_t w_arow[WSTEP ? NIA : 1];
+    int w_k0 = k_begin;
+    if constexpr (WSTEP) {
+        constexpr int SPRA = BM / 8, KPIA = 64 / SPRA, SPRB = BN / 8, KPIB = 64 / SPRB;
+#pragma unroll
+        for (int j = 0; j < NIA; ++j) {
+            w_kra[j] = (wave * NIA + j) * KPIA + lane / SPRA;
+            w_arow[j] = ((uint32_t)w_kra[j] * (uint32_t)g.K + a_mn_off[j]) * 2u;
+        }
+        const int PQ = g.P * g.Q;
+#pragma unroll
+        for (int j = 0; j < NIB; ++j) {
+            w_krb[j] = (wave * NIB + j) * KPIB + lane / SPRB;
+            const int kk = k_begin + w_krb[j];
+            const int n = kk / PQ, pq = kk - n * PQ;
+            const int p = pq / g.Q, q = pq - p * g.Q;
+            w_ih0[j] = p * g.sh - g.ph;
+            w_iw0[j] = q * g.sw - g.pw;
+            w_pix[j] = ((n * g.H + w_ih0[j]) * g.W + w_iw0[j]) * g.C;
+            w_tap[j] = (b_r[j] * g.W + b_s[j]) * g.C + (int)b_mn_off[j];
+        }
+    }
+    // 64 pixels = (dn, dp, dq), and the element offsets of each move (uniform)
+    int w_dq = 0, w_dp = 0, w_dn = 0;
+    if constexpr (WSTEP) {
+        const int PQ = g.P * g.Q, rem = BK % PQ;
+        w_dn = BK / PQ;
+        w_dp = rem / g.Q;
+        w_dq = rem - w_dp * g.Q;
+    }
+    auto w_advance = [&]() {
+        const int qend = g.Q * g.sw - g.pw, pend = g.P * g.sh - g.ph;
+#pragma unroll
+        for (int j = 0; j < NIB; ++j) {
+            int iw = w_iw0[j] + w_dq * g.sw, ih = w_ih0[j] + w_dp * g.sh, pix = w_pix[j];
+            pix += (w_dq * g.sw + w_dp * g.sh * g.W) * g.C;
+            if (iw >= qend) {   // carry into the row
+                iw -= g.Q * g.sw;
+                ih += g.sh;
+                pix += (g.sh * g.W - g.Q * g.sw) * g.C;
+            }
+            if (ih >= pend) {   // carry into the image
+                ih -= g.P * g.sh;
+                pix += (g.H - g.P * g.sh) * g.W * g.C;
+            }
+            w_iw0[j] = iw;
+            w_ih0[j] = ih;
+            w_pix[j] = pix + w_dn * g.H * g.W * g.C;
+        }
+    };
+
     // ------------------------------------------------ issue the loads of one tile
     // Loads j of A are instructions j, loads j of B are NIA + j; issue_range
     // issues those in [lo, hi).
@@ -543,6 +604,28 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
             for (int j = 0; j < NIB; ++j) {
                 const bool ok = live && b_ok[j];
                 const uint32_t boff = ok ? b_rowb[j] + ts_boff : kOOB;
+                if (NIA + j >= lo && NIA + j < hi) dma16<ASM_DMA>(rb, sB + (wave * NIB + j) * 1024, boff);
+            }
+            return;
+        }
+        if constexpr (WSTEP) {
+            if (k0 != w_k0) {   // the next step
+                w_k0 = k0;
+                w_advance();
+            }
+            const int left = k_end - k0;   // k-rows of this step inside the reduction
+            const uint32_t sa = (uint32_t)k0 * (uint32_t)g.K * 2u;
+#pragma unroll
+            for (int j = 0; j < NIA; ++j) {
+                const bool ok = a_ok[j] && w_kra[j] < left;
+                const uint32_t boff = ok ? w_arow[j] + sa : kOOB;
+                if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
+            }
+#pragma unroll
+            for (int j = 0; j < NIB; ++j) {
+                const bool ok = b_ok[j] && w_krb[j] < left && (unsigned)(w_ih0[j] + b_r[j]) < (unsigned)g.H &&
+                                (unsigned)(w_iw0[j] + b_s[j]) < (unsigned)g.W;
+                const uint32_t boff = ok ? (uint32_t)(w_pix[j] + w_tap[j]) * 2u : kOOB;
                 if (NIA + j >= lo && NIA + j < hi) dma16<ASM_DMA>(rb, sB + (wave * NIB + j) * 1024, boff);
             }
             return;
@@ -1906,7 +1989,7 @@ int go_tile(const Tile &t, const Args &a, dim3 grid, hipStream_t st) {
 template <int MODE>
 int go_mode(const Tile &t, const Args &a, dim3 grid, bool unit, hipStream_t st, bool ts = false) {
     if (unit) return go_tile<MODE, true>(t, a, grid, st);
-    if constexpr (MODE == kFwd || MODE == kDgrad) {
+    if constexpr (MODE == kFwd || MODE == kDgrad || MODE == kWgrad) {
         if (ts) return go_tile<MODE, false, true>(t, a, grid, st);
     }
     return go_tile<MODE, false>(t, a, grid, st);
@@ -2572,7 +2655,7 @@ int conv_wgrad(const ConvGeom &g, const void *dy, const void *x, void *dw, void 
     a.dbpart = db ? wsf + used : nullptr;
     a.a_bytes = bytes_of((long)g.N * g.P * g.Q * g.K);
     a.b_bytes = bytes_of((long)g.N * g.H * g.W * g.C);
-    int err = go_mode<kWgrad>(p.t, a, dim3(a.ntm * a.ntn, 1, p.splits), unit_geom(g), st);
+    int err = go_mode<kWgrad>(p.t, a, dim3(a.ntm * a.ntn, 1, p.splits), unit_geom(g), st, true);
     if (err) return err;
     if (p.splits > 1 || db) {
         const int64_t n = p.splits > 1 ? (int64_t)a.M * a.N : 0;
