@@ -520,21 +520,19 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
     // A's rows (dy^T, k-rows = pixels) move by 64 K-element rows.
     constexpr bool WSTEP = TS && !UNIT && MODE == kWgrad;
     int w_ih0[WSTEP ? NIB : 1], w_iw0[WSTEP ? NIB : 1], w_pix[WSTEP ? NIB : 1], w_tap[WSTEP ? NIB : 1];
-    int w_krb[WSTEP ? NIB : 1], w_kra[WSTEP ? NIA : 1];
     uint32_t w_arow[WSTEP ? NIA : 1];
     int w_k0 = k_begin;
+    // k-row of load j within a step (recomputed where needed: registers are short)
+    constexpr int W_SPRA = BM / 8, W_KPIA = 64 / W_SPRA, W_SPRB = BN / 8, W_KPIB = 64 / W_SPRB;
+    auto w_kra = [&](int j) { return (wave * NIA + j) * W_KPIA + lane / W_SPRA; };
+    auto w_krb = [&](int j) { return (wave * NIB + j) * W_KPIB + lane / W_SPRB; };
     if constexpr (WSTEP) {
-        constexpr int SPRA = BM / 8, KPIA = 64 / SPRA, SPRB = BN / 8, KPIB = 64 / SPRB;
 #pragma unroll
-        for (int j = 0; j < NIA; ++j) {
-            w_kra[j] = (wave * NIA + j) * KPIA + lane / SPRA;
-            w_arow[j] = ((uint32_t)w_kra[j] * (uint32_t)g.K + a_mn_off[j]) * 2u;
-        }
+        for (int j = 0; j < NIA; ++j) w_arow[j] = ((uint32_t)w_kra(j) * (uint32_t)g.K + a_mn_off[j]) * 2u;
         const int PQ = g.P * g.Q;
 #pragma unroll
         for (int j = 0; j < NIB; ++j) {
-            w_krb[j] = (wave * NIB + j) * KPIB + lane / SPRB;
-            const int kk = k_begin + w_krb[j];
+            const int kk = k_begin + w_krb(j);
             const int n = kk / PQ, pq = kk - n * PQ;
             const int p = pq / g.Q, q = pq - p * g.Q;
             w_ih0[j] = p * g.sh - g.ph;
@@ -617,13 +615,13 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
             const uint32_t sa = (uint32_t)k0 * (uint32_t)g.K * 2u;
 #pragma unroll
             for (int j = 0; j < NIA; ++j) {
-                const bool ok = a_ok[j] && w_kra[j] < left;
+                const bool ok = a_ok[j] && w_kra(j) < left;
                 const uint32_t boff = ok ? w_arow[j] + sa : kOOB;
                 if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
             }
 #pragma unroll
             for (int j = 0; j < NIB; ++j) {
-                const bool ok = b_ok[j] && w_krb[j] < left && (unsigned)(w_ih0[j] + b_r[j]) < (unsigned)g.H &&
+                const bool ok = b_ok[j] && w_krb(j) < left && (unsigned)(w_ih0[j] + b_r[j]) < (unsigned)g.H &&
                                 (unsigned)(w_iw0[j] + b_s[j]) < (unsigned)g.W;
                 const uint32_t boff = ok ? (uint32_t)(w_pix[j] + w_tap[j]) * 2u : kOOB;
                 if (NIA + j >= lo && NIA + j < hi) dma16<ASM_DMA>(rb, sB + (wave * NIB + j) * 1024, boff);
@@ -1958,7 +1956,10 @@ constexpr bool has_256x256() { return !(MODE == kDgrad && !UNIT); }
 template <int MODE, bool UNIT, bool TS = false>
 int go_tile(const Tile &t, const Args &a, dim3 grid, hipStream_t st) {
     if (t.bm == 256 && t.bn == 256) {
-        if constexpr (has_256x256<MODE, UNIT>()) return go<MODE, 256, 256, 2, 4, 2, 1, UNIT, 1, TS>(a, grid, st);
+        // the weight gradient's 256 x 256 tile has no registers left for the
+        // pixel cursor (it spilled): the generic loads
+        constexpr bool TS2 = TS && MODE != kWgrad;
+        if constexpr (has_256x256<MODE, UNIT>()) return go<MODE, 256, 256, 2, 4, 2, 1, UNIT, 1, TS2>(a, grid, st);
         else return (int)hipErrorInvalidValue;
     }
     if (t.bm == 256 && t.bn == 128) return go<MODE, 256, 128, 2, 4, 3, 1, UNIT, 1, TS>(a, grid, st);
