@@ -1373,12 +1373,14 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
                 for (int j = 0; j < TN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[buf][j], fa[buf][i], acc[i][j], 0, 0, 0);
         };
-        if constexpr (EXACT && KG == 1) {
-            // exactly TAPS_MAX taps: every slice (t, sub) unrolled, fragments
-            // read two slices ahead, slice k in buffer k mod 3
-            constexpr int NSL = 4 * TAPS_MAX;
+        if constexpr (EXACT) {
+            // exactly TAPS_MAX taps: every slice of the group (all four of
+            // each tap, or slices kg and kg + 2 with two k-groups) unrolled,
+            // fragments read two slices ahead, slice k in buffer k mod 3
+            constexpr int SPT = 4 / KG;             // slices per tap and group
+            constexpr int NSL = SPT * TAPS_MAX;
             auto rd = [&](int k) {
-                const int t = k >> 2, sub = k & 3;
+                const int t = k / SPT, sub = KG == 1 ? k % SPT : kg + 2 * (k % SPT);
                 read(tap_r[t], tap_s[t], t, sub, k % 3);
             };
             rd(0);
@@ -2259,7 +2261,9 @@ int run_halo(const bf16 *in, int N, int H, int W, const bf16 *filt, const bf16 *
     const unsigned pk = flip ? kProfDgrad : kProfFwd;
     void *eb = nullptr, *ee = nullptr;
     const bool timed = prof_pair(pk, &eb, &ee);
-    if (NO <= 32)
+    if (NO <= 32 && R * S == 16)   // 4 x 4: the unrolled schedule
+        hipExtLaunchKernelGGL((halo_conv_kernel<32, 16, 2, true>), grid, dim3(512), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
+    else if (NO <= 32)
         hipExtLaunchKernelGGL((halo_conv_kernel<32, 16, 2>), grid, dim3(512), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
     else if (R * S == 9)   // 3 x 3: the unrolled schedule
         hipExtLaunchKernelGGL((halo_conv_kernel<64, 9, 1, true>), grid, dim3(256), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
