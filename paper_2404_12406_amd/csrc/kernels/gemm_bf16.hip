@@ -1783,6 +1783,14 @@ constexpr bool kAutoKc[kNumTiles] = {true, true, true, true, false, true, true, 
 // way it took split reductions whose extra pass made the frozen stack 6%
 // slower.
 constexpr bool kAutoConv[kNumTiles] = {true, false, true, false, false, false, false, true, true, false};
+// tiles for convolutions on the tap-step operand loads (the forward with C,
+// or the input gradient with K, a multiple of BK): without the per-lane
+// divisions the 8-wave 4-stage 128 x 128 tile is the fastest or near it on
+// the ResNet-18-shaped layers and the conv sweep (stage-3 input gradient 36.4
+// -> 25.5 us against the 4-wave tile, stride-2 stage-4 31.2 -> 22.2 us,
+// stage-3 forward 23.9 -> 20.9 us against the k-group tile), and the k-group
+// tiles lose to it
+constexpr bool kAutoTs[kNumTiles] = {true, true, true, true, false, true, false, true, true, false};
 
 // MEMSAVE_GEMM_TILE=<name> forces one tile shape (a debugging and testing
 // knob); returns its index or -1.
@@ -2290,8 +2298,16 @@ bool halo_dgrad_applies(const ConvGeom &g) {
            [&] { int th, tw; return halo_tile(g.W, g.R, g.S, &th, &tw); }();
 }
 
+// The convolution forward and input gradient run on the tap-step operand
+// loads when each BK-deep step lies in one tap.
+bool ts_fwd(const ConvGeom &g) { return !unit_geom(g) && g.C % BK == 0 && g.R * g.S <= 32; }
+bool ts_dgrad(const ConvGeom &g) {
+    return !unit_geom(g) && g.K % BK == 0 && ((g.R + g.sh - 1) / g.sh) * ((g.S + g.sw - 1) / g.sw) <= 32;
+}
+
 GemmPlan fwd_plan(const ConvGeom &g) {
-    return plan_gemm((long)g.N * g.P * g.Q, g.K, (long)g.R * g.S * g.C, 1, 16, true, kKgAuto, kAutoKc);
+    return plan_gemm((long)g.N * g.P * g.Q, g.K, (long)g.R * g.S * g.C, 1, 16, true, kKgAuto,
+                     ts_fwd(g) ? kAutoTs : kAutoKc);
 }
 
 size_t fwd_split_bytes(const ConvGeom &g) {
@@ -2375,8 +2391,7 @@ int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, 
         a2.k_split = cs.p2.k_split;
         return go_mode<kFwd>(cs.p2.t, a2, dim3(a2.ntm * a2.ntn), true, st);
     }
-    const bool ts = g.C % BK == 0 && g.R * g.S <= 32;
-    int err = go_mode<kFwd>(p.t, a, dim3(a.ntm * a.ntn, 1, p.splits), unit_geom(g), st, ts);
+    int err = go_mode<kFwd>(p.t, a, dim3(a.ntm * a.ntn, 1, p.splits), unit_geom(g), st, ts_fwd(g));
     if (err || p.splits <= 1) return err;
     return reduce_partials(a.part, p.splits, n, a.part_stride, (bf16 *)y, (const bf16 *)bias, a.N, st);
 }
@@ -2403,7 +2418,7 @@ DgradChoice dgrad_choice(const ConvGeom &g) {
     const int z = g.sh * g.sw;
     const bool unit = unit_geom(g);
     const int kg = unit ? kKgAuto : kKgForced;
-    const bool *set = unit ? kAutoKc : kAutoConv;
+    const bool *set = unit ? kAutoKc : ts_dgrad(g) ? kAutoTs : kAutoConv;
     const char *e = getenv("MEMSAVE_DGRAD");
     const int forced = forced_tile();
     // the narrow and 192-wide tiles read W through the transposed copy only
@@ -2582,9 +2597,8 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bia
                       : go_mode<kDgrad>(tsp.p2.t, a2, dim3(a2.ntm * a2.ntn), true, st);
     }
     const dim3 grid(a.ntm * a.ntn, 1, g.sh * g.sw * p.splits);
-    const bool ts = g.K % BK == 0 && ((g.R + g.sh - 1) / g.sh) * ((g.S + g.sw - 1) / g.sw) <= 32;
     int err = direct ? go_mode<kDgradN>(p.t, a, grid, unit_geom(g), st)
-                     : go_mode<kDgrad>(p.t, a, grid, unit_geom(g), st, ts);
+                     : go_mode<kDgrad>(p.t, a, grid, unit_geom(g), st, ts_dgrad(g));
     if (err) return err;
     if (cs) {
         err = launch_colsum_finalize(kBF16, a.cspart, (int)colsum_rows(g, p.t), g.K, db, st);

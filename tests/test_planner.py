@@ -122,3 +122,24 @@ def test_weight_gradient_and_refusals(lib):
     assert r == 0 and p["splits"] > 1 and p["kg"] == 1
     # channel counts that are not multiples of 8 are not the fast path's
     assert plan(lib, FWD, (64, 3, 224, 224, 64, 7, 7, 112, 112, 2, 2, 3, 3))[0] == -1
+
+
+def conv(N, C, H, K, R, stride, pad):
+    P = (H + 2 * pad - R) // stride + 1
+    return (N, C, H, H, K, R, R, P, P, stride, stride, pad, pad)
+
+
+def test_tap_step_convs_plan_without_k_groups(lib):
+    """Convolutions whose reduction channels are a multiple of 64 (the
+    forward's C, the input gradient's K) run on the tap-step operand loads
+    and plan over the tiles without k-groups: the ResNet-18-shaped stage-3
+    3x3 layer takes the 8-wave 4-stage 128 x 128 tile both ways, and no
+    tap-step convolution of the stack or the sweep takes a k-group tile."""
+    for pas in (FWD, DGRAD):
+        r, p = plan(lib, pas, conv(64, 256, 14, 256, 3, 1, 1))
+        assert r == 0 and (p["bm"], p["bn"], p["waves"], p["stages"], p["kg"]) == (128, 128, 8, 4, 1)
+    shapes = [conv(64, 64, 56, 128, 3, 2, 1), conv(64, 128, 28, 128, 3, 1, 1), conv(64, 128, 28, 256, 3, 2, 1),
+              conv(64, 256, 14, 512, 3, 2, 1), conv(64, 512, 7, 512, 3, 1, 1), conv(32, 256, 28, 256, 3, 1, 1)]
+    for geom, pas in itertools.product(shapes, (FWD, DGRAD)):
+        r, p = plan(lib, pas, geom)
+        assert r == 0 and p["kg"] == 1, (geom, pas, p)
