@@ -2147,6 +2147,17 @@ struct WgradPlan {
 // the reduction until the CUs are full.  Measured faster than plan_gemm's
 // choice on the 3x3 conv sweep (71 against 81 us), whose constants come from
 // unit-stride contractions.
+// Without the reduction's price the weight gradients took the most splits the
+// CUs allowed (the 4x4 stride-2 decoder layer 128 -> 256 channels: 256 x 256
+// tiles in 32 splits, 64 us; 128 x 128 in 8 splits, 40 us).
+constexpr double kWgradRedUnits = 6.0;
+// Tiles of the convolution weight gradient (pixel-cursor loads): 256 x 128
+// and the 8-wave 128 x 128 tiles.  Forced-tile runs on the ResNet-18-shaped
+// layers, the conv sweep and the decoder had one of them fastest on every
+// shape; 128 x 64 and the 4-wave 128 x 128 were up to 25% slower, and the
+// 256 x 256 tile keeps the generic loads.
+constexpr bool kAutoWg[kNumTiles] = {false, true, false, true, false, true, false, false, false, false};
+
 Tile pick_conv_wgrad(long M, long N, long K, int splits_allowed, int *splits_out) {
     const int z = 1;
     double best = 1e300;
@@ -2156,27 +2167,31 @@ Tile pick_conv_wgrad(long M, long N, long K, int splits_allowed, int *splits_out
     // no k-group or narrow weight gradient: plan as usual
     if (forced >= 0 && (kTiles[forced].kg > 1 || narrow_tile(kTiles[forced]))) forced = -1;
     for (int ti = 0; ti < kNumTiles; ++ti) {
-        if (forced >= 0 ? ti != forced : !kAuto[ti]) continue;
+        if (forced >= 0 ? ti != forced : !kAutoWg[ti]) continue;
         const Tile &t = kTiles[ti];
         if (t.kg > 1 || narrow_tile(t)) continue;   // neither is built for the weight gradient
         const long tiles = ((M + t.bm - 1) / t.bm) * ((N + t.bn - 1) / t.bn) * z;
-        int splits = 1;
-        if (splits_allowed > 1) {
-            const long want = (long)kCUs * t.per_cu;
-            if (tiles < want) splits = (int)std::min<long>((want + tiles - 1) / tiles, splits_allowed);
-        }
-        const long blocks = tiles * splits;
         const long conc = (long)kCUs * t.per_cu;
-        const long waves = (blocks + conc - 1) / conc;
-        // blocks that actually share a CU in the fullest wave
-        const long resident = std::min<long>(t.per_cu, (blocks + kCUs - 1) / kCUs);
-        const double kper = (double)K / splits;
-        const double eff = resident > 1 ? t.eff : t.eff1;
-        const double cost = (double)waves * resident * t.bm * t.bn * (kper + 64.0) / eff;
-        if (cost < best * 0.999) {
-            best = cost;
-            bt = t;
-            bs = splits;
+        // every split count up to the CUs' fill (ceil(fill / tiles) can spill
+        // into a second wave where floor stays in one)
+        const int max_sp = (int)std::max<long>(1, std::min<long>(splits_allowed, (2 * conc + tiles - 1) / tiles));
+        for (int splits = 1; splits <= max_sp; ++splits) {
+            const long blocks = tiles * splits;
+            const long waves = (blocks + conc - 1) / conc;
+            // blocks that actually share a CU in the fullest wave
+            const long resident = std::min<long>(t.per_cu, (blocks + kCUs - 1) / kCUs);
+            const double kper = (double)K / splits;
+            const double eff = resident > 1 ? t.eff : t.eff1;
+            // the split reduction's pass: every split writes and the reduction
+            // reads M x N fp32 partials, priced at kWgradRedUnits per element and
+            // split (8 bytes at about 3 TB/s, in the MFMA units of the first term)
+            const double red = splits > 1 ? kWgradRedUnits * (double)M * N * splits : 0.0;
+            const double cost = (double)waves * resident * t.bm * t.bn * (kper + 64.0) / eff + red;
+            if (cost < best * 0.999) {
+                best = cost;
+                bt = t;
+                bs = splits;
+            }
         }
     }
     if (splits_out) *splits_out = bs;

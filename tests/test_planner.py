@@ -143,3 +143,21 @@ def test_tap_step_convs_plan_without_k_groups(lib):
     for geom, pas in itertools.product(shapes, (FWD, DGRAD)):
         r, p = plan(lib, pas, geom)
         assert r == 0 and p["kg"] == 1, (geom, pas, p)
+
+
+def test_conv_weight_gradient_splits_stay_in_one_wave(lib):
+    """The convolution weight gradient prices its split reduction and tries
+    every split count: the 3x3 sweep layer (256 x 2304 outputs, 36 tiles of
+    128 x 128) takes 7 splits, 252 blocks in one wave of 256 CUs, where
+    ceil(256 / 36) = 8 would spill 32 blocks into a second; no plan of the
+    stack, the sweep or the decoder runs more blocks than one wave holds."""
+    r, p = plan(lib, WGRAD, conv(32, 256, 28, 256, 3, 1, 1))
+    assert r == 0 and (p["bm"], p["bn"], p["splits"]) == (128, 128, 7)
+    shapes = [conv(32, 256, 28, 256, 3, 1, 1), conv(64, 128, 28, 128, 3, 1, 1), conv(64, 128, 28, 256, 3, 2, 1),
+              conv(64, 512, 7, 512, 3, 1, 1), conv(64, 64, 56, 64, 3, 1, 1), conv(32, 128, 56, 256, 4, 2, 1)]
+    for geom in shapes:
+        r, p = plan(lib, WGRAD, geom)
+        N, C, H, _, K, R, S = geom[:7]
+        blocks = tiles(K, R * S * C, p["bm"], p["bn"]) * p["splits"]
+        per_cu = 1 if p["stages"] == 4 or p["bm"] == 256 else 2
+        assert r == 0 and blocks <= 256 * per_cu, (geom, p, blocks)
