@@ -1196,13 +1196,29 @@ struct HaloArgs {
     uint32_t in_bytes, filt_bytes, out_bytes;
 };
 
-constexpr int kHaloMaxPx = 320;                     // halo pixels per buffer (40 KB)
+// Halo pixels per buffer: 320 of 64 channels (40 KB), 640 of 16 (20 KB, the
+// least that holds the epilogue's staging).
+template <int CH> constexpr int halo_max_px() { return CH == 64 ? 320 : 640; }
 
-template <int NP, int TAPS_MAX, int KG, bool EXACT = false>
+// Chunk swizzle of a pixel row of CH channels in LDS: 128-byte rows as the
+// GEMM's k-contiguous tiles (swz_k); 32-byte rows (two 16-byte chunks) swap
+// their chunks every 4 rows, so the 8 rows one 16-byte read reaches at a time
+// cover all 32 banks.
+template <int CH> __device__ __forceinline__ int halo_swz(int row) {
+    if constexpr (CH == 64) return swz_k(row);
+    else return (row >> 2) & 1;
+}
+
+template <int NP, int TAPS_MAX, int KG, bool EXACT = false, int CH = 64>
 __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A) {
+    static_assert(CH == 64 || (CH == 16 && KG == 1 && EXACT), "16-channel pixels: one group, exact taps");
     constexpr int NW = 4 * KG;                      // waves: KG k-groups of four
-    constexpr int FILT_BYTES = TAPS_MAX * NP * 128;
-    constexpr int HALO_BYTES = kHaloMaxPx * 128;
+    constexpr int PB = CH * 2;                      // bytes of a pixel (or filter) row
+    constexpr int CPR = CH / 8;                     // 16-byte chunks per row
+    constexpr int RPI = 64 / CPR;                   // rows per LDS-DMA instruction
+    constexpr int MAXPX = halo_max_px<CH>();
+    constexpr int FILT_BYTES = TAPS_MAX * NP * PB;
+    constexpr int HALO_BYTES = MAXPX * PB;
     constexpr int TN = NP / 32;
     constexpr int TM = 2;                           // row tiles per wave
     constexpr int EPI_PITCH = NP + 8;               // staged row, bf16 elements
@@ -1220,10 +1236,15 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
     const __amdgpu_buffer_rsrc_t rin = rsrc(A.in, A.in_bytes);
     const __amdgpu_buffer_rsrc_t rf = rsrc(A.filt, A.filt_bytes);
     const __amdgpu_buffer_rsrc_t ro = rsrc(A.out, A.out_bytes);
-    // the lane's 16-byte slot of a 128-byte row, and the logical k chunk it
-    // holds in row `row` (the chunk swizzle of frag_kc)
-    const int slot = lane & 7;
-    auto chunk_of = [&](int row) { return slot ^ swz_k(row); };
+    // the lane's 16-byte slot of a row, and the logical k chunk it holds in
+    // row `row`
+    const int slot = lane % CPR;
+    auto chunk_of = [&](int row) { return slot ^ halo_swz<CH>(row); };
+    // fragment of row `row`: chunk pair `sub`, this lane's half
+    auto frag = [&](const char *base, int row, int sub) {
+        const int chunk = 2 * sub + (lane >> 5);
+        return *reinterpret_cast<const bf16x8 *>(base + row * PB + ((chunk ^ halo_swz<CH>(row)) << 4));
+    };
 
     // bias of the lane's output columns (added in fp32 before the rounding):
     // 4 consecutive channels per load through a descriptor of NO entries
@@ -1253,38 +1274,38 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
 
     // ---- the filter, once: LDS row t * NP + n = output channel n at tap t
     {
-        const int rows = taps * NP, ninstr = (rows + 7) / 8;
+        const int rows = taps * NP, ninstr = (rows + RPI - 1) / RPI;
         for (int j = wave; j < ninstr; j += NW) {
-            const int L = j * 8 + (lane >> 3);
+            const int L = j * RPI + lane / CPR;
             const int t = L / NP, n = L - t * NP;
             const int ts = A.flip ? taps - 1 - t : t;
             const bool ok = t < taps && n < A.NO;
-            const uint32_t off = ok ? (uint32_t)((n * taps + ts) * 64 + chunk_of(n) * 8) * 2u : kOOB;
+            const uint32_t off = ok ? (uint32_t)((n * taps + ts) * CH + chunk_of(n) * 8) * 2u : kOOB;
             dma16<false>(rf, sF + j * 1024, off);
         }
     }
     // ---- the halo of tile `tile` into buffer `b`.  Load instruction
-    // j = wave + NW jj carries halo pixels 8 j .. 8 j + 7, the same ones for
-    // every tile: their rows, columns and element offsets within the halo
-    // are worked out once (rows past the halo are sent out of range).
-    constexpr int HJ = (kHaloMaxPx / 8 + NW - 1) / NW;
-    const int ninstr = (HP + 7) / 8;
+    // j = wave + NW jj carries halo pixels RPI j .. RPI j + RPI - 1, the same
+    // ones for every tile: their rows, columns and element offsets within the
+    // halo are worked out once (rows past the halo are sent out of range).
+    constexpr int HJ = (MAXPX / RPI + NW - 1) / NW;
+    const int ninstr = (HP + RPI - 1) / RPI;
     int h_y[HJ], h_x[HJ];
     uint32_t h_c[HJ];
 #pragma unroll
     for (int jj = 0; jj < HJ; ++jj) {
-        const int hp = (wave + jj * NW) * 8 + (lane >> 3);
+        const int hp = (wave + jj * NW) * RPI + lane / CPR;
         const int hy = hp / HWW, hx = hp - hy * HWW;
         h_y[jj] = hp < HP ? hy : -(1 << 20);
         h_x[jj] = hx;
-        h_c[jj] = ((uint32_t)hy * (uint32_t)A.W + (uint32_t)hx) * 64u + (uint32_t)chunk_of(hp) * 8u;
+        h_c[jj] = ((uint32_t)hy * (uint32_t)A.W + (uint32_t)hx) * (uint32_t)CH + (uint32_t)chunk_of(hp) * 8u;
     }
     auto load_halo = [&](int tile, int b) {
         char *dst = smem + FILT_BYTES + b * HALO_BYTES;
         const int img = tile / A.tiles_img, rem = tile - img * A.tiles_img;
         const int ty = rem / A.tiles_w, tx = rem - ty * A.tiles_w;
         const int iy0 = ty * A.TH - A.ph, ix0 = tx * A.TW - A.pw;
-        const int gbase = ((img * A.H + iy0) * A.W + ix0) * 64;
+        const int gbase = ((img * A.H + iy0) * A.W + ix0) * CH;
 #pragma unroll
         for (int jj = 0; jj < HJ; ++jj) {
             const int j = wave + jj * NW;
@@ -1361,10 +1382,10 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
         auto read = [&](int r, int s, int t, int sub, int buf) {
             const int shift = r * HWW + s;
 #pragma unroll
-            for (int i = 0; i < TM; ++i) fa[buf][i] = frag_kc(sH, base[i] + shift, sub, lane);
-            const char *sFt = sF + t * NP * 128;
+            for (int i = 0; i < TM; ++i) fa[buf][i] = frag(sH, base[i] + shift, sub);
+            const char *sFt = sF + t * NP * PB;
 #pragma unroll
-            for (int j = 0; j < TN; ++j) fb[buf][j] = frag_kc(sFt, j * 32 + fr, sub, lane);
+            for (int j = 0; j < TN; ++j) fb[buf][j] = frag(sFt, j * 32 + fr, sub);
         };
         auto mfma = [&](int buf) {
 #pragma unroll
@@ -1377,7 +1398,7 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
             // exactly TAPS_MAX taps: every slice of the group (all four of
             // each tap, or slices kg and kg + 2 with two k-groups) unrolled,
             // fragments read two slices ahead, slice k in buffer k mod 3
-            constexpr int SPT = 4 / KG;             // slices per tap and group
+            constexpr int SPT = CH / 16 / KG;       // slices per tap and group
             constexpr int NSL = SPT * TAPS_MAX;
             auto rd = [&](int k) {
                 const int t = k / SPT, sub = KG == 1 ? k % SPT : kg + 2 * (k % SPT);
@@ -1668,6 +1689,39 @@ __global__ __launch_bounds__(256) void unpack_blocks_kernel(const bf16 *__restri
             for (int c = 0; c < 4; ++c)
                 if (c < C) row[w * C + c] = v.e[4 * b + c];
         }
+    }
+}
+
+// The forward's input in 2 x 2 pixel blocks (at most 4 channels, stride 2
+// in both dimensions): xq[n][i][j][8a + 4b + c] = x[n][2i + a - ph][2j + b - pw][c],
+// zeros outside the image and for c >= C.  One thread writes the 16 channels
+// of one block; its reads go through the buffer descriptor of x, positions
+// outside sent past its range, so all 16 are issued at once.  32-bit
+// indices: the host checks that the blocks and x fit.
+__global__ __launch_bounds__(256) void pack_blocks_kernel(const bf16 *__restrict__ x, uint32_t N, int H, int W, int C,
+                                                          int Hq, int Wq, int ph, int pw, bf16 *__restrict__ xq) {
+    const __amdgpu_buffer_rsrc_t rx = rsrc(x, (uint32_t)N * (uint32_t)H * (uint32_t)W * (uint32_t)C * 2u);
+    const uint32_t total = N * (uint32_t)Hq * (uint32_t)Wq;
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+        const uint32_t ni = i / (uint32_t)Wq, j = i - ni * (uint32_t)Wq;
+        const uint32_t n = ni / (uint32_t)Hq, iq = ni - n * (uint32_t)Hq;
+        unsigned short u[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int a = e >> 3, b = (e >> 2) & 1, c = e & 3;
+            const int h = 2 * (int)iq + a - ph, w = 2 * (int)j + b - pw;
+            const bool ok = c < C && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
+            const uint32_t off = ok ? (((n * (uint32_t)H + (uint32_t)h) * (uint32_t)W + (uint32_t)w) * (uint32_t)C + c) * 2u : kOOB;
+            u[e] = __builtin_amdgcn_raw_buffer_load_b16(rx, (int)off, 0, 0);
+        }
+        u32x4 v0, v1;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            v0[q] = (uint32_t)u[2 * q] | ((uint32_t)u[2 * q + 1] << 16);
+            v1[q] = (uint32_t)u[8 + 2 * q] | ((uint32_t)u[8 + 2 * q + 1] << 16);
+        }
+        *reinterpret_cast<u32x4 *>(xq + (size_t)i * 16) = v0;
+        *reinterpret_cast<u32x4 *>(xq + (size_t)i * 16 + 8) = v1;
     }
 }
 
@@ -2118,6 +2172,15 @@ int pack_block_filter(const ConvGeom &g, const void *w, void *wq, hipStream_t st
     return (int)hipGetLastError();
 }
 
+int pack_blocks(const ConvGeom &g, const void *x, void *xq, hipStream_t st) {
+    const int64_t work = (int64_t)g.N * block_height(g) * pair_width(g);
+    if (work == 0) return 0;
+    if (work > INT32_MAX || (int64_t)g.N * g.H * g.W * g.C * 2 >= (int64_t)kOOB) return (int)hipErrorInvalidValue;
+    hipLaunchKernelGGL(pack_blocks_kernel, dim3(launch_grid(work)), dim3(256), 0, st, (const bf16 *)x, (uint32_t)g.N, g.H,
+                       g.W, g.C, block_height(g), pair_width(g), g.ph, g.pw, (bf16 *)xq);
+    return (int)hipGetLastError();
+}
+
 int unpack_blocks(const ConvGeom &g, const void *dxq, void *dx, hipStream_t st) {
     const int64_t NH = (int64_t)g.N * g.H, work = NH * pair_width(g);
     if (work == 0) return 0;
@@ -2241,14 +2304,15 @@ bool halo_enabled() {
 
 // Output tile of the halo kernel for an output of P x Q pixels with R x S
 // taps: the width split into the fewest column tiles of at most 32, then as
-// many rows as fit both 256 pixels and a halo of at most kHaloMaxPx pixels
+// many rows as fit both 256 pixels and a halo of at most halo_max_px pixels
 // (a tile always computes 256 rows of MFMA tiles, so the largest tile is the
 // cheapest per pixel).  False when no tile fits.
-bool halo_tile(int Q, int R, int S, int *TH, int *TW) {
+bool halo_tile(int Q, int R, int S, int *TH, int *TW, int ch = 64) {
     if (Q <= 0) return false;
     const int ntw = (Q + 31) / 32;
     const int tw = (Q + ntw - 1) / ntw;
-    const int th = std::min(256 / tw, kHaloMaxPx / (tw + S - 1) - (R - 1));
+    const int maxpx = ch == 64 ? halo_max_px<64>() : halo_max_px<16>();
+    const int th = std::min(256 / tw, maxpx / (tw + S - 1) - (R - 1));
     if (th < 1) return false;
     *TH = th;
     *TW = tw;
@@ -2261,14 +2325,16 @@ bool halo_shape_ok(int NO, int taps) {
     return NO % 8 == 0 && NO > 0 && ((NO <= 32 && taps <= 16) || (NO <= 64 && taps <= 9));
 }
 
-// in[N][H][W][64] -> out[N][P][Q][NO] (see halo_conv_kernel).
+// in[N][H][W][ch] -> out[N][P][Q][NO] (see halo_conv_kernel); ch = 64, or
+// 16 (33 to 64 outputs over exactly 16 taps, the stem's 2 x 2 blocks).
 int run_halo(const bf16 *in, int N, int H, int W, const bf16 *filt, const bf16 *bias, int NO, int R, int S, int ph,
-             int pw, bool flip, bf16 *out, int P, int Q, hipStream_t st) {
+             int pw, bool flip, bf16 *out, int P, int Q, hipStream_t st, int ch = 64) {
     HaloArgs a{};
     a.in = in; a.filt = filt; a.bias = bias; a.out = out;
     a.H = H; a.W = W; a.P = P; a.Q = Q; a.R = R; a.S = S; a.ph = ph; a.pw = pw;
     a.NO = NO; a.flip = flip ? 1 : 0;
-    if (!halo_tile(Q, R, S, &a.TH, &a.TW)) return (int)hipErrorInvalidValue;
+    if (ch != 64 && !(ch == 16 && NO > 32 && NO <= 64 && R * S == 16)) return (int)hipErrorInvalidValue;
+    if (!halo_tile(Q, R, S, &a.TH, &a.TW, ch)) return (int)hipErrorInvalidValue;
     const int tiles_h = (P + a.TH - 1) / a.TH;
     a.tiles_w = (Q + a.TW - 1) / a.TW;
     a.tiles_img = tiles_h * a.tiles_w;
@@ -2276,15 +2342,18 @@ int run_halo(const bf16 *in, int N, int H, int W, const bf16 *filt, const bf16 *
     if (tiles == 0) return 0;
     if (tiles > INT32_MAX) return (int)hipErrorInvalidValue;
     a.tiles = (int)tiles;
-    a.in_bytes = bytes_of((long)N * H * W * 64);
-    a.filt_bytes = bytes_of((long)NO * R * S * 64);
+    a.in_bytes = bytes_of((long)N * H * W * ch);
+    a.filt_bytes = bytes_of((long)NO * R * S * ch);
     if (!operand_fits((long)N * P * Q * NO)) return (int)hipErrorInvalidValue;
     a.out_bytes = bytes_of((long)N * P * Q * NO);
     const dim3 grid((unsigned)std::min<long>(tiles, kCUs));
     const unsigned pk = flip ? kProfDgrad : kProfFwd;
     void *eb = nullptr, *ee = nullptr;
     const bool timed = prof_pair(pk, &eb, &ee);
-    if (NO <= 32 && R * S == 16)   // 4 x 4: the unrolled schedule
+    if (ch == 16)
+        hipExtLaunchKernelGGL((halo_conv_kernel<64, 16, 1, true, 16>), grid, dim3(256), 0, st, (hipEvent_t)eb,
+                              (hipEvent_t)ee, 0, a);
+    else if (NO <= 32 && R * S == 16)   // 4 x 4: the unrolled schedule
         hipExtLaunchKernelGGL((halo_conv_kernel<32, 16, 2, true>), grid, dim3(512), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
     else if (NO <= 32)
         hipExtLaunchKernelGGL((halo_conv_kernel<32, 16, 2>), grid, dim3(512), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
@@ -2295,6 +2364,18 @@ int run_halo(const bf16 *in, int N, int H, int W, const bf16 *filt, const bf16 *
     const int err = (int)hipGetLastError();
     if (timed) prof_pair_done(pk, eb, ee, err == 0);
     return err;
+}
+
+// Forward of a layer with at most 4 input channels and stride 2 (the stem)
+// through 2 x 2 pixel blocks: a stride-1 convolution of 16-channel blocks
+// with 4 x 4 taps, 33 to 64 outputs (a multiple of 8).
+bool halo_block_fwd_applies(const ConvGeom &g) {
+    if (!halo_enabled() || !block_applies(g) || (g.R + 1) / 2 != 4 || (g.S + 1) / 2 != 4) return false;
+    if (g.K % 8 != 0 || g.K <= 32 || g.K > 64) return false;
+    const ConvGeom q = blocked(g);
+    int th, tw;
+    return operand_fits((long)g.N * g.P * g.Q * g.K) && operand_fits((long)q.N * q.H * q.W * 16) &&
+           halo_tile(g.Q, 4, 4, &th, &tw, 16);
 }
 
 // Forward: stride 1, 64 input channels, the filter within the kernel's
@@ -2335,6 +2416,7 @@ size_t fwd_split_bytes(const ConvGeom &g) {
 // the padded contraction (split-K partials).
 size_t fwd_workspace(const ConvGeom &g) {
     if (g.C % 8 == 0) return fwd_split_bytes(g);
+    if (halo_block_fwd_applies(g)) return block_x_bytes(g) + block_w_bytes(g);
     if (pair_applies(g)) return pair_x_bytes(g) + pair_w_bytes(g) + fwd_split_bytes(paired(g));
     const int C8 = pad8(g.C);
     return al256((size_t)g.N * g.H * g.W * C8 * 2) + al256((size_t)g.K * g.R * g.S * C8 * 2) +
@@ -2342,6 +2424,18 @@ size_t fwd_workspace(const ConvGeom &g) {
 }
 
 int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, void *y, void *ws, hipStream_t st) {
+    if (g.C % 8 != 0 && halo_block_fwd_applies(g)) {
+        // the stem: 2 x 2 pixel blocks, a stride-1 4 x 4 convolution of 16 channels
+        if (!ws || !al16(ws) || !al16(y)) return -1;
+        char *xq = static_cast<char *>(ws);
+        char *wq = xq + block_x_bytes(g);
+        int err = pack_blocks(g, x, xq, st);
+        if (!err) err = pack_block_filter(g, w, wq, st);
+        if (err) return err;
+        const ConvGeom q = blocked(g);
+        return run_halo((const bf16 *)xq, q.N, q.H, q.W, (const bf16 *)wq, (const bf16 *)bias, g.K, 4, 4, 0, 0, false,
+                        (bf16 *)y, g.P, g.Q, st, 16);
+    }
     if (g.C % 8 != 0 && pair_applies(g)) {
         if (!ws || !al16(ws) || !al16(y)) return -1;
         char *xq = static_cast<char *>(ws);
