@@ -1,7 +1,8 @@
 """The halo convolution path: stride-1 convolutions of 64-channel inputs whose
 filter fits in LDS (the 3x3 64 -> 64 layers of a ResNet stage 1, forward and
-input gradient) and the input gradient of a 3-channel stride-2 stem through
-its 2x2-block form (a 4x4 stride-1 correlation of the 64-channel dy).  Each
+input gradient) and a 3-channel stride-2 stem through its 2x2-block form: the
+forward as a 4x4 stride-1 convolution of 16-channel blocks, the input gradient
+as a 4x4 stride-1 correlation of the 64-channel dy.  Each
 case runs with the halo kernel and with it switched off
 (MEMSAVE_CONV_HALO=off, the implicit GEMM), both against the oracle, on
 ragged tile grids, widths below and above one 32-wide column tile, zero
@@ -29,7 +30,8 @@ CASES = [
     ((2, 64, 10, 9), (48, 64, 2, 3), (1, 1), (1, 1)),      # 48 outputs, 2 x 3 taps: the generic 64-column loop
     ((2, 40, 9, 11), (64, 40, 2, 2), (1, 1), (1, 1)),      # input gradient of 40 channels, 2 x 2 taps
     ((1, 16, 12, 14), (64, 16, 4, 4), (1, 1), (0, 3)),     # input gradient only: 16 channels, 4 x 4 taps
-    ((2, 3, 37, 41), (64, 3, 7, 7), (2, 2), (3, 3)),       # stem: input gradient through 2 x 2 blocks
+    ((2, 3, 37, 41), (64, 3, 7, 7), (2, 2), (3, 3)),       # stem: both ways through 2 x 2 blocks
+    ((2, 2, 21, 18), (48, 2, 7, 7), (2, 2), (3, 3)),       # 16-channel blocks: 48 outputs, 2 input channels
 ]
 
 
