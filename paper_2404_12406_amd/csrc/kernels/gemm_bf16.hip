@@ -1504,50 +1504,43 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
 }
 
 // Wt[c][rs][k] = W[k][rs][c]: the input gradient reads the (frozen) filter
-// with its reduction index k contiguous.  A block moves a 64 (k) x 64 (c)
-// tile of one tap rs through LDS; global reads and writes are 16-byte
-// vectors that cover whole 128-byte rows.  Grid (ceil(C/64), ceil(K/64), R*S).
-__global__ __launch_bounds__(256) void transpose_krsc_kernel(const bf16 *__restrict__ W, bf16 *__restrict__ Wt,
+// with its reduction index k contiguous.  K and C are multiples of 8 (the
+// input gradient's fast path pads C and refuses other K), so W splits into
+// whole 8 (k) x 8 (c) blocks of one tap, and each thread moves one in
+// registers: eight 16-byte row loads (all in flight together), the transpose
+// by 16-bit halves, eight 16-byte stores.  The 16 lanes of a block row take
+// adjacent c blocks (one 256-byte run of a W row per load), the 8 block rows
+// adjacent k blocks (64-byte runs of a Wt row per store, merged in L2).  No
+// LDS and no barrier: a block is 64 k x 128 c of one tap.
+// Grid (ceil(C/128), ceil(K/64), R*S), 128 threads.
+__global__ __launch_bounds__(128) void transpose_krsc_kernel(const bf16 *__restrict__ W, bf16 *__restrict__ Wt,
                                                              int K, int RS, int C) {
-    constexpr int PITCH = 64 + 2;   // odd word pitch: the column reads below hit distinct banks
-    __shared__ bf16 t[64 * PITCH];
-    const int c0 = blockIdx.x * 64, k0 = blockIdx.y * 64, rs = blockIdx.z;
-    const int tid = threadIdx.x;
-    const bool full = c0 + 64 <= C && k0 + 64 <= K && (C % 8) == 0 && (K % 8) == 0;
-    // read: thread -> (row k = tid/8 + 32 p, 8-column chunk tid%8)
+    const int cb = blockIdx.x * 16 + (threadIdx.x & 15);   // 8-column block
+    const int kb = blockIdx.y * 8 + (threadIdx.x >> 4);    // 8-row block
+    const int rs = blockIdx.z;
+    if (cb * 8 >= C || kb * 8 >= K) return;
+    u32x4 v[8];
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
-        const int kl = tid / 8 + 32 * p, cl = (tid % 8) * 8;
-        const int k = k0 + kl;
-        const bf16 *src = W + ((size_t)k * RS + rs) * C + c0 + cl;
-        if (full) {
-            const Vec16<bf16> v = load16(src);
+    for (int r = 0; r < 8; ++r)
+        v[r] = *reinterpret_cast<const u32x4 *>(W + ((size_t)(kb * 8 + r) * RS + rs) * C + cb * 8);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) t[kl * PITCH + cl + e] = v.e[e];
-        } else {
+    for (int c = 0; c < 8; ++c) {
+        // column c of the block: element c of rows 0..7, two per word
+        u32x4 o;
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                t[kl * PITCH + cl + e] = (k < K && c0 + cl + e < C) ? src[e] : (bf16)0.f;
+        for (int q = 0; q < 4; ++q) {
+            const uint32_t lo = v[2 * q][c / 2], hi = v[2 * q + 1][c / 2];
+            o[q] = (c & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
         }
+        *reinterpret_cast<u32x4 *>(Wt + ((size_t)(cb * 8 + c) * RS + rs) * K + kb * 8) = o;
     }
-    __syncthreads();
-    // write: thread -> (row c = tid/8 + 32 p, 8-k chunk tid%8)
-#pragma unroll
-    for (int p = 0; p < 2; ++p) {
-        const int cl = tid / 8 + 32 * p, kl = (tid % 8) * 8;
-        const int c = c0 + cl;
-        Vec16<bf16> v;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v.e[e] = t[(kl + e) * PITCH + cl];
-        bf16 *dst = Wt + ((size_t)c * RS + rs) * K + k0 + kl;
-        if (full) {
-            store16(dst, v);
-        } else if (c < C) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-                if (k0 + kl + e < K) dst[e] = v.e[e];
-        }
-    }
+}
+
+int transpose_krsc(const void *w, bf16 *wt, int K, int RS, int C, hipStream_t st) {
+    if (K % 8 != 0 || C % 8 != 0) return (int)hipErrorInvalidValue;
+    hipLaunchKernelGGL(transpose_krsc_kernel, dim3((C + 127) / 128, (K + 63) / 64, RS), dim3(128), 0, st,
+                       (const bf16 *)w, wt, K, RS, C);
+    return (int)hipGetLastError();
 }
 
 // Channel counts that are not a multiple of 8 (the 3-channel stem): the fast
@@ -2638,9 +2631,7 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bia
         // the correlation of dy with the flipped, transposed filter Wt[c][r][s][k]
         if (!ws || !al16(ws)) return -1;
         bf16 *wt = reinterpret_cast<bf16 *>(ws);
-        hipLaunchKernelGGL(transpose_krsc_kernel, dim3((g.C + 63) / 64, (g.K + 63) / 64, g.R * g.S), dim3(256), 0, st,
-                           (const bf16 *)w, wt, g.K, g.R * g.S, g.C);
-        const int err = (int)hipGetLastError();
+        const int err = transpose_krsc(w, wt, g.K, g.R * g.S, g.C, st);
         if (err) return err;
         return run_halo((const bf16 *)dy, g.N, g.P, g.Q, wt, (const bf16 *)bias, g.C, g.R, g.S, g.R - 1 - g.ph,
                         g.S - 1 - g.pw, true, (bf16 *)dx, g.H, g.W, st);
@@ -2661,9 +2652,7 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bia
     a.K = ((g.R + g.sh - 1) / g.sh) * ((g.S + g.sw - 1) / g.sw) * g.K;
     if (a.M == 0 || a.N == 0) return 0;
     if (!direct) {
-        hipLaunchKernelGGL(transpose_krsc_kernel, dim3((g.C + 63) / 64, (g.K + 63) / 64, g.R * g.S), dim3(256), 0, st,
-                           (const bf16 *)w, wt, g.K, g.R * g.S, g.C);
-        const int err = (int)hipGetLastError();
+        const int err = transpose_krsc(w, wt, g.K, g.R * g.S, g.C, st);
         if (err) return err;
     }
     a.ntm = (a.M + p.t.bm - 1) / p.t.bm; a.ntn = (a.N + p.t.bn - 1) / p.t.bn;
