@@ -286,23 +286,31 @@ struct Cfg {
     // forward: the block's bias columns, loaded once into LDS past the stages
     // (one 16-byte load per lane of wave 0)
     static constexpr int BIAS_OFF = LDS_BYTES;
-    static constexpr int SMEM_BYTES = LDS_BYTES + (MODE == kFwd ? 64 * 16 : 0);
-    static constexpr int NIA = A_BYTES / 1024 / NW;   // load instructions per wave per tile
-    static constexpr int NIB = B_BYTES / 1024 / NW;
+    // 1 KB load instructions per tile, and per wave: where the waves do not
+    // divide A's (12 waves, 32 KB), the last waves' spare slots load zeros
+    // into a dummy area past everything else, so that every wave issues the
+    // same number of loads per stage (the vmcnt waits count them)
+    static constexpr int A_INS = A_BYTES / 1024, B_INS = B_BYTES / 1024;
+    static constexpr int NIA = (A_INS + NW - 1) / NW;
+    static constexpr int NIB = B_INS / NW;
+    static constexpr bool A_SPARE = NIA * NW != A_INS;
+    static constexpr int DUMMY_OFF = LDS_BYTES + (MODE == kFwd ? 64 * 16 : 0);
+    static constexpr int SMEM_BYTES = DUMMY_OFF + (A_SPARE ? 1024 : 0);
     static constexpr int WM = BM / WR, WN = BN / WC;
     static constexpr int TM = WM / 32, TN = WN / 32;   // 32x32 MFMA tiles per wave
     static constexpr int NSUB = BK / 16;               // 16-k slices per step
     static constexpr int EPI_PITCH = WN + 8;           // bf16 elements per staged row
     static constexpr int EPI_ROWS = 32;                // rows staged per pass
-    static_assert(NIA >= 1 && NIB >= 1 && NIA * NW * 1024 == A_BYTES && NIB * NW * 1024 == B_BYTES, "load split");
+    static_assert(NIA >= 1 && NIB >= 1 && A_INS * 1024 == A_BYTES && NIB * NW * 1024 == B_BYTES, "load split");
+    static_assert(!A_SPARE || (A_KC && MODE != kWgrad), "spare A load slots: k-contiguous A only");
     static_assert(TM >= 1 && TN >= 1 && WM % 32 == 0 && WN % 32 == 0, "wave tile");
     static_assert(NW * EPI_ROWS * EPI_PITCH * 2 <= LDS_BYTES, "epilogue staging must fit in LDS");
     static_assert(SMEM_BYTES <= 160 * 1024, "LDS");
     static_assert(BN * 2 <= 64 * 16, "bias columns fit the bias area");
     static_assert(KG == 1 || (KG == 2 && STAGES >= 3 && MODE != kWgrad), "k-groups: spread pipeline, no weight gradient");
-    // block widths that are not a power of two (192) only with both operands
+    // block widths that are not a power of two (192, 288) only with both operands
     // k-contiguous: the transposing reads' slot swizzle needs 2^n slots a row
-    static_assert((BN & (BN - 1)) == 0 || (A_KC && B_KC), "a 192-wide tile reads k-contiguous operands only");
+    static_assert((BN & (BN - 1)) == 0 || (A_KC && B_KC), "a 192- or 288-wide tile reads k-contiguous operands only");
     static_assert(KG == 1 || (WR * WC) * (WM / 32) * (WN / 32) * 16 * 64 * 4 <= LDS_BYTES, "k-group partials fit LDS");
 };
 
@@ -314,6 +322,7 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
     // LDS-DMA issue form (see dma16): assembly when an operand is read with
     // transposing LDS reads
     constexpr bool ASM_DMA = !(G::A_KC && G::B_KC);
+    static_assert(!G::A_SPARE || (UNIT && !TS), "spare A load slots: the unit-geometry loads only");
     __shared__ __attribute__((aligned(1024))) char smem[G::SMEM_BYTES];
 
     const ConvGeom &g = P.g;
@@ -371,8 +380,13 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
     int a_base[NIA], a_y[NIA], a_x[NIA];
     uint32_t a_mn_off[NIA];
     bool a_ok[NIA];
-    int b_base[NIB];
     bool b_ok[NIB];
+    // Unit-geometry A and every k-contiguous B: the rows of a wave's loads
+    // are 8 apart, so their element offsets are one per-lane base plus a
+    // uniform stride per load (a row past the operand is never read: its
+    // load takes the out-of-range offset).  One register instead of one per
+    // load.
+    uint32_t a_u0 = 0, a_urs = 0, b_u0 = 0, b_urs = 0;
     uint32_t b_mn_off[NIB];
     int b_r[NIB], b_s[NIB];
 
@@ -381,11 +395,10 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
         for (int j = 0; j < NIA; ++j) {
             const int row = (wave * NIA + j) * 8 + kc_row;
             const int m = m0 + row;
-            a_ok[j] = m < M;
+            a_ok[j] = m < M && (!G::A_SPARE || wave * NIA + j < G::A_INS);
             const int mm = a_ok[j] ? m : 0;
             if constexpr (UNIT) {
-                a_base[j] = mm * (MODE == kFwd ? g.C : g.K);
-                a_y[j] = a_x[j] = 0;
+                a_base[j] = a_y[j] = a_x[j] = 0;
             } else if constexpr (MODE == kFwd) {
                 const int PQ = g.P * g.Q;
                 const int n = mm / PQ, pq = mm - n * PQ;
@@ -401,6 +414,11 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
                 a_y[j] = i2 + f.dh;
                 a_x[j] = j2 + f.dw;
             }
+        }
+        if constexpr (UNIT) {
+            const uint32_t S = MODE == kFwd ? g.C : g.K;
+            a_u0 = (uint32_t)(m0 + wave * NIA * 8 + kc_row) * S;
+            a_urs = 8u * S;
         }
     } else {
         // WGRAD A = dy^T: k-rows are (n,p,q), slots run along m (the K channels)
@@ -420,9 +438,11 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
             const int row = (wave * NIB + j) * 8 + kc_row;
             const int n = n0 + row;
             b_ok[j] = n < N;
-            // FWD: W[n][(r,s,c)] (row length R*S*C); DGRAD: Wt[c][(r,s,k)] (R*S*K)
-            b_base[j] = (b_ok[j] ? n : 0) * (MODE == kFwd ? Kg : g.R * g.S * g.K);
         }
+        // FWD: W[n][(r,s,c)] (row length R*S*C); DGRAD: Wt[c][(r,s,k)] (R*S*K)
+        const uint32_t L = MODE == kFwd ? Kg : g.R * g.S * g.K;
+        b_u0 = (uint32_t)(n0 + wave * NIB * 8 + kc_row) * L;
+        b_urs = 8u * L;
     } else {
         constexpr int SPR = BN / 8, KPI = 64 / SPR;
 #pragma unroll
@@ -487,7 +507,7 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
 #pragma unroll
         for (int j = 0; j < NIB; ++j) {
             const int v = (wave * NIB + j) & 1;
-            b_rowb[j] = (uint32_t)(b_base[j] + (kc0 ^ v) * 8) * 2u;
+            b_rowb[j] = (b_u0 + (uint32_t)j * b_urs + (uint32_t)((kc0 ^ v) * 8)) * 2u;
         }
     }
     // Tap cursor of the last step issued (uniform).  The steps are issued in
@@ -657,20 +677,23 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
             for (int j = 0; j < NIA; ++j) {
                 const int v = (wave * NIA + j) & 1;
                 bool ok = kin[v] && a_ok[j];
-                int off;
+                uint32_t off;
                 if constexpr (UNIT) {
-                    off = a_base[j] + off_k[v];
+                    off = a_u0 + (uint32_t)j * a_urs + (uint32_t)off_k[v];
                 } else if constexpr (MODE == kFwd) {
                     const int ih = a_y[j] + dr[v], iw = a_x[j] + ds[v];
                     ok = ok && (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
-                    off = a_base[j] + (ih * g.W + iw) * g.C + off_k[v];
+                    off = (uint32_t)(a_base[j] + (ih * g.W + iw) * g.C + off_k[v]);
                 } else {
                     const int p = a_y[j] + dr[v], q = a_x[j] + ds[v];
                     ok = ok && (unsigned)p < (unsigned)g.P && (unsigned)q < (unsigned)g.Q;
-                    off = a_base[j] + (p * g.Q + q) * g.K + off_k[v];
+                    off = (uint32_t)(a_base[j] + (p * g.Q + q) * g.K + off_k[v]);
                 }
-                const uint32_t boff = ok ? (uint32_t)off * 2u : kOOB;
-                if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
+                const uint32_t boff = ok ? off * 2u : kOOB;
+                // a spare slot (its a_ok is false, so it loads zeros) writes the dummy area
+                char *dst = (!G::A_SPARE || wave * NIA + j < G::A_INS) ? sA + (wave * NIA + j) * 1024
+                                                                       : smem + G::DUMMY_OFF;
+                if (j >= lo && j < hi) dma16<ASM_DMA>(ra, dst, boff);
             }
         } else {
             constexpr int SPR = BM / 8, KPI = 64 / SPR;
@@ -702,7 +725,7 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
             for (int j = 0; j < NIB; ++j) {
                 const int v = (wave * NIB + j) & 1;
                 const bool ok = kin[v] && b_ok[j];
-                const uint32_t boff = ok ? (uint32_t)(b_base[j] + off_k[v]) * 2u : kOOB;
+                const uint32_t boff = ok ? (b_u0 + (uint32_t)j * b_urs + (uint32_t)off_k[v]) * 2u : kOOB;
                 if (NIA + j >= lo && NIA + j < hi) dma16<ASM_DMA>(rb, sB + (wave * NIB + j) * 1024, boff);
             }
         } else {
@@ -890,6 +913,41 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
             fb1[j] = fb2[j];
         }
     };
+    // two stages with two fragment buffers (the 12-wave tile, whose three
+    // waves per SIMD leave no registers for a third): fragments are read one
+    // slice ahead, so a wave's last read of tile kt is issued in slice 2 and
+    // the barrier comes at the start of slice 3; the whole refill of tile
+    // kt's stage with tile kt+2 is issued right after it.  The loads still
+    // have a full step to land (until slice 3 of step kt+1), and the other
+    // two waves of the SIMD cover the barrier.  On entry fa0 / fb0 hold
+    // slice 0 of tile kt; on exit, of tile kt+1.
+    auto step_two_lean = [&](int kt) {
+        const int s = kt % STAGES, s1 = (kt + 1) % STAGES;
+        const int rk = k_begin + (kt + STAGES) * BK;
+        __builtin_amdgcn_sched_barrier(0);
+        read_sub(s, 1, fa1, fb1);            // slice 0: read slice 1
+        mfma_sub(fa0, fb0);
+        interleave(0);
+        __builtin_amdgcn_sched_barrier(0);
+        read_sub(s, 2, fa0, fb0);            // slice 1: read slice 2
+        mfma_sub(fa1, fb1);
+        interleave(0);
+        __builtin_amdgcn_sched_barrier(0);
+        read_sub(s, 3, fa1, fb1);            // slice 2: read slice 3
+        mfma_sub(fa0, fb0);
+        interleave(0);
+        __builtin_amdgcn_sched_barrier(0);
+        wait_vmcnt<0>();                     // slice 3: tile kt+1 landed, tile kt read by all
+        wait_lgkm0();
+        block_sync<ASM_DMA>();
+        __builtin_amdgcn_sched_barrier(0);
+        issue_range(s, rk, 0, NVMEM);
+        read_sub(s1, 0, fa0, fb0);
+        mfma_sub(fa1, fb1);
+        interleave(NVMEM);
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    constexpr bool LEAN = STAGES == 2 && G::NW > 8;
     static_assert(NSUB % 2 == 0, "an even number of slices keeps the fragment buffers' roles fixed");
     // two k-groups (three or more stages): group kg does slices 2kg and
     // 2kg+1 of each step.  On entry (fa0, fb0) hold slice 2kg of tile kt.
@@ -940,6 +998,9 @@ __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args
         for (int kt = 0; kt < nk; ++kt) step_kg(kt);
     } else if constexpr (SPREAD) {
         for (int kt = 0; kt < nk; ++kt) step_spread(kt);
+    } else if constexpr (LEAN) {
+        static_assert(NSUB == 4, "the two-stage schedule is written for four slices per step");
+        for (int kt = 0; kt < nk; ++kt) step_two_lean(kt);
     } else {
         static_assert(NSUB == 4, "the two-stage schedule is written for four slices per step");
         read_sub(0, 1, fa1, fb1);
@@ -1797,6 +1858,7 @@ constexpr Tile kTiles[] = {
     {"128x64", 128, 64, 2, 2, 2, 3, 0.75f, 0.75f},        // 4 waves of 64 x 32, 48 KB, three blocks per CU
     {"256x32", 256, 32, 4, 1, 2, 2, 0.70f, 0.70f},        // 4 waves of 64 x 32, 72 KB, two blocks per CU
     {"128x192k2", 128, 192, 2, 2, 3, 1, 0.82f, 0.82f, 2},  // 2 k-groups of 4 waves of 64 x 96, 3 stages (120 KB)
+    {"256x288", 256, 288, 4, 3, 2, 1, 1.10f, 1.10f},      // 12 waves of 64 x 96, 2 stages (137 KB)
 };
 constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 // tiles the planner chooses from
@@ -1805,7 +1867,7 @@ constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 // (weight gradient 4096 x 1024 x 4096: 57 -> 46 us), and the k-group tile
 // beats that one by ~5% on the forward and input gradient of 4096 x 1024
 // outputs with K = 4096 (38.7 -> 36.3 us)
-constexpr bool kAuto[kNumTiles] = {true, true, true, true, false, true, true, true, false, false};
+constexpr bool kAuto[kNumTiles] = {true, true, true, true, false, true, true, true, false, false, false};
 // the narrow 256 x 32 tile is for thin outputs (N <= 32, e.g. the input
 // gradient of a 3-channel image) and exists only for the contractions whose
 // operands are both k-contiguous (forward, input gradient through the
@@ -1816,8 +1878,15 @@ constexpr bool narrow_tile(const Tile &t) { return t.bn < 64; }
 // its block width is not a power of two.  On 8192-row outputs it makes every
 // encoder shape a whole number of waves (8192 x 768: 256 tiles, where
 // 256 x 128 leaves 64 CUs idle).
-constexpr bool kc_only(const Tile &t) { return narrow_tile(t) || t.bn == 192; }
-constexpr bool kAutoKc[kNumTiles] = {true, true, true, true, false, true, true, true, true, true};
+constexpr bool kc_only(const Tile &t) { return narrow_tile(t) || t.bn == 192 || t.bn == 288; }
+constexpr bool kAutoKc[kNumTiles] = {true, true, true, true, false, true, true, true, true, true, false};
+// The 256 x 288 tile (12 waves of 64 x 96, three per SIMD) exists for the
+// Linear forward only (the unit-geometry loads; the input gradient's fused
+// bias column sums leave it short of registers).  An 8192 x 2304 output (the
+// encoder's QKV forward) is 256 of its tiles, one wave, where 256 x 256
+// makes 288 tiles: one wave plus a column-split remainder that runs on half
+// the chip.
+constexpr bool kAutoUnitKc[kNumTiles] = {true, true, true, true, false, true, true, true, true, true, true};
 // tiles the planner chooses from for the input gradient of convolutions
 // that are not 1x1 / stride 1 (implicit-GEMM gathers): on the
 // ResNet-18-shaped stack's layers and the conv sweep the 2-stage 128 x 128
@@ -1829,7 +1898,7 @@ constexpr bool kAutoKc[kNumTiles] = {true, true, true, true, false, true, true, 
 // 0.121 -> 0.116 ms.  The forward keeps the general set: restricted the same
 // way it took split reductions whose extra pass made the frozen stack 6%
 // slower.
-constexpr bool kAutoConv[kNumTiles] = {true, false, true, false, false, false, false, true, true, false};
+constexpr bool kAutoConv[kNumTiles] = {true, false, true, false, false, false, false, true, true, false, false};
 // tiles for convolutions on the tap-step operand loads (the forward with C,
 // or the input gradient with K, a multiple of BK): without the per-lane
 // divisions the 8-wave 4-stage 128 x 128 tile is the fastest or near it on
@@ -1837,7 +1906,7 @@ constexpr bool kAutoConv[kNumTiles] = {true, false, true, false, false, false, f
 // -> 25.5 us against the 4-wave tile, stride-2 stage-4 31.2 -> 22.2 us,
 // stage-3 forward 23.9 -> 20.9 us against the k-group tile), and the k-group
 // tiles lose to it
-constexpr bool kAutoTs[kNumTiles] = {true, true, true, true, false, true, false, true, true, false};
+constexpr bool kAutoTs[kNumTiles] = {true, true, true, true, false, true, false, true, true, false, false};
 
 // MEMSAVE_GEMM_TILE=<name> forces one tile shape (a debugging and testing
 // knob); returns its index or -1.
@@ -1910,6 +1979,8 @@ GemmPlan plan_gemm(long M, long N, long K, int z, int split_cap = 16, bool allow
     if (forced >= 0 && (kTiles[forced].kg > 1 || kc_only(kTiles[forced])) && kgroups == kKgNever) forced = -1;
     // the in-place input gradient (its set is kAuto) has no k-contiguous-only tile: plan as usual
     if (forced >= 0 && kc_only(kTiles[forced]) && auto_set == kAuto) forced = -1;
+    // the 288-wide tile exists for the unit-geometry forward only (its set is kAutoUnitKc)
+    if (forced >= 0 && kTiles[forced].bn == 288 && auto_set != kAutoUnitKc) forced = -1;
     if (forced == 0 && !allow_256x256) forced = 1;   // the next widest tile (256 x 128)
     const int fs = split_cap > 1 ? forced_splits() : 0;
     const int max_splits = (int)std::max<long>(1, std::min<long>(split_cap, K / (4 * BK)));
@@ -1919,11 +1990,14 @@ GemmPlan plan_gemm(long M, long N, long K, int z, int split_cap = 16, bool allow
         if (forced >= 0 ? ti != forced : !auto_set[ti]) continue;
         if (ti == 0 && !allow_256x256) continue;
         if (kTiles[ti].kg > 1 && (kgroups == kKgNever || (kgroups == kKgForced && forced < 0))) continue;
-        // the 192-wide tile pays off only where it fills the CUs in one wave
-        // (encoder shapes, 8192 x {768, 2304, 3072} outputs: 34 against 38 us
-        // at K = 2304 in one wave, 49 against 44 us in three waves at K = 768)
-        if (forced < 0 && kTiles[ti].bn == 192 &&
-            ((M + 127) / 128) * ((N + 191) / 192) * z > (long)kCUs * kTiles[ti].per_cu) continue;
+        // the 192- and 288-wide tiles pay off only where they fill the CUs in
+        // one wave (encoder shapes, 8192 x {768, 2304, 3072} outputs: 34
+        // against 38 us at K = 2304 in one wave, 49 against 44 us in three
+        // waves at K = 768)
+        if (forced < 0 && (kTiles[ti].bn == 192 || kTiles[ti].bn == 288) &&
+            ((M + kTiles[ti].bm - 1) / kTiles[ti].bm) * ((N + kTiles[ti].bn - 1) / kTiles[ti].bn) * z >
+                (long)kCUs * kTiles[ti].per_cu)
+            continue;
         for (int sp = 1; sp <= (fs ? 1 : max_splits); ++sp) {
             const int splits = fs ? fs : sp;
             const double us = est_us(kTiles[ti], M, N, K, z, splits);
@@ -2012,6 +2086,10 @@ constexpr bool has_256x256() { return !(MODE == kDgrad && !UNIT); }
 
 template <int MODE, bool UNIT, bool TS = false>
 int go_tile(const Tile &t, const Args &a, dim3 grid, hipStream_t st) {
+    if (t.bn == 288) {
+        if constexpr (MODE == kFwd && UNIT && !TS) return go<MODE, 256, 288, 4, 3, 2, 1, UNIT>(a, grid, st);
+        else return (int)hipErrorInvalidValue;
+    }
     if (t.bm == 256 && t.bn == 256) {
         // the weight gradient's 256 x 256 tile has no registers left for the
         // pixel cursor (it spilled): the generic loads
@@ -2212,7 +2290,7 @@ constexpr double kWgradRedUnits = 6.0;
 // layers, the conv sweep and the decoder had one of them fastest on every
 // shape; 128 x 64 and the 4-wave 128 x 128 were up to 25% slower, and the
 // 256 x 256 tile keeps the generic loads.
-constexpr bool kAutoWg[kNumTiles] = {false, true, false, true, false, true, false, false, false, false};
+constexpr bool kAutoWg[kNumTiles] = {false, true, false, true, false, true, false, false, false, false, false};
 
 Tile pick_conv_wgrad(long M, long N, long K, int splits_allowed, int *splits_out) {
     const int z = 1;
@@ -2221,11 +2299,11 @@ Tile pick_conv_wgrad(long M, long N, long K, int splits_allowed, int *splits_out
     int bs = 1;
     int forced = forced_tile();
     // no k-group or narrow weight gradient: plan as usual
-    if (forced >= 0 && (kTiles[forced].kg > 1 || narrow_tile(kTiles[forced]))) forced = -1;
+    if (forced >= 0 && (kTiles[forced].kg > 1 || kc_only(kTiles[forced]))) forced = -1;
     for (int ti = 0; ti < kNumTiles; ++ti) {
         if (forced >= 0 ? ti != forced : !kAutoWg[ti]) continue;
         const Tile &t = kTiles[ti];
-        if (t.kg > 1 || narrow_tile(t)) continue;   // neither is built for the weight gradient
+        if (t.kg > 1 || kc_only(t)) continue;   // none of these is built for the weight gradient
         const long tiles = ((M + t.bm - 1) / t.bm) * ((N + t.bn - 1) / t.bn) * z;
         const long conc = (long)kCUs * t.per_cu;
         // every split count up to the CUs' fill (ceil(fill / tiles) can spill
@@ -2396,7 +2474,7 @@ bool ts_dgrad(const ConvGeom &g) {
 
 GemmPlan fwd_plan(const ConvGeom &g) {
     return plan_gemm((long)g.N * g.P * g.Q, g.K, (long)g.R * g.S * g.C, 1, 16, true, kKgAuto,
-                     ts_fwd(g) ? kAutoTs : kAutoKc);
+                     ts_fwd(g) ? kAutoTs : unit_geom(g) ? kAutoUnitKc : kAutoKc);
 }
 
 size_t fwd_split_bytes(const ConvGeom &g) {

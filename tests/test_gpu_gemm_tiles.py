@@ -17,7 +17,7 @@ pytestmark = pytest.mark.gpu
 # biases are drawn at the outputs' scale (N(0, 1)), so a dropped or
 # misplaced bias fails the 2e-2 bar by far
 TILES = ["256x256", "256x128", "128x128", "128x128w8", "128x128s4", "128x128w8s4", "128x128k2", "128x64", "256x32",
-         "128x192k2"]
+         "128x192k2", "256x288"]
 
 CASES = [
     # x shape, w shape, stride, pad

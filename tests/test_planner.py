@@ -36,12 +36,14 @@ def tiles(M, N, bm, bn):
 
 
 def test_headline_shapes(lib):
-    """The encoder linears at 8192 tokens: the forward of QKV and FFN up and
-    the input gradient of FFN down split their output columns at 2048 (256
-    tiles of 256 x 256, one per CU) and cover the rest on a second tile; the
-    768-wide outputs take the 128 x 192 tile (256 tiles, one wave)."""
+    """The encoder linears at 8192 tokens: the QKV forward takes the 256 x 288
+    tile (256 tiles, one wave); the forward of FFN up and the input gradient
+    of FFN down split their output columns at 2048 (256 tiles of 256 x 256,
+    one per CU) and cover the rest on a second tile; the 768-wide outputs
+    take the 128 x 192 tile (256 tiles, one wave)."""
     r, p = plan(lib, FWD, linear(8192, 768, 2304))
-    assert r == 0 and (p["bm"], p["bn"], p["n1"]) == (256, 256, 2048) and p["splits"] == 1
+    assert r == 0 and (p["bm"], p["bn"], p["n1"]) == (256, 288, 0) and p["splits"] == 1
+    assert tiles(8192, 2304, 256, 288) == 256
     r, p = plan(lib, FWD, linear(8192, 768, 3072))
     assert r == 0 and (p["bm"], p["bn"], p["n1"], p["bm2"], p["bn2"]) == (256, 256, 2048, 256, 128)
     r, p = plan(lib, DGRAD, linear(8192, 3072, 768))
@@ -107,7 +109,10 @@ def test_tiles_that_exist_for_some_contractions_only(lib):
         r, p = plan(lib, FWD, linear(M, k_in, n_out))
         if p["bn"] == 192:
             assert tiles(M, n_out, 128, 192) <= 256
+        if p["bn"] == 288:
+            assert tiles(M, n_out, 256, 288) <= 256
         r, p = plan(lib, DGRAD, linear(M, k_in, n_out))
+        assert p["bn"] != 288   # the 288-wide tile is built for the forward only
         if p["direct"]:
             assert p["bn"] not in (32, 192)
         if p["bn"] == 192:
@@ -115,6 +120,19 @@ def test_tiles_that_exist_for_some_contractions_only(lib):
     conv_s2 = (64, 64, 56, 56, 128, 3, 3, 28, 28, 2, 2, 1, 1)
     r, p = plan(lib, DGRAD, conv_s2)
     assert r == 0 and p["direct"] == 0 and p["n1"] == 0
+
+
+
+def test_forced_288_tile_only_where_built(lib, monkeypatch):
+    """MEMSAVE_GEMM_TILE=256x288 is honoured by the Linear (1x1) forward only;
+    a convolution forward, an input gradient and a weight gradient plan as if
+    it were not forced."""
+    monkeypatch.setenv("MEMSAVE_GEMM_TILE", "256x288")
+    r, p = plan(lib, FWD, linear(4096, 512, 1000))
+    assert r == 0 and (p["bm"], p["bn"]) == (256, 288)
+    assert plan(lib, FWD, conv(64, 64, 56, 128, 3, 2, 1))[1]["bn"] != 288
+    assert plan(lib, DGRAD, linear(8192, 768, 2304))[1]["bn"] != 288
+    assert plan(lib, WGRAD, linear(8192, 768, 2304))[1]["bn"] != 288
 
 
 def test_weight_gradient_and_refusals(lib):
