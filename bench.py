@@ -369,8 +369,8 @@ def measure(w, steps, warmup, flush, per_layer=True, reps=None):
 
 # ------------------------------------------------------------------ recorded counters
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_encoder_linears_bf16_hbm_counters.md")
-GEMM_SOURCES = ("paper_2404_12406_amd/csrc/kernels/gemm_bf16.hip", "paper_2404_12406_amd/csrc/kernels/common.h",
-                "paper_2404_12406_amd/csrc/kernels/limits.h")
+GEMM_SOURCES = ("paper_2404_12406_amd/csrc/kernels/gemm_bf16.hip", "paper_2404_12406_amd/csrc/kernels/gemm_block_body.inc",
+                "paper_2404_12406_amd/csrc/kernels/common.h", "paper_2404_12406_amd/csrc/kernels/limits.h")
 
 
 def gemm_sources_sha256():

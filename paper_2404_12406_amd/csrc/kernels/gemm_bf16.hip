@@ -316,908 +316,38 @@ struct Cfg {
 
 template <int MODE, int BM, int BN, int WR, int WC, int STAGES, int OCC, bool UNIT, int KG = 1, bool TS = false>
 __global__ __launch_bounds__(WR * WC * KG * 64, OCC) void gemm_kernel(const Args P) {
-    using G = Cfg<MODE, BM, BN, WR, WC, STAGES, KG>;
-    constexpr int NIA = G::NIA, NIB = G::NIB, TM = G::TM, TN = G::TN, NSUB = G::NSUB;
-    constexpr bool DG = MODE == kDgrad || MODE == kDgradN;
-    // LDS-DMA issue form (see dma16): assembly when an operand is read with
-    // transposing LDS reads
-    constexpr bool ASM_DMA = !(G::A_KC && G::B_KC);
-    static_assert(!G::A_SPARE || (UNIT && !TS), "spare A load slots: the unit-geometry loads only");
-    __shared__ __attribute__((aligned(1024))) char smem[G::SMEM_BYTES];
+    __shared__ __attribute__((aligned(1024))) char smem[Cfg<MODE, BM, BN, WR, WC, STAGES, KG>::SMEM_BYTES];
+    const int bx = (int)blockIdx.x, bz = (int)blockIdx.z;
+#include "gemm_block_body.inc"
+}
 
-    const ConvGeom &g = P.g;
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform: LDS bases stay scalar
-    const int wl = wave % (WR * WC), kg = wave / (WR * WC);   // wave within its k-group, k-group
-    const int wm0 = (wl / WC) * G::WM, wn0 = (wl % WC) * G::WN;
+// The same tile body as a device function, for the paired launch below: the
+// LDS comes in from the kernel, which holds one arena for both tiles.
+template <int MODE, int BM, int BN, int WR, int WC, int STAGES, bool UNIT, int KG, bool TS>
+__device__ __forceinline__ void gemm_pair_block(const Args &P, char *smem, const int bx, const int bz) {
+#include "gemm_block_body.inc"
+}
 
-    int M = P.M, Kg = P.K, ntm = P.ntm;
-    // grid z = (stride phase, split): the input gradient runs one GEMM per
-    // phase, and each split reduces over its own range of k
-    // (the in-place input-gradient variant never splits: its largest tile
-    // has no registers to spare)
-    constexpr bool SPLIT = MODE != kDgradN;
-    const int zsplit = SPLIT ? (int)blockIdx.z % P.splits : 0;
-    const int zphase = SPLIT ? (int)blockIdx.z / P.splits : (int)blockIdx.z;
-    Phase f{};
-    if constexpr (DG) {
-        f = make_phase(g, zphase);
-        M = g.N * f.Hp * f.Wp;
-        Kg = f.Rp * f.Sp * g.K;
-        ntm = (M + BM - 1) / BM;
-    }
-    const int N = P.N;
-    int k_begin = 0, k_end = Kg;
-    if (SPLIT && P.splits > 1) {
-        k_begin = min(Kg, zsplit * P.k_split);
-        k_end = min(Kg, k_begin + P.k_split);
-    }
-    int tm, tn;
-    {
-        const int nb = P.ntm * P.ntn;
-        const int lt = xcd_remap(blockIdx.x, nb);
-        const int GM = 8, per = GM * P.ntn;
-        const int gid = lt / per, first = gid * GM;
-        const int gsz = min(P.ntm - first, GM);
-        const int r = lt - gid * per;
-        tm = first + r % gsz;
-        tn = r / gsz;
-    }
-    if (tm >= ntm || tn >= P.ntn) return;   // before any load: nothing in flight
-    const int m0 = tm * BM, n0 = tn * BN;
-    const int nk = k_end > k_begin ? (k_end - k_begin + BK - 1) / BK : 0;
-
-    const __amdgpu_buffer_rsrc_t ra = rsrc(P.a, P.a_bytes);
-    const __amdgpu_buffer_rsrc_t rb = rsrc(P.b, P.b_bytes);
-
-    // ------------------------------------------------ per-lane load state
-    // K-contiguous operand: instruction j of this wave covers tile rows
-    // (wave*NI + j)*8 + lane/8; the lane's 16-byte slot lane%8 holds k chunk
-    // (lane%8) ^ swz_k(row), which is c0 or c0 ^ 1 by the parity of the
-    // instruction's row group.
-    const int kc_row = lane >> 3;
-    const int kc0 = (lane & 7) ^ kc_row;
-    int a_base[NIA], a_y[NIA], a_x[NIA];
-    uint32_t a_mn_off[NIA];
-    bool a_ok[NIA];
-    bool b_ok[NIB];
-    // Unit-geometry A and every k-contiguous B: the rows of a wave's loads
-    // are 8 apart, so their element offsets are one per-lane base plus a
-    // uniform stride per load (a row past the operand is never read: its
-    // load takes the out-of-range offset).  One register instead of one per
-    // load.
-    uint32_t a_u0 = 0, a_urs = 0, b_u0 = 0, b_urs = 0;
-    uint32_t b_mn_off[NIB];
-    int b_r[NIB], b_s[NIB];
-
-    if constexpr (G::A_KC) {
-#pragma unroll
-        for (int j = 0; j < NIA; ++j) {
-            const int row = (wave * NIA + j) * 8 + kc_row;
-            const int m = m0 + row;
-            a_ok[j] = m < M && (!G::A_SPARE || wave * NIA + j < G::A_INS);
-            const int mm = a_ok[j] ? m : 0;
-            if constexpr (UNIT) {
-                a_base[j] = a_y[j] = a_x[j] = 0;
-            } else if constexpr (MODE == kFwd) {
-                const int PQ = g.P * g.Q;
-                const int n = mm / PQ, pq = mm - n * PQ;
-                const int p = pq / g.Q, q = pq - p * g.Q;
-                a_base[j] = n * g.H * g.W * g.C;
-                a_y[j] = p * g.sh - g.ph;
-                a_x[j] = q * g.sw - g.pw;
-            } else {
-                const int HW = f.Hp * f.Wp;
-                const int n = HW > 0 ? mm / HW : 0, ij = mm - n * HW;
-                const int i2 = f.Wp > 0 ? ij / f.Wp : 0, j2 = ij - i2 * f.Wp;
-                a_base[j] = n * g.P * g.Q * g.K;
-                a_y[j] = i2 + f.dh;
-                a_x[j] = j2 + f.dw;
-            }
-        }
-        if constexpr (UNIT) {
-            const uint32_t S = MODE == kFwd ? g.C : g.K;
-            a_u0 = (uint32_t)(m0 + wave * NIA * 8 + kc_row) * S;
-            a_urs = 8u * S;
-        }
-    } else {
-        // WGRAD A = dy^T: k-rows are (n,p,q), slots run along m (the K channels)
-        constexpr int SPR = BM / 8, KPI = 64 / SPR;
-#pragma unroll
-        for (int j = 0; j < NIA; ++j) {
-            const int krow = (wave * NIA + j) * KPI + lane / SPR;
-            const int slot = (lane % SPR) ^ swz_m<SPR>(krow);
-            const int m = m0 + slot * 8;
-            a_ok[j] = m < M;
-            a_mn_off[j] = m;
-        }
-    }
-    if constexpr (G::B_KC) {
-#pragma unroll
-        for (int j = 0; j < NIB; ++j) {
-            const int row = (wave * NIB + j) * 8 + kc_row;
-            const int n = n0 + row;
-            b_ok[j] = n < N;
-        }
-        // FWD: W[n][(r,s,c)] (row length R*S*C); DGRAD: Wt[c][(r,s,k)] (R*S*K)
-        const uint32_t L = MODE == kFwd ? Kg : g.R * g.S * g.K;
-        b_u0 = (uint32_t)(n0 + wave * NIB * 8 + kc_row) * L;
-        b_urs = 8u * L;
-    } else {
-        constexpr int SPR = BN / 8, KPI = 64 / SPR;
-#pragma unroll
-        for (int j = 0; j < NIB; ++j) {
-            const int krow = (wave * NIB + j) * KPI + lane / SPR;
-            const int slot = (lane % SPR) ^ swz_m<SPR>(krow);
-            const int nn = n0 + slot * 8;
-            b_ok[j] = nn < N;
-            if constexpr (MODE == kWgrad && !UNIT) {
-                const int nv = b_ok[j] ? nn : 0;
-                const int rs = nv / g.C, c = nv - rs * g.C;
-                b_r[j] = rs / g.S;
-                b_s[j] = rs - b_r[j] * g.S;
-                b_mn_off[j] = c;
-            } else {
-                b_r[j] = b_s[j] = 0;
-                b_mn_off[j] = nn;
-            }
-        }
-    }
-
-    // Tap steps (TS, checked by the host): the convolution forward with C a
-    // multiple of BK, or the input gradient through the transposed filter
-    // with K a multiple of BK, with at most 32 taps (of the stride phase).
-    // A BK-deep step is then the channels c0 .. c0 + 63 of one tap t = (r, s),
-    // the same for every lane.  Each A load's pixel offset (with its chunk)
-    // and whether its pixel lies inside the image at tap t (bit t) are worked
-    // out once, as is each B load's row offset, so a step costs a bit test,
-    // an add and a select per load instead of dividing every lane's k.  The
-    // forward's pixel at tap (r, s) is (y + r, x + s) in the H x W input;
-    // the input gradient's is (y - r, x - s) in the P x Q output gradient.
-    constexpr bool TAPSTEP = TS && !UNIT && G::A_KC && G::B_KC && (MODE == kFwd || MODE == kDgrad);
-    constexpr int TSIGN = MODE == kFwd ? 1 : -1;
-    int ts_ch = 1, ts_gh = 1, ts_gw = 1, ts_nr = 1, ts_ns = 1;   // channels, pixel grid, taps
-    uint32_t a_pixb[TAPSTEP ? NIA : 1], a_tmask[TAPSTEP ? NIA : 1], b_rowb[TAPSTEP ? NIB : 1];
-    if constexpr (TAPSTEP) {
-        if constexpr (MODE == kFwd) {
-            ts_ch = g.C; ts_gh = g.H; ts_gw = g.W; ts_nr = g.R; ts_ns = g.S;
-        } else {
-            // (an empty phase, Sp = 0, has no steps: its cursor is never read)
-            ts_ch = g.K; ts_gh = g.P; ts_gw = g.Q; ts_nr = f.Rp; ts_ns = f.Sp > 0 ? f.Sp : 1;
-        }
-#pragma unroll
-        for (int j = 0; j < NIA; ++j) {
-            const int v = (wave * NIA + j) & 1;
-            // element offset of the pixel at tap (0, 0), which may lie in the
-            // padding, where only taps inside the image read from it
-            a_pixb[j] = (uint32_t)(a_base[j] + (a_y[j] * ts_gw + a_x[j]) * ts_ch + (kc0 ^ v) * 8) * 2u;
-            uint32_t m = 0;
-            if (a_ok[j]) {
-                for (int t = 0, r = 0, sx = 0; t < ts_nr * ts_ns; ++t) {
-                    if ((unsigned)(a_y[j] + TSIGN * r) < (unsigned)ts_gh && (unsigned)(a_x[j] + TSIGN * sx) < (unsigned)ts_gw)
-                        m |= 1u << t;
-                    if (++sx == ts_ns) {
-                        sx = 0;
-                        ++r;
-                    }
-                }
-            }
-            a_tmask[j] = m;
-        }
-#pragma unroll
-        for (int j = 0; j < NIB; ++j) {
-            const int v = (wave * NIB + j) & 1;
-            b_rowb[j] = (b_u0 + (uint32_t)j * b_urs + (uint32_t)((kc0 ^ v) * 8)) * 2u;
-        }
-    }
-    // Tap cursor of the last step issued (uniform).  The steps are issued in
-    // order, each BK past the one before (the prologue's STAGES steps from
-    // k_begin, then one refill per step), so the cursor advances by a
-    // channel block, or to the next tap, without dividing.
-    int ts_k0 = k_begin, ts_t = 0, ts_r = 0, ts_s = 0, ts_c0 = 0;
-    if constexpr (TAPSTEP) {
-        ts_t = k_begin / ts_ch;
-        ts_c0 = k_begin - ts_t * ts_ch;
-        ts_r = ts_t / ts_ns;
-        ts_s = ts_t - ts_r * ts_ns;
-    }
-    // byte offsets of the cursor's step: into A (relative to the pixel at
-    // tap (0, 0)) and into B's rows
-    uint32_t ts_aoff = 0, ts_boff = 0;
-    auto ts_offsets = [&]() {
-        ts_aoff = (uint32_t)(TSIGN * (ts_r * ts_gw + ts_s) * ts_ch + ts_c0) * 2u;
-        if constexpr (MODE == kFwd) ts_boff = (uint32_t)((ts_r * g.S + ts_s) * g.C + ts_c0) * 2u;
-        else ts_boff = (uint32_t)(((f.fh + ts_r * g.sh) * g.S + f.fw + ts_s * g.sw) * g.K + ts_c0) * 2u;
-    };
-    if constexpr (TAPSTEP) ts_offsets();
-
-    // Weight gradient by pixel steps (TS, checked by the host): a BK-deep
-    // step is 64 consecutive output pixels, and each lane's k-rows (the same
-    // offsets within every step) move by the same 64 pixels = (dn, dp, dq) in
-    // (image, row, column) from step to step, with at most one carry from q
-    // into p and from p into n.  Each B load keeps its pixel's input row and
-    // column at tap (0, 0) and its element offset, advanced without dividing;
-    // A's rows (dy^T, k-rows = pixels) move by 64 K-element rows.
-    constexpr bool WSTEP = TS && !UNIT && MODE == kWgrad;
-    int w_ih0[WSTEP ? NIB : 1], w_iw0[WSTEP ? NIB : 1], w_pix[WSTEP ? NIB : 1], w_tap[WSTEP ? NIB : 1];
-    uint32_t w_arow[WSTEP ? NIA : 1];
-    int w_k0 = k_begin;
-    // k-row of load j within a step (recomputed where needed: registers are short)
-    constexpr int W_SPRA = BM / 8, W_KPIA = 64 / W_SPRA, W_SPRB = BN / 8, W_KPIB = 64 / W_SPRB;
-    auto w_kra = [&](int j) { return (wave * NIA + j) * W_KPIA + lane / W_SPRA; };
-    auto w_krb = [&](int j) { return (wave * NIB + j) * W_KPIB + lane / W_SPRB; };
-    if constexpr (WSTEP) {
-#pragma unroll
-        for (int j = 0; j < NIA; ++j) w_arow[j] = ((uint32_t)w_kra(j) * (uint32_t)g.K + a_mn_off[j]) * 2u;
-        const int PQ = g.P * g.Q;
-#pragma unroll
-        for (int j = 0; j < NIB; ++j) {
-            const int kk = k_begin + w_krb(j);
-            const int n = kk / PQ, pq = kk - n * PQ;
-            const int p = pq / g.Q, q = pq - p * g.Q;
-            w_ih0[j] = p * g.sh - g.ph;
-            w_iw0[j] = q * g.sw - g.pw;
-            w_pix[j] = ((n * g.H + w_ih0[j]) * g.W + w_iw0[j]) * g.C;
-            w_tap[j] = (b_r[j] * g.W + b_s[j]) * g.C + (int)b_mn_off[j];
-        }
-    }
-    // 64 pixels = (dn, dp, dq), and the element offsets of each move (uniform)
-    int w_dq = 0, w_dp = 0, w_dn = 0;
-    if constexpr (WSTEP) {
-        const int PQ = g.P * g.Q, rem = BK % PQ;
-        w_dn = BK / PQ;
-        w_dp = rem / g.Q;
-        w_dq = rem - w_dp * g.Q;
-    }
-    auto w_advance = [&]() {
-        const int qend = g.Q * g.sw - g.pw, pend = g.P * g.sh - g.ph;
-#pragma unroll
-        for (int j = 0; j < NIB; ++j) {
-            int iw = w_iw0[j] + w_dq * g.sw, ih = w_ih0[j] + w_dp * g.sh, pix = w_pix[j];
-            pix += (w_dq * g.sw + w_dp * g.sh * g.W) * g.C;
-            if (iw >= qend) {   // carry into the row
-                iw -= g.Q * g.sw;
-                ih += g.sh;
-                pix += (g.sh * g.W - g.Q * g.sw) * g.C;
-            }
-            if (ih >= pend) {   // carry into the image
-                ih -= g.P * g.sh;
-                pix += (g.H - g.P * g.sh) * g.W * g.C;
-            }
-            w_iw0[j] = iw;
-            w_ih0[j] = ih;
-            w_pix[j] = pix + w_dn * g.H * g.W * g.C;
-        }
-    };
-
-    // ------------------------------------------------ issue the loads of one tile
-    // Loads j of A are instructions j, loads j of B are NIA + j; issue_range
-    // issues those in [lo, hi).
-    auto issue_range = [&](int stage, int k0, int lo, int hi) {
-        char *sA = smem + stage * G::STAGE_BYTES;
-        char *sB = sA + G::A_BYTES;
-        if constexpr (TAPSTEP) {
-            if (k0 != ts_k0) {   // the next step
-                ts_k0 = k0;
-                ts_c0 += BK;
-                if (ts_c0 == ts_ch) {
-                    ts_c0 = 0;
-                    ++ts_t;
-                    if (++ts_s == ts_ns) {
-                        ts_s = 0;
-                        ++ts_r;
-                    }
-                }
-                ts_offsets();
-            }
-            // steps past the end of the reduction (refills nobody reads) load zeros
-            const bool live = k0 < k_end;
-#pragma unroll
-            for (int j = 0; j < NIA; ++j) {
-                const bool ok = live && ((a_tmask[j] >> (ts_t & 31)) & 1u);
-                const uint32_t boff = ok ? a_pixb[j] + ts_aoff : kOOB;
-                if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
-            }
-#pragma unroll
-            for (int j = 0; j < NIB; ++j) {
-                const bool ok = live && b_ok[j];
-                const uint32_t boff = ok ? b_rowb[j] + ts_boff : kOOB;
-                if (NIA + j >= lo && NIA + j < hi) dma16<ASM_DMA>(rb, sB + (wave * NIB + j) * 1024, boff);
-            }
-            return;
-        }
-        if constexpr (WSTEP) {
-            if (k0 != w_k0) {   // the next step
-                w_k0 = k0;
-                w_advance();
-            }
-            const int left = k_end - k0;   // k-rows of this step inside the reduction
-            const uint32_t sa = (uint32_t)k0 * (uint32_t)g.K * 2u;
-#pragma unroll
-            for (int j = 0; j < NIA; ++j) {
-                const bool ok = a_ok[j] && w_kra(j) < left;
-                const uint32_t boff = ok ? w_arow[j] + sa : kOOB;
-                if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
-            }
-#pragma unroll
-            for (int j = 0; j < NIB; ++j) {
-                const bool ok = b_ok[j] && w_krb(j) < left && (unsigned)(w_ih0[j] + b_r[j]) < (unsigned)g.H &&
-                                (unsigned)(w_iw0[j] + b_s[j]) < (unsigned)g.W;
-                const uint32_t boff = ok ? (uint32_t)(w_pix[j] + w_tap[j]) * 2u : kOOB;
-                if (NIA + j >= lo && NIA + j < hi) dma16<ASM_DMA>(rb, sB + (wave * NIB + j) * 1024, boff);
-            }
-            return;
-        }
-        // ---- A
-        if constexpr (G::A_KC) {
-            // the two chunk variants of this lane: (tap, channel offset) of each
-            int dr[2] = {0, 0}, ds[2] = {0, 0}, off_k[2];
-            bool kin[2];
-#pragma unroll
-            for (int v = 0; v < 2; ++v) {
-                const int kk = k0 + (kc0 ^ v) * 8;
-                kin[v] = kk < k_end;
-                off_k[v] = kk;
-                if constexpr (!UNIT) {
-                    if constexpr (MODE == kFwd) {
-                        const int rs = kk / g.C;
-                        off_k[v] = kk - rs * g.C;
-                        dr[v] = rs / g.S;
-                        ds[v] = rs - dr[v] * g.S;
-                    } else {
-                        const int t = kk / g.K;
-                        off_k[v] = kk - t * g.K;
-                        const int tr = f.Sp > 0 ? t / f.Sp : 0;
-                        dr[v] = -tr;
-                        ds[v] = -(t - tr * f.Sp);
-                    }
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < NIA; ++j) {
-                const int v = (wave * NIA + j) & 1;
-                bool ok = kin[v] && a_ok[j];
-                uint32_t off;
-                if constexpr (UNIT) {
-                    off = a_u0 + (uint32_t)j * a_urs + (uint32_t)off_k[v];
-                } else if constexpr (MODE == kFwd) {
-                    const int ih = a_y[j] + dr[v], iw = a_x[j] + ds[v];
-                    ok = ok && (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
-                    off = (uint32_t)(a_base[j] + (ih * g.W + iw) * g.C + off_k[v]);
-                } else {
-                    const int p = a_y[j] + dr[v], q = a_x[j] + ds[v];
-                    ok = ok && (unsigned)p < (unsigned)g.P && (unsigned)q < (unsigned)g.Q;
-                    off = (uint32_t)(a_base[j] + (p * g.Q + q) * g.K + off_k[v]);
-                }
-                const uint32_t boff = ok ? off * 2u : kOOB;
-                // a spare slot (its a_ok is false, so it loads zeros) writes the dummy area
-                char *dst = (!G::A_SPARE || wave * NIA + j < G::A_INS) ? sA + (wave * NIA + j) * 1024
-                                                                       : smem + G::DUMMY_OFF;
-                if (j >= lo && j < hi) dma16<ASM_DMA>(ra, dst, boff);
-            }
-        } else {
-            constexpr int SPR = BM / 8, KPI = 64 / SPR;
-#pragma unroll
-            for (int j = 0; j < NIA; ++j) {
-                const int kk = k0 + (wave * NIA + j) * KPI + lane / SPR;
-                const bool ok = a_ok[j] && kk < k_end;
-                const uint32_t boff = ok ? ((uint32_t)kk * (uint32_t)g.K + a_mn_off[j]) * 2u : kOOB;
-                if (j >= lo && j < hi) dma16<ASM_DMA>(ra, sA + (wave * NIA + j) * 1024, boff);
-            }
-        }
-        // ---- B
-        if constexpr (G::B_KC) {
-            int off_k[2];
-            bool kin[2];
-#pragma unroll
-            for (int v = 0; v < 2; ++v) {
-                const int kk = k0 + (kc0 ^ v) * 8;
-                kin[v] = kk < k_end;
-                off_k[v] = kk;
-                if constexpr (MODE == kDgrad && !UNIT) {
-                    // kk = (t_r, t_s, k) of this phase -> tap (r, s) of Wt[c][r][s][k]
-                    const int t = kk / g.K, k = kk - t * g.K;
-                    const int tr = f.Sp > 0 ? t / f.Sp : 0, ts = t - tr * f.Sp;
-                    off_k[v] = ((f.fh + tr * g.sh) * g.S + f.fw + ts * g.sw) * g.K + k;
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < NIB; ++j) {
-                const int v = (wave * NIB + j) & 1;
-                const bool ok = kin[v] && b_ok[j];
-                const uint32_t boff = ok ? (b_u0 + (uint32_t)j * b_urs + (uint32_t)off_k[v]) * 2u : kOOB;
-                if (NIA + j >= lo && NIA + j < hi) dma16<ASM_DMA>(rb, sB + (wave * NIB + j) * 1024, boff);
-            }
-        } else {
-            constexpr int SPR = BN / 8, KPI = 64 / SPR;
-#pragma unroll
-            for (int j = 0; j < NIB; ++j) {
-                const int kk = k0 + (wave * NIB + j) * KPI + lane / SPR;
-                bool ok = b_ok[j] && kk < k_end;
-                uint32_t off = 0;
-                if constexpr (MODE == kDgradN) {
-                    // W in place: k-row kk = (t_r, t_s, k) of this phase, slots along c
-                    if constexpr (UNIT) {
-                        off = (uint32_t)kk * (uint32_t)g.C + b_mn_off[j];
-                    } else {
-                        const int t = kk / g.K, k = kk - t * g.K;
-                        const int tr = f.Sp > 0 ? t / f.Sp : 0, ts = t - tr * f.Sp;
-                        off = (uint32_t)(((k * g.R + f.fh + tr * g.sh) * g.S + f.fw + ts * g.sw) * g.C) + b_mn_off[j];
-                    }
-                } else if constexpr (UNIT) {
-                    // WGRAD: x im2col, k-row = (n,p,q), slot along (r,s,c)
-                    off = (uint32_t)kk * (uint32_t)g.C + b_mn_off[j];
-                } else {
-                    const int PQ = g.P * g.Q;
-                    const int n = kk / PQ, pq = kk - n * PQ;
-                    const int p = pq / g.Q, q = pq - p * g.Q;
-                    const int ih = p * g.sh - g.ph + b_r[j], iw = q * g.sw - g.pw + b_s[j];
-                    ok = ok && (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
-                    off = (uint32_t)(((n * g.H + ih) * g.W + iw) * g.C) + b_mn_off[j];
-                }
-                const uint32_t boff = ok ? off * 2u : kOOB;
-                if (NIA + j >= lo && NIA + j < hi) dma16<ASM_DMA>(rb, sB + (wave * NIB + j) * 1024, boff);
-            }
-        }
-    };
-    auto issue = [&](int stage, int k0) { issue_range(stage, k0, 0, NIA + NIB); };
-
-    const int fr = lane & 31, fh = lane >> 5;   // row within a 32-row tile, k half
-    floatx16 acc[TM][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-
-    // fused bias gradient (WGRAD): row sums of dy^T gathered from A fragments
-    const bool db_on = MODE == kWgrad && P.dbpart != nullptr && tn == 0 && wn0 == 0;
-    float dbacc[TM];
-#pragma unroll
-    for (int i = 0; i < TM; ++i) dbacc[i] = 0.f;
-
-    // fragments of one 16-k slice of the tile in `stage`
-    auto read_sub = [&](int stage, int sub, bf16x8 *af, bf16x8 *bfr) {
-        const char *sA = smem + stage * G::STAGE_BYTES;
-        const char *sB = sA + G::A_BYTES;
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-            if constexpr (G::A_KC) af[i] = frag_kc(sA, wm0 + i * 32 + fr, sub, lane);
-            else af[i] = frag_mn<BM>(sA, wm0 + i * 32, sub, lane);
-        }
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            if constexpr (G::B_KC) bfr[j] = frag_kc(sB, wn0 + j * 32 + fr, sub, lane);
-            else bfr[j] = frag_mn<BN>(sB, wn0 + j * 32, sub, lane);
-        }
-    };
-    auto mfma_sub = [&](const bf16x8 *ca, const bf16x8 *cb) {
-        if (db_on) {
-#pragma unroll
-            for (int i = 0; i < TM; ++i) {
-                float sum = 0.f;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) sum += (float)ca[i][e];
-                dbacc[i] += sum;
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cb[j], ca[i], acc[i][j], 0, 0, 0);
-    };
-    constexpr int NVMEM = NIA + NIB;
-    constexpr int NMF = TM * TN;
-    constexpr int NDS = (G::A_KC ? 1 : 2) * TM + (G::B_KC ? 1 : 2) * TN;
-    // every MFMA is followed by its share of the DMA issues and LDS reads
-    auto interleave = [&](int nvmem) {
-#pragma unroll
-        for (int m = 0; m < NMF; ++m) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            constexpr int VPM = (NVMEM + NMF - 1) / NMF;
-            if (m * VPM < nvmem) __builtin_amdgcn_sched_group_barrier(0x020, VPM, 0);
-            constexpr int DPM = (NDS + NMF - 1) / NMF;
-            if (m * DPM < NDS) __builtin_amdgcn_sched_group_barrier(0x100, DPM, 0);
-        }
-    };
-
-    // ------------------------------------------------ main loop
-    // Stage s = kt % STAGES holds tile kt.  On entry to step kt the fragments
-    // of its first slice are in (fa0, fb0).  Each slice reads the next
-    // slice's fragments while its MFMAs run; the last slice first makes sure
-    // every wave has read tile kt (own LDS reads done, barrier) and tile kt+1
-    // has landed (own DMA done, same barrier), then reads tile kt+1's first
-    // slice.  The stage tile kt came from is refilled with tile kt + STAGES:
-    //  * with two stages, right after that barrier (the only window);
-    //  * with three or more, spread over the slices of the next step, so the
-    //    load instructions do not arrive at the texture unit in one burst.
-    // Refills past the end of the reduction take the out-of-range path and
-    // write zeros into a stage that only feeds MFMAs nobody keeps.
-    constexpr bool SPREAD = STAGES >= 3;
-    bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN], fa2[TM], fb2[TN];
-    // three or more stages: refills spread over the next step's slices
-    auto step_spread = [&](int kt) {
-        const int s = kt % STAGES;
-        // refill of the stage step kt-1 consumed
-        const int rs = (kt + STAGES - 1) % STAGES;
-        const int rk = k_begin + (kt - 1 + STAGES) * BK;
-        const bool refill = kt >= 1;
-#pragma unroll
-        for (int sub = 0; sub < NSUB; ++sub) {
-            const bf16x8 *ca = (sub & 1) ? fa1 : fa0;
-            const bf16x8 *cb = (sub & 1) ? fb1 : fb0;
-            bf16x8 *na = (sub & 1) ? fa0 : fa1;
-            bf16x8 *nb = (sub & 1) ? fb0 : fb1;
-            constexpr int PER = (NVMEM + NSUB - 1) / NSUB;
-            const int lo = sub * PER, hi = min(NVMEM, lo + PER);
-            __builtin_amdgcn_sched_barrier(0);
-            if (refill) issue_range(rs, rk, lo, hi);
-            if (sub + 1 < NSUB) {
-                read_sub(s, sub + 1, na, nb);
-                mfma_sub(ca, cb);
-                interleave(hi - lo);
-            } else {
-                wait_vmcnt<(STAGES - 2) * NVMEM>();
-                wait_lgkm0();
-                block_sync<ASM_DMA>();
-                __builtin_amdgcn_sched_barrier(0);
-                read_sub((kt + 1) % STAGES, 0, na, nb);
-                mfma_sub(ca, cb);
-                interleave(0);
-            }
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    };
-    // two stages: fragments are read two slices ahead (three buffers), so a
-    // wave's last read of tile kt is issued in slice 1 and the barrier can
-    // come at the start of slice 2; the refill of tile kt's stage with tile
-    // kt+2 is then spread over slices 2 and 3.  On entry (fa0, fb0) and
-    // (fa1, fb1) hold slices 0 and 1 of tile kt; on exit, of tile kt+1.
-    auto step_two = [&](int kt) {
-        const int s = kt % STAGES, s1 = (kt + 1) % STAGES;
-        const int rk = k_begin + (kt + STAGES) * BK;
-        constexpr int HALF = (NVMEM + 1) / 2;
-        __builtin_amdgcn_sched_barrier(0);
-        read_sub(s, 2, fa2, fb2);            // slice 0: read slice 2
-        mfma_sub(fa0, fb0);
-        interleave(0);
-        __builtin_amdgcn_sched_barrier(0);
-        read_sub(s, 3, fa0, fb0);            // slice 1: read slice 3
-        mfma_sub(fa1, fb1);
-        interleave(0);
-        __builtin_amdgcn_sched_barrier(0);
-        wait_vmcnt<0>();                     // slice 2: tile kt+1 landed, tile kt read by all
-        wait_lgkm0();
-        block_sync<ASM_DMA>();
-        __builtin_amdgcn_sched_barrier(0);
-        issue_range(s, rk, 0, HALF);
-        read_sub(s1, 0, fa1, fb1);
-        mfma_sub(fa2, fb2);
-        interleave(HALF);
-        __builtin_amdgcn_sched_barrier(0);
-        issue_range(s, rk, HALF, NVMEM);     // slice 3
-        read_sub(s1, 1, fa2, fb2);
-        mfma_sub(fa0, fb0);
-        interleave(NVMEM - HALF);
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-            fa0[i] = fa1[i];
-            fa1[i] = fa2[i];
-        }
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            fb0[j] = fb1[j];
-            fb1[j] = fb2[j];
-        }
-    };
-    // two stages with two fragment buffers (the 12-wave tile, whose three
-    // waves per SIMD leave no registers for a third): fragments are read one
-    // slice ahead, so a wave's last read of tile kt is issued in slice 2 and
-    // the barrier comes at the start of slice 3; the whole refill of tile
-    // kt's stage with tile kt+2 is issued right after it.  The loads still
-    // have a full step to land (until slice 3 of step kt+1), and the other
-    // two waves of the SIMD cover the barrier.  On entry fa0 / fb0 hold
-    // slice 0 of tile kt; on exit, of tile kt+1.
-    auto step_two_lean = [&](int kt) {
-        const int s = kt % STAGES, s1 = (kt + 1) % STAGES;
-        const int rk = k_begin + (kt + STAGES) * BK;
-        __builtin_amdgcn_sched_barrier(0);
-        read_sub(s, 1, fa1, fb1);            // slice 0: read slice 1
-        mfma_sub(fa0, fb0);
-        interleave(0);
-        __builtin_amdgcn_sched_barrier(0);
-        read_sub(s, 2, fa0, fb0);            // slice 1: read slice 2
-        mfma_sub(fa1, fb1);
-        interleave(0);
-        __builtin_amdgcn_sched_barrier(0);
-        read_sub(s, 3, fa1, fb1);            // slice 2: read slice 3
-        mfma_sub(fa0, fb0);
-        interleave(0);
-        __builtin_amdgcn_sched_barrier(0);
-        wait_vmcnt<0>();                     // slice 3: tile kt+1 landed, tile kt read by all
-        wait_lgkm0();
-        block_sync<ASM_DMA>();
-        __builtin_amdgcn_sched_barrier(0);
-        issue_range(s, rk, 0, NVMEM);
-        read_sub(s1, 0, fa0, fb0);
-        mfma_sub(fa1, fb1);
-        interleave(NVMEM);
-        __builtin_amdgcn_sched_barrier(0);
-    };
-    constexpr bool LEAN = STAGES == 2 && G::NW > 8;
-    static_assert(NSUB % 2 == 0, "an even number of slices keeps the fragment buffers' roles fixed");
-    // two k-groups (three or more stages): group kg does slices 2kg and
-    // 2kg+1 of each step.  On entry (fa0, fb0) hold slice 2kg of tile kt.
-    // The refill of the stage step kt-1 consumed is split over the two
-    // halves; the wait before the barrier leaves the loads of tiles kt+2 ..
-    // kt+STAGES-1 in flight, so tile kt+1 has landed.
-    auto step_kg = [&](int kt) {
-        const int s = kt % STAGES;
-        const int rs = (kt + STAGES - 1) % STAGES;
-        const int rk = k_begin + (kt - 1 + STAGES) * BK;
-        const bool refill = kt >= 1;
-        constexpr int HALF = (NVMEM + 1) / 2;
-        __builtin_amdgcn_sched_barrier(0);
-        if (refill) issue_range(rs, rk, 0, HALF);
-        read_sub(s, 2 * kg + 1, fa1, fb1);
-        mfma_sub(fa0, fb0);
-        interleave(HALF);
-        __builtin_amdgcn_sched_barrier(0);
-        if (refill) issue_range(rs, rk, HALF, NVMEM);
-        wait_vmcnt<(STAGES - 2) * NVMEM>();
-        wait_lgkm0();
-        block_sync<ASM_DMA>();
-        __builtin_amdgcn_sched_barrier(0);
-        read_sub((kt + 1) % STAGES, 2 * kg, fa0, fb0);
-        mfma_sub(fa1, fb1);
-        interleave(NVMEM - HALF);
-        __builtin_amdgcn_sched_barrier(0);
-    };
-
-    // Forward bias into LDS before the operand loads (so it is the oldest load
-    // of wave 0 and lands with stage 0).  Every block would otherwise read
-    // the same few bias lines in its epilogue, all at once.  Whole 16-byte
-    // chunks only: columns past N read as zeros.
-    bool bias_lds = false;
-    if constexpr (MODE == kFwd) {
-        bias_lds = P.bias != nullptr && P.N % 8 == 0;
-        if (bias_lds && wave == 0) {
-            const uint32_t off = (uint32_t)(n0 + lane * 8) * 2;
-            dma16<ASM_DMA>(rsrc(P.bias, (uint32_t)P.N * 2), smem + G::BIAS_OFF, off);
-        }
-    }
-#pragma unroll
-    for (int s2 = 0; s2 < STAGES; ++s2) issue(s2, k_begin + s2 * BK);
-    wait_vmcnt<(STAGES - 1) * NVMEM>();
-    block_sync<ASM_DMA>();
-    read_sub(0, KG == 2 ? 2 * kg : 0, fa0, fb0);
-    if constexpr (KG == 2) {
-        for (int kt = 0; kt < nk; ++kt) step_kg(kt);
-    } else if constexpr (SPREAD) {
-        for (int kt = 0; kt < nk; ++kt) step_spread(kt);
-    } else if constexpr (LEAN) {
-        static_assert(NSUB == 4, "the two-stage schedule is written for four slices per step");
-        for (int kt = 0; kt < nk; ++kt) step_two_lean(kt);
-    } else {
-        static_assert(NSUB == 4, "the two-stage schedule is written for four slices per step");
-        read_sub(0, 1, fa1, fb1);
-        for (int kt = 0; kt < nk; ++kt) step_two(kt);
-    }
-    // the refills of the last steps are still writing into LDS: drain them
-    // before LDS is reused or the workgroup ends
-    wait_vmcnt<0>();
-
-    // ------------------------------------------------ k-groups: add group 1's accumulators to group 0's
-    if constexpr (KG == 2) {
-        float *red = reinterpret_cast<float *>(smem);
-        // group 1 also sums dy's columns; its first loads go out now, so they
-        // land during the exchange below
-        DyColumnSums<16> cs(ra, M, Kg, m0, BM, tn, P.cs_cw, wl, WR * WC, lane);
-        if constexpr (DG && UNIT) {
-            if (kg == 1 && P.cspart && cs.on) cs.issue(0, cs.rg);
-        }
-        __syncthreads();   // every wave is done with the operand stages
-        if (kg == 1) {
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-#pragma unroll
-                    for (int v = 0; v < 16; ++v) red[(((wl * TM + i) * TN + j) * 16 + v) * 64 + lane] = acc[i][j][v];
-        }
-        __syncthreads();
-        if (kg == 0) {
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-#pragma unroll
-                    for (int v = 0; v < 16; ++v) acc[i][j][v] += red[(((wl * TM + i) * TN + j) * 16 + v) * 64 + lane];
-        }
-        __syncthreads();   // the partials are read before the epilogue reuses LDS
-        if (kg == 1) {
-            // group 1 sums dy's columns while group 0 writes the output tile
-            if constexpr (DG && UNIT) {
-                if (P.cspart) cs.run(true, wl, WR * WC, tm, lane, P.cspart);
-            }
-            return;
-        }
-    }
-
-    // ------------------------------------------------ fused bias-gradient partials
-    if (db_on) {
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-            float v = dbacc[i];
-            v += __shfl_xor(v, 32);
-            const int m = m0 + wm0 + i * 32 + fr;
-            if (fh == 0 && m < M) P.dbpart[(size_t)zsplit * M + m] = v;
-        }
-    }
-
-    // ------------------------------------------------ epilogue
-    // lane holds, for MFMA tile (i, j) and register group q = 0..3,
-    // D[m = wm0 + 32i + lane%32][n = wn0 + 32j + 8q + 4*(lane/32) + 0..3]
-    // split-K: fp32 partials of this split (no bias; the reduce adds it).
-    // Rows of the input gradient go to their dx pixel, so the phases of a
-    // strided layer fill disjoint rows of one [N*H*W][C] array per split.
-    if (SPLIT && P.splits > 1) {
-        float *W = P.part + (size_t)zsplit * (size_t)P.part_stride;
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-            const int m = m0 + wm0 + i * 32 + fr;
-            if (m >= M) continue;
-            size_t row = (size_t)m;
-            if constexpr (DG && !UNIT) {
-                const int HW = f.Hp * f.Wp;
-                const int nimg = m / HW, ij = m - nimg * HW;
-                const int i2 = ij / f.Wp, j2 = ij - i2 * f.Wp;
-                row = (size_t)(nimg * g.H + f.h0 + i2 * g.sh) * g.W + f.w0 + j2 * g.sw;
-            }
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int n = n0 + wn0 + j * 32 + 8 * q + 4 * fh;
-                    const floatx4 o = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
-                                       acc[i][j][4 * q + 3]};
-                    if (n + 3 < N && (N & 3) == 0) {
-                        *reinterpret_cast<floatx4 *>(W + row * N + n) = o;
-                    } else {
-#pragma unroll
-                        for (int v = 0; v < 4; ++v)
-                            if (n + v < N) W[row * N + n + v] = o[v];
-                    }
-                }
-        }
-        return;
-    }
-    // KG == 1: the column sums' first loads are issued here, so they land
-    // while the output tile is written
-    DyColumnSums<8> cs(ra, M, Kg, m0, BM, tn, P.cs_cw, wave, G::NW, lane);
-    if constexpr (DG && UNIT && KG == 1) {
-        if (P.cspart && cs.on) cs.issue(0, cs.rg);
-    }
-    if constexpr (KG == 1) __syncthreads();   // every wave is done with the operand stages
-    bf16 *stage = reinterpret_cast<bf16 *>(smem) + wave * G::EPI_ROWS * G::EPI_PITCH;
-    constexpr int SEG = G::WN / 8;                   // 16-byte segments per staged row
-    constexpr int ROWS_PER_PASS = 64 / SEG;          // rows a wave stores per pass (lanes past
-                                                     // ROWS_PER_PASS * SEG idle when SEG does not divide 64)
-    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-    // bias: the lane's output columns are the same for every row it holds,
-    // so its bias values are read once and added in fp32 before the single
-    // rounding to bf16 (forward: staged in LDS; input gradient, i.e. the
-    // forward of a transposed convolution: read from global memory)
-    float bcol[TN][4][4];
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) bcol[j][q][v] = 0.f;
-    if constexpr (MODE != kWgrad) {
-        if (bias_lds) {
-            // the bias area is past every stage and the staging rows; its
-            // DMA completed before the barrier above
-            const bf16 *bl = reinterpret_cast<const bf16 *>(smem + G::BIAS_OFF);
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const bf16x4 b4 = *reinterpret_cast<const bf16x4 *>(bl + wn0 + j * 32 + 8 * q + 4 * fh);
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) bcol[j][q][v] = (float)b4[v];
-                }
-        } else if (P.bias && (N & 3) == 0) {
-            // 4 consecutive columns per load through a descriptor of N entries
-            // (a load is wholly in range or past it and reads zeros), every
-            // load in flight at once: element-wise loads behind a range test
-            // each waited for the one before
-            typedef unsigned v2u32 __attribute__((ext_vector_type(2)));
-            const __amdgpu_buffer_rsrc_t rbias = rsrc(P.bias, (uint32_t)N * 2u);
-            v2u32 bv[TN][4];
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    bv[j][q] = __builtin_amdgcn_raw_buffer_load_b64(rbias, (n0 + wn0 + j * 32 + 8 * q + 4 * fh) * 2, 0, 0);
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const uint32_t w = bv[j][q][v >> 1];
-                        bcol[j][q][v] = __uint_as_float((v & 1) ? (w & 0xffff0000u) : (w << 16));
-                    }
-        } else if (P.bias) {
-            // N not a multiple of 4: one column per load, through the same
-            // kind of descriptor, so every load is still issued at once
-            const __amdgpu_buffer_rsrc_t rbias = rsrc(P.bias, (uint32_t)N * 2u);
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int n = n0 + wn0 + j * 32 + 8 * q + 4 * fh;
-#pragma unroll
-                    for (int v = 0; v < 4; ++v)
-                        bcol[j][q][v] = __uint_as_float((uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rbias, (n + v) * 2, 0, 0) << 16);
-                }
-        }
-    }
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                bf16x4 o;
-#pragma unroll
-                for (int v = 0; v < 4; ++v) o[v] = (bf16)(acc[i][j][4 * q + v] + bcol[j][q][v]);
-                *reinterpret_cast<bf16x4 *>(stage + fr * G::EPI_PITCH + j * 32 + 8 * q + 4 * fh) = o;
-            }
-        wait_lgkm0();   // this wave's staged rows are written
-        __builtin_amdgcn_wave_barrier();
-#pragma unroll
-        for (int r0 = 0; r0 < G::EPI_ROWS; r0 += ROWS_PER_PASS) {
-            const int rl = r0 + lane / SEG;
-            const int cl = (lane % SEG) * 8;
-            const int m = m0 + wm0 + i * 32 + rl;
-            const int n = n0 + wn0 + cl;
-            if ((64 % SEG != 0 && lane >= ROWS_PER_PASS * SEG) || rl >= G::EPI_ROWS) continue;
-            Vec16<bf16> v;
-            v.u = *reinterpret_cast<const u32x4 *>(stage + rl * G::EPI_PITCH + cl);
-            if (m >= M || n >= N) continue;
-            bf16 *dst;
-            if constexpr (DG && !UNIT) {
-                const int HW = f.Hp * f.Wp;
-                const int nimg = m / HW, ij = m - nimg * HW;
-                const int i2 = ij / f.Wp, j2 = ij - i2 * f.Wp;
-                const int pix = (nimg * g.H + f.h0 + i2 * g.sh) * g.W + f.w0 + j2 * g.sw;
-                dst = P.c + (size_t)pix * g.C + n;
-            } else {
-                dst = P.c + (size_t)m * (P.ldc > 0 ? P.ldc : N) + n;
-            }
-            if (n + 8 <= N) {
-                *reinterpret_cast<u32x4 *>(dst) = v.u;
-            } else {
-                // constant indices only: a runtime index into v would make the
-                // compiler place v in LDS, addressed through the dispatch
-                // packet (a host-memory read per wave at the end of the kernel)
-#pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    if (n + e < N) dst[e] = v.e[e];
-            }
-        }
-        wait_lgkm0();   // reads done before the next pass overwrites
-        __builtin_amdgcn_wave_barrier();
-    }
-    if constexpr (DG && UNIT && KG == 1) {
-        if (P.cspart) cs.run(true, wave, G::NW, tm, lane, P.cspart);
-    }
+// A column-split unit-geometry contraction in one launch: block b computes
+// tile b of the leading columns (P1, on the 256 x 256 tile), then tile b of
+// the remaining columns (P2, on 256 x 128), with the same number of tiles
+// in both parts (one per CU).  Against two launches, a block starts its
+// second tile as soon as its first is written instead of after the slowest
+// block of the first launch, the kernel-end write-back and the next
+// dispatch.  The XCD-aware tile order gives a block the same rows in both
+// parts, so its A rows are still in its XCD's L2.  Both parts are one
+// k-group tiles: every wave runs both bodies to the end, so the barrier
+// between them (LDS reuse) is met by all.
+template <int MODE>
+__global__ __launch_bounds__(512, 1) void gemm_pair_kernel(const Args P1, const Args P2) {
+    using G1 = Cfg<MODE, 256, 256, 2, 4, 2>;
+    using G2 = Cfg<MODE, 256, 128, 2, 4, 3>;
+    static_assert(G1::NW == 8 && G2::NW == 8, "both parts are 8-wave tiles");
+    constexpr int SM = G1::SMEM_BYTES > G2::SMEM_BYTES ? G1::SMEM_BYTES : G2::SMEM_BYTES;
+    __shared__ __attribute__((aligned(1024))) char smem[SM];
+    gemm_pair_block<MODE, 256, 256, 2, 4, 2, true, 1, false>(P1, smem, (int)blockIdx.x, 0);
+    __syncthreads();   // every wave is done with the first tile's LDS
+    gemm_pair_block<MODE, 256, 128, 2, 4, 3, true, 1, false>(P2, smem, (int)blockIdx.x, 0);
 }
 
 // ---------------------------------------------------------------- halo convolution
@@ -2122,6 +1252,31 @@ int go_tile(const Tile &t, const Args &a, dim3 grid, hipStream_t st) {
 // filter, whose steps each lie in one tap (channels of the reduction a
 // multiple of BK, at most 32 taps per stride phase): the tap-cursor operand
 // loads
+// The two launches of a column split as one (gemm_pair_kernel): only for a
+// one-split unit-geometry plan of 256 x 256 then 256 x 128 tiles with as many
+// tiles in both parts; otherwise kPairNotApplicable and the caller launches
+// the two parts.  MEMSAVE_GEMM_PAIR=off forces the two launches (testing knob).
+constexpr int kPairNotApplicable = -2;
+template <int MODE>
+int go_pair(const Tile &t1, const Args &a1, const Tile &t2, const Args &a2, hipStream_t st) {
+    const char *e = getenv("MEMSAVE_GEMM_PAIR");
+    if (e && strcmp(e, "off") == 0) return kPairNotApplicable;
+    if (!(t1.bm == 256 && t1.bn == 256 && t1.kg == 1 && t2.bm == 256 && t2.bn == 128 && t2.kg == 1 &&
+          t2.stages == 3 && t1.stages == 2))
+        return kPairNotApplicable;
+    if (a1.splits > 1 || a2.splits > 1) return kPairNotApplicable;
+    const int nb = a1.ntm * a1.ntn;
+    if (nb != a2.ntm * a2.ntn || nb <= 0) return kPairNotApplicable;
+    const unsigned pk = MODE == kFwd ? kProfFwd : kProfDgrad;
+    void *eb = nullptr, *ee = nullptr;
+    const bool timed = prof_pair(pk, &eb, &ee);
+    hipExtLaunchKernelGGL(gemm_pair_kernel<MODE>, dim3(nb), dim3(512), 0, st, (hipEvent_t)eb, (hipEvent_t)ee, 0,
+                          a1, a2);
+    const int err = (int)hipGetLastError();
+    if (timed) prof_pair_done(pk, eb, ee, err == 0);
+    return err;
+}
+
 template <int MODE>
 int go_mode(const Tile &t, const Args &a, dim3 grid, bool unit, hipStream_t st, bool ts = false) {
     if (unit) return go_tile<MODE, true>(t, a, grid, st);
@@ -2558,8 +1713,6 @@ int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, 
         a.N = cs.n1;
         a.ldc = g.K;
         a.ntn = (a.N + p.t.bn - 1) / p.t.bn;
-        int err = go_mode<kFwd>(p.t, a, dim3(a.ntm * a.ntn), true, st);
-        if (err) return err;
         a2.b += (size_t)cs.n1 * a2.K;
         a2.c += cs.n1;
         if (a2.bias) a2.bias += cs.n1;
@@ -2569,6 +1722,10 @@ int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, 
         a2.ntm = (a2.M + cs.p2.t.bm - 1) / cs.p2.t.bm;
         a2.ntn = (a2.N + cs.p2.t.bn - 1) / cs.p2.t.bn;
         a2.k_split = cs.p2.k_split;
+        const int pr = go_pair<kFwd>(p.t, a, cs.p2.t, a2, st);
+        if (pr != kPairNotApplicable) return pr;
+        const int err = go_mode<kFwd>(p.t, a, dim3(a.ntm * a.ntn), true, st);
+        if (err) return err;
         return go_mode<kFwd>(cs.p2.t, a2, dim3(a2.ntm * a2.ntn), true, st);
     }
     int err = go_mode<kFwd>(p.t, a, dim3(a.ntm * a.ntn, 1, p.splits), unit_geom(g), st, ts_fwd(g));
@@ -2757,9 +1914,6 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bia
         a.N = tsp.n1;
         a.ldc = g.C;
         a.ntn = (a.N + p.t.bn - 1) / p.t.bn;
-        int err = direct ? go_mode<kDgradN>(p.t, a, dim3(a.ntm * a.ntn), true, st)
-                         : go_mode<kDgrad>(p.t, a, dim3(a.ntm * a.ntn), true, st);
-        if (err) return err;
         a2.b += direct ? (size_t)tsp.n1 : (size_t)tsp.n1 * g.K;
         a2.c += tsp.n1;
         if (a2.bias) a2.bias += tsp.n1;
@@ -2769,6 +1923,11 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bia
         a2.ntm = (a2.M + tsp.p2.t.bm - 1) / tsp.p2.t.bm;
         a2.ntn = (a2.N + tsp.p2.t.bn - 1) / tsp.p2.t.bn;
         a2.k_split = tsp.p2.k_split;
+        const int pr = direct ? go_pair<kDgradN>(p.t, a, tsp.p2.t, a2, st) : go_pair<kDgrad>(p.t, a, tsp.p2.t, a2, st);
+        if (pr != kPairNotApplicable) return pr;
+        const int err = direct ? go_mode<kDgradN>(p.t, a, dim3(a.ntm * a.ntn), true, st)
+                               : go_mode<kDgrad>(p.t, a, dim3(a.ntm * a.ntn), true, st);
+        if (err) return err;
         return direct ? go_mode<kDgradN>(tsp.p2.t, a2, dim3(a2.ntm * a2.ntn), true, st)
                       : go_mode<kDgrad>(tsp.p2.t, a2, dim3(a2.ntm * a2.ntn), true, st);
     }

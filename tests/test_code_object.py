@@ -86,8 +86,8 @@ def descriptors():
 
 def test_every_expected_kernel_family_is_present(descriptors):
     names = " ".join(descriptors)
-    for family in ("gemm_kernel", "transpose_krsc_kernel", "bn_fwd_flat_kernel", "rowcol_reduce_kernel",
-                   "finalize_kernel", "igemm_kernel"):
+    for family in ("gemm_kernel", "gemm_pair_kernel", "halo_conv_kernel", "transpose_krsc_kernel",
+                   "bn_fwd_flat_kernel", "rowcol_reduce_kernel", "finalize_kernel", "igemm_kernel"):
         assert family in names, family
 
 

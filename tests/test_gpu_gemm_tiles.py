@@ -4,6 +4,7 @@ strided input gradient and a fused bias gradient), against the oracle."""
 import os
 
 import numpy as np
+import torch
 import pytest
 
 import oracle
@@ -264,3 +265,34 @@ def test_linear_column_split(shape, dgrad_variant, tail_split):
     gy = synth.normal((M, Nout), seed + 3, dtype="bf16")
     (gx,) = [g for g in ms.layer_backward(rec, dev(gy, "bf16")) if g is not None]
     check("dX", host(gx)[rows], oracle.linear_input_grad(gy[rows], w), "bf16")
+
+
+@pytest.mark.parametrize("variant", ["forward", "transposed", "direct"])
+def test_paired_column_split_matches_two_launches(variant, monkeypatch):
+    """An 8192 x 3072 output is a column split of 256 tiles of 256 x 256 and
+    256 tiles of 256 x 128: one paired launch by default, two launches with
+    MEMSAVE_GEMM_PAIR=off.  Same tiles and reduction order, so the outputs
+    agree byte for byte: the forward (its bias added past the split column),
+    and the input gradient through the transposed copy and reading W in
+    place.  The reductions (136 deep) end inside a 64-deep step."""
+    M, K = 8192, 136
+    Kin, Nout = (K, 3072) if variant == "forward" else (3072, K)
+    seed = 7900 + len(variant)
+    x = synth.normal((M, Kin), seed, dtype="bf16")
+    w = synth.normal((Nout, Kin), seed + 1, 0.05, dtype="bf16")
+    b = synth.normal((Nout,), seed + 2, 1.0, dtype="bf16")
+    gy = synth.normal((M, Nout), seed + 3, dtype="bf16")
+    if variant != "forward":
+        monkeypatch.setenv("MEMSAVE_DGRAD", variant)
+    outs = []
+    for pair in ("on", "off"):
+        monkeypatch.setenv("MEMSAVE_GEMM_PAIR", pair)
+        y, rec = ms.layer_forward(ms.Linear(), dev(x, "bf16"), dev(w, "bf16"), dev(b, "bf16"), 1)
+        (gx,) = [g for g in ms.layer_backward(rec, dev(gy, "bf16")) if g is not None]
+        outs.append(y if variant == "forward" else gx)
+    assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
+    rows = np.array([0, 1, 255, 256, 4097, M - 1])
+    if variant == "forward":
+        check("y", host(outs[0])[rows], oracle.linear_forward(x[rows], w, b), "bf16")
+    else:
+        check("dX", host(outs[0])[rows], oracle.linear_input_grad(gy[rows], w), "bf16")
