@@ -400,9 +400,21 @@ template <int CH> __device__ __forceinline__ int halo_swz(int row) {
     else return (row >> 2) & 1;
 }
 
-template <int NP, int TAPS_MAX, int KG, bool EXACT = false, int CH = 64>
+// ST = 2: a stride-2 forward as the sum of its four stride phases.  Phase
+// (a, b) takes the taps r = a, a + 2, ... and s = b, b + 2, ...; their input
+// pixels (ST y + r - ph, ST x + s - pw) are the phase image
+// (ST (y + r') + a - ph, ST (x + s') + b - pw), r = 2 r' + a, read at
+// stride 2, on which the phase is a stride-1 correlation with r' and s'.
+// A tile is then four work items, one halo each ((TH + R2 - 1) x
+// (TW + S2 - 1) pixels of the phase image, R2 = ceil(R / 2), the same shape
+// for every phase so that the lanes' load offsets are worked out once),
+// whose sums accumulate before the one epilogue; the phases of a tile
+// reread neighbouring pixels of the same lines, mostly from L2.
+template <int NP, int TAPS_MAX, int KG, bool EXACT = false, int CH = 64, int ST = 1>
 __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A) {
     static_assert(CH == 64 || (CH == 16 && KG == 1 && EXACT), "16-channel pixels: one group, exact taps");
+    static_assert(ST == 1 || (ST == 2 && KG == 1 && !EXACT && CH == 64), "stride 2: one group, generic taps");
+    constexpr int NPH = ST * ST;                    // work items (stride phases) per tile
     constexpr int NW = 4 * KG;                      // waves: KG k-groups of four
     constexpr int PB = CH * 2;                      // bytes of a pixel (or filter) row
     constexpr int CPR = CH / 8;                     // 16-byte chunks per row
@@ -422,8 +434,9 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int kg = KG == 2 ? wave >> 2 : 0, wl = wave & 3;   // k-group, wave within it
     const int taps = A.R * A.S;
-    const int HWW = A.TW + A.S - 1;                   // halo row length
-    const int HP = (A.TH + A.R - 1) * HWW;            // halo pixels
+    const int R2 = (A.R + ST - 1) / ST, S2 = (A.S + ST - 1) / ST;   // taps per phase, at most
+    const int HWW = A.TW + S2 - 1;                    // halo row length
+    const int HP = (A.TH + R2 - 1) * HWW;             // halo pixels
     const __amdgpu_buffer_rsrc_t rin = rsrc(A.in, A.in_bytes);
     const __amdgpu_buffer_rsrc_t rf = rsrc(A.filt, A.filt_bytes);
     const __amdgpu_buffer_rsrc_t ro = rsrc(A.out, A.out_bytes);
@@ -489,19 +502,21 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
         const int hy = hp / HWW, hx = hp - hy * HWW;
         h_y[jj] = hp < HP ? hy : -(1 << 20);
         h_x[jj] = hx;
-        h_c[jj] = ((uint32_t)hy * (uint32_t)A.W + (uint32_t)hx) * (uint32_t)CH + (uint32_t)chunk_of(hp) * 8u;
+        h_c[jj] = ((uint32_t)(ST * hy) * (uint32_t)A.W + (uint32_t)(ST * hx)) * (uint32_t)CH +
+                  (uint32_t)chunk_of(hp) * 8u;
     }
-    auto load_halo = [&](int tile, int b) {
+    // the halo of phase `ph2` (= 2a + b) of tile `tile`
+    auto load_halo = [&](int tile, int ph2, int b) {
         char *dst = smem + FILT_BYTES + b * HALO_BYTES;
         const int img = tile / A.tiles_img, rem = tile - img * A.tiles_img;
         const int ty = rem / A.tiles_w, tx = rem - ty * A.tiles_w;
-        const int iy0 = ty * A.TH - A.ph, ix0 = tx * A.TW - A.pw;
+        const int iy0 = ST * ty * A.TH + (ph2 >> 1) - A.ph, ix0 = ST * tx * A.TW + (ph2 & 1) - A.pw;
         const int gbase = ((img * A.H + iy0) * A.W + ix0) * CH;
 #pragma unroll
         for (int jj = 0; jj < HJ; ++jj) {
             const int j = wave + jj * NW;
             if (j >= ninstr) break;
-            const int iy = iy0 + h_y[jj], ix = ix0 + h_x[jj];
+            const int iy = iy0 + ST * h_y[jj], ix = ix0 + ST * h_x[jj];
             const bool ok = (unsigned)iy < (unsigned)A.H && (unsigned)ix < (unsigned)A.W;
             // element index below 2^31 (operand_fits), byte offset below kOOB
             const uint32_t off = ok ? ((uint32_t)gbase + h_c[jj]) * 2u : kOOB;
@@ -546,30 +561,38 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
         tap_r[t] = t / A.S;
         tap_s[t] = t - tap_r[t] * A.S;
     }
-    int tile = blockIdx.x;
-    if (tile < A.tiles) load_halo(tile, 0);
-    for (int it = 0; tile < A.tiles; ++it, tile += gridDim.x) {
+    // work item `it` of this block: phase it % NPH of its (it / NPH)-th tile
+    int tile = blockIdx.x, ph2 = 0;
+    if (tile < A.tiles) load_halo(tile, 0, 0);
+    floatx16 acc[TM][TN];
+    for (int it = 0; tile < A.tiles; ++it) {
         const int b = it & 1;
         const char *sH = smem + FILT_BYTES + b * HALO_BYTES;
         // this wave's loads of the filter and of this halo landed (group 0's
-        // stores issued after them may still be in flight)
-        if (it == 0 || kg == 1) wait_vmcnt<0>();
+        // stores, issued after them by the previous tile's epilogue, may
+        // still be in flight)
+        if (it == 0 || kg == 1 || ph2 != 0) wait_vmcnt<0>();
         else wait_vmcnt<TM * NPASS>();
         wait_lgkm0();
         block_sync<true>();     // every wave's loads landed; the other buffer is free
-        const int next = tile + gridDim.x;
-        if (next < A.tiles) load_halo(next, b ^ 1);   // lands while this tile computes
+        {
+            // the next work item's halo lands while this one computes
+            const int nph = ph2 + 1 < NPH ? ph2 + 1 : 0;
+            const int ntile = ph2 + 1 < NPH ? tile : tile + (int)gridDim.x;
+            if (ntile < A.tiles) load_halo(ntile, nph, b ^ 1);
+        }
 
-        floatx16 acc[TM][TN];
+        if (ph2 == 0) {
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+            for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < TN; ++j)
+                for (int j = 0; j < TN; ++j)
 #pragma unroll
-                for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+                    for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+        }
         bf16x8 fa[3][TM], fb[3][TN];
-        // fragments of one slice: the row tiles' halo rows at tap (r, s) and
-        // the filter rows of tap t, chunk pair `sub`
+        // fragments of one slice: the row tiles' halo rows at halo offset
+        // (r, s) and the filter rows of tap t, chunk pair `sub`
         auto read = [&](int r, int s, int t, int sub, int buf) {
             const int shift = r * HWW + s;
 #pragma unroll
@@ -604,14 +627,20 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
             }
         } else {
             // group kg takes slices kg and kg + 2 of every tap (one group: all
-            // four); the next slice's fragments are read while a slice's MFMAs run
-            read(0, 0, 0, kg, 0);
-            for (int t = 0, r = 0, s = 0; t < taps; ++t) {
+            // four); the next slice's fragments are read while a slice's MFMAs
+            // run.  The phase's taps are (a + ST r, b + ST s), r < nr, s < ns,
+            // at halo offset (r, s) (stride 1: every tap, at (r, s)).
+            const int pa = ph2 >> 1, pb = ph2 & 1;
+            const int nr = (A.R - pa + ST - 1) / ST, ns = (A.S - pb + ST - 1) / ST, nt = nr * ns;
+            auto tap_of = [&](int r, int s) { return (pa + ST * r) * A.S + pb + ST * s; };
+            read(0, 0, tap_of(0, 0), kg, 0);
+            for (int i = 0, r = 0, s = 0; i < nt; ++i) {
                 int r1 = r, s1 = s + 1;                 // the next tap
-                if (s1 == A.S) {
+                if (s1 == ns) {
                     s1 = 0;
                     ++r1;
                 }
+                const int t = tap_of(r, s);
                 if constexpr (KG == 2) {
                     read(r, s, t, kg + 2, 1);
                     mfma(0);
@@ -623,7 +652,7 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
                     read(r, s, t, 3, 1);
                     mfma(0);
                 }
-                if (t + 1 < taps) read(r1, s1, t + 1, kg, 0);
+                if (i + 1 < nt) read(r1, s1, tap_of(r1, s1), kg, 0);
                 mfma(1);
                 r = r1;
                 s = s1;
@@ -653,13 +682,20 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
                     for (int v = 0; v < 16; ++v) acc[i][j][v] += red[((wl * TN + j) * 16 + v) * 64 + lane];
             }
         }
+        // the next work item: the tile's next phase, or the block's next tile
+        const int cur_tile = tile;
+        if (++ph2 == NPH) {
+            ph2 = 0;
+            tile += gridDim.x;
+        }
+        if (ph2 != 0) continue;   // the tile's sums are not complete yet
         wait_lgkm0();
         block_sync<true>();   // the halo (and the sums) are read before the staging reuses the buffer
         if (kg == 1) continue;
 
         // ---- epilogue (group 0): stage 32 rows per wave in this tile's halo
         // buffer, 16-byte stores
-        const int img = tile / A.tiles_img, rem = tile - img * A.tiles_img;
+        const int img = cur_tile / A.tiles_img, rem = cur_tile - img * A.tiles_img;
         const int ty0 = (rem / A.tiles_w) * A.TH, tx0 = (rem - (rem / A.tiles_w) * A.tiles_w) * A.TW;
         const int obase = ((img * A.P + ty0) * A.Q + tx0) * A.NO;
         bf16 *stage = reinterpret_cast<bf16 *>(smem + FILT_BYTES + b * HALO_BYTES) + wl * 32 * EPI_PITCH;
@@ -1552,15 +1588,19 @@ bool halo_shape_ok(int NO, int taps) {
 }
 
 // in[N][H][W][ch] -> out[N][P][Q][NO] (see halo_conv_kernel); ch = 64, or
-// 16 (33 to 64 outputs over exactly 16 taps, the stem's 2 x 2 blocks).
+// 16 (33 to 64 outputs over exactly 16 taps, the stem's 2 x 2 blocks);
+// stride 1, or 2 (64 channels, up to 64 outputs and 9 taps, not flipped:
+// the four stride phases, each with at most ceil(R/2) x ceil(S/2) taps).
 int run_halo(const bf16 *in, int N, int H, int W, const bf16 *filt, const bf16 *bias, int NO, int R, int S, int ph,
-             int pw, bool flip, bf16 *out, int P, int Q, hipStream_t st, int ch = 64) {
+             int pw, bool flip, bf16 *out, int P, int Q, hipStream_t st, int ch = 64, int stride = 1) {
     HaloArgs a{};
     a.in = in; a.filt = filt; a.bias = bias; a.out = out;
     a.H = H; a.W = W; a.P = P; a.Q = Q; a.R = R; a.S = S; a.ph = ph; a.pw = pw;
     a.NO = NO; a.flip = flip ? 1 : 0;
     if (ch != 64 && !(ch == 16 && NO > 32 && NO <= 64 && R * S == 16)) return (int)hipErrorInvalidValue;
-    if (!halo_tile(Q, R, S, &a.TH, &a.TW, ch)) return (int)hipErrorInvalidValue;
+    if (stride != 1 && !(stride == 2 && ch == 64 && !flip && NO <= 64 && R * S <= 9)) return (int)hipErrorInvalidValue;
+    if (!halo_tile(Q, (R + stride - 1) / stride, (S + stride - 1) / stride, &a.TH, &a.TW, ch))
+        return (int)hipErrorInvalidValue;
     const int tiles_h = (P + a.TH - 1) / a.TH;
     a.tiles_w = (Q + a.TW - 1) / a.TW;
     a.tiles_img = tiles_h * a.tiles_w;
@@ -1576,7 +1616,10 @@ int run_halo(const bf16 *in, int N, int H, int W, const bf16 *filt, const bf16 *
     const unsigned pk = flip ? kProfDgrad : kProfFwd;
     void *eb = nullptr, *ee = nullptr;
     const bool timed = prof_pair(pk, &eb, &ee);
-    if (ch == 16)
+    if (stride == 2)
+        hipExtLaunchKernelGGL((halo_conv_kernel<64, 9, 1, false, 64, 2>), grid, dim3(256), 0, st, (hipEvent_t)eb,
+                              (hipEvent_t)ee, 0, a);
+    else if (ch == 16)
         hipExtLaunchKernelGGL((halo_conv_kernel<64, 16, 1, true, 16>), grid, dim3(256), 0, st, (hipEvent_t)eb,
                               (hipEvent_t)ee, 0, a);
     else if (NO <= 32 && R * S == 16)   // 4 x 4: the unrolled schedule
@@ -1604,12 +1647,15 @@ bool halo_block_fwd_applies(const ConvGeom &g) {
            halo_tile(g.Q, 4, 4, &th, &tw, 16);
 }
 
-// Forward: stride 1, 64 input channels, the filter within the kernel's
-// instantiations, more than one tap.
+// Forward: 64 input channels, the filter within the kernel's
+// instantiations, more than one tap; stride 1, or 2 with up to 64 outputs
+// and 9 taps (its stride phases).
 bool halo_fwd_applies(const ConvGeom &g) {
-    return halo_enabled() && g.C == 64 && g.sh == 1 && g.sw == 1 && g.R * g.S > 1 && halo_shape_ok(g.K, g.R * g.S) &&
+    const bool s1 = g.sh == 1 && g.sw == 1, s2 = g.sh == 2 && g.sw == 2 && g.K <= 64 && g.R * g.S <= 9;
+    const int st = s2 ? 2 : 1;
+    return halo_enabled() && g.C == 64 && (s1 || s2) && g.R * g.S > 1 && halo_shape_ok(g.K, g.R * g.S) &&
            g.P > 0 && g.Q > 0 && operand_fits((long)g.N * g.P * g.Q * g.K) &&
-           [&] { int th, tw; return halo_tile(g.Q, g.R, g.S, &th, &tw); }();
+           [&] { int th, tw; return halo_tile(g.Q, (g.R + st - 1) / st, (g.S + st - 1) / st, &th, &tw); }();
 }
 
 // Input gradient: the correlation of dy (64 channels) with the flipped,
@@ -1687,7 +1733,7 @@ int conv_fwd(const ConvGeom &g, const void *x, const void *w, const void *bias, 
     if (!operand_fits((long)g.N * g.H * g.W * g.C) || !operand_fits((long)g.K * g.R * g.S * g.C)) return -1;
     if (halo_fwd_applies(g))
         return run_halo((const bf16 *)x, g.N, g.H, g.W, (const bf16 *)w, (const bf16 *)bias, g.K, g.R, g.S, g.ph, g.pw,
-                        false, (bf16 *)y, g.P, g.Q, st);
+                        false, (bf16 *)y, g.P, g.Q, st, 64, g.sh);
     Args a{};
     a.a = (const bf16 *)x; a.b = (const bf16 *)w; a.c = (bf16 *)y; a.g = g;
     a.M = g.N * g.P * g.Q; a.N = g.K; a.K = g.R * g.S * g.C;

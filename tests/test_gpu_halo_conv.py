@@ -1,6 +1,7 @@
 """The halo convolution path: stride-1 convolutions of 64-channel inputs whose
 filter fits in LDS (the 3x3 64 -> 64 layers of a ResNet stage 1, forward and
-input gradient) and a 3-channel stride-2 stem through its 2x2-block form: the
+input gradient), the forward of stride-2 ones through their four stride
+phases (the stage's downsampling layer) and a 3-channel stride-2 stem through its 2x2-block form: the
 forward as a 4x4 stride-1 convolution of 16-channel blocks, the input gradient
 as a 4x4 stride-1 correlation of the 64-channel dy.  Each
 case runs with the halo kernel and with it switched off
@@ -32,6 +33,12 @@ CASES = [
     ((1, 16, 12, 14), (64, 16, 4, 4), (1, 1), (0, 3)),     # input gradient only: 16 channels, 4 x 4 taps
     ((2, 3, 37, 41), (64, 3, 7, 7), (2, 2), (3, 3)),       # stem: both ways through 2 x 2 blocks
     ((2, 2, 21, 18), (48, 2, 7, 7), (2, 2), (3, 3)),       # 16-channel blocks: 48 outputs, 2 input channels
+    # stride 2, forward through the four stride phases
+    ((2, 64, 23, 21), (64, 64, 3, 3), (2, 2), (1, 1)),     # odd input: 12 x 11 outputs, ragged tiles
+    ((1, 64, 112, 112), (64, 64, 3, 3), (2, 2), (1, 1)),   # the ResNet stage-1 downsampling layer, one image
+    ((2, 64, 16, 70), (40, 64, 3, 3), (2, 2), (0, 1)),     # 40 outputs, two column tiles, asymmetric pad
+    ((2, 64, 14, 15), (64, 64, 2, 2), (2, 2), (0, 0)),     # 2 x 2 taps: one tap per phase, no padding
+    ((1, 64, 20, 22), (32, 64, 3, 1), (2, 2), (1, 0)),     # 3 x 1 taps, 32 outputs
 ]
 
 
