@@ -384,12 +384,16 @@ struct HaloArgs {
     int R, S, ph, pw;            // taps, zero padding
     int NO, flip;                // output channels stored; flipped taps
     int TH, TW, tiles_w, tiles_img, tiles;
+    int hr, hs, lor, los;        // output phases: halo taps (rows, columns) and the halo origin's offset
     uint32_t in_bytes, filt_bytes, out_bytes;
 };
 
 // Halo pixels per buffer: 320 of 64 channels (40 KB), 640 of 16 (20 KB, the
 // least that holds the epilogue's staging).
 template <int CH> constexpr int halo_max_px() { return CH == 64 ? 320 : 640; }
+// ... and for the output phases of a stride-2 input gradient, whose
+// epilogues stage in an LDS area of their own (264 pixels, 33 KB)
+constexpr int halo_max_px_oph() { return 264; }
 
 // Chunk swizzle of a pixel row of CH channels in LDS: 128-byte rows as the
 // GEMM's k-contiguous tiles (swz_k); 32-byte rows (two 16-byte chunks) swap
@@ -410,31 +414,47 @@ template <int CH> __device__ __forceinline__ int halo_swz(int row) {
 // for every phase so that the lanes' load offsets are worked out once),
 // whose sums accumulate before the one epilogue; the phases of a tile
 // reread neighbouring pixels of the same lines, mostly from L2.
-template <int NP, int TAPS_MAX, int KG, bool EXACT = false, int CH = 64, int ST = 1>
+//
+// OPH: the input gradient of a stride-2 convolution as its four output
+// phases.  Output pixel (2 i + a, 2 j + b) of dx takes the taps
+// r = r0 + 2 u (r0 = (a + ph) mod 2) and s = s0 + 2 v, which read dy at
+// (i + e_a - u, j + e_b - v), e_a = (a + ph - r0) / 2: each phase is a
+// stride-1 correlation of dy on the phase image (i, j).  All four read the
+// same dy neighbourhood, so a tile of the phase image is one halo (origin
+// (i0 + lor, j0 + los), (TH + hr - 1) x (TW + hs - 1) pixels) and four work
+// items, each with its own taps and epilogue (output rows and columns 2
+// apart).  The epilogues stage in an LDS area of their own, so the halo
+// stays for the next phase; the halo buffers are smaller to make room.
+// (Stores straight from the accumulators, 8 bytes per lane, would free that
+// area, but each one touches 32 pixel lines: 57 against 54 us.)
+template <int NP, int TAPS_MAX, int KG, bool EXACT = false, int CH = 64, int ST = 1, bool OPH = false>
 __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A) {
     static_assert(CH == 64 || (CH == 16 && KG == 1 && EXACT), "16-channel pixels: one group, exact taps");
     static_assert(ST == 1 || (ST == 2 && KG == 1 && !EXACT && CH == 64), "stride 2: one group, generic taps");
-    constexpr int NPH = ST * ST;                    // work items (stride phases) per tile
+    static_assert(!OPH || (ST == 1 && KG == 1 && !EXACT && CH == 64), "output phases: one group, generic taps");
+    constexpr int NPH = OPH ? 4 : ST * ST;          // work items (stride phases) per tile
     constexpr int NW = 4 * KG;                      // waves: KG k-groups of four
     constexpr int PB = CH * 2;                      // bytes of a pixel (or filter) row
     constexpr int CPR = CH / 8;                     // 16-byte chunks per row
     constexpr int RPI = 64 / CPR;                   // rows per LDS-DMA instruction
-    constexpr int MAXPX = halo_max_px<CH>();
+    constexpr int MAXPX = OPH ? halo_max_px_oph() : halo_max_px<CH>();
     constexpr int FILT_BYTES = TAPS_MAX * NP * PB;
     constexpr int HALO_BYTES = MAXPX * PB;
     constexpr int TN = NP / 32;
     constexpr int TM = 2;                           // row tiles per wave
     constexpr int EPI_PITCH = NP + 8;               // staged row, bf16 elements
-    static_assert(FILT_BYTES + 2 * HALO_BYTES <= 160 * 1024, "LDS");
-    static_assert(4 * 32 * EPI_PITCH * 2 <= HALO_BYTES, "epilogue staging fits a halo buffer");
+    constexpr int STAGE_BYTES = OPH ? 4 * 32 * EPI_PITCH * 2 : 0;   // the output phases' own staging
+    static_assert(FILT_BYTES + 2 * HALO_BYTES + STAGE_BYTES <= 160 * 1024, "LDS");
+    static_assert(OPH || 4 * 32 * EPI_PITCH * 2 <= HALO_BYTES, "epilogue staging fits a halo buffer");
     static_assert(KG == 1 || 4 * TN * 16 * 64 * 4 <= HALO_BYTES, "one row tile of group 1's sums fits a halo buffer");
-    __shared__ __attribute__((aligned(1024))) char smem[FILT_BYTES + 2 * HALO_BYTES];
+    __shared__ __attribute__((aligned(1024))) char smem[FILT_BYTES + 2 * HALO_BYTES + STAGE_BYTES];
     char *const sF = smem;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int kg = KG == 2 ? wave >> 2 : 0, wl = wave & 3;   // k-group, wave within it
     const int taps = A.R * A.S;
-    const int R2 = (A.R + ST - 1) / ST, S2 = (A.S + ST - 1) / ST;   // taps per phase, at most
+    // halo taps: per input phase at most (ST = 2), or the output phases' span (OPH)
+    const int R2 = OPH ? A.hr : (A.R + ST - 1) / ST, S2 = OPH ? A.hs : (A.S + ST - 1) / ST;
     const int HWW = A.TW + S2 - 1;                    // halo row length
     const int HP = (A.TH + R2 - 1) * HWW;             // halo pixels
     const __amdgpu_buffer_rsrc_t rin = rsrc(A.in, A.in_bytes);
@@ -510,7 +530,8 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
         char *dst = smem + FILT_BYTES + b * HALO_BYTES;
         const int img = tile / A.tiles_img, rem = tile - img * A.tiles_img;
         const int ty = rem / A.tiles_w, tx = rem - ty * A.tiles_w;
-        const int iy0 = ST * ty * A.TH + (ph2 >> 1) - A.ph, ix0 = ST * tx * A.TW + (ph2 & 1) - A.pw;
+        const int iy0 = OPH ? ty * A.TH + A.lor : ST * ty * A.TH + (ph2 >> 1) - A.ph;
+        const int ix0 = OPH ? tx * A.TW + A.los : ST * tx * A.TW + (ph2 & 1) - A.pw;
         const int gbase = ((img * A.H + iy0) * A.W + ix0) * CH;
 #pragma unroll
         for (int jj = 0; jj < HJ; ++jj) {
@@ -553,7 +574,7 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
             const bool ok = cl < A.NO && p < npx;
             e_y[i][ps] = ok ? oy : (1 << 20);
             e_x[i][ps] = ox;
-            e_c[i][ps] = (oy * A.Q + ox) * A.NO + cl;
+            e_c[i][ps] = ((OPH ? 2 : 1) * oy * A.Q + (OPH ? 2 : 1) * ox) * A.NO + cl;
         }
     int tap_r[TAPS_MAX], tap_s[TAPS_MAX];           // (r, s) of tap t
 #pragma unroll
@@ -566,23 +587,24 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
     if (tile < A.tiles) load_halo(tile, 0, 0);
     floatx16 acc[TM][TN];
     for (int it = 0; tile < A.tiles; ++it) {
-        const int b = it & 1;
+        // one halo per work item, or per tile (OPH)
+        const int b = OPH ? (it / NPH) & 1 : it & 1;
         const char *sH = smem + FILT_BYTES + b * HALO_BYTES;
-        // this wave's loads of the filter and of this halo landed (group 0's
-        // stores, issued after them by the previous tile's epilogue, may
-        // still be in flight)
-        if (it == 0 || kg == 1 || ph2 != 0) wait_vmcnt<0>();
-        else wait_vmcnt<TM * NPASS>();
-        wait_lgkm0();
-        block_sync<true>();     // every wave's loads landed; the other buffer is free
-        {
-            // the next work item's halo lands while this one computes
-            const int nph = ph2 + 1 < NPH ? ph2 + 1 : 0;
-            const int ntile = ph2 + 1 < NPH ? tile : tile + (int)gridDim.x;
+        if (!OPH || ph2 == 0) {
+            // this wave's loads of the filter and of this halo landed (group
+            // 0's stores, issued after them by the previous tile's
+            // epilogue(s), may still be in flight)
+            if (it == 0 || kg == 1 || (!OPH && ph2 != 0)) wait_vmcnt<0>();
+            else wait_vmcnt<(OPH ? NPH : 1) * TM * NPASS>();
+            wait_lgkm0();
+            block_sync<true>();     // every wave's loads landed; the other buffer is free
+            // the next work item's (OPH: tile's) halo lands while this one computes
+            const int nph = !OPH && ph2 + 1 < NPH ? ph2 + 1 : 0;
+            const int ntile = !OPH && ph2 + 1 < NPH ? tile : tile + (int)gridDim.x;
             if (ntile < A.tiles) load_halo(ntile, nph, b ^ 1);
         }
 
-        if (ph2 == 0) {
+        if (OPH || ph2 == 0) {
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -630,29 +652,38 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
             // four); the next slice's fragments are read while a slice's MFMAs
             // run.  The phase's taps are (a + ST r, b + ST s), r < nr, s < ns,
             // at halo offset (r, s) (stride 1: every tap, at (r, s)).
+            // OPH: output phase (pa, pb)'s taps (r0 + 2 r, s0 + 2 s) at halo
+            // offset (er - r - lor, es - s - los)
             const int pa = ph2 >> 1, pb = ph2 & 1;
-            const int nr = (A.R - pa + ST - 1) / ST, ns = (A.S - pb + ST - 1) / ST, nt = nr * ns;
-            auto tap_of = [&](int r, int s) { return (pa + ST * r) * A.S + pb + ST * s; };
-            read(0, 0, tap_of(0, 0), kg, 0);
+            const int r0 = (pa + A.ph) & 1, s0 = (pb + A.pw) & 1;
+            const int er = (pa + A.ph - r0) / 2 - A.lor, es = (pb + A.pw - s0) / 2 - A.los;
+            const int nr = OPH ? (A.R - r0 + 1) / 2 : (A.R - pa + ST - 1) / ST;
+            const int ns = OPH ? (A.S - s0 + 1) / 2 : (A.S - pb + ST - 1) / ST, nt = nr * ns;
+            auto tap_of = [&](int r, int s) {
+                return OPH ? (r0 + 2 * r) * A.S + s0 + 2 * s : (pa + ST * r) * A.S + pb + ST * s;
+            };
+            auto hr_of = [&](int r) { return OPH ? er - r : r; };   // halo offset of tap row r
+            auto hs_of = [&](int s) { return OPH ? es - s : s; };
+            read(hr_of(0), hs_of(0), tap_of(0, 0), kg, 0);
             for (int i = 0, r = 0, s = 0; i < nt; ++i) {
                 int r1 = r, s1 = s + 1;                 // the next tap
                 if (s1 == ns) {
                     s1 = 0;
                     ++r1;
                 }
-                const int t = tap_of(r, s);
+                const int t = tap_of(r, s), hr = hr_of(r), hs = hs_of(s);
                 if constexpr (KG == 2) {
-                    read(r, s, t, kg + 2, 1);
+                    read(hr, hs, t, kg + 2, 1);
                     mfma(0);
                 } else {
-                    read(r, s, t, 1, 1);
+                    read(hr, hs, t, 1, 1);
                     mfma(0);
-                    read(r, s, t, 2, 0);
+                    read(hr, hs, t, 2, 0);
                     mfma(1);
-                    read(r, s, t, 3, 1);
+                    read(hr, hs, t, 3, 1);
                     mfma(0);
                 }
-                if (i + 1 < nt) read(r1, s1, tap_of(r1, s1), kg, 0);
+                if (i + 1 < nt) read(hr_of(r1), hs_of(s1), tap_of(r1, s1), kg, 0);
                 mfma(1);
                 r = r1;
                 s = s1;
@@ -683,23 +714,29 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
             }
         }
         // the next work item: the tile's next phase, or the block's next tile
-        const int cur_tile = tile;
+        const int cur_tile = tile, cur_ph = ph2;
         if (++ph2 == NPH) {
             ph2 = 0;
             tile += gridDim.x;
         }
-        if (ph2 != 0) continue;   // the tile's sums are not complete yet
-        wait_lgkm0();
-        block_sync<true>();   // the halo (and the sums) are read before the staging reuses the buffer
+        if (!OPH && ph2 != 0) continue;   // the tile's sums are not complete yet
+        if constexpr (!OPH) {
+            wait_lgkm0();
+            block_sync<true>();   // the halo (and the sums) are read before the staging reuses the buffer
+        }
         if (kg == 1) continue;
 
         // ---- epilogue (group 0): stage 32 rows per wave in this tile's halo
         // buffer, 16-byte stores
         const int img = cur_tile / A.tiles_img, rem = cur_tile - img * A.tiles_img;
         const int ty0 = (rem / A.tiles_w) * A.TH, tx0 = (rem - (rem / A.tiles_w) * A.tiles_w) * A.TW;
-        const int obase = ((img * A.P + ty0) * A.Q + tx0) * A.NO;
-        bf16 *stage = reinterpret_cast<bf16 *>(smem + FILT_BYTES + b * HALO_BYTES) + wl * 32 * EPI_PITCH;
+        // OPH: output phase (oa, ob), rows and columns 2 apart
+        constexpr int OS = OPH ? 2 : 1;
+        const int oa = OPH ? cur_ph >> 1 : 0, ob = OPH ? cur_ph & 1 : 0;
+        const int obase = ((img * A.P + OS * ty0 + oa) * A.Q + OS * tx0 + ob) * A.NO;
         typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+        // (OPH: in the staging area past the halo buffers, which the next phases still read)
+        bf16 *stage = reinterpret_cast<bf16 *>(smem + FILT_BYTES + (OPH ? 2 : b) * HALO_BYTES) + wl * 32 * EPI_PITCH;
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -718,7 +755,7 @@ __global__ __launch_bounds__(KG * 256, 1) void halo_conv_kernel(const HaloArgs A
                 const int lin = ps * 64 + lane;
                 const int rl = lin / SEG, cl = (lin % SEG) * 8;
                 const u32x4 v = *reinterpret_cast<const u32x4 *>(stage + rl * EPI_PITCH + cl);
-                const bool ok = ty0 + e_y[i][ps] < A.P && tx0 + e_x[i][ps] < A.Q;
+                const bool ok = OS * (ty0 + e_y[i][ps]) + oa < A.P && OS * (tx0 + e_x[i][ps]) + ob < A.Q;
                 // element index below 2^31 (operand_fits on the output)
                 const uint32_t off = ok ? (uint32_t)(obase + e_c[i][ps]) * 2u : kOOB;
                 __builtin_amdgcn_raw_buffer_store_b128(v, ro, (int)off, 0, 0);
@@ -1569,11 +1606,11 @@ bool halo_enabled() {
 // many rows as fit both 256 pixels and a halo of at most halo_max_px pixels
 // (a tile always computes 256 rows of MFMA tiles, so the largest tile is the
 // cheapest per pixel).  False when no tile fits.
-bool halo_tile(int Q, int R, int S, int *TH, int *TW, int ch = 64) {
+bool halo_tile(int Q, int R, int S, int *TH, int *TW, int ch = 64, bool oph = false) {
     if (Q <= 0) return false;
     const int ntw = (Q + 31) / 32;
     const int tw = (Q + ntw - 1) / ntw;
-    const int maxpx = ch == 64 ? halo_max_px<64>() : halo_max_px<16>();
+    const int maxpx = oph ? halo_max_px_oph() : ch == 64 ? halo_max_px<64>() : halo_max_px<16>();
     const int th = std::min(256 / tw, maxpx / (tw + S - 1) - (R - 1));
     if (th < 1) return false;
     *TH = th;
@@ -1587,22 +1624,58 @@ bool halo_shape_ok(int NO, int taps) {
     return NO % 8 == 0 && NO > 0 && ((NO <= 32 && taps <= 16) || (NO <= 64 && taps <= 9));
 }
 
+// Output phases of a stride-2 input gradient along one dimension (R taps,
+// padding ph): phase a takes taps r = r0 + 2u (r0 = (a + ph) mod 2) reading
+// dy at i + e_a - u (e_a = (a + ph - r0) / 2).  *lo = the least dy offset
+// over both phases (the halo origin), *span = the halo taps (offsets lo ..
+// max e_a).  False when a phase has no tap.
+bool oph_span(int R, int ph, int *lo, int *span) {
+    int lo_ = 1 << 20, hi = -(1 << 20);
+    for (int a = 0; a < 2; ++a) {
+        const int r0 = (a + ph) & 1, nu = (R - r0 + 1) / 2, e = (a + ph - r0) / 2;
+        if (nu < 1) return false;
+        lo_ = std::min(lo_, e - (nu - 1));
+        hi = std::max(hi, e);
+    }
+    *lo = lo_;
+    *span = hi - lo_ + 1;
+    return true;
+}
+
+// The output phases' tile (on the phase image of the input gradient), or false.
+bool oph_tile(int Wx, int R, int S, int pw, int ph, int *TH, int *TW, HaloArgs *a = nullptr) {
+    int lor, hr, los, hs;
+    if (!oph_span(R, ph, &lor, &hr) || !oph_span(S, pw, &los, &hs)) return false;
+    if (!halo_tile((Wx + 1) / 2, hr, hs, TH, TW, 64, true)) return false;
+    if (a) {
+        a->hr = hr; a->hs = hs; a->lor = lor; a->los = los;
+    }
+    return true;
+}
+
 // in[N][H][W][ch] -> out[N][P][Q][NO] (see halo_conv_kernel); ch = 64, or
 // 16 (33 to 64 outputs over exactly 16 taps, the stem's 2 x 2 blocks);
 // stride 1, or 2 (64 channels, up to 64 outputs and 9 taps, not flipped:
 // the four stride phases, each with at most ceil(R/2) x ceil(S/2) taps).
+// oph: the input gradient of a stride-2 convolution (in = dy of H x W,
+// out = dx of P x Q, ph / pw the convolution's padding, filt = Wt[NO][R][S][64]
+// not flipped) as its four output phases.
 int run_halo(const bf16 *in, int N, int H, int W, const bf16 *filt, const bf16 *bias, int NO, int R, int S, int ph,
-             int pw, bool flip, bf16 *out, int P, int Q, hipStream_t st, int ch = 64, int stride = 1) {
+             int pw, bool flip, bf16 *out, int P, int Q, hipStream_t st, int ch = 64, int stride = 1,
+             bool oph = false) {
     HaloArgs a{};
     a.in = in; a.filt = filt; a.bias = bias; a.out = out;
     a.H = H; a.W = W; a.P = P; a.Q = Q; a.R = R; a.S = S; a.ph = ph; a.pw = pw;
     a.NO = NO; a.flip = flip ? 1 : 0;
     if (ch != 64 && !(ch == 16 && NO > 32 && NO <= 64 && R * S == 16)) return (int)hipErrorInvalidValue;
     if (stride != 1 && !(stride == 2 && ch == 64 && !flip && NO <= 64 && R * S <= 9)) return (int)hipErrorInvalidValue;
-    if (!halo_tile(Q, (R + stride - 1) / stride, (S + stride - 1) / stride, &a.TH, &a.TW, ch))
+    if (oph && !(stride == 1 && ch == 64 && !flip && NO <= 64 && R * S <= 9)) return (int)hipErrorInvalidValue;
+    if (oph ? !oph_tile(Q, R, S, pw, ph, &a.TH, &a.TW, &a)
+            : !halo_tile(Q, (R + stride - 1) / stride, (S + stride - 1) / stride, &a.TH, &a.TW, ch))
         return (int)hipErrorInvalidValue;
-    const int tiles_h = (P + a.TH - 1) / a.TH;
-    a.tiles_w = (Q + a.TW - 1) / a.TW;
+    // output tiles over the output (OPH: over its phase image, ceil(P/2) x ceil(Q/2))
+    const int tiles_h = ((oph ? (P + 1) / 2 : P) + a.TH - 1) / a.TH;
+    a.tiles_w = ((oph ? (Q + 1) / 2 : Q) + a.TW - 1) / a.TW;
     a.tiles_img = tiles_h * a.tiles_w;
     const long tiles = (long)N * a.tiles_img;
     if (tiles == 0) return 0;
@@ -1613,10 +1686,13 @@ int run_halo(const bf16 *in, int N, int H, int W, const bf16 *filt, const bf16 *
     if (!operand_fits((long)N * P * Q * NO)) return (int)hipErrorInvalidValue;
     a.out_bytes = bytes_of((long)N * P * Q * NO);
     const dim3 grid((unsigned)std::min<long>(tiles, kCUs));
-    const unsigned pk = flip ? kProfDgrad : kProfFwd;
+    const unsigned pk = flip || oph ? kProfDgrad : kProfFwd;   // the input-gradient contractions
     void *eb = nullptr, *ee = nullptr;
     const bool timed = prof_pair(pk, &eb, &ee);
-    if (stride == 2)
+    if (oph)
+        hipExtLaunchKernelGGL((halo_conv_kernel<64, 9, 1, false, 64, 1, true>), grid, dim3(256), 0, st,
+                              (hipEvent_t)eb, (hipEvent_t)ee, 0, a);
+    else if (stride == 2)
         hipExtLaunchKernelGGL((halo_conv_kernel<64, 9, 1, false, 64, 2>), grid, dim3(256), 0, st, (hipEvent_t)eb,
                               (hipEvent_t)ee, 0, a);
     else if (ch == 16)
@@ -1659,11 +1735,19 @@ bool halo_fwd_applies(const ConvGeom &g) {
 }
 
 // Input gradient: the correlation of dy (64 channels) with the flipped,
-// transposed filter and padding R - 1 - ph (stride 1).
+// transposed filter and padding R - 1 - ph (stride 1), or (stride 2, up to
+// 64 input channels and 9 taps) its four output phases.
+bool halo_dgrad_s2(const ConvGeom &g) {
+    int th, tw;
+    return g.sh == 2 && g.sw == 2 && g.C <= 64 && g.R * g.S <= 9 && oph_tile(g.W, g.R, g.S, g.pw, g.ph, &th, &tw);
+}
 bool halo_dgrad_applies(const ConvGeom &g) {
-    return halo_enabled() && g.K == 64 && g.sh == 1 && g.sw == 1 && g.R * g.S > 1 && halo_shape_ok(g.C, g.R * g.S) &&
-           g.ph <= g.R - 1 && g.pw <= g.S - 1 && g.H > 0 && g.W > 0 && operand_fits((long)g.N * g.H * g.W * g.C) &&
-           [&] { int th, tw; return halo_tile(g.W, g.R, g.S, &th, &tw); }();
+    if (!halo_enabled() || g.K != 64 || g.R * g.S <= 1 || !halo_shape_ok(g.C, g.R * g.S) || g.H <= 0 || g.W <= 0 ||
+        !operand_fits((long)g.N * g.H * g.W * g.C))
+        return false;
+    if (g.sh == 1 && g.sw == 1)
+        return g.ph <= g.R - 1 && g.pw <= g.S - 1 && [&] { int th, tw; return halo_tile(g.W, g.R, g.S, &th, &tw); }();
+    return halo_dgrad_s2(g);
 }
 
 // The convolution forward and input gradient run on the tap-step operand
@@ -1914,6 +1998,9 @@ int conv_dgrad(const ConvGeom &g, const void *dy, const void *w, const void *bia
         bf16 *wt = reinterpret_cast<bf16 *>(ws);
         const int err = transpose_krsc(w, wt, g.K, g.R * g.S, g.C, st);
         if (err) return err;
+        if (g.sh == 2)   // the four output phases
+            return run_halo((const bf16 *)dy, g.N, g.P, g.Q, wt, (const bf16 *)bias, g.C, g.R, g.S, g.ph, g.pw, false,
+                            (bf16 *)dx, g.H, g.W, st, 64, 1, true);
         return run_halo((const bf16 *)dy, g.N, g.P, g.Q, wt, (const bf16 *)bias, g.C, g.R, g.S, g.R - 1 - g.ph,
                         g.S - 1 - g.pw, true, (bf16 *)dx, g.H, g.W, st);
     }

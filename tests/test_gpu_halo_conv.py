@@ -1,7 +1,8 @@
 """The halo convolution path: stride-1 convolutions of 64-channel inputs whose
 filter fits in LDS (the 3x3 64 -> 64 layers of a ResNet stage 1, forward and
-input gradient), the forward of stride-2 ones through their four stride
-phases (the stage's downsampling layer) and a 3-channel stride-2 stem through its 2x2-block form: the
+input gradient), stride-2 ones through their four stride phases (the stage's
+downsampling layer: the forward over the input's phases, the input gradient
+over its own) and a 3-channel stride-2 stem through its 2x2-block form: the
 forward as a 4x4 stride-1 convolution of 16-channel blocks, the input gradient
 as a 4x4 stride-1 correlation of the 64-channel dy.  Each
 case runs with the halo kernel and with it switched off
@@ -39,6 +40,10 @@ CASES = [
     ((2, 64, 16, 70), (40, 64, 3, 3), (2, 2), (0, 1)),     # 40 outputs, two column tiles, asymmetric pad
     ((2, 64, 14, 15), (64, 64, 2, 2), (2, 2), (0, 0)),     # 2 x 2 taps: one tap per phase, no padding
     ((1, 64, 20, 22), (32, 64, 3, 1), (2, 2), (1, 0)),     # 3 x 1 taps, 32 outputs
+    # stride 2, input gradient through the four output phases (64 output-gradient channels)
+    ((2, 40, 17, 19), (64, 40, 3, 3), (2, 2), (1, 1)),     # 40 input channels, odd extents
+    ((1, 24, 17, 9), (64, 24, 3, 3), (2, 2), (2, 2)),      # padding 2: the halo starts one pixel early
+    ((1, 32, 18, 18), (64, 32, 2, 3), (2, 2), (1, 1)),     # 2 x 3 taps: one and two taps per phase row
 ]
 
 
@@ -88,4 +93,23 @@ def test_halo_transposed_conv_forward():
     gx, gw, gb = ms.layer_backward(rec, dev(gy, "bf16"))
     check("dx", host(gx), oracle.convt2d_input_grad(gy, w, xs, (1, 1), (1, 1)), "bf16")
     check("dW", host(gw), oracle.convt2d_weight_grad(gy, x, (64, co, 3, 3), (1, 1), (1, 1)), "bf16")
+    check("db", host(gb), oracle.convt2d_bias_grad(gy), "bf16")
+
+
+def test_halo_transposed_conv_forward_stride_2():
+    """A stride-2 transposed convolution of 64 input channels (3x3, pad 1,
+    output padding 1: 2x upsampling) runs its forward through the output
+    phases of the adjoint convolution's input gradient, bias in the
+    epilogue."""
+    xs, co = (2, 64, 9, 13), 48
+    x = synth.normal(xs, 8194, dtype="bf16")
+    w = synth.kaiming_uniform((64, co, 3, 3), 8195, co * 9, dtype="bf16")
+    b = synth.normal((co,), 8196, 1.0, dtype="bf16")
+    y, rec = ms.layer_forward(ms.ConvTranspose2d(2, 1, 1), dev(x, "bf16"), dev(w, "bf16"), dev(b, "bf16"), 7)
+    assert tuple(y.shape) == (2, co, 18, 26)
+    check("y", host(y), oracle.convt2d_forward(x, w, b, (2, 2), (1, 1), (1, 1)), "bf16")
+    gy = synth.normal(tuple(y.shape), 8197, dtype="bf16")
+    gx, gw, gb = ms.layer_backward(rec, dev(gy, "bf16"))
+    check("dx", host(gx), oracle.convt2d_input_grad(gy, w, xs, (2, 2), (1, 1), (1, 1)), "bf16")
+    check("dW", host(gw), oracle.convt2d_weight_grad(gy, x, (64, co, 3, 3), (2, 2), (1, 1), (1, 1)), "bf16")
     check("db", host(gb), oracle.convt2d_bias_grad(gy), "bf16")
