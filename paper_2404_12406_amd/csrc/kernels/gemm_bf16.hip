@@ -949,6 +949,36 @@ __global__ __launch_bounds__(256) void unpack_blocks_kernel(const bf16 *__restri
     }
 }
 
+// The same, with the row staged in LDS so that dx is written in 16-byte
+// vectors: one workgroup per image row (n, h), rows of W * C elements a
+// multiple of 8 (the host checks).  Thread j loads the half block that
+// holds row h for block column j and puts its pixels' C channels in place
+// in the LDS row; then the row leaves as ceil(W * C / 8) 16-byte stores.
+constexpr int kUnpackRowMax = 2048;   // LDS row capacity in elements (4 KB)
+__global__ __launch_bounds__(256) void unpack_blocks_row_kernel(const bf16 *__restrict__ dxq, int H, int W, int C,
+                                                                int Hq, int Wq, int ph, int pw,
+                                                                bf16 *__restrict__ dx) {
+    __shared__ __attribute__((aligned(16))) bf16 row[kUnpackRowMax];
+    const uint32_t nh = blockIdx.x, n = nh / (uint32_t)H, h = nh - n * (uint32_t)H;
+    const uint32_t hp = h + (uint32_t)ph;
+    const bf16 *src = dxq + (((size_t)n * Hq + hp / 2) * Wq) * 16 + 8 * (hp & 1);
+    for (int j = threadIdx.x; j < Wq; j += blockDim.x) {
+        const Vec16<bf16> v = load16(src + (size_t)j * 16);
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const int w = 2 * j + b - pw;
+            if (w < 0 || w >= W) continue;
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                if (c < C) row[w * C + c] = v.e[4 * b + c];
+        }
+    }
+    __syncthreads();
+    const int nv = W * C / 8;
+    u32x4 *out = reinterpret_cast<u32x4 *>(dx + (size_t)nh * W * C);
+    for (int k = threadIdx.x; k < nv; k += blockDim.x) out[k] = reinterpret_cast<const u32x4 *>(row)[k];
+}
+
 // The forward's input in 2 x 2 pixel blocks (at most 4 channels, stride 2
 // in both dimensions): xq[n][i][j][8a + 4b + c] = x[n][2i + a - ph][2j + b - pw][c],
 // zeros outside the image and for c >= C.  One thread writes the 16 channels
@@ -979,6 +1009,39 @@ __global__ __launch_bounds__(256) void pack_blocks_kernel(const bf16 *__restrict
         }
         *reinterpret_cast<u32x4 *>(xq + (size_t)i * 16) = v0;
         *reinterpret_cast<u32x4 *>(xq + (size_t)i * 16 + 8) = v1;
+    }
+}
+
+// The same, with the two input rows of a block row staged in LDS so that x
+// is read in 16-byte vectors: one workgroup per block row (n, i), rows of
+// W * C elements a multiple of 8 (the host checks).  Rows 2i - ph and
+// 2i + 1 - ph land in LDS (zeros outside the image); thread j then gathers
+// block (n, i, j) from LDS and writes its 16 channels as two 16-byte stores.
+__global__ __launch_bounds__(256) void pack_blocks_row_kernel(const bf16 *__restrict__ x, int H, int W, int C, int Hq,
+                                                              int Wq, int ph, int pw, bf16 *__restrict__ xq) {
+    __shared__ __attribute__((aligned(16))) bf16 rows[2][kUnpackRowMax];
+    const uint32_t ni = blockIdx.x, n = ni / (uint32_t)Hq, iq = ni - n * (uint32_t)Hq;
+    const int nv = W * C / 8;
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+        const int h = 2 * (int)iq + a - ph;
+        const bool in = (unsigned)h < (unsigned)H;
+        const u32x4 *src = reinterpret_cast<const u32x4 *>(x + ((size_t)n * H + (in ? h : 0)) * W * C);
+        for (int k = threadIdx.x; k < nv; k += blockDim.x)
+            reinterpret_cast<u32x4 *>(rows[a])[k] = in ? src[k] : u32x4{0u, 0u, 0u, 0u};
+    }
+    __syncthreads();
+    for (int j = threadIdx.x; j < Wq; j += blockDim.x) {
+        Vec16<bf16> v[2];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int a = e >> 3, b = (e >> 2) & 1, c = e & 3;
+            const int w = 2 * j + b - pw;
+            v[e >> 3].e[e & 7] = c < C && (unsigned)w < (unsigned)W ? rows[a][w * C + c] : (bf16)0.f;
+        }
+        bf16 *dst = xq + ((size_t)ni * Wq + j) * 16;
+        store16(dst, v[0]);
+        store16(dst + 8, v[1]);
     }
 }
 
@@ -1475,6 +1538,13 @@ int pack_blocks(const ConvGeom &g, const void *x, void *xq, hipStream_t st) {
     const int64_t work = (int64_t)g.N * block_height(g) * pair_width(g);
     if (work == 0) return 0;
     if (work > INT32_MAX || (int64_t)g.N * g.H * g.W * g.C * 2 >= (int64_t)kOOB) return (int)hipErrorInvalidValue;
+    // rows of whole 16-byte vectors that fit the LDS rows, x 16-byte aligned:
+    // one workgroup per block row, coalesced loads
+    if ((g.W * g.C) % 8 == 0 && g.W * g.C <= kUnpackRowMax && al16(x)) {
+        hipLaunchKernelGGL(pack_blocks_row_kernel, dim3((unsigned)((int64_t)g.N * block_height(g))), dim3(128), 0, st,
+                           (const bf16 *)x, g.H, g.W, g.C, block_height(g), pair_width(g), g.ph, g.pw, (bf16 *)xq);
+        return (int)hipGetLastError();
+    }
     hipLaunchKernelGGL(pack_blocks_kernel, dim3(launch_grid(work)), dim3(256), 0, st, (const bf16 *)x, (uint32_t)g.N, g.H,
                        g.W, g.C, block_height(g), pair_width(g), g.ph, g.pw, (bf16 *)xq);
     return (int)hipGetLastError();
@@ -1484,6 +1554,13 @@ int unpack_blocks(const ConvGeom &g, const void *dxq, void *dx, hipStream_t st) 
     const int64_t NH = (int64_t)g.N * g.H, work = NH * pair_width(g);
     if (work == 0) return 0;
     if (work > INT32_MAX) return (int)hipErrorInvalidValue;
+    // rows of whole 16-byte vectors that fit the LDS row, dx 16-byte aligned:
+    // one workgroup per row, coalesced stores
+    if ((g.W * g.C) % 8 == 0 && g.W * g.C <= kUnpackRowMax && al16(dx) && NH <= INT32_MAX) {
+        hipLaunchKernelGGL(unpack_blocks_row_kernel, dim3((unsigned)NH), dim3(128), 0, st, (const bf16 *)dxq, g.H, g.W,
+                           g.C, block_height(g), pair_width(g), g.ph, g.pw, (bf16 *)dx);
+        return (int)hipGetLastError();
+    }
     hipLaunchKernelGGL(unpack_blocks_kernel, dim3(launch_grid(work)), dim3(256), 0, st, (const bf16 *)dxq,
                        (uint32_t)NH, g.H, g.W, g.C, block_height(g), pair_width(g), g.ph, g.pw, (bf16 *)dx);
     return (int)hipGetLastError();

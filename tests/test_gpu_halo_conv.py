@@ -34,6 +34,8 @@ CASES = [
     ((1, 16, 12, 14), (64, 16, 4, 4), (1, 1), (0, 3)),     # input gradient only: 16 channels, 4 x 4 taps
     ((2, 3, 37, 41), (64, 3, 7, 7), (2, 2), (3, 3)),       # stem: both ways through 2 x 2 blocks
     ((2, 2, 21, 18), (48, 2, 7, 7), (2, 2), (3, 3)),       # 16-channel blocks: 48 outputs, 2 input channels
+    ((2, 3, 30, 32), (64, 3, 7, 7), (2, 2), (3, 3)),       # stem with rows of 16-byte vectors: row-staged packing
+    ((1, 4, 19, 20), (48, 4, 7, 7), (2, 2), (3, 3)),       # 4 channels, odd height, row-staged packing
     # stride 2, forward through the four stride phases
     ((2, 64, 23, 21), (64, 64, 3, 3), (2, 2), (1, 1)),     # odd input: 12 x 11 outputs, ragged tiles
     ((1, 64, 112, 112), (64, 64, 3, 3), (2, 2), (1, 1)),   # the ResNet stage-1 downsampling layer, one image
