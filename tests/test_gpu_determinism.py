@@ -2,8 +2,10 @@
 atomics: split-K GEMMs and their reduce pass, the weight gradient's split
 partials with the fused bias partials, the input gradient's fused column
 sums and their finalize pass, the standalone column sum, the BN-eval
-backward reduction and the fp32 path.  Each reduction adds its partials in a
-fixed order, so the same inputs give the same bytes on every call."""
+backward reduction, the fp32 path, the halo convolutions (stride phases,
+k-group sums) and the 12-wave and paired Linear forwards.  Each reduction adds
+its partials in a fixed order, so the same inputs give the same bytes on
+every call."""
 import os
 
 import pytest
@@ -110,3 +112,35 @@ def test_fp32_path_with_splits():
     """The fp32 kernels (and their split-K reduce) on the fp32 single-conv
     shape with every flag."""
     _twice(_conv_case((8, 16, 32, 32), (32, 16, 3, 3), (1, 1), (1, 1), "f32", 7, 9950))
+
+
+@pytest.mark.parametrize("case", [
+    ((2, 64, 23, 21), (64, 64, 3, 3), (2, 2), (1, 1)),   # halo: stride-2 input phases and output phases
+    ((2, 64, 13, 11), (64, 64, 3, 3), (1, 1), (1, 1)),   # halo: the unrolled 3x3 schedule, both ways
+    ((2, 3, 30, 32), (64, 3, 7, 7), (2, 2), (3, 3)),     # stem blocks: 16-channel forward, two-k-group input gradient
+])
+def test_halo_convolutions(case):
+    """The halo kernels accumulate taps and stride phases in a fixed order
+    (the two-k-group form adds group 1's sums through LDS): every output and
+    gradient repeats byte for byte."""
+    xs, ws, stride, pad = case
+    _twice(_conv_case(xs, ws, stride, pad, "bf16", 7, 9960))
+
+
+@pytest.mark.parametrize("n_out", [2304, 3072])
+def test_twelve_wave_and_paired_linear_forward(n_out):
+    """8192-row Linear forwards on the 256 x 288 tile (2304 outputs, one
+    wave) and on the paired column split (3072 outputs: 256 x 256 then
+    256 x 128 tiles in one launch), with the input gradient of each."""
+    M, Kin = 8192, 136
+    x = dev(synth.normal((M, Kin), 9970, dtype="bf16"), "bf16")
+    w = dev(synth.normal((n_out, Kin), 9971, 0.05, dtype="bf16"), "bf16")
+    b = dev(synth.normal((n_out,), 9972, 1.0, dtype="bf16"), "bf16")
+    gy = dev(synth.normal((M, n_out), 9973, dtype="bf16"), "bf16")
+
+    def run():
+        y, rec = ms.layer_forward(ms.Linear(), x, w, b, 1)
+        grads = ms.layer_backward(rec, gy)
+        torch.cuda.synchronize()
+        return (y, *grads)
+    _twice(run)
