@@ -120,7 +120,11 @@ __device__ __forceinline__ void params_at(__amdgpu_buffer_rsrc_t r, uint32_t i, 
 //    grid, a multiple of nvc).
 // Either way a thread's vectors all hold the same channels, so it folds
 // (s, t) for its V channels once.
-constexpr int kBnU = 8;
+// U = kBnFlatU: 4 beat 8 and 16 on the ResNet-18-shaped stack's layers
+// (stage 1, 51 MB: 12.4 against 13.2 and 13.5 us; the stack's BN-eval
+// forward 165 against 169 us, alternating runs on one box).
+constexpr int kBnFlatU = 4;
+constexpr int kBnU = 8;   // vectors per thread of bn_nchw_kernel (below)
 
 template <typename T, int V>
 __global__ __launch_bounds__(256) void bn_fwd_flat_kernel(const T *__restrict__ x, const T *__restrict__ mean,
@@ -128,7 +132,7 @@ __global__ __launch_bounds__(256) void bn_fwd_flat_kernel(const T *__restrict__ 
                                                           const T *__restrict__ beta, float eps, int64_t nvec,
                                                           int nvc, bool contig, T *__restrict__ y) {
     const int64_t stride = contig ? 256 : (int64_t)gridDim.x * blockDim.x;
-    const int64_t i0 = contig ? (int64_t)blockIdx.x * 256 * kBnU + threadIdx.x
+    const int64_t i0 = contig ? (int64_t)blockIdx.x * 256 * kBnFlatU + threadIdx.x
                               : (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int c0 = (int)(i0 % nvc) * V;
     VecT<T, V> pm, pv, pg, pb;
@@ -145,13 +149,13 @@ __global__ __launch_bounds__(256) void bn_fwd_flat_kernel(const T *__restrict__ 
         s[e] = g * rsqrtf(to_f32(pv.e[e]) + eps);
         t[e] = b - m * s[e];
     }
-    for (int64_t i = i0; i < nvec; i += contig ? nvec : kBnU * stride) {
-        VecT<T, V> v[kBnU];
+    for (int64_t i = i0; i < nvec; i += contig ? nvec : kBnFlatU * stride) {
+        VecT<T, V> v[kBnFlatU];
 #pragma unroll
-        for (int u = 0; u < kBnU; ++u)
+        for (int u = 0; u < kBnFlatU; ++u)
             if (i + u * stride < nvec) v[u].load(x + (i + u * stride) * V);
 #pragma unroll
-        for (int u = 0; u < kBnU; ++u) {
+        for (int u = 0; u < kBnFlatU; ++u) {
             if (i + u * stride < nvec) {
 #pragma unroll
                 for (int e = 0; e < V; ++e) v[u].e[e] = from_f32<T>(fmaf(to_f32(v[u].e[e]), s[e], t[e]));
@@ -501,7 +505,7 @@ int bn_sweep(int dtype, const void *x, const void *mean, const void *var, const 
     const int Ve = vec ? V : 1;
     const int nvc = C / Ve;
     const int64_t nvec = rows * (int64_t)nvc;
-    // one pass of kBnU vectors per thread; the thread count is rounded up to
+    // one pass of kBnFlatU vectors per thread; the thread count is rounded up to
     // a multiple of nvc (block granularity q) so every thread keeps its
     // channels
     int64_t q = 1;
@@ -510,7 +514,7 @@ int bn_sweep(int dtype, const void *x, const void *mean, const void *var, const 
         while (b) { const int64_t r = a % b; a = b; b = r; }
         q = nvc / a;   // nvc / gcd(nvc, 256)
     }
-    int64_t blocks = std::max<int64_t>(1, (nvec + 256 * kBnU - 1) / (256 * kBnU));
+    int64_t blocks = std::max<int64_t>(1, (nvec + 256 * kBnFlatU - 1) / (256 * kBnFlatU));
     const bool contig = 256 % nvc == 0;
     if (!contig) blocks = (blocks + q - 1) / q * q;
     hipStream_t st = (hipStream_t)stream;
