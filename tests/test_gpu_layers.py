@@ -114,6 +114,14 @@ BN_CASES = [
     ((50, 36), "f32", True),           # [N, C] input
     ((4, 64, 9, 9), "bf16", False),    # affine=False
     ((2, 512, 7, 7), "bf16", True),
+    # channels-last sweeps whose row of vectors divides 256 (a block streams one
+    # contiguous range): 256 vectors per row in bf16 and in f32, 4 f32 vectors,
+    # 2 scalar channels, and one 8-channel vector over 3 pixels
+    ((2, 2048, 3, 5), "bf16", True),
+    ((3, 1024, 2, 3), "f32", True),
+    ((5, 16, 3, 3), "f32", True),
+    ((3, 2, 5, 7), "bf16", True),
+    ((1, 8, 1, 3), "bf16", True),
 ]
 
 
