@@ -1054,6 +1054,10 @@ def main():
     ap.add_argument("--per-layer-only", action="store_true",
                     help="with --workload: one untimed step, then only the per-layer kernel timings (every "
                          "layer call preceded by a cache-evicting sweep, so a kernel trace splits at the sweeps)")
+    ap.add_argument("--reduction-only", action="store_true",
+                    help="only the HBM-bound backward passes (BN-eval backward with every flag and with dx "
+                         "alone, the standalone bias column sum) at the stem and stage-1 sizes, each launch "
+                         "after a cache-evicting sweep; for kernel traces and counters")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run three plain 256 MiB device copies, the known-size reference "
                          "for hardware byte counters (FETCH_SIZE / WRITE_SIZE) of the same process")
@@ -1072,6 +1076,9 @@ def main():
     if args.calibrate_copy:
         copy_calibration()
     flush = Flusher()
+    if args.reduction_only:
+        print(json.dumps({"reduction_passes": reduction_bandwidth(args.steps, args.warmup, flush)}), flush=True)
+        return
     if args.workload:
         for name in args.workload.split(","):
             w = workload_by_name(name)
